@@ -1,0 +1,69 @@
+"""One GCN layer, its gradients, the losses, moving average and SGD, in float64.
+
+Layer (Appendix A.1, the layer function and its two gradients, with P the
+local propagation matrix of Algorithm 1 and the mean aggregator of the
+PipeGCN forward equation in Section 3.2):
+
+    A = P H_full            (aggregation; H_full = [H_inner; H_boundary])
+    Z = A W                 (update)
+    H = relu(Z)             (every layer except the last, which returns Z)
+
+    M      = J ∘ 1[Z > 0]   (J itself at the last layer)
+    G      = Aᵀ M           (weight gradient, from the saved A)
+    J_full = Pᵀ (M Wᵀ)      (gradient of every input row, inner and boundary)
+
+The paper writes the aggregation as the product P H W; aggregating first and
+transforming first in the backward are the same matrix products in another
+association (the reading is listed with the others in the design notes).
+
+Pinned by: dense brute force of P (tests), central finite differences of the
+partition-local loss (tests), reduction to full-graph GCN (tests).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def layer_forward(P, H_full: np.ndarray, W: np.ndarray, relu: bool):
+    A = P @ H_full
+    Z = A @ W
+    H = np.maximum(Z, 0.0) if relu else Z
+    return A, Z, H
+
+
+def layer_backward(P, A: np.ndarray, Z: np.ndarray, J: np.ndarray, W: np.ndarray,
+                   relu: bool, input_grad: bool):
+    M = J * (Z > 0.0) if relu else J
+    G = A.T @ M
+    J_full = (P.T @ (M @ W.T)) if input_grad else None
+    return G, J_full
+
+
+def softmax_ce(Z: np.ndarray, y: np.ndarray, scale: float):
+    """Sum over rows of -log softmax(Z)[y], times ``scale``; and its gradient in Z."""
+    zmax = Z.max(axis=1, keepdims=True)
+    e = np.exp(Z - zmax)
+    s = e.sum(axis=1, keepdims=True)
+    logp = Z - zmax - np.log(s)
+    rows = np.arange(Z.shape[0])
+    loss = -logp[rows, y].sum() * scale
+    J = e / s
+    J[rows, y] -= 1.0
+    return loss, J * scale
+
+
+def sigmoid_bce(Z: np.ndarray, Y: np.ndarray, scale: float):
+    """Sum of binary cross-entropy with logits over all entries, times ``scale``."""
+    loss = (np.maximum(Z, 0.0) - Z * Y + np.log1p(np.exp(-np.abs(Z)))).sum() * scale
+    sig = 1.0 / (1.0 + np.exp(-Z))
+    return loss, (sig - Y) * scale
+
+
+def ema(state: np.ndarray, incoming: np.ndarray, gamma: float) -> np.ndarray:
+    """Moving average of Section 3.4: ŝ_t = γ ŝ_{t-1} + (1-γ) s_t."""
+    return gamma * state + (1.0 - gamma) * incoming
+
+
+def sgd(W: np.ndarray, G: np.ndarray, eta: float) -> np.ndarray:
+    """Algorithm 1's update W_t = W_{t-1} - η G."""
+    return W - eta * G
