@@ -1,0 +1,260 @@
+/*
+ * pgcn.h — C ABI of libpgcn: one partition's PipeGCN training step on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow the paper "PipeGCN: Efficient Full-Graph Training of
+ * Graph Convolutional Networks with Pipelined Feature Communication"
+ * (ICLR 2022):
+ *   - Algorithm 1 (per-partition view): set-up of the inner, boundary and
+ *     send sets; forward, loss, backward, AllReduce and SGD per iteration;
+ *   - Section 3.2: the mean aggregator with one-iteration-stale boundary
+ *     features and boundary feature gradients;
+ *   - Section 3.4: moving-average smoothing of stale features and gradients;
+ *   - Appendix A.1: the layer function Z = P H W, H' = σ(Z) and its two
+ *     gradients, with P split into intra- and inter-partition parts.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Status:    every int-returning call returns PGCN_OK (0) or a PGCN_E* code;
+ *            pgcn_last_error() gives a thread-local message for the last
+ *            failure.  No C++ exception crosses this interface.
+ * Memory:    the caller owns every activation, weight, gradient and buffer
+ *            (device memory, fp32 unless stated).  The library owns only the
+ *            partition handle's index arrays.  Scratch memory is passed in as
+ *            `workspace` (size from pgcn_workspace_size()).
+ * Layout:    dense matrices are row-major with an explicit row stride `ld`
+ *            (in elements).  fp32 matrices read by the aggregation kernels
+ *            need ld % 4 == 0 and 16-byte aligned bases; bf16 matrices need
+ *            ld % 8 == 0.  Columns [f, ld) are padding: never read as data;
+ *            the aggregation kernels write zeros there.  Weight matrices W
+ *            and weight gradients dW are compact [f_in x f_out].
+ * Streams:   compute calls only enqueue work on the given stream; nothing
+ *            synchronises the host except pgcn_partition_setup/destroy.
+ * Threads:   a partition handle is immutable after set-up; concurrent calls
+ *            on different streams with disjoint outputs and workspaces are
+ *            safe.
+ * Determinism: no floating-point atomics are used; results are bitwise
+ *            reproducible for identical inputs and launch configuration.
+ */
+#ifndef PGCN_H
+#define PGCN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PGCN_VERSION 100
+
+enum pgcn_status {
+  PGCN_OK = 0,
+  PGCN_EINVAL = 1,        /* null pointer, bad size, bad stride, bad enum       */
+  PGCN_ENOMEM = 2,        /* device or host allocation failed during set-up     */
+  PGCN_EHIP = 3,          /* a HIP runtime call failed (message has its text)   */
+  PGCN_EUNSUPPORTED = 4,  /* device is not gfx950, or an unsupported combination */
+  PGCN_EWORKSPACE = 5     /* workspace missing or smaller than required          */
+};
+
+enum pgcn_dtype { PGCN_F32 = 0, PGCN_BF16 = 1 };
+
+enum pgcn_setup_flags {
+  PGCN_SETUP_HOST_ONLY = 1  /* build the index structures on the host only: no
+                               device upload; compute calls on such a handle
+                               return PGCN_EINVAL (used to test the builder
+                               without a GPU) */
+};
+
+enum pgcn_pack_kind {
+  PGCN_PACK_FEAT = 0,     /* dst[k, :] = src[send_idx[k], :] for k in [0, n_send)       */
+  PGCN_ACCUM_GRAD = 1     /* dst[u, :] += sum_{k : send_idx[k] == u} src[k, :], ascending k */
+};
+
+enum pgcn_loss_kind { PGCN_SOFTMAX_CE = 0, PGCN_SIGMOID_BCE = 1 };
+
+/* Global graph on the host.  Must be symmetric (u in N(v) <=> v in N(u)).
+ * Duplicate entries and self loops are allowed and removed; exactly one
+ * self loop per inner row is added (Ã = A + I, Appendix A.1). */
+typedef struct {
+  int64_t n;               /* global node count                     */
+  const int64_t *rowptr;   /* [n+1], rowptr[0] == 0, non-decreasing */
+  const int32_t *col;      /* [rowptr[n]], values in [0, n)         */
+} pgcn_csr;
+
+/* Which partition owns each node (Algorithm 1's input: partition id i, count n). */
+typedef struct {
+  int32_t nparts;          /* partition count, >= 1                 */
+  int32_t self;            /* the partition to build, in [0, nparts) */
+  const int32_t *owner;    /* [n] host, values in [0, nparts)        */
+} pgcn_boundary_map;
+
+typedef struct pgcn_partition pgcn_partition;
+
+/* Sizes of a built partition. */
+typedef struct {
+  int64_t n_inner;         /* |V_i|                                           */
+  int64_t n_bd;            /* |B_i|                                           */
+  int64_t nnz;             /* non-zeros of P_i, one self loop per inner row   */
+  int64_t n_send;          /* sum_j |S_{i,j}|                                 */
+  int64_t max_row_len;     /* longest row of P_i                              */
+  int64_t max_row_len_t;   /* longest row of P_i^T                            */
+  int32_t nparts;
+  int32_t self;
+  int32_t host_only;       /* 1 if built with PGCN_SETUP_HOST_ONLY            */
+  int32_t spmm_segment;    /* rows longer than this are split (fixed order)   */
+  int64_t spmm_items;      /* work items of the forward aggregation           */
+  int64_t spmm_split_slots;/* partial-sum slots of split rows (forward)       */
+  int64_t spmmt_items;     /* work items of the transposed aggregation        */
+  int64_t spmmt_split_slots;
+} pgcn_info;
+
+/* Caller-allocated host buffers for pgcn_partition_export, sized from pgcn_info.
+ * Local numbering: inner local id = rank of the global id among owner == self;
+ * boundary local id = n_inner + rank by (owner, global id).  Rows of P_i and
+ * P_i^T list columns in ascending local id.  The send list holds S_{i,j} for
+ * ascending j, each in ascending global id. */
+typedef struct {
+  int64_t *inner_gid;      /* [n_inner]                       */
+  int64_t *bd_gid;         /* [n_bd]                          */
+  int64_t *recv_ptr;       /* [nparts+1] boundary rows of owner j: [recv_ptr[j], recv_ptr[j+1]) */
+  int64_t *rowptr;         /* [n_inner+1]                     */
+  int32_t *col;            /* [nnz]                           */
+  int64_t *rowptr_t;       /* [n_inner+n_bd+1]                */
+  int32_t *col_t;          /* [nnz]                           */
+  int64_t *send_ptr;       /* [nparts+1]                      */
+  int32_t *send_idx;       /* [n_send] inner local ids        */
+  int64_t *inv_ptr;        /* [n_inner+1]                     */
+  int32_t *inv_k;          /* [n_send] positions into send_idx, ascending per row */
+} pgcn_arrays;
+
+/*
+ * Partition set-up (Algorithm 1, set-up block; Section 3.1).
+ * Builds V_i, B_i, the CSR of P_i (entries 1/d_v, d_v = row length = degree
+ * + 1), its transpose, the send sets S_{i,j} = B_j ∩ V_i, the inverse send
+ * map and the fixed-order work plan of the aggregation kernels; uploads them
+ * to the current device.  Host-synchronous.  `flags` is a mask of
+ * pgcn_setup_flags.  On success *out receives a handle freed by
+ * pgcn_partition_destroy.  Errors: PGCN_EINVAL (bad graph or map),
+ * PGCN_ENOMEM, PGCN_EHIP, PGCN_EUNSUPPORTED (current device not gfx950).
+ */
+int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map *bmap, uint32_t flags,
+                         pgcn_partition **out);
+int pgcn_partition_info(const pgcn_partition *part, pgcn_info *out);
+/* Copies every index array into caller buffers (host).  Any member may be NULL to skip it. */
+int pgcn_partition_export(const pgcn_partition *part, const pgcn_arrays *host_out);
+void pgcn_partition_destroy(pgcn_partition *part);
+
+/* Bytes of workspace that pgcn_layer_fwd / pgcn_layer_bwd / pgcn_loss_fwd_bwd need
+ * for these widths (the maximum over the three). */
+size_t pgcn_workspace_size(const pgcn_partition *part, int32_t f_in, int32_t f_out, int32_t gemm_dtype);
+
+/*
+ * One layer forward (Algorithm 1's forward update; Section 3.2 forward
+ * equation; Appendix A.1 layer function):
+ *     A = P_i [H_in ; H_bd]        fresh inner rows, stale boundary rows
+ *     Z = A W ;  H_out = relu(Z) if relu else Z
+ * H_bd holds the boundary rows to use (the received stale buffer, or its
+ * smoothing state); NULL means all-zero boundary rows (iteration 1).
+ * With gemm_dtype == PGCN_BF16, A is rounded once to bf16 (round to nearest
+ * even) into A_bf16, W is rounded to bf16 and the product accumulates in
+ * fp32; A (fp32) may then be NULL.  With PGCN_F32, A is required and A_bf16
+ * ignored.
+ */
+typedef struct {
+  int32_t f_in, f_out;
+  int32_t gemm_dtype;          /* pgcn_dtype                                    */
+  int32_t relu;                /* 1: H_out = relu(Z); 0: H_out = Z (last layer)  */
+  int64_t ld_in;               /* stride of H_in, H_bd, A, A_bf16 (elements)     */
+  int64_t ld_out;              /* stride of H_out                                */
+  const float *H_in;           /* [n_inner, ld_in]                               */
+  const float *H_bd;           /* [n_bd, ld_in] or NULL                          */
+  const float *W;              /* [f_in, f_out]                                  */
+  float *A;                    /* [n_inner, ld_in] out                           */
+  uint16_t *A_bf16;            /* [n_inner, ld_in] out (bf16 bits)               */
+  float *H_out;                /* [n_inner, ld_out] out                          */
+  void *workspace;
+  size_t workspace_bytes;
+} pgcn_fwd_args;
+int pgcn_layer_fwd(const pgcn_partition *part, const pgcn_fwd_args *args, hipStream_t stream);
+
+/*
+ * One layer backward (Algorithm 1's weight- and feature-gradient lines;
+ * Appendix A.1 gradients):
+ *     M      = J_out ∘ 1[H_out > 0] if relu else J_out
+ *     dW     = A^T M
+ *     J_full = P_i^T (M W^T)      rows [0, n_inner) -> J_in,
+ *                                 rows [n_inner, n_inner+n_bd) -> J_bd_out
+ * J_in and J_bd_out are both NULL for the first layer (no feature gradient).
+ * Stale gradients from peers are added afterwards with pgcn_pack_boundary
+ * (PGCN_ACCUM_GRAD), as Algorithm 1 does after waiting for them.
+ * dW accumulates split-K partials in a fixed order (deterministic).
+ */
+typedef struct {
+  int32_t f_in, f_out;
+  int32_t gemm_dtype;
+  int32_t relu;
+  int64_t ld_in, ld_out;
+  const float *J_out;          /* [n_inner, ld_out]                              */
+  const float *H_out;          /* [n_inner, ld_out] mask source (when relu)      */
+  const float *A;              /* [n_inner, ld_in] (PGCN_F32)                    */
+  const uint16_t *A_bf16;      /* [n_inner, ld_in] (PGCN_BF16)                   */
+  const float *W;              /* [f_in, f_out]                                  */
+  float *dW;                   /* [f_in, f_out] out                              */
+  float *J_in;                 /* [n_inner, ld_in] out or NULL                   */
+  float *J_bd_out;             /* [n_bd, ld_in] out or NULL                      */
+  void *workspace;
+  size_t workspace_bytes;
+} pgcn_bwd_args;
+int pgcn_layer_bwd(const pgcn_partition *part, const pgcn_bwd_args *args, hipStream_t stream);
+
+/*
+ * Moving-average smoothing of stale features or gradients (Section 3.4):
+ *     state[r, c] = gamma * state[r, c] + (1 - gamma) * incoming[r, c]
+ * for r < rows, c < cols; both matrices share stride ld (ld % 4 == 0).
+ */
+int pgcn_smooth_ema(float *state, const float *incoming, int64_t rows, int32_t cols, int64_t ld,
+                     float gamma, hipStream_t stream);
+
+/*
+ * Boundary packing (Algorithm 1's send of H_{S_{i,j}} and the accumulation of
+ * received gradients C_j into rows S_{i,j}, ascending j):
+ *   PGCN_PACK_FEAT : dst[k, :] = src[send_idx[k], :],   src [n_inner, ld], dst [n_send, ld]
+ *   PGCN_ACCUM_GRAD: dst[u, :] += src[k, :] for each k with send_idx[k] == u, in
+ *                    ascending k;                      src [n_send, ld], dst [n_inner, ld]
+ */
+int pgcn_pack_boundary(const pgcn_partition *part, int32_t kind, const float *src, float *dst,
+                       int32_t cols, int64_t ld, hipStream_t stream);
+
+/*
+ * Loss and its gradient w.r.t. the logits (Algorithm 1's J^(L)):
+ *   PGCN_SOFTMAX_CE : loss = scale * sum_r -log softmax(Z_r)[labels[r]]
+ *                     J_r  = scale * (softmax(Z_r) - onehot(labels[r]))
+ *   PGCN_SIGMOID_BCE: loss = scale * sum_{r,c} BCE(sigmoid(Z_rc), targets_rc)
+ *                     J_rc = scale * (sigmoid(Z_rc) - targets_rc)
+ * Z and J: [rows, ld]; labels: [rows] int32 in [0, classes); targets: [rows, ld_t].
+ * loss_out: one device float, written (not accumulated), reduced in a fixed order.
+ */
+int pgcn_loss_fwd_bwd(int32_t kind, const float *Z, int64_t rows, int32_t classes, int64_t ld,
+                      const int32_t *labels, const float *targets, int64_t ld_t, float scale,
+                      float *J, float *loss_out, void *workspace, size_t workspace_bytes,
+                      hipStream_t stream);
+
+/* Algorithm 1's update after the AllReduce (a sum): W -= eta * (G + G_peer).
+ * G_peer may be NULL (one partition: the AllReduce is the identity). */
+int pgcn_sgd_update(float *W, const float *G, const float *G_peer, int64_t count, float eta,
+                    hipStream_t stream);
+
+/* Refill of a stale buffer (Algorithm 1's send/receive threads; the paper runs
+ * them on a second stream): an asynchronous device copy of `bytes` bytes
+ * enqueued on `stream`. */
+int pgcn_refill_async(void *dst, const void *src, size_t bytes, hipStream_t stream);
+
+const char *pgcn_last_error(void);
+int pgcn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PGCN_H */

@@ -1,0 +1,245 @@
+// C ABI entry points of libpgcn: argument checking and kernel composition.
+#include <cstring>
+
+#include "internal.h"
+
+using namespace pgcn;
+
+namespace {
+
+int check_part(const pgcn_partition *p, const char *fn) {
+  if (!p) return set_error(PGCN_EINVAL, std::string(fn) + ": null partition");
+  if (p->host_only) return set_error(PGCN_EINVAL, std::string(fn) + ": partition was built host-only");
+  int dev = -1;
+  PGCN_HIP(hipGetDevice(&dev));
+  if (dev != p->device) return set_error(PGCN_EINVAL, std::string(fn) + ": current device differs from set-up device");
+  return PGCN_OK;
+}
+
+bool aligned16(const void *q) { return ((uintptr_t)q & 15u) == 0; }
+
+int64_t ld4(int64_t f) { return (f + 3) / 4 * 4; }
+
+size_t fwd_ws(const pgcn_partition *p, int32_t f_in) { return align_up(aggregate_workspace(p->plan, f_in), 256); }
+
+// backward: the split-K partials are consumed before D is written, so they share space
+size_t bwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_grad) {
+  size_t g = gemm_workspace(Gemm::TN_MASK_SPLITK, f_in, f_out, (int32_t)p->n_inner);
+  size_t d = 0;
+  if (input_grad)
+    d = align_up((size_t)p->n_inner * (size_t)ld4(f_in) * sizeof(float), 256) +
+        align_up(aggregate_workspace(p->plan_t, f_in), 256);
+  return align_up(g > d ? g : d, 256);
+}
+
+}  // namespace
+
+extern "C" size_t pgcn_workspace_size(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) {
+  (void)gemm_dtype;
+  if (!p || f_in <= 0 || f_out <= 0) return 0;
+  size_t w = fwd_ws(p, f_in);
+  size_t b = bwd_ws(p, f_in, f_out, true);
+  size_t l = align_up(loss_workspace(p->n_inner), 256);
+  size_t m = w > b ? w : b;
+  return m > l ? m : l;
+}
+
+extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, hipStream_t s) {
+  int rc = check_part(p, "pgcn_layer_fwd");
+  if (rc) return rc;
+  PGCN_REQUIRE(a, "pgcn_layer_fwd: null args");
+  PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_layer_fwd: widths must be >= 1");
+  PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_layer_fwd: bad gemm_dtype");
+  PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_layer_fwd: ld_in must be >= f_in and a multiple of 4");
+  PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0, "pgcn_layer_fwd: ld_out must be >= f_out and a multiple of 4");
+  const bool bf16 = a->gemm_dtype == PGCN_BF16;
+  if (p->n_inner > 0) {
+    PGCN_REQUIRE(a->H_in && a->W && a->H_out, "pgcn_layer_fwd: null H_in, W or H_out");
+    PGCN_REQUIRE(aligned16(a->H_in) && aligned16(a->H_bd), "pgcn_layer_fwd: H_in/H_bd must be 16-byte aligned");
+    if (bf16) {
+      PGCN_REQUIRE(a->A_bf16 && aligned16(a->A_bf16) && a->ld_in % 8 == 0,
+                   "pgcn_layer_fwd: bf16 path needs A_bf16 (16-byte aligned) and ld_in % 8 == 0");
+    } else {
+      PGCN_REQUIRE(a->A, "pgcn_layer_fwd: fp32 path needs A");
+    }
+    PGCN_REQUIRE(!a->A || aligned16(a->A), "pgcn_layer_fwd: A must be 16-byte aligned");
+  }
+  const size_t need = fwd_ws(p, a->f_in);
+  if (need > 0 && (!a->workspace || a->workspace_bytes < need))
+    return set_error(PGCN_EWORKSPACE, "pgcn_layer_fwd: workspace too small");
+  if (p->n_inner == 0) return PGCN_OK;
+
+  AggArgs g{};
+  g.plan = &p->plan;
+  g.col = p->d_col;
+  g.in_split = p->n_inner;
+  g.in_lo = a->H_in;
+  g.in_hi = p->n_bd > 0 ? a->H_bd : nullptr;
+  g.out_split = p->n_inner;
+  g.out_lo = a->A;
+  g.out_hi = nullptr;
+  g.out_bf16 = bf16 ? a->A_bf16 : nullptr;
+  g.scale = p->d_inv_deg;
+  g.f = a->f_in;
+  g.ld_in = a->ld_in;
+  g.ld_out = a->ld_in;
+  g.partials = (float *)a->workspace;
+  rc = launch_aggregate(g, s);
+  if (rc) return rc;
+
+  GemmArgs m{};
+  m.M = (int32_t)p->n_inner;
+  m.N = a->f_out;
+  m.K = a->f_in;
+  m.dtype = a->gemm_dtype;
+  m.A = a->A;
+  m.A16 = a->A_bf16;
+  m.lda = a->ld_in;
+  m.B = a->W;
+  m.ldb = a->f_out;
+  m.C = a->H_out;
+  m.ldc = a->ld_out;
+  return launch_gemm(a->relu ? Gemm::NN_RELU : Gemm::NN_PLAIN, m, s);
+}
+
+extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, hipStream_t s) {
+  int rc = check_part(p, "pgcn_layer_bwd");
+  if (rc) return rc;
+  PGCN_REQUIRE(a, "pgcn_layer_bwd: null args");
+  PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_layer_bwd: widths must be >= 1");
+  PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_layer_bwd: bad gemm_dtype");
+  PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_layer_bwd: ld_in must be >= f_in and a multiple of 4");
+  PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0, "pgcn_layer_bwd: ld_out must be >= f_out and a multiple of 4");
+  const bool bf16 = a->gemm_dtype == PGCN_BF16;
+  const bool input_grad = a->J_in != nullptr || a->J_bd_out != nullptr;
+  PGCN_REQUIRE(a->dW, "pgcn_layer_bwd: null dW");
+  if (input_grad) {
+    PGCN_REQUIRE(a->J_in && (a->J_bd_out || p->n_bd == 0),
+                 "pgcn_layer_bwd: J_in and J_bd_out must both be given (or both NULL)");
+    PGCN_REQUIRE(aligned16(a->J_in) && aligned16(a->J_bd_out), "pgcn_layer_bwd: J_in/J_bd_out must be 16-byte aligned");
+  }
+  if (p->n_inner > 0) {
+    PGCN_REQUIRE(a->J_out && a->W, "pgcn_layer_bwd: null J_out or W");
+    PGCN_REQUIRE(!a->relu || a->H_out, "pgcn_layer_bwd: relu needs H_out as mask source");
+    PGCN_REQUIRE(aligned16(a->J_out) && aligned16(a->H_out), "pgcn_layer_bwd: J_out/H_out must be 16-byte aligned");
+    if (bf16)
+      PGCN_REQUIRE(a->A_bf16 && aligned16(a->A_bf16) && a->ld_in % 8 == 0,
+                   "pgcn_layer_bwd: bf16 path needs A_bf16 (16-byte aligned) and ld_in % 8 == 0");
+    else
+      PGCN_REQUIRE(a->A && aligned16(a->A), "pgcn_layer_bwd: fp32 path needs A (16-byte aligned)");
+  }
+  const size_t need = bwd_ws(p, a->f_in, a->f_out, input_grad);
+  if (need > 0 && (!a->workspace || a->workspace_bytes < need))
+    return set_error(PGCN_EWORKSPACE, "pgcn_layer_bwd: workspace too small");
+
+  // dW = A^T (J ∘ 1[H > 0]); with no inner rows it is zero
+  GemmArgs g{};
+  g.M = a->f_in;
+  g.N = a->f_out;
+  g.K = (int32_t)p->n_inner;
+  g.dtype = a->gemm_dtype;
+  g.A = a->A;
+  g.A16 = a->A_bf16;
+  g.lda = a->ld_in;
+  g.B = a->J_out;
+  g.ldb = a->ld_out;
+  g.Hmask = a->relu ? a->H_out : nullptr;
+  g.ldm = a->ld_out;
+  g.C = a->dW;
+  g.ldc = a->f_out;
+  g.workspace = (float *)a->workspace;
+  g.workspace_bytes = a->workspace_bytes;
+  rc = launch_gemm(Gemm::TN_MASK_SPLITK, g, s);
+  if (rc) return rc;
+  if (!input_grad || p->n_inner == 0) return PGCN_OK;
+
+  // D = diag(1/d) ((J ∘ 1[H > 0]) W^T), then J_full = (P_i^T without the scale) D
+  const int64_t ld_d = ld4(a->f_in);
+  float *D = (float *)a->workspace;
+  float *partials = (float *)((char *)a->workspace + align_up((size_t)p->n_inner * ld_d * sizeof(float), 256));
+  GemmArgs d{};
+  d.M = (int32_t)p->n_inner;
+  d.N = a->f_in;
+  d.K = a->f_out;
+  d.dtype = a->gemm_dtype;
+  d.A = a->J_out;
+  d.lda = a->ld_out;
+  d.Hmask = a->relu ? a->H_out : nullptr;
+  d.ldm = a->ld_out;
+  d.B = a->W;
+  d.ldb = a->f_out;
+  d.C = D;
+  d.ldc = ld_d;
+  d.rowscale = p->d_inv_deg;
+  rc = launch_gemm(Gemm::MASK_NT_ROWSCALE, d, s);
+  if (rc) return rc;
+
+  AggArgs t{};
+  t.plan = &p->plan_t;
+  t.col = p->d_col_t;
+  t.in_split = p->n_inner;
+  t.in_lo = D;
+  t.in_hi = nullptr;
+  t.out_split = p->n_inner;
+  t.out_lo = a->J_in;
+  t.out_hi = a->J_bd_out;
+  t.out_bf16 = nullptr;
+  t.scale = nullptr;
+  t.f = a->f_in;
+  t.ld_in = ld_d;
+  t.ld_out = a->ld_in;
+  t.partials = partials;
+  return launch_aggregate(t, s);
+}
+
+extern "C" int pgcn_smooth_ema(float *state, const float *incoming, int64_t rows, int32_t cols, int64_t ld,
+                               float gamma, hipStream_t s) {
+  PGCN_REQUIRE(rows >= 0 && cols >= 0 && ld >= cols && ld % 4 == 0, "pgcn_smooth_ema: bad shape or stride");
+  if (rows == 0 || cols == 0) return PGCN_OK;
+  PGCN_REQUIRE(state && incoming && aligned16(state) && aligned16(incoming),
+               "pgcn_smooth_ema: null or unaligned buffer");
+  return launch_ema(state, incoming, rows, cols, ld, gamma, s);
+}
+
+extern "C" int pgcn_pack_boundary(const pgcn_partition *p, int32_t kind, const float *src, float *dst, int32_t cols,
+                                  int64_t ld, hipStream_t s) {
+  int rc = check_part(p, "pgcn_pack_boundary");
+  if (rc) return rc;
+  PGCN_REQUIRE(kind == PGCN_PACK_FEAT || kind == PGCN_ACCUM_GRAD, "pgcn_pack_boundary: bad kind");
+  PGCN_REQUIRE(cols >= 0 && ld >= cols && ld % 4 == 0, "pgcn_pack_boundary: bad shape or stride");
+  if (p->n_send == 0 || cols == 0) return PGCN_OK;
+  PGCN_REQUIRE(src && dst && aligned16(src) && aligned16(dst), "pgcn_pack_boundary: null or unaligned buffer");
+  if (kind == PGCN_PACK_FEAT) return launch_pack(p->d_send_idx, p->n_send, src, dst, cols, ld, s);
+  return launch_accum(p->d_inv_ptr, p->d_inv_k, p->n_inner, src, dst, cols, ld, s);
+}
+
+extern "C" int pgcn_loss_fwd_bwd(int32_t kind, const float *Z, int64_t rows, int32_t classes, int64_t ld,
+                                 const int32_t *labels, const float *targets, int64_t ld_t, float scale, float *J,
+                                 float *loss_out, void *workspace, size_t workspace_bytes, hipStream_t s) {
+  PGCN_REQUIRE(kind == PGCN_SOFTMAX_CE || kind == PGCN_SIGMOID_BCE, "pgcn_loss_fwd_bwd: bad kind");
+  PGCN_REQUIRE(rows >= 0 && classes >= 1 && ld >= classes, "pgcn_loss_fwd_bwd: bad shape or stride");
+  PGCN_REQUIRE(loss_out, "pgcn_loss_fwd_bwd: null loss_out");
+  if (rows > 0) {
+    PGCN_REQUIRE(Z && J, "pgcn_loss_fwd_bwd: null Z or J");
+    if (kind == PGCN_SOFTMAX_CE) PGCN_REQUIRE(labels, "pgcn_loss_fwd_bwd: softmax-CE needs labels");
+    else PGCN_REQUIRE(targets && ld_t >= classes, "pgcn_loss_fwd_bwd: BCE needs targets with ld_t >= classes");
+  }
+  if (!workspace || workspace_bytes < loss_workspace(rows))
+    return set_error(PGCN_EWORKSPACE, "pgcn_loss_fwd_bwd: workspace too small");
+  return launch_loss(kind, Z, rows, classes, ld, labels, targets, ld_t, scale, J, loss_out, (float *)workspace, s);
+}
+
+extern "C" int pgcn_sgd_update(float *W, const float *G, const float *G_peer, int64_t count, float eta,
+                               hipStream_t s) {
+  PGCN_REQUIRE(count >= 0, "pgcn_sgd_update: negative count");
+  if (count == 0) return PGCN_OK;
+  PGCN_REQUIRE(W && G, "pgcn_sgd_update: null W or G");
+  return launch_sgd(W, G, G_peer, count, eta, s);
+}
+
+extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return PGCN_OK;
+  PGCN_REQUIRE(dst && src, "pgcn_refill_async: null buffer");
+  PGCN_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, s));
+  return PGCN_OK;
+}

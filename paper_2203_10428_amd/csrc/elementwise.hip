@@ -1,0 +1,200 @@
+// Bandwidth-bound kernels of the partition step:
+//   - moving-average smoothing of stale features / gradients (Section 3.4);
+//   - packing of the rows sent to peers (Algorithm 1's send of H_{S_{i,j}});
+//   - accumulation of received stale gradients into their rows, in ascending
+//     send-list order (Algorithm 1's loop over peers j);
+//   - softmax cross-entropy / sigmoid BCE with their logit gradients
+//     (Algorithm 1's J^(L)), with a fixed-order loss reduction;
+//   - the SGD update (Algorithm 1's last line).
+// All are float4-vectorised over the feature dimension; no float atomics.
+#include "internal.h"
+
+namespace pgcn {
+
+__global__ __launch_bounds__(256) void ema_kernel(float *state, const float *in, int64_t rows, int f4,
+                                                  int64_t ld, float gamma) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * f4) return;
+  const int64_t r = i / f4;
+  const int c = 4 * (int)(i % f4);
+  float4 *s = reinterpret_cast<float4 *>(state + r * ld + c);
+  const float4 x = *reinterpret_cast<const float4 *>(in + r * ld + c);
+  float4 v = *s;
+  const float g1 = 1.0f - gamma;
+  v.x = gamma * v.x + g1 * x.x;
+  v.y = gamma * v.y + g1 * x.y;
+  v.z = gamma * v.z + g1 * x.z;
+  v.w = gamma * v.w + g1 * x.w;
+  *s = v;
+}
+
+int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_t ld, float gamma,
+               hipStream_t s) {
+  const int f4 = (cols + 3) / 4;
+  const int64_t total = rows * f4;
+  if (total == 0) return PGCN_OK;
+  hipLaunchKernelGGL(ema_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, state, in, rows, f4,
+                     ld, gamma);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
+}
+
+__global__ __launch_bounds__(256) void pack_kernel(const int32_t *idx, int64_t count, const float *src,
+                                                   float *dst, int f4, int64_t ld) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= count * f4) return;
+  const int64_t k = i / f4;
+  const int c = 4 * (int)(i % f4);
+  *reinterpret_cast<float4 *>(dst + k * ld + c) =
+      *reinterpret_cast<const float4 *>(src + (int64_t)idx[k] * ld + c);
+}
+
+int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst, int32_t cols, int64_t ld,
+                hipStream_t s) {
+  const int f4 = (cols + 3) / 4;
+  const int64_t total = count * f4;
+  if (total == 0) return PGCN_OK;
+  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, idx, count, src, dst,
+                     f4, ld);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
+}
+
+__global__ __launch_bounds__(256) void accum_kernel(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows,
+                                                    const float *src, float *dst, int f4, int64_t ld) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * f4) return;
+  const int64_t u = i / f4;
+  const int c = 4 * (int)(i % f4);
+  const int64_t b = inv_ptr[u], e = inv_ptr[u + 1];
+  if (b == e) return;
+  float4 *d = reinterpret_cast<float4 *>(dst + u * ld + c);
+  float4 v = *d;
+  for (int64_t q = b; q < e; ++q) {
+    const float4 x = *reinterpret_cast<const float4 *>(src + (int64_t)inv_k[q] * ld + c);
+    v.x += x.x;
+    v.y += x.y;
+    v.z += x.z;
+    v.w += x.w;
+  }
+  *d = v;
+}
+
+int launch_accum(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, const float *src, float *dst,
+                 int32_t cols, int64_t ld, hipStream_t s) {
+  const int f4 = (cols + 3) / 4;
+  const int64_t total = rows * f4;
+  if (total == 0) return PGCN_OK;
+  hipLaunchKernelGGL(accum_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, inv_ptr, inv_k, rows,
+                     src, dst, f4, ld);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
+}
+
+// ---------------------------------------------------------------- losses ---
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// One wave64 per row.
+__global__ __launch_bounds__(256) void softmax_ce_kernel(const float *Z, int64_t rows, int C, int64_t ld,
+                                                         const int32_t *labels, float scale, float *J,
+                                                         float *row_loss) {
+  const int lane = threadIdx.x % 64;
+  const int64_t r = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
+  if (r >= rows) return;
+  const float *z = Z + r * ld;
+  float m = -INFINITY;
+  for (int c = lane; c < C; c += 64) m = fmaxf(m, z[c]);
+  m = wave_max(m);
+  float s = 0.f;
+  for (int c = lane; c < C; c += 64) s += __expf(z[c] - m);
+  s = wave_sum(s);
+  const int y = labels[r];
+  const bool y_ok = y >= 0 && y < C;          // an out-of-range label poisons the loss instead of reading out of the row
+  const float inv_s = 1.0f / s;
+  float *j = J + r * ld;
+  for (int c = lane; c < C; c += 64) {
+    const float p = __expf(z[c] - m) * inv_s;
+    j[c] = scale * (p - (c == y ? 1.0f : 0.0f));
+  }
+  if (lane == 0) row_loss[r] = y_ok ? scale * (m + __logf(s) - z[y]) : __builtin_nanf("");
+}
+
+__global__ __launch_bounds__(256) void sigmoid_bce_kernel(const float *Z, int64_t rows, int C, int64_t ld,
+                                                          const float *T, int64_t ld_t, float scale, float *J,
+                                                          float *row_loss) {
+  const int lane = threadIdx.x % 64;
+  const int64_t r = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
+  if (r >= rows) return;
+  const float *z = Z + r * ld;
+  const float *y = T + r * ld_t;
+  float *j = J + r * ld;
+  float l = 0.f;
+  for (int c = lane; c < C; c += 64) {
+    const float x = z[c], t = y[c];
+    l += fmaxf(x, 0.f) - x * t + log1pf(__expf(-fabsf(x)));
+    const float sg = 1.0f / (1.0f + __expf(-x));
+    j[c] = scale * (sg - t);
+  }
+  l = wave_sum(l);
+  if (lane == 0) row_loss[r] = scale * l;
+}
+
+// Fixed-order reduction of the per-row losses (one block, fp64 partials).
+__global__ __launch_bounds__(1024) void loss_reduce_kernel(const float *row_loss, int64_t rows, float *out) {
+  __shared__ double part[1024];
+  double s = 0.0;
+  for (int64_t r = threadIdx.x; r < rows; r += 1024) s += (double)row_loss[r];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 512; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *out = (float)part[0];
+}
+
+size_t loss_workspace(int64_t rows) { return (size_t)rows * sizeof(float); }
+
+int launch_loss(int32_t kind, const float *Z, int64_t rows, int32_t C, int64_t ld, const int32_t *labels,
+                const float *targets, int64_t ld_t, float scale, float *J, float *loss_out, float *ws,
+                hipStream_t s) {
+  if (rows > 0) {
+    const unsigned blocks = (unsigned)((rows + 3) / 4);
+    if (kind == PGCN_SOFTMAX_CE)
+      hipLaunchKernelGGL(softmax_ce_kernel, dim3(blocks), dim3(256), 0, s, Z, rows, C, ld, labels, scale, J, ws);
+    else
+      hipLaunchKernelGGL(sigmoid_bce_kernel, dim3(blocks), dim3(256), 0, s, Z, rows, C, ld, targets, ld_t, scale,
+                         J, ws);
+    PGCN_HIP(hipGetLastError());
+  }
+  hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(1024), 0, s, (const float *)ws, rows, loss_out);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
+}
+
+__global__ __launch_bounds__(256) void sgd_kernel(float *W, const float *G, const float *G2, int64_t count,
+                                                  float eta) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= count) return;
+  const float g = G2 ? G[i] + G2[i] : G[i];
+  W[i] = W[i] - eta * g;
+}
+
+int launch_sgd(float *W, const float *G, const float *G2, int64_t count, float eta, hipStream_t s) {
+  if (count == 0) return PGCN_OK;
+  hipLaunchKernelGGL(sgd_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, W, G, G2, count, eta);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
+}
+
+}  // namespace pgcn

@@ -1,0 +1,131 @@
+// Internal declarations shared by the libpgcn translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "pgcn.h"
+
+namespace pgcn {
+
+// Aggregation work item: a contiguous run of one CSR row.  `dst >= 0` is the
+// output row (the item covers the whole row); `dst < 0` means partial-sum
+// slot (-dst - 1) of a row that was split into fixed segments.
+struct WorkItem {
+  int64_t begin;
+  int32_t len;
+  int32_t dst;
+};
+
+// A split row: partial slots [first_slot, first_slot + nslots) are summed in
+// slot order into output row `row`.
+struct SplitRow {
+  int32_t row;
+  int32_t first_slot;
+  int32_t nslots;
+  int32_t pad;
+};
+
+// Fixed work plan over one CSR matrix (rows of P_i or of P_i^T).
+struct Plan {
+  std::vector<WorkItem> items;
+  std::vector<SplitRow> splits;
+  int64_t slots = 0;
+  WorkItem *d_items = nullptr;
+  SplitRow *d_splits = nullptr;
+};
+
+}  // namespace pgcn
+
+struct pgcn_partition {
+  int32_t nparts = 0, self = 0, host_only = 0, segment = 0;
+  int64_t n_inner = 0, n_bd = 0, nnz = 0, n_send = 0;
+  int64_t max_row = 0, max_row_t = 0;
+  int device = -1;
+  // host copies (canonical numbering)
+  std::vector<int64_t> inner_gid, bd_gid, recv_ptr, rowptr, rowptr_t, send_ptr, inv_ptr;
+  std::vector<int32_t> col, col_t, send_idx, inv_k;
+  std::vector<float> inv_deg;
+  pgcn::Plan plan, plan_t;
+  // device copies
+  int32_t *d_col = nullptr, *d_col_t = nullptr, *d_send_idx = nullptr, *d_inv_k = nullptr;
+  int64_t *d_inv_ptr = nullptr;
+  float *d_inv_deg = nullptr;
+};
+
+namespace pgcn {
+
+int set_error(int code, const std::string &msg);
+int check_hip(hipError_t e, const char *what);
+
+#define PGCN_HIP(call)                                   \
+  do {                                                   \
+    hipError_t _e = (call);                              \
+    if (_e != hipSuccess) return ::pgcn::check_hip(_e, #call); \
+  } while (0)
+
+#define PGCN_REQUIRE(cond, msg)                                  \
+  do {                                                           \
+    if (!(cond)) return ::pgcn::set_error(PGCN_EINVAL, (msg));   \
+  } while (0)
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---- kernel launchers (defined in the .hip files) -------------------------
+
+// Aggregation over a fixed plan.  Column c < in_split reads in_lo[c], else
+// in_hi[c - in_split] (in_hi == nullptr: zero rows).  Output row r < out_split
+// goes to out_lo[r], else out_hi[r - out_split].  When `scale` is non-null
+// each output row is multiplied by scale[r].  Partial slots go to `partials`.
+struct AggArgs {
+  const Plan *plan;
+  const int32_t *col;
+  int64_t in_split;
+  const float *in_lo, *in_hi;
+  int64_t out_split;
+  float *out_lo, *out_hi;
+  uint16_t *out_bf16;      // optional bf16 copy of out_lo rows (forward, bf16 GEMM path)
+  const float *scale;
+  int32_t f;
+  int64_t ld_in, ld_out;
+  float *partials;
+};
+int launch_aggregate(const AggArgs &a, hipStream_t s);
+size_t aggregate_workspace(const Plan &plan, int64_t f);
+
+enum class Gemm { NN_RELU, NN_PLAIN, MASK_NT_ROWSCALE, TN_MASK_SPLITK };
+struct GemmArgs {
+  int32_t M, N, K;
+  int32_t dtype;            // PGCN_F32 / PGCN_BF16
+  const float *A;           // fp32 operand
+  const uint16_t *A16;      // bf16 operand (activations)
+  int64_t lda;
+  const float *B;           // weights or masked operand source
+  int64_t ldb;
+  const float *Hmask;       // mask source for the masked operand (may be null: no mask)
+  int64_t ldm;
+  float *C;
+  int64_t ldc;
+  const float *rowscale;    // per output row scale (MASK_NT_ROWSCALE)
+  float *workspace;
+  size_t workspace_bytes;
+};
+int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s);
+size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K);
+
+int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_t ld, float gamma,
+               hipStream_t s);
+int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst, int32_t cols,
+                int64_t ld, hipStream_t s);
+int launch_accum(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, const float *src,
+                 float *dst, int32_t cols, int64_t ld, hipStream_t s);
+int launch_loss(int32_t kind, const float *Z, int64_t rows, int32_t classes, int64_t ld,
+                const int32_t *labels, const float *targets, int64_t ld_t, float scale, float *J,
+                float *loss_out, float *ws, hipStream_t s);
+size_t loss_workspace(int64_t rows);
+int launch_sgd(float *W, const float *G, const float *G2, int64_t count, float eta, hipStream_t s);
+
+}  // namespace pgcn

@@ -1,0 +1,321 @@
+// Partition set-up (Algorithm 1's set-up block; Section 3.1): inner set V_i,
+// boundary set B_i, local propagation matrix P_i and its transpose, send sets
+// S_{i,j} = B_j ∩ V_i, the inverse send map and the fixed work plans of the
+// aggregation kernels.  Host code; the result is uploaded once.
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <numeric>
+
+#include "internal.h"
+
+namespace pgcn {
+
+static thread_local std::string g_error;
+
+int set_error(int code, const std::string &msg) {
+  g_error = msg;
+  return code;
+}
+
+int check_hip(hipError_t e, const char *what) {
+  return set_error(PGCN_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Rows longer than `segment` are cut into fixed segments whose partial sums are
+// added in segment order by a second pass, so results never depend on timing.
+static void build_plan(const std::vector<int64_t> &rowptr, int64_t nrows, int32_t segment, Plan &p) {
+  p.items.clear();
+  p.splits.clear();
+  p.slots = 0;
+  std::vector<int64_t> order;
+  order.reserve(nrows);
+  for (int64_t r = 0; r < nrows; ++r) {
+    int64_t len = rowptr[r + 1] - rowptr[r];
+    if (len > segment) {
+      int32_t nseg = (int32_t)((len + segment - 1) / segment);
+      p.splits.push_back(SplitRow{(int32_t)r, (int32_t)p.slots, nseg, 0});
+      for (int32_t s = 0; s < nseg; ++s) {
+        int64_t b = rowptr[r] + (int64_t)s * segment;
+        int64_t e = std::min<int64_t>(b + segment, rowptr[r + 1]);
+        p.items.push_back(WorkItem{b, (int32_t)(e - b), (int32_t)(-(p.slots + s) - 1)});
+      }
+      p.slots += nseg;
+    } else {
+      order.push_back(r);
+    }
+  }
+  // whole rows, longest first (ties by row id): long items start early and
+  // items of similar length share a wavefront
+  std::stable_sort(order.begin(), order.end(), [&](int64_t a, int64_t b) {
+    return rowptr[a + 1] - rowptr[a] > rowptr[b + 1] - rowptr[b];
+  });
+  for (int64_t r : order)
+    p.items.push_back(WorkItem{rowptr[r], (int32_t)(rowptr[r + 1] - rowptr[r]), (int32_t)r});
+}
+
+template <class T>
+static int upload(T **dptr, const std::vector<T> &h) {
+  *dptr = nullptr;
+  if (h.empty()) return PGCN_OK;
+  hipError_t e = hipMalloc((void **)dptr, h.size() * sizeof(T));
+  if (e != hipSuccess) {
+    *dptr = nullptr;
+    return set_error(PGCN_ENOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+  }
+  PGCN_HIP(hipMemcpy(*dptr, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice));
+  return PGCN_OK;
+}
+
+static void free_device(pgcn_partition *p) {
+  void *ptrs[] = {p->d_col, p->d_col_t, p->d_send_idx, p->d_inv_k, p->d_inv_ptr, p->d_inv_deg,
+                  p->plan.d_items, p->plan.d_splits, p->plan_t.d_items, p->plan_t.d_splits};
+  for (void *q : ptrs)
+    if (q) (void)hipFree(q);
+  p->d_col = p->d_col_t = p->d_send_idx = p->d_inv_k = nullptr;
+  p->d_inv_ptr = nullptr;
+  p->d_inv_deg = nullptr;
+  p->plan.d_items = p->plan_t.d_items = nullptr;
+  p->plan.d_splits = p->plan_t.d_splits = nullptr;
+}
+
+static int check_device() {
+  int dev = 0;
+  PGCN_HIP(hipGetDevice(&dev));
+  hipDeviceProp_t prop;
+  PGCN_HIP(hipGetDeviceProperties(&prop, dev));
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return set_error(PGCN_EUNSUPPORTED, std::string("libpgcn is built for gfx950, device is ") + prop.gcnArchName);
+  return PGCN_OK;
+}
+
+static int default_segment() {
+  const char *s = std::getenv("PGCN_SEGMENT");
+  if (s) {
+    int v = std::atoi(s);
+    if (v >= 16 && v <= (1 << 20)) return v;
+  }
+  return 512;
+}
+
+}  // namespace pgcn
+
+using namespace pgcn;
+
+extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map *bmap, uint32_t flags,
+                                    pgcn_partition **out) {
+  PGCN_REQUIRE(csr && bmap && out, "pgcn_partition_setup: null argument");
+  *out = nullptr;
+  const int64_t n = csr->n;
+  PGCN_REQUIRE(n >= 0 && n <= INT32_MAX, "pgcn_partition_setup: n out of range");
+  PGCN_REQUIRE(csr->rowptr && bmap->owner, "pgcn_partition_setup: null rowptr or owner");
+  PGCN_REQUIRE(bmap->nparts >= 1 && bmap->self >= 0 && bmap->self < bmap->nparts,
+               "pgcn_partition_setup: bad partition count or self");
+  const int64_t *rp = csr->rowptr;
+  const int32_t *cl = csr->col;
+  const int32_t *owner = bmap->owner;
+  const int32_t self = bmap->self, nparts = bmap->nparts;
+  PGCN_REQUIRE(rp[0] == 0, "pgcn_partition_setup: rowptr[0] != 0");
+  for (int64_t v = 0; v < n; ++v)
+    PGCN_REQUIRE(rp[v + 1] >= rp[v], "pgcn_partition_setup: rowptr decreases");
+  PGCN_REQUIRE(rp[n] == 0 || cl, "pgcn_partition_setup: null col");
+  for (int64_t k = 0; k < rp[n]; ++k)
+    PGCN_REQUIRE(cl[k] >= 0 && cl[k] < n, "pgcn_partition_setup: column out of range");
+  for (int64_t v = 0; v < n; ++v)
+    PGCN_REQUIRE(owner[v] >= 0 && owner[v] < nparts, "pgcn_partition_setup: owner out of range");
+  if (!(flags & PGCN_SETUP_HOST_ONLY)) {
+    int rc = check_device();
+    if (rc) return rc;
+  }
+
+  pgcn_partition *p = new (std::nothrow) pgcn_partition();
+  if (!p) return set_error(PGCN_ENOMEM, "pgcn_partition_setup: out of host memory");
+  p->nparts = nparts;
+  p->self = self;
+  p->host_only = (flags & PGCN_SETUP_HOST_ONLY) ? 1 : 0;
+  p->segment = default_segment();
+
+  // V_i in ascending global id; local id = rank
+  std::vector<int64_t> local_of(n, -1);
+  for (int64_t v = 0; v < n; ++v)
+    if (owner[v] == self) {
+      local_of[v] = (int64_t)p->inner_gid.size();
+      p->inner_gid.push_back(v);
+    }
+  const int64_t n_in = (int64_t)p->inner_gid.size();
+  p->n_inner = n_in;
+
+  // N(v) of inner rows: self loops and duplicates removed
+  std::vector<int64_t> nb_ptr(n_in + 1, 0);
+  std::vector<int32_t> nb;
+  {
+    size_t total = 0;
+    for (int64_t i = 0; i < n_in; ++i) total += rp[p->inner_gid[i] + 1] - rp[p->inner_gid[i]];
+    nb.reserve(total);
+  }
+  for (int64_t i = 0; i < n_in; ++i) {
+    int64_t v = p->inner_gid[i];
+    size_t start = nb.size();
+    for (int64_t k = rp[v]; k < rp[v + 1]; ++k)
+      if (cl[k] != v) nb.push_back(cl[k]);
+    std::sort(nb.begin() + start, nb.end());
+    nb.erase(std::unique(nb.begin() + start, nb.end()), nb.end());
+    nb_ptr[i + 1] = (int64_t)nb.size();
+  }
+
+  // B_i ordered by (owner, global id)
+  {
+    std::vector<int32_t> bd;
+    for (int32_t u : nb)
+      if (owner[u] != self) bd.push_back(u);
+    std::sort(bd.begin(), bd.end(), [&](int32_t a, int32_t b) {
+      return owner[a] != owner[b] ? owner[a] < owner[b] : a < b;
+    });
+    bd.erase(std::unique(bd.begin(), bd.end()), bd.end());
+    p->bd_gid.assign(bd.begin(), bd.end());
+  }
+  const int64_t n_bd = (int64_t)p->bd_gid.size();
+  p->n_bd = n_bd;
+  for (int64_t k = 0; k < n_bd; ++k) local_of[p->bd_gid[k]] = n_in + k;
+  p->recv_ptr.assign(nparts + 1, 0);
+  for (int64_t g : p->bd_gid) p->recv_ptr[owner[g] + 1]++;
+  for (int32_t j = 0; j < nparts; ++j) p->recv_ptr[j + 1] += p->recv_ptr[j];
+
+  // P_i: N(v) ∪ {v}, ascending local id
+  p->rowptr.assign(n_in + 1, 0);
+  p->col.reserve(nb.size() + n_in);
+  for (int64_t i = 0; i < n_in; ++i) {
+    size_t start = p->col.size();
+    p->col.push_back((int32_t)i);
+    for (int64_t k = nb_ptr[i]; k < nb_ptr[i + 1]; ++k) p->col.push_back((int32_t)local_of[nb[k]]);
+    std::sort(p->col.begin() + start, p->col.end());
+    p->rowptr[i + 1] = (int64_t)p->col.size();
+  }
+  std::vector<int32_t>().swap(nb);
+  p->nnz = (int64_t)p->col.size();
+  p->inv_deg.resize(n_in);
+  for (int64_t i = 0; i < n_in; ++i) {
+    int64_t len = p->rowptr[i + 1] - p->rowptr[i];
+    p->inv_deg[i] = 1.0f / (float)len;
+    p->max_row = std::max(p->max_row, len);
+  }
+
+  // P_i^T by counting sort; rows visited in ascending order keep columns ascending
+  const int64_t n_all = n_in + n_bd;
+  p->rowptr_t.assign(n_all + 1, 0);
+  for (int32_t c : p->col) p->rowptr_t[c + 1]++;
+  for (int64_t r = 0; r < n_all; ++r) p->rowptr_t[r + 1] += p->rowptr_t[r];
+  p->col_t.resize(p->nnz);
+  {
+    std::vector<int64_t> fill(p->rowptr_t.begin(), p->rowptr_t.end() - 1);
+    for (int64_t i = 0; i < n_in; ++i)
+      for (int64_t k = p->rowptr[i]; k < p->rowptr[i + 1]; ++k) p->col_t[fill[p->col[k]]++] = (int32_t)i;
+  }
+  for (int64_t r = 0; r < n_all; ++r) p->max_row_t = std::max(p->max_row_t, p->rowptr_t[r + 1] - p->rowptr_t[r]);
+
+  // S_{i,j} = B_j ∩ V_i: inner u adjacent to some w owned by j (w's row lists u)
+  p->send_ptr.assign(nparts + 1, 0);
+  {
+    std::vector<uint8_t> mark((size_t)nparts * (size_t)n_in, 0);
+    for (int64_t w = 0; w < n; ++w) {
+      int32_t j = owner[w];
+      if (j == self) continue;
+      for (int64_t k = rp[w]; k < rp[w + 1]; ++k) {
+        int32_t u = cl[k];
+        if (u != w && owner[u] == self) mark[(size_t)j * n_in + local_of[u]] = 1;
+      }
+    }
+    for (int32_t j = 0; j < nparts; ++j) {
+      if (j != self)
+        for (int64_t u = 0; u < n_in; ++u)
+          if (mark[(size_t)j * n_in + u]) p->send_idx.push_back((int32_t)u);
+      p->send_ptr[j + 1] = (int64_t)p->send_idx.size();
+    }
+  }
+  p->n_send = (int64_t)p->send_idx.size();
+
+  // inverse send map: positions k per inner row, ascending k
+  p->inv_ptr.assign(n_in + 1, 0);
+  for (int32_t u : p->send_idx) p->inv_ptr[u + 1]++;
+  for (int64_t u = 0; u < n_in; ++u) p->inv_ptr[u + 1] += p->inv_ptr[u];
+  p->inv_k.resize(p->n_send);
+  {
+    std::vector<int64_t> fill(p->inv_ptr.begin(), p->inv_ptr.end() - 1);
+    for (int64_t k = 0; k < p->n_send; ++k) p->inv_k[fill[p->send_idx[k]]++] = (int32_t)k;
+  }
+
+  build_plan(p->rowptr, n_in, p->segment, p->plan);
+  build_plan(p->rowptr_t, n_all, p->segment, p->plan_t);
+
+  if (!p->host_only) {
+    PGCN_HIP(hipGetDevice(&p->device));
+    int rc = PGCN_OK;
+    if (!rc) rc = upload(&p->d_col, p->col);
+    if (!rc) rc = upload(&p->d_col_t, p->col_t);
+    if (!rc) rc = upload(&p->d_send_idx, p->send_idx);
+    if (!rc) rc = upload(&p->d_inv_k, p->inv_k);
+    if (!rc) rc = upload(&p->d_inv_ptr, p->inv_ptr);
+    if (!rc) rc = upload(&p->d_inv_deg, p->inv_deg);
+    if (!rc) rc = upload(&p->plan.d_items, p->plan.items);
+    if (!rc) rc = upload(&p->plan.d_splits, p->plan.splits);
+    if (!rc) rc = upload(&p->plan_t.d_items, p->plan_t.items);
+    if (!rc) rc = upload(&p->plan_t.d_splits, p->plan_t.splits);
+    if (rc) {
+      free_device(p);
+      delete p;
+      return rc;
+    }
+  }
+  *out = p;
+  return PGCN_OK;
+}
+
+extern "C" int pgcn_partition_info(const pgcn_partition *p, pgcn_info *o) {
+  PGCN_REQUIRE(p && o, "pgcn_partition_info: null argument");
+  o->n_inner = p->n_inner;
+  o->n_bd = p->n_bd;
+  o->nnz = p->nnz;
+  o->n_send = p->n_send;
+  o->max_row_len = p->max_row;
+  o->max_row_len_t = p->max_row_t;
+  o->nparts = p->nparts;
+  o->self = p->self;
+  o->host_only = p->host_only;
+  o->spmm_segment = p->segment;
+  o->spmm_items = (int64_t)p->plan.items.size();
+  o->spmm_split_slots = p->plan.slots;
+  o->spmmt_items = (int64_t)p->plan_t.items.size();
+  o->spmmt_split_slots = p->plan_t.slots;
+  return PGCN_OK;
+}
+
+template <class T>
+static void copy_out(T *dst, const std::vector<T> &src) {
+  if (dst && !src.empty()) std::memcpy(dst, src.data(), src.size() * sizeof(T));
+}
+
+extern "C" int pgcn_partition_export(const pgcn_partition *p, const pgcn_arrays *h) {
+  PGCN_REQUIRE(p && h, "pgcn_partition_export: null argument");
+  copy_out(h->inner_gid, p->inner_gid);
+  copy_out(h->bd_gid, p->bd_gid);
+  copy_out(h->recv_ptr, p->recv_ptr);
+  copy_out(h->rowptr, p->rowptr);
+  copy_out(h->col, p->col);
+  copy_out(h->rowptr_t, p->rowptr_t);
+  copy_out(h->col_t, p->col_t);
+  copy_out(h->send_ptr, p->send_ptr);
+  copy_out(h->send_idx, p->send_idx);
+  copy_out(h->inv_ptr, p->inv_ptr);
+  copy_out(h->inv_k, p->inv_k);
+  return PGCN_OK;
+}
+
+extern "C" void pgcn_partition_destroy(pgcn_partition *p) {
+  if (!p) return;
+  if (!p->host_only) free_device(p);
+  delete p;
+}
+
+extern "C" const char *pgcn_last_error(void) { return g_error.c_str(); }
+
+extern "C" int pgcn_version(void) { return PGCN_VERSION; }

@@ -1,0 +1,205 @@
+"""One partition's PipeGCN training step on one GPU (Algorithm 1, per-partition view).
+
+Every computation is a libpgcn call (``binding``); torch provides device
+memory, streams and events only.
+
+Pipeline emulation on one GPU: Algorithm 1 exchanges boundary features and
+boundary feature gradients with the peer partitions in background threads
+and consumes what arrived in the previous iteration.  Here each stale buffer
+is double-buffered: in iteration t the compute stream reads ``cur`` while a
+side stream refills ``next`` from an emulated peer source, ordered after this
+iteration's send (pack) by an event; the compute stream waits for that refill
+only in iteration t+1 (the paper batches all layers' communication on a
+second stream, as here).  Copy modes for measurement:
+
+* ``"pipe"``   refills on the side stream (PipeGCN);
+* ``"serial"`` refills on the compute stream before the layer that needs them
+  (the synchronous exchange of vanilla partition-parallel training);
+* ``"none"``   no refills (compute only).
+
+Smoothing (Section 3.4): ``smooth_f`` and ``smooth_g`` keep a moving average
+of the received boundary features / gradients, updated when a message is
+consumed (iteration 2 on), starting from zero.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+
+def ld_of(f: int) -> int:
+    """Row stride used for every activation matrix: a multiple of 8 elements."""
+    return (f + 7) // 8 * 8
+
+
+@dataclass
+class StepOptions:
+    smooth_f: bool = True
+    smooth_g: bool = True
+    gamma: float = 0.95
+    eta: float = 0.01
+    relu_last: bool = False
+    copy_mode: str = "pipe"          # "pipe" | "serial" | "none"
+
+
+class PartitionTrainer:
+    """Device state of one partition and its training step."""
+
+    def __init__(self, graph, X_global: np.ndarray, labels_global: np.ndarray, W0: list, widths, loss: str,
+                 loss_scale: float, gemm_dtype: str, opts: StepOptions, device="cuda:0",
+                 remote_seed: int = 1234):
+        self.dev = torch.device(device)
+        self.opts = opts
+        self.widths = list(widths)
+        self.L = len(widths) - 1
+        self.loss_kind = B.PGCN_SOFTMAX_CE if loss == "softmax_ce" else B.PGCN_SIGMOID_BCE
+        self.loss_scale = float(loss_scale)
+        self.dtype = B.PGCN_BF16 if gemm_dtype == "bf16" else B.PGCN_F32
+        with torch.cuda.device(self.dev):
+            self.part = B.pgcn_partition_setup(graph.n, graph.rowptr, graph.col, graph.owner, graph.nparts,
+                                               graph.self_part)
+        self.info = B.pgcn_partition_info(self.part)
+        n, b, s = self.info["n_inner"], self.info["n_bd"], self.info["n_send"]
+        self.n, self.b, self.s = n, b, s
+        ex = B.pgcn_partition_export(self.part)
+        self.inner_gid, self.bd_gid = ex["inner_gid"], ex["bd_gid"]
+        self.send_idx = ex["send_idx"]
+
+        z = lambda r, f, dt=torch.float32: torch.zeros((r, ld_of(f)), dtype=dt, device=self.dev)
+        L, wd = self.L, self.widths
+        f32 = self.dtype == B.PGCN_F32
+        # inputs
+        self.X = z(n, wd[0])
+        self.X[:, : wd[0]] = torch.from_numpy(np.ascontiguousarray(X_global[self.inner_gid])).to(self.dev)
+        if self.loss_kind == B.PGCN_SOFTMAX_CE:
+            self.labels = torch.from_numpy(labels_global[self.inner_gid].astype(np.int32)).to(self.dev)
+            self.targets = None
+        else:
+            self.labels = None
+            self.targets = z(n, wd[-1])
+            self.targets[:, : wd[-1]] = torch.from_numpy(labels_global[self.inner_gid]).to(self.dev)
+        self.W = [torch.from_numpy(np.ascontiguousarray(w, dtype=np.float32)).to(self.dev) for w in W0]
+        self.dW = [torch.zeros_like(w) for w in self.W]
+        self.G_peer = [None] * L
+        # activations, indexed by layer 1..L
+        self.A = {l: (z(n, wd[l - 1]) if f32 else None) for l in range(1, L + 1)}
+        self.A16 = {l: (None if f32 else z(n, wd[l - 1], torch.bfloat16)) for l in range(1, L + 1)}
+        self.H = {l: z(n, wd[l]) for l in range(1, L + 1)}
+        self.J_top = z(n, wd[L])
+        self.J_in = {l: z(n, wd[l - 1]) for l in range(2, L + 1)}
+        self.J_bd_out = {l: z(b, wd[l - 1]) for l in range(2, L + 1)}
+        # stale feature buffers (layer l reads boundary rows of H^(l-1)), gradient buffers for l >= 2
+        self.feat = {l: [z(b, wd[l - 1]), z(b, wd[l - 1])] for l in range(1, L + 1)}
+        self.ema_f = {l: z(b, wd[l - 1]) for l in range(1, L + 1)}
+        self.send_f = {l: z(s, wd[l - 1]) for l in range(1, L + 1)}
+        self.grad = {l: [z(s, wd[l - 1]), z(s, wd[l - 1])] for l in range(2, L + 1)}
+        self.ema_g = {l: z(s, wd[l - 1]) for l in range(2, L + 1)}
+        # emulated peers: what the other partitions send each iteration
+        g = torch.Generator(device="cpu").manual_seed(remote_seed)
+        self.remote_f = {l: z(b, wd[l - 1]) for l in range(1, L + 1)}
+        self.remote_g = {l: z(s, wd[l - 1]) for l in range(2, L + 1)}
+        for l in range(1, L + 1):
+            self.remote_f[l][:, : wd[l - 1]] = torch.randn((b, wd[l - 1]), generator=g).to(self.dev)
+        for l in range(2, L + 1):
+            self.remote_g[l][:, : wd[l - 1]] = (1e-3 * torch.randn((s, wd[l - 1]), generator=g)).to(self.dev)
+        self.cur = 0                      # index of the buffer read in this iteration
+        self.t = 0
+        self.loss = torch.zeros(1, dtype=torch.float32, device=self.dev)
+        ws = max(B.pgcn_workspace_size(self.part, wd[l - 1], wd[l], self.dtype) for l in range(1, L + 1))
+        self.ws_bytes = max(ws, 256)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
+        self.stream = torch.cuda.Stream(device=self.dev)
+        self.side = torch.cuda.Stream(device=self.dev)
+        self.ev_pack = {l: torch.cuda.Event() for l in range(1, L + 1)}
+        self.ev_feat = {l: torch.cuda.Event() for l in range(1, L + 1)}
+        self.ev_bwd = {l: torch.cuda.Event() for l in range(2, L + 1)}
+        self.ev_grad = {l: torch.cuda.Event() for l in range(2, L + 1)}
+        torch.cuda.synchronize(self.dev)
+
+    # ------------------------------------------------------------------
+    def _relu(self, l):
+        return l < self.L or self.opts.relu_last
+
+    def _refill(self, dst, src, stream):
+        B.pgcn_refill_async(dst, src, dst.numel() * dst.element_size(), stream)
+
+    def step(self):
+        o, L, wd = self.opts, self.L, self.widths
+        n, b, s = self.n, self.b, self.s
+        st, side = self.stream, self.side
+        self.t += 1
+        t = self.t
+        cur, nxt = self.cur, 1 - self.cur
+        mode = o.copy_mode
+
+        # ---- forward --------------------------------------------------
+        for l in range(1, L + 1):
+            f = wd[l - 1]
+            H_in = self.X if l == 1 else self.H[l - 1]
+            H_bd = None
+            if mode == "serial":
+                self._refill(self.feat[l][cur], self.remote_f[l], st)
+            if t > 1 or mode == "serial":
+                if mode == "pipe":
+                    st.wait_event(self.ev_feat[l])
+                H_bd = self.feat[l][cur]
+                if o.smooth_f:
+                    B.pgcn_smooth_ema(self.ema_f[l], H_bd, b, f, ld_of(f), o.gamma, st)
+                    H_bd = self.ema_f[l]
+            B.pgcn_pack_boundary(self.part, B.PGCN_PACK_FEAT, H_in, self.send_f[l], f, ld_of(f), st)
+            if mode == "pipe":
+                self.ev_pack[l].record(st)
+                side.wait_event(self.ev_pack[l])
+                self._refill(self.feat[l][nxt], self.remote_f[l], side)
+                self.ev_feat[l].record(side)
+            B.pgcn_layer_fwd(self.part, f_in=f, f_out=wd[l], gemm_dtype=self.dtype, relu=self._relu(l),
+                             ld_in=ld_of(f), ld_out=ld_of(wd[l]), H_in=H_in, H_bd=H_bd, W=self.W[l - 1],
+                             A=self.A[l], A_bf16=self.A16[l], H_out=self.H[l], workspace=self.ws,
+                             workspace_bytes=self.ws_bytes, stream=st)
+
+        # ---- loss -----------------------------------------------------
+        C_ = wd[L]
+        B.pgcn_loss_fwd_bwd(self.loss_kind, self.H[L], n, C_, ld_of(C_), self.labels, self.targets, ld_of(C_),
+                            self.loss_scale, self.J_top, self.loss, self.ws, self.ws_bytes, st)
+
+        # ---- backward -------------------------------------------------
+        for l in range(L, 0, -1):
+            f = wd[l - 1]
+            J_out = self.J_top if l == L else self.J_in[l + 1]
+            B.pgcn_layer_bwd(self.part, f_in=f, f_out=wd[l], gemm_dtype=self.dtype, relu=self._relu(l),
+                             ld_in=ld_of(f), ld_out=ld_of(wd[l]), J_out=J_out, H_out=self.H[l], A=self.A[l],
+                             A_bf16=self.A16[l], W=self.W[l - 1], dW=self.dW[l - 1],
+                             J_in=self.J_in.get(l), J_bd_out=self.J_bd_out.get(l), workspace=self.ws,
+                             workspace_bytes=self.ws_bytes, stream=st)
+            if l == 1:
+                break
+            if mode == "serial":
+                self._refill(self.grad[l][cur], self.remote_g[l], st)
+            if t > 1 or mode == "serial":
+                if mode == "pipe":
+                    st.wait_event(self.ev_grad[l])
+                C = self.grad[l][cur]
+                if o.smooth_g:
+                    B.pgcn_smooth_ema(self.ema_g[l], C, s, f, ld_of(f), o.gamma, st)
+                    C = self.ema_g[l]
+                B.pgcn_pack_boundary(self.part, B.PGCN_ACCUM_GRAD, C, self.J_in[l], f, ld_of(f), st)
+            if mode == "pipe":
+                self.ev_bwd[l].record(st)
+                side.wait_event(self.ev_bwd[l])
+                self._refill(self.grad[l][nxt], self.remote_g[l], side)
+                self.ev_grad[l].record(side)
+
+        # ---- AllReduce (identity on one partition, or + the injected peer sum) and SGD
+        for l in range(L):
+            B.pgcn_sgd_update(self.W[l], self.dW[l], self.G_peer[l], self.W[l].numel(), o.eta, st)
+        if mode == "pipe":
+            self.cur = nxt
+        return self.loss
+
+    def synchronize(self):
+        self.stream.synchronize()
+        self.side.synchronize()

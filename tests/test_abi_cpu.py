@@ -1,0 +1,145 @@
+"""CPU checks of the C ABI: exported symbols, the host-side partition builder
+(bit-exact against the oracle's builder) and argument errors.  No kernel is
+launched here; the partition is built with PGCN_SETUP_HOST_ONLY.
+"""
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from oracle.partition import build_partition
+from paper_2203_10428_amd import binding as B
+from paper_2203_10428_amd import configs, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "pgcn.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pgcn_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    syms = declared_symbols()
+    assert len(syms) >= 14
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (pgcn_\w+)", out))
+    missing = [s for s in syms if s not in exported]
+    assert not missing, missing
+    assert set(syms) == set(B.SIGNATURES), "binding signatures must cover exactly the header"
+    for s in syms:
+        assert getattr(B.lib, s) is not None
+    assert B.pgcn_version() == 100
+
+
+def compare(g_n, rowptr, col, owner, nparts, part):
+    ref = build_partition(g_n, rowptr, col, owner, part, nparts)
+    h = B.pgcn_partition_setup(g_n, rowptr, col, owner, nparts, part, host_only=True)
+    info = B.pgcn_partition_info(h)
+    assert info["host_only"] == 1
+    assert (info["n_inner"], info["n_bd"], info["nnz"], info["n_send"]) == \
+        (ref.n_inner, ref.n_bd, ref.nnz, len(ref.send_idx))
+    ex = B.pgcn_partition_export(h)
+    for k in ("inner_gid", "bd_gid", "recv_ptr", "rowptr", "col", "rowptr_t", "col_t", "send_ptr", "send_idx",
+              "inv_ptr", "inv_k"):
+        a, b = ex[k], getattr(ref, k)
+        assert a.shape == b.shape and np.array_equal(a, b.astype(a.dtype)), k
+    if ref.n_inner:
+        assert info["max_row_len"] == int(np.diff(ref.rowptr).max())
+    return info
+
+
+def random_sym(n, m, nparts, seed):
+    rng = np.random.default_rng(seed)
+    u, v = rng.integers(0, n, m), rng.integers(0, n, m)
+    src, dst = np.concatenate([u, v, u[:5]]), np.concatenate([v, u, v[:5]])   # duplicates + self loops
+    o = np.lexsort((dst, src))
+    rowptr = np.zeros(n + 1, np.int64)
+    np.cumsum(np.bincount(src, minlength=n), out=rowptr[1:])
+    return rowptr, dst[o].astype(np.int32), rng.integers(0, nparts, n).astype(np.int32)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_setup_bit_exact_small(seed):
+    n, nparts = [5, 40, 64, 1, 33, 90][seed], [2, 3, 4, 1, 5, 3][seed]
+    rowptr, col, owner = random_sym(n, 3 * n, nparts, seed)
+    for part in range(nparts):
+        compare(n, rowptr, col, owner, nparts, part)
+
+
+def test_setup_bit_exact_tiny_workload():
+    g = synth.tiny_uniform()
+    for part in range(2):
+        compare(g.n, g.rowptr, g.col, g.owner, g.nparts, part)
+
+
+def test_setup_empty_partition_and_isolated_nodes():
+    # partition 2 owns nothing; node 0 is isolated
+    n = 6
+    rowptr = np.array([0, 0, 1, 2, 3, 4, 4], np.int64)
+    col = np.array([2, 1, 4, 3], np.int32)
+    owner = np.array([0, 0, 1, 0, 1, 1], np.int32)
+    for part in range(3):
+        info = compare(n, rowptr, col, owner, 3, part)
+        if part == 2:
+            assert info["n_inner"] == 0 and info["nnz"] == 0
+
+
+def test_setup_heavy_rows_are_split_into_fixed_segments():
+    # a star: the hub's row is longer than the default segment
+    n = 1500
+    hub_nb = np.arange(1, n, dtype=np.int32)
+    rowptr = np.zeros(n + 1, np.int64)
+    rowptr[1] = n - 1
+    rowptr[2:] = n - 1 + np.arange(1, n)
+    col = np.concatenate([hub_nb, np.zeros(n - 1, np.int32)])
+    owner = (np.arange(n) % 2).astype(np.int32)
+    info = compare(n, rowptr, col, owner, 2, 0)
+    assert info["spmm_split_slots"] >= 2
+
+
+@pytest.mark.parametrize("bad", ["rowptr0", "decreasing", "col_range", "owner_range", "self_range"])
+def test_setup_rejects_bad_input(bad):
+    n = 4
+    rowptr = np.array([0, 1, 2, 3, 4], np.int64)
+    col = np.array([1, 0, 3, 2], np.int32)
+    owner = np.array([0, 0, 1, 1], np.int32)
+    nparts, part = 2, 0
+    if bad == "rowptr0":
+        rowptr = rowptr + 1
+    elif bad == "decreasing":
+        rowptr = np.array([0, 2, 1, 3, 4], np.int64)
+    elif bad == "col_range":
+        col = np.array([1, 0, 7, 2], np.int32)
+    elif bad == "owner_range":
+        owner = np.array([0, 0, 2, 1], np.int32)
+    else:
+        part = 2
+    with pytest.raises(B.PgcnError) as e:
+        B.pgcn_partition_setup(n, rowptr, col, owner, nparts, part, host_only=True)
+    assert e.value.code == B.PGCN_EINVAL
+    assert B.pgcn_last_error()
+
+
+def test_compute_calls_reject_host_only_handle():
+    g = synth.tiny_uniform()
+    h = B.pgcn_partition_setup(g.n, g.rowptr, g.col, g.owner, 2, 0, host_only=True)
+    with pytest.raises(B.PgcnError) as e:
+        B.pgcn_pack_boundary(h, B.PGCN_PACK_FEAT, 0, 0, 4, 4)
+    assert e.value.code == B.PGCN_EINVAL
+    # argument errors are reported without touching the device
+    with pytest.raises(B.PgcnError):
+        B.pgcn_smooth_ema(0, 0, 10, 8, 6, 0.9)          # ld < cols
+    with pytest.raises(B.PgcnError):
+        B.pgcn_loss_fwd_bwd(7, 0, 1, 1, 1, None, None, 1, 1.0, 0, 0, 0, 0)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["reddit-like-1of4", "yelp-like-1of3"])
+def test_setup_bit_exact_full_size(name):
+    w = configs.WORKLOADS[name]
+    g = configs.make_graph(w)
+    compare(g.n, g.rowptr, g.col, g.owner, g.nparts, 0)

@@ -1,0 +1,210 @@
+"""GPU parity of each libpgcn entry point against the fp64 oracle, element by
+element, on seeded random partitions (several tiles, ragged feature widths,
+rows split into segments, empty boundary input)."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import TOL, dev, host, random_partition_graph, rel_err
+from oracle import layers
+from oracle.partition import build_partition, propagation_matrix
+from paper_2203_10428_amd import binding as B
+from paper_2203_10428_amd.step import ld_of
+
+pytestmark = pytest.mark.gpu
+
+
+class Graph:
+    def __init__(self, n_inner=3000, n_pool=1500, nparts=4, mean_deg=12, seed=0, hub_deg=0):
+        self.n, self.rowptr, self.col, self.owner = random_partition_graph(n_inner, n_pool, nparts, mean_deg, seed,
+                                                                           hub_deg)
+        self.nparts = nparts
+        self.ref = build_partition(self.n, self.rowptr, self.col, self.owner, 0, nparts)
+        self.P = propagation_matrix(self.ref)
+        self.part = B.pgcn_partition_setup(self.n, self.rowptr, self.col, self.owner, nparts, 0)
+        self.info = B.pgcn_partition_info(self.part)
+
+
+@pytest.fixture(scope="module")
+def graphs():
+    return {"plain": Graph(), "hub": Graph(n_inner=2500, n_pool=900, seed=1, hub_deg=3000)}
+
+
+def ws_for(g, f_in, f_out, dt):
+    nbytes = max(B.pgcn_workspace_size(g.part, f_in, f_out, dt), 256)
+    return torch.empty(nbytes, dtype=torch.uint8, device="cuda"), nbytes
+
+
+def test_partition_device_build_matches_oracle(graphs):
+    for g in graphs.values():
+        ex = B.pgcn_partition_export(g.part)
+        for k in ("inner_gid", "bd_gid", "rowptr", "col", "rowptr_t", "col_t", "send_idx", "inv_ptr", "inv_k"):
+            assert np.array_equal(ex[k], getattr(g.ref, k).astype(ex[k].dtype)), k
+    assert graphs["hub"].info["spmm_split_slots"] > 0
+
+
+@pytest.mark.parametrize("gname", ["plain", "hub"])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("f_in,f_out", [(1, 3), (41, 47), (100, 128), (128, 64), (300, 512), (602, 256)])
+@pytest.mark.parametrize("with_bd", [True, False])
+def test_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
+    g = graphs[gname]
+    rng = np.random.default_rng(f_in * 1000 + f_out)
+    n, b = g.ref.n_inner, g.ref.n_bd
+    H_in = rng.standard_normal((n, f_in))
+    H_bd = rng.standard_normal((b, f_in)) if with_bd else np.zeros((b, f_in))
+    W = rng.uniform(-0.2, 0.2, (f_in, f_out)).astype(np.float32)
+    relu = f_out != 3
+    A_ref, Z_ref, H_ref = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), relu)
+    dtype = B.PGCN_BF16 if dt == "bf16" else B.PGCN_F32
+    dH_in = dev(H_in)
+    dH_bd = dev(H_bd) if with_bd else None
+    dW = torch.from_numpy(W).cuda()
+    A = dev(np.zeros((n, f_in)))
+    A16 = torch.zeros((n, ld_of(f_in)), dtype=torch.bfloat16, device="cuda") if dt == "bf16" else None
+    H = dev(np.zeros((n, f_out)))
+    ws, nb = ws_for(g, f_in, f_out, dtype)
+    B.pgcn_layer_fwd(g.part, f_in=f_in, f_out=f_out, gemm_dtype=dtype, relu=relu, ld_in=ld_of(f_in),
+                     ld_out=ld_of(f_out), H_in=dH_in, H_bd=dH_bd, W=dW, A=A, A_bf16=A16, H_out=H,
+                     workspace=ws, workspace_bytes=nb)
+    tol = TOL[dt]["act"]
+    assert rel_err(host(A, f_in), A_ref) < 1e-5          # aggregation is fp32 on both paths
+    if dt == "bf16":
+        assert rel_err(host(A16, f_in), A_ref) < 1e-2    # one bf16 rounding
+    assert rel_err(host(H, f_out), H_ref) < tol
+    # padding columns [f, round_up(f, 4)) of A are written as zeros
+    pad = host(A, ld_of(f_in))[:, f_in:(f_in + 3) // 4 * 4]
+    assert np.all(pad == 0)
+
+
+@pytest.mark.parametrize("gname", ["plain", "hub"])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("f_in,f_out", [(3, 1), (47, 41), (128, 100), (256, 256), (300, 512), (602, 256)])
+@pytest.mark.parametrize("input_grad", [True, False])
+def test_layer_backward(graphs, gname, dt, f_in, f_out, input_grad):
+    g = graphs[gname]
+    rng = np.random.default_rng(f_in * 7 + f_out)
+    n, b = g.ref.n_inner, g.ref.n_bd
+    A = rng.standard_normal((n, f_in))
+    Z = rng.standard_normal((n, f_out))
+    J = rng.standard_normal((n, f_out)) * 1e-2
+    W = rng.uniform(-0.2, 0.2, (f_in, f_out)).astype(np.float32)
+    relu = f_out != 1
+    dtype = B.PGCN_BF16 if dt == "bf16" else B.PGCN_F32
+    if dt == "bf16":   # the bf16 path reads A as bf16: give the oracle the same rounded A
+        A = torch.from_numpy(A).to(torch.bfloat16).double().numpy()
+    G_ref, Jf_ref = layers.layer_backward(g.P, A, Z, J, W.astype(np.float64), relu, input_grad)
+    H_out = np.maximum(Z, 0) if relu else Z                          # mask source: H > 0 <=> Z > 0
+    dA = dev(A) if dt == "f32" else None
+    dA16 = dev(A, dtype=torch.bfloat16) if dt == "bf16" else None
+    dJ, dH, dWt = dev(J), dev(H_out), torch.from_numpy(W).cuda()
+    dG = torch.zeros((f_in, f_out), device="cuda")
+    J_in = dev(np.zeros((n, f_in))) if input_grad else None
+    J_bd = dev(np.zeros((b, f_in))) if input_grad else None
+    ws, nb = ws_for(g, f_in, f_out, dtype)
+    B.pgcn_layer_bwd(g.part, f_in=f_in, f_out=f_out, gemm_dtype=dtype, relu=relu, ld_in=ld_of(f_in),
+                     ld_out=ld_of(f_out), J_out=dJ, H_out=dH, A=dA, A_bf16=dA16, W=dWt, dW=dG, J_in=J_in,
+                     J_bd_out=J_bd, workspace=ws, workspace_bytes=nb)
+    tol = TOL[dt]["grad"]
+    torch.cuda.synchronize()
+    assert rel_err(dG.cpu().numpy(), G_ref) < tol
+    if input_grad:
+        assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol
+        assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
+
+
+def test_backward_is_deterministic(graphs):
+    g = graphs["hub"]
+    rng = np.random.default_rng(3)
+    n, b = g.ref.n_inner, g.ref.n_bd
+    f_in, f_out = 300, 128
+    args = dict(f_in=f_in, f_out=f_out, gemm_dtype=B.PGCN_F32, relu=True, ld_in=ld_of(f_in), ld_out=ld_of(f_out),
+                J_out=dev(rng.standard_normal((n, f_out))), H_out=dev(rng.standard_normal((n, f_out))),
+                A=dev(rng.standard_normal((n, f_in))), A_bf16=None,
+                W=torch.from_numpy(rng.standard_normal((f_in, f_out)).astype(np.float32)).cuda())
+    outs = []
+    for _ in range(2):
+        dG = torch.zeros((f_in, f_out), device="cuda")
+        J_in, J_bd = dev(np.zeros((n, f_in))), dev(np.zeros((b, f_in)))
+        ws, nb = ws_for(g, f_in, f_out, B.PGCN_F32)
+        B.pgcn_layer_bwd(g.part, dW=dG, J_in=J_in, J_bd_out=J_bd, workspace=ws, workspace_bytes=nb, **args)
+        torch.cuda.synchronize()
+        outs.append((dG.cpu(), J_in.cpu(), J_bd.cpu()))
+    for a, b_ in zip(*outs):
+        assert torch.equal(a, b_)
+
+
+@pytest.mark.parametrize("f", [1, 5, 64, 602])
+def test_pack_and_accumulate(f):
+    # 5 partitions: an inner node is typically in several send sets (duplicates in the send list)
+    g = Graph(n_inner=1200, n_pool=2000, nparts=5, mean_deg=10, seed=7)
+    p = g.ref
+    assert len(p.send_idx) > len(np.unique(p.send_idx))
+    rng = np.random.default_rng(f)
+    H = rng.standard_normal((p.n_inner, f))
+    C = rng.standard_normal((len(p.send_idx), f))
+    Jin = rng.standard_normal((p.n_inner, f))
+    send = dev(np.zeros((len(p.send_idx), f)))
+    B.pgcn_pack_boundary(g.part, B.PGCN_PACK_FEAT, dev(H), send, f, ld_of(f))
+    assert np.array_equal(host(send, f), H[p.send_idx].astype(np.float32))
+    dJ = dev(Jin)
+    B.pgcn_pack_boundary(g.part, B.PGCN_ACCUM_GRAD, dev(C), dJ, f, ld_of(f))
+    ref = Jin.copy()
+    for j in range(g.nparts):                        # Algorithm 1: ascending peer j
+        a, b = p.send_ptr[j], p.send_ptr[j + 1]
+        ref[p.send_idx[a:b]] += C[a:b]
+    assert rel_err(host(dJ, f), ref) < 1e-6
+
+
+@pytest.mark.parametrize("rows,f", [(1, 1), (1000, 602), (4099, 41)])
+def test_smooth_ema(rows, f):
+    rng = np.random.default_rng(rows)
+    s, x = rng.standard_normal((rows, f)), rng.standard_normal((rows, f))
+    ds = dev(s)
+    B.pgcn_smooth_ema(ds, dev(x), rows, f, ld_of(f), 0.95)
+    assert rel_err(host(ds, f), layers.ema(s, x, 0.95)) < 1e-6
+
+
+@pytest.mark.parametrize("kind", ["softmax_ce", "sigmoid_bce"])
+@pytest.mark.parametrize("rows,C", [(1, 1), (5000, 41), (3001, 100), (777, 130)])
+def test_loss(kind, rows, C):
+    rng = np.random.default_rng(rows + C)
+    Z = rng.standard_normal((rows, C)) * 3
+    scale = 1.0 / (3 * rows)
+    J = dev(np.zeros((rows, C)))
+    loss = torch.zeros(1, device="cuda")
+    ws = torch.empty(max(4 * rows, 256), dtype=torch.uint8, device="cuda")
+    if kind == "softmax_ce":
+        y = rng.integers(0, C, rows).astype(np.int32)
+        B.pgcn_loss_fwd_bwd(B.PGCN_SOFTMAX_CE, dev(Z), rows, C, ld_of(C), torch.from_numpy(y).cuda(), None, 0,
+                            scale, J, loss, ws, ws.numel())
+        l_ref, J_ref = layers.softmax_ce(Z, y, scale)
+    else:
+        Y = (rng.random((rows, C)) < 0.05).astype(np.float64)
+        B.pgcn_loss_fwd_bwd(B.PGCN_SIGMOID_BCE, dev(Z), rows, C, ld_of(C), None, dev(Y), ld_of(C), scale, J, loss,
+                            ws, ws.numel())
+        l_ref, J_ref = layers.sigmoid_bce(Z, Y, scale)
+    assert abs(loss.item() - l_ref) <= 1e-4 * abs(l_ref)
+    assert rel_err(host(J, C), J_ref) < 1e-4
+
+
+def test_sgd_update():
+    rng = np.random.default_rng(0)
+    W, G, G2 = (rng.standard_normal(1000).astype(np.float32) for _ in range(3))
+    dW = torch.from_numpy(W).cuda()
+    B.pgcn_sgd_update(dW, torch.from_numpy(G).cuda(), torch.from_numpy(G2).cuda(), 1000, 0.01)
+    torch.cuda.synchronize()
+    assert rel_err(dW.cpu().numpy(), layers.sgd(W.astype(np.float64), G + G2.astype(np.float64), 0.01)) < 1e-6
+
+
+def test_entry_points_reject_bad_arguments(graphs):
+    g = graphs["hub"]                        # has split rows: the forward needs workspace
+    x = dev(np.zeros((g.ref.n_inner, 8)))
+    with pytest.raises(B.PgcnError) as e:
+        B.pgcn_layer_fwd(g.part, f_in=8, f_out=8, gemm_dtype=B.PGCN_F32, relu=True, ld_in=8, ld_out=8, H_in=x,
+                         H_bd=None, W=torch.zeros((8, 8), device="cuda"), A=x, A_bf16=None, H_out=x,
+                         workspace=None, workspace_bytes=0)
+    assert e.value.code == B.PGCN_EWORKSPACE
+    with pytest.raises(B.PgcnError) as e:   # stride not a multiple of 4
+        B.pgcn_smooth_ema(x, x, 10, 6, 6, 0.5)
+    assert e.value.code == B.PGCN_EINVAL
