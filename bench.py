@@ -1,0 +1,249 @@
+#!/usr/bin/env python3
+"""Benchmark of one partition's PipeGCN training step on one MI355X.
+
+Default workload: one of 4 partitions of a 233K-node dense-community graph
+(58,000 inner nodes, ~30,000 boundary nodes, power-law degree with mean row
+length ~495 and max ~18.6K, 602-dim features, 4 GCN layers 602-256-256-256-41,
+softmax cross-entropy, fp32 update GEMMs, fp32 aggregation), PipeGCN-GF
+(smoothing of stale features and gradients, decay 0.95), stale-buffer
+refills on a side stream.  One "step" is one full iteration of Algorithm 1
+for the partition: forward, loss, backward, stale-gradient accumulation,
+smoothing, packing, refills and the SGD update.
+
+Prints ONE JSON line.  ``value`` = partition train-steps/s with all inputs
+resident in HBM.  ``roofline`` is computed for the kernel with the largest
+total time, from per-launch durations measured with HIP events recorded on
+the launch stream during the timed steps.  ``cpu_baseline`` is the fp64
+oracle's per-partition step timed on the host for a bounded sample of the
+same workload, scaled to the full partition.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+VARIANTS = {"PipeGCN": (False, False), "PipeGCN-G": (False, True), "PipeGCN-F": (True, False),
+            "PipeGCN-GF": (True, True)}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_work(tr, w):
+    """Per-step algorithmic bytes / flops of each kernel kind.
+
+    Aggregation, compulsory model: every index once, every input feature row
+    once, every output row once.  Gather model: every non-zero gathers one
+    full input row.  GEMMs: 2*M*N*K flops.
+    """
+    i = tr.info
+    n, b, e = i["n_inner"], i["n_bd"], i["nnz"]
+    items, items_t = i["spmm_items"], i["spmmt_items"]
+    L, wd = tr.L, tr.widths
+    bf16 = w.gemm_dtype == "bf16"
+    f4 = lambda f: (f + 3) // 4 * 4
+    out = {k: 0.0 for k in ("agg_fwd", "agg_bwd", "agg_fwd_gather", "agg_bwd_gather", "gemm_fwd", "gemm_dgrad",
+                            "gemm_wgrad")}
+    for l in range(1, L + 1):
+        f = wd[l - 1]
+        idx = e * 4 + items * 16
+        out["agg_fwd"] += idx + (n + b) * f * 4 + n * f4(f) * (6 if bf16 else 4)
+        out["agg_fwd_gather"] += idx + e * f4(f) * 4 + n * f4(f) * (6 if bf16 else 4)
+        out["gemm_fwd"] += 2.0 * n * f * wd[l]
+        out["gemm_wgrad"] += 2.0 * n * f * wd[l]
+        if l > 1:
+            idx_t = e * 4 + items_t * 16
+            out["agg_bwd"] += idx_t + n * f * 4 + (n + b) * f4(f) * 4
+            out["agg_bwd_gather"] += idx_t + e * f4(f) * 4 + (n + b) * f4(f) * 4
+            out["gemm_dgrad"] += 2.0 * n * f * wd[l]
+    return out
+
+
+def cpu_baseline(w, scale: float):
+    """Time the fp64 oracle's per-partition step on a sample of the workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle.partition import build_partition, propagation_matrix
+    from oracle.pipegcn import Options, partition_step
+    from paper_2203_10428_amd import configs
+
+    ws = configs.with_inner_scale(w, scale)
+    g = configs.make_graph(ws)
+    d = configs.make_dense(ws, g.n)
+    p = build_partition(g.n, g.rowptr, g.col, g.owner, 0, g.nparts)
+    P = propagation_matrix(p)
+    rng = np.random.default_rng(7)
+    L = w.layers
+    recv_f = {l: rng.standard_normal((p.n_bd, w.widths[l - 1])) for l in range(1, L + 1)}
+    recv_g = {l: 1e-3 * rng.standard_normal((len(p.send_idx), w.widths[l - 1])) for l in range(2, L + 1)}
+    ema_f = {l: np.zeros_like(v) for l, v in recv_f.items()}
+    ema_g = {l: np.zeros_like(v) for l, v in recv_g.items()}
+    sf, sg = VARIANTS["PipeGCN-GF"]
+    opts = Options(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, loss=w.loss, loss_scale=w.loss_scale,
+                   gemm="bf16" if w.gemm_dtype == "bf16" else "f64")
+    y = d.labels[p.inner_gid]
+    X_in = d.X[p.inner_gid]
+    t0 = time.perf_counter()
+    partition_step(p, P, X_in, y, [x.astype(np.float64) for x in d.W], recv_f, recv_g, ema_f, ema_g, 2, opts)
+    sec = time.perf_counter() - t0
+    blas_threads = max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
+    return sec, p.n_inner, p.nnz, blas_threads
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="reddit-like-1of4")
+    ap.add_argument("--variant", default="PipeGCN-GF", choices=list(VARIANTS))
+    ap.add_argument("--no-copy-modes", action="store_true", help="skip the serial / no-refill comparison")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=float, default=0.25, help="inner-node fraction timed on the CPU")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one partition on one GPU; runs on more than one GPU are not part of this "
+              "build (the multi-GPU exchange is a design, see DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2203_10428_amd import binding as B
+    from paper_2203_10428_amd import configs
+    from paper_2203_10428_amd.step import PartitionTrainer, StepOptions
+
+    w = configs.WORKLOADS[args.workload]
+    t0 = time.perf_counter()
+    g = configs.make_graph(w)
+    d = configs.make_dense(w, g.n)
+    log(f"workload {w.name}: graph {g.stats} generated in {time.perf_counter() - t0:.1f}s")
+    sf, sg = VARIANTS[args.variant]
+    tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, w.gemm_dtype,
+                          StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe"))
+    del d
+    log(f"partition set up: {tr.info}")
+
+    def timed(k, mode):
+        tr.opts.copy_mode = mode
+        torch.cuda.synchronize()
+        s = time.perf_counter()
+        for _ in range(k):
+            tr.step()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - s) / k * 1e3
+
+    for _ in range(args.warmup):
+        tr.step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    # timed region: exactly --steps steps, kernel events recorded on their launch streams
+    B.pgcn_trace_enable(max(1024, args.steps * 256))
+    ms_per_step = timed(args.steps, "pipe")
+    records = B.pgcn_trace_collect(args.steps * 256)
+    B.pgcn_trace_disable()
+    loss = tr.loss.item()
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, loss {loss:.6f}")
+
+    kinds = {}
+    for k, ms in records:
+        c = kinds.setdefault(k, [0, 0.0])
+        c[0] += 1
+        c[1] += ms
+    per_step = {k: {"launches": c[0] / args.steps, "ms_per_step": c[1] / args.steps,
+                    "avg_launch_ms": c[1] / c[0]} for k, c in kinds.items()}
+    work = algorithmic_work(tr, w)
+    dt = "bf16" if w.gemm_dtype == "bf16" else "f32"
+    compute_kinds = ["agg_fwd", "agg_bwd", "gemm_fwd", "gemm_dgrad", "gemm_wgrad"]
+    dominant = max((k for k in compute_kinds if k in per_step), key=lambda k: per_step[k]["ms_per_step"])
+    util = {}
+    for k in compute_kinds:
+        if k not in per_step:
+            continue
+        sec = per_step[k]["ms_per_step"] / 1e3
+        if k.startswith("agg"):
+            util[k] = {"GBps_compulsory": work[k] / sec / 1e9, "GBps_gather_model": work[k + "_gather"] / sec / 1e9}
+        else:
+            util[k] = {"TFLOPs": work[k] / sec / 1e12, "mfma_frac": work[k] / sec / 1e12 / MFMA_PEAK_TFLOPS[dt]}
+    if dominant.startswith("agg"):
+        ach = util[dominant]["GBps_compulsory"]
+        roof = {"bound": "hbm", "kernel": dominant, "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": ach / HBM_PEAK_GBPS, "traffic": None,
+                "gather_model_GBps": util[dominant]["GBps_gather_model"],
+                "algorithmic_bytes_per_step": work[dominant],
+                "launches_per_step": per_step[dominant]["launches"],
+                "avg_launch_ms": per_step[dominant]["avg_launch_ms"]}
+    else:
+        ach = util[dominant]["TFLOPs"]
+        roof = {"bound": "mfma", "kernel": dominant, "achieved": ach, "peak": MFMA_PEAK_TFLOPS[dt],
+                "unit": "TFLOP/s", "frac": ach / MFMA_PEAK_TFLOPS[dt], "traffic": None,
+                "algorithmic_flops_per_step": work[dominant],
+                "launches_per_step": per_step[dominant]["launches"],
+                "avg_launch_ms": per_step[dominant]["avg_launch_ms"]}
+
+    copy_modes = None
+    if not args.no_copy_modes:
+        k2 = max(3, args.steps // 2)
+        copy_modes = {m: timed(k2, m) for m in ("none", "serial", "pipe")}
+        copy_modes["hidden"] = copy_modes["pipe"] <= 1.03 * copy_modes["none"]
+        log(f"copy modes (ms/step): {copy_modes}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        try:
+            sec, n_s, nnz_s, threads = cpu_baseline(w, args.cpu_sample)
+            scale = tr.info["nnz"] / nnz_s
+            cpu = {"value": 1.0 / (sec * scale), "unit": "steps/s", "cores": threads, "kind": "oracle",
+                   "sample": (f"fp64 oracle per-partition step (PipeGCN-GF, t=2) on the same graph law at "
+                              f"{args.cpu_sample:g} of the inner/pool nodes ({n_s} inner rows, {nnz_s} nnz) took "
+                              f"{sec:.2f}s; scaled by the nnz ratio {scale:.2f} to the full partition; SciPy's "
+                              f"sparse products run single-threaded, dense products use {threads} BLAS threads")}
+            log(f"cpu baseline: {cpu}")
+        except Exception as exc:  # the baseline must never hide the GPU result
+            cpu = {"value": None, "unit": "steps/s", "cores": os.cpu_count(), "kind": "oracle",
+                   "sample": f"failed: {exc!r}"}
+
+    i = tr.info
+    line = {
+        "metric": "partition train-steps/sec (fwd+bwd, 4-layer); SpMM HBM GB/s; GEMM MFMA util",
+        "value": 1e3 / ms_per_step,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic",
+        "config": {"workload": w.name, "variant": args.variant, "copy_mode": "pipe", "widths": list(w.widths),
+                   "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",
+                   "n_inner": i["n_inner"], "n_bd": i["n_bd"], "n_send": i["n_send"], "nnz": i["nnz"],
+                   "max_row_len": i["max_row_len"], "parallelism": "1 partition / 1 GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernels": per_step,
+        "utilisation": util,
+        "copy_modes_ms_per_step": copy_modes,
+        "loss": loss,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -251,6 +251,24 @@ int pgcn_sgd_update(float *W, const float *G, const float *G_peer, int64_t count
  * enqueued on `stream`. */
 int pgcn_refill_async(void *dst, const void *src, size_t bytes, hipStream_t stream);
 
+/*
+ * Kernel tracing (measurement support).  While enabled, every kernel launch
+ * (and every refill copy) of the library is bracketed by a HIP event pair
+ * recorded on the launch stream; pgcn_trace_collect waits for the recorded
+ * pairs and returns each launch's kind (pgcn_trace_kind) and duration in ms,
+ * then clears the record.  pgcn_trace_enable creates `capacity` event pairs
+ * up front; launches beyond the capacity are not recorded.  Not for use
+ * under graph capture.
+ */
+enum pgcn_trace_kind {
+  PGCN_TK_AGG_FWD = 0, PGCN_TK_AGG_BWD = 1, PGCN_TK_AGG_FIXUP = 2, PGCN_TK_GEMM_FWD = 3,
+  PGCN_TK_GEMM_DGRAD = 4, PGCN_TK_GEMM_WGRAD = 5, PGCN_TK_WGRAD_REDUCE = 6, PGCN_TK_EMA = 7,
+  PGCN_TK_PACK = 8, PGCN_TK_ACCUM = 9, PGCN_TK_LOSS = 10, PGCN_TK_SGD = 11, PGCN_TK_REFILL = 12
+};
+int pgcn_trace_enable(int32_t capacity);
+int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t max_records, int32_t *count);
+int pgcn_trace_disable(void);
+
 const char *pgcn_last_error(void);
 int pgcn_version(void);
 

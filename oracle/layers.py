@@ -12,6 +12,11 @@ PipeGCN forward equation in Section 3.2):
     G      = Aᵀ M           (weight gradient, from the saved A)
     J_full = Pᵀ (M Wᵀ)      (gradient of every input row, inner and boundary)
 
+The paper fixes no precision.  ``gemm="bf16"`` is the reading used for the
+bf16 update-GEMM path: the aggregation stays exact, and the operands of the
+three products (A, W, M) are rounded to bfloat16 before an exact product, so
+that the ReLU mask is decided from the same rounded operands as on the GPU.
+
 The paper writes the aggregation as the product P H W; aggregating first and
 transforming first in the backward are the same matrix products in another
 association (the reading is listed with the others in the design notes).
@@ -24,18 +29,42 @@ from __future__ import annotations
 import numpy as np
 
 
-def layer_forward(P, H_full: np.ndarray, W: np.ndarray, relu: bool):
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round to bfloat16, nearest-even, through float32 (the GPU rounds its fp32 values).
+
+    bfloat16 keeps the sign, the 8 exponent bits and the top 7 mantissa bits of
+    a float32; rounding adds half of the dropped part's unit, with ties to the
+    even kept value.  NaN stays NaN.
+    """
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    r = (((u + 0x7FFF + lsb) >> 16) << 16).astype(np.uint32)
+    out = r.view(np.float32).astype(np.float64)
+    nan = np.isnan(f)
+    if nan.any():
+        out[nan] = np.nan
+    return out
+
+
+def _operand(x, gemm: str):
+    return round_bf16(x) if gemm == "bf16" else x
+
+
+def layer_forward(P, H_full: np.ndarray, W: np.ndarray, relu: bool, gemm: str = "f64"):
+    """``gemm="bf16"`` rounds both GEMM operands to bf16 first (products and sums stay fp64)."""
     A = P @ H_full
-    Z = A @ W
+    Z = _operand(A, gemm) @ _operand(W, gemm)
     H = np.maximum(Z, 0.0) if relu else Z
     return A, Z, H
 
 
 def layer_backward(P, A: np.ndarray, Z: np.ndarray, J: np.ndarray, W: np.ndarray,
-                   relu: bool, input_grad: bool):
+                   relu: bool, input_grad: bool, gemm: str = "f64"):
     M = J * (Z > 0.0) if relu else J
-    G = A.T @ M
-    J_full = (P.T @ (M @ W.T)) if input_grad else None
+    Mq = _operand(M, gemm)
+    G = _operand(A, gemm).T @ Mq
+    J_full = (P.T @ (Mq @ _operand(W, gemm).T)) if input_grad else None
     return G, J_full
 
 

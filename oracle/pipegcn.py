@@ -56,6 +56,7 @@ class Options:
     relu_last: bool = False
     x_bd_preload: bool = False
     ema_init: str = "zero"          # "zero" | "first"
+    gemm: str = "f64"               # "f64" | "bf16" (operands of the update products rounded to bf16)
 
 
 @dataclass
@@ -162,7 +163,7 @@ class Simulation:
                     Hbd = self.state[i].feat_buf[l]
                 rec[i]["H_bd_used"][l] = Hbd.copy()
                 A, Z, H = layers.layer_forward(self.P[i], np.vstack([H_prev[i], Hbd]), self.W[l - 1],
-                                               self._relu(l))
+                                               self._relu(l), o.gemm)
                 rec[i]["A"][l], rec[i]["Z"][l], rec[i]["H"][l] = A, Z, H
                 H_prev[i] = H
             if pipe:
@@ -183,7 +184,7 @@ class Simulation:
             J_full = [None] * self.nparts
             for i, p in enumerate(self.parts):
                 G, Jf = layers.layer_backward(self.P[i], rec[i]["A"][l], rec[i]["Z"][l], J[i],
-                                              self.W[l - 1], self._relu(l), l > 1)
+                                              self.W[l - 1], self._relu(l), l > 1, o.gemm)
                 rec[i]["G"][l] = G
                 G_sum[l - 1] = G if G_sum[l - 1] is None else G_sum[l - 1] + G
                 J_full[i] = Jf
@@ -242,3 +243,51 @@ def run(n, rowptr, col, owner, nparts, X, labels, W0, T, opts: Options):
     """Simulate T iterations; returns the simulation and the per-iteration records."""
     sim = Simulation(n, rowptr, col, owner, nparts, X, labels, W0, opts)
     return sim, [sim.step() for _ in range(T)]
+
+
+def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: dict, ema_f: dict, ema_g: dict,
+                   t: int, opts: Options):
+    """One iteration of Algorithm 1 for one partition, given what it received.
+
+    ``received_f[l]`` ([b, f_{l-1}]) and ``received_g[l]`` ([s, f_{l-1}], l >= 2)
+    are the messages of iteration t-1 (ignored at t = 1); ``ema_f`` / ``ema_g``
+    are the smoothing states, updated in place when a message is consumed.
+    Returns a record with the same keys as a Simulation record (A, Z, H, loss,
+    J_full, G, send_f) and the partition's weight gradients, without applying
+    the update.  Pipelined mode; ``ema_init`` "zero"; no boundary preload.
+    """
+    o = opts
+    L = len(W)
+    rec = dict(A={}, Z={}, H={}, J_full={}, G={}, send_f={})
+    H = np.asarray(X_in, dtype=np.float64)
+    for l in range(1, L + 1):
+        rec["send_f"][l] = H[p.send_idx]
+        if t > 1:
+            Hbd = received_f[l]
+            if o.smooth_f:
+                ema_f[l] = layers.ema(ema_f[l], Hbd, o.gamma)
+                Hbd = ema_f[l]
+        else:
+            Hbd = np.zeros((p.n_bd, H.shape[1]))
+        relu = l < L or o.relu_last
+        A, Z, H = layers.layer_forward(P, np.vstack([H, Hbd]), W[l - 1], relu, o.gemm)
+        rec["A"][l], rec["Z"][l], rec["H"][l] = A, Z, H
+    f = layers.softmax_ce if o.loss == "softmax_ce" else layers.sigmoid_bce
+    rec["loss"], J = f(H, y, o.loss_scale)
+    for l in range(L, 0, -1):
+        relu = l < L or o.relu_last
+        G, Jf = layers.layer_backward(P, rec["A"][l], rec["Z"][l], J, W[l - 1], relu, l > 1, o.gemm)
+        rec["G"][l] = G
+        if l == 1:
+            break
+        if t > 1:
+            C = received_g[l]
+            if o.smooth_g:
+                ema_g[l] = layers.ema(ema_g[l], C, o.gamma)
+                C = ema_g[l]
+            for j in range(len(p.send_ptr) - 1):
+                a, b = p.send_ptr[j], p.send_ptr[j + 1]
+                Jf[p.send_idx[a:b]] += C[a:b]
+        rec["J_full"][l] = Jf
+        J = Jf[: p.n_inner]
+    return rec

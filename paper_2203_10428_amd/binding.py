@@ -12,6 +12,10 @@ import ctypes as C
 import os
 
 import numpy as np
+# torch ships its own HIP runtime (SONAME libamdhip64.so.7).  Loading torch
+# first makes libpgcn bind to that already-loaded runtime, so the process has
+# one HIP/HSA runtime shared by torch's allocator and streams and libpgcn.
+import torch  # noqa: F401
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libpgcn.so")
@@ -73,6 +77,9 @@ SIGNATURES = {
     "pgcn_loss_fwd_bwd": (_i32, [_i32, _vp, _i64, _i32, _i64, _vp, _vp, _i64, _f32, _vp, _vp, _vp, _sz, _vp]),
     "pgcn_sgd_update": (_i32, [_vp, _vp, _vp, _i64, _f32, _vp]),
     "pgcn_refill_async": (_i32, [_vp, _vp, _sz, _vp]),
+    "pgcn_trace_enable": (_i32, [_i32]),
+    "pgcn_trace_collect": (_i32, [_vp, _vp, _i32, C.POINTER(_i32)]),
+    "pgcn_trace_disable": (_i32, []),
     "pgcn_last_error": (C.c_char_p, []),
     "pgcn_version": (_i32, []),
 }
@@ -217,6 +224,27 @@ def pgcn_sgd_update(W, G, G_peer, count: int, eta: float, stream=None):
 
 def pgcn_refill_async(dst, src, nbytes: int, stream=None):
     _check(lib.pgcn_refill_async(_ptr(dst), _ptr(src), nbytes, _stream(stream)), "pgcn_refill_async")
+
+
+TRACE_KINDS = ["agg_fwd", "agg_bwd", "agg_fixup", "gemm_fwd", "gemm_dgrad", "gemm_wgrad", "wgrad_reduce", "ema",
+               "pack", "accum", "loss", "sgd", "refill"]
+
+
+def pgcn_trace_enable(capacity: int):
+    _check(lib.pgcn_trace_enable(capacity), "pgcn_trace_enable")
+
+
+def pgcn_trace_collect(max_records: int = 1 << 16):
+    """[(kind name, ms)] of the launches recorded since the last collect."""
+    kinds = np.zeros(max_records, np.int32)
+    ms = np.zeros(max_records, np.float32)
+    cnt = C.c_int32(0)
+    _check(lib.pgcn_trace_collect(kinds.ctypes.data, ms.ctypes.data, max_records, C.byref(cnt)), "pgcn_trace_collect")
+    return [(TRACE_KINDS[k], float(v)) for k, v in zip(kinds[: cnt.value], ms[: cnt.value])]
+
+
+def pgcn_trace_disable():
+    _check(lib.pgcn_trace_disable(), "pgcn_trace_disable")
 
 
 def pgcn_last_error() -> str:

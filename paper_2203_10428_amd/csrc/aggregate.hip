@@ -148,7 +148,8 @@ __global__ __launch_bounds__(256) void agg_fixup_kernel(AggParams p, const Split
 }
 
 template <int LPR, int NV>
-static void launch_variant(const AggParams &p, hipStream_t s) {
+static void launch_variant(const AggParams &p, hipStream_t s, int32_t trace_kind) {
+  TraceScope ts(trace_kind, s);
   constexpr int U = NV >= 3 ? 2 : (NV == 2 ? 4 : 8);
   const int64_t groups = 256 / LPR;
   const int64_t blocks = (p.n_items + groups - 1) / groups;
@@ -186,16 +187,17 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
     const int cnt = f4 - off < 256 ? f4 - off : 256;
     p.c4_off = off;
     p.c4_cnt = cnt;
-    if (cnt <= 4) launch_variant<4, 1>(p, s);
-    else if (cnt <= 8) launch_variant<8, 1>(p, s);
-    else if (cnt <= 16) launch_variant<16, 1>(p, s);
-    else if (cnt <= 32) launch_variant<32, 1>(p, s);
-    else if (cnt <= 64) launch_variant<64, 1>(p, s);
-    else if (cnt <= 128) launch_variant<64, 2>(p, s);
-    else if (cnt <= 192) launch_variant<64, 3>(p, s);
-    else launch_variant<64, 4>(p, s);
+    if (cnt <= 4) launch_variant<4, 1>(p, s, a.trace_kind);
+    else if (cnt <= 8) launch_variant<8, 1>(p, s, a.trace_kind);
+    else if (cnt <= 16) launch_variant<16, 1>(p, s, a.trace_kind);
+    else if (cnt <= 32) launch_variant<32, 1>(p, s, a.trace_kind);
+    else if (cnt <= 64) launch_variant<64, 1>(p, s, a.trace_kind);
+    else if (cnt <= 128) launch_variant<64, 2>(p, s, a.trace_kind);
+    else if (cnt <= 192) launch_variant<64, 3>(p, s, a.trace_kind);
+    else launch_variant<64, 4>(p, s, a.trace_kind);
     PGCN_HIP(hipGetLastError());
     if (!plan.splits.empty()) {
+      TraceScope ts(PGCN_TK_AGG_FIXUP, s);
       hipLaunchKernelGGL(agg_fixup_kernel, dim3((unsigned)plan.splits.size()), dim3(256), 0, s, p,
                          plan.d_splits);
       PGCN_HIP(hipGetLastError());

@@ -84,6 +84,7 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   g.ld_in = a->ld_in;
   g.ld_out = a->ld_in;
   g.partials = (float *)a->workspace;
+  g.trace_kind = PGCN_TK_AGG_FWD;
   rc = launch_aggregate(g, s);
   if (rc) return rc;
 
@@ -189,6 +190,7 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   t.ld_in = ld_d;
   t.ld_out = a->ld_in;
   t.partials = partials;
+  t.trace_kind = PGCN_TK_AGG_BWD;
   return launch_aggregate(t, s);
 }
 
@@ -240,6 +242,7 @@ extern "C" int pgcn_sgd_update(float *W, const float *G, const float *G_peer, in
 extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, hipStream_t s) {
   if (bytes == 0) return PGCN_OK;
   PGCN_REQUIRE(dst && src, "pgcn_refill_async: null buffer");
+  TraceScope ts(PGCN_TK_REFILL, s);
   PGCN_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, s));
   return PGCN_OK;
 }

@@ -33,6 +33,7 @@ int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_
   const int f4 = (cols + 3) / 4;
   const int64_t total = rows * f4;
   if (total == 0) return PGCN_OK;
+  TraceScope ts(PGCN_TK_EMA, s);
   hipLaunchKernelGGL(ema_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, state, in, rows, f4,
                      ld, gamma);
   PGCN_HIP(hipGetLastError());
@@ -54,6 +55,7 @@ int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst,
   const int f4 = (cols + 3) / 4;
   const int64_t total = count * f4;
   if (total == 0) return PGCN_OK;
+  TraceScope ts(PGCN_TK_PACK, s);
   hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, idx, count, src, dst,
                      f4, ld);
   PGCN_HIP(hipGetLastError());
@@ -85,6 +87,7 @@ int launch_accum(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, con
   const int f4 = (cols + 3) / 4;
   const int64_t total = rows * f4;
   if (total == 0) return PGCN_OK;
+  TraceScope ts(PGCN_TK_ACCUM, s);
   hipLaunchKernelGGL(accum_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, inv_ptr, inv_k, rows,
                      src, dst, f4, ld);
   PGCN_HIP(hipGetLastError());
@@ -168,6 +171,7 @@ size_t loss_workspace(int64_t rows) { return (size_t)rows * sizeof(float); }
 int launch_loss(int32_t kind, const float *Z, int64_t rows, int32_t C, int64_t ld, const int32_t *labels,
                 const float *targets, int64_t ld_t, float scale, float *J, float *loss_out, float *ws,
                 hipStream_t s) {
+  TraceScope ts(PGCN_TK_LOSS, s);
   if (rows > 0) {
     const unsigned blocks = (unsigned)((rows + 3) / 4);
     if (kind == PGCN_SOFTMAX_CE)
@@ -192,6 +196,7 @@ __global__ __launch_bounds__(256) void sgd_kernel(float *W, const float *G, cons
 
 int launch_sgd(float *W, const float *G, const float *G2, int64_t count, float eta, hipStream_t s) {
   if (count == 0) return PGCN_OK;
+  TraceScope ts(PGCN_TK_SGD, s);
   hipLaunchKernelGGL(sgd_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, W, G, G2, count, eta);
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;

@@ -477,6 +477,7 @@ size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K) {
 
 template <int BN, int AK, int BKd, int EK>
 static int run(const GP &p0, int bf16, int splits, hipStream_t s) {
+  TraceScope ts(EK == E_PARTIAL ? PGCN_TK_GEMM_WGRAD : (EK == E_ROWSCALE ? PGCN_TK_GEMM_DGRAD : PGCN_TK_GEMM_FWD), s);
   constexpr int BM = 128;
   GP p = p0;
   const int tm = (p.M + BM - 1) / BM, tn = (p.N + BN - 1) / BN;
@@ -539,6 +540,7 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
       int rc = run_bn<A_KM_F32, B_KN_MASK, E_PARTIAL>(p, bf16, splits, s);
       if (rc) return rc;
       const int64_t mn = (int64_t)g.M * g.N;
+      TraceScope ts(PGCN_TK_WGRAD_REDUCE, s);
       hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0, s,
                          (const float *)g.workspace, splits, mn, g.C);
       PGCN_HIP(hipGetLastError());

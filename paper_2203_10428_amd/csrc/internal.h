@@ -59,6 +59,20 @@ struct pgcn_partition {
 namespace pgcn {
 
 int set_error(int code, const std::string &msg);
+
+// Records a HIP event pair around a kernel launch on stream `s` while tracing
+// is enabled (pgcn_trace_enable); does nothing otherwise.
+class TraceScope {
+ public:
+  TraceScope(int32_t kind, hipStream_t s);
+  ~TraceScope();
+  TraceScope(const TraceScope &) = delete;
+  TraceScope &operator=(const TraceScope &) = delete;
+
+ private:
+  hipStream_t s_;
+  int64_t slot_ = -1;
+};
 int check_hip(hipError_t e, const char *what);
 
 #define PGCN_HIP(call)                                   \
@@ -92,6 +106,7 @@ struct AggArgs {
   int32_t f;
   int64_t ld_in, ld_out;
   float *partials;
+  int32_t trace_kind;      // PGCN_TK_AGG_FWD or PGCN_TK_AGG_BWD
 };
 int launch_aggregate(const AggArgs &a, hipStream_t s);
 size_t aggregate_workspace(const Plan &plan, int64_t f);

@@ -1,0 +1,87 @@
+// Kernel tracing: when enabled, every kernel launch of the library is
+// bracketed by a pair of HIP events recorded on the launch stream, so the
+// caller can read per-kernel durations measured on the stream the kernel ran
+// on.  Event pairs are created once by pgcn_trace_enable (no allocation while
+// tracing); launches beyond the capacity are not recorded.
+#include <mutex>
+
+#include "internal.h"
+
+namespace pgcn {
+
+namespace {
+struct TraceState {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> start, stop;
+  std::vector<int32_t> kind;
+  size_t used = 0;
+};
+TraceState &state() {
+  static TraceState s;
+  return s;
+}
+}  // namespace
+
+TraceScope::TraceScope(int32_t kind, hipStream_t s) : s_(s) {
+  TraceState &t = state();
+  if (!t.on) return;
+  std::lock_guard<std::mutex> g(t.mu);
+  if (!t.on || t.used >= t.start.size()) return;
+  slot_ = (int64_t)t.used++;
+  t.kind[slot_] = kind;
+  (void)hipEventRecord(t.start[slot_], s_);
+}
+
+TraceScope::~TraceScope() {
+  if (slot_ < 0) return;
+  TraceState &t = state();
+  (void)hipEventRecord(t.stop[slot_], s_);
+}
+
+}  // namespace pgcn
+
+using namespace pgcn;
+
+extern "C" int pgcn_trace_enable(int32_t capacity) {
+  PGCN_REQUIRE(capacity > 0 && capacity <= (1 << 20), "pgcn_trace_enable: capacity out of range");
+  TraceState &t = state();
+  std::lock_guard<std::mutex> g(t.mu);
+  for (auto e : t.start) (void)hipEventDestroy(e);
+  for (auto e : t.stop) (void)hipEventDestroy(e);
+  t.start.assign(capacity, nullptr);
+  t.stop.assign(capacity, nullptr);
+  t.kind.assign(capacity, -1);
+  for (int32_t i = 0; i < capacity; ++i) {
+    PGCN_HIP(hipEventCreate(&t.start[i]));
+    PGCN_HIP(hipEventCreate(&t.stop[i]));
+  }
+  t.used = 0;
+  t.on = true;
+  return PGCN_OK;
+}
+
+extern "C" int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t max_records, int32_t *count) {
+  PGCN_REQUIRE(count && max_records >= 0 && (max_records == 0 || (kinds && ms)), "pgcn_trace_collect: bad arguments");
+  TraceState &t = state();
+  std::lock_guard<std::mutex> g(t.mu);
+  const int32_t n = (int32_t)(t.used < (size_t)max_records ? t.used : (size_t)max_records);
+  for (int32_t i = 0; i < n; ++i) {
+    PGCN_HIP(hipEventSynchronize(t.stop[i]));
+    float v = 0.f;
+    PGCN_HIP(hipEventElapsedTime(&v, t.start[i], t.stop[i]));
+    kinds[i] = t.kind[i];
+    ms[i] = v;
+  }
+  *count = n;
+  t.used = 0;
+  return PGCN_OK;
+}
+
+extern "C" int pgcn_trace_disable(void) {
+  TraceState &t = state();
+  std::lock_guard<std::mutex> g(t.mu);
+  t.on = false;
+  t.used = 0;
+  return PGCN_OK;
+}

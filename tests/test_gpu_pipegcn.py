@@ -27,12 +27,12 @@ VARIANTS = {"PipeGCN": (False, False), "PipeGCN-G": (False, True), "PipeGCN-F": 
             "PipeGCN-GF": (True, True)}
 
 
-def tiny_setup(T, smooth_f, smooth_g):
+def tiny_setup(T, smooth_f, smooth_g, gemm="f64"):
     w = configs.TINY
     g = configs.make_graph(w)
     d = configs.make_dense(w, g.n)
     opts = Options(mode="pipe", smooth_f=smooth_f, smooth_g=smooth_g, gamma=w.gamma, eta=w.eta,
-                   loss=w.loss, loss_scale=w.loss_scale)
+                   loss=w.loss, loss_scale=w.loss_scale, gemm=gemm)
     sim, recs = run(g.n, g.rowptr, g.col, g.owner, g.nparts, d.X, d.labels, d.W, T, opts)
     return w, g, d, sim, recs
 
@@ -76,7 +76,8 @@ def compare_step(tr: PartitionTrainer, rec0, dt, L, widths, check_state=True):
 def test_tiny_injected(variant, dt):
     sf, sg = VARIANTS[variant]
     T = 3
-    w, g, d, sim, recs = tiny_setup(T, sf, sg)
+    # the bf16 path is compared with the oracle's bf16-operand reading (same mask decisions)
+    w, g, d, sim, recs = tiny_setup(T, sf, sg, "bf16" if dt == "bf16" else "f64")
     L = w.layers
     tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, dt,
                           StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="none"))

@@ -376,3 +376,47 @@ def test_gamma_zero_smoothing_is_plain_pipegcn():
     for ra, rb in zip(a, b):
         for wa, wb in zip(ra[0]["W_out"], rb[0]["W_out"]):
             assert np.array_equal(wa, wb)
+
+
+def test_bf16_rounding_matches_torch():
+    """The oracle's bf16 rounding equals torch's float32 -> bfloat16 conversion (nearest even)."""
+    import torch
+    rng = np.random.default_rng(9)
+    x = np.concatenate([rng.standard_normal(20000).astype(np.float32) * 10.0 ** rng.integers(-30, 30, 20000),
+                        np.array([0.0, -0.0, 1.0, 1.00390625, 1.01171875, 3.0e38, -3.0e38, 1e-40, np.inf, -np.inf],
+                                 np.float32)])
+    # exact ties: the dropped 16 bits are 0x8000, kept mantissa even and odd
+    ties = (np.arange(64, dtype=np.uint32) << 17 | 0x3F800000 | 0x8000).view(np.float32)
+    ties_odd = ((np.arange(64, dtype=np.uint32) << 17) | 0x3F810000 | 0x8000).view(np.float32)
+    x = np.concatenate([x, ties, ties_odd])
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    got = layers.round_bf16(x)
+    assert np.array_equal(got, ref)
+    assert np.isnan(layers.round_bf16(np.array([np.nan], np.float32))[0])
+
+
+@pytest.mark.parametrize("sf,sg", [(False, False), (True, True), (True, False)])
+def test_partition_step_matches_simulation(sf, sg):
+    """The per-partition view reproduces partition 0 of the multi-partition simulation."""
+    from oracle.pipegcn import partition_step
+    g = synth.tiny_uniform()
+    n, rowptr, col, owner = g.n, g.rowptr, g.col, g.owner
+    X, W, y = tiny_problem((n, rowptr, col, owner), [5, 4, 3])
+    opts = Options(smooth_f=sf, smooth_g=sg, gamma=0.9, eta=0.3, loss_scale=1.0 / n)
+    sim, recs = run(n, rowptr, col, owner, 2, X, y, W, 4, opts)
+    p, P = sim.parts[0], sim.P[0]
+    for t in range(1, 5):
+        r = recs[t - 1][0]
+        si = r["state_in"]
+        ema_f = {k: v.copy() for k, v in si.ema_f.items()}
+        ema_g = {k: v.copy() for k, v in si.ema_g.items()}
+        out = partition_step(p, P, X[p.inner_gid], y[p.inner_gid], r["W_in"], si.feat_buf, si.grad_buf,
+                             ema_f, ema_g, t, opts)
+        assert np.isclose(out["loss"], r["loss"], rtol=1e-14)
+        for l in (1, 2):
+            assert np.array_equal(out["H"][l], r["H"][l])
+            assert np.array_equal(out["G"][l], r["G"][l])
+            assert np.array_equal(out["send_f"][l], r["send_f"][l])
+            assert np.array_equal(ema_f[l], r["state_out"].ema_f[l])
+        assert np.array_equal(out["J_full"][2], r["J_full"][2])
+        assert np.array_equal(ema_g[2], r["state_out"].ema_g[2])
