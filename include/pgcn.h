@@ -108,6 +108,8 @@ typedef struct {
   int64_t spmm_split_slots;/* partial-sum slots of split rows (forward)       */
   int64_t spmmt_items;     /* work items of the transposed aggregation        */
   int64_t spmmt_split_slots;
+  int32_t spmm_chunks;     /* column chunks (cache blocking) of P_i           */
+  int32_t spmmt_chunks;    /* column chunks of P_i^T                          */
 } pgcn_info;
 
 /* Caller-allocated host buffers for pgcn_partition_export, sized from pgcn_info.

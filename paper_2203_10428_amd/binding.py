@@ -42,7 +42,8 @@ class pgcn_info(C.Structure):
     _fields_ = [("n_inner", _i64), ("n_bd", _i64), ("nnz", _i64), ("n_send", _i64),
                 ("max_row_len", _i64), ("max_row_len_t", _i64), ("nparts", _i32), ("self", _i32),
                 ("host_only", _i32), ("spmm_segment", _i32), ("spmm_items", _i64),
-                ("spmm_split_slots", _i64), ("spmmt_items", _i64), ("spmmt_split_slots", _i64)]
+                ("spmm_split_slots", _i64), ("spmmt_items", _i64), ("spmmt_split_slots", _i64),
+                ("spmm_chunks", _i32), ("spmmt_chunks", _i32)]
 
 
 class pgcn_arrays(C.Structure):

@@ -9,13 +9,24 @@
 // go to two different buffers (inner feature gradient, outgoing boundary
 // gradient).
 //
-// Mapping for CDNA4 (wave64): a group of LPR lanes owns one work item (a
-// whole row, or a fixed segment of a long row); each lane holds NV float4
-// column vectors, so one nnz gathers one feature row with LPR*NV 16-byte
-// loads.  Column indices are read once per nnz by every lane of the group
-// (same address: one cache line per group).  No floating-point atomics: a
-// long row's segments write partial sums that a second pass adds in segment
-// order.
+// Mapping for CDNA4 (8 XCDs, 4 MB L2 each, wave64):
+//  * The feature columns are cut into S slices (S in {1,2,4,8}) of SL float4
+//    (SL a multiple of 4: 64-byte aligned, about 256-320 bytes per row).
+//    Workgroup b works on slice b % S; the hardware deals workgroups to the
+//    8 XCDs round robin, so every XCD only ever touches one slice of every
+//    feature row, which multiplies its L2 reach by the slice count.
+//  * The columns of the sparse matrix (the gathered rows) are cut into C
+//    chunks, one launch per chunk, so that one chunk's slice of the gathered
+//    matrix stays in L2 while it is reused (cache blocking; C = 1 for short
+//    rows).  Chunk c adds its partial sum to the output in chunk order; the
+//    last chunk applies the row scale.
+//  * One wave owns one work item (a row's run of non-zeros inside a chunk):
+//    G = 64 / SL lane groups take non-zeros k, k+1, ..., k+G-1, U of them
+//    per group in flight (masked at the row's end), then the groups are
+//    added in group order.
+//  * Runs longer than a fixed segment are split; segments write partial sums
+//    that a second pass adds in segment order.  No floating-point atomics:
+//    results are bitwise reproducible.
 #include "internal.h"
 
 namespace pgcn {
@@ -28,16 +39,20 @@ struct AggParams {
   const float *in_lo;
   const float *in_hi;
   int64_t out_split;
-  float *out_lo;
-  float *out_hi;
-  uint16_t *out_bf16;
+  float *out_lo;          // fp32 rows [0, out_split) (final result or running sum)
+  float *out_hi;          // fp32 rows [out_split, ...)
+  uint16_t *out_bf16;     // bf16 copy of rows [0, out_split) (final chunk only)
   const float *scale;
-  int32_t f;          // feature columns (total)
-  int32_t c4_off;     // first float4 column of this launch
-  int32_t c4_cnt;     // float4 columns of this launch
-  int64_t ld_in, ld_out, ld_part;
+  int32_t f;              // feature columns (total)
+  int32_t c4_off;         // first float4 column of this launch
+  int32_t c4_cnt;         // float4 columns of this launch
+  int32_t slices;         // S
+  int32_t mode;           // AGG_FIRST | AGG_LAST
+  int64_t ld_in, ld_out, ld_bf16, ld_part;
   float *partials;
 };
+
+enum { AGG_FIRST = 1, AGG_LAST = 2 };
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
   uint32_t b = __float_as_uint(x);
@@ -46,126 +61,156 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
   return (uint16_t)(b >> 16);
 }
 
-__device__ __forceinline__ void store_row(const AggParams &p, int64_t r, int c4, float4 v) {
-  const int c = 4 * c4;
-  float s = p.scale ? p.scale[r] : 1.0f;
-  float4 o;
-  o.x = (c + 0 < p.f) ? v.x * s : 0.0f;
-  o.y = (c + 1 < p.f) ? v.y * s : 0.0f;
-  o.z = (c + 2 < p.f) ? v.z * s : 0.0f;
-  o.w = (c + 3 < p.f) ? v.w * s : 0.0f;
-  if (r < p.out_split) {
-    if (p.out_lo) *reinterpret_cast<float4 *>(p.out_lo + r * p.ld_out + c) = o;
-    if (p.out_bf16) {
-      uint2 w;
-      w.x = (uint32_t)f32_to_bf16_rne(o.x) | ((uint32_t)f32_to_bf16_rne(o.y) << 16);
-      w.y = (uint32_t)f32_to_bf16_rne(o.z) | ((uint32_t)f32_to_bf16_rne(o.w) << 16);
-      *reinterpret_cast<uint2 *>(p.out_bf16 + r * p.ld_out + c) = w;
-    }
-  } else {
-    *reinterpret_cast<float4 *>(p.out_hi + (r - p.out_split) * p.ld_out + c) = o;
-  }
-}
-
 __device__ __forceinline__ float4 add4(float4 a, float4 b) {
   return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
 }
 
-template <int LPR, int NV, int U>
+__device__ __forceinline__ float *out_row(const AggParams &p, int64_t r) {
+  if (r < p.out_split) return p.out_lo ? p.out_lo + r * p.ld_out : nullptr;
+  return p.out_hi + (r - p.out_split) * p.ld_out;
+}
+
+// Combine this chunk's sum of float4 column c4 of row r with the running sum
+// and store it (scaled, padding zeroed, bf16 copy) when this is the last chunk.
+__device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, float4 v) {
+  const int c = 4 * c4;
+  float *o = out_row(p, r);
+  if (!(p.mode & AGG_FIRST)) v = add4(v, *reinterpret_cast<const float4 *>(o + c));
+  if (!(p.mode & AGG_LAST)) {
+    *reinterpret_cast<float4 *>(o + c) = v;
+    return;
+  }
+  const float s = p.scale ? p.scale[r] : 1.0f;
+  float4 q;
+  q.x = (c + 0 < p.f) ? v.x * s : 0.0f;
+  q.y = (c + 1 < p.f) ? v.y * s : 0.0f;
+  q.z = (c + 2 < p.f) ? v.z * s : 0.0f;
+  q.w = (c + 3 < p.f) ? v.w * s : 0.0f;
+  if (o) *reinterpret_cast<float4 *>(o + c) = q;
+  if (p.out_bf16 && r < p.out_split) {
+    uint2 w;
+    w.x = (uint32_t)f32_to_bf16_rne(q.x) | ((uint32_t)f32_to_bf16_rne(q.y) << 16);
+    w.y = (uint32_t)f32_to_bf16_rne(q.z) | ((uint32_t)f32_to_bf16_rne(q.w) << 16);
+    *reinterpret_cast<uint2 *>(p.out_bf16 + r * p.ld_bf16 + c) = w;
+  }
+}
+
+template <int SL, int U>
 __global__ __launch_bounds__(256) void agg_kernel(AggParams p) {
-  constexpr int GROUPS = 256 / LPR;
-  const int lane = threadIdx.x % LPR;
-  int64_t item = (int64_t)blockIdx.x * GROUPS + threadIdx.x / LPR;
-  if (LPR == 64) item = __builtin_amdgcn_readfirstlane((int)item);
+  constexpr int G = 64 / SL;
+  const int S = p.slices;
+  const int slice = blockIdx.x % S;
+  int64_t item = (int64_t)(blockIdx.x / S) * 4 + threadIdx.x / 64;
+  item = __builtin_amdgcn_readfirstlane((int)item);
   if (item >= p.n_items) return;
+  const int lane = threadIdx.x % 64, g = lane / SL;
+  const int cs = slice * SL + lane % SL;                // float4 column inside this launch
+  const bool act = g < G && cs < p.c4_cnt;
+  const int gg = g < G ? g : 0;
+  const int cbase = 4 * (p.c4_off + cs);
   const WorkItem it = p.items[item];
   const int32_t *cols = p.col + it.begin;
   const int len = it.len;
 
-  float4 acc[NV];
-#pragma unroll
-  for (int v = 0; v < NV; ++v) acc[v] = make_float4(0.f, 0.f, 0.f, 0.f);
-
-  bool active[NV];
-#pragma unroll
-  for (int v = 0; v < NV; ++v) active[v] = (lane + v * LPR) < p.c4_cnt;
-  const int cbase = 4 * (p.c4_off + lane);
-
-  int k = 0;
-  for (; k + U <= len; k += U) {
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int k = 0; k < len; k += G * U) {
     int32_t c[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) c[u] = cols[k + u];
-    float4 x[U][NV];
+    for (int u = 0; u < U; ++u) {
+      const int q = k + u * G + gg;
+      c[u] = q < len ? __builtin_nontemporal_load(cols + q) : -1;
+    }
+    float4 x[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const float *src;
-      if (c[u] < p.in_split) src = p.in_lo + (int64_t)c[u] * p.ld_in;
-      else src = p.in_hi ? p.in_hi + (int64_t)(c[u] - p.in_split) * p.ld_in : nullptr;
-#pragma unroll
-      for (int v = 0; v < NV; ++v)
-        x[u][v] = (src && active[v]) ? *reinterpret_cast<const float4 *>(src + cbase + 4 * v * LPR)
-                                     : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float *src = nullptr;
+      if (c[u] >= 0) {
+        if (c[u] < p.in_split) src = p.in_lo + (int64_t)c[u] * p.ld_in;
+        else if (p.in_hi) src = p.in_hi + (int64_t)(c[u] - p.in_split) * p.ld_in;
+      }
+      x[u] = (act && src) ? *reinterpret_cast<const float4 *>(src + cbase) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int v = 0; v < NV; ++v) acc[v] = add4(acc[v], x[u][v]);
+    for (int u = 0; u < U; ++u) acc = add4(acc, x[u]);
   }
-  for (; k < len; ++k) {
-    const int32_t c = cols[k];
-    const float *src;
-    if (c < p.in_split) src = p.in_lo + (int64_t)c * p.ld_in;
-    else src = p.in_hi ? p.in_hi + (int64_t)(c - p.in_split) * p.ld_in : nullptr;
-    if (src) {
+  // groups are added in group order (fixed): ((g0 + g1) + g2) + ...
+  float4 tot = acc;
 #pragma unroll
-      for (int v = 0; v < NV; ++v)
-        if (active[v]) acc[v] = add4(acc[v], *reinterpret_cast<const float4 *>(src + cbase + 4 * v * LPR));
-    }
+  for (int q = 1; q < G; ++q) {
+    const int from = lane % SL + q * SL;
+    tot.x += __shfl(acc.x, from);
+    tot.y += __shfl(acc.y, from);
+    tot.z += __shfl(acc.z, from);
+    tot.w += __shfl(acc.w, from);
   }
-
+  if (g != 0 || cs >= p.c4_cnt) return;
   if (it.dst >= 0) {
-#pragma unroll
-    for (int v = 0; v < NV; ++v)
-      if (active[v]) store_row(p, it.dst, p.c4_off + lane + v * LPR, acc[v]);
+    finish(p, it.dst, p.c4_off + cs, tot);
   } else {
-    float *dst = p.partials + (int64_t)(-it.dst - 1) * p.ld_part;
-#pragma unroll
-    for (int v = 0; v < NV; ++v)
-      if (active[v]) *reinterpret_cast<float4 *>(dst + cbase + 4 * v * LPR) = acc[v];
+    *reinterpret_cast<float4 *>(p.partials + (int64_t)(-it.dst - 1) * p.ld_part + cbase) = tot;
   }
 }
 
-// Sum the partial slots of each split row in slot order, then scale and store.
+// Sum the partial slots of each split row in slot order, then combine and store.
 __global__ __launch_bounds__(256) void agg_fixup_kernel(AggParams p, const SplitRow *splits) {
   const SplitRow s = splits[blockIdx.x];
   for (int c4 = p.c4_off + threadIdx.x; c4 < p.c4_off + p.c4_cnt; c4 += blockDim.x) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int j = 0; j < s.nslots; ++j)
       acc = add4(acc, *reinterpret_cast<const float4 *>(p.partials + (int64_t)(s.first_slot + j) * p.ld_part + 4 * c4));
-    store_row(p, s.row, c4, acc);
+    finish(p, s.row, c4, acc);
   }
 }
 
-template <int LPR, int NV>
-static void launch_variant(const AggParams &p, hipStream_t s, int32_t trace_kind) {
-  TraceScope ts(trace_kind, s);
-  constexpr int U = NV >= 3 ? 2 : (NV == 2 ? 4 : 8);
-  const int64_t groups = 256 / LPR;
-  const int64_t blocks = (p.n_items + groups - 1) / groups;
-  hipLaunchKernelGGL((agg_kernel<LPR, NV, U>), dim3((unsigned)blocks), dim3(256), 0, s, p);
+template <int SL>
+static void launch_sl(const AggParams &p, hipStream_t s) {
+  constexpr int U = SL <= 32 ? 8 : 4;
+  const int64_t blocks = (p.n_items + 3) / 4 * p.slices;
+  hipLaunchKernelGGL((agg_kernel<SL, U>), dim3((unsigned)blocks), dim3(256), 0, s, p);
+}
+
+static void launch_dispatch(const AggParams &p, int sl, hipStream_t s) {
+  switch (sl) {
+    case 4: launch_sl<4>(p, s); break;
+    case 8: launch_sl<8>(p, s); break;
+    case 12: launch_sl<12>(p, s); break;
+    case 16: launch_sl<16>(p, s); break;
+    case 20: launch_sl<20>(p, s); break;
+    case 24: launch_sl<24>(p, s); break;
+    case 32: launch_sl<32>(p, s); break;
+    case 48: launch_sl<48>(p, s); break;
+    default: launch_sl<64>(p, s); break;
+  }
+}
+
+// Slice count (power of two, at most 8) and slice width (float4, multiple of 4)
+// for a launch of c4 float4 columns: slices of at most ~320 bytes, one slice
+// per XCD when the row is wide.
+static void choose_slices(int c4, int *S, int *SL) {
+  int s = 1;
+  while (s < 8 && s * 20 < c4) s *= 2;
+  int need = (c4 + s - 1) / s;
+  need = (need + 3) / 4 * 4;
+  static const int widths[] = {4, 8, 12, 16, 20, 24, 32, 48, 64};
+  int sl = 64;
+  for (int w : widths)
+    if (w >= need) {
+      sl = w;
+      break;
+    }
+  *S = s;
+  *SL = sl;
 }
 
 size_t aggregate_workspace(const Plan &plan, int64_t f) {
   const int64_t ld_part = (f + 3) / 4 * 4;
-  return (size_t)plan.slots * (size_t)ld_part * sizeof(float);
+  return (size_t)plan.max_chunk_slots * (size_t)ld_part * sizeof(float);
 }
 
 int launch_aggregate(const AggArgs &a, hipStream_t s) {
   const Plan &plan = *a.plan;
+  if (plan.items.empty()) return PGCN_OK;
   AggParams p{};
-  p.items = plan.d_items;
-  p.n_items = (int64_t)plan.items.size();
   p.col = a.col;
   p.in_split = a.in_split;
   p.in_lo = a.in_lo;
@@ -178,29 +223,35 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
   p.f = a.f;
   p.ld_in = a.ld_in;
   p.ld_out = a.ld_out;
+  p.ld_bf16 = a.ld_bf16;
   p.ld_part = (a.f + 3) / 4 * 4;
   p.partials = a.partials;
-  if (p.n_items == 0) return PGCN_OK;
   const int f4 = (a.f + 3) / 4;
-  // one launch per chunk of at most 256 float4 columns (1024 features)
-  for (int off = 0; off < f4; off += 256) {
-    const int cnt = f4 - off < 256 ? f4 - off : 256;
+  const int C = plan.chunks;
+  // launches of at most 8 x 64 float4 columns (2,048 features)
+  for (int off = 0; off < f4; off += 512) {
+    const int cnt = f4 - off < 512 ? f4 - off : 512;
+    int S = 1, SL = 64;
+    choose_slices(cnt, &S, &SL);
     p.c4_off = off;
     p.c4_cnt = cnt;
-    if (cnt <= 4) launch_variant<4, 1>(p, s, a.trace_kind);
-    else if (cnt <= 8) launch_variant<8, 1>(p, s, a.trace_kind);
-    else if (cnt <= 16) launch_variant<16, 1>(p, s, a.trace_kind);
-    else if (cnt <= 32) launch_variant<32, 1>(p, s, a.trace_kind);
-    else if (cnt <= 64) launch_variant<64, 1>(p, s, a.trace_kind);
-    else if (cnt <= 128) launch_variant<64, 2>(p, s, a.trace_kind);
-    else if (cnt <= 192) launch_variant<64, 3>(p, s, a.trace_kind);
-    else launch_variant<64, 4>(p, s, a.trace_kind);
-    PGCN_HIP(hipGetLastError());
-    if (!plan.splits.empty()) {
-      TraceScope ts(PGCN_TK_AGG_FIXUP, s);
-      hipLaunchKernelGGL(agg_fixup_kernel, dim3((unsigned)plan.splits.size()), dim3(256), 0, s, p,
-                         plan.d_splits);
-      PGCN_HIP(hipGetLastError());
+    p.slices = S;
+    for (int c = 0; c < C; ++c) {
+      p.mode = (c == 0 ? AGG_FIRST : 0) | (c == C - 1 ? AGG_LAST : 0);
+      p.items = plan.d_items + plan.chunk_items[c];
+      p.n_items = plan.chunk_items[c + 1] - plan.chunk_items[c];
+      if (p.n_items > 0) {
+        TraceScope ts(a.trace_kind, s);
+        launch_dispatch(p, SL, s);
+        PGCN_HIP(hipGetLastError());
+      }
+      const int64_t ns = plan.chunk_splits[c + 1] - plan.chunk_splits[c];
+      if (ns > 0) {
+        TraceScope ts(PGCN_TK_AGG_FIXUP, s);
+        hipLaunchKernelGGL(agg_fixup_kernel, dim3((unsigned)ns), dim3(256), 0, s, p,
+                           (const SplitRow *)(plan.d_splits + plan.chunk_splits[c]));
+        PGCN_HIP(hipGetLastError());
+      }
     }
   }
   return PGCN_OK;

@@ -20,7 +20,15 @@ bool aligned16(const void *q) { return ((uintptr_t)q & 15u) == 0; }
 
 int64_t ld4(int64_t f) { return (f + 3) / 4 * 4; }
 
-size_t fwd_ws(const pgcn_partition *p, int32_t f_in) { return align_up(aggregate_workspace(p->plan, f_in), 256); }
+// forward: split-row partials, plus an fp32 running sum over the column chunks
+// when the caller keeps no fp32 A (bf16 path)
+size_t fwd_acc_bytes(const pgcn_partition *p, int32_t f_in, int32_t gemm_dtype) {
+  if (p->plan.chunks <= 1 || gemm_dtype != PGCN_BF16) return 0;
+  return align_up((size_t)p->n_inner * (size_t)ld4(f_in) * sizeof(float), 256);
+}
+size_t fwd_ws(const pgcn_partition *p, int32_t f_in, int32_t gemm_dtype) {
+  return align_up(aggregate_workspace(p->plan, f_in), 256) + fwd_acc_bytes(p, f_in, gemm_dtype);
+}
 
 // backward: the split-K partials are consumed before D is written, so they share space
 size_t bwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_grad) {
@@ -35,9 +43,8 @@ size_t bwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_g
 }  // namespace
 
 extern "C" size_t pgcn_workspace_size(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) {
-  (void)gemm_dtype;
   if (!p || f_in <= 0 || f_out <= 0) return 0;
-  size_t w = fwd_ws(p, f_in);
+  size_t w = fwd_ws(p, f_in, gemm_dtype);
   size_t b = bwd_ws(p, f_in, f_out, true);
   size_t l = align_up(loss_workspace(p->n_inner), 256);
   size_t m = w > b ? w : b;
@@ -64,7 +71,7 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
     }
     PGCN_REQUIRE(!a->A || aligned16(a->A), "pgcn_layer_fwd: A must be 16-byte aligned");
   }
-  const size_t need = fwd_ws(p, a->f_in);
+  const size_t need = fwd_ws(p, a->f_in, a->gemm_dtype);
   if (need > 0 && (!a->workspace || a->workspace_bytes < need))
     return set_error(PGCN_EWORKSPACE, "pgcn_layer_fwd: workspace too small");
   if (p->n_inner == 0) return PGCN_OK;
@@ -83,7 +90,12 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   g.f = a->f_in;
   g.ld_in = a->ld_in;
   g.ld_out = a->ld_in;
+  g.ld_bf16 = a->ld_in;
   g.partials = (float *)a->workspace;
+  if (!a->A && p->plan.chunks > 1) {   // running sum over chunks in the workspace
+    g.out_lo = (float *)((char *)a->workspace + align_up(aggregate_workspace(p->plan, a->f_in), 256));
+    g.ld_out = ld4(a->f_in);
+  }
   g.trace_kind = PGCN_TK_AGG_FWD;
   rc = launch_aggregate(g, s);
   if (rc) return rc;
@@ -189,6 +201,7 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   t.f = a->f_in;
   t.ld_in = ld_d;
   t.ld_out = a->ld_in;
+  t.ld_bf16 = 0;
   t.partials = partials;
   t.trace_kind = PGCN_TK_AGG_BWD;
   return launch_aggregate(t, s);

@@ -29,11 +29,18 @@ struct SplitRow {
   int32_t pad;
 };
 
-// Fixed work plan over one CSR matrix (rows of P_i or of P_i^T).
+// Fixed work plan over one CSR matrix (rows of P_i or of P_i^T).  The
+// matrix columns are cut into `chunks` equal ranges; chunk c's items are
+// items[chunk_items[c] .. chunk_items[c+1]) (one per row and chunk, or one per
+// segment of a long run) and its split rows splits[chunk_splits[c] ..
+// chunk_splits[c+1]), whose partial slots restart at 0 in every chunk.
 struct Plan {
+  int32_t chunks = 1;
   std::vector<WorkItem> items;
   std::vector<SplitRow> splits;
-  int64_t slots = 0;
+  std::vector<int64_t> chunk_items, chunk_splits;
+  int64_t slots = 0;            // total partial slots over all chunks
+  int64_t max_chunk_slots = 0;  // partial slots needed at once
   WorkItem *d_items = nullptr;
   SplitRow *d_splits = nullptr;
 };
@@ -104,7 +111,7 @@ struct AggArgs {
   uint16_t *out_bf16;      // optional bf16 copy of out_lo rows (forward, bf16 GEMM path)
   const float *scale;
   int32_t f;
-  int64_t ld_in, ld_out;
+  int64_t ld_in, ld_out, ld_bf16;
   float *partials;
   int32_t trace_kind;      // PGCN_TK_AGG_FWD or PGCN_TK_AGG_BWD
 };

@@ -22,36 +22,67 @@ int check_hip(hipError_t e, const char *what) {
   return set_error(PGCN_EHIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-// Rows longer than `segment` are cut into fixed segments whose partial sums are
-// added in segment order by a second pass, so results never depend on timing.
-static void build_plan(const std::vector<int64_t> &rowptr, int64_t nrows, int32_t segment, Plan &p) {
+// Number of column chunks of a CSR matrix for cache blocking: enough that one
+// chunk's slice (up to 320 bytes per gathered row) of the gathered rows spans
+// about 6 MB, but only while a row keeps >= 64 non-zeros per chunk on average.
+static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz) {
+  const char *env = std::getenv("PGCN_AGG_CHUNKS");
+  if (env) {
+    int v = std::atoi(env);
+    if (v >= 1 && v <= 64) return v;
+  }
+  if (nrows == 0 || ncols == 0) return 1;
+  const int64_t by_cache = (ncols * 320 + (6 << 20) - 1) / (6 << 20);
+  const int64_t by_len = (nnz / nrows) / 64;
+  int64_t c = std::min(by_cache, by_len);
+  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, 16));
+}
+
+// Rows (runs inside a chunk) longer than `segment` are cut into fixed
+// segments whose partial sums are added in segment order by a second pass,
+// so results never depend on timing.  Whole runs are scheduled longest first.
+static void build_plan(const std::vector<int64_t> &rowptr, const std::vector<int32_t> &col, int64_t nrows,
+                       int64_t ncols, int32_t segment, Plan &p) {
   p.items.clear();
   p.splits.clear();
   p.slots = 0;
-  std::vector<int64_t> order;
+  p.max_chunk_slots = 0;
+  const int64_t nnz = nrows ? rowptr[nrows] : 0;
+  p.chunks = choose_chunks(nrows, ncols, nnz);
+  const int32_t C = p.chunks;
+  p.chunk_items.assign(C + 1, 0);
+  p.chunk_splits.assign(C + 1, 0);
+  std::vector<int64_t> b(nrows), e(nrows), order;
   order.reserve(nrows);
-  for (int64_t r = 0; r < nrows; ++r) {
-    int64_t len = rowptr[r + 1] - rowptr[r];
-    if (len > segment) {
-      int32_t nseg = (int32_t)((len + segment - 1) / segment);
-      p.splits.push_back(SplitRow{(int32_t)r, (int32_t)p.slots, nseg, 0});
-      for (int32_t s = 0; s < nseg; ++s) {
-        int64_t b = rowptr[r] + (int64_t)s * segment;
-        int64_t e = std::min<int64_t>(b + segment, rowptr[r + 1]);
-        p.items.push_back(WorkItem{b, (int32_t)(e - b), (int32_t)(-(p.slots + s) - 1)});
+  for (int32_t c = 0; c < C; ++c) {
+    const int32_t lo = (int32_t)(ncols * c / C), hi = (int32_t)(ncols * (c + 1) / C);
+    int64_t slots = 0;
+    order.clear();
+    for (int64_t r = 0; r < nrows; ++r) {
+      const int32_t *rb = col.data() + rowptr[r], *re = col.data() + rowptr[r + 1];
+      b[r] = (C == 1) ? rowptr[r] : rowptr[r] + (std::lower_bound(rb, re, lo) - rb);
+      e[r] = (C == 1) ? rowptr[r + 1] : rowptr[r] + (std::lower_bound(rb, re, hi) - rb);
+      const int64_t len = e[r] - b[r];
+      if (len > segment) {
+        const int32_t nseg = (int32_t)((len + segment - 1) / segment);
+        p.splits.push_back(SplitRow{(int32_t)r, (int32_t)slots, nseg, 0});
+        for (int32_t q = 0; q < nseg; ++q) {
+          const int64_t sb = b[r] + (int64_t)q * segment;
+          const int64_t se = std::min<int64_t>(sb + segment, e[r]);
+          p.items.push_back(WorkItem{sb, (int32_t)(se - sb), (int32_t)(-(slots + q) - 1)});
+        }
+        slots += nseg;
+      } else {
+        order.push_back(r);
       }
-      p.slots += nseg;
-    } else {
-      order.push_back(r);
     }
+    std::stable_sort(order.begin(), order.end(), [&](int64_t x, int64_t y) { return e[x] - b[x] > e[y] - b[y]; });
+    for (int64_t r : order) p.items.push_back(WorkItem{b[r], (int32_t)(e[r] - b[r]), (int32_t)r});
+    p.chunk_items[c + 1] = (int64_t)p.items.size();
+    p.chunk_splits[c + 1] = (int64_t)p.splits.size();
+    p.slots += slots;
+    p.max_chunk_slots = std::max(p.max_chunk_slots, slots);
   }
-  // whole rows, longest first (ties by row id): long items start early and
-  // items of similar length share a wavefront
-  std::stable_sort(order.begin(), order.end(), [&](int64_t a, int64_t b) {
-    return rowptr[a + 1] - rowptr[a] > rowptr[b + 1] - rowptr[b];
-  });
-  for (int64_t r : order)
-    p.items.push_back(WorkItem{rowptr[r], (int32_t)(rowptr[r + 1] - rowptr[r]), (int32_t)r});
 }
 
 template <class T>
@@ -244,8 +275,8 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
     for (int64_t k = 0; k < p->n_send; ++k) p->inv_k[fill[p->send_idx[k]]++] = (int32_t)k;
   }
 
-  build_plan(p->rowptr, n_in, p->segment, p->plan);
-  build_plan(p->rowptr_t, n_all, p->segment, p->plan_t);
+  build_plan(p->rowptr, p->col, n_in, n_all, p->segment, p->plan);
+  build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, p->plan_t);
 
   if (!p->host_only) {
     PGCN_HIP(hipGetDevice(&p->device));
@@ -286,6 +317,8 @@ extern "C" int pgcn_partition_info(const pgcn_partition *p, pgcn_info *o) {
   o->spmm_split_slots = p->plan.slots;
   o->spmmt_items = (int64_t)p->plan_t.items.size();
   o->spmmt_split_slots = p->plan_t.slots;
+  o->spmm_chunks = p->plan.chunks;
+  o->spmmt_chunks = p->plan_t.chunks;
   return PGCN_OK;
 }
 

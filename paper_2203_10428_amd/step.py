@@ -135,6 +135,8 @@ class PartitionTrainer:
         t = self.t
         cur, nxt = self.cur, 1 - self.cur
         mode = o.copy_mode
+        caller = torch.cuda.current_stream(self.dev)
+        st.wait_stream(caller)          # inputs written by the caller's stream are visible
 
         # ---- forward --------------------------------------------------
         for l in range(1, L + 1):
@@ -198,6 +200,7 @@ class PartitionTrainer:
             B.pgcn_sgd_update(self.W[l], self.dW[l], self.G_peer[l], self.W[l].numel(), o.eta, st)
         if mode == "pipe":
             self.cur = nxt
+        caller.wait_stream(st)          # results are ordered before the caller's next work
         return self.loss
 
     def synchronize(self):

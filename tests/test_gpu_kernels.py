@@ -1,6 +1,8 @@
 """GPU parity of each libpgcn entry point against the fp64 oracle, element by
 element, on seeded random partitions (several tiles, ragged feature widths,
 rows split into segments, empty boundary input)."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -15,19 +17,31 @@ pytestmark = pytest.mark.gpu
 
 
 class Graph:
-    def __init__(self, n_inner=3000, n_pool=1500, nparts=4, mean_deg=12, seed=0, hub_deg=0):
+    def __init__(self, n_inner=3000, n_pool=1500, nparts=4, mean_deg=12, seed=0, hub_deg=0, env=None):
         self.n, self.rowptr, self.col, self.owner = random_partition_graph(n_inner, n_pool, nparts, mean_deg, seed,
                                                                            hub_deg)
         self.nparts = nparts
         self.ref = build_partition(self.n, self.rowptr, self.col, self.owner, 0, nparts)
         self.P = propagation_matrix(self.ref)
-        self.part = B.pgcn_partition_setup(self.n, self.rowptr, self.col, self.owner, nparts, 0)
+        old = {k: os.environ.get(k) for k in (env or {})}
+        os.environ.update(env or {})           # set-up tuning knobs: column chunks, segment length
+        try:
+            self.part = B.pgcn_partition_setup(self.n, self.rowptr, self.col, self.owner, nparts, 0)
+        finally:
+            for k, v in old.items():
+                if v is None:
+                    os.environ.pop(k, None)
+                else:
+                    os.environ[k] = v
         self.info = B.pgcn_partition_info(self.part)
 
 
 @pytest.fixture(scope="module")
 def graphs():
-    return {"plain": Graph(), "hub": Graph(n_inner=2500, n_pool=900, seed=1, hub_deg=3000)}
+    return {"plain": Graph(), "hub": Graph(n_inner=2500, n_pool=900, seed=1, hub_deg=3000),
+            # cache-blocked plan: 3 column chunks, runs split every 16 non-zeros (partials in every chunk)
+            "chunked": Graph(n_inner=2000, n_pool=1200, seed=2, mean_deg=60, hub_deg=2000,
+                             env={"PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "16"})}
 
 
 def ws_for(g, f_in, f_out, dt):
@@ -41,11 +55,13 @@ def test_partition_device_build_matches_oracle(graphs):
         for k in ("inner_gid", "bd_gid", "rowptr", "col", "rowptr_t", "col_t", "send_idx", "inv_ptr", "inv_k"):
             assert np.array_equal(ex[k], getattr(g.ref, k).astype(ex[k].dtype)), k
     assert graphs["hub"].info["spmm_split_slots"] > 0
+    assert graphs["chunked"].info["spmm_chunks"] == 3 and graphs["chunked"].info["spmmt_chunks"] == 3
 
 
-@pytest.mark.parametrize("gname", ["plain", "hub"])
-@pytest.mark.parametrize("dt", ["f32", "bf16"])
-@pytest.mark.parametrize("f_in,f_out", [(1, 3), (41, 47), (100, 128), (128, 64), (300, 512), (602, 256)])
+@pytest.mark.parametrize("gname", ["plain", "hub", "chunked"])
+@pytest.mark.parametrize("dt", ["f32", "bf16", "bf16-noA"])
+@pytest.mark.parametrize("f_in,f_out", [(1, 3), (41, 47), (100, 128), (128, 64), (300, 512), (602, 256), (1100, 16),
+                                        (2100, 8)])
 @pytest.mark.parametrize("with_bd", [True, False])
 def test_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
     g = graphs[gname]
@@ -55,12 +71,15 @@ def test_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
     H_bd = rng.standard_normal((b, f_in)) if with_bd else np.zeros((b, f_in))
     W = rng.uniform(-0.2, 0.2, (f_in, f_out)).astype(np.float32)
     relu = f_out != 3
-    A_ref, Z_ref, H_ref = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), relu)
+    no_A = dt == "bf16-noA"                  # bf16 path without an fp32 copy of A
+    dt = "bf16" if no_A else dt
+    A_ref, Z_ref, H_ref = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), relu,
+                                               "bf16" if dt == "bf16" else "f64")
     dtype = B.PGCN_BF16 if dt == "bf16" else B.PGCN_F32
     dH_in = dev(H_in)
     dH_bd = dev(H_bd) if with_bd else None
     dW = torch.from_numpy(W).cuda()
-    A = dev(np.zeros((n, f_in)))
+    A = None if no_A else dev(np.zeros((n, f_in)))
     A16 = torch.zeros((n, ld_of(f_in)), dtype=torch.bfloat16, device="cuda") if dt == "bf16" else None
     H = dev(np.zeros((n, f_out)))
     ws, nb = ws_for(g, f_in, f_out, dtype)
@@ -68,18 +87,19 @@ def test_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
                      ld_out=ld_of(f_out), H_in=dH_in, H_bd=dH_bd, W=dW, A=A, A_bf16=A16, H_out=H,
                      workspace=ws, workspace_bytes=nb)
     tol = TOL[dt]["act"]
-    assert rel_err(host(A, f_in), A_ref) < 1e-5          # aggregation is fp32 on both paths
+    if A is not None:
+        assert rel_err(host(A, f_in), A_ref) < 1e-5      # aggregation is fp32 on both paths
+        # padding columns [f, round_up(f, 4)) of A are written as zeros
+        pad = host(A, ld_of(f_in))[:, f_in:(f_in + 3) // 4 * 4]
+        assert np.all(pad == 0)
     if dt == "bf16":
         assert rel_err(host(A16, f_in), A_ref) < 1e-2    # one bf16 rounding
     assert rel_err(host(H, f_out), H_ref) < tol
-    # padding columns [f, round_up(f, 4)) of A are written as zeros
-    pad = host(A, ld_of(f_in))[:, f_in:(f_in + 3) // 4 * 4]
-    assert np.all(pad == 0)
 
 
-@pytest.mark.parametrize("gname", ["plain", "hub"])
+@pytest.mark.parametrize("gname", ["plain", "hub", "chunked"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
-@pytest.mark.parametrize("f_in,f_out", [(3, 1), (47, 41), (128, 100), (256, 256), (300, 512), (602, 256)])
+@pytest.mark.parametrize("f_in,f_out", [(3, 1), (47, 41), (128, 100), (256, 256), (300, 512), (602, 256), (1100, 16)])
 @pytest.mark.parametrize("input_grad", [True, False])
 def test_layer_backward(graphs, gname, dt, f_in, f_out, input_grad):
     g = graphs[gname]
@@ -113,8 +133,9 @@ def test_layer_backward(graphs, gname, dt, f_in, f_out, input_grad):
         assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
 
 
-def test_backward_is_deterministic(graphs):
-    g = graphs["hub"]
+@pytest.mark.parametrize("gname", ["hub", "chunked"])
+def test_backward_is_deterministic(graphs, gname):
+    g = graphs[gname]
     rng = np.random.default_rng(3)
     n, b = g.ref.n_inner, g.ref.n_bd
     f_in, f_out = 300, 128
