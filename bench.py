@@ -109,6 +109,7 @@ def main():
     ap.add_argument("--workload", default="reddit-like-1of4")
     ap.add_argument("--variant", default="PipeGCN-GF", choices=list(VARIANTS))
     ap.add_argument("--no-copy-modes", action="store_true", help="skip the serial / no-refill comparison")
+    ap.add_argument("--refill", default="dma", choices=["dma", "blit"], help="engine of the stale-buffer refills")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=0.25, help="inner-node fraction timed on the CPU")
     args = ap.parse_args()
@@ -133,7 +134,8 @@ def main():
     log(f"workload {w.name}: graph {g.stats} generated in {time.perf_counter() - t0:.1f}s")
     sf, sg = VARIANTS[args.variant]
     tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, w.gemm_dtype,
-                          StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe"))
+                          StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
+                                      refill_dma=args.refill == "dma"))
     del d
     log(f"partition set up: {tr.info}")
 
@@ -200,6 +202,10 @@ def main():
         k2 = max(3, args.steps // 2)
         copy_modes = {m: timed(k2, m) for m in ("none", "serial", "pipe")}
         copy_modes["hidden"] = copy_modes["pipe"] <= 1.03 * copy_modes["none"]
+        tr.opts.refill_dma = not tr.opts.refill_dma
+        copy_modes["pipe_other_engine"] = timed(k2, "pipe")
+        copy_modes["refill_engine"] = args.refill
+        tr.opts.refill_dma = not tr.opts.refill_dma
         log(f"copy modes (ms/step): {copy_modes}")
 
     cpu = None
@@ -231,7 +237,8 @@ def main():
         "vs_baseline": None,
         "dtype": dt,
         "data": "synthetic",
-        "config": {"workload": w.name, "variant": args.variant, "copy_mode": "pipe", "widths": list(w.widths),
+        "config": {"workload": w.name, "variant": args.variant, "copy_mode": "pipe", "refill": args.refill,
+                   "widths": list(w.widths),
                    "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",
                    "n_inner": i["n_inner"], "n_bd": i["n_bd"], "n_send": i["n_send"], "nnz": i["nnz"],
                    "max_row_len": i["max_row_len"], "parallelism": "1 partition / 1 GPU"},

@@ -249,9 +249,12 @@ int pgcn_sgd_update(float *W, const float *G, const float *G_peer, int64_t count
                     hipStream_t stream);
 
 /* Refill of a stale buffer (Algorithm 1's send/receive threads; the paper runs
- * them on a second stream): an asynchronous device copy of `bytes` bytes
- * enqueued on `stream`. */
-int pgcn_refill_async(void *dst, const void *src, size_t bytes, hipStream_t stream);
+ * them on a second stream): an asynchronous device-to-device copy of `bytes`
+ * bytes enqueued on `stream`.  flags = 0: the runtime's copy (a blit kernel on
+ * the compute units); PGCN_REFILL_DMA: a copy by the DMA engines that uses no
+ * compute units (as a transfer arriving from a peer GPU would). */
+enum pgcn_refill_flags { PGCN_REFILL_DMA = 1 };
+int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, hipStream_t stream);
 
 /*
  * Kernel tracing (measurement support).  While enabled, every kernel launch

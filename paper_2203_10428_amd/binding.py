@@ -25,6 +25,7 @@ PGCN_F32, PGCN_BF16 = 0, 1
 PGCN_SETUP_HOST_ONLY = 1
 PGCN_PACK_FEAT, PGCN_ACCUM_GRAD = 0, 1
 PGCN_SOFTMAX_CE, PGCN_SIGMOID_BCE = 0, 1
+PGCN_REFILL_DMA = 1
 
 _vp = C.c_void_p
 _i32, _i64, _u32, _f32, _sz = C.c_int32, C.c_int64, C.c_uint32, C.c_float, C.c_size_t
@@ -77,7 +78,7 @@ SIGNATURES = {
     "pgcn_pack_boundary": (_i32, [_vp, _i32, _vp, _vp, _i32, _i64, _vp]),
     "pgcn_loss_fwd_bwd": (_i32, [_i32, _vp, _i64, _i32, _i64, _vp, _vp, _i64, _f32, _vp, _vp, _vp, _sz, _vp]),
     "pgcn_sgd_update": (_i32, [_vp, _vp, _vp, _i64, _f32, _vp]),
-    "pgcn_refill_async": (_i32, [_vp, _vp, _sz, _vp]),
+    "pgcn_refill_async": (_i32, [_vp, _vp, _sz, _u32, _vp]),
     "pgcn_trace_enable": (_i32, [_i32]),
     "pgcn_trace_collect": (_i32, [_vp, _vp, _i32, C.POINTER(_i32)]),
     "pgcn_trace_disable": (_i32, []),
@@ -223,8 +224,8 @@ def pgcn_sgd_update(W, G, G_peer, count: int, eta: float, stream=None):
     _check(lib.pgcn_sgd_update(_ptr(W), _ptr(G), _ptr(G_peer), count, eta, _stream(stream)), "pgcn_sgd_update")
 
 
-def pgcn_refill_async(dst, src, nbytes: int, stream=None):
-    _check(lib.pgcn_refill_async(_ptr(dst), _ptr(src), nbytes, _stream(stream)), "pgcn_refill_async")
+def pgcn_refill_async(dst, src, nbytes: int, flags: int = 0, stream=None):
+    _check(lib.pgcn_refill_async(_ptr(dst), _ptr(src), nbytes, flags, _stream(stream)), "pgcn_refill_async")
 
 
 TRACE_KINDS = ["agg_fwd", "agg_bwd", "agg_fixup", "gemm_fwd", "gemm_dgrad", "gemm_wgrad", "wgrad_reduce", "ema",

@@ -10,23 +10,27 @@
 // gradient).
 //
 // Mapping for CDNA4 (8 XCDs, 4 MB L2 each, wave64):
-//  * The feature columns are cut into S slices (S in {1,2,4,8}) of SL float4
-//    (SL a multiple of 4: 64-byte aligned, about 256-320 bytes per row).
-//    Workgroup b works on slice b % S; the hardware deals workgroups to the
-//    8 XCDs round robin, so every XCD only ever touches one slice of every
-//    feature row, which multiplies its L2 reach by the slice count.
+//  * Rows wider than 1 KB are cut into S slices (S in {1,2,4,8}) of SL float4
+//    (SL a multiple of 4: 64-byte aligned, at most 1 KB).  Workgroup b works
+//    on slice b % S; the hardware deals workgroups to the 8 XCDs round robin,
+//    so every XCD only ever touches one slice of every feature row.
 //  * The columns of the sparse matrix (the gathered rows) are cut into C
-//    chunks, one launch per chunk, so that one chunk's slice of the gathered
-//    matrix stays in L2 while it is reused (cache blocking; C = 1 for short
-//    rows).  Chunk c adds its partial sum to the output in chunk order; the
-//    last chunk applies the row scale.
-//  * One wave owns one work item (a row's run of non-zeros inside a chunk):
-//    G = 64 / SL lane groups take non-zeros k, k+1, ..., k+G-1, U of them
-//    per group in flight (masked at the row's end), then the groups are
-//    added in group order.
+//    chunks of about 11,000 rows, one launch per chunk, so that the rows one
+//    launch gathers from stay in the caches while they are reused (cache
+//    blocking; C = 1 for short rows, where each gathered row is used only a
+//    few times anyway).  Chunk c adds its partial sum to the output in chunk
+//    order; the last chunk applies the row scale.
+//  * Long runs: one wave owns one work item (a row's run of non-zeros inside
+//    a chunk): G = 64 / SL lane groups take non-zeros k, k+1, ..., k+G-1, U
+//    of them per group in flight (masked at the row's end), then the groups
+//    are added in group order.  Short runs (fewer than G*U non-zeros): each
+//    lane group owns its own item, U non-zeros in flight; items are sorted by
+//    length, so the groups of a wave finish together.
 //  * Runs longer than a fixed segment are split; segments write partial sums
 //    that a second pass adds in segment order.  No floating-point atomics:
 //    results are bitwise reproducible.
+#include <cstdlib>
+
 #include "internal.h"
 
 namespace pgcn {
@@ -93,6 +97,42 @@ __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, fl
     w.y = (uint32_t)f32_to_bf16_rne(q.z) | ((uint32_t)f32_to_bf16_rne(q.w) << 16);
     *reinterpret_cast<uint2 *>(p.out_bf16 + r * p.ld_bf16 + c) = w;
   }
+}
+
+// Short runs: lane group g of a wave owns item (wave * G + g).
+template <int SL, int U>
+__global__ __launch_bounds__(256) void agg_multi_kernel(AggParams p) {
+  constexpr int G = 64 / SL;
+  const int S = p.slices;
+  const int slice = blockIdx.x % S;
+  const int lane = threadIdx.x % 64, g = lane / SL;
+  const int64_t item = ((int64_t)(blockIdx.x / S) * 4 + threadIdx.x / 64) * G + g;
+  const int cs = slice * SL + lane % SL;
+  if (g >= G || item >= p.n_items || cs >= p.c4_cnt) return;
+  const int cbase = 4 * (p.c4_off + cs);
+  const WorkItem it = p.items[item];
+  const int32_t *cols = p.col + it.begin;
+  const int len = it.len;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int k = 0; k < len; k += U) {
+    int32_t c[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) c[u] = k + u < len ? __builtin_nontemporal_load(cols + k + u) : -1;
+    float4 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float *src = nullptr;
+      if (c[u] >= 0) {
+        if (c[u] < p.in_split) src = p.in_lo + (int64_t)c[u] * p.ld_in;
+        else if (p.in_hi) src = p.in_hi + (int64_t)(c[u] - p.in_split) * p.ld_in;
+      }
+      x[u] = src ? *reinterpret_cast<const float4 *>(src + cbase) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc = add4(acc, x[u]);
+  }
+  if (it.dst >= 0) finish(p, it.dst, p.c4_off + cs, acc);
+  else *reinterpret_cast<float4 *>(p.partials + (int64_t)(-it.dst - 1) * p.ld_part + cbase) = acc;
 }
 
 template <int SL, int U>
@@ -163,35 +203,61 @@ __global__ __launch_bounds__(256) void agg_fixup_kernel(AggParams p, const Split
 }
 
 template <int SL>
-static void launch_sl(const AggParams &p, hipStream_t s) {
+static void launch_sl(const AggParams &p, bool multi, hipStream_t s) {
   constexpr int U = SL <= 32 ? 8 : 4;
-  const int64_t blocks = (p.n_items + 3) / 4 * p.slices;
-  hipLaunchKernelGGL((agg_kernel<SL, U>), dim3((unsigned)blocks), dim3(256), 0, s, p);
+  constexpr int G = 64 / SL;
+  if (multi) {
+    const int64_t blocks = (p.n_items + 4 * G - 1) / (4 * G) * p.slices;
+    hipLaunchKernelGGL((agg_multi_kernel<SL, U>), dim3((unsigned)blocks), dim3(256), 0, s, p);
+  } else {
+    const int64_t blocks = (p.n_items + 3) / 4 * p.slices;
+    hipLaunchKernelGGL((agg_kernel<SL, U>), dim3((unsigned)blocks), dim3(256), 0, s, p);
+  }
 }
 
-static void launch_dispatch(const AggParams &p, int sl, hipStream_t s) {
+static void launch_dispatch(const AggParams &p, int sl, bool multi, hipStream_t s) {
   switch (sl) {
-    case 4: launch_sl<4>(p, s); break;
-    case 8: launch_sl<8>(p, s); break;
-    case 12: launch_sl<12>(p, s); break;
-    case 16: launch_sl<16>(p, s); break;
-    case 20: launch_sl<20>(p, s); break;
-    case 24: launch_sl<24>(p, s); break;
-    case 32: launch_sl<32>(p, s); break;
-    case 48: launch_sl<48>(p, s); break;
-    default: launch_sl<64>(p, s); break;
+    case 4: launch_sl<4>(p, multi, s); break;
+    case 8: launch_sl<8>(p, multi, s); break;
+    case 12: launch_sl<12>(p, multi, s); break;
+    case 16: launch_sl<16>(p, multi, s); break;
+    case 20: launch_sl<20>(p, multi, s); break;
+    case 24: launch_sl<24>(p, multi, s); break;
+    case 32: launch_sl<32>(p, multi, s); break;
+    case 40: launch_sl<40>(p, multi, s); break;
+    case 48: launch_sl<48>(p, multi, s); break;
+    default: launch_sl<64>(p, multi, s); break;
   }
+}
+
+// Items of a chunk are split segments first, then whole runs by decreasing
+// length: the first whole run shorter than `threshold` starts the short part.
+static int64_t first_short(const Plan &plan, int64_t b, int64_t e, int threshold) {
+  int64_t lo = b, hi = e;
+  while (lo < hi && plan.items[lo].dst < 0) ++lo;     // segments (at most a few per split row)
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo) / 2;
+    if (plan.items[mid].len >= threshold) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
 }
 
 // Slice count (power of two, at most 8) and slice width (float4, multiple of 4)
 // for a launch of c4 float4 columns: slices of at most ~320 bytes, one slice
 // per XCD when the row is wide.
 static void choose_slices(int c4, int *S, int *SL) {
+  int target = 64;                                           // float4 per slice
+  if (const char *env = std::getenv("PGCN_AGG_SLICE_F4")) {  // tuning override
+    const int v = std::atoi(env);
+    if (v >= 4 && v <= 64) target = v;
+  }
   int s = 1;
-  while (s < 8 && s * 20 < c4) s *= 2;
+  while (s < 8 && s * target < c4) s *= 2;
+  while (s < 8 && s * 64 < c4) s *= 2;                       // a slice holds at most 64 float4
   int need = (c4 + s - 1) / s;
   need = (need + 3) / 4 * 4;
-  static const int widths[] = {4, 8, 12, 16, 20, 24, 32, 48, 64};
+  static const int widths[] = {4, 8, 12, 16, 20, 24, 32, 40, 48, 64};
   int sl = 64;
   for (int w : widths)
     if (w >= need) {
@@ -236,13 +302,24 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
     p.c4_off = off;
     p.c4_cnt = cnt;
     p.slices = S;
+    const int U = SL <= 32 ? 8 : 4;
+    const int threshold = (64 / SL) * U;
     for (int c = 0; c < C; ++c) {
       p.mode = (c == 0 ? AGG_FIRST : 0) | (c == C - 1 ? AGG_LAST : 0);
-      p.items = plan.d_items + plan.chunk_items[c];
-      p.n_items = plan.chunk_items[c + 1] - plan.chunk_items[c];
-      if (p.n_items > 0) {
+      const int64_t b = plan.chunk_items[c], e = plan.chunk_items[c + 1];
+      const int64_t m = first_short(plan, b, e, threshold);
+      if (m > b) {                     // long runs: lane groups share an item
+        p.items = plan.d_items + b;
+        p.n_items = m - b;
         TraceScope ts(a.trace_kind, s);
-        launch_dispatch(p, SL, s);
+        launch_dispatch(p, SL, false, s);
+        PGCN_HIP(hipGetLastError());
+      }
+      if (e > m) {                     // short runs: one item per lane group
+        p.items = plan.d_items + m;
+        p.n_items = e - m;
+        TraceScope ts(a.trace_kind, s);
+        launch_dispatch(p, SL, true, s);
         PGCN_HIP(hipGetLastError());
       }
       const int64_t ns = plan.chunk_splits[c + 1] - plan.chunk_splits[c];

@@ -252,10 +252,11 @@ extern "C" int pgcn_sgd_update(float *W, const float *G, const float *G_peer, in
   return launch_sgd(W, G, G_peer, count, eta, s);
 }
 
-extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, hipStream_t s) {
+extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, hipStream_t s) {
   if (bytes == 0) return PGCN_OK;
   PGCN_REQUIRE(dst && src, "pgcn_refill_async: null buffer");
+  PGCN_REQUIRE((flags & ~(uint32_t)PGCN_REFILL_DMA) == 0, "pgcn_refill_async: unknown flags");
   TraceScope ts(PGCN_TK_REFILL, s);
-  PGCN_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, s));
+  PGCN_HIP(hipMemcpyAsync(dst, src, bytes, (flags & PGCN_REFILL_DMA) ? hipMemcpyDeviceToDeviceNoCU : hipMemcpyDeviceToDevice, s));
   return PGCN_OK;
 }

@@ -11,85 +11,97 @@
 
 namespace pgcn {
 
-__global__ __launch_bounds__(256) void ema_kernel(float *state, const float *in, int64_t rows, int f4,
-                                                  int64_t ld, float gamma) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= rows * f4) return;
-  const int64_t r = i / f4;
-  const int c = 4 * (int)(i % f4);
-  float4 *s = reinterpret_cast<float4 *>(state + r * ld + c);
-  const float4 x = *reinterpret_cast<const float4 *>(in + r * ld + c);
-  float4 v = *s;
+// Row-block mapping shared by the streaming kernels: a 256-thread block covers
+// 256 >> shift rows; the (1 << shift) lanes of a row stride over its float4
+// columns.  shift is chosen so that 1 << shift is the smallest power of two
+// >= the row's float4 count (at most 64 lanes).
+static int lane_shift(int f4) {
+  int sh = 0;
+  while (sh < 6 && (1 << sh) < f4) ++sh;
+  return sh;
+}
+
+static unsigned row_blocks(int64_t rows, int sh) {
+  const int64_t rpb = 256 >> sh;
+  return (unsigned)((rows + rpb - 1) / rpb);
+}
+
+__global__ __launch_bounds__(256) void ema_kernel(float *state, const float *in, int64_t rows, int f4, int64_t ld,
+                                                  float gamma, int sh) {
+  const int64_t r = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
+  if (r >= rows) return;
   const float g1 = 1.0f - gamma;
-  v.x = gamma * v.x + g1 * x.x;
-  v.y = gamma * v.y + g1 * x.y;
-  v.z = gamma * v.z + g1 * x.z;
-  v.w = gamma * v.w + g1 * x.w;
-  *s = v;
+  for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) {
+    float4 *sp = reinterpret_cast<float4 *>(state + r * ld) + c4;
+    const float4 x = reinterpret_cast<const float4 *>(in + r * ld)[c4];
+    float4 v = *sp;
+    v.x = gamma * v.x + g1 * x.x;
+    v.y = gamma * v.y + g1 * x.y;
+    v.z = gamma * v.z + g1 * x.z;
+    v.w = gamma * v.w + g1 * x.w;
+    *sp = v;
+  }
 }
 
 int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_t ld, float gamma,
                hipStream_t s) {
   const int f4 = (cols + 3) / 4;
-  const int64_t total = rows * f4;
-  if (total == 0) return PGCN_OK;
+  if (rows == 0 || f4 == 0) return PGCN_OK;
+  const int sh = lane_shift(f4);
   TraceScope ts(PGCN_TK_EMA, s);
-  hipLaunchKernelGGL(ema_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, state, in, rows, f4,
-                     ld, gamma);
+  hipLaunchKernelGGL(ema_kernel, dim3(row_blocks(rows, sh)), dim3(256), 0, s, state, in, rows, f4, ld, gamma, sh);
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;
 }
 
 __global__ __launch_bounds__(256) void pack_kernel(const int32_t *idx, int64_t count, const float *src,
-                                                   float *dst, int f4, int64_t ld) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= count * f4) return;
-  const int64_t k = i / f4;
-  const int c = 4 * (int)(i % f4);
-  *reinterpret_cast<float4 *>(dst + k * ld + c) =
-      *reinterpret_cast<const float4 *>(src + (int64_t)idx[k] * ld + c);
+                                                   float *dst, int f4, int64_t ld, int sh) {
+  const int64_t k = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
+  if (k >= count) return;
+  const float4 *from = reinterpret_cast<const float4 *>(src + (int64_t)idx[k] * ld);
+  float4 *to = reinterpret_cast<float4 *>(dst + k * ld);
+  for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) to[c4] = from[c4];
 }
 
 int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst, int32_t cols, int64_t ld,
                 hipStream_t s) {
   const int f4 = (cols + 3) / 4;
-  const int64_t total = count * f4;
-  if (total == 0) return PGCN_OK;
+  if (count == 0 || f4 == 0) return PGCN_OK;
+  const int sh = lane_shift(f4);
   TraceScope ts(PGCN_TK_PACK, s);
-  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, idx, count, src, dst,
-                     f4, ld);
+  hipLaunchKernelGGL(pack_kernel, dim3(row_blocks(count, sh)), dim3(256), 0, s, idx, count, src, dst, f4, ld, sh);
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;
 }
 
 __global__ __launch_bounds__(256) void accum_kernel(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows,
-                                                    const float *src, float *dst, int f4, int64_t ld) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= rows * f4) return;
-  const int64_t u = i / f4;
-  const int c = 4 * (int)(i % f4);
+                                                    const float *src, float *dst, int f4, int64_t ld, int sh) {
+  const int64_t u = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
+  if (u >= rows) return;
   const int64_t b = inv_ptr[u], e = inv_ptr[u + 1];
   if (b == e) return;
-  float4 *d = reinterpret_cast<float4 *>(dst + u * ld + c);
-  float4 v = *d;
-  for (int64_t q = b; q < e; ++q) {
-    const float4 x = *reinterpret_cast<const float4 *>(src + (int64_t)inv_k[q] * ld + c);
-    v.x += x.x;
-    v.y += x.y;
-    v.z += x.z;
-    v.w += x.w;
+  float4 *d = reinterpret_cast<float4 *>(dst + u * ld);
+  for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) {
+    float4 v = d[c4];
+    for (int64_t q = b; q < e; ++q) {   // ascending send-list position: ascending peer
+      const float4 x = reinterpret_cast<const float4 *>(src + (int64_t)inv_k[q] * ld)[c4];
+      v.x += x.x;
+      v.y += x.y;
+      v.z += x.z;
+      v.w += x.w;
+    }
+    d[c4] = v;
   }
-  *d = v;
 }
 
 int launch_accum(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, const float *src, float *dst,
                  int32_t cols, int64_t ld, hipStream_t s) {
   const int f4 = (cols + 3) / 4;
-  const int64_t total = rows * f4;
-  if (total == 0) return PGCN_OK;
+  if (rows == 0 || f4 == 0) return PGCN_OK;
+  const int sh = lane_shift(f4);
   TraceScope ts(PGCN_TK_ACCUM, s);
-  hipLaunchKernelGGL(accum_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, inv_ptr, inv_k, rows,
-                     src, dst, f4, ld);
+  hipLaunchKernelGGL(accum_kernel, dim3(row_blocks(rows, sh)), dim3(256), 0, s, inv_ptr, inv_k, rows, src, dst, f4,
+                     ld, sh);
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;
 }

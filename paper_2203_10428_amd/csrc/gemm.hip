@@ -447,13 +447,21 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GP p) {
       }
 }
 
-// Fixed-order sum of split partials: out[i] = sum_z ws[z][i], z ascending.
+// Fixed-order sum of split partials.  A block owns 64 consecutive outputs and
+// 4 quarters of the split range; quarter q adds its splits in ascending order,
+// then the quarters are added in order q = 0, 1, 2, 3.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *ws, int splits, int64_t mn, float *out) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= mn) return;
+  __shared__ float part[4][64];
+  const int o = threadIdx.x % 64, q = threadIdx.x / 64;
+  const int64_t i = (int64_t)blockIdx.x * 64 + o;
+  const int per = (splits + 3) / 4;
+  const int z0 = q * per, z1 = min(splits, z0 + per);
   float s = 0.f;
-  for (int z = 0; z < splits; ++z) s += ws[(int64_t)z * mn + i];
-  out[i] = s;
+  if (i < mn)
+    for (int z = z0; z < z1; ++z) s += ws[(int64_t)z * mn + i];
+  part[q][o] = s;
+  __syncthreads();
+  if (q == 0 && i < mn) out[i] = ((part[0][o] + part[1][o]) + part[2][o]) + part[3][o];
 }
 
 // ---------------------------------------------------------------- launch ---
@@ -541,7 +549,7 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
       if (rc) return rc;
       const int64_t mn = (int64_t)g.M * g.N;
       TraceScope ts(PGCN_TK_WGRAD_REDUCE, s);
-      hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0, s,
+      hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((mn + 63) / 64)), dim3(256), 0, s,
                          (const float *)g.workspace, splits, mn, g.C);
       PGCN_HIP(hipGetLastError());
       return PGCN_OK;

@@ -22,9 +22,9 @@ int check_hip(hipError_t e, const char *what) {
   return set_error(PGCN_EHIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-// Number of column chunks of a CSR matrix for cache blocking: enough that one
-// chunk's slice (up to 320 bytes per gathered row) of the gathered rows spans
-// about 6 MB, but only while a row keeps >= 64 non-zeros per chunk on average.
+// Number of column chunks of a CSR matrix for cache blocking: chunks of about
+// 11,000 gathered rows (the measured optimum for 1 KB rows on MI355X), but
+// only while a row keeps >= 32 non-zeros per chunk on average.
 static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz) {
   const char *env = std::getenv("PGCN_AGG_CHUNKS");
   if (env) {
@@ -32,8 +32,8 @@ static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz) {
     if (v >= 1 && v <= 64) return v;
   }
   if (nrows == 0 || ncols == 0) return 1;
-  const int64_t by_cache = (ncols * 320 + (6 << 20) - 1) / (6 << 20);
-  const int64_t by_len = (nnz / nrows) / 64;
+  const int64_t by_cache = (ncols + 10999) / 11000;
+  const int64_t by_len = (nnz / nrows) / 32;
   int64_t c = std::min(by_cache, by_len);
   return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, 16));
 }

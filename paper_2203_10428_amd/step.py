@@ -44,6 +44,7 @@ class StepOptions:
     eta: float = 0.01
     relu_last: bool = False
     copy_mode: str = "pipe"          # "pipe" | "serial" | "none"
+    refill_dma: bool = False         # refills by the DMA engines instead of a blit kernel
 
 
 class PartitionTrainer:
@@ -125,7 +126,8 @@ class PartitionTrainer:
         return l < self.L or self.opts.relu_last
 
     def _refill(self, dst, src, stream):
-        B.pgcn_refill_async(dst, src, dst.numel() * dst.element_size(), stream)
+        B.pgcn_refill_async(dst, src, dst.numel() * dst.element_size(),
+                            B.PGCN_REFILL_DMA if self.opts.refill_dma else 0, stream)
 
     def step(self):
         o, L, wd = self.opts, self.L, self.widths

@@ -101,14 +101,16 @@ def test_tiny_injected(variant, dt):
         compare_step(tr, r0, dt, L, w.widths)
 
 
+@pytest.mark.parametrize("refill_dma", [False, True])
 @pytest.mark.parametrize("variant", list(VARIANTS))
-def test_tiny_autonomous_pipeline(variant):
+def test_tiny_autonomous_pipeline(variant, refill_dma):
     sf, sg = VARIANTS[variant]
     T = 4
     w, g, d, sim, recs = tiny_setup(T, sf, sg)
     L = w.layers
     tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, "f32",
-                          StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe"))
+                          StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
+                                      refill_dma=refill_dma))
     for t in range(1, T + 1):
         r0, r1 = recs[t - 1][0], recs[t - 1][1]
         so = r0["state_out"]
@@ -126,11 +128,12 @@ def test_tiny_autonomous_pipeline(variant):
         compare_step(tr, r0, "f32", L, w.widths, check_state=True)
 
 
-def test_tiny_stale_buffers_never_read_before_refill():
+@pytest.mark.parametrize("refill_dma", [False, True])
+def test_tiny_stale_buffers_never_read_before_refill(refill_dma):
     """A NaN sentinel in the buffer being refilled must never reach an output."""
     w, g, d, sim, recs = tiny_setup(1, True, True)
     tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, "f32",
-                          StepOptions(copy_mode="pipe"))
+                          StepOptions(copy_mode="pipe", refill_dma=refill_dma))
     for _ in range(3):
         torch.cuda.synchronize()
         nxt = 1 - tr.cur
