@@ -69,6 +69,25 @@ def algorithmic_work(tr, w):
     return out
 
 
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per step of `kernel` from committed counter runs, if still valid.
+
+    profiles/traffic_<workload>.json holds FETCH_SIZE and WRITE_SIZE summed over
+    the kernel's dispatches of one step, scaled by the same counters on a plain
+    copy of known size, and the SHA-256 of the kernel source they were taken
+    with.  If the source has changed since, the figure no longer applies (None).
+    """
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = os.path.join(ROOT, "paper_2203_10428_amd", "csrc", rec["source"])
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+        return None
+    return rec["kernels"].get(kernel)
+
+
 def cpu_baseline(w, scale: float):
     """Time the fp64 oracle's per-partition step on a sample of the workload."""
     import numpy as np
@@ -112,7 +131,19 @@ def main():
     ap.add_argument("--refill", default="dma", choices=["dma", "blit"], help="engine of the stale-buffer refills")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=0.25, help="inner-node fraction timed on the CPU")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run 5 plain device copies of BYTES bytes (counter calibration) and exit")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        n = args.calibrate_copy // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n * 4, "copies": 5}))
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -183,8 +214,11 @@ def main():
             util[k] = {"TFLOPs": work[k] / sec / 1e12, "mfma_frac": work[k] / sec / 1e12 / MFMA_PEAK_TFLOPS[dt]}
     if dominant.startswith("agg"):
         ach = util[dominant]["GBps_compulsory"]
+        tr_bytes = measured_traffic(w.name, dominant)
         roof = {"bound": "hbm", "kernel": dominant, "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": ach / HBM_PEAK_GBPS, "traffic": None,
+                "frac": ach / HBM_PEAK_GBPS,
+                "traffic": None if tr_bytes is None else tr_bytes / per_step[dominant]["launches"],
+                "traffic_GBps": None if tr_bytes is None else tr_bytes / (per_step[dominant]["ms_per_step"] / 1e3) / 1e9,
                 "gather_model_GBps": util[dominant]["GBps_gather_model"],
                 "algorithmic_bytes_per_step": work[dominant],
                 "launches_per_step": per_step[dominant]["launches"],
