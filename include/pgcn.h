@@ -268,7 +268,8 @@ int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, 
 enum pgcn_trace_kind {
   PGCN_TK_AGG_FWD = 0, PGCN_TK_AGG_BWD = 1, PGCN_TK_AGG_FIXUP = 2, PGCN_TK_GEMM_FWD = 3,
   PGCN_TK_GEMM_DGRAD = 4, PGCN_TK_GEMM_WGRAD = 5, PGCN_TK_WGRAD_REDUCE = 6, PGCN_TK_EMA = 7,
-  PGCN_TK_PACK = 8, PGCN_TK_ACCUM = 9, PGCN_TK_LOSS = 10, PGCN_TK_SGD = 11, PGCN_TK_REFILL = 12
+  PGCN_TK_PACK = 8, PGCN_TK_ACCUM = 9, PGCN_TK_LOSS = 10, PGCN_TK_SGD = 11, PGCN_TK_REFILL = 12,
+  PGCN_TK_GEMM_PACK = 13
 };
 int pgcn_trace_enable(int32_t capacity);
 int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t max_records, int32_t *count);

@@ -229,7 +229,7 @@ def pgcn_refill_async(dst, src, nbytes: int, flags: int = 0, stream=None):
 
 
 TRACE_KINDS = ["agg_fwd", "agg_bwd", "agg_fixup", "gemm_fwd", "gemm_dgrad", "gemm_wgrad", "wgrad_reduce", "ema",
-               "pack", "accum", "loss", "sgd", "refill"]
+               "pack", "accum", "loss", "sgd", "refill", "gemm_pack"]
 
 
 def pgcn_trace_enable(capacity: int):

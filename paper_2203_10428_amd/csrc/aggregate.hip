@@ -204,7 +204,7 @@ __global__ __launch_bounds__(256) void agg_fixup_kernel(AggParams p, const Split
 
 template <int SL>
 static void launch_sl(const AggParams &p, bool multi, hipStream_t s) {
-  constexpr int U = SL <= 32 ? 8 : 4;
+  constexpr int U = 8;
   constexpr int G = 64 / SL;
   if (multi) {
     const int64_t blocks = (p.n_items + 4 * G - 1) / (4 * G) * p.slices;
@@ -302,7 +302,7 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
     p.c4_off = off;
     p.c4_cnt = cnt;
     p.slices = S;
-    const int U = SL <= 32 ? 8 : 4;
+    const int U = 8;
     const int threshold = (64 / SL) * U;
     for (int c = 0; c < C; ++c) {
       p.mode = (c == 0 ? AGG_FIRST : 0) | (c == C - 1 ? AGG_LAST : 0);

@@ -26,12 +26,18 @@ size_t fwd_acc_bytes(const pgcn_partition *p, int32_t f_in, int32_t gemm_dtype) 
   if (p->plan.chunks <= 1 || gemm_dtype != PGCN_BF16) return 0;
   return align_up((size_t)p->n_inner * (size_t)ld4(f_in) * sizeof(float), 256);
 }
-size_t fwd_ws(const pgcn_partition *p, int32_t f_in, int32_t gemm_dtype) {
+// forward workspace: [aggregation partials | running sum | packed weights]
+size_t fwd_agg_bytes(const pgcn_partition *p, int32_t f_in, int32_t gemm_dtype) {
   return align_up(aggregate_workspace(p->plan, f_in), 256) + fwd_acc_bytes(p, f_in, gemm_dtype);
 }
+size_t fwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) {
+  return fwd_agg_bytes(p, f_in, gemm_dtype) + gemm_nk_workspace(f_out, f_in, gemm_dtype);
+}
 
-// backward: the split-K partials are consumed before D is written, so they share space
-size_t bwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_grad) {
+// backward workspace: [region 0 | packed weights].  Region 0 first holds the
+// split-K partials of the weight gradient, which are consumed before it is
+// reused for D and the transposed aggregation's partials.
+size_t bwd_region0(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_grad) {
   size_t g = gemm_workspace(Gemm::TN_MASK_SPLITK, f_in, f_out, (int32_t)p->n_inner);
   size_t d = 0;
   if (input_grad)
@@ -39,13 +45,16 @@ size_t bwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_g
         align_up(aggregate_workspace(p->plan_t, f_in), 256);
   return align_up(g > d ? g : d, 256);
 }
+size_t bwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_grad, int32_t gemm_dtype) {
+  return bwd_region0(p, f_in, f_out, input_grad) + (input_grad ? gemm_nk_workspace(f_in, f_out, gemm_dtype) : 0);
+}
 
 }  // namespace
 
 extern "C" size_t pgcn_workspace_size(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) {
   if (!p || f_in <= 0 || f_out <= 0) return 0;
-  size_t w = fwd_ws(p, f_in, gemm_dtype);
-  size_t b = bwd_ws(p, f_in, f_out, true);
+  size_t w = fwd_ws(p, f_in, f_out, gemm_dtype);
+  size_t b = bwd_ws(p, f_in, f_out, true, gemm_dtype);
   size_t l = align_up(loss_workspace(p->n_inner), 256);
   size_t m = w > b ? w : b;
   return m > l ? m : l;
@@ -71,7 +80,7 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
     }
     PGCN_REQUIRE(!a->A || aligned16(a->A), "pgcn_layer_fwd: A must be 16-byte aligned");
   }
-  const size_t need = fwd_ws(p, a->f_in, a->gemm_dtype);
+  const size_t need = fwd_ws(p, a->f_in, a->f_out, a->gemm_dtype);
   if (need > 0 && (!a->workspace || a->workspace_bytes < need))
     return set_error(PGCN_EWORKSPACE, "pgcn_layer_fwd: workspace too small");
   if (p->n_inner == 0) return PGCN_OK;
@@ -112,7 +121,9 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   m.ldb = a->f_out;
   m.C = a->H_out;
   m.ldc = a->ld_out;
-  return launch_gemm(a->relu ? Gemm::NN_RELU : Gemm::NN_PLAIN, m, s);
+  m.workspace = (float *)((char *)a->workspace + fwd_agg_bytes(p, a->f_in, a->gemm_dtype));
+  m.workspace_bytes = gemm_nk_workspace(a->f_out, a->f_in, a->gemm_dtype);
+  return launch_gemm_nk(a->relu ? Gemm::NN_RELU : Gemm::NN_PLAIN, m, s);
 }
 
 extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, hipStream_t s) {
@@ -141,7 +152,7 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
     else
       PGCN_REQUIRE(a->A && aligned16(a->A), "pgcn_layer_bwd: fp32 path needs A (16-byte aligned)");
   }
-  const size_t need = bwd_ws(p, a->f_in, a->f_out, input_grad);
+  const size_t need = bwd_ws(p, a->f_in, a->f_out, input_grad, a->gemm_dtype);
   if (need > 0 && (!a->workspace || a->workspace_bytes < need))
     return set_error(PGCN_EWORKSPACE, "pgcn_layer_bwd: workspace too small");
 
@@ -184,7 +195,9 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   d.C = D;
   d.ldc = ld_d;
   d.rowscale = p->d_inv_deg;
-  rc = launch_gemm(Gemm::MASK_NT_ROWSCALE, d, s);
+  d.workspace = (float *)((char *)a->workspace + bwd_region0(p, a->f_in, a->f_out, input_grad));
+  d.workspace_bytes = gemm_nk_workspace(a->f_in, a->f_out, a->gemm_dtype);
+  rc = launch_gemm_nk(Gemm::MASK_NT_ROWSCALE, d, s);
   if (rc) return rc;
 
   AggArgs t{};

@@ -111,7 +111,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GP p) {
   float rb[SB];
   float4 rbv[VB];
 
-  auto load = [&](int kt) {
+  auto load = [&](int kt) __attribute__((always_inline)) {
     if (AK == A_MK_F32 || AK == A_MK_MASK) {
 #pragma unroll
       for (int v = 0; v < VA; ++v) {
@@ -163,7 +163,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GP p) {
     }
   };
 
-  auto store = [&]() {
+  auto store = [&]() __attribute__((always_inline)) {
     if (AK == A_MK_F32 || AK == A_MK_MASK) {
 #pragma unroll
       for (int v = 0; v < VA; ++v) {
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GP p) {
     return make_uint4(w[0], w[1], w[2], w[3]);
   };
 
-  auto load = [&](int kt) {
+  auto load = [&](int kt) __attribute__((always_inline)) {
     if (AK == A_MK_BF16) {
 #pragma unroll
       for (int v = 0; v < VA; ++v) {
@@ -359,7 +359,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GP p) {
     }
   };
 
-  auto store = [&]() {
+  auto store = [&]() __attribute__((always_inline)) {
     if (AK == A_KM_BF16) {
 #pragma unroll
       for (int v = 0; v < VA; ++v) {

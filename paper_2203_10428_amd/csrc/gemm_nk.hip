@@ -1,0 +1,389 @@
+// Node-major update GEMMs of a GCN layer (Appendix A.1), C[M x N] = A[M x K] B^T
+// with M = inner rows:
+//   forward       Z = A W,                         A = aggregated features, B(n,k) = W[k][n]
+//   feature grad  D = diag(1/d) ((J ∘ 1[H>0]) W^T), A = masked gradient,     B(n,k) = W[n][k]
+//
+// The right operand (the layer's weights, at most a few MB) is first packed
+// once per call into an n-major, k-contiguous matrix zero-padded to a 128-row
+// and 64-column multiple (fp32, or bf16 rounded to nearest even for the bf16
+// path), so the main loop loads both operands as 16-byte vectors with no
+// bounds checks on the weights.
+//
+// Main loop for CDNA4: a 256-thread workgroup (4 wave64s, 2 x 2) computes a
+// 128 x BN tile; both tiles sit in LDS with k contiguous and are double
+// buffered, so one barrier per k-slab suffices while the next slab's global
+// loads are in flight.  The MFMA k order is permuted so that each lane's
+// fragments over a slab are contiguous in LDS and load with 128-bit reads:
+//   fp32, v_mfma_f32_32x32x2f32, slab of 32: step s uses k = 16*h + s for
+//        lane half h (lanes 32h .. 32h+31);
+//   bf16, v_mfma_f32_32x32x16_bf16, slab of 64: step j uses k = 32*h + 8*j
+//        .. 32*h + 8*j + 7 for lane half h.
+// Every k of the slab is used exactly once per output element.
+#include "internal.h"
+
+namespace pgcn {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+struct NKParams {
+  int M, N, K;
+  int tiles_n;
+  const float *A;          // fp32 activations [M, lda] (k contiguous)
+  const uint16_t *A16;     // bf16 activations [M, lda]
+  int64_t lda;
+  const float *Am;         // mask source of A (ReLU output), or null
+  int64_t ldam;
+  const void *B;           // packed weights [rows >= tiles_n * BN, ldb]
+  int64_t ldb;
+  float *C;
+  int64_t ldc;
+  const float *rowscale;
+};
+
+enum NKA { NK_A_F32, NK_A_BF16, NK_A_MASK };
+enum NKE { NK_E_RELU, NK_E_PLAIN, NK_E_ROWSCALE };
+
+__device__ __forceinline__ uint16_t nk_bf16(float x) {
+  uint32_t b = __float_as_uint(x);
+  if ((b & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((b >> 16) | 0x40u);
+  b += 0x7fffu + ((b >> 16) & 1u);
+  return (uint16_t)(b >> 16);
+}
+
+__device__ __forceinline__ int nk_xcd_remap(int b, int g) {
+  if (g % 8 != 0) return b;
+  return (b % 8) * (g / 8) + b / 8;
+}
+
+__device__ __forceinline__ float4 nk_ld4(const float *p, int valid) {
+  float4 v = *reinterpret_cast<const float4 *>(p);
+  if (valid < 4) {
+    v.w = 0.f;
+    if (valid < 3) v.z = 0.f;
+    if (valid < 2) v.y = 0.f;
+    if (valid < 1) v.x = 0.f;
+  }
+  return v;
+}
+
+__device__ __forceinline__ float4 nk_mask(float4 j, const float *h) {
+  const float4 m = *reinterpret_cast<const float4 *>(h);
+  j.x = m.x > 0.f ? j.x : 0.f;
+  j.y = m.y > 0.f ? j.y : 0.f;
+  j.z = m.z > 0.f ? j.z : 0.f;
+  j.w = m.w > 0.f ? j.w : 0.f;
+  return j;
+}
+
+template <int EK>
+__device__ __forceinline__ void nk_store(const NKParams &p, int row, int col, float v) {
+  if (row >= p.M || col >= p.N) return;
+  float *c = p.C + (int64_t)row * p.ldc + col;
+  if (EK == NK_E_RELU) *c = v > 0.f ? v : 0.f;
+  else if (EK == NK_E_PLAIN) *c = v;
+  else *c = v * p.rowscale[row];
+}
+
+// out[n][k] = (n < N && k < K) ? (trans ? W[k*ldw + n] : W[n*ldw + k]) : 0, for n < rows, k < ldk
+template <bool BF16>
+__global__ __launch_bounds__(256) void pack_b_kernel(const float *W, int ldw, int trans, int N, int K, int rows,
+                                                     int ldk, void *out) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * ldk) return;
+  const int n = i / ldk, k = i - n * ldk;
+  const float v = (n < N && k < K) ? (trans ? W[(int64_t)k * ldw + n] : W[(int64_t)n * ldw + k]) : 0.f;
+  if (BF16) reinterpret_cast<uint16_t *>(out)[i] = nk_bf16(v);
+  else reinterpret_cast<float *>(out)[i] = v;
+}
+
+template <int EK, int TM, int TN>
+__device__ __forceinline__ void nk_epilogue(const NKParams &p, const f32x16 (&acc)[TM][TN], int m0, int n0,
+                                            int lane) {
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        nk_store<EK>(p, m0 + i * 32 + 8 * (r / 4) + 4 * (lane / 32) + (r % 4), n0 + j * 32 + lane % 32,
+                     acc[i][j][r]);
+}
+
+// ------------------------------------------------------------------ fp32 ---
+
+template <int BM, int BN, int AK, int EK>
+__global__ __launch_bounds__(256, 2) void gemm_nk_f32(NKParams p) {
+  constexpr int BK = 32, LK = BK + 4;
+  constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
+  constexpr int VA = BM * BK / 4 / 256, VB = BN * BK / 4 / 256;
+  __shared__ __attribute__((aligned(16))) float As[2][BM * LK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LK];
+
+  const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+  const int tile = nk_xcd_remap(blockIdx.x, gridDim.x);
+  const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
+  const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
+  const float *Bp = reinterpret_cast<const float *>(p.B);
+
+  f32x4 ra[VA], rb[VB];
+  auto load = [&](int kt) __attribute__((always_inline)) {
+#pragma unroll
+    for (int v = 0; v < VA; ++v) {
+      const int idx = t + 256 * v, m = idx >> 3, k4 = idx & 7;
+      const int gm = m0 + m, gk = kt + 4 * k4;
+      float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (gm < p.M && gk < p.K) {
+        x = nk_ld4(p.A + (int64_t)gm * p.lda + gk, p.K - gk);
+        if (AK == NK_A_MASK && p.Am) x = nk_mask(x, p.Am + (int64_t)gm * p.ldam + gk);
+      }
+      ra[v] = f32x4{x.x, x.y, x.z, x.w};
+    }
+#pragma unroll
+    for (int v = 0; v < VB; ++v) {
+      const int idx = t + 256 * v, n = idx >> 3, k4 = idx & 7;
+      rb[v] = *reinterpret_cast<const f32x4 *>(Bp + (int64_t)(n0 + n) * p.ldb + kt + 4 * k4);
+    }
+  };
+  auto store = [&](int b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int v = 0; v < VA; ++v) {
+      const int idx = t + 256 * v;
+      *reinterpret_cast<f32x4 *>(&As[b][(idx >> 3) * LK + 4 * (idx & 7)]) = ra[v];
+    }
+#pragma unroll
+    for (int v = 0; v < VB; ++v) {
+      const int idx = t + 256 * v;
+      *reinterpret_cast<f32x4 *>(&Bs[b][(idx >> 3) * LK + 4 * (idx & 7)]) = rb[v];
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
+
+  const int h = lane >> 5, r = lane & 31;
+  load(0);
+  store(0);
+  __syncthreads();
+  int it = 0;
+  for (int kt = 0; kt < p.K; kt += BK, ++it) {
+    const int cur = it & 1;
+    // next slab's global loads in flight during this slab's MFMAs; the last
+    // iteration reloads the current slab into the idle buffer (keeps the
+    // staging registers free of control flow)
+    load(kt + BK < p.K ? kt + BK : kt);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      f32x4 a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        a[i] = *reinterpret_cast<const f32x4 *>(&As[cur][(wm0 + i * 32 + r) * LK + 16 * h + 4 * q]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        b[j] = *reinterpret_cast<const f32x4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + 16 * h + 4 * q]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
+    }
+    store(cur ^ 1);
+    __syncthreads();
+  }
+  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane);
+}
+
+// ------------------------------------------------------------------ bf16 ---
+
+template <int BM, int BN, int AK, int EK>
+__global__ __launch_bounds__(256, 2) void gemm_nk_bf16(NKParams p) {
+  constexpr int BK = 64, LK = BK + 8;                  // bf16 elements; 144-byte rows
+  constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
+  constexpr int VA = BM * BK / 8 / 256, VB = BN * BK / 8 / 256;
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LK];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LK];
+
+  const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+  const int tile = nk_xcd_remap(blockIdx.x, gridDim.x);
+  const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
+  const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
+  const uint16_t *Bp = reinterpret_cast<const uint16_t *>(p.B);
+
+  auto pack8 = [](float4 x, float4 y) {
+    uint4 o;
+    o.x = (uint32_t)nk_bf16(x.x) | ((uint32_t)nk_bf16(x.y) << 16);
+    o.y = (uint32_t)nk_bf16(x.z) | ((uint32_t)nk_bf16(x.w) << 16);
+    o.z = (uint32_t)nk_bf16(y.x) | ((uint32_t)nk_bf16(y.y) << 16);
+    o.w = (uint32_t)nk_bf16(y.z) | ((uint32_t)nk_bf16(y.w) << 16);
+    return o;
+  };
+  auto zero_tail = [](uint4 v, int valid) {       // zero bf16 elements >= valid
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (e >= valid) w[e / 2] &= (e % 2) ? 0x0000ffffu : 0xffff0000u;
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  };
+
+  u32x4 ra[VA], rb[VB];
+  auto load = [&](int kt) __attribute__((always_inline)) {
+#pragma unroll
+    for (int v = 0; v < VA; ++v) {
+      const int idx = t + 256 * v, m = idx >> 3, k8 = idx & 7;
+      const int gm = m0 + m, gk = kt + 8 * k8;
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (gm < p.M && gk < p.K) {
+        if (AK == NK_A_BF16) {
+          x = *reinterpret_cast<const uint4 *>(p.A16 + (int64_t)gm * p.lda + gk);
+          if (p.K - gk < 8) x = zero_tail(x, p.K - gk);
+        } else {
+          const float *row = p.A + (int64_t)gm * p.lda + gk;
+          float4 x0 = nk_ld4(row, p.K - gk), x1 = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (AK == NK_A_MASK && p.Am) x0 = nk_mask(x0, p.Am + (int64_t)gm * p.ldam + gk);
+          if (gk + 4 < p.K) {
+            x1 = nk_ld4(row + 4, p.K - gk - 4);
+            if (AK == NK_A_MASK && p.Am) x1 = nk_mask(x1, p.Am + (int64_t)gm * p.ldam + gk + 4);
+          }
+          x = pack8(x0, x1);
+        }
+      }
+      ra[v] = u32x4{x.x, x.y, x.z, x.w};
+    }
+#pragma unroll
+    for (int v = 0; v < VB; ++v) {
+      const int idx = t + 256 * v, n = idx >> 3, k8 = idx & 7;
+      rb[v] = *reinterpret_cast<const u32x4 *>(Bp + (int64_t)(n0 + n) * p.ldb + kt + 8 * k8);
+    }
+  };
+  auto store = [&](int b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int v = 0; v < VA; ++v) {
+      const int idx = t + 256 * v;
+      *reinterpret_cast<u32x4 *>(&As[b][(idx >> 3) * LK + 8 * (idx & 7)]) = ra[v];
+    }
+#pragma unroll
+    for (int v = 0; v < VB; ++v) {
+      const int idx = t + 256 * v;
+      *reinterpret_cast<u32x4 *>(&Bs[b][(idx >> 3) * LK + 8 * (idx & 7)]) = rb[v];
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
+
+  const int h = lane >> 5, r = lane & 31;
+  load(0);
+  store(0);
+  __syncthreads();
+  int it = 0;
+  for (int kt = 0; kt < p.K; kt += BK, ++it) {
+    const int cur = it & 1;
+    // next slab's global loads in flight during this slab's MFMAs; the last
+    // iteration reloads the current slab into the idle buffer (keeps the
+    // staging registers free of control flow)
+    load(kt + BK < p.K ? kt + BK : kt);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      bf16x8 a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&As[cur][(wm0 + i * 32 + r) * LK + 32 * h + 8 * q]));
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + 32 * h + 8 * q]));
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    store(cur ^ 1);
+    __syncthreads();
+  }
+  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane);
+}
+
+// ---------------------------------------------------------------- launch ---
+
+static int64_t nk_ldk(int K) { return ((int64_t)K + 63) / 64 * 64; }
+static int64_t nk_rows(int N) { return ((int64_t)N + 127) / 128 * 128; }
+
+size_t gemm_nk_workspace(int32_t N, int32_t K, int32_t dtype) {
+  const size_t el = dtype == PGCN_BF16 ? 2 : 4;
+  return align_up((size_t)nk_rows(N) * (size_t)nk_ldk(K) * el, 256);
+}
+
+template <int BN, int AK, int EK>
+static void nk_launch(const NKParams &p0, bool bf16, hipStream_t s) {
+  constexpr int BM = 128;
+  NKParams p = p0;
+  const int tm = (p.M + BM - 1) / BM, tn = (p.N + BN - 1) / BN;
+  p.tiles_n = tn;
+  if (bf16) {
+    constexpr int AKb = AK == NK_A_F32 ? NK_A_BF16 : AK;
+    hipLaunchKernelGGL((gemm_nk_bf16<BM, BN, AKb, EK>), dim3((unsigned)(tm * tn)), dim3(256), 0, s, p);
+  } else {
+    hipLaunchKernelGGL((gemm_nk_f32<BM, BN, AK, EK>), dim3((unsigned)(tm * tn)), dim3(256), 0, s, p);
+  }
+}
+
+template <int AK, int EK>
+static void nk_launch_bn(const NKParams &p, bool bf16, hipStream_t s) {
+  if (p.N <= 64) nk_launch<64, AK, EK>(p, bf16, s);
+  else nk_launch<128, AK, EK>(p, bf16, s);
+}
+
+// kind: NN_RELU / NN_PLAIN (forward: B(n,k) = W[k][n]) or MASK_NT_ROWSCALE
+// (feature gradient: B(n,k) = W[n][k]); g.workspace holds the packed weights.
+int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return PGCN_OK;
+  const bool bf16 = g.dtype == PGCN_BF16;
+  const size_t need = gemm_nk_workspace(g.N, g.K, g.dtype);
+  if (!g.workspace || g.workspace_bytes < need)
+    return set_error(PGCN_EWORKSPACE, "update GEMM: workspace too small for the packed weights");
+  const int rows = (int)nk_rows(g.N), ldk = (int)nk_ldk(g.K);
+  const bool fwd = kind == Gemm::NN_RELU || kind == Gemm::NN_PLAIN;
+  {
+    TraceScope ts(PGCN_TK_GEMM_PACK, s);
+    const unsigned blocks = (unsigned)(((int64_t)rows * ldk + 255) / 256);
+    if (bf16)
+      hipLaunchKernelGGL(pack_b_kernel<true>, dim3(blocks), dim3(256), 0, s, g.B, (int)g.ldb, fwd ? 1 : 0, g.N, g.K,
+                         rows, ldk, (void *)g.workspace);
+    else
+      hipLaunchKernelGGL(pack_b_kernel<false>, dim3(blocks), dim3(256), 0, s, g.B, (int)g.ldb, fwd ? 1 : 0, g.N,
+                         g.K, rows, ldk, (void *)g.workspace);
+    PGCN_HIP(hipGetLastError());
+  }
+  NKParams p{};
+  p.M = g.M;
+  p.N = g.N;
+  p.K = g.K;
+  p.A = g.A;
+  p.A16 = g.A16;
+  p.lda = g.lda;
+  p.Am = g.Hmask;
+  p.ldam = g.ldm;
+  p.B = g.workspace;
+  p.ldb = ldk;
+  p.C = g.C;
+  p.ldc = g.ldc;
+  p.rowscale = g.rowscale;
+  TraceScope ts(fwd ? PGCN_TK_GEMM_FWD : PGCN_TK_GEMM_DGRAD, s);
+  if (kind == Gemm::NN_RELU) nk_launch_bn<NK_A_F32, NK_E_RELU>(p, bf16, s);
+  else if (kind == Gemm::NN_PLAIN) nk_launch_bn<NK_A_F32, NK_E_PLAIN>(p, bf16, s);
+  else nk_launch_bn<NK_A_MASK, NK_E_ROWSCALE>(p, bf16, s);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
+}
+
+}  // namespace pgcn

@@ -137,6 +137,9 @@ struct GemmArgs {
 };
 int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s);
 size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K);
+// forward and feature-gradient GEMMs: weights packed into g.workspace first
+int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s);
+size_t gemm_nk_workspace(int32_t N, int32_t K, int32_t dtype);
 
 int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_t ld, float gamma,
                hipStream_t s);
