@@ -12,12 +12,16 @@
 // Main loop for CDNA4: a 256-thread workgroup (4 wave64s, 2 x 2) computes a
 // 128 x BN tile; both tiles sit in LDS with k contiguous and are double
 // buffered, so one barrier per k-slab suffices while the next slab's global
-// loads are in flight.  The MFMA k order is permuted so that each lane's
-// fragments over a slab are contiguous in LDS and load with 128-bit reads:
-//   fp32, v_mfma_f32_32x32x2f32, slab of 32: step s uses k = 16*h + s for
+// loads are in flight.  Slabs are short (16 fp32 / 32 bf16 values of k) so
+// that three workgroups fit per CU: the staging of one workgroup's next slab
+// (global load -> registers -> LDS) hides behind the others' MFMAs, which
+// measured faster than longer slabs at two workgroups per CU.  The MFMA k
+// order is permuted so that each lane's fragments over a slab are contiguous
+// in LDS and load with 128-bit reads:
+//   fp32, v_mfma_f32_32x32x2f32, slab of 16: step s uses k = 8*h + s for
 //        lane half h (lanes 32h .. 32h+31);
-//   bf16, v_mfma_f32_32x32x16_bf16, slab of 64: step j uses k = 32*h + 8*j
-//        .. 32*h + 8*j + 7 for lane half h.
+//   bf16, v_mfma_f32_32x32x16_bf16, slab of 32: step j uses k = 16*h + 8*j
+//        .. 16*h + 8*j + 7 for lane half h.
 // Every k of the slab is used exactly once per output element.
 #include "internal.h"
 
@@ -115,8 +119,8 @@ __device__ __forceinline__ void nk_epilogue(const NKParams &p, const f32x16 (&ac
 // ------------------------------------------------------------------ fp32 ---
 
 template <int BM, int BN, int AK, int EK>
-__global__ __launch_bounds__(256, 2) void gemm_nk_f32(NKParams p) {
-  constexpr int BK = 32, LK = BK + 4;
+__global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
+  constexpr int BK = 16, LK = BK + 4, KV = BK / 4;
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
   constexpr int VA = BM * BK / 4 / 256, VB = BN * BK / 4 / 256;
   __shared__ __attribute__((aligned(16))) float As[2][BM * LK];
@@ -132,7 +136,7 @@ __global__ __launch_bounds__(256, 2) void gemm_nk_f32(NKParams p) {
   auto load = [&](int kt) __attribute__((always_inline)) {
 #pragma unroll
     for (int v = 0; v < VA; ++v) {
-      const int idx = t + 256 * v, m = idx >> 3, k4 = idx & 7;
+      const int idx = t + 256 * v, m = idx / KV, k4 = idx % KV;
       const int gm = m0 + m, gk = kt + 4 * k4;
       float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
       if (gm < p.M && gk < p.K) {
@@ -143,7 +147,7 @@ __global__ __launch_bounds__(256, 2) void gemm_nk_f32(NKParams p) {
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
-      const int idx = t + 256 * v, n = idx >> 3, k4 = idx & 7;
+      const int idx = t + 256 * v, n = idx / KV, k4 = idx % KV;
       rb[v] = *reinterpret_cast<const f32x4 *>(Bp + (int64_t)(n0 + n) * p.ldb + kt + 4 * k4);
     }
   };
@@ -151,12 +155,12 @@ __global__ __launch_bounds__(256, 2) void gemm_nk_f32(NKParams p) {
 #pragma unroll
     for (int v = 0; v < VA; ++v) {
       const int idx = t + 256 * v;
-      *reinterpret_cast<f32x4 *>(&As[b][(idx >> 3) * LK + 4 * (idx & 7)]) = ra[v];
+      *reinterpret_cast<f32x4 *>(&As[b][(idx / KV) * LK + 4 * (idx % KV)]) = ra[v];
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
       const int idx = t + 256 * v;
-      *reinterpret_cast<f32x4 *>(&Bs[b][(idx >> 3) * LK + 4 * (idx & 7)]) = rb[v];
+      *reinterpret_cast<f32x4 *>(&Bs[b][(idx / KV) * LK + 4 * (idx % KV)]) = rb[v];
     }
   };
 
@@ -178,14 +182,14 @@ __global__ __launch_bounds__(256, 2) void gemm_nk_f32(NKParams p) {
     // staging registers free of control flow)
     load(kt + BK < p.K ? kt + BK : kt);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < BK / 8; ++q) {
       f32x4 a[TM], b[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        a[i] = *reinterpret_cast<const f32x4 *>(&As[cur][(wm0 + i * 32 + r) * LK + 16 * h + 4 * q]);
+        a[i] = *reinterpret_cast<const f32x4 *>(&As[cur][(wm0 + i * 32 + r) * LK + (BK / 2) * h + 4 * q]);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        b[j] = *reinterpret_cast<const f32x4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + 16 * h + 4 * q]);
+        b[j] = *reinterpret_cast<const f32x4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + (BK / 2) * h + 4 * q]);
 #pragma unroll
       for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -203,8 +207,8 @@ __global__ __launch_bounds__(256, 2) void gemm_nk_f32(NKParams p) {
 // ------------------------------------------------------------------ bf16 ---
 
 template <int BM, int BN, int AK, int EK>
-__global__ __launch_bounds__(256, 2) void gemm_nk_bf16(NKParams p) {
-  constexpr int BK = 64, LK = BK + 8;                  // bf16 elements; 144-byte rows
+__global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
+  constexpr int BK = 32, LK = BK + 8, KV = BK / 8;     // bf16 elements; 80-byte rows
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
   constexpr int VA = BM * BK / 8 / 256, VB = BN * BK / 8 / 256;
   __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LK];
@@ -236,7 +240,7 @@ __global__ __launch_bounds__(256, 2) void gemm_nk_bf16(NKParams p) {
   auto load = [&](int kt) __attribute__((always_inline)) {
 #pragma unroll
     for (int v = 0; v < VA; ++v) {
-      const int idx = t + 256 * v, m = idx >> 3, k8 = idx & 7;
+      const int idx = t + 256 * v, m = idx / KV, k8 = idx % KV;
       const int gm = m0 + m, gk = kt + 8 * k8;
       uint4 x = make_uint4(0, 0, 0, 0);
       if (gm < p.M && gk < p.K) {
@@ -258,7 +262,7 @@ __global__ __launch_bounds__(256, 2) void gemm_nk_bf16(NKParams p) {
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
-      const int idx = t + 256 * v, n = idx >> 3, k8 = idx & 7;
+      const int idx = t + 256 * v, n = idx / KV, k8 = idx % KV;
       rb[v] = *reinterpret_cast<const u32x4 *>(Bp + (int64_t)(n0 + n) * p.ldb + kt + 8 * k8);
     }
   };
@@ -266,12 +270,12 @@ __global__ __launch_bounds__(256, 2) void gemm_nk_bf16(NKParams p) {
 #pragma unroll
     for (int v = 0; v < VA; ++v) {
       const int idx = t + 256 * v;
-      *reinterpret_cast<u32x4 *>(&As[b][(idx >> 3) * LK + 8 * (idx & 7)]) = ra[v];
+      *reinterpret_cast<u32x4 *>(&As[b][(idx / KV) * LK + 8 * (idx % KV)]) = ra[v];
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
       const int idx = t + 256 * v;
-      *reinterpret_cast<u32x4 *>(&Bs[b][(idx >> 3) * LK + 8 * (idx & 7)]) = rb[v];
+      *reinterpret_cast<u32x4 *>(&Bs[b][(idx / KV) * LK + 8 * (idx % KV)]) = rb[v];
     }
   };
 
@@ -293,14 +297,14 @@ __global__ __launch_bounds__(256, 2) void gemm_nk_bf16(NKParams p) {
     // staging registers free of control flow)
     load(kt + BK < p.K ? kt + BK : kt);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < BK / 16; ++q) {
       bf16x8 a[TM], b[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&As[cur][(wm0 + i * 32 + r) * LK + 32 * h + 8 * q]));
+        a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&As[cur][(wm0 + i * 32 + r) * LK + (BK / 2) * h + 8 * q]));
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + 32 * h + 8 * q]));
+        b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + (BK / 2) * h + 8 * q]));
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
