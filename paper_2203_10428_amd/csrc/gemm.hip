@@ -1,204 +1,147 @@
-// Dense update GEMMs of a GCN layer on CDNA4 matrix cores (Appendix A.1):
-//   forward       Z = A W, H = relu(Z)                  (NN, ReLU epilogue)
-//   feature grad  D = diag(1/d) ((J ∘ 1[H>0]) W^T)      (mask prologue, row-scale epilogue)
-//   weight grad   G = A^T (J ∘ 1[H>0])                  (split over the node dimension,
-//                                                         partials added in a fixed order)
-// fp32 operands use v_mfma_f32_32x32x2f32; the bf16 path rounds operands to
-// bf16 (round to nearest even) while staging them into LDS and uses
-// v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
+// Weight-gradient GEMM of a GCN layer (Appendix A.1; the G of Algorithm 1):
+//     G = A^T (J ∘ 1[H > 0])        [f_in x f_out], a sum over the inner rows
+// A [n, f_in], J and H [n, f_out] are node-major, so the reduction index k is
+// the node.  The node range is cut into fixed splits; each workgroup computes
+// one output tile over one split into a partial tile, and a second kernel adds
+// the partials in split order (deterministic, no atomics).
 //
-// Tiling: 256 threads = 4 wave64s arranged 2x2 over a BM x BN tile; each wave
-// owns (BM/2) x (BN/2) = several 32x32 MFMA tiles.  Tiles are staged through
-// LDS with a register prefetch of the next K-slab while the current one is
-// multiplied.  Block ids are remapped so that tiles sharing an A row-block run
-// on the same XCD (same L2).
+// Main loop for CDNA4: 256 threads (4 wave64s, 2 x 2) per 128 x BN tile; slabs
+// of nodes are staged through double-buffered LDS, one barrier per slab, with
+// the next slab's global loads in flight during the MFMAs.  Both operands are
+// transposed on the way into LDS (one row per feature, nodes contiguous) so a
+// lane's MFMA fragments over a slab are contiguous and load with 128-bit
+// reads: a thread loads a block of 4 nodes x 4 features (fp32; 8 features for
+// bf16 A) as 16-byte vectors and writes one node-contiguous vector per
+// feature.  Feature 4u + e (8u + e for bf16 A) is kept in LDS row e * U + u
+// (U = tile width / 4 or / 8), which puts the lanes of one LDS write on
+// distinct banks; the epilogue maps rows back to features.  The ReLU mask and
+// the bf16 rounding are applied after the MFMAs, just before the LDS write, so
+// the global loads stay in flight under the MFMAs.
+//   fp32: slabs of 16 nodes, v_mfma_f32_32x32x2f32; step e of group q uses
+//         node 8h + 4q + e for lane half h;
+//   bf16: slabs of 32 nodes, A already bf16 in memory, J ∘ mask rounded to
+//         bf16 (nearest even); v_mfma_f32_32x32x16_bf16, step q uses nodes
+//         16q + 8h .. 16q + 8h + 7 for lane half h.
+// The grid is one-dimensional over (split, tile) with the tiles of a split
+// adjacent and on the same XCD, so each split's rows of A, J and H come from
+// HBM about once and are re-read from that XCD's L2.
 #include "internal.h"
 
 namespace pgcn {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-enum AKind { A_MK_F32, A_MK_BF16, A_MK_MASK, A_KM_F32, A_KM_BF16 };
-enum BKind { B_KN_W, B_NK_W, B_KN_MASK };
-enum EKind { E_RELU, E_PLAIN, E_ROWSCALE, E_PARTIAL };
-
-struct GP {
-  int M, N, K;
-  int kchunk;
-  int tiles_n;
-  const float *A;
-  const uint16_t *A16;
+struct TNParams {
+  int M, N, K;            // M = f_in, N = f_out, K = node count
+  int kchunk;             // nodes per split (a multiple of the slab)
+  int tiles, tiles_n;
+  const float *A;         // fp32 [K, lda]
+  const uint16_t *A16;    // bf16 [K, lda]
   int64_t lda;
-  const float *Am;       // mask source of A (A_MK_MASK), may be null
-  int64_t ldam;
-  const float *B;
+  const float *J;         // [K, ldb]
   int64_t ldb;
-  const float *Bm;       // mask source of B (B_KN_MASK), may be null
-  int64_t ldbm;
-  float *C;
-  int64_t ldc;
-  const float *rowscale;
+  const float *H;         // mask source [K, ldh], or null (no ReLU)
+  int64_t ldh;
+  float *partials;        // [splits, M, N]
 };
 
-__device__ __forceinline__ uint16_t bf16_rne(float x) {
+__device__ __forceinline__ uint32_t tn_bf16(float x) {
   uint32_t b = __float_as_uint(x);
-  if ((b & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((b >> 16) | 0x40u);
+  if ((b & 0x7fffffffu) > 0x7f800000u) return (b >> 16) | 0x40u;
   b += 0x7fffu + ((b >> 16) & 1u);
-  return (uint16_t)(b >> 16);
+  return b >> 16;
 }
 
-__device__ __forceinline__ int xcd_remap(int b, int g) {
-  if (g % 8 != 0) return b;
-  return (b % 8) * (g / 8) + b / 8;
+// (split, tile) of this workgroup: logical index l = split * tiles + tile, with
+// workgroup b (dispatched to XCD b % 8) taking l = (b % 8) * (G / 8) + b / 8
+__device__ __forceinline__ void tn_coords(int tiles, int &split, int &tile) {
+  const int g = gridDim.x, b = blockIdx.x;
+  const int l = (g % 8 == 0) ? (b % 8) * (g / 8) + b / 8 : b;
+  split = l / tiles;
+  tile = l - split * tiles;
 }
 
-__device__ __forceinline__ float4 ld4_masked(const float *p, int valid) {
-  float4 v = *reinterpret_cast<const float4 *>(p);
-  if (valid < 4) {
-    if (valid < 4) v.w = 0.f;
-    if (valid < 3) v.z = 0.f;
-    if (valid < 2) v.y = 0.f;
-    if (valid < 1) v.x = 0.f;
-  }
-  return v;
-}
-
-__device__ __forceinline__ float4 apply_mask(float4 j, const float *h) {
-  float4 m = *reinterpret_cast<const float4 *>(h);
-  j.x = m.x > 0.f ? j.x : 0.f;
-  j.y = m.y > 0.f ? j.y : 0.f;
-  j.z = m.z > 0.f ? j.z : 0.f;
-  j.w = m.w > 0.f ? j.w : 0.f;
-  return j;
-}
-
-template <int EK>
-__device__ __forceinline__ void epilogue_store(const GP &p, int row, int col, float v) {
-  if (row >= p.M || col >= p.N) return;
-  if (EK == E_RELU) {
-    p.C[(int64_t)row * p.ldc + col] = v > 0.f ? v : 0.f;
-  } else if (EK == E_PLAIN) {
-    p.C[(int64_t)row * p.ldc + col] = v;
-  } else if (EK == E_ROWSCALE) {
-    p.C[(int64_t)row * p.ldc + col] = v * p.rowscale[row];
-  } else {
-    p.C[(int64_t)blockIdx.z * p.M * p.N + (int64_t)row * p.N + col] = v;
+// partial[split][fm][fn] for the accumulators of one wave; LDS row c holds
+// feature 4 * (c % UA) + c / UA of the A tile (VA features per vector)
+template <int TM, int TN, int UA, int VA, int UB>
+__device__ __forceinline__ void tn_store_partial(const TNParams &p, const f32x16 (&acc)[TM][TN], int split, int m0,
+                                                 int n0, int wm0, int wn0, int lane) {
+  float *out = p.partials + (int64_t)split * p.M * p.N;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int cn = wn0 + j * 32 + lane % 32;
+    const int fn = n0 + 4 * (cn % UB) + cn / UB;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int cm = wm0 + i * 32 + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
+        const int fm = m0 + VA * (cm % UA) + cm / UA;
+        if (fm < p.M && fn < p.N) out[(int64_t)fm * p.N + fn] = acc[i][j][r];
+      }
   }
 }
 
 // ------------------------------------------------------------------ fp32 ---
 
-template <int BM, int BN, int AK, int BKd, int EK>
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GP p) {
-  constexpr int BK = 16, PAD = 4;
+template <int BN>
+__global__ __launch_bounds__(256, 3) void gemm_tn_f32(TNParams p) {
+  constexpr int BM = 128, BK = 16, LK = BK + 4;
+  constexpr int UA = BM / 4, UB = BN / 4;
+  constexpr int NA = UA * (BK / 4), NB = UB * (BK / 4);
+  static_assert(NA + NB <= 256, "staging items exceed the workgroup");
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
-  constexpr int VA = BM * BK / 4 / 256;       // float4 per thread for A
-  constexpr int SB = BK * BN / 256;           // scalars per thread for W operands
-  constexpr int VB = BK * BN / 4 / 256;       // float4 per thread for masked B
-  static_assert(VA >= 1 && SB >= 1 && VB >= 1, "tile too small");
-  __shared__ float As[BK][BM + PAD];
-  __shared__ float Bs[BK][BN + PAD];
+  __shared__ __attribute__((aligned(16))) float As[2][BM * LK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LK];
 
   const int t = threadIdx.x, lane = t % 64, wave = t / 64;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  int split, tile;
+  tn_coords(p.tiles, split, tile);
   const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
-  const int kbeg = blockIdx.z * p.kchunk;
+  const int kbeg = split * p.kchunk;
   const int kend = min(p.K, kbeg + p.kchunk);
   const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
 
-  float4 ra[VA];
-  float rb[SB];
-  float4 rbv[VB];
+  // staging role (uniform per wave): A block for t < NA, J/H block after
+  const bool isA = t < NA;
+  const int item = isA ? t : t - NA;
+  const bool active = isA || item < NB;
+  const int U = isA ? UA : UB;
+  const int u = item % U, k4 = item / U;
+  const int f0 = (isA ? m0 : n0) + 4 * u;
+  const bool fok = active && f0 < (isA ? p.M : p.N);
+  const float *src = isA ? p.A : p.J;
+  const int64_t ld = isA ? p.lda : p.ldb;
+  const bool masked = !isA && p.H != nullptr;
 
+  f32x4 x[4], hm[4];
   auto load = [&](int kt) __attribute__((always_inline)) {
-    if (AK == A_MK_F32 || AK == A_MK_MASK) {
+    const int gk = kt + 4 * k4;
 #pragma unroll
-      for (int v = 0; v < VA; ++v) {
-        const int idx = t + 256 * v, m = idx / (BK / 4), k4 = idx % (BK / 4);
-        const int gm = m0 + m, gk = kt + 4 * k4;
-        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (gm < p.M && gk < kend) {
-          x = ld4_masked(p.A + (int64_t)gm * p.lda + gk, kend - gk);
-          if (AK == A_MK_MASK && p.Am) x = apply_mask(x, p.Am + (int64_t)gm * p.ldam + gk);
-        }
-        ra[v] = x;
-      }
-    } else {  // A_KM_F32: element (m, k) at A[k * lda + m]
-#pragma unroll
-      for (int v = 0; v < VA; ++v) {
-        const int idx = t + 256 * v, k = idx / (BM / 4), m4 = idx % (BM / 4);
-        const int gk = kt + k, gm = m0 + 4 * m4;
-        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (gk < kend && gm < p.M) x = ld4_masked(p.A + (int64_t)gk * p.lda + gm, p.M - gm);
-        ra[v] = x;
-      }
-    }
-    if (BKd == B_KN_W) {
-#pragma unroll
-      for (int s = 0; s < SB; ++s) {
-        const int idx = t + 256 * s, k = idx / BN, n = idx % BN;
-        const int gk = kt + k, gn = n0 + n;
-        rb[s] = (gk < kend && gn < p.N) ? p.B[(int64_t)gk * p.ldb + gn] : 0.f;
-      }
-    } else if (BKd == B_NK_W) {
-#pragma unroll
-      for (int s = 0; s < SB; ++s) {
-        const int idx = t + 256 * s, n = idx / BK, k = idx % BK;
-        const int gk = kt + k, gn = n0 + n;
-        rb[s] = (gk < kend && gn < p.N) ? p.B[(int64_t)gn * p.ldb + gk] : 0.f;
-      }
-    } else {  // B_KN_MASK
-#pragma unroll
-      for (int v = 0; v < VB; ++v) {
-        const int idx = t + 256 * v, k = idx / (BN / 4), n4 = idx % (BN / 4);
-        const int gk = kt + k, gn = n0 + 4 * n4;
-        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (gk < kend && gn < p.N) {
-          x = ld4_masked(p.B + (int64_t)gk * p.ldb + gn, p.N - gn);
-          if (p.Bm) x = apply_mask(x, p.Bm + (int64_t)gk * p.ldbm + gn);
-        }
-        rbv[v] = x;
-      }
+    for (int s = 0; s < 4; ++s) {
+      const bool ok = fok && gk + s < kend;
+      x[s] = ok ? *reinterpret_cast<const f32x4 *>(src + (int64_t)(gk + s) * ld + f0) : f32x4{0.f, 0.f, 0.f, 0.f};
+      if (masked)
+        hm[s] = ok ? *reinterpret_cast<const f32x4 *>(p.H + (int64_t)(gk + s) * p.ldh + f0)
+                   : f32x4{0.f, 0.f, 0.f, 0.f};
     }
   };
-
-  auto store = [&]() __attribute__((always_inline)) {
-    if (AK == A_MK_F32 || AK == A_MK_MASK) {
+  auto store = [&](int b) __attribute__((always_inline)) {
+    if (!active) return;
+    if (masked) {
 #pragma unroll
-      for (int v = 0; v < VA; ++v) {
-        const int idx = t + 256 * v, m = idx / (BK / 4), k4 = idx % (BK / 4);
-        As[4 * k4 + 0][m] = ra[v].x;
-        As[4 * k4 + 1][m] = ra[v].y;
-        As[4 * k4 + 2][m] = ra[v].z;
-        As[4 * k4 + 3][m] = ra[v].w;
-      }
-    } else {
+      for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int v = 0; v < VA; ++v) {
-        const int idx = t + 256 * v, k = idx / (BM / 4), m4 = idx % (BM / 4);
-        *reinterpret_cast<float4 *>(&As[k][4 * m4]) = ra[v];
-      }
+        for (int e = 0; e < 4; ++e) x[s][e] = hm[s][e] > 0.f ? x[s][e] : 0.f;
     }
-    if (BKd == B_KN_W) {
+    float *base = isA ? As[b] : Bs[b];
 #pragma unroll
-      for (int s = 0; s < SB; ++s) {
-        const int idx = t + 256 * s;
-        Bs[idx / BN][idx % BN] = rb[s];
-      }
-    } else if (BKd == B_NK_W) {
-#pragma unroll
-      for (int s = 0; s < SB; ++s) {
-        const int idx = t + 256 * s;
-        Bs[idx % BK][idx / BK] = rb[s];
-      }
-    } else {
-#pragma unroll
-      for (int v = 0; v < VB; ++v) {
-        const int idx = t + 256 * v, k = idx / (BN / 4), n4 = idx % (BN / 4);
-        *reinterpret_cast<float4 *>(&Bs[k][4 * n4]) = rbv[v];
-      }
-    }
+    for (int e = 0; e < 4; ++e)
+      *reinterpret_cast<f32x4 *>(&base[(e * U + u) * LK + 4 * k4]) = f32x4{x[0][e], x[1][e], x[2][e], x[3][e]};
   };
 
   f32x16 acc[TM][TN];
@@ -207,194 +150,115 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GP p) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
 
+  const int h = lane >> 5, r = lane & 31;
   if (kbeg < kend) {
     load(kbeg);
-    store();
+    store(0);
     __syncthreads();
-    for (int kt = kbeg; kt < kend; kt += BK) {
-      const bool more = kt + BK < kend;
-      if (more) load(kt + BK);
+    int it = 0;
+    for (int kt = kbeg; kt < kend; kt += BK, ++it) {
+      const int cur = it & 1;
+      load(kt + BK < kend ? kt + BK : kt);     // the last slab refills the idle buffer with itself
 #pragma unroll
-      for (int kk = 0; kk < BK; kk += 2) {
-        float a[TM], b[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) a[i] = As[kk + lane / 32][wm0 + i * 32 + lane % 32];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) b[j] = Bs[kk + lane / 32][wn0 + j * 32 + lane % 32];
+      for (int q = 0; q < BK / 8; ++q) {
+        f32x4 a[TM], b[TN];
 #pragma unroll
         for (int i = 0; i < TM; ++i)
+          a[i] = *reinterpret_cast<const f32x4 *>(&As[cur][(wm0 + i * 32 + r) * LK + 8 * h + 4 * q]);
 #pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TN; ++j)
+          b[j] = *reinterpret_cast<const f32x4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + 8 * h + 4 * q]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
       }
+      store(cur ^ 1);
       __syncthreads();
-      if (more) {
-        store();
-        __syncthreads();
-      }
     }
   }
-
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm0 + i * 32 + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
-        const int col = n0 + wn0 + j * 32 + lane % 32;
-        epilogue_store<EK>(p, row, col, acc[i][j][r]);
-      }
+  tn_store_partial<TM, TN, UA, 4, UB>(p, acc, split, m0, n0, wm0, wn0, lane);
 }
 
 // ------------------------------------------------------------------ bf16 ---
 
-template <int BM, int BN, int AK, int BKd, int EK>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GP p) {
-  constexpr int BK = 32, PAD = 8;
+template <int BN>
+__global__ __launch_bounds__(256, 3) void gemm_tn_bf16(TNParams p) {
+  constexpr int BM = 128, BK = 32, LK = BK + 8;       // bf16 elements; 80-byte rows
+  constexpr int UA = BM / 8, UB = BN / 4;
+  constexpr int NA = UA * (BK / 4), NB = UB * (BK / 4);
+  static_assert(NA <= 256 && NB <= 256 && (NB == 256 || NA + NB <= 256), "staging items exceed the workgroup");
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
-  constexpr int VA = BM * BK / 8 / 256;       // 8-element vectors per thread for A
-  constexpr int SB = BK * BN / 256;
-  constexpr int VB = BK * BN / 4 / 256;
-  static_assert(VA >= 1 && SB >= 1 && VB >= 1, "tile too small");
-  __shared__ __attribute__((aligned(16))) uint16_t As[BM][BK + PAD];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[BN][BK + PAD];
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LK];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LK];
 
   const int t = threadIdx.x, lane = t % 64, wave = t / 64;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  int split, tile;
+  tn_coords(p.tiles, split, tile);
   const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
-  const int kbeg = blockIdx.z * p.kchunk;
+  const int kbeg = split * p.kchunk;
   const int kend = min(p.K, kbeg + p.kchunk);
   const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
 
-  uint4 ra[VA];
-  float rb[SB];
-  float4 rbv[VB];
+  // A blocks (4 nodes x 8 features) on threads [0, NA); J/H blocks (4 nodes x
+  // 4 features) on every thread when there are 256 of them, else after the A threads
+  const bool hasA = t < NA;
+  const int ua = t % UA, ka = t / UA;
+  const bool aok = hasA && m0 + 8 * ua < p.M;
+  const int ib = NB == 256 ? t : t - NA;
+  const bool hasB = ib >= 0 && ib < NB;
+  const int ub = ib % UB, kb = ib / UB;
+  const bool bok = hasB && n0 + 4 * ub < p.N;
+  const bool masked = p.H != nullptr;
 
-  auto pack8 = [](float4 a, float4 b) {
-    uint4 r;
-    r.x = (uint32_t)bf16_rne(a.x) | ((uint32_t)bf16_rne(a.y) << 16);
-    r.y = (uint32_t)bf16_rne(a.z) | ((uint32_t)bf16_rne(a.w) << 16);
-    r.z = (uint32_t)bf16_rne(b.x) | ((uint32_t)bf16_rne(b.y) << 16);
-    r.w = (uint32_t)bf16_rne(b.z) | ((uint32_t)bf16_rne(b.w) << 16);
-    return r;
-  };
-  auto mask16 = [](uint4 v, int valid) {   // zero bf16 elements >= valid
-    uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (e >= valid) w[e / 2] &= (e % 2) ? 0x0000ffffu : 0xffff0000u;
-    return make_uint4(w[0], w[1], w[2], w[3]);
-  };
-
+  u32x4 xa[4];
+  f32x4 xb[4], hm[4];
   auto load = [&](int kt) __attribute__((always_inline)) {
-    if (AK == A_MK_BF16) {
+    if (hasA) {
+      const int gk = kt + 4 * ka;
 #pragma unroll
-      for (int v = 0; v < VA; ++v) {
-        const int idx = t + 256 * v, m = idx / (BK / 8), k8 = idx % (BK / 8);
-        const int gm = m0 + m, gk = kt + 8 * k8;
-        uint4 x = make_uint4(0, 0, 0, 0);
-        if (gm < p.M && gk < kend) {
-          x = *reinterpret_cast<const uint4 *>(p.A16 + (int64_t)gm * p.lda + gk);
-          if (kend - gk < 8) x = mask16(x, kend - gk);
-        }
-        ra[v] = x;
-      }
-    } else if (AK == A_MK_MASK || AK == A_MK_F32) {
-#pragma unroll
-      for (int v = 0; v < VA; ++v) {
-        const int idx = t + 256 * v, m = idx / (BK / 8), k8 = idx % (BK / 8);
-        const int gm = m0 + m, gk = kt + 8 * k8;
-        float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
-        if (gm < p.M && gk < kend) {
-          const float *row = p.A + (int64_t)gm * p.lda + gk;
-          x0 = ld4_masked(row, kend - gk);
-          if (AK == A_MK_MASK && p.Am) x0 = apply_mask(x0, p.Am + (int64_t)gm * p.ldam + gk);
-          if (gk + 4 < kend) {
-            x1 = ld4_masked(row + 4, kend - gk - 4);
-            if (AK == A_MK_MASK && p.Am) x1 = apply_mask(x1, p.Am + (int64_t)gm * p.ldam + gk + 4);
-          }
-        }
-        ra[v] = pack8(x0, x1);
-      }
-    } else {  // A_KM_BF16: element (m, k) at A16[k * lda + m]
-#pragma unroll
-      for (int v = 0; v < VA; ++v) {
-        const int idx = t + 256 * v, k = idx / (BM / 8), m8 = idx % (BM / 8);
-        const int gk = kt + k, gm = m0 + 8 * m8;
-        uint4 x = make_uint4(0, 0, 0, 0);
-        if (gk < kend && gm < p.M) {
-          x = *reinterpret_cast<const uint4 *>(p.A16 + (int64_t)gk * p.lda + gm);
-          if (p.M - gm < 8) x = mask16(x, p.M - gm);
-        }
-        ra[v] = x;
-      }
+      for (int s = 0; s < 4; ++s)
+        xa[s] = (aok && gk + s < kend)
+                    ? *reinterpret_cast<const u32x4 *>(p.A16 + (int64_t)(gk + s) * p.lda + m0 + 8 * ua)
+                    : u32x4{0u, 0u, 0u, 0u};
     }
-    if (BKd == B_KN_W) {
+    if (hasB) {
+      const int gk = kt + 4 * kb;
 #pragma unroll
-      for (int s = 0; s < SB; ++s) {
-        const int idx = t + 256 * s, k = idx / BN, n = idx % BN;
-        const int gk = kt + k, gn = n0 + n;
-        rb[s] = (gk < kend && gn < p.N) ? p.B[(int64_t)gk * p.ldb + gn] : 0.f;
-      }
-    } else if (BKd == B_NK_W) {
-#pragma unroll
-      for (int s = 0; s < SB; ++s) {
-        const int idx = t + 256 * s, n = idx / BK, k = idx % BK;
-        const int gk = kt + k, gn = n0 + n;
-        rb[s] = (gk < kend && gn < p.N) ? p.B[(int64_t)gn * p.ldb + gk] : 0.f;
-      }
-    } else {
-#pragma unroll
-      for (int v = 0; v < VB; ++v) {
-        const int idx = t + 256 * v, k = idx / (BN / 4), n4 = idx % (BN / 4);
-        const int gk = kt + k, gn = n0 + 4 * n4;
-        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (gk < kend && gn < p.N) {
-          x = ld4_masked(p.B + (int64_t)gk * p.ldb + gn, p.N - gn);
-          if (p.Bm) x = apply_mask(x, p.Bm + (int64_t)gk * p.ldbm + gn);
-        }
-        rbv[v] = x;
+      for (int s = 0; s < 4; ++s) {
+        const bool ok = bok && gk + s < kend;
+        xb[s] = ok ? *reinterpret_cast<const f32x4 *>(p.J + (int64_t)(gk + s) * p.ldb + n0 + 4 * ub)
+                   : f32x4{0.f, 0.f, 0.f, 0.f};
+        if (masked)
+          hm[s] = ok ? *reinterpret_cast<const f32x4 *>(p.H + (int64_t)(gk + s) * p.ldh + n0 + 4 * ub)
+                     : f32x4{0.f, 0.f, 0.f, 0.f};
       }
     }
   };
-
-  auto store = [&]() __attribute__((always_inline)) {
-    if (AK == A_KM_BF16) {
+  auto store = [&](int b) __attribute__((always_inline)) {
+    if (hasA) {
 #pragma unroll
-      for (int v = 0; v < VA; ++v) {
-        const int idx = t + 256 * v, k = idx / (BM / 8), m8 = idx % (BM / 8);
-        const uint32_t w[4] = {ra[v].x, ra[v].y, ra[v].z, ra[v].w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) As[8 * m8 + e][k] = (uint16_t)(w[e / 2] >> (16 * (e % 2)));
-      }
-    } else {
-#pragma unroll
-      for (int v = 0; v < VA; ++v) {
-        const int idx = t + 256 * v, m = idx / (BK / 8), k8 = idx % (BK / 8);
-        *reinterpret_cast<uint4 *>(&As[m][8 * k8]) = ra[v];
+      for (int w = 0; w < 4; ++w) {            // features 2w (low halves) and 2w + 1 (high halves)
+        const u32x2 lo{(xa[0][w] & 0xffffu) | (xa[1][w] << 16), (xa[2][w] & 0xffffu) | (xa[3][w] << 16)};
+        const u32x2 hi{(xa[0][w] >> 16) | (xa[1][w] & 0xffff0000u), (xa[2][w] >> 16) | (xa[3][w] & 0xffff0000u)};
+        *reinterpret_cast<u32x2 *>(&As[b][((2 * w) * UA + ua) * LK + 4 * ka]) = lo;
+        *reinterpret_cast<u32x2 *>(&As[b][((2 * w + 1) * UA + ua) * LK + 4 * ka]) = hi;
       }
     }
-    if (BKd == B_KN_W) {
+    if (hasB) {
+      if (masked) {
 #pragma unroll
-      for (int s = 0; s < SB; ++s) {
-        const int idx = t + 256 * s;
-        Bs[idx % BN][idx / BN] = bf16_rne(rb[s]);
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) xb[s][e] = hm[s][e] > 0.f ? xb[s][e] : 0.f;
       }
-    } else if (BKd == B_NK_W) {
 #pragma unroll
-      for (int s = 0; s < SB; ++s) {
-        const int idx = t + 256 * s;
-        Bs[idx / BK][idx % BK] = bf16_rne(rb[s]);
-      }
-    } else {
-#pragma unroll
-      for (int v = 0; v < VB; ++v) {
-        const int idx = t + 256 * v, k = idx / (BN / 4), n4 = idx % (BN / 4);
-        Bs[4 * n4 + 0][k] = bf16_rne(rbv[v].x);
-        Bs[4 * n4 + 1][k] = bf16_rne(rbv[v].y);
-        Bs[4 * n4 + 2][k] = bf16_rne(rbv[v].z);
-        Bs[4 * n4 + 3][k] = bf16_rne(rbv[v].w);
+      for (int e = 0; e < 4; ++e) {
+        const u32x2 v{tn_bf16(xb[0][e]) | (tn_bf16(xb[1][e]) << 16), tn_bf16(xb[2][e]) | (tn_bf16(xb[3][e]) << 16)};
+        *reinterpret_cast<u32x2 *>(&Bs[b][(e * UB + ub) * LK + 4 * kb]) = v;
       }
     }
   };
@@ -405,46 +269,37 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GP p) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
 
+  const int h = lane >> 5, r = lane & 31;
   if (kbeg < kend) {
     load(kbeg);
-    store();
+    store(0);
     __syncthreads();
-    for (int kt = kbeg; kt < kend; kt += BK) {
-      const bool more = kt + BK < kend;
-      if (more) load(kt + BK);
+    int it = 0;
+    for (int kt = kbeg; kt < kend; kt += BK, ++it) {
+      const int cur = it & 1;
+      load(kt + BK < kend ? kt + BK : kt);
 #pragma unroll
-      for (int ks = 0; ks < BK; ks += 16) {
+      for (int q = 0; q < BK / 16; ++q) {
         bf16x8 a[TM], b[TN];
 #pragma unroll
         for (int i = 0; i < TM; ++i)
-          a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&As[wm0 + i * 32 + lane % 32][ks + 8 * (lane / 32)]));
+          a[i] = __builtin_bit_cast(bf16x8,
+                                    *reinterpret_cast<const u32x4 *>(&As[cur][(wm0 + i * 32 + r) * LK + 16 * q + 8 * h]));
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&Bs[wn0 + j * 32 + lane % 32][ks + 8 * (lane / 32)]));
+          b[j] = __builtin_bit_cast(bf16x8,
+                                    *reinterpret_cast<const u32x4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + 16 * q + 8 * h]));
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
       }
+      store(cur ^ 1);
       __syncthreads();
-      if (more) {
-        store();
-        __syncthreads();
-      }
     }
   }
-
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm0 + i * 32 + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
-        const int col = n0 + wn0 + j * 32 + lane % 32;
-        epilogue_store<EK>(p, row, col, acc[i][j][r]);
-      }
+  tn_store_partial<TM, TN, UA, 8, UB>(p, acc, split, m0, n0, wm0, wn0, lane);
 }
 
 // Fixed-order sum of split partials.  A block owns 64 consecutive outputs and
@@ -466,96 +321,78 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *ws, int
 
 // ---------------------------------------------------------------- launch ---
 
-static int splitk_count(int M, int N, int K, int BM, int BN, int BK) {
-  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  int s = (1024 + tiles - 1) / tiles;
+static int tn_tiles(int M, int N) {
+  const int BN = N <= 64 ? 64 : 128;
+  return ((M + 127) / 128) * ((N + BN - 1) / BN);
+}
+
+// Splits over the nodes: tiles x splits about one round of resident
+// workgroups (three per CU on 256 CUs), at least 256 nodes per split, and
+// tiles x splits a multiple of 8 when possible (XCD mapping).
+static int splitk_count(int M, int N, int K) {
+  const int tiles = tn_tiles(M, N);
+  int s = 768 / tiles;
   const int max_s = (K + 255) / 256;
   if (s > max_s) s = max_s;
   if (s < 1) s = 1;
-  (void)BK;
+  int r = s;
+  while (r > 1 && (tiles * r) % 8 != 0) --r;
+  if ((tiles * r) % 8 == 0 && 2 * r >= s) s = r;
   return s;
 }
 
 size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K) {
   if (kind != Gemm::TN_MASK_SPLITK) return 0;
-  const int BN = N <= 64 ? 64 : 128;
-  const int s = splitk_count(M, N, K, 128, BN, 16);
-  return (size_t)s * (size_t)M * (size_t)N * sizeof(float);
+  return (size_t)splitk_count(M, N, K) * (size_t)M * (size_t)N * sizeof(float);
 }
 
-template <int BN, int AK, int BKd, int EK>
-static int run(const GP &p0, int bf16, int splits, hipStream_t s) {
-  TraceScope ts(EK == E_PARTIAL ? PGCN_TK_GEMM_WGRAD : (EK == E_ROWSCALE ? PGCN_TK_GEMM_DGRAD : PGCN_TK_GEMM_FWD), s);
+template <int BN>
+static void tn_launch(TNParams p, bool bf16, int splits, hipStream_t s) {
   constexpr int BM = 128;
-  GP p = p0;
-  const int tm = (p.M + BM - 1) / BM, tn = (p.N + BN - 1) / BN;
-  p.tiles_n = tn;
-  const int BK = bf16 ? 32 : 16;
+  p.tiles_n = (p.N + BN - 1) / BN;
+  p.tiles = ((p.M + BM - 1) / BM) * p.tiles_n;
+  const int slab = bf16 ? 32 : 16;
   int kchunk = (p.K + splits - 1) / splits;
-  kchunk = (kchunk + BK - 1) / BK * BK;
-  if (kchunk == 0) kchunk = BK;
+  kchunk = (kchunk + slab - 1) / slab * slab;
+  if (kchunk == 0) kchunk = slab;
   p.kchunk = kchunk;
-  dim3 grid((unsigned)(tm * tn), 1, (unsigned)splits);
-  if (bf16) {
-    constexpr int AKb = AK == A_MK_F32 ? A_MK_BF16 : (AK == A_KM_F32 ? A_KM_BF16 : AK);
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, AKb, BKd, EK>), grid, dim3(256), 0, s, p);
-  } else {
-    hipLaunchKernelGGL((gemm_f32_kernel<BM, BN, AK, BKd, EK>), grid, dim3(256), 0, s, p);
-  }
-  PGCN_HIP(hipGetLastError());
-  return PGCN_OK;
-}
-
-template <int AK, int BKd, int EK>
-static int run_bn(const GP &p, int bf16, int splits, hipStream_t s) {
-  if (p.N <= 64) return run<64, AK, BKd, EK>(p, bf16, splits, s);
-  return run<128, AK, BKd, EK>(p, bf16, splits, s);
+  const dim3 grid((unsigned)(p.tiles * splits));
+  if (bf16) hipLaunchKernelGGL((gemm_tn_bf16<BN>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((gemm_tn_f32<BN>), grid, dim3(256), 0, s, p);
 }
 
 int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
+  if (kind != Gemm::TN_MASK_SPLITK) return set_error(PGCN_EINVAL, "launch_gemm: only the weight-gradient GEMM");
   if (g.M <= 0 || g.N <= 0) return PGCN_OK;
-  GP p{};
+  const int splits = splitk_count(g.M, g.N, g.K);
+  const size_t need = (size_t)splits * (size_t)g.M * (size_t)g.N * sizeof(float);
+  if (!g.workspace || g.workspace_bytes < need)
+    return set_error(PGCN_EWORKSPACE, "weight-gradient GEMM: workspace too small");
+  TNParams p{};
   p.M = g.M;
   p.N = g.N;
   p.K = g.K;
   p.A = g.A;
   p.A16 = g.A16;
   p.lda = g.lda;
-  p.B = g.B;
+  p.J = g.B;
   p.ldb = g.ldb;
-  p.C = g.C;
-  p.ldc = g.ldc;
-  p.rowscale = g.rowscale;
-  const int bf16 = g.dtype == PGCN_BF16;
-  switch (kind) {
-    case Gemm::NN_RELU:
-      return run_bn<A_MK_F32, B_KN_W, E_RELU>(p, bf16, 1, s);
-    case Gemm::NN_PLAIN:
-      return run_bn<A_MK_F32, B_KN_W, E_PLAIN>(p, bf16, 1, s);
-    case Gemm::MASK_NT_ROWSCALE:
-      p.Am = g.Hmask;
-      p.ldam = g.ldm;
-      return run_bn<A_MK_MASK, B_NK_W, E_ROWSCALE>(p, bf16, 1, s);
-    case Gemm::TN_MASK_SPLITK: {
-      p.Bm = g.Hmask;
-      p.ldbm = g.ldm;
-      const int BN = g.N <= 64 ? 64 : 128;
-      const int splits = splitk_count(g.M, g.N, g.K, 128, BN, 16);
-      const size_t need = (size_t)splits * (size_t)g.M * (size_t)g.N * sizeof(float);
-      if (!g.workspace || g.workspace_bytes < need)
-        return set_error(PGCN_EWORKSPACE, "weight-gradient GEMM: workspace too small");
-      p.C = g.workspace;
-      int rc = run_bn<A_KM_F32, B_KN_MASK, E_PARTIAL>(p, bf16, splits, s);
-      if (rc) return rc;
-      const int64_t mn = (int64_t)g.M * g.N;
-      TraceScope ts(PGCN_TK_WGRAD_REDUCE, s);
-      hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((mn + 63) / 64)), dim3(256), 0, s,
-                         (const float *)g.workspace, splits, mn, g.C);
-      PGCN_HIP(hipGetLastError());
-      return PGCN_OK;
-    }
+  p.H = g.Hmask;
+  p.ldh = g.ldm;
+  p.partials = g.workspace;
+  const bool bf16 = g.dtype == PGCN_BF16;
+  {
+    TraceScope ts(PGCN_TK_GEMM_WGRAD, s);
+    if (g.N <= 64) tn_launch<64>(p, bf16, splits, s);
+    else tn_launch<128>(p, bf16, splits, s);
+    PGCN_HIP(hipGetLastError());
   }
-  return set_error(PGCN_EINVAL, "unknown GEMM kind");
+  const int64_t mn = (int64_t)g.M * g.N;
+  TraceScope ts(PGCN_TK_WGRAD_REDUCE, s);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((mn + 63) / 64)), dim3(256), 0, s,
+                     (const float *)g.workspace, splits, mn, g.C);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
 }
 
 }  // namespace pgcn

@@ -62,26 +62,6 @@ __device__ __forceinline__ int nk_xcd_remap(int b, int g) {
   return (b % 8) * (g / 8) + b / 8;
 }
 
-__device__ __forceinline__ float4 nk_ld4(const float *p, int valid) {
-  float4 v = *reinterpret_cast<const float4 *>(p);
-  if (valid < 4) {
-    v.w = 0.f;
-    if (valid < 3) v.z = 0.f;
-    if (valid < 2) v.y = 0.f;
-    if (valid < 1) v.x = 0.f;
-  }
-  return v;
-}
-
-__device__ __forceinline__ float4 nk_mask(float4 j, const float *h) {
-  const float4 m = *reinterpret_cast<const float4 *>(h);
-  j.x = m.x > 0.f ? j.x : 0.f;
-  j.y = m.y > 0.f ? j.y : 0.f;
-  j.z = m.z > 0.f ? j.z : 0.f;
-  j.w = m.w > 0.f ? j.w : 0.f;
-  return j;
-}
-
 template <int EK>
 __device__ __forceinline__ void nk_store(const NKParams &p, int row, int col, float v) {
   if (row >= p.M || col >= p.N) return;
@@ -132,18 +112,21 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
   const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
   const float *Bp = reinterpret_cast<const float *>(p.B);
 
-  f32x4 ra[VA], rb[VB];
+  // raw loads only (whole vectors, predicated); the row-tail zeroing and the
+  // ReLU mask are applied in store(), after the MFMAs that hide the loads
+  f32x4 ra[VA], rh[VA], rb[VB];
+  int kl = 0;                                          // k of the staged slab
   auto load = [&](int kt) __attribute__((always_inline)) {
+    kl = kt;
 #pragma unroll
     for (int v = 0; v < VA; ++v) {
       const int idx = t + 256 * v, m = idx / KV, k4 = idx % KV;
       const int gm = m0 + m, gk = kt + 4 * k4;
-      float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (gm < p.M && gk < p.K) {
-        x = nk_ld4(p.A + (int64_t)gm * p.lda + gk, p.K - gk);
-        if (AK == NK_A_MASK && p.Am) x = nk_mask(x, p.Am + (int64_t)gm * p.ldam + gk);
-      }
-      ra[v] = f32x4{x.x, x.y, x.z, x.w};
+      const bool ok = gm < p.M && gk < p.K;
+      ra[v] = ok ? *reinterpret_cast<const f32x4 *>(p.A + (int64_t)gm * p.lda + gk) : f32x4{0.f, 0.f, 0.f, 0.f};
+      if (AK == NK_A_MASK)
+        rh[v] = (ok && p.Am) ? *reinterpret_cast<const f32x4 *>(p.Am + (int64_t)gm * p.ldam + gk)
+                             : f32x4{1.f, 1.f, 1.f, 1.f};
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
@@ -155,7 +138,14 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
 #pragma unroll
     for (int v = 0; v < VA; ++v) {
       const int idx = t + 256 * v;
-      *reinterpret_cast<f32x4 *>(&As[b][(idx / KV) * LK + 4 * (idx % KV)]) = ra[v];
+      f32x4 x = ra[v];
+      const int valid = p.K - (kl + 4 * (idx % KV));   // zero the k >= K tail of the row
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (e >= valid) x[e] = 0.f;
+        if (AK == NK_A_MASK) x[e] = rh[v][e] > 0.f ? x[e] : 0.f;
+      }
+      *reinterpret_cast<f32x4 *>(&As[b][(idx / KV) * LK + 4 * (idx % KV)]) = x;
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
@@ -220,45 +210,33 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
   const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
   const uint16_t *Bp = reinterpret_cast<const uint16_t *>(p.B);
 
-  auto pack8 = [](float4 x, float4 y) {
-    uint4 o;
-    o.x = (uint32_t)nk_bf16(x.x) | ((uint32_t)nk_bf16(x.y) << 16);
-    o.y = (uint32_t)nk_bf16(x.z) | ((uint32_t)nk_bf16(x.w) << 16);
-    o.z = (uint32_t)nk_bf16(y.x) | ((uint32_t)nk_bf16(y.y) << 16);
-    o.w = (uint32_t)nk_bf16(y.z) | ((uint32_t)nk_bf16(y.w) << 16);
-    return o;
-  };
-  auto zero_tail = [](uint4 v, int valid) {       // zero bf16 elements >= valid
-    uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (e >= valid) w[e / 2] &= (e % 2) ? 0x0000ffffu : 0xffff0000u;
-    return make_uint4(w[0], w[1], w[2], w[3]);
-  };
-
+  // raw loads only (whole vectors, predicated); the row-tail zeroing, the ReLU
+  // mask and the bf16 rounding are applied in store(), after the MFMAs
+  constexpr bool SRC32 = AK != NK_A_BF16;              // fp32 source rounded to bf16 in store()
   u32x4 ra[VA], rb[VB];
+  f32x4 rx[SRC32 ? 2 * VA : 1], rh[AK == NK_A_MASK ? 2 * VA : 1];
+  int kl = 0;                                          // k of the staged slab
   auto load = [&](int kt) __attribute__((always_inline)) {
+    kl = kt;
 #pragma unroll
     for (int v = 0; v < VA; ++v) {
       const int idx = t + 256 * v, m = idx / KV, k8 = idx % KV;
       const int gm = m0 + m, gk = kt + 8 * k8;
-      uint4 x = make_uint4(0, 0, 0, 0);
-      if (gm < p.M && gk < p.K) {
-        if (AK == NK_A_BF16) {
-          x = *reinterpret_cast<const uint4 *>(p.A16 + (int64_t)gm * p.lda + gk);
-          if (p.K - gk < 8) x = zero_tail(x, p.K - gk);
-        } else {
-          const float *row = p.A + (int64_t)gm * p.lda + gk;
-          float4 x0 = nk_ld4(row, p.K - gk), x1 = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (AK == NK_A_MASK && p.Am) x0 = nk_mask(x0, p.Am + (int64_t)gm * p.ldam + gk);
-          if (gk + 4 < p.K) {
-            x1 = nk_ld4(row + 4, p.K - gk - 4);
-            if (AK == NK_A_MASK && p.Am) x1 = nk_mask(x1, p.Am + (int64_t)gm * p.ldam + gk + 4);
-          }
-          x = pack8(x0, x1);
+      const bool ok = gm < p.M && gk < p.K;
+      if (!SRC32) {
+        ra[v] = ok ? *reinterpret_cast<const u32x4 *>(p.A16 + (int64_t)gm * p.lda + gk) : u32x4{0u, 0u, 0u, 0u};
+      } else {
+        // the second half-vector exists when gk + 4 < K (ld is a multiple of 4)
+        const float *row = p.A + (int64_t)gm * p.lda + gk;
+        const bool ok1 = ok && gk + 4 < p.K;
+        rx[2 * v] = ok ? *reinterpret_cast<const f32x4 *>(row) : f32x4{0.f, 0.f, 0.f, 0.f};
+        rx[2 * v + 1] = ok1 ? *reinterpret_cast<const f32x4 *>(row + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        if (AK == NK_A_MASK) {
+          const float *hrow = p.Am + (int64_t)gm * p.ldam + gk;
+          rh[2 * v] = (ok && p.Am) ? *reinterpret_cast<const f32x4 *>(hrow) : f32x4{1.f, 1.f, 1.f, 1.f};
+          rh[2 * v + 1] = (ok1 && p.Am) ? *reinterpret_cast<const f32x4 *>(hrow + 4) : f32x4{1.f, 1.f, 1.f, 1.f};
         }
       }
-      ra[v] = u32x4{x.x, x.y, x.z, x.w};
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
@@ -270,7 +248,26 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
 #pragma unroll
     for (int v = 0; v < VA; ++v) {
       const int idx = t + 256 * v;
-      *reinterpret_cast<u32x4 *>(&As[b][(idx / KV) * LK + 8 * (idx % KV)]) = ra[v];
+      const int valid = p.K - (kl + 8 * (idx % KV));   // zero the k >= K tail of the row
+      u32x4 o;
+      if (!SRC32) {
+        o = ra[v];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e >= valid) o[e / 2] &= (e % 2) ? 0x0000ffffu : 0xffff0000u;
+      } else {
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          x[e] = rx[2 * v + e / 4][e % 4];
+          if (AK == NK_A_MASK) x[e] = rh[2 * v + e / 4][e % 4] > 0.f ? x[e] : 0.f;
+          if (e >= valid) x[e] = 0.f;
+        }
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          o[w] = (uint32_t)nk_bf16(x[2 * w]) | ((uint32_t)nk_bf16(x[2 * w + 1]) << 16);
+      }
+      *reinterpret_cast<u32x4 *>(&As[b][(idx / KV) * LK + 8 * (idx % KV)]) = o;
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
