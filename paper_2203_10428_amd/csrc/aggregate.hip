@@ -10,10 +10,14 @@
 // gradient).
 //
 // Mapping for CDNA4 (8 XCDs, 4 MB L2 each, wave64):
-//  * Rows wider than 1 KB are cut into S slices (S in {1,2,4,8}) of SL float4
-//    (SL a multiple of 4: 64-byte aligned, at most 1 KB).  Workgroup b works
-//    on slice b % S; the hardware deals workgroups to the 8 XCDs round robin,
-//    so every XCD only ever touches one slice of every feature row.
+//  * A wave's vector load costs the per-CU texture data path the same time
+//    whether or not all 64 lanes are active (measured: ~32 cycles per
+//    64 x 16-byte load, about 20 TB/s for the chip on cache-resident rows),
+//    so lanes are kept full: the float4 columns of a row are cut into full
+//    slices of 64 float4 (S <= 8 per launch) plus one remainder launch of
+//    width SL < 64 in which G = 64 / SL lane groups share a wave.  Workgroup
+//    b works on slice b % S; the hardware deals workgroups to the 8 XCDs
+//    round robin, so an XCD only ever touches one slice of every feature row.
 //  * The columns of the sparse matrix (the gathered rows) are cut into C
 //    chunks of about 11,000 rows, one launch per chunk, so that the rows one
 //    launch gathers from stay in the caches while they are reused (cache
@@ -25,12 +29,13 @@
 //    of them per group in flight (masked at the row's end), then the groups
 //    are added in group order.  Short runs (fewer than G*U non-zeros): each
 //    lane group owns its own item, U non-zeros in flight; items are sorted by
-//    length, so the groups of a wave finish together.
+//    length, so the groups of a wave finish together.  With several lane
+//    groups the column indices are fetched by one load per wave (one index
+//    per lane) and handed out with lane shuffles, which keeps index fetches
+//    off the texture data path.
 //  * Runs longer than a fixed segment are split; segments write partial sums
 //    that a second pass adds in segment order.  No floating-point atomics:
 //    results are bitwise reproducible.
-#include <cstdlib>
-
 #include "internal.h"
 
 namespace pgcn {
@@ -103,12 +108,15 @@ __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, fl
 template <int SL, int U>
 __global__ __launch_bounds__(256) void agg_multi_kernel(AggParams p) {
   constexpr int G = 64 / SL;
+  constexpr int NL = (U + SL - 1) / SL;                 // index loads per step (G > 1)
   const int S = p.slices;
   const int slice = blockIdx.x % S;
-  const int lane = threadIdx.x % 64, g = lane / SL;
+  const int lane = threadIdx.x % 64, g = lane / SL, j = lane % SL;
   const int64_t item = ((int64_t)(blockIdx.x / S) * 4 + threadIdx.x / 64) * G + g;
-  const int cs = slice * SL + lane % SL;
-  if (g >= G || item >= p.n_items || cs >= p.c4_cnt) return;
+  // a whole lane group leaves together (it is its own shuffle source)
+  if (g >= G || item >= p.n_items) return;
+  const int cs = slice * SL + j;
+  const bool act = cs < p.c4_cnt;
   const int cbase = 4 * (p.c4_off + cs);
   const WorkItem it = p.items[item];
   const int32_t *cols = p.col + it.begin;
@@ -116,8 +124,19 @@ __global__ __launch_bounds__(256) void agg_multi_kernel(AggParams p) {
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int k = 0; k < len; k += U) {
     int32_t c[U];
+    if (G == 1) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) c[u] = k + u < len ? __builtin_nontemporal_load(cols + k + u) : -1;
+      for (int u = 0; u < U; ++u) c[u] = k + u < len ? __builtin_nontemporal_load(cols + k + u) : -1;
+    } else {
+      int32_t mine[NL];
+#pragma unroll
+      for (int t = 0; t < NL; ++t) {
+        const int q = k + t * SL + j;
+        mine[t] = (t * SL + j < U && q < len) ? __builtin_nontemporal_load(cols + q) : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) c[u] = __shfl(mine[u / SL], g * SL + u % SL);
+    }
     float4 x[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -126,11 +145,12 @@ __global__ __launch_bounds__(256) void agg_multi_kernel(AggParams p) {
         if (c[u] < p.in_split) src = p.in_lo + (int64_t)c[u] * p.ld_in;
         else if (p.in_hi) src = p.in_hi + (int64_t)(c[u] - p.in_split) * p.ld_in;
       }
-      x[u] = src ? *reinterpret_cast<const float4 *>(src + cbase) : make_float4(0.f, 0.f, 0.f, 0.f);
+      x[u] = (act && src) ? *reinterpret_cast<const float4 *>(src + cbase) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) acc = add4(acc, x[u]);
   }
+  if (!act) return;
   if (it.dst >= 0) finish(p, it.dst, p.c4_off + cs, acc);
   else *reinterpret_cast<float4 *>(p.partials + (int64_t)(-it.dst - 1) * p.ld_part + cbase) = acc;
 }
@@ -155,10 +175,19 @@ __global__ __launch_bounds__(256) void agg_kernel(AggParams p) {
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int k = 0; k < len; k += G * U) {
     int32_t c[U];
+    if (G == 1) {                                      // uniform: scalar loads
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int q = k + u * G + gg;
-      c[u] = q < len ? __builtin_nontemporal_load(cols + q) : -1;
+      for (int u = 0; u < U; ++u) c[u] = k + u < len ? __builtin_nontemporal_load(cols + k + u) : -1;
+    } else {                                           // one index per lane, then shuffles
+      constexpr int NB = (G * U + 63) / 64;            // G divides 64 whenever G * U > 64
+      int32_t mine[NB];
+#pragma unroll
+      for (int t = 0; t < NB; ++t) {
+        const int q = 64 * t + lane;
+        mine[t] = (q < G * U && k + q < len) ? __builtin_nontemporal_load(cols + k + q) : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) c[u] = __shfl(mine[(u * G) / 64], (u * G) % 64 + gg);
     }
     float4 x[U];
 #pragma unroll
@@ -243,29 +272,34 @@ static int64_t first_short(const Plan &plan, int64_t b, int64_t e, int threshold
   return lo;
 }
 
-// Slice count (power of two, at most 8) and slice width (float4, multiple of 4)
-// for a launch of c4 float4 columns: slices of at most ~320 bytes, one slice
-// per XCD when the row is wide.
-static void choose_slices(int c4, int *S, int *SL) {
-  int target = 64;                                           // float4 per slice
-  if (const char *env = std::getenv("PGCN_AGG_SLICE_F4")) {  // tuning override
-    const int v = std::atoi(env);
-    if (v >= 4 && v <= 64) target = v;
+// Column launches of a row of f4 float4: full slices of 64 float4 (at most 8
+// per launch), then the remainder (if any) in one launch whose slice width is
+// the smallest supported width that holds it.
+struct ColLaunch {
+  int off, cnt, S, SL;
+};
+constexpr int kMaxAggF4 = 31 * 512 + 63;                 // 32 launches at most
+
+static int col_launches(int f4, ColLaunch *out, int max_out) {
+  int n = 0;
+  const int full = f4 / 64 * 64;
+  if ((full + 511) / 512 + (f4 > full ? 1 : 0) > max_out) return -1;
+  for (int off = 0; off < full; off += 512) {
+    const int cnt = full - off < 512 ? full - off : 512;
+    out[n++] = ColLaunch{off, cnt, cnt / 64, 64};
   }
-  int s = 1;
-  while (s < 8 && s * target < c4) s *= 2;
-  while (s < 8 && s * 64 < c4) s *= 2;                       // a slice holds at most 64 float4
-  int need = (c4 + s - 1) / s;
-  need = (need + 3) / 4 * 4;
-  static const int widths[] = {4, 8, 12, 16, 20, 24, 32, 40, 48, 64};
-  int sl = 64;
-  for (int w : widths)
-    if (w >= need) {
-      sl = w;
-      break;
-    }
-  *S = s;
-  *SL = sl;
+  const int rem = f4 - full;
+  if (rem > 0) {
+    static const int widths[] = {4, 8, 12, 16, 20, 24, 32, 40, 48, 64};
+    int sl = 64;
+    for (int w : widths)
+      if (w >= rem) {
+        sl = w;
+        break;
+      }
+    out[n++] = ColLaunch{full, rem, 1, sl};
+  }
+  return n;
 }
 
 size_t aggregate_workspace(const Plan &plan, int64_t f) {
@@ -294,13 +328,13 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
   p.partials = a.partials;
   const int f4 = (a.f + 3) / 4;
   const int C = plan.chunks;
-  // launches of at most 8 x 64 float4 columns (2,048 features)
-  for (int off = 0; off < f4; off += 512) {
-    const int cnt = f4 - off < 512 ? f4 - off : 512;
-    int S = 1, SL = 64;
-    choose_slices(cnt, &S, &SL);
-    p.c4_off = off;
-    p.c4_cnt = cnt;
+  if (f4 > kMaxAggF4) return set_error(PGCN_EINVAL, "aggregation: feature widths above 63,740 are not supported");
+  ColLaunch cl[32];
+  const int ncl = col_launches(f4, cl, 32);
+  for (int li = 0; li < ncl; ++li) {
+    const int S = cl[li].S, SL = cl[li].SL;
+    p.c4_off = cl[li].off;
+    p.c4_cnt = cl[li].cnt;
     p.slices = S;
     const int U = 8;
     const int threshold = (64 / SL) * U;
