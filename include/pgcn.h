@@ -262,8 +262,12 @@ int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, 
  * recorded on the launch stream; pgcn_trace_collect waits for the recorded
  * pairs and returns each launch's kind (pgcn_trace_kind) and duration in ms,
  * then clears the record.  pgcn_trace_enable creates `capacity` event pairs
- * up front; launches beyond the capacity are not recorded.  Not for use
- * under graph capture.
+ * up front (timing-only events without the system-scope cache flush a
+ * default event record performs, so tracing does not disturb the caches of
+ * the kernels it brackets) and resets the kind filter to "all kinds";
+ * launches beyond the capacity are not recorded.  pgcn_trace_filter limits
+ * recording to the kinds whose bit (1u << kind) is set in `kind_mask`.  Not
+ * for use under graph capture.
  */
 enum pgcn_trace_kind {
   PGCN_TK_AGG_FWD = 0, PGCN_TK_AGG_BWD = 1, PGCN_TK_AGG_FIXUP = 2, PGCN_TK_GEMM_FWD = 3,
@@ -272,6 +276,7 @@ enum pgcn_trace_kind {
   PGCN_TK_GEMM_PACK = 13
 };
 int pgcn_trace_enable(int32_t capacity);
+int pgcn_trace_filter(uint32_t kind_mask);
 int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t max_records, int32_t *count);
 int pgcn_trace_disable(void);
 

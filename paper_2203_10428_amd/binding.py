@@ -80,6 +80,7 @@ SIGNATURES = {
     "pgcn_sgd_update": (_i32, [_vp, _vp, _vp, _i64, _f32, _vp]),
     "pgcn_refill_async": (_i32, [_vp, _vp, _sz, _u32, _vp]),
     "pgcn_trace_enable": (_i32, [_i32]),
+    "pgcn_trace_filter": (_i32, [C.c_uint32]),
     "pgcn_trace_collect": (_i32, [_vp, _vp, _i32, C.POINTER(_i32)]),
     "pgcn_trace_disable": (_i32, []),
     "pgcn_last_error": (C.c_char_p, []),
@@ -234,6 +235,12 @@ TRACE_KINDS = ["agg_fwd", "agg_bwd", "agg_fixup", "gemm_fwd", "gemm_dgrad", "gem
 
 def pgcn_trace_enable(capacity: int):
     _check(lib.pgcn_trace_enable(capacity), "pgcn_trace_enable")
+
+
+def pgcn_trace_filter(kinds=None):
+    """Record only the named kinds (names of TRACE_KINDS); None records all."""
+    mask = 0xFFFFFFFF if kinds is None else sum(1 << TRACE_KINDS.index(k) for k in kinds)
+    _check(lib.pgcn_trace_filter(mask), "pgcn_trace_filter")
 
 
 def pgcn_trace_collect(max_records: int = 1 << 16):

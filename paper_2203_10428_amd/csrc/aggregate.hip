@@ -36,6 +36,8 @@
 //  * Runs longer than a fixed segment are split; segments write partial sums
 //    that a second pass adds in segment order.  No floating-point atomics:
 //    results are bitwise reproducible.
+#include <cstdlib>
+
 #include "internal.h"
 
 namespace pgcn {
@@ -272,21 +274,28 @@ static int64_t first_short(const Plan &plan, int64_t b, int64_t e, int threshold
   return lo;
 }
 
-// Column launches of a row of f4 float4: full slices of 64 float4 (at most 8
-// per launch), then the remainder (if any) in one launch whose slice width is
-// the smallest supported width that holds it.
+// Column launches of a row of f4 float4: full slices of W float4 (W = 64 by
+// default; at most 8 slices per launch), then the remainder (if any) in one
+// launch whose slice width is the smallest supported width that holds it.
 struct ColLaunch {
   int off, cnt, S, SL;
 };
 constexpr int kMaxAggF4 = 31 * 512 + 63;                 // 32 launches at most
 
+static int slice_width() {
+  const char *env = std::getenv("PGCN_AGG_SLICE_F4");    // tuning override: 16, 32 or 64
+  const int v = env ? std::atoi(env) : 64;
+  return (v == 16 || v == 32) ? v : 64;
+}
+
 static int col_launches(int f4, ColLaunch *out, int max_out) {
+  const int W = slice_width();
   int n = 0;
-  const int full = f4 / 64 * 64;
-  if ((full + 511) / 512 + (f4 > full ? 1 : 0) > max_out) return -1;
-  for (int off = 0; off < full; off += 512) {
-    const int cnt = full - off < 512 ? full - off : 512;
-    out[n++] = ColLaunch{off, cnt, cnt / 64, 64};
+  const int full = f4 / W * W;
+  if ((full + 8 * W - 1) / (8 * W) + (f4 > full ? 1 : 0) > max_out) return -1;
+  for (int off = 0; off < full; off += 8 * W) {
+    const int cnt = full - off < 8 * W ? full - off : 8 * W;
+    out[n++] = ColLaunch{off, cnt, cnt / W, W};
   }
   const int rem = f4 - full;
   if (rem > 0) {
@@ -329,8 +338,9 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
   const int f4 = (a.f + 3) / 4;
   const int C = plan.chunks;
   if (f4 > kMaxAggF4) return set_error(PGCN_EINVAL, "aggregation: feature widths above 63,740 are not supported");
-  ColLaunch cl[32];
-  const int ncl = col_launches(f4, cl, 32);
+  ColLaunch cl[128];
+  const int ncl = col_launches(f4, cl, 128);
+  if (ncl < 0) return set_error(PGCN_EINVAL, "aggregation: too many column launches");
   for (int li = 0; li < ncl; ++li) {
     const int S = cl[li].S, SL = cl[li].SL;
     p.c4_off = cl[li].off;

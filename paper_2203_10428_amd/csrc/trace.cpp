@@ -1,8 +1,11 @@
-// Kernel tracing: when enabled, every kernel launch of the library is
-// bracketed by a pair of HIP events recorded on the launch stream, so the
-// caller can read per-kernel durations measured on the stream the kernel ran
-// on.  Event pairs are created once by pgcn_trace_enable (no allocation while
-// tracing); launches beyond the capacity are not recorded.
+// Kernel tracing: when enabled, every kernel launch of the library (of the
+// kinds selected by the filter) is bracketed by a pair of HIP events recorded
+// on the launch stream, so the caller can read per-kernel durations measured
+// on the stream the kernel ran on.  Event pairs are created once by
+// pgcn_trace_enable (no allocation while tracing) without the system-scope
+// fence of a default event: a fenced record writes back and invalidates the
+// caches, which would slow the traced kernels themselves.  Launches beyond
+// the capacity are not recorded.
 #include <mutex>
 
 #include "internal.h"
@@ -13,6 +16,7 @@ namespace {
 struct TraceState {
   std::mutex mu;
   bool on = false;
+  uint32_t mask = 0xffffffffu;
   std::vector<hipEvent_t> start, stop;
   std::vector<int32_t> kind;
   size_t used = 0;
@@ -27,7 +31,7 @@ TraceScope::TraceScope(int32_t kind, hipStream_t s) : s_(s) {
   TraceState &t = state();
   if (!t.on) return;
   std::lock_guard<std::mutex> g(t.mu);
-  if (!t.on || t.used >= t.start.size()) return;
+  if (!t.on || t.used >= t.start.size() || kind < 0 || kind > 31 || !((t.mask >> kind) & 1u)) return;
   slot_ = (int64_t)t.used++;
   t.kind[slot_] = kind;
   (void)hipEventRecord(t.start[slot_], s_);
@@ -53,11 +57,19 @@ extern "C" int pgcn_trace_enable(int32_t capacity) {
   t.stop.assign(capacity, nullptr);
   t.kind.assign(capacity, -1);
   for (int32_t i = 0; i < capacity; ++i) {
-    PGCN_HIP(hipEventCreate(&t.start[i]));
-    PGCN_HIP(hipEventCreate(&t.stop[i]));
+    PGCN_HIP(hipEventCreateWithFlags(&t.start[i], hipEventDisableSystemFence));
+    PGCN_HIP(hipEventCreateWithFlags(&t.stop[i], hipEventDisableSystemFence));
   }
   t.used = 0;
+  t.mask = 0xffffffffu;
   t.on = true;
+  return PGCN_OK;
+}
+
+extern "C" int pgcn_trace_filter(uint32_t kind_mask) {
+  TraceState &t = state();
+  std::lock_guard<std::mutex> g(t.mu);
+  t.mask = kind_mask;
   return PGCN_OK;
 }
 
