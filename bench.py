@@ -74,17 +74,19 @@ def measured_traffic(workload: str, kernel: str):
 
     profiles/traffic_<workload>.json holds FETCH_SIZE and WRITE_SIZE summed over
     the kernel's dispatches of one step, scaled by the same counters on a plain
-    copy of known size, and the SHA-256 of the kernel source they were taken
-    with.  If the source has changed since, the figure no longer applies (None).
+    copy of known size, and the SHA-256 of the kernel and work-plan sources
+    they were taken with.  If a source has changed since, the figure no longer
+    applies (None).
     """
     import hashlib
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = os.path.join(ROOT, "paper_2203_10428_amd", "csrc", rec["source"])
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
-        return None
+    for name, digest in rec["sources"].items():
+        src = os.path.join(ROOT, "paper_2203_10428_amd", "csrc", name)
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != digest:
+            return None
     return rec["kernels"].get(kernel)
 
 
