@@ -132,7 +132,7 @@ def main():
     ap.add_argument("--no-copy-modes", action="store_true", help="skip the serial / no-refill comparison")
     ap.add_argument("--refill", default="dma", choices=["dma", "blit"], help="engine of the stale-buffer refills")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=float, default=0.25, help="inner-node fraction timed on the CPU")
+    ap.add_argument("--cpu-sample", type=float, default=0.4, help="inner-node fraction timed on the CPU")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 5 plain device copies of BYTES bytes (counter calibration) and exit")
     args = ap.parse_args()
