@@ -14,10 +14,10 @@
 //    whether or not all 64 lanes are active (measured: ~32 cycles per
 //    64 x 16-byte load, about 20 TB/s for the chip on cache-resident rows),
 //    so lanes are kept full: the float4 columns of a row are cut into full
-//    slices of 64 float4 (S <= 8 per launch) plus one remainder launch of
-//    width SL < 64 in which G = 64 / SL lane groups share a wave.  Workgroup
-//    b works on slice b % S; the hardware deals workgroups to the 8 XCDs
-//    round robin, so an XCD only ever touches one slice of every feature row.
+//    slices of 64 float4 (S = 8, 4, 2 or 1 per launch) plus one remainder
+//    launch of width SL < 64 in which G = 64 / SL lane groups share a wave.
+//    Workgroup b works on slice b % S; the hardware deals workgroups to the
+//    8 XCDs round robin, so an XCD only ever touches one slice of every row.
 //  * The columns of the sparse matrix (the gathered rows) are cut into C
 //    chunks of about 11,000 rows, one launch per chunk, so that the rows one
 //    launch gathers from stay in the caches while they are reused (cache
@@ -29,13 +29,15 @@
 //    of them per group in flight (masked at the row's end), then the groups
 //    are added in group order.  Short runs (fewer than G*U non-zeros): each
 //    lane group owns its own item, U non-zeros in flight; items are sorted by
-//    length, so the groups of a wave finish together.  With several lane
-//    groups the column indices are fetched by one load per wave (one index
-//    per lane) and handed out with lane shuffles, which keeps index fetches
-//    off the texture data path.
-//  * Runs longer than a fixed segment are split; segments write partial sums
-//    that a second pass adds in segment order.  No floating-point atomics:
-//    results are bitwise reproducible.
+//    length, so the groups of a wave finish together.  Both kinds run in
+//    one launch (long-run workgroups first).  Column indices are fetched by
+//    one load of up to 64 per wave (one per lane) and handed out by
+//    v_readlane or lane shuffles, which keeps index fetches off the texture
+//    data path.
+//  * A row with a run longer than a fixed segment is a split row: all its
+//    runs are cut into segments that write partial sums, and one pass after
+//    the last chunk adds them in (chunk, segment) order.  No floating-point
+//    atomics: results are bitwise reproducible.
 #include <cstdlib>
 
 #include "internal.h"
@@ -43,8 +45,10 @@
 namespace pgcn {
 
 struct AggParams {
-  const WorkItem *items;
+  const WorkItem *items;  // long-run items [0, n_long), then short-run items [n_long, n_items)
   int64_t n_items;
+  int64_t n_long;
+  int64_t long_blocks;    // workgroups of the long-run part (a multiple of slices)
   const int32_t *col;
   int64_t in_split;
   const float *in_lo;
@@ -106,15 +110,15 @@ __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, fl
   }
 }
 
-// Short runs: lane group g of a wave owns item (wave * G + g).
+// Short runs: lane group g of a wave owns item n_long + (wave * G + g).
 template <int SL, int U>
-__global__ __launch_bounds__(256) void agg_multi_kernel(AggParams p) {
+__device__ __forceinline__ void agg_short(const AggParams &p, int64_t blk) {
   constexpr int G = 64 / SL;
   constexpr int NL = (U + SL - 1) / SL;                 // index loads per step (G > 1)
   const int S = p.slices;
-  const int slice = blockIdx.x % S;
+  const int slice = (int)(blk % S);
   const int lane = threadIdx.x % 64, g = lane / SL, j = lane % SL;
-  const int64_t item = ((int64_t)(blockIdx.x / S) * 4 + threadIdx.x / 64) * G + g;
+  const int64_t item = p.n_long + ((blk / S) * 4 + threadIdx.x / 64) * G + g;
   // a whole lane group leaves together (it is its own shuffle source)
   if (g >= G || item >= p.n_items) return;
   const int cs = slice * SL + j;
@@ -126,9 +130,10 @@ __global__ __launch_bounds__(256) void agg_multi_kernel(AggParams p) {
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int k = 0; k < len; k += U) {
     int32_t c[U];
-    if (G == 1) {
+    if (G == 1) {                                      // one item per wave: lane u loads index u
+      const int32_t mine = (lane < U && k + lane < len) ? __builtin_nontemporal_load(cols + k + lane) : -1;
 #pragma unroll
-      for (int u = 0; u < U; ++u) c[u] = k + u < len ? __builtin_nontemporal_load(cols + k + u) : -1;
+      for (int u = 0; u < U; ++u) c[u] = __builtin_amdgcn_readlane(mine, u);
     } else {
       int32_t mine[NL];
 #pragma unroll
@@ -157,14 +162,15 @@ __global__ __launch_bounds__(256) void agg_multi_kernel(AggParams p) {
   else *reinterpret_cast<float4 *>(p.partials + (int64_t)(-it.dst - 1) * p.ld_part + cbase) = acc;
 }
 
+// Long runs: one wave owns item (blk / S) * 4 + wave.
 template <int SL, int U>
-__global__ __launch_bounds__(256) void agg_kernel(AggParams p) {
+__device__ __forceinline__ void agg_long(const AggParams &p, int64_t blk) {
   constexpr int G = 64 / SL;
   const int S = p.slices;
-  const int slice = blockIdx.x % S;
-  int64_t item = (int64_t)(blockIdx.x / S) * 4 + threadIdx.x / 64;
+  const int slice = (int)(blk % S);
+  int64_t item = (blk / S) * 4 + threadIdx.x / 64;
   item = __builtin_amdgcn_readfirstlane((int)item);
-  if (item >= p.n_items) return;
+  if (item >= p.n_long) return;
   const int lane = threadIdx.x % 64, g = lane / SL;
   const int cs = slice * SL + lane % SL;                // float4 column inside this launch
   const bool act = g < G && cs < p.c4_cnt;
@@ -174,35 +180,41 @@ __global__ __launch_bounds__(256) void agg_kernel(AggParams p) {
   const int32_t *cols = p.col + it.begin;
   const int len = it.len;
 
+  // column indices: one load of up to 64 per wave (one per lane), handed out
+  // by v_readlane (one lane group) or lane shuffles (several groups)
+  constexpr int GU = G * U;                            // non-zeros per step
+  constexpr int KB = GU <= 64 ? (64 / GU) * GU : GU;   // non-zeros per index load (G divides 64 if GU > 64)
+  constexpr int NB = (KB + 63) / 64;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int k = 0; k < len; k += G * U) {
-    int32_t c[U];
-    if (G == 1) {                                      // uniform: scalar loads
+  for (int k0 = 0; k0 < len; k0 += KB) {
+    int32_t mine[NB];
 #pragma unroll
-      for (int u = 0; u < U; ++u) c[u] = k + u < len ? __builtin_nontemporal_load(cols + k + u) : -1;
-    } else {                                           // one index per lane, then shuffles
-      constexpr int NB = (G * U + 63) / 64;            // G divides 64 whenever G * U > 64
-      int32_t mine[NB];
+    for (int t = 0; t < NB; ++t) {
+      const int q = 64 * t + lane;
+      mine[t] = (q < KB && k0 + q < len) ? __builtin_nontemporal_load(cols + k0 + q) : -1;
+    }
+    const int kn = len - k0 < KB ? len - k0 : KB;
+    for (int j = 0; j < kn; j += GU) {
+      int32_t c[U];
 #pragma unroll
-      for (int t = 0; t < NB; ++t) {
-        const int q = 64 * t + lane;
-        mine[t] = (q < G * U && k + q < len) ? __builtin_nontemporal_load(cols + k + q) : -1;
+      for (int u = 0; u < U; ++u) {
+        if (G == 1) c[u] = __builtin_amdgcn_readlane(mine[0], j + u);
+        else if (NB == 1) c[u] = __shfl(mine[0], j + u * G + gg);
+        else c[u] = __shfl(mine[(u * G) / 64], (u * G) % 64 + gg);    // KB == GU: j == 0
+      }
+      float4 x[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float *src = nullptr;
+        if (c[u] >= 0) {
+          if (c[u] < p.in_split) src = p.in_lo + (int64_t)c[u] * p.ld_in;
+          else if (p.in_hi) src = p.in_hi + (int64_t)(c[u] - p.in_split) * p.ld_in;
+        }
+        x[u] = (act && src) ? *reinterpret_cast<const float4 *>(src + cbase) : make_float4(0.f, 0.f, 0.f, 0.f);
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u) c[u] = __shfl(mine[(u * G) / 64], (u * G) % 64 + gg);
+      for (int u = 0; u < U; ++u) acc = add4(acc, x[u]);
     }
-    float4 x[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const float *src = nullptr;
-      if (c[u] >= 0) {
-        if (c[u] < p.in_split) src = p.in_lo + (int64_t)c[u] * p.ld_in;
-        else if (p.in_hi) src = p.in_hi + (int64_t)(c[u] - p.in_split) * p.ld_in;
-      }
-      x[u] = (act && src) ? *reinterpret_cast<const float4 *>(src + cbase) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) acc = add4(acc, x[u]);
   }
   // groups are added in group order (fixed): ((g0 + g1) + g2) + ...
   float4 tot = acc;
@@ -222,7 +234,15 @@ __global__ __launch_bounds__(256) void agg_kernel(AggParams p) {
   }
 }
 
-// Sum the partial slots of each split row in slot order, then combine and store.
+// One launch per chunk and column range: the first long_blocks workgroups
+// take the long runs, the rest the short runs.
+template <int SL, int U>
+__global__ __launch_bounds__(256) void agg_kernel(AggParams p) {
+  if ((int64_t)blockIdx.x < p.long_blocks) agg_long<SL, U>(p, blockIdx.x);
+  else agg_short<SL, U>(p, (int64_t)blockIdx.x - p.long_blocks);
+}
+
+// Sum the partial slots of each split row in slot order, then store.
 __global__ __launch_bounds__(256) void agg_fixup_kernel(AggParams p, const SplitRow *splits) {
   const SplitRow s = splits[blockIdx.x];
   for (int c4 = p.c4_off + threadIdx.x; c4 < p.c4_off + p.c4_cnt; c4 += blockDim.x) {
@@ -234,38 +254,33 @@ __global__ __launch_bounds__(256) void agg_fixup_kernel(AggParams p, const Split
 }
 
 template <int SL>
-static void launch_sl(const AggParams &p, bool multi, hipStream_t s) {
+static void launch_sl(AggParams p, hipStream_t s) {
   constexpr int U = 8;
   constexpr int G = 64 / SL;
-  if (multi) {
-    const int64_t blocks = (p.n_items + 4 * G - 1) / (4 * G) * p.slices;
-    hipLaunchKernelGGL((agg_multi_kernel<SL, U>), dim3((unsigned)blocks), dim3(256), 0, s, p);
-  } else {
-    const int64_t blocks = (p.n_items + 3) / 4 * p.slices;
-    hipLaunchKernelGGL((agg_kernel<SL, U>), dim3((unsigned)blocks), dim3(256), 0, s, p);
-  }
+  p.long_blocks = (p.n_long + 3) / 4 * p.slices;
+  const int64_t short_blocks = (p.n_items - p.n_long + 4 * G - 1) / (4 * G) * p.slices;
+  hipLaunchKernelGGL((agg_kernel<SL, U>), dim3((unsigned)(p.long_blocks + short_blocks)), dim3(256), 0, s, p);
 }
 
-static void launch_dispatch(const AggParams &p, int sl, bool multi, hipStream_t s) {
+static void launch_dispatch(const AggParams &p, int sl, hipStream_t s) {
   switch (sl) {
-    case 4: launch_sl<4>(p, multi, s); break;
-    case 8: launch_sl<8>(p, multi, s); break;
-    case 12: launch_sl<12>(p, multi, s); break;
-    case 16: launch_sl<16>(p, multi, s); break;
-    case 20: launch_sl<20>(p, multi, s); break;
-    case 24: launch_sl<24>(p, multi, s); break;
-    case 32: launch_sl<32>(p, multi, s); break;
-    case 40: launch_sl<40>(p, multi, s); break;
-    case 48: launch_sl<48>(p, multi, s); break;
-    default: launch_sl<64>(p, multi, s); break;
+    case 4: launch_sl<4>(p, s); break;
+    case 8: launch_sl<8>(p, s); break;
+    case 12: launch_sl<12>(p, s); break;
+    case 16: launch_sl<16>(p, s); break;
+    case 20: launch_sl<20>(p, s); break;
+    case 24: launch_sl<24>(p, s); break;
+    case 32: launch_sl<32>(p, s); break;
+    case 40: launch_sl<40>(p, s); break;
+    case 48: launch_sl<48>(p, s); break;
+    default: launch_sl<64>(p, s); break;
   }
 }
 
-// Items of a chunk are split segments first, then whole runs by decreasing
-// length: the first whole run shorter than `threshold` starts the short part.
-static int64_t first_short(const Plan &plan, int64_t b, int64_t e, int threshold) {
-  int64_t lo = b, hi = e;
-  while (lo < hi && plan.items[lo].dst < 0) ++lo;     // segments (at most a few per split row)
+// First short run of chunk c: whole runs are sorted by decreasing length
+// after the split segments (which always take the long-run path).
+static int64_t first_short(const Plan &plan, int c, int threshold) {
+  int64_t lo = plan.chunk_whole[c], hi = plan.chunk_items[c + 1];
   while (lo < hi) {
     const int64_t mid = lo + (hi - lo) / 2;
     if (plan.items[mid].len >= threshold) lo = mid + 1;
@@ -275,7 +290,7 @@ static int64_t first_short(const Plan &plan, int64_t b, int64_t e, int threshold
 }
 
 // Column launches of a row of f4 float4: full slices of W float4 (W = 64 by
-// default; at most 8 slices per launch), then the remainder (if any) in one
+// default; 8, 4, 2 or 1 slices per launch), then the remainder (if any) in one
 // launch whose slice width is the smallest supported width that holds it.
 struct ColLaunch {
   int off, cnt, S, SL;
@@ -292,11 +307,16 @@ static int col_launches(int f4, ColLaunch *out, int max_out) {
   const int W = slice_width();
   int n = 0;
   const int full = f4 / W * W;
-  if ((full + 8 * W - 1) / (8 * W) + (f4 > full ? 1 : 0) > max_out) return -1;
-  for (int off = 0; off < full; off += 8 * W) {
-    const int cnt = full - off < 8 * W ? full - off : 8 * W;
-    out[n++] = ColLaunch{off, cnt, cnt / W, W};
+  // full slices in launches of 8, 4, 2 or 1 slices: slice b % S of workgroup b
+  // then matches its XCD b % 8
+  for (int off = 0; off < full;) {
+    int S = 8;
+    while (S * W > full - off) S /= 2;
+    if (n == max_out) return -1;
+    out[n++] = ColLaunch{off, S * W, S, W};
+    off += S * W;
   }
+  if (f4 > full && n == max_out) return -1;
   const int rem = f4 - full;
   if (rem > 0) {
     static const int widths[] = {4, 8, 12, 16, 20, 24, 32, 40, 48, 64};
@@ -313,7 +333,7 @@ static int col_launches(int f4, ColLaunch *out, int max_out) {
 
 size_t aggregate_workspace(const Plan &plan, int64_t f) {
   const int64_t ld_part = (f + 3) / 4 * 4;
-  return (size_t)plan.max_chunk_slots * (size_t)ld_part * sizeof(float);
+  return (size_t)plan.slots * (size_t)ld_part * sizeof(float);
 }
 
 int launch_aggregate(const AggArgs &a, hipStream_t s) {
@@ -351,28 +371,20 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
     for (int c = 0; c < C; ++c) {
       p.mode = (c == 0 ? AGG_FIRST : 0) | (c == C - 1 ? AGG_LAST : 0);
       const int64_t b = plan.chunk_items[c], e = plan.chunk_items[c + 1];
-      const int64_t m = first_short(plan, b, e, threshold);
-      if (m > b) {                     // long runs: lane groups share an item
-        p.items = plan.d_items + b;
-        p.n_items = m - b;
-        TraceScope ts(a.trace_kind, s);
-        launch_dispatch(p, SL, false, s);
-        PGCN_HIP(hipGetLastError());
-      }
-      if (e > m) {                     // short runs: one item per lane group
-        p.items = plan.d_items + m;
-        p.n_items = e - m;
-        TraceScope ts(a.trace_kind, s);
-        launch_dispatch(p, SL, true, s);
-        PGCN_HIP(hipGetLastError());
-      }
-      const int64_t ns = plan.chunk_splits[c + 1] - plan.chunk_splits[c];
-      if (ns > 0) {
-        TraceScope ts(PGCN_TK_AGG_FIXUP, s);
-        hipLaunchKernelGGL(agg_fixup_kernel, dim3((unsigned)ns), dim3(256), 0, s, p,
-                           (const SplitRow *)(plan.d_splits + plan.chunk_splits[c]));
-        PGCN_HIP(hipGetLastError());
-      }
+      if (e == b) continue;
+      p.items = plan.d_items + b;
+      p.n_items = e - b;
+      p.n_long = first_short(plan, c, threshold) - b;
+      TraceScope ts(a.trace_kind, s);
+      launch_dispatch(p, SL, s);
+      PGCN_HIP(hipGetLastError());
+    }
+    if (!plan.splits.empty()) {       // split rows: all their slots, in (chunk, segment) order
+      p.mode = AGG_FIRST | AGG_LAST;
+      TraceScope ts(PGCN_TK_AGG_FIXUP, s);
+      hipLaunchKernelGGL(agg_fixup_kernel, dim3((unsigned)plan.splits.size()), dim3(256), 0, s, p,
+                         (const SplitRow *)plan.d_splits);
+      PGCN_HIP(hipGetLastError());
     }
   }
   return PGCN_OK;

@@ -31,16 +31,16 @@ struct SplitRow {
 
 // Fixed work plan over one CSR matrix (rows of P_i or of P_i^T).  The
 // matrix columns are cut into `chunks` equal ranges; chunk c's items are
-// items[chunk_items[c] .. chunk_items[c+1]) (one per row and chunk, or one per
-// segment of a long run) and its split rows splits[chunk_splits[c] ..
-// chunk_splits[c+1]), whose partial slots restart at 0 in every chunk.
+// items[chunk_items[c] .. chunk_items[c+1]): first the segments of split rows
+// (items[.. chunk_whole[c])), then one item per other row's run, longest
+// first.  Split rows own `slots` partial slots in total, contiguous per row in
+// (chunk, segment) order; `splits` lists them for the fix-up pass.
 struct Plan {
   int32_t chunks = 1;
   std::vector<WorkItem> items;
   std::vector<SplitRow> splits;
-  std::vector<int64_t> chunk_items, chunk_splits;
-  int64_t slots = 0;            // total partial slots over all chunks
-  int64_t max_chunk_slots = 0;  // partial slots needed at once
+  std::vector<int64_t> chunk_items, chunk_whole;
+  int64_t slots = 0;            // partial slots of all split rows
   WorkItem *d_items = nullptr;
   SplitRow *d_splits = nullptr;
 };

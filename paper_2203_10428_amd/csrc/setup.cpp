@@ -38,50 +38,74 @@ static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz) {
   return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, 16));
 }
 
-// Rows (runs inside a chunk) longer than `segment` are cut into fixed
-// segments whose partial sums are added in segment order by a second pass,
-// so results never depend on timing.  Whole runs are scheduled longest first.
+// Work plan of one aggregation.  A row whose run inside some chunk is longer
+// than `segment` is a split row: every run of it, in every chunk, is cut into
+// segments of at most `segment` non-zeros that write partial slots; the row's
+// slots are contiguous in (chunk, segment) order, and one fix-up pass after
+// the last chunk adds them in that order, so results never depend on timing.
+// Every other row adds its run of each chunk to the output in chunk order
+// (empty runs are skipped except in the first and last chunk, which write
+// and finish the row).  Whole runs are scheduled longest first.
 static void build_plan(const std::vector<int64_t> &rowptr, const std::vector<int32_t> &col, int64_t nrows,
                        int64_t ncols, int32_t segment, Plan &p) {
   p.items.clear();
   p.splits.clear();
   p.slots = 0;
-  p.max_chunk_slots = 0;
   const int64_t nnz = nrows ? rowptr[nrows] : 0;
   p.chunks = choose_chunks(nrows, ncols, nnz);
   const int32_t C = p.chunks;
   p.chunk_items.assign(C + 1, 0);
-  p.chunk_splits.assign(C + 1, 0);
-  std::vector<int64_t> b(nrows), e(nrows), order;
+  p.chunk_whole.assign(C, 0);
+  // run bounds: row r's run in chunk c is [bnd[r*(C+1)+c], bnd[r*(C+1)+c+1])
+  std::vector<int64_t> bnd((size_t)nrows * (C + 1));
+  for (int64_t r = 0; r < nrows; ++r) {
+    const int32_t *rb = col.data() + rowptr[r], *re = col.data() + rowptr[r + 1];
+    int64_t *q = bnd.data() + (size_t)r * (C + 1);
+    q[0] = rowptr[r];
+    for (int32_t c = 1; c < C; ++c) q[c] = rowptr[r] + (std::lower_bound(rb, re, (int32_t)(ncols * c / C)) - rb);
+    q[C] = rowptr[r + 1];
+  }
+  // split rows and their slot ranges
+  std::vector<int64_t> cursor(nrows, -1);
+  for (int64_t r = 0; r < nrows; ++r) {
+    const int64_t *q = bnd.data() + (size_t)r * (C + 1);
+    bool split = false;
+    int64_t nseg = 0;
+    for (int32_t c = 0; c < C; ++c) {
+      const int64_t len = q[c + 1] - q[c];
+      split |= len > segment;
+      nseg += (len + segment - 1) / segment;
+    }
+    if (!split) continue;
+    p.splits.push_back(SplitRow{(int32_t)r, (int32_t)p.slots, (int32_t)nseg, 0});
+    cursor[r] = p.slots;
+    p.slots += nseg;
+  }
+  std::vector<int64_t> order;
   order.reserve(nrows);
   for (int32_t c = 0; c < C; ++c) {
-    const int32_t lo = (int32_t)(ncols * c / C), hi = (int32_t)(ncols * (c + 1) / C);
-    int64_t slots = 0;
     order.clear();
     for (int64_t r = 0; r < nrows; ++r) {
-      const int32_t *rb = col.data() + rowptr[r], *re = col.data() + rowptr[r + 1];
-      b[r] = (C == 1) ? rowptr[r] : rowptr[r] + (std::lower_bound(rb, re, lo) - rb);
-      e[r] = (C == 1) ? rowptr[r + 1] : rowptr[r] + (std::lower_bound(rb, re, hi) - rb);
-      const int64_t len = e[r] - b[r];
-      if (len > segment) {
-        const int32_t nseg = (int32_t)((len + segment - 1) / segment);
-        p.splits.push_back(SplitRow{(int32_t)r, (int32_t)slots, nseg, 0});
-        for (int32_t q = 0; q < nseg; ++q) {
-          const int64_t sb = b[r] + (int64_t)q * segment;
-          const int64_t se = std::min<int64_t>(sb + segment, e[r]);
-          p.items.push_back(WorkItem{sb, (int32_t)(se - sb), (int32_t)(-(slots + q) - 1)});
+      const int64_t b = bnd[(size_t)r * (C + 1) + c], e = bnd[(size_t)r * (C + 1) + c + 1];
+      if (cursor[r] >= 0) {
+        for (int64_t sb = b; sb < e; sb += segment) {
+          const int64_t se = std::min<int64_t>(sb + segment, e);
+          p.items.push_back(WorkItem{sb, (int32_t)(se - sb), (int32_t)(-cursor[r]++ - 1)});
         }
-        slots += nseg;
-      } else {
+      } else if (e > b || c == 0 || c == C - 1) {
         order.push_back(r);
       }
     }
-    std::stable_sort(order.begin(), order.end(), [&](int64_t x, int64_t y) { return e[x] - b[x] > e[y] - b[y]; });
-    for (int64_t r : order) p.items.push_back(WorkItem{b[r], (int32_t)(e[r] - b[r]), (int32_t)r});
+    p.chunk_whole[c] = (int64_t)p.items.size();
+    std::stable_sort(order.begin(), order.end(), [&](int64_t x, int64_t y) {
+      const int64_t *qx = bnd.data() + (size_t)x * (C + 1) + c, *qy = bnd.data() + (size_t)y * (C + 1) + c;
+      return qx[1] - qx[0] > qy[1] - qy[0];
+    });
+    for (int64_t r : order) {
+      const int64_t b = bnd[(size_t)r * (C + 1) + c], e = bnd[(size_t)r * (C + 1) + c + 1];
+      p.items.push_back(WorkItem{b, (int32_t)(e - b), (int32_t)r});
+    }
     p.chunk_items[c + 1] = (int64_t)p.items.size();
-    p.chunk_splits[c + 1] = (int64_t)p.splits.size();
-    p.slots += slots;
-    p.max_chunk_slots = std::max(p.max_chunk_slots, slots);
   }
 }
 
