@@ -292,6 +292,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": breakdown,
+        "algorithmic_work_per_step": work,
         "utilisation": util,
         "copy_modes_ms_per_step": copy_modes,
         "loss": loss,
