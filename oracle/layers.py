@@ -21,8 +21,26 @@ The paper writes the aggregation as the product P H W; aggregating first and
 transforming first in the backward are the same matrix products in another
 association (the reading is listed with the others in the design notes).
 
+GraphSAGE layer (Section 2: the update takes CONCAT(z_v, h_v); the paper's
+experiments train GraphSAGE), with P the mean over N(v) without a self loop
+and X the layer input after dropout (dropout is applied to the received rows
+too, after communication, with one mask for the forward and the backward):
+
+    z     = P X_full                      (n x f)
+    Z     = [z, X_inner] W                (W is 2f x f_out: rows 0..f-1 act on z)
+    H     = relu(Z)
+
+    M      = J ∘ 1[Z > 0]
+    G      = [z, X_inner]ᵀ M
+    [dz, ds] = M Wᵀ
+    J_full = Pᵀ dz, plus ds on the inner rows   (gradient of the dropped input;
+                                                  the caller applies the mask)
+
+Adam (Kingma and Ba, ICLR 2015, Algorithm 1), the experiments' optimiser.
+
 Pinned by: dense brute force of P (tests), central finite differences of the
-partition-local loss (tests), reduction to full-graph GCN (tests).
+partition-local loss (tests), reduction to full-graph GCN / GraphSAGE (tests),
+torch.optim.Adam (tests).
 """
 from __future__ import annotations
 
@@ -96,3 +114,38 @@ def ema(state: np.ndarray, incoming: np.ndarray, gamma: float) -> np.ndarray:
 def sgd(W: np.ndarray, G: np.ndarray, eta: float) -> np.ndarray:
     """Algorithm 1's update W_t = W_{t-1} - η G."""
     return W - eta * G
+
+
+def sage_forward(P, X_full: np.ndarray, n_inner: int, W: np.ndarray, relu: bool, gemm: str = "f64"):
+    """Returns (z, Z, H); X_full = [X_inner; X_boundary] is the (dropped) layer input."""
+    z = P @ X_full
+    Xc = np.hstack([z, X_full[:n_inner]])
+    Z = _operand(Xc, gemm) @ _operand(W, gemm)
+    H = np.maximum(Z, 0.0) if relu else Z
+    return z, Z, H
+
+
+def sage_backward(P, z: np.ndarray, X_inner: np.ndarray, Z: np.ndarray, J: np.ndarray, W: np.ndarray,
+                  relu: bool, input_grad: bool, gemm: str = "f64"):
+    """Returns (G, J_full): J_full is the gradient of the dropped input rows (inner, then boundary)."""
+    M = J * (Z > 0.0) if relu else J
+    Mq = _operand(M, gemm)
+    Xc = np.hstack([z, X_inner])
+    G = _operand(Xc, gemm).T @ Mq
+    if not input_grad:
+        return G, None
+    f = z.shape[1]
+    dX = Mq @ _operand(W, gemm).T
+    J_full = P.T @ dX[:, :f]
+    J_full[: z.shape[0]] += dX[:, f:]
+    return G, J_full
+
+
+def adam(W: np.ndarray, G: np.ndarray, m: np.ndarray, v: np.ndarray, t: int, lr: float,
+         beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8):
+    """One Adam step (t >= 1): moments m, v updated; returns (W, m, v)."""
+    m = beta1 * m + (1.0 - beta1) * G
+    v = beta2 * v + (1.0 - beta2) * G * G
+    m_hat = m / (1.0 - beta1 ** t)
+    v_hat = v / (1.0 - beta2 ** t)
+    return W - lr * m_hat / (np.sqrt(v_hat) + eps), m, v

@@ -8,7 +8,11 @@ Definitions followed (Algorithm 1's set-up block and Section 3.1):
 * receive     S_{j,i} = B_i ∩ V_j  (the owner-j block of B_i);
 * the local propagation matrix P_i keeps the inner rows of the row-normalised
   D̃⁻¹(A + I) and the columns of V_i ∪ B_i (Appendix A.1 splits P into
-  P_in + P_bd; here both halves are columns of one matrix).
+  P_in + P_bd; here both halves are columns of one matrix);
+* for the GraphSAGE layer (Section 2: the update takes CONCAT(z_v, h_v) with
+  z_v aggregated over N(v)) the matrix is the mean over N(v) alone,
+  D⁻¹A, with no self loop (``self_loop=False``); a row without neighbours
+  is zero.
 
 Canonical numbering (the papers leaves numbering open; this one makes the
 C++ builder's output comparable bit for bit):
@@ -16,7 +20,7 @@ C++ builder's output comparable bit for bit):
 * inner local id   = rank of the global id among the nodes with owner i;
 * boundary local id = n_inner + rank by (owner, global id);
 * CSR columns ascending by local id, duplicates removed, one self loop per
-  inner row;
+  inner row (none with ``self_loop=False``);
 * the transpose CSR has rows 0 .. n_inner+n_bd-1, columns ascending;
 * the concatenated send list holds S_{i,j} for ascending j, each ascending by
   global id (equal to ascending local id);
@@ -91,7 +95,7 @@ def _csr(nrows: int, r: np.ndarray, c: np.ndarray):
 
 
 def build_partition(n: int, rowptr: np.ndarray, col: np.ndarray, owner: np.ndarray,
-                    part: int, nparts: int) -> Partition:
+                    part: int, nparts: int, self_loop: bool = True) -> Partition:
     rowptr = np.asarray(rowptr, dtype=np.int64)
     col = np.asarray(col, dtype=np.int64)
     owner = np.asarray(owner, dtype=np.int64)
@@ -116,9 +120,10 @@ def build_partition(n: int, rowptr: np.ndarray, col: np.ndarray, owner: np.ndarr
     recv_ptr = np.zeros(nparts + 1, dtype=np.int64)
     np.cumsum(np.bincount(bd_owner, minlength=nparts), out=recv_ptr[1:])
 
-    # P_i pattern: N(v) ∪ {v} for inner v, in local ids
-    lr = np.concatenate([local_of[r], np.arange(n_in)])
-    lc = np.concatenate([local_of[c], np.arange(n_in)])
+    # P_i pattern: N(v) ∪ {v} for inner v (N(v) alone without self loops), in local ids
+    diag = np.arange(n_in) if self_loop else np.zeros(0, dtype=np.int64)
+    lr = np.concatenate([local_of[r], diag])
+    lc = np.concatenate([local_of[c], diag])
     p_rowptr, p_col = _csr(n_in, lr, lc)
     # P_iᵀ pattern
     t_rowptr, t_col = _csr(n_in + len(bd_gid), lc, lr)
@@ -149,9 +154,12 @@ def build_partition(n: int, rowptr: np.ndarray, col: np.ndarray, owner: np.ndarr
 
 
 def propagation_matrix(p: Partition):
-    """P_i as a SciPy CSR matrix, entries 1/d_v with d_v the row length (degree + 1)."""
+    """P_i as a SciPy CSR matrix, entries 1/d_v with d_v the row length (degree + 1, or the
+    degree without self loops)."""
     import scipy.sparse as sp
-    d = np.diff(p.rowptr).astype(np.float64)
-    vals = np.repeat(1.0 / d, np.diff(p.rowptr))
+    d = np.diff(p.rowptr)
+    inv = np.zeros(len(d))
+    inv[d > 0] = 1.0 / d[d > 0]
+    vals = np.repeat(inv, d)
     return sp.csr_matrix((vals, p.col.astype(np.int64), p.rowptr),
                          shape=(p.n_inner, p.n_inner + p.n_bd))

@@ -28,7 +28,17 @@ Readings of points the paper leaves open (each is a keyword here):
   contributions C_j, which equals smoothing each remote node's δz before the
   1/d_v weighting because the weighting is fixed across iterations.
 * the received gradients are added for ascending peer j (Algorithm 1's loop).
-* the AllReduce is a sum; the optimiser is Algorithm 1's SGD.
+* the AllReduce is a sum; the optimiser is Algorithm 1's SGD, or Adam (the
+  experiments' optimiser) with ``optimizer="adam"``.
+* ``model="sage"`` trains the experiments' GraphSAGE layer (Section 2's
+  CONCAT update; mean over N(v) without a self loop) instead of the GCN
+  layer of Algorithm 1.
+* ``dropout`` p drops each layer's whole input (inner and received boundary
+  rows, after smoothing) with one mask for the forward and the backward, as
+  the paper's implementation notes require; the mask is drawn from
+  Philox4x32-10 keyed by (``seed``, partition) and counted by (element,
+  layer, iteration) (``oracle.philox``).  The input gradient is multiplied
+  by the same mask before it is sent or accumulated.
 
 Pinned by: reduction to full-graph GCN in vanilla mode, equality of the
 modes with one partition, the η = 0 / γ = 0 staleness-timing fixed point, and
@@ -42,6 +52,7 @@ import numpy as np
 
 from . import layers
 from .partition import Partition, build_partition, propagation_matrix
+from .philox import dropout_mask
 
 
 @dataclass
@@ -57,6 +68,13 @@ class Options:
     x_bd_preload: bool = False
     ema_init: str = "zero"          # "zero" | "first"
     gemm: str = "f64"               # "f64" | "bf16" (operands of the update products rounded to bf16)
+    model: str = "gcn"              # "gcn" | "sage"
+    dropout: float = 0.0
+    seed: int = 0
+    optimizer: str = "sgd"          # "sgd" | "adam" (learning rate eta)
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
 
 
 @dataclass
@@ -79,14 +97,17 @@ class Simulation:
     def __init__(self, n, rowptr, col, owner, nparts, X, labels, W0, opts: Options):
         self.opts = opts
         self.nparts = nparts
-        self.parts: list[Partition] = [build_partition(n, rowptr, col, owner, i, nparts)
+        self.parts: list[Partition] = [build_partition(n, rowptr, col, owner, i, nparts,
+                                                       self_loop=opts.model == "gcn")
                                        for i in range(nparts)]
         self.P = [propagation_matrix(p) for p in self.parts]
         self.X = np.asarray(X, dtype=np.float64)
         self.labels = labels
         self.W = [np.asarray(w, dtype=np.float64).copy() for w in W0]
         self.L = len(self.W)
-        self.widths = [self.W[0].shape[0]] + [w.shape[1] for w in self.W]
+        self.widths = [self.W[0].shape[0] // (2 if opts.model == "sage" else 1)] + [w.shape[1] for w in self.W]
+        self.adam_m = [np.zeros_like(w) for w in self.W]
+        self.adam_v = [np.zeros_like(w) for w in self.W]
         self.t = 0
         self.state = []
         for p in self.parts:
@@ -143,7 +164,7 @@ class Simulation:
         t = self.t
         pipe = o.mode == "pipe"
         rec = [dict(t=t, W_in=[w.copy() for w in self.W], state_in=self.state[i].copy(),
-                    A={}, Z={}, H={}, H_bd_used={}, C_used={}, J_full={}, G={},
+                    A={}, Z={}, H={}, H_bd_used={}, C_used={}, J_full={}, G={}, X_in={}, mask={},
                     send_f={}, send_g={}) for i in range(self.nparts)]
         H_prev = [self.X[p.inner_gid] for p in self.parts]
 
@@ -162,8 +183,12 @@ class Simulation:
                 else:
                     Hbd = self.state[i].feat_buf[l]
                 rec[i]["H_bd_used"][l] = Hbd.copy()
-                A, Z, H = layers.layer_forward(self.P[i], np.vstack([H_prev[i], Hbd]), self.W[l - 1],
-                                               self._relu(l), o.gemm)
+                X, mask = self._dropped_input(i, l, t, H_prev[i], Hbd)
+                rec[i]["X_in"][l], rec[i]["mask"][l] = X[: p.n_inner], mask
+                if o.model == "sage":
+                    A, Z, H = layers.sage_forward(self.P[i], X, p.n_inner, self.W[l - 1], self._relu(l), o.gemm)
+                else:
+                    A, Z, H = layers.layer_forward(self.P[i], X, self.W[l - 1], self._relu(l), o.gemm)
                 rec[i]["A"][l], rec[i]["Z"][l], rec[i]["H"][l] = A, Z, H
                 H_prev[i] = H
             if pipe:
@@ -183,8 +208,14 @@ class Simulation:
         for l in range(self.L, 0, -1):
             J_full = [None] * self.nparts
             for i, p in enumerate(self.parts):
-                G, Jf = layers.layer_backward(self.P[i], rec[i]["A"][l], rec[i]["Z"][l], J[i],
-                                              self.W[l - 1], self._relu(l), l > 1, o.gemm)
+                if o.model == "sage":
+                    G, Jf = layers.sage_backward(self.P[i], rec[i]["A"][l], rec[i]["X_in"][l], rec[i]["Z"][l], J[i],
+                                                 self.W[l - 1], self._relu(l), l > 1, o.gemm)
+                else:
+                    G, Jf = layers.layer_backward(self.P[i], rec[i]["A"][l], rec[i]["Z"][l], J[i],
+                                                  self.W[l - 1], self._relu(l), l > 1, o.gemm)
+                if Jf is not None:
+                    Jf = Jf * rec[i]["mask"][l]
                 rec[i]["G"][l] = G
                 G_sum[l - 1] = G if G_sum[l - 1] is None else G_sum[l - 1] + G
                 J_full[i] = Jf
@@ -209,14 +240,25 @@ class Simulation:
                 for i in range(self.nparts):
                     self.state[i].grad_buf[l] = self._gather_gradients(i, l, gsends)
 
-        # AllReduce (sum) and SGD
+        # AllReduce (sum) and the update
         for l in range(self.L):
-            self.W[l] = layers.sgd(self.W[l], G_sum[l], o.eta)
+            if o.optimizer == "adam":
+                self.W[l], self.adam_m[l], self.adam_v[l] = layers.adam(
+                    self.W[l], G_sum[l], self.adam_m[l], self.adam_v[l], t, o.eta, o.beta1, o.beta2, o.eps)
+            else:
+                self.W[l] = layers.sgd(self.W[l], G_sum[l], o.eta)
         for i in range(self.nparts):
             rec[i]["G_sum"] = [g.copy() for g in G_sum]
             rec[i]["W_out"] = [w.copy() for w in self.W]
             rec[i]["state_out"] = self.state[i].copy()
         return rec
+
+    def _dropped_input(self, i, l, t, H_inner, H_bd):
+        """Layer l's input of partition i after dropout, and the mask (ones without dropout)."""
+        o, p = self.opts, self.parts[i]
+        X = np.vstack([H_inner, H_bd])
+        mask = dropout_mask(X.shape[0], X.shape[1], o.dropout, o.seed, p.part, l, t)
+        return X * mask, mask
 
     def _gather_features(self, j, l, sends):
         """Boundary block of partition j owned by i is what i sent to j."""
@@ -253,12 +295,14 @@ def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: di
     are the messages of iteration t-1 (ignored at t = 1); ``ema_f`` / ``ema_g``
     are the smoothing states, updated in place when a message is consumed.
     Returns a record with the same keys as a Simulation record (A, Z, H, loss,
-    J_full, G, send_f) and the partition's weight gradients, without applying
-    the update.  Pipelined mode; ``ema_init`` "zero"; no boundary preload.
+    J_full, G, send_f, X_in, mask) and the partition's weight gradients,
+    without applying the update.  Pipelined mode; ``ema_init`` "zero"; no
+    boundary preload.  ``P`` must match ``opts.model`` (self loops for GCN).
     """
     o = opts
     L = len(W)
-    rec = dict(A={}, Z={}, H={}, J_full={}, G={}, send_f={})
+    sage = o.model == "sage"
+    rec = dict(A={}, Z={}, H={}, J_full={}, G={}, send_f={}, X_in={}, mask={})
     H = np.asarray(X_in, dtype=np.float64)
     for l in range(1, L + 1):
         rec["send_f"][l] = H[p.send_idx]
@@ -270,16 +314,28 @@ def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: di
         else:
             Hbd = np.zeros((p.n_bd, H.shape[1]))
         relu = l < L or o.relu_last
-        A, Z, H = layers.layer_forward(P, np.vstack([H, Hbd]), W[l - 1], relu, o.gemm)
+        X = np.vstack([H, Hbd])
+        mask = dropout_mask(X.shape[0], X.shape[1], o.dropout, o.seed, p.part, l, t)
+        X = X * mask
+        rec["X_in"][l], rec["mask"][l] = X[: p.n_inner], mask
+        if sage:
+            A, Z, H = layers.sage_forward(P, X, p.n_inner, W[l - 1], relu, o.gemm)
+        else:
+            A, Z, H = layers.layer_forward(P, X, W[l - 1], relu, o.gemm)
         rec["A"][l], rec["Z"][l], rec["H"][l] = A, Z, H
     f = layers.softmax_ce if o.loss == "softmax_ce" else layers.sigmoid_bce
     rec["loss"], J = f(H, y, o.loss_scale)
     for l in range(L, 0, -1):
         relu = l < L or o.relu_last
-        G, Jf = layers.layer_backward(P, rec["A"][l], rec["Z"][l], J, W[l - 1], relu, l > 1, o.gemm)
+        if sage:
+            G, Jf = layers.sage_backward(P, rec["A"][l], rec["X_in"][l], rec["Z"][l], J, W[l - 1], relu, l > 1,
+                                         o.gemm)
+        else:
+            G, Jf = layers.layer_backward(P, rec["A"][l], rec["Z"][l], J, W[l - 1], relu, l > 1, o.gemm)
         rec["G"][l] = G
         if l == 1:
             break
+        Jf = Jf * rec["mask"][l]
         if t > 1:
             C = received_g[l]
             if o.smooth_g:
