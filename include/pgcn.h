@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 100
+#define PGCN_VERSION 110
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -61,10 +61,15 @@ enum pgcn_status {
 enum pgcn_dtype { PGCN_F32 = 0, PGCN_BF16 = 1 };
 
 enum pgcn_setup_flags {
-  PGCN_SETUP_HOST_ONLY = 1  /* build the index structures on the host only: no
-                               device upload; compute calls on such a handle
-                               return PGCN_EINVAL (used to test the builder
-                               without a GPU) */
+  PGCN_SETUP_HOST_ONLY = 1,     /* build the index structures on the host only: no
+                                   device upload; compute calls on such a handle
+                                   return PGCN_EINVAL (used to test the builder
+                                   without a GPU) */
+  PGCN_SETUP_NO_SELF_LOOP = 2   /* P_i is the mean over N(v) without the self loop
+                                   (the GraphSAGE layer's aggregation, Section 2):
+                                   entries 1/d_v with d_v = degree; a row without
+                                   neighbours is zero.  The sets V_i, B_i, S_{i,j}
+                                   are unchanged. */
 };
 
 enum pgcn_pack_kind {
@@ -76,7 +81,8 @@ enum pgcn_loss_kind { PGCN_SOFTMAX_CE = 0, PGCN_SIGMOID_BCE = 1 };
 
 /* Global graph on the host.  Must be symmetric (u in N(v) <=> v in N(u)).
  * Duplicate entries and self loops are allowed and removed; exactly one
- * self loop per inner row is added (Ã = A + I, Appendix A.1). */
+ * self loop per inner row is added (Ã = A + I, Appendix A.1) unless the
+ * partition is built with PGCN_SETUP_NO_SELF_LOOP. */
 typedef struct {
   int64_t n;               /* global node count                     */
   const int64_t *rowptr;   /* [n+1], rowptr[0] == 0, non-decreasing */
@@ -96,7 +102,8 @@ typedef struct pgcn_partition pgcn_partition;
 typedef struct {
   int64_t n_inner;         /* |V_i|                                           */
   int64_t n_bd;            /* |B_i|                                           */
-  int64_t nnz;             /* non-zeros of P_i, one self loop per inner row   */
+  int64_t nnz;             /* non-zeros of P_i (with one self loop per inner row
+                              unless built with PGCN_SETUP_NO_SELF_LOOP)      */
   int64_t n_send;          /* sum_j |S_{i,j}|                                 */
   int64_t max_row_len;     /* longest row of P_i                              */
   int64_t max_row_len_t;   /* longest row of P_i^T                            */
@@ -248,6 +255,102 @@ int pgcn_loss_fwd_bwd(int32_t kind, const float *Z, int64_t rows, int32_t classe
 int pgcn_sgd_update(float *W, const float *G, const float *G_peer, int64_t count, float eta,
                     hipStream_t stream);
 
+/*
+ * Adam update after the AllReduce (the optimiser of the paper's experiments,
+ * its setup table; Kingma and Ba, ICLR 2015, Algorithm 1), element-wise for
+ * i < count, with g = G + G_peer (G_peer may be NULL):
+ *     m = beta1 m + (1 - beta1) g ;  v = beta2 v + (1 - beta2) g^2
+ *     W -= lr * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ * t >= 1 is the step count; m and v (caller-owned, zero before the first
+ * step) are updated in place.  The coefficients (beta, 1 - beta, the bias
+ * corrections) are computed on the host in double precision and rounded
+ * once to fp32; the element-wise update runs in fp32.
+ */
+int pgcn_adam_update(float *W, const float *G, const float *G_peer, float *m, float *v, int64_t count, double lr,
+                     double beta1, double beta2, double eps, int32_t t, hipStream_t stream);
+
+/*
+ * Dropout of a layer input, applied after the boundary receive with one mask
+ * for the forward and the backward (the paper's implementation notes; rates
+ * in its setup table).  For r < rows, c < cols, with global row R = row0 + r
+ * (the partition's local numbering: inner rows, then boundary rows at
+ * row0 = n_inner) and element index q = R * cols + c:
+ *     u = word (q mod 4) of Philox4x32-10(counter = (lo32(q / 4), hi32(q / 4),
+ *         layer, iteration), key = (seed, part))
+ *     out[r, c] = u < floor(p * 2^32) ? 0 : in[r, c] * (1 / (1 - p))
+ * Philox4x32-10 is the counter-based generator of Salmon, Moraes, Dror and
+ * Shaw (SC 2011).  The same call on a gradient (same arguments) applies the
+ * forward's mask in the backward.  in and out share stride ld (ld % 4 == 0,
+ * 16-byte aligned) and may alias.  out_bf16 (optional, stride ld_bf16,
+ * ld_bf16 % 8 == 0) receives out rounded to bf16 (nearest even).  0 <= p < 1.
+ */
+int pgcn_dropout(float *out, const float *in, int64_t rows, int32_t cols, int64_t ld, int64_t row0, double p,
+                 uint32_t seed, uint32_t part, uint32_t layer, uint32_t iteration, uint16_t *out_bf16,
+                 int64_t ld_bf16, hipStream_t stream);
+
+/*
+ * GraphSAGE layer forward (Section 2: the update function takes
+ * CONCAT(z_v, h_v); the model of the paper's experiments), on a partition
+ * built with PGCN_SETUP_NO_SELF_LOOP:
+ *     z = P_i [X_in ; X_bd]          (mean over N(v); stale boundary rows)
+ *     Z = [z, X_in] W ;  H_out = relu(Z) if relu else Z
+ * X_in / X_bd are the layer input after dropout (pgcn_dropout); X_bd NULL
+ * means all-zero boundary rows.  W is [2 f_in, f_out]: rows [0, f_in) act
+ * on z, rows [f_in, 2 f_in) on X_in.  The product is evaluated as z W_top
+ * followed by an accumulation of X_in W_bot (two passes over H_out).
+ * PGCN_F32: z -> A (required).  PGCN_BF16: z rounded once to bf16 -> A_bf16,
+ * and X_in_bf16 (the bf16 copy of X_in, e.g. from pgcn_dropout) is the
+ * self operand; W is rounded to bf16; fp32 accumulation.
+ * Workspace: pgcn_workspace_size(part, f_in, f_out, gemm_dtype).
+ */
+typedef struct {
+  int32_t f_in, f_out;
+  int32_t gemm_dtype;
+  int32_t relu;
+  int64_t ld_in, ld_out;       /* strides of X_in, X_bd, A, A_bf16, X_in_bf16 / of H_out */
+  const float *X_in;           /* [n_inner, ld_in]                               */
+  const uint16_t *X_in_bf16;   /* [n_inner, ld_in] (PGCN_BF16)                   */
+  const float *X_bd;           /* [n_bd, ld_in] or NULL                          */
+  const float *W;              /* [2 f_in, f_out]                                */
+  float *A;                    /* [n_inner, ld_in] out: z (PGCN_F32)             */
+  uint16_t *A_bf16;            /* [n_inner, ld_in] out: z in bf16 (PGCN_BF16)    */
+  float *H_out;                /* [n_inner, ld_out] out                          */
+  void *workspace;
+  size_t workspace_bytes;
+} pgcn_sage_fwd_args;
+int pgcn_sage_layer_fwd(const pgcn_partition *part, const pgcn_sage_fwd_args *args, hipStream_t stream);
+
+/*
+ * GraphSAGE layer backward (gradients of the forward above):
+ *     M        = J_out ∘ 1[H_out > 0] if relu else J_out
+ *     dW       = [z, X_in]^T M          (rows [0, f_in): z^T M; rows [f_in, 2 f_in): X_in^T M)
+ *     [dz, ds] = M W^T
+ *     J_full   = P_i^T dz, plus ds on the inner rows:
+ *                rows [0, n_inner) -> J_in, rows [n_inner, n_inner + n_bd) -> J_bd_out
+ * J_full is the gradient of the dropped input; apply the dropout mask to it
+ * with pgcn_dropout (same arguments as in the forward) before it is sent or
+ * accumulated.  J_in and J_bd_out are both NULL for the first layer.
+ */
+typedef struct {
+  int32_t f_in, f_out;
+  int32_t gemm_dtype;
+  int32_t relu;
+  int64_t ld_in, ld_out;
+  const float *J_out;          /* [n_inner, ld_out]                              */
+  const float *H_out;          /* [n_inner, ld_out] mask source (when relu)      */
+  const float *A;              /* [n_inner, ld_in] z (PGCN_F32)                  */
+  const uint16_t *A_bf16;      /* [n_inner, ld_in] z (PGCN_BF16)                 */
+  const float *X_in;           /* [n_inner, ld_in] (PGCN_F32)                    */
+  const uint16_t *X_in_bf16;   /* [n_inner, ld_in] (PGCN_BF16)                   */
+  const float *W;              /* [2 f_in, f_out]                                */
+  float *dW;                   /* [2 f_in, f_out] out                            */
+  float *J_in;                 /* [n_inner, ld_in] out or NULL                   */
+  float *J_bd_out;             /* [n_bd, ld_in] out or NULL                      */
+  void *workspace;
+  size_t workspace_bytes;
+} pgcn_sage_bwd_args;
+int pgcn_sage_layer_bwd(const pgcn_partition *part, const pgcn_sage_bwd_args *args, hipStream_t stream);
+
 /* Refill of a stale buffer (Algorithm 1's send/receive threads; the paper runs
  * them on a second stream): an asynchronous device-to-device copy of `bytes`
  * bytes enqueued on `stream`.  flags = 0: the runtime's copy (a blit kernel on
@@ -273,7 +376,7 @@ enum pgcn_trace_kind {
   PGCN_TK_AGG_FWD = 0, PGCN_TK_AGG_BWD = 1, PGCN_TK_AGG_FIXUP = 2, PGCN_TK_GEMM_FWD = 3,
   PGCN_TK_GEMM_DGRAD = 4, PGCN_TK_GEMM_WGRAD = 5, PGCN_TK_WGRAD_REDUCE = 6, PGCN_TK_EMA = 7,
   PGCN_TK_PACK = 8, PGCN_TK_ACCUM = 9, PGCN_TK_LOSS = 10, PGCN_TK_SGD = 11, PGCN_TK_REFILL = 12,
-  PGCN_TK_GEMM_PACK = 13
+  PGCN_TK_GEMM_PACK = 13, PGCN_TK_DROPOUT = 14, PGCN_TK_ADAM = 15
 };
 int pgcn_trace_enable(int32_t capacity);
 int pgcn_trace_filter(uint32_t kind_mask);

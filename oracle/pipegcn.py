@@ -164,6 +164,7 @@ class Simulation:
         t = self.t
         pipe = o.mode == "pipe"
         rec = [dict(t=t, W_in=[w.copy() for w in self.W], state_in=self.state[i].copy(),
+                    adam_in=([m.copy() for m in self.adam_m], [v.copy() for v in self.adam_v]),
                     A={}, Z={}, H={}, H_bd_used={}, C_used={}, J_full={}, G={}, X_in={}, mask={},
                     send_f={}, send_g={}) for i in range(self.nparts)]
         H_prev = [self.X[p.inner_gid] for p in self.parts]

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_PKG, "libpgcn.so")
 
 PGCN_OK, PGCN_EINVAL, PGCN_ENOMEM, PGCN_EHIP, PGCN_EUNSUPPORTED, PGCN_EWORKSPACE = range(6)
 PGCN_F32, PGCN_BF16 = 0, 1
-PGCN_SETUP_HOST_ONLY = 1
+PGCN_SETUP_HOST_ONLY, PGCN_SETUP_NO_SELF_LOOP = 1, 2
 PGCN_PACK_FEAT, PGCN_ACCUM_GRAD = 0, 1
 PGCN_SOFTMAX_CE, PGCN_SIGMOID_BCE = 0, 1
 PGCN_REFILL_DMA = 1
@@ -65,6 +65,19 @@ class pgcn_bwd_args(C.Structure):
                 ("workspace", _vp), ("workspace_bytes", _sz)]
 
 
+class pgcn_sage_fwd_args(C.Structure):
+    _fields_ = [("f_in", _i32), ("f_out", _i32), ("gemm_dtype", _i32), ("relu", _i32),
+                ("ld_in", _i64), ("ld_out", _i64), ("X_in", _vp), ("X_in_bf16", _vp), ("X_bd", _vp), ("W", _vp),
+                ("A", _vp), ("A_bf16", _vp), ("H_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz)]
+
+
+class pgcn_sage_bwd_args(C.Structure):
+    _fields_ = [("f_in", _i32), ("f_out", _i32), ("gemm_dtype", _i32), ("relu", _i32),
+                ("ld_in", _i64), ("ld_out", _i64), ("J_out", _vp), ("H_out", _vp), ("A", _vp),
+                ("A_bf16", _vp), ("X_in", _vp), ("X_in_bf16", _vp), ("W", _vp), ("dW", _vp), ("J_in", _vp),
+                ("J_bd_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz)]
+
+
 # every symbol include/pgcn.h declares, with its ctypes signature
 SIGNATURES = {
     "pgcn_partition_setup": (_i32, [C.POINTER(pgcn_csr), C.POINTER(pgcn_boundary_map), _u32, C.POINTER(_vp)]),
@@ -78,6 +91,12 @@ SIGNATURES = {
     "pgcn_pack_boundary": (_i32, [_vp, _i32, _vp, _vp, _i32, _i64, _vp]),
     "pgcn_loss_fwd_bwd": (_i32, [_i32, _vp, _i64, _i32, _i64, _vp, _vp, _i64, _f32, _vp, _vp, _vp, _sz, _vp]),
     "pgcn_sgd_update": (_i32, [_vp, _vp, _vp, _i64, _f32, _vp]),
+    "pgcn_adam_update": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, C.c_double, C.c_double, C.c_double, C.c_double,
+                                _i32, _vp]),
+    "pgcn_dropout": (_i32, [_vp, _vp, _i64, _i32, _i64, _i64, C.c_double, _u32, _u32, _u32, _u32, _vp, _i64,
+                            _vp]),
+    "pgcn_sage_layer_fwd": (_i32, [_vp, C.POINTER(pgcn_sage_fwd_args), _vp]),
+    "pgcn_sage_layer_bwd": (_i32, [_vp, C.POINTER(pgcn_sage_bwd_args), _vp]),
     "pgcn_refill_async": (_i32, [_vp, _vp, _sz, _u32, _vp]),
     "pgcn_trace_enable": (_i32, [_i32]),
     "pgcn_trace_filter": (_i32, [C.c_uint32]),
@@ -154,15 +173,15 @@ class Partition:
 
 
 def pgcn_partition_setup(n: int, rowptr: np.ndarray, col: np.ndarray, owner: np.ndarray,
-                         nparts: int, self_part: int, host_only: bool = False) -> Partition:
+                         nparts: int, self_part: int, host_only: bool = False, self_loop: bool = True) -> Partition:
     rowptr = np.ascontiguousarray(rowptr, dtype=np.int64)
     col = np.ascontiguousarray(col, dtype=np.int32)
     owner = np.ascontiguousarray(owner, dtype=np.int32)
     csr = pgcn_csr(n, rowptr.ctypes.data, col.ctypes.data if len(col) else None)
     bmap = pgcn_boundary_map(nparts, self_part, owner.ctypes.data)
     out = _vp()
-    _check(lib.pgcn_partition_setup(C.byref(csr), C.byref(bmap), PGCN_SETUP_HOST_ONLY if host_only else 0,
-                                    C.byref(out)), "pgcn_partition_setup")
+    flags = (PGCN_SETUP_HOST_ONLY if host_only else 0) | (0 if self_loop else PGCN_SETUP_NO_SELF_LOOP)
+    _check(lib.pgcn_partition_setup(C.byref(csr), C.byref(bmap), flags, C.byref(out)), "pgcn_partition_setup")
     return Partition(out.value)
 
 
@@ -225,12 +244,40 @@ def pgcn_sgd_update(W, G, G_peer, count: int, eta: float, stream=None):
     _check(lib.pgcn_sgd_update(_ptr(W), _ptr(G), _ptr(G_peer), count, eta, _stream(stream)), "pgcn_sgd_update")
 
 
+def pgcn_adam_update(W, G, G_peer, m, v, count: int, lr: float, beta1: float, beta2: float, eps: float, t: int,
+                     stream=None):
+    _check(lib.pgcn_adam_update(_ptr(W), _ptr(G), _ptr(G_peer), _ptr(m), _ptr(v), count, lr, beta1, beta2, eps, t,
+                                _stream(stream)), "pgcn_adam_update")
+
+
+def pgcn_dropout(out, inp, rows: int, cols: int, ld: int, row0: int, p: float, seed: int, part: int, layer: int,
+                 iteration: int, out_bf16=None, ld_bf16: int = 0, stream=None):
+    _check(lib.pgcn_dropout(_ptr(out), _ptr(inp), rows, cols, ld, row0, p, seed, part, layer, iteration,
+                            _ptr(out_bf16), ld_bf16, _stream(stream)), "pgcn_dropout")
+
+
+def pgcn_sage_layer_fwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, X_in, X_in_bf16, X_bd, W,
+                        A, A_bf16, H_out, workspace, workspace_bytes, stream=None):
+    a = pgcn_sage_fwd_args(f_in, f_out, gemm_dtype, int(relu), ld_in, ld_out, _ptr(X_in), _ptr(X_in_bf16),
+                           _ptr(X_bd), _ptr(W), _ptr(A), _ptr(A_bf16), _ptr(H_out), _ptr(workspace),
+                           workspace_bytes)
+    _check(lib.pgcn_sage_layer_fwd(part.handle, C.byref(a), _stream(stream)), "pgcn_sage_layer_fwd")
+
+
+def pgcn_sage_layer_bwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, J_out, H_out, A, A_bf16,
+                        X_in, X_in_bf16, W, dW, J_in, J_bd_out, workspace, workspace_bytes, stream=None):
+    a = pgcn_sage_bwd_args(f_in, f_out, gemm_dtype, int(relu), ld_in, ld_out, _ptr(J_out), _ptr(H_out), _ptr(A),
+                           _ptr(A_bf16), _ptr(X_in), _ptr(X_in_bf16), _ptr(W), _ptr(dW), _ptr(J_in),
+                           _ptr(J_bd_out), _ptr(workspace), workspace_bytes)
+    _check(lib.pgcn_sage_layer_bwd(part.handle, C.byref(a), _stream(stream)), "pgcn_sage_layer_bwd")
+
+
 def pgcn_refill_async(dst, src, nbytes: int, flags: int = 0, stream=None):
     _check(lib.pgcn_refill_async(_ptr(dst), _ptr(src), nbytes, flags, _stream(stream)), "pgcn_refill_async")
 
 
 TRACE_KINDS = ["agg_fwd", "agg_bwd", "agg_fixup", "gemm_fwd", "gemm_dgrad", "gemm_wgrad", "wgrad_reduce", "ema",
-               "pack", "accum", "loss", "sgd", "refill", "gemm_pack"]
+               "pack", "accum", "loss", "sgd", "refill", "gemm_pack", "dropout", "adam"]
 
 
 def pgcn_trace_enable(capacity: int):

@@ -28,6 +28,9 @@ class Workload:
     gamma: float = 0.95
     eta: float = 0.01
     seed: int = 0
+    # the experiments' GraphSAGE training (setup table): dropout rate and Adam learning rate
+    sage_dropout: float = 0.0
+    sage_lr: float = 0.01
 
     @property
     def layers(self) -> int:
@@ -47,22 +50,22 @@ class Workload:
 
 TINY = Workload(
     name="tiny-2k-2parts", widths=(32, 16, 8), loss="softmax_ce", gemm_dtype="f32",
-    n_global_labels=2000, graph_kind="tiny_uniform", graph_args=(2000, 10000, 2))
+    n_global_labels=2000, graph_kind="tiny_uniform", graph_args=(2000, 10000, 2), sage_dropout=0.3)
 
 REDDIT = Workload(
     name="reddit-like-1of4", widths=(602, 256, 256, 256, 41), loss="softmax_ce", gemm_dtype="f32",
     n_global_labels=233000, graph_kind="chung_lu",
-    graph_args=(58000, 30000, 4, 491.0, 26000.0, 2.3, 0.5, 1.07))
+    graph_args=(58000, 30000, 4, 491.0, 26000.0, 2.3, 0.5, 1.07), sage_dropout=0.5, sage_lr=0.01)
 
 PRODUCTS = Workload(
     name="products-like-1of8", widths=(100, 128, 128, 47), loss="softmax_ce", gemm_dtype="bf16",
     n_global_labels=2449000, graph_kind="chung_lu",
-    graph_args=(306000, 150000, 8, 51.0, 5000.0, 2.3, 0.7, 1.0))
+    graph_args=(306000, 150000, 8, 51.0, 5000.0, 2.3, 0.7, 1.0), sage_dropout=0.3, sage_lr=0.003)
 
 YELP = Workload(
     name="yelp-like-1of3", widths=(300, 512, 512, 512, 100), loss="sigmoid_bce", gemm_dtype="f32",
     n_global_labels=717000, graph_kind="er_hubs",
-    graph_args=(239000, 100000, 3, 19.0, 2000, 0.05, 0.6))
+    graph_args=(239000, 100000, 3, 19.0, 2000, 0.05, 0.6), sage_dropout=0.1, sage_lr=0.001)
 
 STRESS = Workload(
     name="stress-rmat-2M", widths=(128,) + (256,) * 7 + (64,), loss="softmax_ce", gemm_dtype="bf16",
@@ -104,15 +107,18 @@ def make_graph(w: Workload) -> synth.GlobalGraph:
 @dataclass
 class DenseInputs:
     X: np.ndarray                    # [n_global_or_local, f_0] features of every global node
-    W: list                          # Glorot weights per layer [f_{l-1}, f_l]
+    W: list                          # Glorot weights per layer [f_{l-1}, f_l] ([2 f_{l-1}, f_l] for GraphSAGE)
     labels: np.ndarray               # int32 [n] or float32 [n, C]
 
 
-def make_dense(w: Workload, n_nodes: int) -> DenseInputs:
-    """Features for every global node, initial weights and labels (all seeded)."""
+def make_dense(w: Workload, n_nodes: int, model: str = "gcn") -> DenseInputs:
+    """Features for every global node, initial weights and labels (all seeded).
+
+    GraphSAGE weights are [2 f_{l-1}, f_l] (they act on CONCAT(z, h))."""
     rx, rw, ry = synth.dense_streams(w.seed, 3)
     X = synth.features(rx, n_nodes, w.widths[0])
-    W = [synth.glorot_uniform(rw, w.widths[l], w.widths[l + 1]) for l in range(w.layers)]
+    k = 2 if model == "sage" else 1
+    W = [synth.glorot_uniform(rw, k * w.widths[l], w.widths[l + 1]) for l in range(w.layers)]
     if w.loss == "softmax_ce":
         y = synth.labels_single(ry, n_nodes, w.classes)
     else:

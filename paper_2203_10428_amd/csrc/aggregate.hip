@@ -63,6 +63,7 @@ struct AggParams {
   int32_t c4_cnt;         // float4 columns of this launch
   int32_t slices;         // S
   int32_t mode;           // AGG_FIRST | AGG_LAST
+  int32_t accum_lo;       // rows < out_split add to the output's previous content
   int64_t ld_in, ld_out, ld_bf16, ld_part;
   float *partials;
 };
@@ -86,11 +87,12 @@ __device__ __forceinline__ float *out_row(const AggParams &p, int64_t r) {
 }
 
 // Combine this chunk's sum of float4 column c4 of row r with the running sum
+// (or, with accum_lo, with what an inner row held before the first chunk)
 // and store it (scaled, padding zeroed, bf16 copy) when this is the last chunk.
 __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, float4 v) {
   const int c = 4 * c4;
   float *o = out_row(p, r);
-  if (!(p.mode & AGG_FIRST)) v = add4(v, *reinterpret_cast<const float4 *>(o + c));
+  if (!(p.mode & AGG_FIRST) || (p.accum_lo && r < p.out_split)) v = add4(v, *reinterpret_cast<const float4 *>(o + c));
   if (!(p.mode & AGG_LAST)) {
     *reinterpret_cast<float4 *>(o + c) = v;
     return;
@@ -355,6 +357,7 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
   p.ld_bf16 = a.ld_bf16;
   p.ld_part = (a.f + 3) / 4 * 4;
   p.partials = a.partials;
+  p.accum_lo = a.accum_lo;
   const int f4 = (a.f + 3) / 4;
   const int C = plan.chunks;
   if (f4 > kMaxAggF4) return set_error(PGCN_EINVAL, "aggregation: feature widths above 63,740 are not supported");

@@ -1,4 +1,5 @@
 // C ABI entry points of libpgcn: argument checking and kernel composition.
+#include <cmath>
 #include <cstring>
 
 #include "internal.h"
@@ -63,6 +64,7 @@ extern "C" size_t pgcn_workspace_size(const pgcn_partition *p, int32_t f_in, int
 extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, hipStream_t s) {
   int rc = check_part(p, "pgcn_layer_fwd");
   if (rc) return rc;
+  PGCN_REQUIRE(p->self_loop, "pgcn_layer_fwd: the GCN layer needs a partition built with self loops");
   PGCN_REQUIRE(a, "pgcn_layer_fwd: null args");
   PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_layer_fwd: widths must be >= 1");
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_layer_fwd: bad gemm_dtype");
@@ -129,6 +131,7 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
 extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, hipStream_t s) {
   int rc = check_part(p, "pgcn_layer_bwd");
   if (rc) return rc;
+  PGCN_REQUIRE(p->self_loop, "pgcn_layer_bwd: the GCN layer needs a partition built with self loops");
   PGCN_REQUIRE(a, "pgcn_layer_bwd: null args");
   PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_layer_bwd: widths must be >= 1");
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_layer_bwd: bad gemm_dtype");
@@ -218,6 +221,222 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   t.partials = partials;
   t.trace_kind = PGCN_TK_AGG_BWD;
   return launch_aggregate(t, s);
+}
+
+// ---------------------------------------------------------------- GraphSAGE ---
+
+extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_args *a, hipStream_t s) {
+  int rc = check_part(p, "pgcn_sage_layer_fwd");
+  if (rc) return rc;
+  PGCN_REQUIRE(!p->self_loop, "pgcn_sage_layer_fwd: the partition must be built with PGCN_SETUP_NO_SELF_LOOP");
+  PGCN_REQUIRE(a, "pgcn_sage_layer_fwd: null args");
+  PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_sage_layer_fwd: widths must be >= 1");
+  PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_sage_layer_fwd: bad gemm_dtype");
+  PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_sage_layer_fwd: ld_in must be >= f_in and a multiple of 4");
+  PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0,
+               "pgcn_sage_layer_fwd: ld_out must be >= f_out and a multiple of 4");
+  const bool bf16 = a->gemm_dtype == PGCN_BF16;
+  if (p->n_inner > 0) {
+    PGCN_REQUIRE(a->X_in && a->W && a->H_out, "pgcn_sage_layer_fwd: null X_in, W or H_out");
+    PGCN_REQUIRE(aligned16(a->X_in) && aligned16(a->X_bd), "pgcn_sage_layer_fwd: X_in/X_bd must be 16-byte aligned");
+    if (bf16) {
+      PGCN_REQUIRE(a->A_bf16 && a->X_in_bf16 && aligned16(a->A_bf16) && aligned16(a->X_in_bf16) && a->ld_in % 8 == 0,
+                   "pgcn_sage_layer_fwd: bf16 path needs A_bf16 and X_in_bf16 (16-byte aligned) and ld_in % 8 == 0");
+    } else {
+      PGCN_REQUIRE(a->A, "pgcn_sage_layer_fwd: fp32 path needs A");
+    }
+    PGCN_REQUIRE(!a->A || aligned16(a->A), "pgcn_sage_layer_fwd: A must be 16-byte aligned");
+  }
+  const size_t need = fwd_ws(p, a->f_in, a->f_out, a->gemm_dtype);
+  if (need > 0 && (!a->workspace || a->workspace_bytes < need))
+    return set_error(PGCN_EWORKSPACE, "pgcn_sage_layer_fwd: workspace too small");
+  if (p->n_inner == 0) return PGCN_OK;
+
+  // z = P_i [X_in ; X_bd] (mean over N(v))
+  AggArgs g{};
+  g.plan = &p->plan;
+  g.col = p->d_col;
+  g.in_split = p->n_inner;
+  g.in_lo = a->X_in;
+  g.in_hi = p->n_bd > 0 ? a->X_bd : nullptr;
+  g.out_split = p->n_inner;
+  g.out_lo = a->A;
+  g.out_bf16 = bf16 ? a->A_bf16 : nullptr;
+  g.scale = p->d_inv_deg;
+  g.f = a->f_in;
+  g.ld_in = a->ld_in;
+  g.ld_out = a->ld_in;
+  g.ld_bf16 = a->ld_in;
+  g.partials = (float *)a->workspace;
+  if (!a->A && p->plan.chunks > 1) {
+    g.out_lo = (float *)((char *)a->workspace + align_up(aggregate_workspace(p->plan, a->f_in), 256));
+    g.ld_out = ld4(a->f_in);
+  }
+  g.trace_kind = PGCN_TK_AGG_FWD;
+  rc = launch_aggregate(g, s);
+  if (rc) return rc;
+
+  // H_out = z W_top, then H_out = act(H_out + X_in W_bot)
+  GemmArgs m{};
+  m.M = (int32_t)p->n_inner;
+  m.N = a->f_out;
+  m.K = a->f_in;
+  m.dtype = a->gemm_dtype;
+  m.A = a->A;
+  m.A16 = a->A_bf16;
+  m.lda = a->ld_in;
+  m.B = a->W;
+  m.ldb = a->f_out;
+  m.C = a->H_out;
+  m.ldc = a->ld_out;
+  m.workspace = (float *)((char *)a->workspace + fwd_agg_bytes(p, a->f_in, a->gemm_dtype));
+  m.workspace_bytes = gemm_nk_workspace(a->f_out, a->f_in, a->gemm_dtype);
+  rc = launch_gemm_nk(Gemm::NN_PLAIN, m, s);
+  if (rc) return rc;
+  m.A = a->X_in;
+  m.A16 = a->X_in_bf16;
+  m.B = a->W + (size_t)a->f_in * a->f_out;
+  return launch_gemm_nk(a->relu ? Gemm::NN_ACC_RELU : Gemm::NN_ACC_PLAIN, m, s);
+}
+
+extern "C" int pgcn_sage_layer_bwd(const pgcn_partition *p, const pgcn_sage_bwd_args *a, hipStream_t s) {
+  int rc = check_part(p, "pgcn_sage_layer_bwd");
+  if (rc) return rc;
+  PGCN_REQUIRE(!p->self_loop, "pgcn_sage_layer_bwd: the partition must be built with PGCN_SETUP_NO_SELF_LOOP");
+  PGCN_REQUIRE(a, "pgcn_sage_layer_bwd: null args");
+  PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_sage_layer_bwd: widths must be >= 1");
+  PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_sage_layer_bwd: bad gemm_dtype");
+  PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_sage_layer_bwd: ld_in must be >= f_in and a multiple of 4");
+  PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0,
+               "pgcn_sage_layer_bwd: ld_out must be >= f_out and a multiple of 4");
+  const bool bf16 = a->gemm_dtype == PGCN_BF16;
+  const bool input_grad = a->J_in != nullptr || a->J_bd_out != nullptr;
+  PGCN_REQUIRE(a->dW, "pgcn_sage_layer_bwd: null dW");
+  if (input_grad) {
+    PGCN_REQUIRE(a->J_in && (a->J_bd_out || p->n_bd == 0),
+                 "pgcn_sage_layer_bwd: J_in and J_bd_out must both be given (or both NULL)");
+    PGCN_REQUIRE(aligned16(a->J_in) && aligned16(a->J_bd_out),
+                 "pgcn_sage_layer_bwd: J_in/J_bd_out must be 16-byte aligned");
+  }
+  if (p->n_inner > 0) {
+    PGCN_REQUIRE(a->J_out && a->W, "pgcn_sage_layer_bwd: null J_out or W");
+    PGCN_REQUIRE(!a->relu || a->H_out, "pgcn_sage_layer_bwd: relu needs H_out as mask source");
+    PGCN_REQUIRE(aligned16(a->J_out) && aligned16(a->H_out), "pgcn_sage_layer_bwd: J_out/H_out must be 16-byte aligned");
+    if (bf16)
+      PGCN_REQUIRE(a->A_bf16 && a->X_in_bf16 && aligned16(a->A_bf16) && aligned16(a->X_in_bf16) && a->ld_in % 8 == 0,
+                   "pgcn_sage_layer_bwd: bf16 path needs A_bf16 and X_in_bf16 (16-byte aligned) and ld_in % 8 == 0");
+    else
+      PGCN_REQUIRE(a->A && a->X_in && aligned16(a->A) && aligned16(a->X_in),
+                   "pgcn_sage_layer_bwd: fp32 path needs A and X_in (16-byte aligned)");
+  }
+  const size_t need = bwd_ws(p, a->f_in, a->f_out, input_grad, a->gemm_dtype);
+  if (need > 0 && (!a->workspace || a->workspace_bytes < need))
+    return set_error(PGCN_EWORKSPACE, "pgcn_sage_layer_bwd: workspace too small");
+
+  // dW = [z, X_in]^T (J ∘ 1[H > 0]): the two row blocks of dW; zero without inner rows
+  const size_t half = (size_t)a->f_in * a->f_out;
+  GemmArgs g{};
+  g.M = a->f_in;
+  g.N = a->f_out;
+  g.K = (int32_t)p->n_inner;
+  g.dtype = a->gemm_dtype;
+  g.A = a->A;
+  g.A16 = a->A_bf16;
+  g.lda = a->ld_in;
+  g.B = a->J_out;
+  g.ldb = a->ld_out;
+  g.Hmask = a->relu ? a->H_out : nullptr;
+  g.ldm = a->ld_out;
+  g.C = a->dW;
+  g.ldc = a->f_out;
+  g.workspace = (float *)a->workspace;
+  g.workspace_bytes = a->workspace_bytes;
+  rc = launch_gemm(Gemm::TN_MASK_SPLITK, g, s);
+  if (rc) return rc;
+  g.A = a->X_in;
+  g.A16 = a->X_in_bf16;
+  g.C = a->dW + half;
+  rc = launch_gemm(Gemm::TN_MASK_SPLITK, g, s);
+  if (rc) return rc;
+  if (!input_grad || p->n_inner == 0) return PGCN_OK;
+
+  // J_in = (J ∘ 1[H > 0]) W_bot^T (the self term), D = diag(1/d) ((J ∘ 1[H > 0]) W_top^T),
+  // then J_full = (P_i^T without the scale) D, added to the inner rows
+  const int64_t ld_d = ld4(a->f_in);
+  float *D = (float *)a->workspace;
+  float *partials = (float *)((char *)a->workspace + align_up((size_t)p->n_inner * ld_d * sizeof(float), 256));
+  GemmArgs d{};
+  d.M = (int32_t)p->n_inner;
+  d.N = a->f_in;
+  d.K = a->f_out;
+  d.dtype = a->gemm_dtype;
+  d.A = a->J_out;
+  d.lda = a->ld_out;
+  d.Hmask = a->relu ? a->H_out : nullptr;
+  d.ldm = a->ld_out;
+  d.B = a->W + half;
+  d.ldb = a->f_out;
+  d.C = a->J_in;
+  d.ldc = a->ld_in;
+  d.workspace = (float *)((char *)a->workspace + bwd_region0(p, a->f_in, a->f_out, input_grad));
+  d.workspace_bytes = gemm_nk_workspace(a->f_in, a->f_out, a->gemm_dtype);
+  rc = launch_gemm_nk(Gemm::MASK_NT_PLAIN, d, s);
+  if (rc) return rc;
+  d.B = a->W;
+  d.C = D;
+  d.ldc = ld_d;
+  d.rowscale = p->d_inv_deg;
+  rc = launch_gemm_nk(Gemm::MASK_NT_ROWSCALE, d, s);
+  if (rc) return rc;
+
+  AggArgs t{};
+  t.plan = &p->plan_t;
+  t.col = p->d_col_t;
+  t.in_split = p->n_inner;
+  t.in_lo = D;
+  t.out_split = p->n_inner;
+  t.out_lo = a->J_in;
+  t.out_hi = a->J_bd_out;
+  t.f = a->f_in;
+  t.ld_in = ld_d;
+  t.ld_out = a->ld_in;
+  t.partials = partials;
+  t.trace_kind = PGCN_TK_AGG_BWD;
+  t.accum_lo = 1;
+  return launch_aggregate(t, s);
+}
+
+extern "C" int pgcn_dropout(float *out, const float *in, int64_t rows, int32_t cols, int64_t ld, int64_t row0,
+                            double p, uint32_t seed, uint32_t part, uint32_t layer, uint32_t iteration,
+                            uint16_t *out_bf16, int64_t ld_bf16, hipStream_t s) {
+  PGCN_REQUIRE(rows >= 0 && cols >= 0 && ld >= cols && ld % 4 == 0 && row0 >= 0, "pgcn_dropout: bad shape or stride");
+  PGCN_REQUIRE(p >= 0.0 && p < 1.0, "pgcn_dropout: p must be in [0, 1)");
+  if (rows == 0 || cols == 0) return PGCN_OK;
+  PGCN_REQUIRE(out && in && aligned16(out) && aligned16(in), "pgcn_dropout: null or unaligned buffer");
+  PGCN_REQUIRE(!out_bf16 || (aligned16(out_bf16) && ld_bf16 >= ld4(cols) && ld_bf16 % 8 == 0),
+               "pgcn_dropout: out_bf16 needs 16-byte alignment and ld_bf16 % 8 == 0, >= cols");
+  const double t = std::floor(p * 4294967296.0);
+  const uint32_t thr = t >= 4294967295.0 ? 0xffffffffu : (uint32_t)t;
+  const float scale = (float)(1.0 / (1.0 - p));
+  return launch_dropout(out, in, rows, cols, ld, row0, thr, scale, seed, part, layer, iteration, out_bf16, ld_bf16, s);
+}
+
+extern "C" int pgcn_adam_update(float *W, const float *G, const float *G_peer, float *m, float *v, int64_t count,
+                                double lr, double beta1, double beta2, double eps, int32_t t, hipStream_t s) {
+  PGCN_REQUIRE(count >= 0 && t >= 1, "pgcn_adam_update: count must be >= 0 and t >= 1");
+  PGCN_REQUIRE(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0, "pgcn_adam_update: betas must be in [0, 1)");
+  if (count == 0) return PGCN_OK;
+  PGCN_REQUIRE(W && G && m && v, "pgcn_adam_update: null buffer");
+  AdamCoef c;
+  c.lr = (float)lr;
+  c.eps = (float)eps;
+  c.b1 = (float)beta1;
+  c.b2 = (float)beta2;
+  c.omb1 = (float)(1.0 - beta1);
+  c.omb2 = (float)(1.0 - beta2);
+  c.c1 = (float)(1.0 / (1.0 - std::pow(beta1, (double)t)));
+  c.c2 = (float)(1.0 / (1.0 - std::pow(beta2, (double)t)));
+  return launch_adam(W, G, G_peer, m, v, count, c, s);
 }
 
 extern "C" int pgcn_smooth_ema(float *state, const float *incoming, int64_t rows, int32_t cols, int64_t ld,

@@ -6,6 +6,10 @@
 //   - softmax cross-entropy / sigmoid BCE with their logit gradients
 //     (Algorithm 1's J^(L)), with a fixed-order loss reduction;
 //   - the SGD update (Algorithm 1's last line).
+//   - dropout of a layer input with a Philox4x32-10 mask (after the boundary
+//     receive, one mask for the forward and the backward: the paper's
+//     implementation notes);
+//   - the Adam update (the optimiser of the paper's experiments).
 // All are float4-vectorised over the feature dimension; no float atomics.
 #include "internal.h"
 
@@ -210,6 +214,109 @@ int launch_sgd(float *W, const float *G, const float *G2, int64_t count, float e
   if (count == 0) return PGCN_OK;
   TraceScope ts(PGCN_TK_SGD, s);
   hipLaunchKernelGGL(sgd_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, W, G, G2, count, eta);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
+}
+
+// float -> bf16 bits, round to nearest even (NaN stays a quiet NaN)
+__device__ __forceinline__ uint16_t f32_to_bf16(float x) {
+  uint32_t b = __float_as_uint(x);
+  if ((b & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((b >> 16) | 0x40u);
+  b += 0x7fffu + ((b >> 16) & 1u);
+  return (uint16_t)(b >> 16);
+}
+
+// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC 2011): ten rounds of
+// (c0, c1, c2, c3) <- (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0))
+// with the key advanced by the Weyl constants after every round.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    c = make_uint4((uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c.w ^ k1, (uint32_t)p0);
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+__device__ __forceinline__ uint32_t word_of(const uint4 &a, int i) {
+  return i == 0 ? a.x : i == 1 ? a.y : i == 2 ? a.z : a.w;
+}
+
+// Element q = (row0 + r) * cols + c is dropped when word q % 4 of
+// Philox(counter = (q / 4 low, q / 4 high, layer, iteration), key = (seed, part))
+// is below thr; kept elements are scaled.  Padding columns are written as 0.
+__global__ __launch_bounds__(256) void dropout_kernel(float *out, const float *in, int64_t rows, int f4, int cols,
+                                                      int64_t ld, int64_t row0, uint32_t thr, float scale,
+                                                      uint32_t seed, uint32_t part, uint32_t layer, uint32_t iter,
+                                                      uint16_t *out16, int64_t ld16, int sh) {
+  const int64_t r = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
+  if (r >= rows) return;
+  for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) {
+    const int c = 4 * c4;
+    const float4 x = *reinterpret_cast<const float4 *>(in + r * ld + c);
+    float v[4] = {x.x, x.y, x.z, x.w};
+    if (thr != 0u) {
+      const uint64_t q0 = (uint64_t)(row0 + r) * (uint64_t)cols + (uint64_t)c;
+      const uint64_t g = q0 >> 2;
+      const int w0 = (int)(q0 & 3u);
+      const uint4 a = philox4x32_10(make_uint4((uint32_t)g, (uint32_t)(g >> 32), layer, iter), seed, part);
+      uint4 b = a;
+      if (w0 != 0)
+        b = philox4x32_10(make_uint4((uint32_t)(g + 1), (uint32_t)((g + 1) >> 32), layer, iter), seed, part);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = w0 + e;
+        const uint32_t u = i < 4 ? word_of(a, i) : word_of(b, i - 4);
+        v[e] = u < thr ? 0.f : v[e] * scale;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (c + e >= cols) v[e] = 0.f;
+    *reinterpret_cast<float4 *>(out + r * ld + c) = make_float4(v[0], v[1], v[2], v[3]);
+    if (out16) {
+      uint2 w;
+      w.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+      w.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+      *reinterpret_cast<uint2 *>(out16 + r * ld16 + c) = w;
+    }
+  }
+}
+
+int launch_dropout(float *out, const float *in, int64_t rows, int32_t cols, int64_t ld, int64_t row0, uint32_t thr,
+                   float scale, uint32_t seed, uint32_t part, uint32_t layer, uint32_t iteration, uint16_t *out16,
+                   int64_t ld16, hipStream_t s) {
+  const int f4 = (cols + 3) / 4;
+  if (rows == 0 || f4 == 0) return PGCN_OK;
+  const int sh = lane_shift(f4);
+  TraceScope ts(PGCN_TK_DROPOUT, s);
+  hipLaunchKernelGGL(dropout_kernel, dim3(row_blocks(rows, sh)), dim3(256), 0, s, out, in, rows, f4, cols, ld, row0,
+                     thr, scale, seed, part, layer, iteration, out16, ld16, sh);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
+}
+
+// Adam (Kingma and Ba, Algorithm 1) with host-computed coefficients.
+__global__ __launch_bounds__(256) void adam_kernel(float *W, const float *G, const float *Gp, float *m, float *v,
+                                                   int64_t count, AdamCoef c) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= count) return;
+  const float g = Gp ? G[i] + Gp[i] : G[i];
+  const float mi = c.b1 * m[i] + c.omb1 * g;
+  const float vi = c.b2 * v[i] + c.omb2 * (g * g);
+  m[i] = mi;
+  v[i] = vi;
+  W[i] -= c.lr * (mi * c.c1) / (sqrtf(vi * c.c2) + c.eps);
+}
+
+int launch_adam(float *W, const float *G, const float *Gp, float *m, float *v, int64_t count, const AdamCoef &c,
+                hipStream_t s) {
+  if (count == 0) return PGCN_OK;
+  TraceScope ts(PGCN_TK_ADAM, s);
+  hipLaunchKernelGGL(adam_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, W, G, Gp, m, v, count, c);
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;
 }

@@ -2,6 +2,9 @@
 // with M = inner rows:
 //   forward       Z = A W,                         A = aggregated features, B(n,k) = W[k][n]
 //   feature grad  D = diag(1/d) ((J ∘ 1[H>0]) W^T), A = masked gradient,     B(n,k) = W[n][k]
+// The GraphSAGE layer (Section 2's CONCAT update) uses the same kernels on
+// the two halves of its weights: Z = z W_top, then Z = relu(Z + X W_bot)
+// (accumulating epilogue), and the feature gradient without the row scale.
 //
 // The right operand (the layer's weights, at most a few MB) is first packed
 // once per call into an n-major, k-contiguous matrix zero-padded to a 128-row
@@ -48,7 +51,7 @@ struct NKParams {
 };
 
 enum NKA { NK_A_F32, NK_A_BF16, NK_A_MASK };
-enum NKE { NK_E_RELU, NK_E_PLAIN, NK_E_ROWSCALE };
+enum NKE { NK_E_RELU, NK_E_PLAIN, NK_E_ROWSCALE, NK_E_ACC_RELU, NK_E_ACC_PLAIN };
 
 __device__ __forceinline__ uint16_t nk_bf16(float x) {
   uint32_t b = __float_as_uint(x);
@@ -68,7 +71,11 @@ __device__ __forceinline__ void nk_store(const NKParams &p, int row, int col, fl
   float *c = p.C + (int64_t)row * p.ldc + col;
   if (EK == NK_E_RELU) *c = v > 0.f ? v : 0.f;
   else if (EK == NK_E_PLAIN) *c = v;
-  else *c = v * p.rowscale[row];
+  else if (EK == NK_E_ROWSCALE) *c = v * p.rowscale[row];
+  else {                                               // accumulate onto C, then the activation
+    const float u = *c + v;
+    *c = (EK == NK_E_ACC_RELU && u <= 0.f) ? 0.f : u;
+  }
 }
 
 // out[n][k] = (n < N && k < K) ? (trans ? W[k*ldw + n] : W[n*ldw + k]) : 0, for n < rows, k < ldk
@@ -344,8 +351,8 @@ static void nk_launch_bn(const NKParams &p, bool bf16, hipStream_t s) {
   else nk_launch<128, AK, EK>(p, bf16, s);
 }
 
-// kind: NN_RELU / NN_PLAIN (forward: B(n,k) = W[k][n]) or MASK_NT_ROWSCALE
-// (feature gradient: B(n,k) = W[n][k]); g.workspace holds the packed weights.
+// kind: NN_* (forward: B(n,k) = W[k][n]) or MASK_NT_* (feature gradient:
+// B(n,k) = W[n][k]); g.workspace holds the packed weights.
 int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return PGCN_OK;
   const bool bf16 = g.dtype == PGCN_BF16;
@@ -353,7 +360,8 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
   if (!g.workspace || g.workspace_bytes < need)
     return set_error(PGCN_EWORKSPACE, "update GEMM: workspace too small for the packed weights");
   const int rows = (int)nk_rows(g.N), ldk = (int)nk_ldk(g.K);
-  const bool fwd = kind == Gemm::NN_RELU || kind == Gemm::NN_PLAIN;
+  const bool fwd = kind == Gemm::NN_RELU || kind == Gemm::NN_PLAIN || kind == Gemm::NN_ACC_RELU ||
+                   kind == Gemm::NN_ACC_PLAIN;
   {
     TraceScope ts(PGCN_TK_GEMM_PACK, s);
     const unsigned blocks = (unsigned)(((int64_t)rows * ldk + 255) / 256);
@@ -380,9 +388,15 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
   p.ldc = g.ldc;
   p.rowscale = g.rowscale;
   TraceScope ts(fwd ? PGCN_TK_GEMM_FWD : PGCN_TK_GEMM_DGRAD, s);
-  if (kind == Gemm::NN_RELU) nk_launch_bn<NK_A_F32, NK_E_RELU>(p, bf16, s);
-  else if (kind == Gemm::NN_PLAIN) nk_launch_bn<NK_A_F32, NK_E_PLAIN>(p, bf16, s);
-  else nk_launch_bn<NK_A_MASK, NK_E_ROWSCALE>(p, bf16, s);
+  switch (kind) {
+    case Gemm::NN_RELU: nk_launch_bn<NK_A_F32, NK_E_RELU>(p, bf16, s); break;
+    case Gemm::NN_PLAIN: nk_launch_bn<NK_A_F32, NK_E_PLAIN>(p, bf16, s); break;
+    case Gemm::NN_ACC_RELU: nk_launch_bn<NK_A_F32, NK_E_ACC_RELU>(p, bf16, s); break;
+    case Gemm::NN_ACC_PLAIN: nk_launch_bn<NK_A_F32, NK_E_ACC_PLAIN>(p, bf16, s); break;
+    case Gemm::MASK_NT_ROWSCALE: nk_launch_bn<NK_A_MASK, NK_E_ROWSCALE>(p, bf16, s); break;
+    case Gemm::MASK_NT_PLAIN: nk_launch_bn<NK_A_MASK, NK_E_PLAIN>(p, bf16, s); break;
+    default: return set_error(PGCN_EINVAL, "launch_gemm_nk: not a node-major GEMM");
+  }
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;
 }

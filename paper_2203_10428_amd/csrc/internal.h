@@ -48,7 +48,7 @@ struct Plan {
 }  // namespace pgcn
 
 struct pgcn_partition {
-  int32_t nparts = 0, self = 0, host_only = 0, segment = 0;
+  int32_t nparts = 0, self = 0, host_only = 0, segment = 0, self_loop = 1;
   int64_t n_inner = 0, n_bd = 0, nnz = 0, n_send = 0;
   int64_t max_row = 0, max_row_t = 0;
   int device = -1;
@@ -114,11 +114,14 @@ struct AggArgs {
   int64_t ld_in, ld_out, ld_bf16;
   float *partials;
   int32_t trace_kind;      // PGCN_TK_AGG_FWD or PGCN_TK_AGG_BWD
+  int32_t accum_lo;        // 1: rows [0, out_split) add to what out_lo holds (GraphSAGE self term)
 };
 int launch_aggregate(const AggArgs &a, hipStream_t s);
 size_t aggregate_workspace(const Plan &plan, int64_t f);
 
-enum class Gemm { NN_RELU, NN_PLAIN, MASK_NT_ROWSCALE, TN_MASK_SPLITK };
+// NN_*: C (=|+=) A W, with ReLU for *_RELU (ACC: C = act(C + A W));
+// MASK_NT_*: C = (J ∘ mask) W^T, row-scaled or plain; TN_MASK_SPLITK: C = A^T (J ∘ mask)
+enum class Gemm { NN_RELU, NN_PLAIN, NN_ACC_RELU, NN_ACC_PLAIN, MASK_NT_ROWSCALE, MASK_NT_PLAIN, TN_MASK_SPLITK };
 struct GemmArgs {
   int32_t M, N, K;
   int32_t dtype;            // PGCN_F32 / PGCN_BF16
@@ -143,6 +146,15 @@ size_t gemm_nk_workspace(int32_t N, int32_t K, int32_t dtype);
 
 int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_t ld, float gamma,
                hipStream_t s);
+int launch_dropout(float *out, const float *in, int64_t rows, int32_t cols, int64_t ld, int64_t row0, uint32_t thr,
+                   float scale, uint32_t seed, uint32_t part, uint32_t layer, uint32_t iteration, uint16_t *out16,
+                   int64_t ld16, hipStream_t s);
+// Adam coefficients, each computed in double on the host and rounded once
+struct AdamCoef {
+  float lr, eps, b1, b2, omb1, omb2, c1, c2;   // omb = 1 - beta; c = 1 / (1 - beta^t)
+};
+int launch_adam(float *W, const float *G, const float *Gp, float *m, float *v, int64_t count, const AdamCoef &c,
+                hipStream_t s);
 int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst, int32_t cols,
                 int64_t ld, hipStream_t s);
 int launch_accum(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, const float *src,

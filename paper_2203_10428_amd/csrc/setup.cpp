@@ -236,12 +236,14 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
   for (int64_t g : p->bd_gid) p->recv_ptr[owner[g] + 1]++;
   for (int32_t j = 0; j < nparts; ++j) p->recv_ptr[j + 1] += p->recv_ptr[j];
 
-  // P_i: N(v) ∪ {v}, ascending local id
+  // P_i: N(v) ∪ {v} (N(v) alone for the GraphSAGE aggregation), ascending local id
+  const bool self_loop = !(flags & PGCN_SETUP_NO_SELF_LOOP);
+  p->self_loop = self_loop ? 1 : 0;
   p->rowptr.assign(n_in + 1, 0);
   p->col.reserve(nb.size() + n_in);
   for (int64_t i = 0; i < n_in; ++i) {
     size_t start = p->col.size();
-    p->col.push_back((int32_t)i);
+    if (self_loop) p->col.push_back((int32_t)i);
     for (int64_t k = nb_ptr[i]; k < nb_ptr[i + 1]; ++k) p->col.push_back((int32_t)local_of[nb[k]]);
     std::sort(p->col.begin() + start, p->col.end());
     p->rowptr[i + 1] = (int64_t)p->col.size();
@@ -251,7 +253,7 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
   p->inv_deg.resize(n_in);
   for (int64_t i = 0; i < n_in; ++i) {
     int64_t len = p->rowptr[i + 1] - p->rowptr[i];
-    p->inv_deg[i] = 1.0f / (float)len;
+    p->inv_deg[i] = len > 0 ? 1.0f / (float)len : 0.0f;     // a row without neighbours is zero
     p->max_row = std::max(p->max_row, len);
   }
 

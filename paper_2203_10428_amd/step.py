@@ -20,6 +20,14 @@ second stream, as here).  Copy modes for measurement:
 Smoothing (Section 3.4): ``smooth_f`` and ``smooth_g`` keep a moving average
 of the received boundary features / gradients, updated when a message is
 consumed (iteration 2 on), starting from zero.
+
+Model: ``"gcn"`` (Algorithm 1's layer) or ``"sage"`` (the experiments'
+GraphSAGE layer, Section 2's CONCAT update; the partition is built without
+self loops).  ``dropout`` p drops each layer's whole input after the receive
+and smoothing, and the same mask multiplies the input gradient before it is
+sent or accumulated (the paper's implementation notes); the mask comes from
+the library's counter-based generator keyed by (``seed``, partition) and
+counted by (layer, iteration).  ``optimizer``: Algorithm 1's SGD or Adam.
 """
 from __future__ import annotations
 
@@ -45,6 +53,13 @@ class StepOptions:
     relu_last: bool = False
     copy_mode: str = "pipe"          # "pipe" | "serial" | "none"
     refill_dma: bool = False         # refills by the DMA engines instead of a blit kernel
+    model: str = "gcn"               # "gcn" | "sage"
+    dropout: float = 0.0
+    seed: int = 0
+    optimizer: str = "sgd"           # "sgd" | "adam" (learning rate eta)
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
 
 
 class PartitionTrainer:
@@ -60,9 +75,11 @@ class PartitionTrainer:
         self.loss_kind = B.PGCN_SOFTMAX_CE if loss == "softmax_ce" else B.PGCN_SIGMOID_BCE
         self.loss_scale = float(loss_scale)
         self.dtype = B.PGCN_BF16 if gemm_dtype == "bf16" else B.PGCN_F32
+        self.sage = opts.model == "sage"
+        self.self_part = graph.self_part
         with torch.cuda.device(self.dev):
             self.part = B.pgcn_partition_setup(graph.n, graph.rowptr, graph.col, graph.owner, graph.nparts,
-                                               graph.self_part)
+                                               graph.self_part, self_loop=not self.sage)
         self.info = B.pgcn_partition_info(self.part)
         n, b, s = self.info["n_inner"], self.info["n_bd"], self.info["n_send"]
         self.n, self.b, self.s = n, b, s
@@ -84,7 +101,18 @@ class PartitionTrainer:
             self.targets = z(n, wd[-1])
             self.targets[:, : wd[-1]] = torch.from_numpy(labels_global[self.inner_gid]).to(self.dev)
         self.W = [torch.from_numpy(np.ascontiguousarray(w, dtype=np.float32)).to(self.dev) for w in W0]
+        k = 2 if self.sage else 1
+        for l, w in enumerate(self.W):
+            assert tuple(w.shape) == (k * wd[l], wd[l + 1]), (l, tuple(w.shape))
         self.dW = [torch.zeros_like(w) for w in self.W]
+        self.adam_m = [torch.zeros_like(w) for w in self.W] if opts.optimizer == "adam" else None
+        self.adam_v = [torch.zeros_like(w) for w in self.W] if opts.optimizer == "adam" else None
+        # dropped layer inputs (dropout, or the bf16 copy of the GraphSAGE self operand)
+        self.use_drop = opts.dropout > 0.0 or (self.sage and not f32)
+        self.Xd_in = {l: z(n, wd[l - 1]) for l in range(1, L + 1)} if self.use_drop else {}
+        self.Xd_bd = {l: z(b, wd[l - 1]) for l in range(1, L + 1)} if self.use_drop else {}
+        self.Xd_16 = {l: z(n, wd[l - 1], torch.bfloat16) for l in range(1, L + 1)} \
+            if (self.sage and not f32) else {}
         self.G_peer = [None] * L
         # activations, indexed by layer 1..L
         self.A = {l: (z(n, wd[l - 1]) if f32 else None) for l in range(1, L + 1)}
@@ -107,6 +135,7 @@ class PartitionTrainer:
             self.remote_f[l][:, : wd[l - 1]] = torch.randn((b, wd[l - 1]), generator=g).to(self.dev)
         for l in range(2, L + 1):
             self.remote_g[l][:, : wd[l - 1]] = (1e-3 * torch.randn((s, wd[l - 1]), generator=g)).to(self.dev)
+        self.X_used = {}                  # layer input the forward used (the GraphSAGE self operand)
         self.cur = 0                      # index of the buffer read in this iteration
         self.t = 0
         self.loss = torch.zeros(1, dtype=torch.float32, device=self.dev)
@@ -128,6 +157,46 @@ class PartitionTrainer:
     def _refill(self, dst, src, stream):
         B.pgcn_refill_async(dst, src, dst.numel() * dst.element_size(),
                             B.PGCN_REFILL_DMA if self.opts.refill_dma else 0, stream)
+
+    def _dropout(self, out, inp, rows, l, row0, out16, st):
+        o, f = self.opts, self.widths[l - 1]
+        B.pgcn_dropout(out, inp, rows, f, ld_of(f), row0, o.dropout, o.seed, self.self_part, l, self.t, out16,
+                       ld_of(f) if out16 is not None else 0, st)
+
+    def _forward_layer(self, l, H_in, H_bd, st):
+        """Dropout of the layer input (after the receive), then the GCN or GraphSAGE layer."""
+        wd, f = self.widths, self.widths[l - 1]
+        X_in, X_bd, X16 = H_in, H_bd, None
+        if self.use_drop:
+            X16 = self.Xd_16.get(l)
+            self._dropout(self.Xd_in[l], H_in, self.n, l, 0, X16, st)
+            X_in = self.Xd_in[l]
+            if H_bd is not None:
+                self._dropout(self.Xd_bd[l], H_bd, self.b, l, self.n, None, st)
+                X_bd = self.Xd_bd[l]
+        common = dict(f_in=f, f_out=wd[l], gemm_dtype=self.dtype, relu=self._relu(l), ld_in=ld_of(f),
+                      ld_out=ld_of(wd[l]), W=self.W[l - 1], A=self.A[l], A_bf16=self.A16[l], H_out=self.H[l],
+                      workspace=self.ws, workspace_bytes=self.ws_bytes, stream=st)
+        if self.sage:
+            B.pgcn_sage_layer_fwd(self.part, X_in=X_in, X_in_bf16=X16, X_bd=X_bd, **common)
+        else:
+            B.pgcn_layer_fwd(self.part, H_in=X_in, H_bd=X_bd, **common)
+        self.X_used[l] = X_in
+
+    def _backward_layer(self, l, J_out, st):
+        """Layer gradients; the input gradient then takes the forward's dropout mask."""
+        wd, f = self.widths, self.widths[l - 1]
+        common = dict(f_in=f, f_out=wd[l], gemm_dtype=self.dtype, relu=self._relu(l), ld_in=ld_of(f),
+                      ld_out=ld_of(wd[l]), J_out=J_out, H_out=self.H[l], A=self.A[l], A_bf16=self.A16[l],
+                      W=self.W[l - 1], dW=self.dW[l - 1], J_in=self.J_in.get(l), J_bd_out=self.J_bd_out.get(l),
+                      workspace=self.ws, workspace_bytes=self.ws_bytes, stream=st)
+        if self.sage:
+            B.pgcn_sage_layer_bwd(self.part, X_in=self.X_used[l], X_in_bf16=self.Xd_16.get(l), **common)
+        else:
+            B.pgcn_layer_bwd(self.part, **common)
+        if l > 1 and self.opts.dropout > 0.0:
+            self._dropout(self.J_in[l], self.J_in[l], self.n, l, 0, None, st)
+            self._dropout(self.J_bd_out[l], self.J_bd_out[l], self.b, l, self.n, None, st)
 
     def step(self):
         o, L, wd = self.opts, self.L, self.widths
@@ -160,10 +229,7 @@ class PartitionTrainer:
                 side.wait_event(self.ev_pack[l])
                 self._refill(self.feat[l][nxt], self.remote_f[l], side)
                 self.ev_feat[l].record(side)
-            B.pgcn_layer_fwd(self.part, f_in=f, f_out=wd[l], gemm_dtype=self.dtype, relu=self._relu(l),
-                             ld_in=ld_of(f), ld_out=ld_of(wd[l]), H_in=H_in, H_bd=H_bd, W=self.W[l - 1],
-                             A=self.A[l], A_bf16=self.A16[l], H_out=self.H[l], workspace=self.ws,
-                             workspace_bytes=self.ws_bytes, stream=st)
+            self._forward_layer(l, H_in, H_bd, st)
 
         # ---- loss -----------------------------------------------------
         C_ = wd[L]
@@ -174,11 +240,7 @@ class PartitionTrainer:
         for l in range(L, 0, -1):
             f = wd[l - 1]
             J_out = self.J_top if l == L else self.J_in[l + 1]
-            B.pgcn_layer_bwd(self.part, f_in=f, f_out=wd[l], gemm_dtype=self.dtype, relu=self._relu(l),
-                             ld_in=ld_of(f), ld_out=ld_of(wd[l]), J_out=J_out, H_out=self.H[l], A=self.A[l],
-                             A_bf16=self.A16[l], W=self.W[l - 1], dW=self.dW[l - 1],
-                             J_in=self.J_in.get(l), J_bd_out=self.J_bd_out.get(l), workspace=self.ws,
-                             workspace_bytes=self.ws_bytes, stream=st)
+            self._backward_layer(l, J_out, st)
             if l == 1:
                 break
             if mode == "serial":
@@ -197,9 +259,13 @@ class PartitionTrainer:
                 self._refill(self.grad[l][nxt], self.remote_g[l], side)
                 self.ev_grad[l].record(side)
 
-        # ---- AllReduce (identity on one partition, or + the injected peer sum) and SGD
+        # ---- AllReduce (identity on one partition, or + the injected peer sum) and the update
         for l in range(L):
-            B.pgcn_sgd_update(self.W[l], self.dW[l], self.G_peer[l], self.W[l].numel(), o.eta, st)
+            if o.optimizer == "adam":
+                B.pgcn_adam_update(self.W[l], self.dW[l], self.G_peer[l], self.adam_m[l], self.adam_v[l],
+                                   self.W[l].numel(), o.eta, o.beta1, o.beta2, o.eps, t, st)
+            else:
+                B.pgcn_sgd_update(self.W[l], self.dW[l], self.G_peer[l], self.W[l].numel(), o.eta, st)
         if mode == "pipe":
             self.cur = nxt
         caller.wait_stream(st)          # results are ordered before the caller's next work

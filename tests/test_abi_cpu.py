@@ -32,12 +32,12 @@ def test_library_exports_every_declared_symbol():
     assert set(syms) == set(B.SIGNATURES), "binding signatures must cover exactly the header"
     for s in syms:
         assert getattr(B.lib, s) is not None
-    assert B.pgcn_version() == 100
+    assert B.pgcn_version() == 110
 
 
-def compare(g_n, rowptr, col, owner, nparts, part):
-    ref = build_partition(g_n, rowptr, col, owner, part, nparts)
-    h = B.pgcn_partition_setup(g_n, rowptr, col, owner, nparts, part, host_only=True)
+def compare(g_n, rowptr, col, owner, nparts, part, self_loop=True):
+    ref = build_partition(g_n, rowptr, col, owner, part, nparts, self_loop=self_loop)
+    h = B.pgcn_partition_setup(g_n, rowptr, col, owner, nparts, part, host_only=True, self_loop=self_loop)
     info = B.pgcn_partition_info(h)
     assert info["host_only"] == 1
     assert (info["n_inner"], info["n_bd"], info["nnz"], info["n_send"]) == \
@@ -62,18 +62,20 @@ def random_sym(n, m, nparts, seed):
     return rowptr, dst[o].astype(np.int32), rng.integers(0, nparts, n).astype(np.int32)
 
 
+@pytest.mark.parametrize("self_loop", [True, False])
 @pytest.mark.parametrize("seed", range(6))
-def test_setup_bit_exact_small(seed):
+def test_setup_bit_exact_small(seed, self_loop):
     n, nparts = [5, 40, 64, 1, 33, 90][seed], [2, 3, 4, 1, 5, 3][seed]
     rowptr, col, owner = random_sym(n, 3 * n, nparts, seed)
     for part in range(nparts):
-        compare(n, rowptr, col, owner, nparts, part)
+        compare(n, rowptr, col, owner, nparts, part, self_loop)
 
 
-def test_setup_bit_exact_tiny_workload():
+@pytest.mark.parametrize("self_loop", [True, False])
+def test_setup_bit_exact_tiny_workload(self_loop):
     g = synth.tiny_uniform()
     for part in range(2):
-        compare(g.n, g.rowptr, g.col, g.owner, g.nparts, part)
+        compare(g.n, g.rowptr, g.col, g.owner, g.nparts, part, self_loop)
 
 
 def test_setup_empty_partition_and_isolated_nodes():
