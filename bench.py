@@ -39,7 +39,7 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def algorithmic_work(tr, w):
+def algorithmic_work(tr, w, model="gcn"):
     """Per-step algorithmic bytes / flops of each kernel kind.
 
     Aggregation, compulsory model: every index once, every input feature row
@@ -51,6 +51,7 @@ def algorithmic_work(tr, w):
     items, items_t = i["spmm_items"], i["spmmt_items"]
     L, wd = tr.L, tr.widths
     bf16 = w.gemm_dtype == "bf16"
+    k = 2 if model == "sage" else 1          # GraphSAGE's update takes CONCAT(z, h): K = 2 f
     f4 = lambda f: (f + 3) // 4 * 4
     out = {k: 0.0 for k in ("agg_fwd", "agg_bwd", "agg_fwd_gather", "agg_bwd_gather", "gemm_fwd", "gemm_dgrad",
                             "gemm_wgrad")}
@@ -59,13 +60,13 @@ def algorithmic_work(tr, w):
         idx = e * 4 + items * 16
         out["agg_fwd"] += idx + (n + b) * f * 4 + n * f4(f) * (6 if bf16 else 4)
         out["agg_fwd_gather"] += idx + e * f4(f) * 4 + n * f4(f) * (6 if bf16 else 4)
-        out["gemm_fwd"] += 2.0 * n * f * wd[l]
-        out["gemm_wgrad"] += 2.0 * n * f * wd[l]
+        out["gemm_fwd"] += 2.0 * n * k * f * wd[l]
+        out["gemm_wgrad"] += 2.0 * n * k * f * wd[l]
         if l > 1:
             idx_t = e * 4 + items_t * 16
             out["agg_bwd"] += idx_t + n * f * 4 + (n + b) * f4(f) * 4
             out["agg_bwd_gather"] += idx_t + e * f4(f) * 4 + (n + b) * f4(f) * 4
-            out["gemm_dgrad"] += 2.0 * n * f * wd[l]
+            out["gemm_dgrad"] += 2.0 * n * k * f * wd[l]
     return out
 
 
@@ -90,7 +91,7 @@ def measured_traffic(workload: str, kernel: str):
     return rec["kernels"].get(kernel)
 
 
-def cpu_baseline(w, scale: float):
+def cpu_baseline(w, scale: float, model: str = "gcn"):
     """Time the fp64 oracle's per-partition step on a sample of the workload."""
     import numpy as np
     from threadpoolctl import threadpool_info
@@ -101,8 +102,8 @@ def cpu_baseline(w, scale: float):
 
     ws = configs.with_inner_scale(w, scale)
     g = configs.make_graph(ws)
-    d = configs.make_dense(ws, g.n)
-    p = build_partition(g.n, g.rowptr, g.col, g.owner, 0, g.nparts)
+    d = configs.make_dense(ws, g.n, model=model)
+    p = build_partition(g.n, g.rowptr, g.col, g.owner, 0, g.nparts, self_loop=model == "gcn")
     P = propagation_matrix(p)
     rng = np.random.default_rng(7)
     L = w.layers
@@ -113,6 +114,9 @@ def cpu_baseline(w, scale: float):
     sf, sg = VARIANTS["PipeGCN-GF"]
     opts = Options(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, loss=w.loss, loss_scale=w.loss_scale,
                    gemm="bf16" if w.gemm_dtype == "bf16" else "f64")
+    if model == "sage":
+        opts = Options(**{**opts.__dict__, "model": "sage", "dropout": w.sage_dropout, "optimizer": "adam",
+                          "eta": w.sage_lr})
     y = d.labels[p.inner_gid]
     X_in = d.X[p.inner_gid]
     t0 = time.perf_counter()
@@ -129,10 +133,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="reddit-like-1of4")
     ap.add_argument("--variant", default="PipeGCN-GF", choices=list(VARIANTS))
+    ap.add_argument("--model", default="gcn", choices=["gcn", "sage"],
+                    help="gcn: Algorithm 1's GCN layer with SGD; sage: the experiments' GraphSAGE layer with the "
+                         "setup table's dropout and Adam learning rate")
     ap.add_argument("--no-copy-modes", action="store_true", help="skip the serial / no-refill comparison")
     ap.add_argument("--refill", default="dma", choices=["dma", "blit"], help="engine of the stale-buffer refills")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=float, default=0.4, help="inner-node fraction timed on the CPU")
+    ap.add_argument("--cpu-sample", type=float, default=None,
+                    help="inner-node fraction timed on the CPU (default 0.4; 0.15 for the GraphSAGE model, whose "
+                         "oracle also draws the dropout masks)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 5 plain device copies of BYTES bytes (counter calibration) and exit")
     args = ap.parse_args()
@@ -163,12 +172,15 @@ def main():
     w = configs.WORKLOADS[args.workload]
     t0 = time.perf_counter()
     g = configs.make_graph(w)
-    d = configs.make_dense(w, g.n)
+    d = configs.make_dense(w, g.n, model=args.model)
     log(f"workload {w.name}: graph {g.stats} generated in {time.perf_counter() - t0:.1f}s")
     sf, sg = VARIANTS[args.variant]
-    tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, w.gemm_dtype,
-                          StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
-                                      refill_dma=args.refill == "dma"))
+    so = StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
+                     refill_dma=args.refill == "dma")
+    if args.model == "sage":
+        so = StepOptions(**{**so.__dict__, "model": "sage", "dropout": w.sage_dropout, "optimizer": "adam",
+                            "eta": w.sage_lr})
+    tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, w.gemm_dtype, so)
     del d
     log(f"partition set up: {tr.info}")
 
@@ -214,7 +226,7 @@ def main():
     loss = tr.loss.item()
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, loss {loss:.6f}")
 
-    work = algorithmic_work(tr, w)
+    work = algorithmic_work(tr, w, args.model)
     dt = "bf16" if w.gemm_dtype == "bf16" else "f32"
     util = {}
     for k in compute_kinds:
@@ -258,10 +270,12 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         try:
-            sec, n_s, nnz_s, threads = cpu_baseline(w, args.cpu_sample)
+            if args.cpu_sample is None:
+                args.cpu_sample = 0.4 if args.model == "gcn" else 0.15
+            sec, n_s, nnz_s, threads = cpu_baseline(w, args.cpu_sample, args.model)
             scale = tr.info["nnz"] / nnz_s
             cpu = {"value": 1.0 / (sec * scale), "unit": "steps/s", "cores": threads, "kind": "oracle",
-                   "sample": (f"fp64 oracle per-partition step (PipeGCN-GF, t=2) on the same graph law at "
+                   "sample": (f"fp64 oracle per-partition step ({args.model}, PipeGCN-GF, t=2) on the same graph law at "
                               f"{args.cpu_sample:g} of the inner/pool nodes ({n_s} inner rows, {nnz_s} nnz) took "
                               f"{sec:.2f}s; scaled by the nnz ratio {scale:.2f} to the full partition; SciPy's "
                               f"sparse products run single-threaded, dense products use {threads} BLAS threads")}
@@ -284,7 +298,9 @@ def main():
         "vs_baseline": None,
         "dtype": dt,
         "data": "synthetic",
-        "config": {"workload": w.name, "variant": args.variant, "copy_mode": "pipe", "refill": args.refill,
+        "config": {"workload": w.name, "variant": args.variant,
+                   "layer": "graphsage-concat" if args.model == "sage" else "gcn",
+                   "optimizer": so.optimizer, "dropout": so.dropout, "copy_mode": "pipe", "refill": args.refill,
                    "widths": list(w.widths),
                    "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",
                    "n_inner": i["n_inner"], "n_bd": i["n_bd"], "n_send": i["n_send"], "nnz": i["nnz"],
