@@ -31,6 +31,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+XGMI_LINK_GBPS = 153.0                   # one xGMI link of MI355X, per direction
 VARIANTS = {"PipeGCN": (False, False), "PipeGCN-G": (False, True), "PipeGCN-F": (True, False),
             "PipeGCN-GF": (True, True)}
 
@@ -138,6 +139,9 @@ def main():
                          "setup table's dropout and Adam learning rate")
     ap.add_argument("--no-copy-modes", action="store_true", help="skip the serial / no-refill comparison")
     ap.add_argument("--refill", default="dma", choices=["dma", "blit"], help="engine of the stale-buffer refills")
+    ap.add_argument("--remote", default="device", choices=["device", "host"],
+                    help="where the emulated peers' data lives: device memory, or pinned host memory (refills "
+                         "cross the host link, as in the paper's CPU-staged exchange)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=None,
                     help="inner-node fraction timed on the CPU (default 0.4; 0.15 for the GraphSAGE model, whose "
@@ -176,7 +180,7 @@ def main():
     log(f"workload {w.name}: graph {g.stats} generated in {time.perf_counter() - t0:.1f}s")
     sf, sg = VARIANTS[args.variant]
     so = StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
-                     refill_dma=args.refill == "dma")
+                     refill_dma=args.refill == "dma", remote=args.remote)
     if args.model == "sage":
         so = StepOptions(**{**so.__dict__, "model": "sage", "dropout": w.sage_dropout, "optimizer": "adam",
                             "eta": w.sage_lr})
@@ -299,7 +303,7 @@ def main():
         "dtype": dt,
         "data": "synthetic",
         "config": {"workload": w.name, "variant": args.variant,
-                   "layer": "graphsage-concat" if args.model == "sage" else "gcn",
+                   "layer": "graphsage-concat" if args.model == "sage" else "gcn", "remote": args.remote,
                    "optimizer": so.optimizer, "dropout": so.dropout, "copy_mode": "pipe", "refill": args.refill,
                    "widths": list(w.widths),
                    "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",
@@ -311,6 +315,9 @@ def main():
         "algorithmic_work_per_step": work,
         "utilisation": util,
         "copy_modes_ms_per_step": copy_modes,
+        # what the refills move per step, and the time one xGMI link (~153 GB/s) would take for it
+        "refill_bytes_per_step": tr.refill_bytes,
+        "xgmi_link_ms_per_step": tr.refill_bytes / XGMI_LINK_GBPS / 1e6,
         "loss": loss,
     }
     print(json.dumps(line), flush=True)

@@ -352,11 +352,14 @@ typedef struct {
 int pgcn_sage_layer_bwd(const pgcn_partition *part, const pgcn_sage_bwd_args *args, hipStream_t stream);
 
 /* Refill of a stale buffer (Algorithm 1's send/receive threads; the paper runs
- * them on a second stream): an asynchronous device-to-device copy of `bytes`
- * bytes enqueued on `stream`.  flags = 0: the runtime's copy (a blit kernel on
- * the compute units); PGCN_REFILL_DMA: a copy by the DMA engines that uses no
- * compute units (as a transfer arriving from a peer GPU would). */
-enum pgcn_refill_flags { PGCN_REFILL_DMA = 1 };
+ * them on a second stream): an asynchronous copy of `bytes` bytes into device
+ * memory `dst`, enqueued on `stream`.  flags = 0: device-to-device by the
+ * runtime's copy (a blit kernel on the compute units); PGCN_REFILL_DMA:
+ * device-to-device by the DMA engines, using no compute units (as a transfer
+ * arriving from a peer GPU would); PGCN_REFILL_FROM_HOST: `src` is pinned
+ * (page-locked) host memory, copied by DMA over the host link (the paper's
+ * CPU-staged exchange); other host memory is rejected with PGCN_EINVAL. */
+enum pgcn_refill_flags { PGCN_REFILL_DMA = 1, PGCN_REFILL_FROM_HOST = 2 };
 int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, hipStream_t stream);
 
 /*

@@ -25,7 +25,7 @@ PGCN_F32, PGCN_BF16 = 0, 1
 PGCN_SETUP_HOST_ONLY, PGCN_SETUP_NO_SELF_LOOP = 1, 2
 PGCN_PACK_FEAT, PGCN_ACCUM_GRAD = 0, 1
 PGCN_SOFTMAX_CE, PGCN_SIGMOID_BCE = 0, 1
-PGCN_REFILL_DMA = 1
+PGCN_REFILL_DMA, PGCN_REFILL_FROM_HOST = 1, 2
 
 _vp = C.c_void_p
 _i32, _i64, _u32, _f32, _sz = C.c_int32, C.c_int64, C.c_uint32, C.c_float, C.c_size_t

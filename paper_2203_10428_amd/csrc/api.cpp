@@ -487,7 +487,17 @@ extern "C" int pgcn_sgd_update(float *W, const float *G, const float *G_peer, in
 extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, hipStream_t s) {
   if (bytes == 0) return PGCN_OK;
   PGCN_REQUIRE(dst && src, "pgcn_refill_async: null buffer");
-  PGCN_REQUIRE((flags & ~(uint32_t)PGCN_REFILL_DMA) == 0, "pgcn_refill_async: unknown flags");
+  PGCN_REQUIRE((flags & ~(uint32_t)(PGCN_REFILL_DMA | PGCN_REFILL_FROM_HOST)) == 0, "pgcn_refill_async: unknown flags");
+  if (flags & PGCN_REFILL_FROM_HOST) {
+    hipPointerAttribute_t attr{};
+    const hipError_t e = hipPointerGetAttributes(&attr, src);
+    if (e != hipSuccess) (void)hipGetLastError();        // unregistered host memory: clear the sticky error
+    PGCN_REQUIRE(e == hipSuccess && attr.type == hipMemoryTypeHost,
+                 "pgcn_refill_async: PGCN_REFILL_FROM_HOST needs a pinned host source");
+    TraceScope ts(PGCN_TK_REFILL, s);
+    PGCN_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s));
+    return PGCN_OK;
+  }
   TraceScope ts(PGCN_TK_REFILL, s);
   PGCN_HIP(hipMemcpyAsync(dst, src, bytes, (flags & PGCN_REFILL_DMA) ? hipMemcpyDeviceToDeviceNoCU : hipMemcpyDeviceToDevice, s));
   return PGCN_OK;

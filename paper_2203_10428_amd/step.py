@@ -53,6 +53,7 @@ class StepOptions:
     relu_last: bool = False
     copy_mode: str = "pipe"          # "pipe" | "serial" | "none"
     refill_dma: bool = False         # refills by the DMA engines instead of a blit kernel
+    remote: str = "device"           # emulated peers' data in "device" memory or pinned "host" memory
     model: str = "gcn"               # "gcn" | "sage"
     dropout: float = 0.0
     seed: int = 0
@@ -129,12 +130,19 @@ class PartitionTrainer:
         self.ema_g = {l: z(s, wd[l - 1]) for l in range(2, L + 1)}
         # emulated peers: what the other partitions send each iteration
         g = torch.Generator(device="cpu").manual_seed(remote_seed)
-        self.remote_f = {l: z(b, wd[l - 1]) for l in range(1, L + 1)}
-        self.remote_g = {l: z(s, wd[l - 1]) for l in range(2, L + 1)}
+        if opts.remote == "host":          # pinned host memory: refills cross the host link (CPU-staged exchange)
+            zr = lambda r, f: torch.zeros((r, ld_of(f)), dtype=torch.float32, pin_memory=True)
+        else:
+            zr = z
+        self.remote_f = {l: zr(b, wd[l - 1]) for l in range(1, L + 1)}
+        self.remote_g = {l: zr(s, wd[l - 1]) for l in range(2, L + 1)}
         for l in range(1, L + 1):
-            self.remote_f[l][:, : wd[l - 1]] = torch.randn((b, wd[l - 1]), generator=g).to(self.dev)
+            self.remote_f[l][:, : wd[l - 1]] = torch.randn((b, wd[l - 1]), generator=g).to(self.remote_f[l].device)
         for l in range(2, L + 1):
-            self.remote_g[l][:, : wd[l - 1]] = (1e-3 * torch.randn((s, wd[l - 1]), generator=g)).to(self.dev)
+            self.remote_g[l][:, : wd[l - 1]] = (1e-3 * torch.randn((s, wd[l - 1]), generator=g)).to(
+                self.remote_g[l].device)
+        self.refill_bytes = sum(t.numel() * 4 for t in self.remote_f.values()) + \
+            sum(t.numel() * 4 for t in self.remote_g.values())
         self.X_used = {}                  # layer input the forward used (the GraphSAGE self operand)
         self.cur = 0                      # index of the buffer read in this iteration
         self.t = 0
@@ -155,8 +163,11 @@ class PartitionTrainer:
         return l < self.L or self.opts.relu_last
 
     def _refill(self, dst, src, stream):
-        B.pgcn_refill_async(dst, src, dst.numel() * dst.element_size(),
-                            B.PGCN_REFILL_DMA if self.opts.refill_dma else 0, stream)
+        if self.opts.remote == "host":
+            flags = B.PGCN_REFILL_FROM_HOST
+        else:
+            flags = B.PGCN_REFILL_DMA if self.opts.refill_dma else 0
+        B.pgcn_refill_async(dst, src, dst.numel() * dst.element_size(), flags, stream)
 
     def _dropout(self, out, inp, rows, l, row0, out16, st):
         o, f = self.opts, self.widths[l - 1]

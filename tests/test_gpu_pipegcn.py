@@ -101,16 +101,18 @@ def test_tiny_injected(variant, dt):
         compare_step(tr, r0, dt, L, w.widths)
 
 
-@pytest.mark.parametrize("refill_dma", [False, True])
+@pytest.mark.parametrize("refill", ["blit", "dma", "host"])
 @pytest.mark.parametrize("variant", list(VARIANTS))
-def test_tiny_autonomous_pipeline(variant, refill_dma):
+def test_tiny_autonomous_pipeline(variant, refill):
     sf, sg = VARIANTS[variant]
     T = 4
     w, g, d, sim, recs = tiny_setup(T, sf, sg)
     L = w.layers
     tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, "f32",
                           StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
-                                      refill_dma=refill_dma))
+                                      refill_dma=refill == "dma", remote="host" if refill == "host" else "device"))
+    if refill == "host":
+        assert tr.remote_f[1].is_pinned() and not tr.remote_f[1].is_cuda
     for t in range(1, T + 1):
         r0, r1 = recs[t - 1][0], recs[t - 1][1]
         so = r0["state_out"]
@@ -152,3 +154,16 @@ def test_tiny_stale_buffers_never_read_before_refill(refill_dma):
             assert torch.equal(tr.feat[l][cur], before[l])        # the buffer being read is not written
         for W in tr.W:
             assert torch.isfinite(W).all()
+
+
+def test_refill_from_host_needs_pinned_memory():
+    from paper_2203_10428_amd import binding as B
+    dst = torch.zeros(1024, device="cuda")
+    pinned = torch.arange(1024, dtype=torch.float32).pin_memory()
+    B.pgcn_refill_async(dst, pinned, 4096, B.PGCN_REFILL_FROM_HOST)
+    torch.cuda.synchronize()
+    assert torch.equal(dst.cpu(), pinned)
+    with pytest.raises(B.PgcnError, match="pinned host"):
+        B.pgcn_refill_async(dst, torch.zeros(1024), 4096, B.PGCN_REFILL_FROM_HOST)
+    with pytest.raises(B.PgcnError, match="unknown flags"):
+        B.pgcn_refill_async(dst, pinned, 4096, 8)
