@@ -1,0 +1,116 @@
+"""Staleness-error diagnostics of PipeGCN, in float64 (test infrastructure).
+
+Section 3.3's analysis bounds the error that one-iteration-stale boundary
+features and feature gradients put into the gradient, and Section 3.4
+motivates smoothing by that error.  Measured here, on the oracle's
+multi-partition simulation:
+
+* feature staleness error of layer l at iteration t: the boundary rows a
+  partition uses (the received buffer, or its moving average) against the
+  rows their owners hold in the same iteration (what they send at t),
+  ||H_used - H_now||_F / ||H_now||_F summed over all partitions;
+* gradient staleness error of layer l: the received gradient contributions
+  used (or their moving average) against what the peers compute at t;
+* weight-gradient error: the summed G of the pipelined step against vanilla
+  partition-parallel training (exact, Section 3.1) evaluated at the same
+  weights W_{t-1}; the convergence analysis bounds it by a multiple of the
+  learning rate (its corollary on the gradient error), so it scales about
+  linearly with eta.
+
+Pinned by: exact zeros where the pipeline carries no error (a constant
+input layer, eta = 0 after warm-up), the gamma = 0 reduction, and the
+linear scaling in eta (tests).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .pipegcn import Options, Simulation, run
+
+
+def _rel(pairs):
+    num = sum(float(np.sum((a - b) ** 2)) for a, b in pairs)
+    den = sum(float(np.sum(b ** 2)) for _, b in pairs)
+    return np.sqrt(num / den) if den > 0 else np.sqrt(num)
+
+
+def staleness_errors(n, rowptr, col, owner, nparts, X, labels, W0, T, opts: Options, vanilla_g: bool = True):
+    """Per iteration t >= 2: {"feat": {l: err}, "grad": {l: err}, "G": err} (G only with vanilla_g)."""
+    assert opts.mode == "pipe"
+    sim, recs = run(n, rowptr, col, owner, nparts, X, labels, W0, T, opts)
+    L = sim.L
+    out = []
+    for t in range(2, T + 1):
+        rec = recs[t - 1]
+        feat = {l: _rel([(rec[i]["H_bd_used"][l], rec[i]["state_out"].feat_buf[l]) for i in range(nparts)])
+                for l in range(1, L + 1)}
+        grad = {l: _rel([(rec[i]["C_used"][l], rec[i]["state_out"].grad_buf[l]) for i in range(nparts)])
+                for l in range(2, L + 1)}
+        row = {"t": t, "feat": feat, "grad": grad}
+        if vanilla_g:
+            # vanilla at the same weights and the same iteration index (the same dropout masks)
+            vo = Options(**{**opts.__dict__, "mode": "vanilla", "smooth_f": False, "smooth_g": False})
+            vs = Simulation(n, rowptr, col, owner, nparts, X, labels, rec[0]["W_in"], vo)
+            vs.t = t - 1
+            v = vs.step()[0]
+            row["G"] = _rel([(rec[0]["G_sum"][l], v["G_sum"][l]) for l in range(L)])
+        out.append(row)
+    return out
+
+
+VARIANTS = (("PipeGCN", False, False), ("PipeGCN-F", True, False), ("PipeGCN-G", False, True),
+            ("PipeGCN-GF", True, True))
+
+
+def sweep(graph, X, labels, W0, T, base: Options, gammas=(0.0, 0.5, 0.7, 0.95), first=None, variants=VARIANTS):
+    """Mean errors over iterations >= first for the variants at each gamma."""
+    n, rowptr, col, owner, nparts = graph
+    first = first if first is not None else max(2, T // 3)
+    table = []
+    for name, sf, sg in variants:
+        for gamma in (gammas if (sf or sg) else (None,)):
+            o = Options(**{**base.__dict__, "mode": "pipe", "smooth_f": sf, "smooth_g": sg,
+                           "gamma": gamma if gamma is not None else base.gamma})
+            rows = [r for r in staleness_errors(n, rowptr, col, owner, nparts, X, labels, W0, T, o) if r["t"] >= first]
+            L = len(W0)
+            table.append(dict(variant=name, gamma=gamma,
+                              feat={l: float(np.mean([r["feat"][l] for r in rows])) for l in range(2, L + 1)},
+                              grad={l: float(np.mean([r["grad"][l] for r in rows])) for l in range(2, L + 1)},
+                              G=float(np.mean([r["G"] for r in rows]))))
+    return table
+
+
+def main(ema_init: str = "zero", variants=VARIANTS):
+    """γ sweep on a seeded 4-partition uniform graph (8,000 nodes, mean degree 12, widths 48-32-32-16):
+    GCN with SGD, and GraphSAGE with dropout 0.5 and Adam (the experiments' setting)."""
+    import sys
+    sys.path.insert(0, __file__.rsplit("/oracle/", 1)[0])
+    from paper_2203_10428_amd import synth
+    g = synth.tiny_uniform(8000, 48000, 4, seed=3)
+    graph = (g.n, g.rowptr, g.col, g.owner, g.nparts)
+    widths = [48, 32, 32, 16]
+    rx, rw, ry = synth.dense_streams(3, 3)
+    X = synth.features(rx, g.n, widths[0])
+    y = synth.labels_single(ry, g.n, widths[-1])
+    for model, base in (("gcn", Options(eta=0.5, loss_scale=1.0 / g.n, ema_init=ema_init)),
+                        ("sage", Options(model="sage", dropout=0.5, seed=1, optimizer="adam", eta=0.01,
+                                         loss_scale=1.0 / g.n, ema_init=ema_init))):
+        k = 2 if model == "sage" else 1
+        W0 = [synth.glorot_uniform(rw, k * widths[l], widths[l + 1]) for l in range(3)]
+        tab = sweep(graph, X, y, W0, 40, base, first=15, variants=variants)
+        print(f"\n{model}, smoothing state initialised '{ema_init}': mean over iterations 15..40 "
+              f"(relative Frobenius errors)\n")
+        print("| variant | γ | features l=2 | features l=3 | gradients l=2 | gradients l=3 | weight gradient |")
+        print("|---|---|---|---|---|---|---|")
+        for r in tab:
+            gm = "—" if r["gamma"] is None else f"{r['gamma']:g}"
+            print(f"| {r['variant']} | {gm} | {r['feat'][2]:.4f} | {r['feat'][3]:.4f} | {r['grad'][2]:.4f} | "
+                  f"{r['grad'][3]:.4f} | {r['G']:.4f} |")
+
+
+if __name__ == "__main__":
+    import sys
+    if len(sys.argv) > 1 and sys.argv[1] == "first":
+        main("first", variants=(VARIANTS[3],))
+    else:
+        main()
