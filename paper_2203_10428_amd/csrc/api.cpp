@@ -35,9 +35,9 @@ size_t fwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm
   return fwd_agg_bytes(p, f_in, gemm_dtype) + gemm_nk_workspace(f_out, f_in, gemm_dtype);
 }
 
-// backward workspace: [region 0 | packed weights].  Region 0 first holds the
-// split-K partials of the weight gradient, which are consumed before it is
-// reused for D and the transposed aggregation's partials.
+// Region 0 of the backward workspace first holds the split-K partials of the
+// weight gradient, which are consumed before it is reused for D and the
+// transposed aggregation's partials.
 size_t bwd_region0(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_grad) {
   size_t g = gemm_workspace(Gemm::TN_MASK_SPLITK, f_in, f_out, (int32_t)p->n_inner);
   size_t d = 0;
@@ -46,8 +46,21 @@ size_t bwd_region0(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool in
         align_up(aggregate_workspace(p->plan_t, f_in), 256);
   return align_up(g > d ? g : d, 256);
 }
+// bf16 path with a feature gradient: the masked operand in bf16, written by the
+// weight-gradient kernel and read by the feature-gradient GEMM
+int64_t ld_m16(int32_t f_out) { return ((int64_t)f_out + 7) / 8 * 8; }
+size_t m16_bytes(const pgcn_partition *p, int32_t f_out, bool input_grad, int32_t gemm_dtype) {
+  if (!input_grad || gemm_dtype != PGCN_BF16) return 0;
+  return align_up((size_t)p->n_inner * (size_t)ld_m16(f_out) * sizeof(uint16_t), 256);
+}
+// backward workspace: [region 0 | packed weights | bf16 masked operand]
 size_t bwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_grad, int32_t gemm_dtype) {
-  return bwd_region0(p, f_in, f_out, input_grad) + (input_grad ? gemm_nk_workspace(f_in, f_out, gemm_dtype) : 0);
+  return bwd_region0(p, f_in, f_out, input_grad) + (input_grad ? gemm_nk_workspace(f_in, f_out, gemm_dtype) : 0) +
+         m16_bytes(p, f_out, input_grad, gemm_dtype);
+}
+uint16_t *m16_ptr(const pgcn_partition *p, void *ws, int32_t f_in, int32_t f_out, bool input_grad, int32_t dt) {
+  if (!m16_bytes(p, f_out, input_grad, dt)) return nullptr;
+  return (uint16_t *)((char *)ws + bwd_region0(p, f_in, f_out, input_grad) + gemm_nk_workspace(f_in, f_out, dt));
 }
 
 }  // namespace
@@ -176,6 +189,9 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   g.ldc = a->f_out;
   g.workspace = (float *)a->workspace;
   g.workspace_bytes = a->workspace_bytes;
+  uint16_t *M16 = p->n_inner > 0 ? m16_ptr(p, a->workspace, a->f_in, a->f_out, input_grad, a->gemm_dtype) : nullptr;
+  g.M16 = M16;
+  g.ldm16 = ld_m16(a->f_out);
   rc = launch_gemm(Gemm::TN_MASK_SPLITK, g, s);
   if (rc) return rc;
   if (!input_grad || p->n_inner == 0) return PGCN_OK;
@@ -200,7 +216,13 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   d.rowscale = p->d_inv_deg;
   d.workspace = (float *)((char *)a->workspace + bwd_region0(p, a->f_in, a->f_out, input_grad));
   d.workspace_bytes = gemm_nk_workspace(a->f_in, a->f_out, a->gemm_dtype);
-  rc = launch_gemm_nk(Gemm::MASK_NT_ROWSCALE, d, s);
+  if (M16) {                       // bf16 path: the masked operand as the weight-gradient kernel rounded it
+    d.A = nullptr;
+    d.A16 = M16;
+    d.lda = ld_m16(a->f_out);
+    d.Hmask = nullptr;
+  }
+  rc = launch_gemm_nk(M16 ? Gemm::NT16_ROWSCALE : Gemm::MASK_NT_ROWSCALE, d, s);
   if (rc) return rc;
 
   AggArgs t{};
@@ -351,11 +373,15 @@ extern "C" int pgcn_sage_layer_bwd(const pgcn_partition *p, const pgcn_sage_bwd_
   g.ldc = a->f_out;
   g.workspace = (float *)a->workspace;
   g.workspace_bytes = a->workspace_bytes;
+  uint16_t *M16 = p->n_inner > 0 ? m16_ptr(p, a->workspace, a->f_in, a->f_out, input_grad, a->gemm_dtype) : nullptr;
+  g.M16 = M16;
+  g.ldm16 = ld_m16(a->f_out);
   rc = launch_gemm(Gemm::TN_MASK_SPLITK, g, s);
   if (rc) return rc;
   g.A = a->X_in;
   g.A16 = a->X_in_bf16;
   g.C = a->dW + half;
+  g.M16 = nullptr;
   rc = launch_gemm(Gemm::TN_MASK_SPLITK, g, s);
   if (rc) return rc;
   if (!input_grad || p->n_inner == 0) return PGCN_OK;
@@ -380,13 +406,19 @@ extern "C" int pgcn_sage_layer_bwd(const pgcn_partition *p, const pgcn_sage_bwd_
   d.ldc = a->ld_in;
   d.workspace = (float *)((char *)a->workspace + bwd_region0(p, a->f_in, a->f_out, input_grad));
   d.workspace_bytes = gemm_nk_workspace(a->f_in, a->f_out, a->gemm_dtype);
-  rc = launch_gemm_nk(Gemm::MASK_NT_PLAIN, d, s);
+  if (M16) {                       // bf16 path: the masked operand as the weight-gradient kernel rounded it
+    d.A = nullptr;
+    d.A16 = M16;
+    d.lda = ld_m16(a->f_out);
+    d.Hmask = nullptr;
+  }
+  rc = launch_gemm_nk(M16 ? Gemm::NT16_PLAIN : Gemm::MASK_NT_PLAIN, d, s);
   if (rc) return rc;
   d.B = a->W;
   d.C = D;
   d.ldc = ld_d;
   d.rowscale = p->d_inv_deg;
-  rc = launch_gemm_nk(Gemm::MASK_NT_ROWSCALE, d, s);
+  rc = launch_gemm_nk(M16 ? Gemm::NT16_ROWSCALE : Gemm::MASK_NT_ROWSCALE, d, s);
   if (rc) return rc;
 
   AggArgs t{};

@@ -21,7 +21,9 @@
 //         node 8h + 4q + e for lane half h;
 //   bf16: slabs of 32 nodes, A already bf16 in memory, J ∘ mask rounded to
 //         bf16 (nearest even); v_mfma_f32_32x32x16_bf16, step q uses nodes
-//         16q + 8h .. 16q + 8h + 7 for lane half h.
+//         16q + 8h .. 16q + 8h + 7 for lane half h.  The first row of tiles
+//         can also write the rounded J ∘ mask node-major for the feature
+//         gradient.
 // The grid is one-dimensional over (split, tile) with the tiles of a split
 // adjacent and on the same XCD, so each split's rows of A, J and H come from
 // HBM about once and are re-read from that XCD's L2.
@@ -47,6 +49,8 @@ struct TNParams {
   const float *H;         // mask source [K, ldh], or null (no ReLU)
   int64_t ldh;
   float *partials;        // [splits, M, N]
+  uint16_t *M16;          // bf16 path: bf16(J ∘ mask) [K, ldm16] written by the first row of tiles, or null
+  int64_t ldm16;
 };
 
 __device__ __forceinline__ uint32_t tn_bf16(float x) {
@@ -98,7 +102,7 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_f32(TNParams p) {
   __shared__ __attribute__((aligned(16))) float As[2][BM * LK];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * LK];
 
-  const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+  const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
   int split, tile;
   tn_coords(p.tiles, split, tile);
   const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
@@ -195,7 +199,7 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_bf16(TNParams p) {
   __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LK];
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LK];
 
-  const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+  const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
   int split, tile;
   tn_coords(p.tiles, split, tile);
   const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
@@ -214,9 +218,12 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_bf16(TNParams p) {
   const bool bok = hasB && n0 + 4 * ub < p.N;
   const bool masked = p.H != nullptr;
 
+  const bool write_m16 = p.M16 != nullptr && m0 == 0 && bok;
   u32x4 xa[4];
   f32x4 xb[4], hm[4];
+  int kl = 0;                                          // node of the staged slab
   auto load = [&](int kt) __attribute__((always_inline)) {
+    kl = kt;
     if (hasA) {
       const int gk = kt + 4 * ka;
 #pragma unroll
@@ -255,10 +262,23 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_bf16(TNParams p) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) xb[s][e] = hm[s][e] > 0.f ? xb[s][e] : 0.f;
       }
+      uint32_t q[4][4];                                // bf16 bits of node s, feature e
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) q[s][e] = tn_bf16(xb[s][e]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const u32x2 v{tn_bf16(xb[0][e]) | (tn_bf16(xb[1][e]) << 16), tn_bf16(xb[2][e]) | (tn_bf16(xb[3][e]) << 16)};
+        const u32x2 v{q[0][e] | (q[1][e] << 16), q[2][e] | (q[3][e] << 16)};
         *reinterpret_cast<u32x2 *>(&Bs[b][(e * UB + ub) * LK + 4 * kb]) = v;
+      }
+      if (write_m16) {                                 // the masked operand, node-major, for the feature gradient
+        const int gk = kl + 4 * kb;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          if (gk + s < kend)
+            *reinterpret_cast<u32x2 *>(p.M16 + (int64_t)(gk + s) * p.ldm16 + n0 + 4 * ub) =
+                u32x2{q[s][0] | (q[s][1] << 16), q[s][2] | (q[s][3] << 16)};
       }
     }
   };
@@ -381,6 +401,12 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   p.ldh = g.ldm;
   p.partials = g.workspace;
   const bool bf16 = g.dtype == PGCN_BF16;
+  if (g.M16) {
+    if (!bf16 || g.ldm16 < g.N || g.ldm16 % 4 != 0 || ((uintptr_t)g.M16 & 7u))
+      return set_error(PGCN_EINVAL, "weight-gradient GEMM: bad bf16 operand output");
+    p.M16 = g.M16;
+    p.ldm16 = g.ldm16;
+  }
   {
     TraceScope ts(PGCN_TK_GEMM_WGRAD, s);
     if (g.N <= 64) tn_launch<64>(p, bf16, splits, s);

@@ -5,6 +5,9 @@
 // The GraphSAGE layer (Section 2's CONCAT update) uses the same kernels on
 // the two halves of its weights: Z = z W_top, then Z = relu(Z + X W_bot)
 // (accumulating epilogue), and the feature gradient without the row scale.
+// On the bf16 path the feature gradient reads the masked operand as bf16,
+// written once by the weight-gradient kernel (2 bytes per element instead of
+// the 8 of fp32 J and H).
 //
 // The right operand (the layer's weights, at most a few MB) is first packed
 // once per call into an n-major, k-contiguous matrix zero-padded to a 128-row
@@ -65,19 +68,6 @@ __device__ __forceinline__ int nk_xcd_remap(int b, int g) {
   return (b % 8) * (g / 8) + b / 8;
 }
 
-template <int EK>
-__device__ __forceinline__ void nk_store(const NKParams &p, int row, int col, float v) {
-  if (row >= p.M || col >= p.N) return;
-  float *c = p.C + (int64_t)row * p.ldc + col;
-  if (EK == NK_E_RELU) *c = v > 0.f ? v : 0.f;
-  else if (EK == NK_E_PLAIN) *c = v;
-  else if (EK == NK_E_ROWSCALE) *c = v * p.rowscale[row];
-  else {                                               // accumulate onto C, then the activation
-    const float u = *c + v;
-    *c = (EK == NK_E_ACC_RELU && u <= 0.f) ? 0.f : u;
-  }
-}
-
 // out[n][k] = (n < N && k < K) ? (trans ? W[k*ldw + n] : W[n*ldw + k]) : 0, for n < rows, k < ldk
 template <bool BF16>
 __global__ __launch_bounds__(256) void pack_b_kernel(const float *W, int ldw, int trans, int N, int K, int rows,
@@ -90,17 +80,63 @@ __global__ __launch_bounds__(256) void pack_b_kernel(const float *W, int ldw, in
   else reinterpret_cast<float *>(out)[i] = v;
 }
 
+// Final value of one output element.
+template <int EK>
+__device__ __forceinline__ float nk_out(float v, float sc, float old) {
+  if (EK == NK_E_RELU) return v > 0.f ? v : 0.f;
+  if (EK == NK_E_PLAIN) return v;
+  if (EK == NK_E_ROWSCALE) return v * sc;
+  const float u = old + v;                             // accumulate onto C, then the activation
+  return (EK == NK_E_ACC_RELU && u <= 0.f) ? 0.f : u;
+}
+
+// Stores the accumulators of one wave.  The values an epilogue reads (the row
+// scales, or C for the accumulating forms) are loaded for a whole 32 x 32 tile
+// before any of its stores, and tiles that lie inside C (all but the edge
+// tiles; a wave-uniform test) store without per-element branches, so the
+// loads are in flight together and the stores do not wait for one another.
 template <int EK, int TM, int TN>
 __device__ __forceinline__ void nk_epilogue(const NKParams &p, const f32x16 (&acc)[TM][TN], int m0, int n0,
                                             int lane) {
+  constexpr bool ACC = EK == NK_E_ACC_RELU || EK == NK_E_ACC_PLAIN;
+  const int h = lane / 32, cl = lane % 32;
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < TM; ++i) {
+    const int rbase = m0 + i * 32 + 4 * h;
+    const bool rows_in = m0 + i * 32 + 32 <= p.M;
+    float sc[16];
+    if (EK == NK_E_ROWSCALE) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int r = 0; r < 16; ++r) {
+        const int row = rbase + 8 * (r / 4) + (r % 4);
+        sc[r] = (rows_in || row < p.M) ? p.rowscale[row] : 0.f;
+      }
+    }
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        nk_store<EK>(p, m0 + i * 32 + 8 * (r / 4) + 4 * (lane / 32) + (r % 4), n0 + j * 32 + lane % 32,
-                     acc[i][j][r]);
+    for (int j = 0; j < TN; ++j) {
+      const int col = n0 + j * 32 + cl;
+      float *c0 = p.C + (int64_t)rbase * p.ldc + col;
+      float old[16];
+      if (rows_in && n0 + j * 32 + 32 <= p.N) {
+        if (ACC) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) old[r] = c0[(int64_t)(8 * (r / 4) + (r % 4)) * p.ldc];
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          c0[(int64_t)(8 * (r / 4) + (r % 4)) * p.ldc] = nk_out<EK>(acc[i][j][r], sc[r], old[r]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = rbase + 8 * (r / 4) + (r % 4);
+          if (row < p.M && col < p.N) {
+            const float o = ACC ? c0[(int64_t)(8 * (r / 4) + (r % 4)) * p.ldc] : 0.f;
+            c0[(int64_t)(8 * (r / 4) + (r % 4)) * p.ldc] = nk_out<EK>(acc[i][j][r], sc[r], o);
+          }
+        }
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------------ fp32 ---
@@ -113,7 +149,7 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
   __shared__ __attribute__((aligned(16))) float As[2][BM * LK];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * LK];
 
-  const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+  const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
   const int tile = nk_xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
   const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
@@ -211,7 +247,7 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
   __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LK];
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LK];
 
-  const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+  const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
   const int tile = nk_xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
   const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
@@ -395,6 +431,12 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
     case Gemm::NN_ACC_PLAIN: nk_launch_bn<NK_A_F32, NK_E_ACC_PLAIN>(p, bf16, s); break;
     case Gemm::MASK_NT_ROWSCALE: nk_launch_bn<NK_A_MASK, NK_E_ROWSCALE>(p, bf16, s); break;
     case Gemm::MASK_NT_PLAIN: nk_launch_bn<NK_A_MASK, NK_E_PLAIN>(p, bf16, s); break;
+    case Gemm::NT16_ROWSCALE:
+    case Gemm::NT16_PLAIN:
+      if (!bf16 || !p.A16) return set_error(PGCN_EINVAL, "launch_gemm_nk: NT16 needs the bf16 path and A16");
+      if (kind == Gemm::NT16_ROWSCALE) nk_launch_bn<NK_A_F32, NK_E_ROWSCALE>(p, true, s);
+      else nk_launch_bn<NK_A_F32, NK_E_PLAIN>(p, true, s);
+      break;
     default: return set_error(PGCN_EINVAL, "launch_gemm_nk: not a node-major GEMM");
   }
   PGCN_HIP(hipGetLastError());

@@ -120,8 +120,13 @@ int launch_aggregate(const AggArgs &a, hipStream_t s);
 size_t aggregate_workspace(const Plan &plan, int64_t f);
 
 // NN_*: C (=|+=) A W, with ReLU for *_RELU (ACC: C = act(C + A W));
-// MASK_NT_*: C = (J ∘ mask) W^T, row-scaled or plain; TN_MASK_SPLITK: C = A^T (J ∘ mask)
-enum class Gemm { NN_RELU, NN_PLAIN, NN_ACC_RELU, NN_ACC_PLAIN, MASK_NT_ROWSCALE, MASK_NT_PLAIN, TN_MASK_SPLITK };
+// MASK_NT_*: C = (J ∘ mask) W^T, row-scaled or plain (fp32 J and mask; rounded to bf16 on the
+// bf16 path); NT16_*: the same with the masked operand already bf16 in A16;
+// TN_MASK_SPLITK: C = A^T (J ∘ mask)
+enum class Gemm {
+  NN_RELU, NN_PLAIN, NN_ACC_RELU, NN_ACC_PLAIN, MASK_NT_ROWSCALE, MASK_NT_PLAIN, NT16_ROWSCALE, NT16_PLAIN,
+  TN_MASK_SPLITK
+};
 struct GemmArgs {
   int32_t M, N, K;
   int32_t dtype;            // PGCN_F32 / PGCN_BF16
@@ -137,6 +142,8 @@ struct GemmArgs {
   const float *rowscale;    // per output row scale (MASK_NT_ROWSCALE)
   float *workspace;
   size_t workspace_bytes;
+  uint16_t *M16;            // TN_MASK_SPLITK, bf16 path: also write bf16(B ∘ mask) [K, ldm16] (or null)
+  int64_t ldm16;
 };
 int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s);
 size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K);
