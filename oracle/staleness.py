@@ -80,9 +80,10 @@ def sweep(graph, X, labels, W0, T, base: Options, gammas=(0.0, 0.5, 0.7, 0.95), 
     return table
 
 
-def main(ema_init: str = "zero", variants=VARIANTS):
+def main(ema_init: str = "zero", variants=VARIANTS, lr_scale: float = 1.0):
     """γ sweep on a seeded 4-partition uniform graph (8,000 nodes, mean degree 12, widths 48-32-32-16):
-    GCN with SGD, and GraphSAGE with dropout 0.5 and Adam (the experiments' setting)."""
+    GCN with SGD (eta 0.5), and GraphSAGE with dropout 0.5 and Adam (lr 0.01, the experiments'
+    Reddit setting); both learning rates times lr_scale."""
     import sys
     sys.path.insert(0, __file__.rsplit("/oracle/", 1)[0])
     from paper_2203_10428_amd import synth
@@ -92,13 +93,14 @@ def main(ema_init: str = "zero", variants=VARIANTS):
     rx, rw, ry = synth.dense_streams(3, 3)
     X = synth.features(rx, g.n, widths[0])
     y = synth.labels_single(ry, g.n, widths[-1])
-    for model, base in (("gcn", Options(eta=0.5, loss_scale=1.0 / g.n, ema_init=ema_init)),
-                        ("sage", Options(model="sage", dropout=0.5, seed=1, optimizer="adam", eta=0.01,
+    for model, base in (("gcn", Options(eta=0.5 * lr_scale, loss_scale=1.0 / g.n, ema_init=ema_init)),
+                        ("sage", Options(model="sage", dropout=0.5, seed=1, optimizer="adam", eta=0.01 * lr_scale,
                                          loss_scale=1.0 / g.n, ema_init=ema_init))):
         k = 2 if model == "sage" else 1
         W0 = [synth.glorot_uniform(rw, k * widths[l], widths[l + 1]) for l in range(3)]
         tab = sweep(graph, X, y, W0, 40, base, first=15, variants=variants)
-        print(f"\n{model}, smoothing state initialised '{ema_init}': mean over iterations 15..40 "
+        print(f"\n{model}, learning rate x{lr_scale:g}, smoothing state initialised '{ema_init}': "
+              f"mean over iterations 15..40 "
               f"(relative Frobenius errors)\n")
         print("| variant | γ | features l=2 | features l=3 | gradients l=2 | gradients l=3 | weight gradient |")
         print("|---|---|---|---|---|---|---|")
@@ -109,8 +111,10 @@ def main(ema_init: str = "zero", variants=VARIANTS):
 
 
 if __name__ == "__main__":
-    import sys
-    if len(sys.argv) > 1 and sys.argv[1] == "first":
-        main("first", variants=(VARIANTS[3],))
-    else:
-        main()
+    import argparse
+    ap = argparse.ArgumentParser(description=main.__doc__)
+    ap.add_argument("--ema-init", choices=("zero", "first"), default="zero")
+    ap.add_argument("--lr-scale", type=float, default=1.0)
+    ap.add_argument("--gf-only", action="store_true", help="only PipeGCN-GF")
+    a = ap.parse_args()
+    main(a.ema_init, variants=(VARIANTS[3],) if a.gf_only else VARIANTS, lr_scale=a.lr_scale)

@@ -51,6 +51,7 @@ struct NKParams {
   float *C;
   int64_t ldc;
   const float *rowscale;
+  int vec;                 // C rows 16-byte aligned: ldc % 4 == 0 and C 16-byte aligned
 };
 
 enum NKA { NK_A_F32, NK_A_BF16, NK_A_MASK };
@@ -90,49 +91,73 @@ __device__ __forceinline__ float nk_out(float v, float sc, float old) {
   return (EK == NK_E_ACC_RELU && u <= 0.f) ? 0.f : u;
 }
 
-// Stores the accumulators of one wave.  The values an epilogue reads (the row
-// scales, or C for the accumulating forms) are loaded for a whole 32 x 32 tile
-// before any of its stores, and tiles that lie inside C (all but the edge
-// tiles; a wave-uniform test) store without per-element branches, so the
-// loads are in flight together and the stores do not wait for one another.
+// Orders a wave's LDS accesses before and after this point (LDS operations of
+// one wave complete in order; this keeps the compiler from moving them).
+__device__ __forceinline__ void nk_wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+constexpr int kNkStageLd = 36;                         // floats per staged row (32 + 4)
+constexpr int kNkStageFloats = 4 * 32 * kNkStageLd;    // one 32 x 32 block per wave
+
+// Stores the accumulators of one wave.  The MFMAs compute every 32 x 32 block
+// transposed (the packed weights are the matrix core's left operand), so lane
+// l holds output row l % 32 and, in registers 4q .. 4q+3, the columns
+// 8q + 4(l / 32) .. +3 of the block; one row scale per lane suffices.  Each
+// block passes through the wave's own LDS region and leaves as 16-byte
+// vectors, eight lanes per row: every store instruction writes 8 whole rows of
+// the block (128 contiguous bytes each).  Blocks inside C (all but the edge
+// blocks; a wave-uniform test) load the old C of the accumulating forms before
+// any store and store without per-element branches.
 template <int EK, int TM, int TN>
 __device__ __forceinline__ void nk_epilogue(const NKParams &p, const f32x16 (&acc)[TM][TN], int m0, int n0,
-                                            int lane) {
+                                            int lane, float *stage) {
   constexpr bool ACC = EK == NK_E_ACC_RELU || EK == NK_E_ACC_PLAIN;
   const int h = lane / 32, cl = lane % 32;
+  const int rr = lane / 8, g = lane % 8;               // read layout: rows rr + 8s, columns 4g .. 4g+3
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int rbase = m0 + i * 32 + 4 * h;
-    const bool rows_in = m0 + i * 32 + 32 <= p.M;
-    float sc[16];
-    if (EK == NK_E_ROWSCALE) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = rbase + 8 * (r / 4) + (r % 4);
-        sc[r] = (rows_in || row < p.M) ? p.rowscale[row] : 0.f;
-      }
-    }
+    const int mb = m0 + i * 32;
+    const bool rows_in = mb + 32 <= p.M;
+    const float sc = (EK == NK_E_ROWSCALE && mb + cl < p.M) ? p.rowscale[mb + cl] : 0.f;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int col = n0 + j * 32 + cl;
-      float *c0 = p.C + (int64_t)rbase * p.ldc + col;
-      float old[16];
-      if (rows_in && n0 + j * 32 + 32 <= p.N) {
-        if (ACC) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) old[r] = c0[(int64_t)(8 * (r / 4) + (r % 4)) * p.ldc];
+      for (int q = 0; q < 4; ++q) {
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = ACC ? acc[i][j][4 * q + e] : nk_out<EK>(acc[i][j][4 * q + e], sc, 0.f);
+        *reinterpret_cast<f32x4 *>(stage + cl * kNkStageLd + 8 * q + 4 * h) = v;
+      }
+      nk_wave_sync();
+      f32x4 v[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) v[s] = *reinterpret_cast<const f32x4 *>(stage + (rr + 8 * s) * kNkStageLd + 4 * g);
+      nk_wave_sync();                                  // the next block's staging comes after these reads
+      const int cb = n0 + j * 32 + 4 * g;
+      float *c0 = p.C + (int64_t)(mb + rr) * p.ldc + cb;
+      if (p.vec && rows_in && n0 + j * 32 + 32 <= p.N) {
+        if (ACC) {
+          f32x4 old[4];
+#pragma unroll
+          for (int s = 0; s < 4; ++s) old[s] = *reinterpret_cast<const f32x4 *>(c0 + (int64_t)(8 * s) * p.ldc);
+#pragma unroll
+          for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[s][e] = nk_out<EK>(v[s][e], 0.f, old[s][e]);
         }
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          c0[(int64_t)(8 * (r / 4) + (r % 4)) * p.ldc] = nk_out<EK>(acc[i][j][r], sc[r], old[r]);
+        for (int s = 0; s < 4; ++s) *reinterpret_cast<f32x4 *>(c0 + (int64_t)(8 * s) * p.ldc) = v[s];
       } else {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = rbase + 8 * (r / 4) + (r % 4);
-          if (row < p.M && col < p.N) {
-            const float o = ACC ? c0[(int64_t)(8 * (r / 4) + (r % 4)) * p.ldc] : 0.f;
-            c0[(int64_t)(8 * (r / 4) + (r % 4)) * p.ldc] = nk_out<EK>(acc[i][j][r], sc[r], o);
-          }
+        for (int s = 0; s < 4; ++s) {
+          if (mb + rr + 8 * s >= p.M) continue;
+          float *c = c0 + (int64_t)(8 * s) * p.ldc;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (cb + e < p.N) c[e] = ACC ? nk_out<EK>(v[s][e], 0.f, c[e]) : v[s][e];
         }
       }
     }
@@ -229,12 +254,15 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(b[j][e], a[i][e], acc[i][j], 0, 0, 0);
     }
     store(cur ^ 1);
     __syncthreads();
   }
-  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane);
+  // the last barrier of the loop ends every LDS read of the main loop
+  static_assert(sizeof(As) >= kNkStageFloats * sizeof(float), "epilogue staging does not fit");
+  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane,
+                          reinterpret_cast<float *>(&As[0][0]) + wave * 32 * kNkStageLd);
 }
 
 // ------------------------------------------------------------------ bf16 ---
@@ -349,12 +377,14 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
     }
     store(cur ^ 1);
     __syncthreads();
   }
-  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane);
+  static_assert(sizeof(As) >= kNkStageFloats * sizeof(float), "epilogue staging does not fit");
+  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane,
+                          reinterpret_cast<float *>(&As[0][0]) + wave * 32 * kNkStageLd);
 }
 
 // ---------------------------------------------------------------- launch ---
@@ -423,6 +453,7 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
   p.C = g.C;
   p.ldc = g.ldc;
   p.rowscale = g.rowscale;
+  p.vec = (g.ldc % 4 == 0 && (reinterpret_cast<uintptr_t>(g.C) & 15) == 0) ? 1 : 0;
   TraceScope ts(fwd ? PGCN_TK_GEMM_FWD : PGCN_TK_GEMM_DGRAD, s);
   switch (kind) {
     case Gemm::NN_RELU: nk_launch_bn<NK_A_F32, NK_E_RELU>(p, bf16, s); break;
