@@ -21,6 +21,17 @@ The paper writes the aggregation as the product P H W; aggregating first and
 transforming first in the backward are the same matrix products in another
 association (the reading is listed with the others in the design notes).
 
+``order="transform"`` evaluates the same layer in the other association,
+worth it when the layer narrows (f_out < f_in: fewer columns to aggregate):
+
+    Z      = P (H_full W)
+    T      = Pᵀ M               (n + b rows)
+    G      = H_fullᵀ T
+    J_full = T Wᵀ
+
+With ``gemm="bf16"`` the rounded operands are then H_full, W and T (the
+products' inputs in this association).
+
 GraphSAGE layer (Section 2: the update takes CONCAT(z_v, h_v); the paper's
 experiments train GraphSAGE), with P the mean over N(v) without a self loop
 and X the layer input after dropout (dropout is applied to the received rows
@@ -69,17 +80,27 @@ def _operand(x, gemm: str):
     return round_bf16(x) if gemm == "bf16" else x
 
 
-def layer_forward(P, H_full: np.ndarray, W: np.ndarray, relu: bool, gemm: str = "f64"):
-    """``gemm="bf16"`` rounds both GEMM operands to bf16 first (products and sums stay fp64)."""
+def layer_forward(P, H_full: np.ndarray, W: np.ndarray, relu: bool, gemm: str = "f64", order: str = "agg"):
+    """``gemm="bf16"`` rounds both GEMM operands to bf16 first (products and sums stay fp64).
+    Returns (A, Z, H) with A = P H_full in both orders."""
     A = P @ H_full
-    Z = _operand(A, gemm) @ _operand(W, gemm)
+    if order == "transform":
+        Z = P @ (_operand(H_full, gemm) @ _operand(W, gemm))
+    else:
+        Z = _operand(A, gemm) @ _operand(W, gemm)
     H = np.maximum(Z, 0.0) if relu else Z
     return A, Z, H
 
 
 def layer_backward(P, A: np.ndarray, Z: np.ndarray, J: np.ndarray, W: np.ndarray,
-                   relu: bool, input_grad: bool, gemm: str = "f64"):
+                   relu: bool, input_grad: bool, gemm: str = "f64", order: str = "agg", H_full=None):
+    """``order="transform"`` needs the layer input H_full (inner and boundary rows) instead of A."""
     M = J * (Z > 0.0) if relu else J
+    if order == "transform":
+        Tq = _operand(P.T @ M, gemm)
+        G = _operand(H_full, gemm).T @ Tq
+        J_full = (Tq @ _operand(W, gemm).T) if input_grad else None
+        return G, J_full
     Mq = _operand(M, gemm)
     G = _operand(A, gemm).T @ Mq
     J_full = (P.T @ (Mq @ _operand(W, gemm).T)) if input_grad else None

@@ -68,6 +68,7 @@ class Options:
     x_bd_preload: bool = False
     ema_init: str = "zero"          # "zero" | "first"
     gemm: str = "f64"               # "f64" | "bf16" (operands of the update products rounded to bf16)
+    order: str = "agg"              # GCN layer association: "agg" (P H) W, "transform" P (H W), "auto": transform if f_out < f_in
     model: str = "gcn"              # "gcn" | "sage"
     dropout: float = 0.0
     seed: int = 0
@@ -75,6 +76,14 @@ class Options:
     beta1: float = 0.9
     beta2: float = 0.999
     eps: float = 1e-8
+
+
+def layer_order(o: Options, W: np.ndarray) -> str:
+    """The association a GCN layer with weights W [f_in, f_out] is evaluated in."""
+    if o.order == "auto":
+        return "transform" if W.shape[1] < W.shape[0] else "agg"
+    assert o.order in ("agg", "transform")
+    return o.order
 
 
 @dataclass
@@ -122,6 +131,9 @@ class Simulation:
     def _relu(self, l):
         return l < self.L or self.opts.relu_last
 
+    def _order(self, l):
+        return layer_order(self.opts, self.W[l - 1])
+
     def _use_features(self, i, l, t):
         """Boundary rows that layer l of partition i reads at iteration t."""
         st, p, o = self.state[i], self.parts[i], self.opts
@@ -165,7 +177,7 @@ class Simulation:
         pipe = o.mode == "pipe"
         rec = [dict(t=t, W_in=[w.copy() for w in self.W], state_in=self.state[i].copy(),
                     adam_in=([m.copy() for m in self.adam_m], [v.copy() for v in self.adam_v]),
-                    A={}, Z={}, H={}, H_bd_used={}, C_used={}, J_full={}, G={}, X_in={}, mask={},
+                    A={}, Z={}, H={}, H_bd_used={}, C_used={}, J_full={}, G={}, X_in={}, X_full={}, mask={},
                     send_f={}, send_g={}) for i in range(self.nparts)]
         H_prev = [self.X[p.inner_gid] for p in self.parts]
 
@@ -189,8 +201,10 @@ class Simulation:
                 if o.model == "sage":
                     A, Z, H = layers.sage_forward(self.P[i], X, p.n_inner, self.W[l - 1], self._relu(l), o.gemm)
                 else:
-                    A, Z, H = layers.layer_forward(self.P[i], X, self.W[l - 1], self._relu(l), o.gemm)
+                    A, Z, H = layers.layer_forward(self.P[i], X, self.W[l - 1], self._relu(l), o.gemm,
+                                                   self._order(l))
                 rec[i]["A"][l], rec[i]["Z"][l], rec[i]["H"][l] = A, Z, H
+                rec[i]["X_full"][l] = X
                 H_prev[i] = H
             if pipe:
                 # messages sent in this iteration are consumed in the next one
@@ -214,7 +228,8 @@ class Simulation:
                                                  self.W[l - 1], self._relu(l), l > 1, o.gemm)
                 else:
                     G, Jf = layers.layer_backward(self.P[i], rec[i]["A"][l], rec[i]["Z"][l], J[i],
-                                                  self.W[l - 1], self._relu(l), l > 1, o.gemm)
+                                                  self.W[l - 1], self._relu(l), l > 1, o.gemm,
+                                                  self._order(l), rec[i]["X_full"][l])
                 if Jf is not None:
                     Jf = Jf * rec[i]["mask"][l]
                 rec[i]["G"][l] = G
@@ -303,7 +318,7 @@ def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: di
     o = opts
     L = len(W)
     sage = o.model == "sage"
-    rec = dict(A={}, Z={}, H={}, J_full={}, G={}, send_f={}, X_in={}, mask={})
+    rec = dict(A={}, Z={}, H={}, J_full={}, G={}, send_f={}, X_in={}, X_full={}, mask={})
     H = np.asarray(X_in, dtype=np.float64)
     for l in range(1, L + 1):
         rec["send_f"][l] = H[p.send_idx]
@@ -322,8 +337,9 @@ def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: di
         if sage:
             A, Z, H = layers.sage_forward(P, X, p.n_inner, W[l - 1], relu, o.gemm)
         else:
-            A, Z, H = layers.layer_forward(P, X, W[l - 1], relu, o.gemm)
+            A, Z, H = layers.layer_forward(P, X, W[l - 1], relu, o.gemm, layer_order(o, W[l - 1]))
         rec["A"][l], rec["Z"][l], rec["H"][l] = A, Z, H
+        rec["X_full"][l] = X
     f = layers.softmax_ce if o.loss == "softmax_ce" else layers.sigmoid_bce
     rec["loss"], J = f(H, y, o.loss_scale)
     for l in range(L, 0, -1):
@@ -332,7 +348,8 @@ def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: di
             G, Jf = layers.sage_backward(P, rec["A"][l], rec["X_in"][l], rec["Z"][l], J, W[l - 1], relu, l > 1,
                                          o.gemm)
         else:
-            G, Jf = layers.layer_backward(P, rec["A"][l], rec["Z"][l], J, W[l - 1], relu, l > 1, o.gemm)
+            G, Jf = layers.layer_backward(P, rec["A"][l], rec["Z"][l], J, W[l - 1], relu, l > 1, o.gemm,
+                                          layer_order(o, W[l - 1]), rec["X_full"][l])
         rec["G"][l] = G
         if l == 1:
             break
