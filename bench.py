@@ -47,6 +47,7 @@ def algorithmic_work(tr, w, model="gcn"):
     once, every output row once.  Gather model: every non-zero gathers one
     full input row.  GEMMs: 2*M*N*K flops.
     """
+    from paper_2203_10428_amd import binding as B
     i = tr.info
     n, b, e = i["n_inner"], i["n_bd"], i["nnz"]
     items, items_t = i["spmm_items"], i["spmmt_items"]
@@ -56,18 +57,29 @@ def algorithmic_work(tr, w, model="gcn"):
     f4 = lambda f: (f + 3) // 4 * 4
     out = {k: 0.0 for k in ("agg_fwd", "agg_bwd", "agg_fwd_gather", "agg_bwd_gather", "gemm_fwd", "gemm_dgrad",
                             "gemm_wgrad")}
+    idx, idx_t = e * 4 + items * 16, e * 4 + items_t * 16
     for l in range(1, L + 1):
-        f = wd[l - 1]
-        idx = e * 4 + items * 16
+        f, fo = wd[l - 1], wd[l]
+        if tr.order[l] == B.PGCN_ORDER_TRANSFORM:
+            # P (H W): the aggregations move f_out-wide rows (Y forward, T = P^T M backward, at every
+            # layer), and the GEMMs run over the n + b inner and boundary rows
+            out["agg_fwd"] += idx + (n + b) * f4(fo) * 4 + n * f4(fo) * 4
+            out["agg_fwd_gather"] += idx + e * f4(fo) * 4 + n * f4(fo) * 4
+            out["agg_bwd"] += idx_t + n * f4(fo) * 4 + (n + b) * f4(fo) * 4
+            out["agg_bwd_gather"] += idx_t + e * f4(fo) * 4 + (n + b) * f4(fo) * 4
+            out["gemm_fwd"] += 2.0 * (n + b) * f * fo
+            out["gemm_wgrad"] += 2.0 * (n + b) * f * fo
+            if l > 1:
+                out["gemm_dgrad"] += 2.0 * (n + b) * f * fo
+            continue
         out["agg_fwd"] += idx + (n + b) * f * 4 + n * f4(f) * (6 if bf16 else 4)
         out["agg_fwd_gather"] += idx + e * f4(f) * 4 + n * f4(f) * (6 if bf16 else 4)
-        out["gemm_fwd"] += 2.0 * n * k * f * wd[l]
-        out["gemm_wgrad"] += 2.0 * n * k * f * wd[l]
+        out["gemm_fwd"] += 2.0 * n * k * f * fo
+        out["gemm_wgrad"] += 2.0 * n * k * f * fo
         if l > 1:
-            idx_t = e * 4 + items_t * 16
             out["agg_bwd"] += idx_t + n * f * 4 + (n + b) * f4(f) * 4
             out["agg_bwd_gather"] += idx_t + e * f4(f) * 4 + (n + b) * f4(f) * 4
-            out["gemm_dgrad"] += 2.0 * n * k * f * wd[l]
+            out["gemm_dgrad"] += 2.0 * n * k * f * fo
     return out
 
 
@@ -137,6 +149,8 @@ def main():
     ap.add_argument("--model", default="gcn", choices=["gcn", "sage"],
                     help="gcn: Algorithm 1's GCN layer with SGD; sage: the experiments' GraphSAGE layer with the "
                          "setup table's dropout and Adam learning rate")
+    ap.add_argument("--order", default="auto", choices=["agg", "transform", "auto"],
+                    help="GCN layer association: (P H) W, P (H W), or P (H W) where the layer narrows")
     ap.add_argument("--no-copy-modes", action="store_true", help="skip the serial / no-refill comparison")
     ap.add_argument("--refill", default="dma", choices=["dma", "blit"], help="engine of the stale-buffer refills")
     ap.add_argument("--remote", default="device", choices=["device", "host"],
@@ -180,7 +194,7 @@ def main():
     log(f"workload {w.name}: graph {g.stats} generated in {time.perf_counter() - t0:.1f}s")
     sf, sg = VARIANTS[args.variant]
     so = StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
-                     refill_dma=args.refill == "dma", remote=args.remote)
+                     refill_dma=args.refill == "dma", remote=args.remote, order=args.order)
     if args.model == "sage":
         so = StepOptions(**{**so.__dict__, "model": "sage", "dropout": w.sage_dropout, "optimizer": "adam",
                             "eta": w.sage_lr})
@@ -305,6 +319,8 @@ def main():
         "config": {"workload": w.name, "variant": args.variant,
                    "layer": "graphsage-concat" if args.model == "sage" else "gcn", "remote": args.remote,
                    "optimizer": so.optimizer, "dropout": so.dropout, "copy_mode": "pipe", "refill": args.refill,
+                   "order": args.order,
+                   "transform_first_layers": [l for l in range(1, tr.L + 1) if tr.order[l] == B.PGCN_ORDER_TRANSFORM],
                    "widths": list(w.widths),
                    "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",
                    "n_inner": i["n_inner"], "n_bd": i["n_bd"], "n_send": i["n_send"], "nnz": i["nnz"],

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 110
+#define PGCN_VERSION 120
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -78,6 +78,12 @@ enum pgcn_pack_kind {
 };
 
 enum pgcn_loss_kind { PGCN_SOFTMAX_CE = 0, PGCN_SIGMOID_BCE = 1 };
+
+/* Association in which a GCN layer evaluates its product P H W (Appendix
+ * A.1's layer function; the paper fixes none): aggregate first, (P H) W, or
+ * transform first, P (H W), which aggregates f_out instead of f_in columns
+ * and pays when the layer narrows (f_out < f_in). */
+enum pgcn_layer_order { PGCN_ORDER_AGG = 0, PGCN_ORDER_TRANSFORM = 1 };
 
 /* Global graph on the host.  Must be symmetric (u in N(v) <=> v in N(u)).
  * Duplicate entries and self loops are allowed and removed; exactly one
@@ -156,8 +162,12 @@ int pgcn_partition_export(const pgcn_partition *part, const pgcn_arrays *host_ou
 void pgcn_partition_destroy(pgcn_partition *part);
 
 /* Bytes of workspace that pgcn_layer_fwd / pgcn_layer_bwd / pgcn_loss_fwd_bwd need
- * for these widths (the maximum over the three). */
+ * for these widths (the maximum over the three), aggregate-first layers. */
 size_t pgcn_workspace_size(const pgcn_partition *part, int32_t f_in, int32_t f_out, int32_t gemm_dtype);
+/* The same for a layer evaluated in `order` (pgcn_layer_order); returns 0 for a
+ * bad order.  PGCN_ORDER_AGG gives pgcn_workspace_size. */
+size_t pgcn_layer_workspace_size(const pgcn_partition *part, int32_t f_in, int32_t f_out, int32_t gemm_dtype,
+                                 int32_t order);
 
 /*
  * One layer forward (Algorithm 1's forward update; Section 3.2 forward
@@ -170,6 +180,13 @@ size_t pgcn_workspace_size(const pgcn_partition *part, int32_t f_in, int32_t f_o
  * even) into A_bf16, W is rounded to bf16 and the product accumulates in
  * fp32; A (fp32) may then be NULL.  With PGCN_F32, A is required and A_bf16
  * ignored.
+ * order == PGCN_ORDER_TRANSFORM evaluates the same layer as
+ *     Y = [H_in ; H_bd] W            (n_inner + n_bd rows, in the workspace)
+ *     H_out = relu(P_i Y) if relu else P_i Y
+ * (bf16 path: H and W rounded to bf16, fp32 accumulation; the aggregation
+ * stays fp32).  A and A_bf16 are then unused and may be NULL; the backward
+ * takes the layer input instead.  Workspace: pgcn_layer_workspace_size with
+ * the same order.
  */
 typedef struct {
   int32_t f_in, f_out;
@@ -185,6 +202,7 @@ typedef struct {
   float *H_out;                /* [n_inner, ld_out] out                          */
   void *workspace;
   size_t workspace_bytes;
+  int32_t order;               /* pgcn_layer_order (0: aggregate first)           */
 } pgcn_fwd_args;
 int pgcn_layer_fwd(const pgcn_partition *part, const pgcn_fwd_args *args, hipStream_t stream);
 
@@ -199,6 +217,13 @@ int pgcn_layer_fwd(const pgcn_partition *part, const pgcn_fwd_args *args, hipStr
  * Stale gradients from peers are added afterwards with pgcn_pack_boundary
  * (PGCN_ACCUM_GRAD), as Algorithm 1 does after waiting for them.
  * dW accumulates split-K partials in a fixed order (deterministic).
+ * order == PGCN_ORDER_TRANSFORM (the layer's forward used that order):
+ *     T      = P_i^T M               [n_inner + n_bd, f_out], in the workspace
+ *     dW     = [H_in ; H_bd]^T T
+ *     J_full = T W^T                 rows split into J_in / J_bd_out as above
+ * H_in / H_bd are the input rows the forward used (stride ld_in; H_bd NULL
+ * means zero boundary rows); A and A_bf16 are unused.  bf16 path: H, T and W
+ * rounded to bf16 (nearest even) for the products, fp32 accumulation.
  */
 typedef struct {
   int32_t f_in, f_out;
@@ -215,6 +240,9 @@ typedef struct {
   float *J_bd_out;             /* [n_bd, ld_in] out or NULL                      */
   void *workspace;
   size_t workspace_bytes;
+  int32_t order;               /* pgcn_layer_order (0: aggregate first)           */
+  const float *H_in;           /* [n_inner, ld_in] layer input (PGCN_ORDER_TRANSFORM) */
+  const float *H_bd;           /* [n_bd, ld_in] or NULL       (PGCN_ORDER_TRANSFORM) */
 } pgcn_bwd_args;
 int pgcn_layer_bwd(const pgcn_partition *part, const pgcn_bwd_args *args, hipStream_t stream);
 
@@ -379,7 +407,7 @@ enum pgcn_trace_kind {
   PGCN_TK_AGG_FWD = 0, PGCN_TK_AGG_BWD = 1, PGCN_TK_AGG_FIXUP = 2, PGCN_TK_GEMM_FWD = 3,
   PGCN_TK_GEMM_DGRAD = 4, PGCN_TK_GEMM_WGRAD = 5, PGCN_TK_WGRAD_REDUCE = 6, PGCN_TK_EMA = 7,
   PGCN_TK_PACK = 8, PGCN_TK_ACCUM = 9, PGCN_TK_LOSS = 10, PGCN_TK_SGD = 11, PGCN_TK_REFILL = 12,
-  PGCN_TK_GEMM_PACK = 13, PGCN_TK_DROPOUT = 14, PGCN_TK_ADAM = 15
+  PGCN_TK_GEMM_PACK = 13, PGCN_TK_DROPOUT = 14, PGCN_TK_ADAM = 15, PGCN_TK_MASK_SCALE = 16
 };
 int pgcn_trace_enable(int32_t capacity);
 int pgcn_trace_filter(uint32_t kind_mask);

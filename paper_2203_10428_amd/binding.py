@@ -26,6 +26,7 @@ PGCN_SETUP_HOST_ONLY, PGCN_SETUP_NO_SELF_LOOP = 1, 2
 PGCN_PACK_FEAT, PGCN_ACCUM_GRAD = 0, 1
 PGCN_SOFTMAX_CE, PGCN_SIGMOID_BCE = 0, 1
 PGCN_REFILL_DMA, PGCN_REFILL_FROM_HOST = 1, 2
+PGCN_ORDER_AGG, PGCN_ORDER_TRANSFORM = 0, 1
 
 _vp = C.c_void_p
 _i32, _i64, _u32, _f32, _sz = C.c_int32, C.c_int64, C.c_uint32, C.c_float, C.c_size_t
@@ -55,14 +56,15 @@ class pgcn_arrays(C.Structure):
 class pgcn_fwd_args(C.Structure):
     _fields_ = [("f_in", _i32), ("f_out", _i32), ("gemm_dtype", _i32), ("relu", _i32),
                 ("ld_in", _i64), ("ld_out", _i64), ("H_in", _vp), ("H_bd", _vp), ("W", _vp),
-                ("A", _vp), ("A_bf16", _vp), ("H_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz)]
+                ("A", _vp), ("A_bf16", _vp), ("H_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz),
+                ("order", _i32)]
 
 
 class pgcn_bwd_args(C.Structure):
     _fields_ = [("f_in", _i32), ("f_out", _i32), ("gemm_dtype", _i32), ("relu", _i32),
                 ("ld_in", _i64), ("ld_out", _i64), ("J_out", _vp), ("H_out", _vp), ("A", _vp),
                 ("A_bf16", _vp), ("W", _vp), ("dW", _vp), ("J_in", _vp), ("J_bd_out", _vp),
-                ("workspace", _vp), ("workspace_bytes", _sz)]
+                ("workspace", _vp), ("workspace_bytes", _sz), ("order", _i32), ("H_in", _vp), ("H_bd", _vp)]
 
 
 class pgcn_sage_fwd_args(C.Structure):
@@ -85,6 +87,7 @@ SIGNATURES = {
     "pgcn_partition_export": (_i32, [_vp, C.POINTER(pgcn_arrays)]),
     "pgcn_partition_destroy": (None, [_vp]),
     "pgcn_workspace_size": (_sz, [_vp, _i32, _i32, _i32]),
+    "pgcn_layer_workspace_size": (_sz, [_vp, _i32, _i32, _i32, _i32]),
     "pgcn_layer_fwd": (_i32, [_vp, C.POINTER(pgcn_fwd_args), _vp]),
     "pgcn_layer_bwd": (_i32, [_vp, C.POINTER(pgcn_bwd_args), _vp]),
     "pgcn_smooth_ema": (_i32, [_vp, _vp, _i64, _i32, _i64, _f32, _vp]),
@@ -208,18 +211,24 @@ def pgcn_workspace_size(part: Partition, f_in: int, f_out: int, gemm_dtype: int 
     return int(lib.pgcn_workspace_size(part.handle, f_in, f_out, gemm_dtype))
 
 
+def pgcn_layer_workspace_size(part: Partition, f_in: int, f_out: int, gemm_dtype: int = PGCN_F32,
+                              order: int = PGCN_ORDER_AGG) -> int:
+    return int(lib.pgcn_layer_workspace_size(part.handle, f_in, f_out, gemm_dtype, order))
+
+
 def pgcn_layer_fwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, H_in, H_bd, W, A, A_bf16,
-                   H_out, workspace, workspace_bytes, stream=None):
+                   H_out, workspace, workspace_bytes, order=PGCN_ORDER_AGG, stream=None):
     a = pgcn_fwd_args(f_in, f_out, gemm_dtype, int(relu), ld_in, ld_out, _ptr(H_in), _ptr(H_bd), _ptr(W),
-                      _ptr(A), _ptr(A_bf16), _ptr(H_out), _ptr(workspace), workspace_bytes)
+                      _ptr(A), _ptr(A_bf16), _ptr(H_out), _ptr(workspace), workspace_bytes, order)
     _check(lib.pgcn_layer_fwd(part.handle, C.byref(a), _stream(stream)), "pgcn_layer_fwd")
 
 
 def pgcn_layer_bwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, J_out, H_out, A, A_bf16,
-                   W, dW, J_in, J_bd_out, workspace, workspace_bytes, stream=None):
+                   W, dW, J_in, J_bd_out, workspace, workspace_bytes, order=PGCN_ORDER_AGG, H_in=None, H_bd=None,
+                   stream=None):
     a = pgcn_bwd_args(f_in, f_out, gemm_dtype, int(relu), ld_in, ld_out, _ptr(J_out), _ptr(H_out), _ptr(A),
                       _ptr(A_bf16), _ptr(W), _ptr(dW), _ptr(J_in), _ptr(J_bd_out), _ptr(workspace),
-                      workspace_bytes)
+                      workspace_bytes, order, _ptr(H_in), _ptr(H_bd))
     _check(lib.pgcn_layer_bwd(part.handle, C.byref(a), _stream(stream)), "pgcn_layer_bwd")
 
 
@@ -277,7 +286,7 @@ def pgcn_refill_async(dst, src, nbytes: int, flags: int = 0, stream=None):
 
 
 TRACE_KINDS = ["agg_fwd", "agg_bwd", "agg_fixup", "gemm_fwd", "gemm_dgrad", "gemm_wgrad", "wgrad_reduce", "ema",
-               "pack", "accum", "loss", "sgd", "refill", "gemm_pack", "dropout", "adam"]
+               "pack", "accum", "loss", "sgd", "refill", "gemm_pack", "dropout", "adam", "mask_scale"]
 
 
 def pgcn_trace_enable(capacity: int):

@@ -64,6 +64,7 @@ struct AggParams {
   int32_t slices;         // S
   int32_t mode;           // AGG_FIRST | AGG_LAST
   int32_t accum_lo;       // rows < out_split add to the output's previous content
+  int32_t relu;           // final rows are max(x, 0)
   int64_t ld_in, ld_out, ld_bf16, ld_part;
   float *partials;
 };
@@ -88,7 +89,8 @@ __device__ __forceinline__ float *out_row(const AggParams &p, int64_t r) {
 
 // Combine this chunk's sum of float4 column c4 of row r with the running sum
 // (or, with accum_lo, with what an inner row held before the first chunk)
-// and store it (scaled, padding zeroed, bf16 copy) when this is the last chunk.
+// and store it (scaled, ReLU when asked, padding zeroed, bf16 copy) when this
+// is the last chunk.
 __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, float4 v) {
   const int c = 4 * c4;
   float *o = out_row(p, r);
@@ -103,6 +105,12 @@ __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, fl
   q.y = (c + 1 < p.f) ? v.y * s : 0.0f;
   q.z = (c + 2 < p.f) ? v.z * s : 0.0f;
   q.w = (c + 3 < p.f) ? v.w * s : 0.0f;
+  if (p.relu) {
+    q.x = q.x > 0.f ? q.x : 0.f;
+    q.y = q.y > 0.f ? q.y : 0.f;
+    q.z = q.z > 0.f ? q.z : 0.f;
+    q.w = q.w > 0.f ? q.w : 0.f;
+  }
   if (o) *reinterpret_cast<float4 *>(o + c) = q;
   if (p.out_bf16 && r < p.out_split) {
     uint2 w;
@@ -358,6 +366,7 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
   p.ld_part = (a.f + 3) / 4 * 4;
   p.partials = a.partials;
   p.accum_lo = a.accum_lo;
+  p.relu = a.relu;
   const int f4 = (a.f + 3) / 4;
   const int C = plan.chunks;
   if (f4 > kMaxAggF4) return set_error(PGCN_EINVAL, "aggregation: feature widths above 63,740 are not supported");

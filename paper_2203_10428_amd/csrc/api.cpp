@@ -63,7 +63,44 @@ uint16_t *m16_ptr(const pgcn_partition *p, void *ws, int32_t f_in, int32_t f_out
   return (uint16_t *)((char *)ws + bwd_region0(p, f_in, f_out, input_grad) + gemm_nk_workspace(f_in, f_out, dt));
 }
 
+// Transform-first layers.  Forward workspace: [Y (n+b rows, f_out wide) |
+// aggregation partials | packed weights].  Backward workspace: [T (n+b rows,
+// f_out wide) | region R | packed weights]; region R first holds D = diag(1/d)
+// M and the transposed aggregation's partials, then (both consumed) the
+// split-K partials of the weight gradient.
+int64_t ld_y(int32_t f_out) { return ld4(f_out); }
+size_t y_bytes(const pgcn_partition *p, int32_t f_out) {
+  return align_up((size_t)(p->n_inner + p->n_bd) * (size_t)ld_y(f_out) * sizeof(float), 256);
+}
+size_t fwd_tf_agg_off(const pgcn_partition *p, int32_t f_out) { return y_bytes(p, f_out); }
+size_t fwd_tf_gemm_off(const pgcn_partition *p, int32_t f_out) {
+  return y_bytes(p, f_out) + align_up(aggregate_workspace(p->plan, f_out), 256);
+}
+size_t fwd_ws_tf(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t dt) {
+  return fwd_tf_gemm_off(p, f_out) + gemm_nk_workspace(f_out, f_in, dt);
+}
+size_t bwd_tf_region(const pgcn_partition *p, int32_t f_in, int32_t f_out) {
+  const size_t g = gemm_workspace(Gemm::TN_MASK_SPLITK, f_in, f_out, (int32_t)(p->n_inner + p->n_bd));
+  const size_t d = align_up((size_t)p->n_inner * (size_t)ld_y(f_out) * sizeof(float), 256) +
+                   align_up(aggregate_workspace(p->plan_t, f_out), 256);
+  return align_up(g > d ? g : d, 256);
+}
+size_t bwd_ws_tf(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool input_grad, int32_t dt) {
+  return y_bytes(p, f_out) + bwd_tf_region(p, f_in, f_out) + (input_grad ? gemm_nk_workspace(f_in, f_out, dt) : 0);
+}
+
 }  // namespace
+
+extern "C" size_t pgcn_layer_workspace_size(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype,
+                                            int32_t order) {
+  if (order == PGCN_ORDER_AGG) return pgcn_workspace_size(p, f_in, f_out, gemm_dtype);
+  if (order != PGCN_ORDER_TRANSFORM || !p || f_in <= 0 || f_out <= 0) return 0;
+  const size_t w = fwd_ws_tf(p, f_in, f_out, gemm_dtype);
+  const size_t b = bwd_ws_tf(p, f_in, f_out, true, gemm_dtype);
+  const size_t l = align_up(loss_workspace(p->n_inner), 256);
+  const size_t m = w > b ? w : b;
+  return m > l ? m : l;
+}
 
 extern "C" size_t pgcn_workspace_size(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) {
   if (!p || f_in <= 0 || f_out <= 0) return 0;
@@ -74,6 +111,148 @@ extern "C" size_t pgcn_workspace_size(const pgcn_partition *p, int32_t f_in, int
   return m > l ? m : l;
 }
 
+namespace {
+
+// Y = [H_in ; H_bd] W, then H_out = act(P_i Y): the layer function of
+// Appendix A.1 in the association P (H W).
+int layer_fwd_transform(const pgcn_partition *p, const pgcn_fwd_args *a, hipStream_t s) {
+  if (p->n_inner > 0) {
+    PGCN_REQUIRE(a->H_in && a->W && a->H_out, "pgcn_layer_fwd: null H_in, W or H_out");
+    PGCN_REQUIRE(aligned16(a->H_in) && aligned16(a->H_bd) && aligned16(a->H_out),
+                 "pgcn_layer_fwd: H_in/H_bd/H_out must be 16-byte aligned");
+  }
+  const size_t need = fwd_ws_tf(p, a->f_in, a->f_out, a->gemm_dtype);
+  if (!a->workspace || a->workspace_bytes < need) return set_error(PGCN_EWORKSPACE, "pgcn_layer_fwd: workspace too small");
+  if (p->n_inner == 0) return PGCN_OK;
+  const int64_t ldy = ld_y(a->f_out);
+  float *Y = (float *)a->workspace;
+  const bool bd = p->n_bd > 0 && a->H_bd != nullptr;
+  GemmArgs m{};
+  m.N = a->f_out;
+  m.K = a->f_in;
+  m.dtype = a->gemm_dtype;
+  m.lda = a->ld_in;
+  m.B = a->W;
+  m.ldb = a->f_out;
+  m.ldc = ldy;
+  m.workspace = (float *)((char *)a->workspace + fwd_tf_gemm_off(p, a->f_out));
+  m.workspace_bytes = gemm_nk_workspace(a->f_out, a->f_in, a->gemm_dtype);
+  for (int part = 0; part < (bd ? 2 : 1); ++part) {
+    m.M = (int32_t)(part ? p->n_bd : p->n_inner);
+    m.A = part ? a->H_bd : a->H_in;
+    m.C = part ? Y + p->n_inner * ldy : Y;
+    int rc = launch_gemm_nk(Gemm::NN_SRC32_PLAIN, m, s);
+    if (rc) return rc;
+  }
+  AggArgs g{};
+  g.plan = &p->plan;
+  g.col = p->d_col;
+  g.in_split = p->n_inner;
+  g.in_lo = Y;
+  g.in_hi = bd ? Y + p->n_inner * ldy : nullptr;
+  g.out_split = p->n_inner;
+  g.out_lo = a->H_out;
+  g.scale = p->d_inv_deg;
+  g.f = a->f_out;
+  g.ld_in = ldy;
+  g.ld_out = a->ld_out;
+  g.partials = (float *)((char *)a->workspace + fwd_tf_agg_off(p, a->f_out));
+  g.relu = a->relu ? 1 : 0;
+  g.trace_kind = PGCN_TK_AGG_FWD;
+  return launch_aggregate(g, s);
+}
+
+// T = P_i^T M, dW = [H_in ; H_bd]^T T, J_full = T W^T.
+int layer_bwd_transform(const pgcn_partition *p, const pgcn_bwd_args *a, hipStream_t s) {
+  const bool input_grad = a->J_in != nullptr || a->J_bd_out != nullptr;
+  PGCN_REQUIRE(a->dW, "pgcn_layer_bwd: null dW");
+  if (input_grad) {
+    PGCN_REQUIRE(a->J_in && (a->J_bd_out || p->n_bd == 0),
+                 "pgcn_layer_bwd: J_in and J_bd_out must both be given (or both NULL)");
+    PGCN_REQUIRE(aligned16(a->J_in) && aligned16(a->J_bd_out), "pgcn_layer_bwd: J_in/J_bd_out must be 16-byte aligned");
+  }
+  if (p->n_inner > 0) {
+    PGCN_REQUIRE(a->J_out && a->W && a->H_in, "pgcn_layer_bwd: null J_out, W or H_in");
+    PGCN_REQUIRE(!a->relu || a->H_out, "pgcn_layer_bwd: relu needs H_out as mask source");
+    PGCN_REQUIRE(aligned16(a->J_out) && aligned16(a->H_out) && aligned16(a->H_in) && aligned16(a->H_bd),
+                 "pgcn_layer_bwd: J_out/H_out/H_in/H_bd must be 16-byte aligned");
+  }
+  const size_t need = bwd_ws_tf(p, a->f_in, a->f_out, input_grad, a->gemm_dtype);
+  if (!a->workspace || a->workspace_bytes < need) return set_error(PGCN_EWORKSPACE, "pgcn_layer_bwd: workspace too small");
+  if (p->n_inner == 0) {             // no rows (so no boundary rows): dW = 0, a split-K GEMM over no nodes
+    GemmArgs z{};
+    z.M = a->f_in;
+    z.N = a->f_out;
+    z.dtype = a->gemm_dtype;
+    z.C = a->dW;
+    z.workspace = (float *)a->workspace;
+    z.workspace_bytes = a->workspace_bytes;
+    return launch_gemm(Gemm::TN_MASK_SPLITK, z, s);
+  }
+  const int64_t ldt = ld_y(a->f_out);
+  float *T = (float *)a->workspace;
+  char *R = (char *)a->workspace + y_bytes(p, a->f_out);
+  float *D = (float *)R;
+  float *partials = (float *)(R + align_up((size_t)p->n_inner * ldt * sizeof(float), 256));
+  int rc = launch_mask_scale(a->J_out, a->ld_out, a->relu ? a->H_out : nullptr, a->ld_out, p->d_inv_deg, p->n_inner,
+                             a->f_out, D, ldt, s);
+  if (rc) return rc;
+  AggArgs t{};
+  t.plan = &p->plan_t;
+  t.col = p->d_col_t;
+  t.in_split = p->n_inner;
+  t.in_lo = D;
+  t.out_split = p->n_inner;
+  t.out_lo = T;
+  t.out_hi = T + p->n_inner * ldt;
+  t.f = a->f_out;
+  t.ld_in = ldt;
+  t.ld_out = ldt;
+  t.partials = partials;
+  t.trace_kind = PGCN_TK_AGG_BWD;
+  rc = launch_aggregate(t, s);
+  if (rc) return rc;
+
+  GemmArgs g{};
+  g.M = a->f_in;
+  g.N = a->f_out;
+  g.K = (int32_t)(p->n_inner + p->n_bd);
+  g.dtype = a->gemm_dtype;
+  g.A = a->H_in;
+  g.A_hi = p->n_bd > 0 ? a->H_bd : nullptr;
+  g.k_split = p->n_inner;
+  g.lda = a->ld_in;
+  g.B = T;
+  g.ldb = ldt;
+  g.C = a->dW;
+  g.ldc = a->f_out;
+  g.workspace = (float *)R;
+  g.workspace_bytes = bwd_tf_region(p, a->f_in, a->f_out);
+  rc = launch_gemm(Gemm::TN_MASK_SPLITK, g, s);
+  if (rc || !input_grad) return rc;
+
+  GemmArgs d{};
+  d.N = a->f_in;
+  d.K = a->f_out;
+  d.dtype = a->gemm_dtype;
+  d.lda = ldt;
+  d.B = a->W;
+  d.ldb = a->f_out;
+  d.ldc = a->ld_in;
+  d.workspace = (float *)(R + bwd_tf_region(p, a->f_in, a->f_out));
+  d.workspace_bytes = gemm_nk_workspace(a->f_in, a->f_out, a->gemm_dtype);
+  for (int part = 0; part < (p->n_bd > 0 ? 2 : 1); ++part) {
+    d.M = (int32_t)(part ? p->n_bd : p->n_inner);
+    d.A = part ? T + p->n_inner * ldt : T;
+    d.C = part ? a->J_bd_out : a->J_in;
+    rc = launch_gemm_nk(Gemm::MASK_NT_PLAIN, d, s);
+    if (rc) return rc;
+  }
+  return PGCN_OK;
+}
+
+}  // namespace
+
 extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, hipStream_t s) {
   int rc = check_part(p, "pgcn_layer_fwd");
   if (rc) return rc;
@@ -83,6 +262,8 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_layer_fwd: bad gemm_dtype");
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_layer_fwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0, "pgcn_layer_fwd: ld_out must be >= f_out and a multiple of 4");
+  PGCN_REQUIRE(a->order == PGCN_ORDER_AGG || a->order == PGCN_ORDER_TRANSFORM, "pgcn_layer_fwd: bad order");
+  if (a->order == PGCN_ORDER_TRANSFORM) return layer_fwd_transform(p, a, s);
   const bool bf16 = a->gemm_dtype == PGCN_BF16;
   if (p->n_inner > 0) {
     PGCN_REQUIRE(a->H_in && a->W && a->H_out, "pgcn_layer_fwd: null H_in, W or H_out");
@@ -150,6 +331,8 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_layer_bwd: bad gemm_dtype");
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_layer_bwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0, "pgcn_layer_bwd: ld_out must be >= f_out and a multiple of 4");
+  PGCN_REQUIRE(a->order == PGCN_ORDER_AGG || a->order == PGCN_ORDER_TRANSFORM, "pgcn_layer_bwd: bad order");
+  if (a->order == PGCN_ORDER_TRANSFORM) return layer_bwd_transform(p, a, s);
   const bool bf16 = a->gemm_dtype == PGCN_BF16;
   const bool input_grad = a->J_in != nullptr || a->J_bd_out != nullptr;
   PGCN_REQUIRE(a->dW, "pgcn_layer_bwd: null dW");

@@ -9,7 +9,10 @@
 //   - dropout of a layer input with a Philox4x32-10 mask (after the boundary
 //     receive, one mask for the forward and the backward: the paper's
 //     implementation notes);
-//   - the Adam update (the optimiser of the paper's experiments).
+//   - the Adam update (the optimiser of the paper's experiments);
+//   - the masked, row-scaled gradient diag(1/d) (J ∘ 1[H > 0]) that a
+//     transform-first layer aggregates in its backward (Appendix A.1's
+//     gradients in the other association).
 // All are float4-vectorised over the feature dimension; no float atomics.
 #include "internal.h"
 
@@ -45,6 +48,44 @@ __global__ __launch_bounds__(256) void ema_kernel(float *state, const float *in,
     v.w = gamma * v.w + g1 * x.w;
     *sp = v;
   }
+}
+
+// out[r, 4 c4 + e] = (H == null || H[r, .] > 0 ? J[r, .] : 0) * scale[r]; zero past cols
+__global__ __launch_bounds__(256) void mask_scale_kernel(const float *J, int64_t ldj, const float *H, int64_t ldh,
+                                                         const float *scale, int64_t rows, int cols, int f4,
+                                                         float *out, int64_t ldo, int sh) {
+  const int64_t r = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
+  if (r >= rows) return;
+  const float sc = scale[r];
+  for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) {
+    float4 j = reinterpret_cast<const float4 *>(J + r * ldj)[c4];
+    if (H) {
+      const float4 h = reinterpret_cast<const float4 *>(H + r * ldh)[c4];
+      j.x = h.x > 0.f ? j.x : 0.f;
+      j.y = h.y > 0.f ? j.y : 0.f;
+      j.z = h.z > 0.f ? j.z : 0.f;
+      j.w = h.w > 0.f ? j.w : 0.f;
+    }
+    const int c = 4 * c4;
+    float4 o;
+    o.x = c + 0 < cols ? j.x * sc : 0.f;
+    o.y = c + 1 < cols ? j.y * sc : 0.f;
+    o.z = c + 2 < cols ? j.z * sc : 0.f;
+    o.w = c + 3 < cols ? j.w * sc : 0.f;
+    reinterpret_cast<float4 *>(out + r * ldo)[c4] = o;
+  }
+}
+
+int launch_mask_scale(const float *J, int64_t ldj, const float *H, int64_t ldh, const float *scale, int64_t rows,
+                      int32_t cols, float *out, int64_t ldo, hipStream_t s) {
+  const int f4 = (cols + 3) / 4;
+  if (rows == 0 || f4 == 0) return PGCN_OK;
+  const int sh = lane_shift(f4);
+  TraceScope ts(PGCN_TK_MASK_SCALE, s);
+  hipLaunchKernelGGL(mask_scale_kernel, dim3(row_blocks(rows, sh)), dim3(256), 0, s, J, ldj, H, ldh, scale, rows,
+                     cols, f4, out, ldo, sh);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
 }
 
 int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_t ld, float gamma,

@@ -27,6 +27,9 @@
 // The grid is one-dimensional over (split, tile) with the tiles of a split
 // adjacent and on the same XCD, so each split's rows of A, J and H come from
 // HBM about once and are re-read from that XCD's L2.
+// A transform-first layer sums over inner and boundary rows: rows k >= ksplit
+// of the left operand come from a second matrix (A_hi), and on the bf16 path
+// that operand is fp32 in memory and rounded while staged (template A32).
 #include "internal.h"
 
 namespace pgcn {
@@ -41,9 +44,11 @@ struct TNParams {
   int M, N, K;            // M = f_in, N = f_out, K = node count
   int kchunk;             // nodes per split (a multiple of the slab)
   int tiles, tiles_n;
-  const float *A;         // fp32 [K, lda]
+  const float *A;         // fp32 [min(K, ksplit), lda]
   const uint16_t *A16;    // bf16 [K, lda]
   int64_t lda;
+  const float *A_hi;      // fp32 rows k >= ksplit (row k - ksplit, stride lda), or null: zero rows
+  int ksplit;             // K when there is no second matrix
   const float *J;         // [K, ldb]
   int64_t ldb;
   const float *H;         // mask source [K, ldh], or null (no ReLU)
@@ -118,7 +123,6 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_f32(TNParams p) {
   const int u = item % U, k4 = item / U;
   const int f0 = (isA ? m0 : n0) + 4 * u;
   const bool fok = active && f0 < (isA ? p.M : p.N);
-  const float *src = isA ? p.A : p.J;
   const int64_t ld = isA ? p.lda : p.ldb;
   const bool masked = !isA && p.H != nullptr;
 
@@ -127,8 +131,12 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_f32(TNParams p) {
     const int gk = kt + 4 * k4;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const bool ok = fok && gk + s < kend;
-      x[s] = ok ? *reinterpret_cast<const f32x4 *>(src + (int64_t)(gk + s) * ld + f0) : f32x4{0.f, 0.f, 0.f, 0.f};
+      const int node = gk + s;
+      const bool hi = isA && node >= p.ksplit;        // boundary rows of a transform-first layer
+      const float *src = isA ? (hi ? p.A_hi : p.A) : p.J;
+      const bool ok = fok && node < kend && (!hi || src != nullptr);
+      const int64_t row = hi ? node - p.ksplit : node;
+      x[s] = ok ? *reinterpret_cast<const f32x4 *>(src + row * ld + f0) : f32x4{0.f, 0.f, 0.f, 0.f};
       if (masked)
         hm[s] = ok ? *reinterpret_cast<const f32x4 *>(p.H + (int64_t)(gk + s) * p.ldh + f0)
                    : f32x4{0.f, 0.f, 0.f, 0.f};
@@ -189,7 +197,7 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_f32(TNParams p) {
 
 // ------------------------------------------------------------------ bf16 ---
 
-template <int BN>
+template <int BN, bool A32>
 __global__ __launch_bounds__(256, 3) void gemm_tn_bf16(TNParams p) {
   constexpr int BM = 128, BK = 32, LK = BK + 8;       // bf16 elements; 80-byte rows
   constexpr int UA = BM / 8, UB = BN / 4;
@@ -219,7 +227,9 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_bf16(TNParams p) {
   const bool masked = p.H != nullptr;
 
   const bool write_m16 = p.M16 != nullptr && m0 == 0 && bok;
+  const bool aok1 = aok && m0 + 8 * ua + 4 < p.M;     // A32: the second half-vector lies inside the row
   u32x4 xa[4];
+  f32x4 xf[A32 ? 8 : 1];                               // A32: fp32 rows, rounded in store()
   f32x4 xb[4], hm[4];
   int kl = 0;                                          // node of the staged slab
   auto load = [&](int kt) __attribute__((always_inline)) {
@@ -227,10 +237,21 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_bf16(TNParams p) {
     if (hasA) {
       const int gk = kt + 4 * ka;
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
-        xa[s] = (aok && gk + s < kend)
-                    ? *reinterpret_cast<const u32x4 *>(p.A16 + (int64_t)(gk + s) * p.lda + m0 + 8 * ua)
-                    : u32x4{0u, 0u, 0u, 0u};
+      for (int s = 0; s < 4; ++s) {
+        if (A32) {
+          const int node = gk + s;
+          const bool hi = node >= p.ksplit;
+          const float *src = hi ? p.A_hi : p.A;
+          const bool ok = aok && node < kend && src != nullptr;
+          const float *row = src + (int64_t)(hi ? node - p.ksplit : node) * p.lda + m0 + 8 * ua;
+          xf[2 * s] = ok ? *reinterpret_cast<const f32x4 *>(row) : f32x4{0.f, 0.f, 0.f, 0.f};
+          xf[2 * s + 1] = (ok && aok1) ? *reinterpret_cast<const f32x4 *>(row + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        } else {
+          xa[s] = (aok && gk + s < kend)
+                      ? *reinterpret_cast<const u32x4 *>(p.A16 + (int64_t)(gk + s) * p.lda + m0 + 8 * ua)
+                      : u32x4{0u, 0u, 0u, 0u};
+        }
+      }
     }
     if (hasB) {
       const int gk = kt + 4 * kb;
@@ -247,6 +268,13 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_bf16(TNParams p) {
   };
   auto store = [&](int b) __attribute__((always_inline)) {
     if (hasA) {
+      if (A32) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int w = 0; w < 4; ++w)
+            xa[s][w] = tn_bf16(xf[2 * s + w / 2][2 * (w % 2)]) | (tn_bf16(xf[2 * s + w / 2][2 * (w % 2) + 1]) << 16);
+      }
 #pragma unroll
       for (int w = 0; w < 4; ++w) {            // features 2w (low halves) and 2w + 1 (high halves)
         const u32x2 lo{(xa[0][w] & 0xffffu) | (xa[1][w] << 16), (xa[2][w] & 0xffffu) | (xa[3][w] << 16)};
@@ -367,7 +395,7 @@ size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K) {
 }
 
 template <int BN>
-static void tn_launch(TNParams p, bool bf16, int splits, hipStream_t s) {
+static void tn_launch(TNParams p, bool bf16, bool a32, int splits, hipStream_t s) {
   constexpr int BM = 128;
   p.tiles_n = (p.N + BN - 1) / BN;
   p.tiles = ((p.M + BM - 1) / BM) * p.tiles_n;
@@ -377,7 +405,8 @@ static void tn_launch(TNParams p, bool bf16, int splits, hipStream_t s) {
   if (kchunk == 0) kchunk = slab;
   p.kchunk = kchunk;
   const dim3 grid((unsigned)(p.tiles * splits));
-  if (bf16) hipLaunchKernelGGL((gemm_tn_bf16<BN>), grid, dim3(256), 0, s, p);
+  if (bf16 && a32) hipLaunchKernelGGL((gemm_tn_bf16<BN, true>), grid, dim3(256), 0, s, p);
+  else if (bf16) hipLaunchKernelGGL((gemm_tn_bf16<BN, false>), grid, dim3(256), 0, s, p);
   else hipLaunchKernelGGL((gemm_tn_f32<BN>), grid, dim3(256), 0, s, p);
 }
 
@@ -401,6 +430,11 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   p.ldh = g.ldm;
   p.partials = g.workspace;
   const bool bf16 = g.dtype == PGCN_BF16;
+  const bool a32 = g.k_split > 0;                      // second left matrix; fp32 left operand on both paths
+  p.A_hi = a32 ? g.A_hi : nullptr;
+  p.ksplit = a32 ? (int)g.k_split : g.K;
+  if (a32 && (!g.A || g.k_split > g.K || g.M16 || (g.lda % 4) != 0))
+    return set_error(PGCN_EINVAL, "weight-gradient GEMM: bad split left operand");
   if (g.M16) {
     if (!bf16 || g.ldm16 < g.N || g.ldm16 % 4 != 0 || ((uintptr_t)g.M16 & 7u))
       return set_error(PGCN_EINVAL, "weight-gradient GEMM: bad bf16 operand output");
@@ -409,8 +443,8 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   }
   {
     TraceScope ts(PGCN_TK_GEMM_WGRAD, s);
-    if (g.N <= 64) tn_launch<64>(p, bf16, splits, s);
-    else tn_launch<128>(p, bf16, splits, s);
+    if (g.N <= 64) tn_launch<64>(p, bf16, a32, splits, s);
+    else tn_launch<128>(p, bf16, a32, splits, s);
     PGCN_HIP(hipGetLastError());
   }
   const int64_t mn = (int64_t)g.M * g.N;

@@ -115,6 +115,7 @@ struct AggArgs {
   float *partials;
   int32_t trace_kind;      // PGCN_TK_AGG_FWD or PGCN_TK_AGG_BWD
   int32_t accum_lo;        // 1: rows [0, out_split) add to what out_lo holds (GraphSAGE self term)
+  int32_t relu;            // 1: the final rows are max(x, 0) (transform-first forward)
 };
 int launch_aggregate(const AggArgs &a, hipStream_t s);
 size_t aggregate_workspace(const Plan &plan, int64_t f);
@@ -122,10 +123,11 @@ size_t aggregate_workspace(const Plan &plan, int64_t f);
 // NN_*: C (=|+=) A W, with ReLU for *_RELU (ACC: C = act(C + A W));
 // MASK_NT_*: C = (J ∘ mask) W^T, row-scaled or plain (fp32 J and mask; rounded to bf16 on the
 // bf16 path); NT16_*: the same with the masked operand already bf16 in A16;
-// TN_MASK_SPLITK: C = A^T (J ∘ mask)
+// NN_SRC32_PLAIN: C = A W from the fp32 operand on both paths (rounded to bf16 while staged on
+// the bf16 path); TN_MASK_SPLITK: C = A^T (J ∘ mask)
 enum class Gemm {
   NN_RELU, NN_PLAIN, NN_ACC_RELU, NN_ACC_PLAIN, MASK_NT_ROWSCALE, MASK_NT_PLAIN, NT16_ROWSCALE, NT16_PLAIN,
-  TN_MASK_SPLITK
+  NN_SRC32_PLAIN, TN_MASK_SPLITK
 };
 struct GemmArgs {
   int32_t M, N, K;
@@ -144,6 +146,11 @@ struct GemmArgs {
   size_t workspace_bytes;
   uint16_t *M16;            // TN_MASK_SPLITK, bf16 path: also write bf16(B ∘ mask) [K, ldm16] (or null)
   int64_t ldm16;
+  // TN_MASK_SPLITK with k_split > 0: rows k >= k_split of the left operand come from
+  // A_hi[k - k_split] (null: zero rows), and on the bf16 path A (fp32) is rounded
+  // while staged instead of reading A16
+  const float *A_hi;
+  int64_t k_split;
 };
 int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s);
 size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K);
@@ -151,6 +158,9 @@ size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K);
 int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s);
 size_t gemm_nk_workspace(int32_t N, int32_t K, int32_t dtype);
 
+// out[r, c] = (H == null || H[r, c] > 0 ? J[r, c] : 0) * scale[r] for c < cols, 0 for c in [cols, ld4(cols))
+int launch_mask_scale(const float *J, int64_t ldj, const float *H, int64_t ldh, const float *scale, int64_t rows,
+                      int32_t cols, float *out, int64_t ldo, hipStream_t s);
 int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_t ld, float gamma,
                hipStream_t s);
 int launch_dropout(float *out, const float *in, int64_t rows, int32_t cols, int64_t ld, int64_t row0, uint32_t thr,

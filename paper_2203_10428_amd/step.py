@@ -28,6 +28,10 @@ and smoothing, and the same mask multiplies the input gradient before it is
 sent or accumulated (the paper's implementation notes); the mask comes from
 the library's counter-based generator keyed by (``seed``, partition) and
 counted by (layer, iteration).  ``optimizer``: Algorithm 1's SGD or Adam.
+
+``order`` picks the association of each GCN layer's product P H W:
+``"agg"`` (P H) W, ``"transform"`` P (H W), ``"auto"`` transform-first where
+the layer narrows (f_out < f_in), which aggregates fewer columns.
 """
 from __future__ import annotations
 
@@ -61,6 +65,14 @@ class StepOptions:
     beta1: float = 0.9
     beta2: float = 0.999
     eps: float = 1e-8
+    order: str = "agg"               # "agg" | "transform" | "auto" (GCN layers)
+
+
+def layer_order(order: str, f_in: int, f_out: int) -> int:
+    """libpgcn order of a GCN layer f_in -> f_out under the option ``order``."""
+    assert order in ("agg", "transform", "auto"), order
+    tf = order == "transform" or (order == "auto" and f_out < f_in)
+    return B.PGCN_ORDER_TRANSFORM if tf else B.PGCN_ORDER_AGG
 
 
 class PartitionTrainer:
@@ -115,9 +127,12 @@ class PartitionTrainer:
         self.Xd_16 = {l: z(n, wd[l - 1], torch.bfloat16) for l in range(1, L + 1)} \
             if (self.sage and not f32) else {}
         self.G_peer = [None] * L
-        # activations, indexed by layer 1..L
-        self.A = {l: (z(n, wd[l - 1]) if f32 else None) for l in range(1, L + 1)}
-        self.A16 = {l: (None if f32 else z(n, wd[l - 1], torch.bfloat16)) for l in range(1, L + 1)}
+        self.order = {l: (B.PGCN_ORDER_AGG if self.sage else layer_order(opts.order, wd[l - 1], wd[l]))
+                      for l in range(1, L + 1)}
+        # activations, indexed by layer 1..L (a transform-first layer keeps no aggregate)
+        agg = {l: self.order[l] == B.PGCN_ORDER_AGG for l in range(1, L + 1)}
+        self.A = {l: (z(n, wd[l - 1]) if f32 and agg[l] else None) for l in range(1, L + 1)}
+        self.A16 = {l: (None if f32 or not agg[l] else z(n, wd[l - 1], torch.bfloat16)) for l in range(1, L + 1)}
         self.H = {l: z(n, wd[l]) for l in range(1, L + 1)}
         self.J_top = z(n, wd[L])
         self.J_in = {l: z(n, wd[l - 1]) for l in range(2, L + 1)}
@@ -144,10 +159,12 @@ class PartitionTrainer:
         self.refill_bytes = sum(t.numel() * 4 for t in self.remote_f.values()) + \
             sum(t.numel() * 4 for t in self.remote_g.values())
         self.X_used = {}                  # layer input the forward used (the GraphSAGE self operand)
+        self.X_bd_used = {}               # boundary rows the forward used (transform-first backward)
         self.cur = 0                      # index of the buffer read in this iteration
         self.t = 0
         self.loss = torch.zeros(1, dtype=torch.float32, device=self.dev)
-        ws = max(B.pgcn_workspace_size(self.part, wd[l - 1], wd[l], self.dtype) for l in range(1, L + 1))
+        ws = max(B.pgcn_layer_workspace_size(self.part, wd[l - 1], wd[l], self.dtype, self.order[l])
+                 for l in range(1, L + 1))
         self.ws_bytes = max(ws, 256)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
         self.stream = torch.cuda.Stream(device=self.dev)
@@ -191,8 +208,9 @@ class PartitionTrainer:
         if self.sage:
             B.pgcn_sage_layer_fwd(self.part, X_in=X_in, X_in_bf16=X16, X_bd=X_bd, **common)
         else:
-            B.pgcn_layer_fwd(self.part, H_in=X_in, H_bd=X_bd, **common)
+            B.pgcn_layer_fwd(self.part, H_in=X_in, H_bd=X_bd, order=self.order[l], **common)
         self.X_used[l] = X_in
+        self.X_bd_used[l] = X_bd
 
     def _backward_layer(self, l, J_out, st):
         """Layer gradients; the input gradient then takes the forward's dropout mask."""
@@ -204,7 +222,7 @@ class PartitionTrainer:
         if self.sage:
             B.pgcn_sage_layer_bwd(self.part, X_in=self.X_used[l], X_in_bf16=self.Xd_16.get(l), **common)
         else:
-            B.pgcn_layer_bwd(self.part, **common)
+            B.pgcn_layer_bwd(self.part, order=self.order[l], H_in=self.X_used[l], H_bd=self.X_bd_used[l], **common)
         if l > 1 and self.opts.dropout > 0.0:
             self._dropout(self.J_in[l], self.J_in[l], self.n, l, 0, None, st)
             self._dropout(self.J_bd_out[l], self.J_bd_out[l], self.b, l, self.n, None, st)

@@ -14,9 +14,16 @@ computes one by one from the definitions, straight from the global graph:
 Sampled rows include random rows, the longest rows (split into segments) and
 boundary rows.  Local numbering is recomputed here from its definition (rank
 of the global id; boundary by (owner, id)), independent of the library.
+
+The transform-first layers the bench runs (every narrowing layer: the last
+one, and the first on the Reddit-like workload) are checked the same way:
+forward rows from (sum of the neighbourhood's H rows) W / d_v, and the
+backward from T = P_i^T M built here as a sparse matrix from the global
+graph (G columns = H_full^T T, sampled rows of J = T W^T).
 """
 import numpy as np
 import pytest
+import scipy.sparse as sp
 import torch
 
 from gpu_helpers import TOL
@@ -52,6 +59,27 @@ class Full:
         self.local_inner = np.full(g.n, -1, np.int64)
         self.local_inner[self.inner] = np.arange(self.n)
 
+    def local_ids(self):
+        """Local id of every global node (inner by rank, boundary after them by (owner, id)); -1 elsewhere."""
+        loc = np.full(self.g.n, -1, np.int64)
+        loc[self.inner] = np.arange(self.n)
+        loc[self.bd] = self.n + np.arange(self.b)
+        return loc
+
+    def propagation_t(self):
+        """P_i^T as a sparse [(n + b) x n] matrix: entry (u, v) = 1 / d_v for u in N(v) or u = v."""
+        g = self.g
+        starts, lens = g.rowptr[self.inner], self.deg[self.inner]
+        idx = np.repeat(starts - np.concatenate([[0], np.cumsum(lens)[:-1]]), lens) + np.arange(lens.sum())
+        rows = np.repeat(np.arange(self.n), lens)
+        cols = self.local_ids()[g.col[idx]]
+        assert (cols >= 0).all()
+        d = (lens + 1).astype(np.float64)
+        vals = np.concatenate([1.0 / d[rows], 1.0 / d])
+        r = np.concatenate([cols, np.arange(self.n)])
+        c = np.concatenate([rows, np.arange(self.n)])
+        return sp.csr_matrix((vals, (r, c)), shape=(self.n + self.b, self.n))
+
     def neighbours(self, gid):
         return self.g.col[self.g.rowptr[gid]:self.g.rowptr[gid + 1]].astype(np.int64)
 
@@ -63,9 +91,7 @@ class Full:
 
 
 def full(name) -> Full:
-    if name not in _CACHE:
-        _CACHE.clear()                                   # one large workload resident at a time
-        torch.cuda.empty_cache()
+    if name not in _CACHE:                               # the four partitions stay resident (a few GB)
         _CACHE[name] = Full(name)
     return _CACHE[name]
 
@@ -180,8 +206,9 @@ def test_backward_layer_full_size(name):
     assert rel(got_bd, ref_bd) < tol, name
 
 
+@pytest.mark.parametrize("order", ["agg", "auto"])
 @pytest.mark.parametrize("name", WORKLOADS)
-def test_full_step_is_finite_and_deterministic(name):
+def test_full_step_is_finite_and_deterministic(name, order):
     """Three PipeGCN-GF iterations of the bench configuration, run twice: finite and bitwise equal."""
     from paper_2203_10428_amd.step import PartitionTrainer, StepOptions
     F = full(name)
@@ -190,7 +217,8 @@ def test_full_step_is_finite_and_deterministic(name):
     outs = []
     for _ in range(2):
         tr = PartitionTrainer(F.g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, w.gemm_dtype,
-                              StepOptions(smooth_f=True, smooth_g=True, gamma=w.gamma, eta=w.eta, copy_mode="pipe"))
+                              StepOptions(smooth_f=True, smooth_g=True, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
+                                          order=order))
         losses = []
         for _ in range(3):
             tr.step()
@@ -203,3 +231,79 @@ def test_full_step_is_finite_and_deterministic(name):
     assert outs[0][0] == outs[1][0]
     for a, b in zip(outs[0][1], outs[1][1]):
         assert torch.equal(a, b)
+
+
+def narrowing_layers(w):
+    return [l for l in range(1, len(w.widths)) if w.widths[l] < w.widths[l - 1]]
+
+
+@pytest.mark.parametrize("name", WORKLOADS)
+def test_transform_forward_full_size(name):
+    F = full(name)
+    w = F.w
+    dt = B.PGCN_BF16 if w.gemm_dtype == "bf16" else B.PGCN_F32
+    tol = TOL["bf16" if dt == B.PGCN_BF16 else "f32"]["act"]
+    rng = np.random.default_rng(11)
+    L = len(w.widths) - 1
+    for layer in narrowing_layers(w):
+        f_in, f_out = w.widths[layer - 1], w.widths[layer]
+        relu = layer < L
+        Hg = rng.standard_normal((F.g.n, f_in)).astype(np.float32)
+        W = rng.uniform(-0.1, 0.1, (f_in, f_out)).astype(np.float32)
+        H = torch.zeros((F.n, ld_of(f_out)), device="cuda")
+        nb = B.pgcn_layer_workspace_size(F.part, f_in, f_out, dt, B.PGCN_ORDER_TRANSFORM)
+        ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        B.pgcn_layer_fwd(F.part, f_in=f_in, f_out=f_out, gemm_dtype=dt, relu=relu, ld_in=ld_of(f_in),
+                         ld_out=ld_of(f_out), H_in=upload(Hg[F.inner]), H_bd=upload(Hg[F.bd]),
+                         W=torch.from_numpy(W).cuda(), A=None, A_bf16=None, H_out=H, workspace=ws,
+                         workspace_bytes=nb, order=B.PGCN_ORDER_TRANSFORM)
+        torch.cuda.synchronize()
+        rows = F.sample_inner(48, layer + 7)
+        H_gpu = H[torch.from_numpy(rows).cuda(), :f_out].cpu().numpy()
+        Hd = round_bf16(Hg) if dt == B.PGCN_BF16 else Hg.astype(np.float64)
+        Wd = round_bf16(W) if dt == B.PGCN_BF16 else W.astype(np.float64)
+        Z_ref = np.zeros((len(rows), f_out))
+        for k, r in enumerate(rows):
+            gid = F.inner[r]
+            nbrs = F.neighbours(gid)
+            Z_ref[k] = ((Hd[gid] + Hd[nbrs].sum(0)) @ Wd) / (len(nbrs) + 1)
+        ref = np.maximum(Z_ref, 0) if relu else Z_ref
+        assert rel(H_gpu, ref) < tol, (name, layer)
+        del H, ws
+
+
+@pytest.mark.parametrize("name", WORKLOADS)
+def test_transform_backward_full_size(name):
+    F = full(name)
+    w = F.w
+    dt = B.PGCN_BF16 if w.gemm_dtype == "bf16" else B.PGCN_F32
+    tol = TOL["bf16" if dt == B.PGCN_BF16 else "f32"]["grad"]
+    rng = np.random.default_rng(12)
+    L = len(w.widths) - 1
+    f_in, f_out = w.widths[L - 1], w.widths[L]           # the last layer: narrowing, with an input gradient
+    H_full = rng.standard_normal((F.n + F.b, f_in)).astype(np.float32)
+    J = (rng.standard_normal((F.n, f_out)) * 1e-3).astype(np.float32)
+    W = rng.uniform(-0.1, 0.1, (f_in, f_out)).astype(np.float32)
+    dG = torch.zeros((f_in, f_out), device="cuda")
+    J_in = torch.zeros((F.n, ld_of(f_in)), device="cuda")
+    J_bd = torch.zeros((F.b, ld_of(f_in)), device="cuda")
+    nb = B.pgcn_layer_workspace_size(F.part, f_in, f_out, dt, B.PGCN_ORDER_TRANSFORM)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    B.pgcn_layer_bwd(F.part, f_in=f_in, f_out=f_out, gemm_dtype=dt, relu=False, ld_in=ld_of(f_in),
+                     ld_out=ld_of(f_out), J_out=upload(J), H_out=None, A=None, A_bf16=None,
+                     W=torch.from_numpy(W).cuda(), dW=dG, J_in=J_in, J_bd_out=J_bd, workspace=ws,
+                     workspace_bytes=nb, order=B.PGCN_ORDER_TRANSFORM, H_in=upload(H_full[:F.n]),
+                     H_bd=upload(H_full[F.n:]))
+    torch.cuda.synchronize()
+    T = F.propagation_t() @ J.astype(np.float64)          # no ReLU on the last layer: M = J
+    Hd, Wd = H_full.astype(np.float64), W.astype(np.float64)
+    if dt == B.PGCN_BF16:
+        T, Hd, Wd = round_bf16(T), round_bf16(Hd), round_bf16(Wd)
+    cols = rng.choice(f_out, 6, replace=False)
+    assert rel(dG.cpu().numpy()[:, cols], Hd.T @ T[:, cols]) < tol, name
+    rows_in = F.sample_inner(24, 13)
+    got_in = J_in[torch.from_numpy(rows_in).cuda(), :f_in].cpu().numpy()
+    assert rel(got_in, T[rows_in] @ Wd.T) < tol, name
+    rows_bd = np.unique(np.concatenate([rng.choice(F.b, 24, replace=False), np.argsort(-F.deg[F.bd])[:2]]))
+    got_bd = J_bd[torch.from_numpy(rows_bd).cuda(), :f_in].cpu().numpy()
+    assert rel(got_bd, T[F.n + rows_bd] @ Wd.T) < tol, name

@@ -52,7 +52,7 @@ def compare_step(tr: PartitionTrainer, rec0, dt, L, widths, check_state=True):
     n = tr.n
     errs = {}
     for l in range(1, L + 1):
-        if dt == "f32":
+        if dt == "f32" and tr.A[l] is not None:          # a transform-first layer keeps no aggregate
             errs[f"A{l}"] = (rel_err(get(tr.A[l], widths[l - 1]), rec0["A"][l]), tol["act"])
         errs[f"H{l}"] = (rel_err(get(tr.H[l], widths[l]), rec0["H"][l]), tol["act"])
         errs[f"send_f{l}"] = (rel_err(get(tr.send_f[l], widths[l - 1]), rec0["send_f"][l]), tol["act"])
