@@ -30,6 +30,8 @@
 // A transform-first layer sums over inner and boundary rows: rows k >= ksplit
 // of the left operand come from a second matrix (A_hi), and on the bf16 path
 // that operand is fp32 in memory and rounded while staged (template A32).
+#include <algorithm>
+
 #include "internal.h"
 
 namespace pgcn {
@@ -96,16 +98,23 @@ __device__ __forceinline__ void tn_store_partial(const TNParams &p, const f32x16
 }
 
 // ------------------------------------------------------------------ fp32 ---
+//
+// v_mfma_f32_32x32x2f32 takes one node per lane half (k = lane / 32), so the
+// fp32 kernel keeps both tiles node-major in LDS (rows of 128 + 32 floats: the
+// two lane halves read rows k and k + 1 on disjoint banks) and needs no
+// transpose: every thread stages 16-byte vectors of whole node rows (A, J and
+// H alike, coalesced over the row), and the next-but-one slab is loaded into a
+// second register set, so each load has two slabs of MFMAs to arrive.
 
 template <int BN>
-__global__ __launch_bounds__(256, 3) void gemm_tn_f32(TNParams p) {
-  constexpr int BM = 128, BK = 16, LK = BK + 4;
-  constexpr int UA = BM / 4, UB = BN / 4;
-  constexpr int NA = UA * (BK / 4), NB = UB * (BK / 4);
-  static_assert(NA + NB <= 256, "staging items exceed the workgroup");
+__global__ __launch_bounds__(256, BN == 128 ? 2 : 3) void gemm_tn_f32(TNParams p) {
+  constexpr int BM = 128, BK = 16;                     // BK nodes per slab
+  constexpr int LDA = BM + 32, LDB = BN + 32;
+  constexpr int VA = BK * BM / 4 / 256, VB = BK * BN / 4 / 256;
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
-  __shared__ __attribute__((aligned(16))) float As[2][BM * LK];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LK];
+  static_assert(VA >= 1 && VB >= 1, "slab smaller than the workgroup");
+  __shared__ __attribute__((aligned(16))) float As[2][BK * LDA];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BK * LDB];
 
   const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
   int split, tile;
@@ -114,46 +123,49 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_f32(TNParams p) {
   const int kbeg = split * p.kchunk;
   const int kend = min(p.K, kbeg + p.kchunk);
   const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
+  const bool masked = p.H != nullptr;
+  // vector v of this thread: node (t + 256 v) / (B/4) of the slab, features 4 ((t + 256 v) % (B/4)) ..
+  const int ca = 4 * (t % (BM / 4)), na = t / (BM / 4);
+  const int cb = 4 * (t % (BN / 4)), nb = t / (BN / 4);
+  constexpr int SA = 256 / (BM / 4), SB = 256 / (BN / 4);   // node step between a thread's vectors
+  const bool fa = m0 + ca < p.M, fb = n0 + cb < p.N;
 
-  // staging role (uniform per wave): A block for t < NA, J/H block after
-  const bool isA = t < NA;
-  const int item = isA ? t : t - NA;
-  const bool active = isA || item < NB;
-  const int U = isA ? UA : UB;
-  const int u = item % U, k4 = item / U;
-  const int f0 = (isA ? m0 : n0) + 4 * u;
-  const bool fok = active && f0 < (isA ? p.M : p.N);
-  const int64_t ld = isA ? p.lda : p.ldb;
-  const bool masked = !isA && p.H != nullptr;
-
-  f32x4 x[4], hm[4];
-  auto load = [&](int kt) __attribute__((always_inline)) {
-    const int gk = kt + 4 * k4;
+  struct Regs {
+    f32x4 a[VA], b[VB], h[VB];
+  };
+  auto load = [&](Regs &R, int kt) __attribute__((always_inline)) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int node = gk + s;
-      const bool hi = isA && node >= p.ksplit;        // boundary rows of a transform-first layer
-      const float *src = isA ? (hi ? p.A_hi : p.A) : p.J;
-      const bool ok = fok && node < kend && (!hi || src != nullptr);
+    for (int v = 0; v < VA; ++v) {
+      const int node = kt + na + SA * v;
+      const bool hi = node >= p.ksplit;                 // boundary rows of a transform-first layer
+      const float *src = hi ? p.A_hi : p.A;
+      const bool ok = fa && node < kend && src != nullptr;
       const int64_t row = hi ? node - p.ksplit : node;
-      x[s] = ok ? *reinterpret_cast<const f32x4 *>(src + row * ld + f0) : f32x4{0.f, 0.f, 0.f, 0.f};
+      R.a[v] = ok ? *reinterpret_cast<const f32x4 *>(src + row * p.lda + m0 + ca) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int v = 0; v < VB; ++v) {
+      const int node = kt + nb + SB * v;
+      const bool ok = fb && node < kend;
+      R.b[v] = ok ? *reinterpret_cast<const f32x4 *>(p.J + (int64_t)node * p.ldb + n0 + cb)
+                  : f32x4{0.f, 0.f, 0.f, 0.f};
       if (masked)
-        hm[s] = ok ? *reinterpret_cast<const f32x4 *>(p.H + (int64_t)(gk + s) * p.ldh + f0)
-                   : f32x4{0.f, 0.f, 0.f, 0.f};
+        R.h[v] = ok ? *reinterpret_cast<const f32x4 *>(p.H + (int64_t)node * p.ldh + n0 + cb)
+                    : f32x4{0.f, 0.f, 0.f, 0.f};
     }
   };
-  auto store = [&](int b) __attribute__((always_inline)) {
-    if (!active) return;
-    if (masked) {
+  auto store = [&](Regs &R, int buf) __attribute__((always_inline)) {
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
+    for (int v = 0; v < VA; ++v) *reinterpret_cast<f32x4 *>(&As[buf][(na + SA * v) * LDA + ca]) = R.a[v];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) x[s][e] = hm[s][e] > 0.f ? x[s][e] : 0.f;
+    for (int v = 0; v < VB; ++v) {
+      f32x4 x = R.b[v];
+      if (masked) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = R.h[v][e] > 0.f ? x[e] : 0.f;
+      }
+      *reinterpret_cast<f32x4 *>(&Bs[buf][(nb + SB * v) * LDB + cb]) = x;
     }
-    float *base = isA ? As[b] : Bs[b];
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      *reinterpret_cast<f32x4 *>(&base[(e * U + u) * LK + 4 * k4]) = f32x4{x[0][e], x[1][e], x[2][e], x[3][e]};
   };
 
   f32x16 acc[TM][TN];
@@ -163,42 +175,62 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_f32(TNParams p) {
     for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
 
   const int h = lane >> 5, r = lane & 31;
-  if (kbeg < kend) {
-    load(kbeg);
-    store(0);
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < BK / 2; ++s) {                 // nodes 2s (lanes 0-31) and 2s + 1 (lanes 32-63)
+      const float *ar = &As[buf][(2 * s + h) * LDA + wm0 + r];
+      const float *br = &Bs[buf][(2 * s + h) * LDB + wn0 + r];
+      float a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) a[i] = ar[i * 32];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) b[j] = br[j * 32];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  const int ns = (kend - kbeg + BK - 1) / BK;          // slabs of this split (<= 0: none)
+  if (ns > 0) {
+    Regs R0, R1;
+    load(R0, kbeg);
+    load(R1, kbeg + BK);                               // past kend: zero vectors, no loads
+    store(R0, 0);
     __syncthreads();
-    int it = 0;
-    for (int kt = kbeg; kt < kend; kt += BK, ++it) {
-      const int cur = it & 1;
-      load(kt + BK < kend ? kt + BK : kt);     // the last slab refills the idle buffer with itself
-#pragma unroll
-      for (int q = 0; q < BK / 8; ++q) {
-        f32x4 a[TM], b[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          a[i] = *reinterpret_cast<const f32x4 *>(&As[cur][(wm0 + i * 32 + r) * LK + 8 * h + 4 * q]);
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          b[j] = *reinterpret_cast<const f32x4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + 8 * h + 4 * q]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
-      }
-      store(cur ^ 1);
+    for (int sl = 0; sl < ns; sl += 2) {
+      load(R0, kbeg + (sl + 2) * BK);
+      compute(0);
+      store(R1, 1);
+      __syncthreads();
+      if (sl + 1 >= ns) break;
+      load(R1, kbeg + (sl + 3) * BK);
+      compute(1);
+      store(R0, 0);
       __syncthreads();
     }
   }
-  tn_store_partial<TM, TN, UA, 4, UB>(p, acc, split, m0, n0, wm0, wn0, lane);
+
+  // output: row = A feature m0 + wm0 + 32 i + 8 (reg / 4) + 4 h + reg % 4, column = J feature n0 + wn0 + 32 j + r
+  float *out = p.partials + (int64_t)split * p.M * p.N;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int fn = n0 + wn0 + j * 32 + r;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int fm = m0 + wm0 + i * 32 + 8 * (q / 4) + 4 * h + (q % 4);
+        if (fm < p.M && fn < p.N) out[(int64_t)fm * p.N + fn] = acc[i][j][q];
+      }
+  }
 }
 
 // ------------------------------------------------------------------ bf16 ---
 
 template <int BN, bool A32>
-__global__ __launch_bounds__(256, 3) void gemm_tn_bf16(TNParams p) {
+__global__ __launch_bounds__(256, (BN == 128 && A32) ? 2 : 3) void gemm_tn_bf16(TNParams p) {
   constexpr int BM = 128, BK = 32, LK = BK + 8;       // bf16 elements; 80-byte rows
   constexpr int UA = BM / 8, UB = BN / 4;
   constexpr int NA = UA * (BK / 4), NB = UB * (BK / 4);
@@ -374,12 +406,19 @@ static int tn_tiles(int M, int N) {
   return ((M + 127) / 128) * ((N + BN - 1) / BN);
 }
 
+// Resident workgroups of a variant on 256 CUs: three per CU, two for the
+// 128-wide tiles whose staging holds two slabs (fp32) or fp32 rows (bf16 with
+// an fp32 left operand).
+static int tn_slots(int N, bool bf16, bool a32) {
+  return (N > 64 && (!bf16 || a32)) ? 512 : 768;
+}
+
 // Splits over the nodes: tiles x splits about one round of resident
-// workgroups (three per CU on 256 CUs), at least 256 nodes per split, and
-// tiles x splits a multiple of 8 when possible (XCD mapping).
-static int splitk_count(int M, int N, int K) {
+// workgroups, at least 256 nodes per split, and tiles x splits a multiple of 8
+// when possible (XCD mapping).
+static int splitk_count(int M, int N, int K, int slots) {
   const int tiles = tn_tiles(M, N);
-  int s = 768 / tiles;
+  int s = slots / tiles;
   const int max_s = (K + 255) / 256;
   if (s > max_s) s = max_s;
   if (s < 1) s = 1;
@@ -391,7 +430,8 @@ static int splitk_count(int M, int N, int K) {
 
 size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K) {
   if (kind != Gemm::TN_MASK_SPLITK) return 0;
-  return (size_t)splitk_count(M, N, K) * (size_t)M * (size_t)N * sizeof(float);
+  const int s = std::max(splitk_count(M, N, K, 512), splitk_count(M, N, K, 768));   // any variant
+  return (size_t)s * (size_t)M * (size_t)N * sizeof(float);
 }
 
 template <int BN>
@@ -413,7 +453,9 @@ static void tn_launch(TNParams p, bool bf16, bool a32, int splits, hipStream_t s
 int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   if (kind != Gemm::TN_MASK_SPLITK) return set_error(PGCN_EINVAL, "launch_gemm: only the weight-gradient GEMM");
   if (g.M <= 0 || g.N <= 0) return PGCN_OK;
-  const int splits = splitk_count(g.M, g.N, g.K);
+  const bool bf16 = g.dtype == PGCN_BF16;
+  const bool a32 = g.k_split > 0;                      // second left matrix; fp32 left operand on both paths
+  const int splits = splitk_count(g.M, g.N, g.K, tn_slots(g.N, bf16, a32));
   const size_t need = (size_t)splits * (size_t)g.M * (size_t)g.N * sizeof(float);
   if (!g.workspace || g.workspace_bytes < need)
     return set_error(PGCN_EWORKSPACE, "weight-gradient GEMM: workspace too small");
@@ -429,8 +471,6 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   p.H = g.Hmask;
   p.ldh = g.ldm;
   p.partials = g.workspace;
-  const bool bf16 = g.dtype == PGCN_BF16;
-  const bool a32 = g.k_split > 0;                      // second left matrix; fp32 left operand on both paths
   p.A_hi = a32 ? g.A_hi : nullptr;
   p.ksplit = a32 ? (int)g.k_split : g.K;
   if (a32 && (!g.A || g.k_split > g.K || g.M16 || (g.lda % 4) != 0))
