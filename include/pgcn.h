@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 120
+#define PGCN_VERSION 130
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -265,6 +265,19 @@ int pgcn_pack_boundary(const pgcn_partition *part, int32_t kind, const float *sr
                        int32_t cols, int64_t ld, hipStream_t stream);
 
 /*
+ * Smoothing of the received gradients (Section 3.4) fused with their
+ * accumulation (Algorithm 1's loop over peers j): for every send row k,
+ *     state[k, :] = gamma * state[k, :] + (1 - gamma) * incoming[k, :]
+ * and dst[u, :] += state[k, :] for each k with send_idx[k] == u, in ascending
+ * k.  The same values as pgcn_smooth_ema(state, incoming, n_send, ...)
+ * followed by pgcn_pack_boundary(PGCN_ACCUM_GRAD, state, dst, ...), in one
+ * pass.  incoming and state: [n_send, ld]; dst: [n_inner, ld]; ld % 4 == 0,
+ * 16-byte aligned; state must not alias incoming or dst.
+ */
+int pgcn_accum_smoothed(const pgcn_partition *part, const float *incoming, float *state, float gamma, float *dst,
+                        int32_t cols, int64_t ld, hipStream_t stream);
+
+/*
  * Loss and its gradient w.r.t. the logits (Algorithm 1's J^(L)):
  *   PGCN_SOFTMAX_CE : loss = scale * sum_r -log softmax(Z_r)[labels[r]]
  *                     J_r  = scale * (softmax(Z_r) - onehot(labels[r]))
@@ -407,7 +420,8 @@ enum pgcn_trace_kind {
   PGCN_TK_AGG_FWD = 0, PGCN_TK_AGG_BWD = 1, PGCN_TK_AGG_FIXUP = 2, PGCN_TK_GEMM_FWD = 3,
   PGCN_TK_GEMM_DGRAD = 4, PGCN_TK_GEMM_WGRAD = 5, PGCN_TK_WGRAD_REDUCE = 6, PGCN_TK_EMA = 7,
   PGCN_TK_PACK = 8, PGCN_TK_ACCUM = 9, PGCN_TK_LOSS = 10, PGCN_TK_SGD = 11, PGCN_TK_REFILL = 12,
-  PGCN_TK_GEMM_PACK = 13, PGCN_TK_DROPOUT = 14, PGCN_TK_ADAM = 15, PGCN_TK_MASK_SCALE = 16
+  PGCN_TK_GEMM_PACK = 13, PGCN_TK_DROPOUT = 14, PGCN_TK_ADAM = 15, PGCN_TK_MASK_SCALE = 16,
+  PGCN_TK_ACCUM_EMA = 17
 };
 int pgcn_trace_enable(int32_t capacity);
 int pgcn_trace_filter(uint32_t kind_mask);

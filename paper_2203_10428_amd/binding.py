@@ -92,6 +92,7 @@ SIGNATURES = {
     "pgcn_layer_bwd": (_i32, [_vp, C.POINTER(pgcn_bwd_args), _vp]),
     "pgcn_smooth_ema": (_i32, [_vp, _vp, _i64, _i32, _i64, _f32, _vp]),
     "pgcn_pack_boundary": (_i32, [_vp, _i32, _vp, _vp, _i32, _i64, _vp]),
+    "pgcn_accum_smoothed": (_i32, [_vp, _vp, _vp, _f32, _vp, _i32, _i64, _vp]),
     "pgcn_loss_fwd_bwd": (_i32, [_i32, _vp, _i64, _i32, _i64, _vp, _vp, _i64, _f32, _vp, _vp, _vp, _sz, _vp]),
     "pgcn_sgd_update": (_i32, [_vp, _vp, _vp, _i64, _f32, _vp]),
     "pgcn_adam_update": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, C.c_double, C.c_double, C.c_double, C.c_double,
@@ -281,12 +282,18 @@ def pgcn_sage_layer_bwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in
     _check(lib.pgcn_sage_layer_bwd(part.handle, C.byref(a), _stream(stream)), "pgcn_sage_layer_bwd")
 
 
+def pgcn_accum_smoothed(part: Partition, incoming, state, gamma: float, dst, cols: int, ld: int, stream=None):
+    _check(lib.pgcn_accum_smoothed(part.handle, _ptr(incoming), _ptr(state), gamma, _ptr(dst), cols, ld,
+                                   _stream(stream)), "pgcn_accum_smoothed")
+
+
 def pgcn_refill_async(dst, src, nbytes: int, flags: int = 0, stream=None):
     _check(lib.pgcn_refill_async(_ptr(dst), _ptr(src), nbytes, flags, _stream(stream)), "pgcn_refill_async")
 
 
 TRACE_KINDS = ["agg_fwd", "agg_bwd", "agg_fixup", "gemm_fwd", "gemm_dgrad", "gemm_wgrad", "wgrad_reduce", "ema",
-               "pack", "accum", "loss", "sgd", "refill", "gemm_pack", "dropout", "adam", "mask_scale"]
+               "pack", "accum", "loss", "sgd", "refill", "gemm_pack", "dropout", "adam", "mask_scale",
+               "accum_ema"]
 
 
 def pgcn_trace_enable(capacity: int):

@@ -675,6 +675,19 @@ extern "C" int pgcn_pack_boundary(const pgcn_partition *p, int32_t kind, const f
   return launch_accum(p->d_inv_ptr, p->d_inv_k, p->n_inner, src, dst, cols, ld, s);
 }
 
+extern "C" int pgcn_accum_smoothed(const pgcn_partition *p, const float *incoming, float *state, float gamma,
+                                   float *dst, int32_t cols, int64_t ld, hipStream_t s) {
+  int rc = check_part(p, "pgcn_accum_smoothed");
+  if (rc) return rc;
+  PGCN_REQUIRE(cols >= 0 && ld >= cols && ld % 4 == 0, "pgcn_accum_smoothed: bad shape or stride");
+  PGCN_REQUIRE(std::isfinite(gamma), "pgcn_accum_smoothed: gamma must be finite");
+  if (p->n_send == 0 || cols == 0) return PGCN_OK;
+  PGCN_REQUIRE(incoming && state && dst && aligned16(incoming) && aligned16(state) && aligned16(dst),
+               "pgcn_accum_smoothed: null or unaligned buffer");
+  PGCN_REQUIRE(state != incoming && state != dst, "pgcn_accum_smoothed: state aliases another buffer");
+  return launch_accum_ema(p->d_inv_ptr, p->d_inv_k, p->n_inner, incoming, state, gamma, dst, cols, ld, s);
+}
+
 extern "C" int pgcn_loss_fwd_bwd(int32_t kind, const float *Z, int64_t rows, int32_t classes, int64_t ld,
                                  const int32_t *labels, const float *targets, int64_t ld_t, float scale, float *J,
                                  float *loss_out, void *workspace, size_t workspace_bytes, hipStream_t s) {

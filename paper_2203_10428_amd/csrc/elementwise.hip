@@ -139,6 +139,53 @@ __global__ __launch_bounds__(256) void accum_kernel(const int64_t *inv_ptr, cons
   }
 }
 
+// The gradient smoothing of Section 3.4 fused into the accumulation: every
+// send row k belongs to exactly one inner row u (send_idx[k] == u), so the
+// thread that adds row k into u also updates its moving average, once:
+//     state[k] = gamma state[k] + (1 - gamma) src[k];  dst[u] += state[k]
+// (the moving average is read once instead of twice).
+__global__ __launch_bounds__(256) void accum_ema_kernel(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows,
+                                                        const float *src, float *state, float gamma, float *dst,
+                                                        int f4, int64_t ld, int sh) {
+  const int64_t u = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
+  if (u >= rows) return;
+  const int64_t b = inv_ptr[u], e = inv_ptr[u + 1];
+  if (b == e) return;
+  const float g1 = 1.0f - gamma;
+  float4 *d = reinterpret_cast<float4 *>(dst + u * ld);
+  for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) {
+    float4 v = d[c4];
+    for (int64_t q = b; q < e; ++q) {   // ascending send-list position: ascending peer
+      const int64_t k = inv_k[q];
+      const float4 x = reinterpret_cast<const float4 *>(src + k * ld)[c4];
+      float4 *sp = reinterpret_cast<float4 *>(state + k * ld) + c4;
+      float4 m = *sp;
+      m.x = gamma * m.x + g1 * x.x;
+      m.y = gamma * m.y + g1 * x.y;
+      m.z = gamma * m.z + g1 * x.z;
+      m.w = gamma * m.w + g1 * x.w;
+      *sp = m;
+      v.x += m.x;
+      v.y += m.y;
+      v.z += m.z;
+      v.w += m.w;
+    }
+    d[c4] = v;
+  }
+}
+
+int launch_accum_ema(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, const float *src, float *state,
+                     float gamma, float *dst, int32_t cols, int64_t ld, hipStream_t s) {
+  const int f4 = (cols + 3) / 4;
+  if (rows == 0 || f4 == 0) return PGCN_OK;
+  const int sh = lane_shift(f4);
+  TraceScope ts(PGCN_TK_ACCUM_EMA, s);
+  hipLaunchKernelGGL(accum_ema_kernel, dim3(row_blocks(rows, sh)), dim3(256), 0, s, inv_ptr, inv_k, rows, src,
+                     state, gamma, dst, f4, ld, sh);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
+}
+
 int launch_accum(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, const float *src, float *dst,
                  int32_t cols, int64_t ld, hipStream_t s) {
   const int f4 = (cols + 3) / 4;

@@ -383,20 +383,47 @@ __global__ __launch_bounds__(256, (BN == 128 && A32) ? 2 : 3) void gemm_tn_bf16(
 }
 
 // Fixed-order sum of split partials.  A block owns 64 consecutive outputs and
-// 4 quarters of the split range; quarter q adds its splits in ascending order,
-// then the quarters are added in order q = 0, 1, 2, 3.
+// G ranges of the split index: thread (g, c) adds the splits of range g in
+// ascending order for outputs V c .. V c + V - 1 (16-byte loads when
+// mn % 4 == 0, V = 4, G = 16), then the G range sums of each output are added
+// in order g = 0 .. G - 1.  Many short independent sums keep enough loads in
+// flight for partials that number in the hundreds per output.
+template <int V>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *ws, int splits, int64_t mn, float *out) {
-  __shared__ float part[4][64];
-  const int o = threadIdx.x % 64, q = threadIdx.x / 64;
-  const int64_t i = (int64_t)blockIdx.x * 64 + o;
-  const int per = (splits + 3) / 4;
-  const int z0 = q * per, z1 = min(splits, z0 + per);
-  float s = 0.f;
-  if (i < mn)
-    for (int z = z0; z < z1; ++z) s += ws[(int64_t)z * mn + i];
-  part[q][o] = s;
+  constexpr int C = 64 / V, G = 256 / C;
+  __shared__ float part[G][64];
+  const int c = threadIdx.x % C, g = threadIdx.x / C;
+  const int64_t i0 = (int64_t)blockIdx.x * 64 + V * c;
+  const int per = (splits + G - 1) / G;
+  const int z0 = g * per, z1 = min(splits, z0 + per);
+  float s[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) s[e] = 0.f;
+  if (i0 < mn) {                                       // V = 4: mn % 4 == 0, so i0 + 3 < mn
+#pragma unroll 4
+    for (int z = z0; z < z1; ++z) {
+      if constexpr (V == 4) {
+        const float4 x = *reinterpret_cast<const float4 *>(ws + (int64_t)z * mn + i0);
+        s[0] += x.x;
+        s[1] += x.y;
+        s[2] += x.z;
+        s[3] += x.w;
+      } else {
+        s[0] += ws[(int64_t)z * mn + i0];
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < V; ++e) part[g][V * c + e] = s[e];
   __syncthreads();
-  if (q == 0 && i < mn) out[i] = ((part[0][o] + part[1][o]) + part[2][o]) + part[3][o];
+  const int o = threadIdx.x;
+  const int64_t i = (int64_t)blockIdx.x * 64 + o;
+  if (o < 64 && i < mn) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < G; ++k) t += part[k][o];
+    out[i] = t;
+  }
 }
 
 // ---------------------------------------------------------------- launch ---
@@ -489,8 +516,11 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   }
   const int64_t mn = (int64_t)g.M * g.N;
   TraceScope ts(PGCN_TK_WGRAD_REDUCE, s);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((mn + 63) / 64)), dim3(256), 0, s,
-                     (const float *)g.workspace, splits, mn, g.C);
+  const dim3 rgrid((unsigned)((mn + 63) / 64));
+  if (mn % 4 == 0 && ((uintptr_t)g.workspace & 15u) == 0)   // every partial [M x N] starts 16-byte aligned
+    hipLaunchKernelGGL(splitk_reduce_kernel<4>, rgrid, dim3(256), 0, s, (const float *)g.workspace, splits, mn, g.C);
+  else
+    hipLaunchKernelGGL(splitk_reduce_kernel<1>, rgrid, dim3(256), 0, s, (const float *)g.workspace, splits, mn, g.C);
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;
 }

@@ -176,6 +176,8 @@ int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst,
                 int64_t ld, hipStream_t s);
 int launch_accum(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, const float *src,
                  float *dst, int32_t cols, int64_t ld, hipStream_t s);
+int launch_accum_ema(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, const float *src, float *state,
+                     float gamma, float *dst, int32_t cols, int64_t ld, hipStream_t s);
 int launch_loss(int32_t kind, const float *Z, int64_t rows, int32_t classes, int64_t ld,
                 const int32_t *labels, const float *targets, int64_t ld_t, float scale, float *J,
                 float *loss_out, float *ws, hipStream_t s);

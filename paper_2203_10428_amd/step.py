@@ -278,10 +278,10 @@ class PartitionTrainer:
                 if mode == "pipe":
                     st.wait_event(self.ev_grad[l])
                 C = self.grad[l][cur]
-                if o.smooth_g:
-                    B.pgcn_smooth_ema(self.ema_g[l], C, s, f, ld_of(f), o.gamma, st)
-                    C = self.ema_g[l]
-                B.pgcn_pack_boundary(self.part, B.PGCN_ACCUM_GRAD, C, self.J_in[l], f, ld_of(f), st)
+                if o.smooth_g:      # smoothing of the received rows fused with their accumulation
+                    B.pgcn_accum_smoothed(self.part, C, self.ema_g[l], o.gamma, self.J_in[l], f, ld_of(f), st)
+                else:
+                    B.pgcn_pack_boundary(self.part, B.PGCN_ACCUM_GRAD, C, self.J_in[l], f, ld_of(f), st)
             if mode == "pipe":
                 self.ev_bwd[l].record(st)
                 side.wait_event(self.ev_bwd[l])

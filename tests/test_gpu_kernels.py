@@ -177,6 +177,35 @@ def test_pack_and_accumulate(f):
     assert rel_err(host(dJ, f), ref) < 1e-6
 
 
+@pytest.mark.parametrize("f", [1, 5, 64, 602])
+def test_accum_smoothed(f):
+    """Gradient smoothing fused with the accumulation: the moving average of every send row,
+    then each row added into its inner row in ascending send-list order."""
+    g = Graph(n_inner=1200, n_pool=2000, nparts=5, mean_deg=10, seed=7)
+    p = g.ref
+    rng = np.random.default_rng(f + 100)
+    C = rng.standard_normal((len(p.send_idx), f))
+    state = rng.standard_normal((len(p.send_idx), f))
+    Jin = rng.standard_normal((p.n_inner, f))
+    gamma = 0.95
+    d_state, dJ, dC = dev(state), dev(Jin), dev(C)
+    B.pgcn_accum_smoothed(g.part, dC, d_state, gamma, dJ, f, ld_of(f))
+    st_ref = layers.ema(state, C, gamma)
+    ref = Jin.copy()
+    for j in range(g.nparts):                        # Algorithm 1: ascending peer j
+        a, b = p.send_ptr[j], p.send_ptr[j + 1]
+        ref[p.send_idx[a:b]] += st_ref[a:b]
+    assert rel_err(host(d_state, f), st_ref) < 1e-6
+    assert rel_err(host(dJ, f), ref) < 1e-6
+    # the same as the two separate calls
+    d_state2, dJ2 = dev(state), dev(Jin)
+    B.pgcn_smooth_ema(d_state2, dC, len(p.send_idx), f, ld_of(f), gamma)
+    B.pgcn_pack_boundary(g.part, B.PGCN_ACCUM_GRAD, d_state2, dJ2, f, ld_of(f))
+    assert rel_err(host(d_state2, f), host(d_state, f)) < 1e-6 and rel_err(host(dJ2, f), host(dJ, f)) < 1e-6
+    with pytest.raises(B.PgcnError, match="aliases"):
+        B.pgcn_accum_smoothed(g.part, dC, dC, gamma, dJ, f, ld_of(f))
+
+
 @pytest.mark.parametrize("rows,f", [(1, 1), (1000, 602), (4099, 41)])
 def test_smooth_ema(rows, f):
     rng = np.random.default_rng(rows)
