@@ -27,6 +27,12 @@ C++ builder's output comparable bit for bit):
 * the inverse send map lists, per inner row u, the positions k of the send
   list with send[k] == u, ascending.
 
+Symmetric normalisation (the D̃^{-1/2} Ã D̃^{-1/2} of the paper's appendix,
+``norm="sym"`` in ``propagation_matrix``): entry (v, u) of P_i is
+1 / sqrt(d̃_v d̃_u) with d̃ = degree + 1 of the whole graph, so the degrees of
+the boundary nodes (``deg``) come from their full neighbourhoods, not only
+from the edges to partition i.
+
 Pinned by: a pure-Python brute force from the dense adjacency (tests).
 """
 from __future__ import annotations
@@ -52,6 +58,7 @@ class Partition:
     send_idx: np.ndarray       # int32 [s]  inner local ids, S_{i,0} .. S_{i,nparts-1}
     inv_ptr: np.ndarray        # int64 [n+1]
     inv_k: np.ndarray          # int32 [s]
+    deg: np.ndarray            # int64 [n+b]  whole-graph degree + 1 of every local node
 
     @property
     def n_inner(self) -> int:
@@ -149,17 +156,31 @@ def build_partition(n: int, rowptr: np.ndarray, col: np.ndarray, owner: np.ndarr
     inv_ptr = np.zeros(n_in + 1, dtype=np.int64)
     np.cumsum(np.bincount(send_idx, minlength=n_in), out=inv_ptr[1:])
 
+    # whole-graph degree + 1 of the inner and boundary nodes (distinct neighbours, no self loop)
+    loc_gid = np.concatenate([inner_gid, bd_gid])
+    rr, cc = _row_pairs(rowptr, col, loc_gid)
+    rr = np.unique(rr * n + cc) // n
+    deg = np.bincount(np.searchsorted(np.sort(loc_gid), rr), minlength=len(loc_gid))
+    deg = deg[np.argsort(np.argsort(loc_gid))].astype(np.int64) + 1
+
     return Partition(part, nparts, inner_gid, bd_gid, bd_owner, recv_ptr,
-                     p_rowptr, p_col, t_rowptr, t_col, send_ptr, send_idx, inv_ptr, inv_k)
+                     p_rowptr, p_col, t_rowptr, t_col, send_ptr, send_idx, inv_ptr, inv_k, deg)
 
 
-def propagation_matrix(p: Partition):
-    """P_i as a SciPy CSR matrix, entries 1/d_v with d_v the row length (degree + 1, or the
-    degree without self loops)."""
+def propagation_matrix(p: Partition, norm: str = "mean"):
+    """P_i as a SciPy CSR matrix.  ``mean``: entries 1/d_v with d_v the row length (degree + 1,
+    or the degree without self loops).  ``sym``: entries 1/sqrt(d̃_v d̃_u), d̃ = whole-graph
+    degree + 1 (self loops required)."""
     import scipy.sparse as sp
     d = np.diff(p.rowptr)
-    inv = np.zeros(len(d))
-    inv[d > 0] = 1.0 / d[d > 0]
-    vals = np.repeat(inv, d)
+    if norm == "sym":
+        assert np.array_equal(d, p.deg[: p.n_inner]), "symmetric normalisation needs the self loops"
+        rows = np.repeat(np.arange(p.n_inner), d)
+        vals = 1.0 / np.sqrt(p.deg[rows].astype(np.float64) * p.deg[p.col].astype(np.float64))
+    else:
+        assert norm == "mean", norm
+        inv = np.zeros(len(d))
+        inv[d > 0] = 1.0 / d[d > 0]
+        vals = np.repeat(inv, d)
     return sp.csr_matrix((vals, p.col.astype(np.int64), p.rowptr),
                          shape=(p.n_inner, p.n_inner + p.n_bd))

@@ -69,6 +69,7 @@ class Options:
     ema_init: str = "zero"          # "zero" | "first"
     gemm: str = "f64"               # "f64" | "bf16" (operands of the update products rounded to bf16)
     order: str = "agg"              # GCN layer association: "agg" (P H) W, "transform" P (H W), "auto": transform if f_out < f_in
+    norm: str = "mean"              # GCN propagation matrix: "mean" D̃⁻¹Ã, "sym" D̃^{-1/2} Ã D̃^{-1/2}
     model: str = "gcn"              # "gcn" | "sage"
     dropout: float = 0.0
     seed: int = 0
@@ -109,7 +110,7 @@ class Simulation:
         self.parts: list[Partition] = [build_partition(n, rowptr, col, owner, i, nparts,
                                                        self_loop=opts.model == "gcn")
                                        for i in range(nparts)]
-        self.P = [propagation_matrix(p) for p in self.parts]
+        self.P = [propagation_matrix(p, opts.norm) for p in self.parts]
         self.X = np.asarray(X, dtype=np.float64)
         self.labels = labels
         self.W = [np.asarray(w, dtype=np.float64).copy() for w in W0]
