@@ -104,8 +104,9 @@ def measured_traffic(workload: str, kernel: str):
     return rec["kernels"].get(kernel)
 
 
-def cpu_baseline(w, scale: float, model: str = "gcn"):
-    """Time the fp64 oracle's per-partition step on a sample of the workload."""
+def cpu_baseline(w, scale: float, model: str = "gcn", order: str = "agg", norm: str = "mean"):
+    """Time the fp64 oracle's per-partition step on a sample of the workload (same layer
+    association and normalisation as the GPU run)."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -117,7 +118,7 @@ def cpu_baseline(w, scale: float, model: str = "gcn"):
     g = configs.make_graph(ws)
     d = configs.make_dense(ws, g.n, model=model)
     p = build_partition(g.n, g.rowptr, g.col, g.owner, 0, g.nparts, self_loop=model == "gcn")
-    P = propagation_matrix(p)
+    P = propagation_matrix(p, norm)
     rng = np.random.default_rng(7)
     L = w.layers
     recv_f = {l: rng.standard_normal((p.n_bd, w.widths[l - 1])) for l in range(1, L + 1)}
@@ -126,7 +127,7 @@ def cpu_baseline(w, scale: float, model: str = "gcn"):
     ema_g = {l: np.zeros_like(v) for l, v in recv_g.items()}
     sf, sg = VARIANTS["PipeGCN-GF"]
     opts = Options(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, loss=w.loss, loss_scale=w.loss_scale,
-                   gemm="bf16" if w.gemm_dtype == "bf16" else "f64")
+                   gemm="bf16" if w.gemm_dtype == "bf16" else "f64", order=order, norm=norm)
     if model == "sage":
         opts = Options(**{**opts.__dict__, "model": "sage", "dropout": w.sage_dropout, "optimizer": "adam",
                           "eta": w.sage_lr})
@@ -151,6 +152,8 @@ def main():
                          "setup table's dropout and Adam learning rate")
     ap.add_argument("--order", default="auto", choices=["agg", "transform", "auto"],
                     help="GCN layer association: (P H) W, P (H W), or P (H W) where the layer narrows")
+    ap.add_argument("--norm", default="mean", choices=["mean", "sym"],
+                    help="GCN propagation matrix: mean D^-1 (A+I) or symmetric D^-1/2 (A+I) D^-1/2")
     ap.add_argument("--no-copy-modes", action="store_true", help="skip the serial / no-refill comparison")
     ap.add_argument("--refill", default="dma", choices=["dma", "blit"], help="engine of the stale-buffer refills")
     ap.add_argument("--remote", default="device", choices=["device", "host"],
@@ -194,7 +197,7 @@ def main():
     log(f"workload {w.name}: graph {g.stats} generated in {time.perf_counter() - t0:.1f}s")
     sf, sg = VARIANTS[args.variant]
     so = StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
-                     refill_dma=args.refill == "dma", remote=args.remote, order=args.order)
+                     refill_dma=args.refill == "dma", remote=args.remote, order=args.order, norm=args.norm)
     if args.model == "sage":
         so = StepOptions(**{**so.__dict__, "model": "sage", "dropout": w.sage_dropout, "optimizer": "adam",
                             "eta": w.sage_lr})
@@ -290,7 +293,7 @@ def main():
         try:
             if args.cpu_sample is None:
                 args.cpu_sample = 0.4 if args.model == "gcn" else 0.15
-            sec, n_s, nnz_s, threads = cpu_baseline(w, args.cpu_sample, args.model)
+            sec, n_s, nnz_s, threads = cpu_baseline(w, args.cpu_sample, args.model, args.order, args.norm)
             scale = tr.info["nnz"] / nnz_s
             cpu = {"value": 1.0 / (sec * scale), "unit": "steps/s", "cores": threads, "kind": "oracle",
                    "sample": (f"fp64 oracle per-partition step ({args.model}, PipeGCN-GF, t=2) on the same graph law at "
@@ -319,7 +322,7 @@ def main():
         "config": {"workload": w.name, "variant": args.variant,
                    "layer": "graphsage-concat" if args.model == "sage" else "gcn", "remote": args.remote,
                    "optimizer": so.optimizer, "dropout": so.dropout, "copy_mode": "pipe", "refill": args.refill,
-                   "order": args.order,
+                   "order": args.order, "norm": args.norm,
                    "transform_first_layers": [l for l in range(1, tr.L + 1) if tr.order[l] == B.PGCN_ORDER_TRANSFORM],
                    "widths": list(w.widths),
                    "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",

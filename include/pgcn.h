@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 130
+#define PGCN_VERSION 140
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -65,11 +65,18 @@ enum pgcn_setup_flags {
                                    device upload; compute calls on such a handle
                                    return PGCN_EINVAL (used to test the builder
                                    without a GPU) */
-  PGCN_SETUP_NO_SELF_LOOP = 2   /* P_i is the mean over N(v) without the self loop
+  PGCN_SETUP_NO_SELF_LOOP = 2,  /* P_i is the mean over N(v) without the self loop
                                    (the GraphSAGE layer's aggregation, Section 2):
                                    entries 1/d_v with d_v = degree; a row without
                                    neighbours is zero.  The sets V_i, B_i, S_{i,j}
                                    are unchanged. */
+  PGCN_SETUP_SYMMETRIC = 4      /* P_i is the symmetric normalisation of Appendix
+                                   A.1, rows of D̃^{-1/2} (A + I) D̃^{-1/2}: entries
+                                   1 / sqrt(d̃_v d̃_u) with d̃ the whole-graph degree + 1
+                                   of every inner and boundary node (the boundary
+                                   nodes' degrees come from their full rows of the
+                                   global CSR).  GCN layers only; not with
+                                   PGCN_SETUP_NO_SELF_LOOP. */
 };
 
 enum pgcn_pack_kind {
@@ -123,6 +130,8 @@ typedef struct {
   int64_t spmmt_split_slots;
   int32_t spmm_chunks;     /* column chunks (cache blocking) of P_i           */
   int32_t spmmt_chunks;    /* column chunks of P_i^T                          */
+  int32_t symmetric;       /* 1 if built with PGCN_SETUP_SYMMETRIC            */
+  int32_t self_loop;       /* 0 if built with PGCN_SETUP_NO_SELF_LOOP         */
 } pgcn_info;
 
 /* Caller-allocated host buffers for pgcn_partition_export, sized from pgcn_info.
@@ -142,6 +151,8 @@ typedef struct {
   int32_t *send_idx;       /* [n_send] inner local ids        */
   int64_t *inv_ptr;        /* [n_inner+1]                     */
   int32_t *inv_k;          /* [n_send] positions into send_idx, ascending per row */
+  int64_t *deg;            /* [n_inner+n_bd] whole-graph degree + 1 (distinct
+                              neighbours, no self loop, plus one) */
 } pgcn_arrays;
 
 /*

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_PKG, "libpgcn.so")
 
 PGCN_OK, PGCN_EINVAL, PGCN_ENOMEM, PGCN_EHIP, PGCN_EUNSUPPORTED, PGCN_EWORKSPACE = range(6)
 PGCN_F32, PGCN_BF16 = 0, 1
-PGCN_SETUP_HOST_ONLY, PGCN_SETUP_NO_SELF_LOOP = 1, 2
+PGCN_SETUP_HOST_ONLY, PGCN_SETUP_NO_SELF_LOOP, PGCN_SETUP_SYMMETRIC = 1, 2, 4
 PGCN_PACK_FEAT, PGCN_ACCUM_GRAD = 0, 1
 PGCN_SOFTMAX_CE, PGCN_SIGMOID_BCE = 0, 1
 PGCN_REFILL_DMA, PGCN_REFILL_FROM_HOST = 1, 2
@@ -45,12 +45,12 @@ class pgcn_info(C.Structure):
                 ("max_row_len", _i64), ("max_row_len_t", _i64), ("nparts", _i32), ("self", _i32),
                 ("host_only", _i32), ("spmm_segment", _i32), ("spmm_items", _i64),
                 ("spmm_split_slots", _i64), ("spmmt_items", _i64), ("spmmt_split_slots", _i64),
-                ("spmm_chunks", _i32), ("spmmt_chunks", _i32)]
+                ("spmm_chunks", _i32), ("spmmt_chunks", _i32), ("symmetric", _i32), ("self_loop", _i32)]
 
 
 class pgcn_arrays(C.Structure):
     _fields_ = [(n, _vp) for n in ("inner_gid", "bd_gid", "recv_ptr", "rowptr", "col", "rowptr_t",
-                                    "col_t", "send_ptr", "send_idx", "inv_ptr", "inv_k")]
+                                    "col_t", "send_ptr", "send_idx", "inv_ptr", "inv_k", "deg")]
 
 
 class pgcn_fwd_args(C.Structure):
@@ -177,14 +177,16 @@ class Partition:
 
 
 def pgcn_partition_setup(n: int, rowptr: np.ndarray, col: np.ndarray, owner: np.ndarray,
-                         nparts: int, self_part: int, host_only: bool = False, self_loop: bool = True) -> Partition:
+                         nparts: int, self_part: int, host_only: bool = False, self_loop: bool = True,
+                         symmetric: bool = False) -> Partition:
     rowptr = np.ascontiguousarray(rowptr, dtype=np.int64)
     col = np.ascontiguousarray(col, dtype=np.int32)
     owner = np.ascontiguousarray(owner, dtype=np.int32)
     csr = pgcn_csr(n, rowptr.ctypes.data, col.ctypes.data if len(col) else None)
     bmap = pgcn_boundary_map(nparts, self_part, owner.ctypes.data)
     out = _vp()
-    flags = (PGCN_SETUP_HOST_ONLY if host_only else 0) | (0 if self_loop else PGCN_SETUP_NO_SELF_LOOP)
+    flags = (PGCN_SETUP_HOST_ONLY if host_only else 0) | (0 if self_loop else PGCN_SETUP_NO_SELF_LOOP) | \
+        (PGCN_SETUP_SYMMETRIC if symmetric else 0)
     _check(lib.pgcn_partition_setup(C.byref(csr), C.byref(bmap), flags, C.byref(out)), "pgcn_partition_setup")
     return Partition(out.value)
 
@@ -202,7 +204,7 @@ def pgcn_partition_export(part: Partition) -> dict:
                rowptr=np.empty(n + 1, np.int64), col=np.empty(nnz, np.int32),
                rowptr_t=np.empty(n + b + 1, np.int64), col_t=np.empty(nnz, np.int32),
                send_ptr=np.empty(P + 1, np.int64), send_idx=np.empty(s, np.int32),
-               inv_ptr=np.empty(n + 1, np.int64), inv_k=np.empty(s, np.int32))
+               inv_ptr=np.empty(n + 1, np.int64), inv_k=np.empty(s, np.int32), deg=np.empty(n + b, np.int64))
     arr = pgcn_arrays(**{k: (v.ctypes.data if v.size else None) for k, v in out.items()})
     _check(lib.pgcn_partition_export(part.handle, C.byref(arr)), "pgcn_partition_export")
     return out

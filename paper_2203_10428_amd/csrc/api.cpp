@@ -31,8 +31,14 @@ size_t fwd_acc_bytes(const pgcn_partition *p, int32_t f_in, int32_t gemm_dtype) 
 size_t fwd_agg_bytes(const pgcn_partition *p, int32_t f_in, int32_t gemm_dtype) {
   return align_up(aggregate_workspace(p->plan, f_in), 256) + fwd_acc_bytes(p, f_in, gemm_dtype);
 }
-size_t fwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) {
+// symmetric normalisation, aggregate-first: the gathered rows scaled by d̃_u^{-1/2}
+size_t fwd_sym_off(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) {
   return fwd_agg_bytes(p, f_in, gemm_dtype) + gemm_nk_workspace(f_out, f_in, gemm_dtype);
+}
+size_t fwd_ws(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) {
+  const size_t sym = p->symmetric ? align_up((size_t)(p->n_inner + p->n_bd) * (size_t)ld4(f_in) * sizeof(float), 256)
+                                  : 0;
+  return fwd_sym_off(p, f_in, f_out, gemm_dtype) + sym;
 }
 
 // Region 0 of the backward workspace first holds the split-K partials of the
@@ -137,11 +143,12 @@ int layer_fwd_transform(const pgcn_partition *p, const pgcn_fwd_args *a, hipStre
   m.ldc = ldy;
   m.workspace = (float *)((char *)a->workspace + fwd_tf_gemm_off(p, a->f_out));
   m.workspace_bytes = gemm_nk_workspace(a->f_out, a->f_in, a->gemm_dtype);
-  for (int part = 0; part < (bd ? 2 : 1); ++part) {
+  for (int part = 0; part < (bd ? 2 : 1); ++part) {    // symmetric: rows of Y scaled by d̃_u^{-1/2}
     m.M = (int32_t)(part ? p->n_bd : p->n_inner);
     m.A = part ? a->H_bd : a->H_in;
     m.C = part ? Y + p->n_inner * ldy : Y;
-    int rc = launch_gemm_nk(Gemm::NN_SRC32_PLAIN, m, s);
+    m.rowscale = p->d_col_scale ? p->d_col_scale + (part ? p->n_inner : 0) : nullptr;
+    int rc = launch_gemm_nk(p->d_col_scale ? Gemm::NN_SRC32_ROWSCALE : Gemm::NN_SRC32_PLAIN, m, s);
     if (rc) return rc;
   }
   AggArgs g{};
@@ -152,7 +159,7 @@ int layer_fwd_transform(const pgcn_partition *p, const pgcn_fwd_args *a, hipStre
   g.in_hi = bd ? Y + p->n_inner * ldy : nullptr;
   g.out_split = p->n_inner;
   g.out_lo = a->H_out;
-  g.scale = p->d_inv_deg;
+  g.scale = p->d_row_scale;
   g.f = a->f_out;
   g.ld_in = ldy;
   g.ld_out = a->ld_out;
@@ -194,7 +201,7 @@ int layer_bwd_transform(const pgcn_partition *p, const pgcn_bwd_args *a, hipStre
   char *R = (char *)a->workspace + y_bytes(p, a->f_out);
   float *D = (float *)R;
   float *partials = (float *)(R + align_up((size_t)p->n_inner * ldt * sizeof(float), 256));
-  int rc = launch_mask_scale(a->J_out, a->ld_out, a->relu ? a->H_out : nullptr, a->ld_out, p->d_inv_deg, p->n_inner,
+  int rc = launch_mask_scale(a->J_out, a->ld_out, a->relu ? a->H_out : nullptr, a->ld_out, p->d_row_scale, p->n_inner,
                              a->f_out, D, ldt, s);
   if (rc) return rc;
   AggArgs t{};
@@ -205,6 +212,7 @@ int layer_bwd_transform(const pgcn_partition *p, const pgcn_bwd_args *a, hipStre
   t.out_split = p->n_inner;
   t.out_lo = T;
   t.out_hi = T + p->n_inner * ldt;
+  t.scale = p->d_col_scale;
   t.f = a->f_out;
   t.ld_in = ldt;
   t.ld_out = ldt;
@@ -281,19 +289,33 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
     return set_error(PGCN_EWORKSPACE, "pgcn_layer_fwd: workspace too small");
   if (p->n_inner == 0) return PGCN_OK;
 
+  const float *in_lo = a->H_in, *in_hi = p->n_bd > 0 ? a->H_bd : nullptr;
+  int64_t ld_agg = a->ld_in;
+  if (p->d_col_scale) {              // symmetric: the gathered rows scaled by d̃_u^{-1/2} first
+    const int64_t lds = ld4(a->f_in);
+    float *Hs = (float *)((char *)a->workspace + fwd_sym_off(p, a->f_in, a->f_out, a->gemm_dtype));
+    rc = launch_mask_scale(a->H_in, a->ld_in, nullptr, 0, p->d_col_scale, p->n_inner, a->f_in, Hs, lds, s);
+    if (!rc && in_hi)
+      rc = launch_mask_scale(in_hi, a->ld_in, nullptr, 0, p->d_col_scale + p->n_inner, p->n_bd, a->f_in,
+                             Hs + p->n_inner * lds, lds, s);
+    if (rc) return rc;
+    in_lo = Hs;
+    in_hi = in_hi ? Hs + p->n_inner * lds : nullptr;
+    ld_agg = lds;
+  }
   AggArgs g{};
   g.plan = &p->plan;
   g.col = p->d_col;
   g.in_split = p->n_inner;
-  g.in_lo = a->H_in;
-  g.in_hi = p->n_bd > 0 ? a->H_bd : nullptr;
+  g.in_lo = in_lo;
+  g.in_hi = in_hi;
   g.out_split = p->n_inner;
   g.out_lo = a->A;
   g.out_hi = nullptr;
   g.out_bf16 = bf16 ? a->A_bf16 : nullptr;
-  g.scale = p->d_inv_deg;
+  g.scale = p->d_row_scale;
   g.f = a->f_in;
-  g.ld_in = a->ld_in;
+  g.ld_in = ld_agg;
   g.ld_out = a->ld_in;
   g.ld_bf16 = a->ld_in;
   g.partials = (float *)a->workspace;
@@ -396,7 +418,7 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   d.ldb = a->f_out;
   d.C = D;
   d.ldc = ld_d;
-  d.rowscale = p->d_inv_deg;
+  d.rowscale = p->d_row_scale;
   d.workspace = (float *)((char *)a->workspace + bwd_region0(p, a->f_in, a->f_out, input_grad));
   d.workspace_bytes = gemm_nk_workspace(a->f_in, a->f_out, a->gemm_dtype);
   if (M16) {                       // bf16 path: the masked operand as the weight-gradient kernel rounded it
@@ -418,7 +440,7 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   t.out_lo = a->J_in;
   t.out_hi = a->J_bd_out;
   t.out_bf16 = nullptr;
-  t.scale = nullptr;
+  t.scale = p->d_col_scale;           // symmetric: d̃_u^{-1/2} of the gradient's rows
   t.f = a->f_in;
   t.ld_in = ld_d;
   t.ld_out = a->ld_in;

@@ -427,7 +427,7 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
     return set_error(PGCN_EWORKSPACE, "update GEMM: workspace too small for the packed weights");
   const int rows = (int)nk_rows(g.N), ldk = (int)nk_ldk(g.K);
   const bool fwd = kind == Gemm::NN_RELU || kind == Gemm::NN_PLAIN || kind == Gemm::NN_ACC_RELU ||
-                   kind == Gemm::NN_ACC_PLAIN || kind == Gemm::NN_SRC32_PLAIN;
+                   kind == Gemm::NN_ACC_PLAIN || kind == Gemm::NN_SRC32_PLAIN || kind == Gemm::NN_SRC32_ROWSCALE;
   {
     TraceScope ts(PGCN_TK_GEMM_PACK, s);
     const unsigned blocks = (unsigned)(((int64_t)rows * ldk + 255) / 256);
@@ -461,10 +461,18 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
     case Gemm::NN_ACC_RELU: nk_launch_bn<NK_A_F32, NK_E_ACC_RELU>(p, bf16, s); break;
     case Gemm::NN_ACC_PLAIN: nk_launch_bn<NK_A_F32, NK_E_ACC_PLAIN>(p, bf16, s); break;
     case Gemm::NN_SRC32_PLAIN:                         // fp32 operand; on the bf16 path rounded while staged
+    case Gemm::NN_SRC32_ROWSCALE:
       if (!p.A) return set_error(PGCN_EINVAL, "launch_gemm_nk: NN_SRC32 needs the fp32 operand");
+      if (kind == Gemm::NN_SRC32_ROWSCALE && !p.rowscale)
+        return set_error(PGCN_EINVAL, "launch_gemm_nk: NN_SRC32_ROWSCALE needs the row scales");
       p.Am = nullptr;
-      if (bf16) nk_launch_bn<NK_A_MASK, NK_E_PLAIN>(p, true, s);
-      else nk_launch_bn<NK_A_F32, NK_E_PLAIN>(p, false, s);
+      if (kind == Gemm::NN_SRC32_PLAIN) {
+        if (bf16) nk_launch_bn<NK_A_MASK, NK_E_PLAIN>(p, true, s);
+        else nk_launch_bn<NK_A_F32, NK_E_PLAIN>(p, false, s);
+      } else {
+        if (bf16) nk_launch_bn<NK_A_MASK, NK_E_ROWSCALE>(p, true, s);
+        else nk_launch_bn<NK_A_F32, NK_E_ROWSCALE>(p, false, s);
+      }
       break;
     case Gemm::MASK_NT_ROWSCALE: nk_launch_bn<NK_A_MASK, NK_E_ROWSCALE>(p, bf16, s); break;
     case Gemm::MASK_NT_PLAIN: nk_launch_bn<NK_A_MASK, NK_E_PLAIN>(p, bf16, s); break;

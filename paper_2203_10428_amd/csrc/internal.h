@@ -48,7 +48,7 @@ struct Plan {
 }  // namespace pgcn
 
 struct pgcn_partition {
-  int32_t nparts = 0, self = 0, host_only = 0, segment = 0, self_loop = 1;
+  int32_t nparts = 0, self = 0, host_only = 0, segment = 0, self_loop = 1, symmetric = 0;
   int64_t n_inner = 0, n_bd = 0, nnz = 0, n_send = 0;
   int64_t max_row = 0, max_row_t = 0;
   int device = -1;
@@ -56,11 +56,18 @@ struct pgcn_partition {
   std::vector<int64_t> inner_gid, bd_gid, recv_ptr, rowptr, rowptr_t, send_ptr, inv_ptr;
   std::vector<int32_t> col, col_t, send_idx, inv_k;
   std::vector<float> inv_deg;
+  std::vector<int64_t> deg;        // whole-graph degree + 1 of the n_inner + n_bd local nodes
+  std::vector<float> sym_scale;    // d̃^{-1/2} of the local nodes (symmetric partitions)
   pgcn::Plan plan, plan_t;
   // device copies
   int32_t *d_col = nullptr, *d_col_t = nullptr, *d_send_idx = nullptr, *d_inv_k = nullptr;
   int64_t *d_inv_ptr = nullptr;
   float *d_inv_deg = nullptr;
+  float *d_sym_scale = nullptr;
+  // P_i = diag(row_scale) pattern diag(col_scale): the mean (1/d, no column scale) or the
+  // symmetric normalisation (d̃^{-1/2} on both sides)
+  const float *d_row_scale = nullptr;   // [n_inner]
+  const float *d_col_scale = nullptr;   // [n_inner + n_bd] or null
 };
 
 namespace pgcn {
@@ -123,11 +130,11 @@ size_t aggregate_workspace(const Plan &plan, int64_t f);
 // NN_*: C (=|+=) A W, with ReLU for *_RELU (ACC: C = act(C + A W));
 // MASK_NT_*: C = (J ∘ mask) W^T, row-scaled or plain (fp32 J and mask; rounded to bf16 on the
 // bf16 path); NT16_*: the same with the masked operand already bf16 in A16;
-// NN_SRC32_PLAIN: C = A W from the fp32 operand on both paths (rounded to bf16 while staged on
-// the bf16 path); TN_MASK_SPLITK: C = A^T (J ∘ mask)
+// NN_SRC32_PLAIN / _ROWSCALE: C = (diag(rowscale)) A W from the fp32 operand on both paths
+// (rounded to bf16 while staged on the bf16 path); TN_MASK_SPLITK: C = A^T (J ∘ mask)
 enum class Gemm {
   NN_RELU, NN_PLAIN, NN_ACC_RELU, NN_ACC_PLAIN, MASK_NT_ROWSCALE, MASK_NT_PLAIN, NT16_ROWSCALE, NT16_PLAIN,
-  NN_SRC32_PLAIN, TN_MASK_SPLITK
+  NN_SRC32_PLAIN, NN_SRC32_ROWSCALE, TN_MASK_SPLITK
 };
 struct GemmArgs {
   int32_t M, N, K;

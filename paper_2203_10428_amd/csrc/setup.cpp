@@ -3,6 +3,7 @@
 // S_{i,j} = B_j ∩ V_i, the inverse send map and the fixed work plans of the
 // aggregation kernels.  Host code; the result is uploaded once.
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 #include <cstring>
 #include <numeric>
@@ -123,13 +124,14 @@ static int upload(T **dptr, const std::vector<T> &h) {
 }
 
 static void free_device(pgcn_partition *p) {
-  void *ptrs[] = {p->d_col, p->d_col_t, p->d_send_idx, p->d_inv_k, p->d_inv_ptr, p->d_inv_deg,
+  void *ptrs[] = {p->d_col, p->d_col_t, p->d_send_idx, p->d_inv_k, p->d_inv_ptr, p->d_inv_deg, p->d_sym_scale,
                   p->plan.d_items, p->plan.d_splits, p->plan_t.d_items, p->plan_t.d_splits};
   for (void *q : ptrs)
     if (q) (void)hipFree(q);
   p->d_col = p->d_col_t = p->d_send_idx = p->d_inv_k = nullptr;
   p->d_inv_ptr = nullptr;
-  p->d_inv_deg = nullptr;
+  p->d_inv_deg = p->d_sym_scale = nullptr;
+  p->d_row_scale = p->d_col_scale = nullptr;
   p->plan.d_items = p->plan_t.d_items = nullptr;
   p->plan.d_splits = p->plan_t.d_splits = nullptr;
 }
@@ -166,6 +168,10 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
   PGCN_REQUIRE(csr->rowptr && bmap->owner, "pgcn_partition_setup: null rowptr or owner");
   PGCN_REQUIRE(bmap->nparts >= 1 && bmap->self >= 0 && bmap->self < bmap->nparts,
                "pgcn_partition_setup: bad partition count or self");
+  PGCN_REQUIRE((flags & ~(uint32_t)(PGCN_SETUP_HOST_ONLY | PGCN_SETUP_NO_SELF_LOOP | PGCN_SETUP_SYMMETRIC)) == 0,
+               "pgcn_partition_setup: unknown flags");
+  PGCN_REQUIRE(!((flags & PGCN_SETUP_SYMMETRIC) && (flags & PGCN_SETUP_NO_SELF_LOOP)),
+               "pgcn_partition_setup: the symmetric normalisation needs the self loops");
   const int64_t *rp = csr->rowptr;
   const int32_t *cl = csr->col;
   const int32_t *owner = bmap->owner;
@@ -236,9 +242,30 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
   for (int64_t g : p->bd_gid) p->recv_ptr[owner[g] + 1]++;
   for (int32_t j = 0; j < nparts; ++j) p->recv_ptr[j + 1] += p->recv_ptr[j];
 
+  // whole-graph degree + 1 of every local node: inner rows from N(v), boundary
+  // nodes from their own rows of the global CSR (distinct neighbours, no self loop)
+  p->deg.resize(n_in + n_bd);
+  for (int64_t i = 0; i < n_in; ++i) p->deg[i] = nb_ptr[i + 1] - nb_ptr[i] + 1;
+  {
+    std::vector<int32_t> row;
+    for (int64_t k = 0; k < n_bd; ++k) {
+      const int64_t u = p->bd_gid[k];
+      row.clear();
+      for (int64_t q = rp[u]; q < rp[u + 1]; ++q)
+        if (cl[q] != u) row.push_back(cl[q]);
+      std::sort(row.begin(), row.end());
+      p->deg[n_in + k] = (int64_t)(std::unique(row.begin(), row.end()) - row.begin()) + 1;
+    }
+  }
+
   // P_i: N(v) ∪ {v} (N(v) alone for the GraphSAGE aggregation), ascending local id
   const bool self_loop = !(flags & PGCN_SETUP_NO_SELF_LOOP);
   p->self_loop = self_loop ? 1 : 0;
+  p->symmetric = (flags & PGCN_SETUP_SYMMETRIC) ? 1 : 0;
+  if (p->symmetric) {                // d̃^{-1/2}, computed in double and rounded once
+    p->sym_scale.resize(n_in + n_bd);
+    for (int64_t k = 0; k < n_in + n_bd; ++k) p->sym_scale[k] = (float)(1.0 / std::sqrt((double)p->deg[k]));
+  }
   p->rowptr.assign(n_in + 1, 0);
   p->col.reserve(nb.size() + n_in);
   for (int64_t i = 0; i < n_in; ++i) {
@@ -313,6 +340,7 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
     if (!rc) rc = upload(&p->d_inv_k, p->inv_k);
     if (!rc) rc = upload(&p->d_inv_ptr, p->inv_ptr);
     if (!rc) rc = upload(&p->d_inv_deg, p->inv_deg);
+    if (!rc && p->symmetric) rc = upload(&p->d_sym_scale, p->sym_scale);
     if (!rc) rc = upload(&p->plan.d_items, p->plan.items);
     if (!rc) rc = upload(&p->plan.d_splits, p->plan.splits);
     if (!rc) rc = upload(&p->plan_t.d_items, p->plan_t.items);
@@ -322,6 +350,8 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
       delete p;
       return rc;
     }
+    p->d_row_scale = p->symmetric ? p->d_sym_scale : p->d_inv_deg;
+    p->d_col_scale = p->symmetric ? p->d_sym_scale : nullptr;
   }
   *out = p;
   return PGCN_OK;
@@ -345,6 +375,8 @@ extern "C" int pgcn_partition_info(const pgcn_partition *p, pgcn_info *o) {
   o->spmmt_split_slots = p->plan_t.slots;
   o->spmm_chunks = p->plan.chunks;
   o->spmmt_chunks = p->plan_t.chunks;
+  o->symmetric = p->symmetric;
+  o->self_loop = p->self_loop;
   return PGCN_OK;
 }
 
@@ -366,6 +398,7 @@ extern "C" int pgcn_partition_export(const pgcn_partition *p, const pgcn_arrays 
   copy_out(h->send_idx, p->send_idx);
   copy_out(h->inv_ptr, p->inv_ptr);
   copy_out(h->inv_k, p->inv_k);
+  copy_out(h->deg, p->deg);
   return PGCN_OK;
 }
 

@@ -66,6 +66,7 @@ class StepOptions:
     beta2: float = 0.999
     eps: float = 1e-8
     order: str = "agg"               # "agg" | "transform" | "auto" (GCN layers)
+    norm: str = "mean"               # GCN propagation: "mean" D̃⁻¹Ã or "sym" D̃^{-1/2} Ã D̃^{-1/2}
 
 
 def layer_order(order: str, f_in: int, f_out: int) -> int:
@@ -91,8 +92,9 @@ class PartitionTrainer:
         self.sage = opts.model == "sage"
         self.self_part = graph.self_part
         with torch.cuda.device(self.dev):
+            assert opts.norm in ("mean", "sym") and not (self.sage and opts.norm == "sym"), opts.norm
             self.part = B.pgcn_partition_setup(graph.n, graph.rowptr, graph.col, graph.owner, graph.nparts,
-                                               graph.self_part, self_loop=not self.sage)
+                                               graph.self_part, self_loop=not self.sage, symmetric=opts.norm == "sym")
         self.info = B.pgcn_partition_info(self.part)
         n, b, s = self.info["n_inner"], self.info["n_bd"], self.info["n_send"]
         self.n, self.b, self.s = n, b, s

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
     assert set(syms) == set(B.SIGNATURES), "binding signatures must cover exactly the header"
     for s in syms:
         assert getattr(B.lib, s) is not None
-    assert B.pgcn_version() == 130
+    assert B.pgcn_version() == 140
 
 
 def compare(g_n, rowptr, col, owner, nparts, part, self_loop=True):
@@ -44,7 +44,7 @@ def compare(g_n, rowptr, col, owner, nparts, part, self_loop=True):
         (ref.n_inner, ref.n_bd, ref.nnz, len(ref.send_idx))
     ex = B.pgcn_partition_export(h)
     for k in ("inner_gid", "bd_gid", "recv_ptr", "rowptr", "col", "rowptr_t", "col_t", "send_ptr", "send_idx",
-              "inv_ptr", "inv_k"):
+              "inv_ptr", "inv_k", "deg"):
         a, b = ex[k], getattr(ref, k)
         assert a.shape == b.shape and np.array_equal(a, b.astype(a.dtype)), k
     if ref.n_inner:
@@ -124,6 +124,26 @@ def test_setup_rejects_bad_input(bad):
         B.pgcn_partition_setup(n, rowptr, col, owner, nparts, part, host_only=True)
     assert e.value.code == B.PGCN_EINVAL
     assert B.pgcn_last_error()
+
+
+def test_setup_symmetric_flag():
+    g = synth.tiny_uniform()
+    h = B.pgcn_partition_setup(g.n, g.rowptr, g.col, g.owner, g.nparts, 0, host_only=True, symmetric=True)
+    info = B.pgcn_partition_info(h)
+    assert info["symmetric"] == 1 and info["self_loop"] == 1
+    ref = build_partition(g.n, g.rowptr, g.col, g.owner, 0, g.nparts)
+    assert np.array_equal(B.pgcn_partition_export(h)["deg"], ref.deg)
+    with pytest.raises(B.PgcnError, match="self loops"):
+        B.pgcn_partition_setup(g.n, g.rowptr, g.col, g.owner, g.nparts, 0, host_only=True, self_loop=False,
+                               symmetric=True)
+    flags_bad = B.PGCN_SETUP_HOST_ONLY | 64
+    csr = B.pgcn_csr(g.n, np.ascontiguousarray(g.rowptr, np.int64).ctypes.data,
+                     np.ascontiguousarray(g.col, np.int32).ctypes.data)
+    owner = np.ascontiguousarray(g.owner, np.int32)
+    bmap = B.pgcn_boundary_map(g.nparts, 0, owner.ctypes.data)
+    out = B._vp()
+    assert B.lib.pgcn_partition_setup(B.C.byref(csr), B.C.byref(bmap), flags_bad, B.C.byref(out)) == B.PGCN_EINVAL
+    assert "unknown flags" in B.pgcn_last_error()
 
 
 def test_compute_calls_reject_host_only_handle():
