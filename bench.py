@@ -154,6 +154,9 @@ def main():
                     help="GCN layer association: (P H) W, P (H W), or P (H W) where the layer narrows")
     ap.add_argument("--norm", default="mean", choices=["mean", "sym"],
                     help="GCN propagation matrix: mean D^-1 (A+I) or symmetric D^-1/2 (A+I) D^-1/2")
+    ap.add_argument("--cache-layer1", action="store_true",
+                    help="variant: keep layer 1's aggregate across steps (constant input features); it reuses "
+                         "outputs across steps, so its line is a variant, not the step's measurement")
     ap.add_argument("--no-copy-modes", action="store_true", help="skip the serial / no-refill comparison")
     ap.add_argument("--refill", default="dma", choices=["dma", "blit"], help="engine of the stale-buffer refills")
     ap.add_argument("--remote", default="device", choices=["device", "host"],
@@ -197,7 +200,8 @@ def main():
     log(f"workload {w.name}: graph {g.stats} generated in {time.perf_counter() - t0:.1f}s")
     sf, sg = VARIANTS[args.variant]
     so = StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
-                     refill_dma=args.refill == "dma", remote=args.remote, order=args.order, norm=args.norm)
+                     refill_dma=args.refill == "dma", remote=args.remote, order=args.order, norm=args.norm,
+                     cache_layer1=args.cache_layer1)
     if args.model == "sage":
         so = StepOptions(**{**so.__dict__, "model": "sage", "dropout": w.sage_dropout, "optimizer": "adam",
                             "eta": w.sage_lr})
@@ -322,7 +326,7 @@ def main():
         "config": {"workload": w.name, "variant": args.variant,
                    "layer": "graphsage-concat" if args.model == "sage" else "gcn", "remote": args.remote,
                    "optimizer": so.optimizer, "dropout": so.dropout, "copy_mode": "pipe", "refill": args.refill,
-                   "order": args.order, "norm": args.norm,
+                   "order": args.order, "norm": args.norm, "layer1_cached": args.cache_layer1,
                    "transform_first_layers": [l for l in range(1, tr.L + 1) if tr.order[l] == B.PGCN_ORDER_TRANSFORM],
                    "widths": list(w.widths),
                    "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 140
+#define PGCN_VERSION 150
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -189,8 +189,9 @@ size_t pgcn_layer_workspace_size(const pgcn_partition *part, int32_t f_in, int32
  * smoothing state); NULL means all-zero boundary rows (iteration 1).
  * With gemm_dtype == PGCN_BF16, A is rounded once to bf16 (round to nearest
  * even) into A_bf16, W is rounded to bf16 and the product accumulates in
- * fp32; A (fp32) may then be NULL.  With PGCN_F32, A is required and A_bf16
- * ignored.
+ * fp32; A (fp32) may then be NULL, or A_bf16 may be NULL when A is given
+ * (A is then rounded while staged: the same values).  With PGCN_F32, A is
+ * required and A_bf16 ignored.
  * order == PGCN_ORDER_TRANSFORM evaluates the same layer as
  *     Y = [H_in ; H_bd] W            (n_inner + n_bd rows, in the workspace)
  *     H_out = relu(P_i Y) if relu else P_i Y
@@ -198,6 +199,9 @@ size_t pgcn_layer_workspace_size(const pgcn_partition *part, int32_t f_in, int32
  * stays fp32).  A and A_bf16 are then unused and may be NULL; the backward
  * takes the layer input instead.  Workspace: pgcn_layer_workspace_size with
  * the same order.
+ * a_given == 1 (aggregate first only) skips the aggregation: A is an input
+ * holding P_i [H_in ; H_bd], e.g. a layer-1 aggregate kept across iterations
+ * (the input features are constant); H_in / H_bd are then not read.
  */
 typedef struct {
   int32_t f_in, f_out;
@@ -214,6 +218,9 @@ typedef struct {
   void *workspace;
   size_t workspace_bytes;
   int32_t order;               /* pgcn_layer_order (0: aggregate first)           */
+  int32_t a_given;             /* 1: A (fp32) already holds P_i [H_in ; H_bd]; only
+                                  the update runs (aggregate first; on the bf16
+                                  path A is rounded while staged, A_bf16 unused) */
 } pgcn_fwd_args;
 int pgcn_layer_fwd(const pgcn_partition *part, const pgcn_fwd_args *args, hipStream_t stream);
 
@@ -235,6 +242,8 @@ int pgcn_layer_fwd(const pgcn_partition *part, const pgcn_fwd_args *args, hipStr
  * H_in / H_bd are the input rows the forward used (stride ld_in; H_bd NULL
  * means zero boundary rows); A and A_bf16 are unused.  bf16 path: H, T and W
  * rounded to bf16 (nearest even) for the products, fp32 accumulation.
+ * Aggregate first on the bf16 path, A_bf16 may be NULL when A (fp32) is
+ * given: A is then rounded to bf16 while staged (the same values).
  */
 typedef struct {
   int32_t f_in, f_out;

@@ -271,18 +271,46 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_layer_fwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0, "pgcn_layer_fwd: ld_out must be >= f_out and a multiple of 4");
   PGCN_REQUIRE(a->order == PGCN_ORDER_AGG || a->order == PGCN_ORDER_TRANSFORM, "pgcn_layer_fwd: bad order");
+  PGCN_REQUIRE(a->a_given == 0 || a->a_given == 1, "pgcn_layer_fwd: a_given must be 0 or 1");
+  PGCN_REQUIRE(!(a->a_given && a->order == PGCN_ORDER_TRANSFORM),
+               "pgcn_layer_fwd: a given aggregate needs the aggregate-first order");
   if (a->order == PGCN_ORDER_TRANSFORM) return layer_fwd_transform(p, a, s);
   const bool bf16 = a->gemm_dtype == PGCN_BF16;
+  if (a->a_given) {                  // only the update: Z = A W from the given fp32 aggregate
+    if (p->n_inner > 0) {
+      PGCN_REQUIRE(a->A && a->W && a->H_out, "pgcn_layer_fwd: a_given needs A, W and H_out");
+      PGCN_REQUIRE(aligned16(a->A), "pgcn_layer_fwd: A must be 16-byte aligned");
+    }
+    const size_t gneed = gemm_nk_workspace(a->f_out, a->f_in, a->gemm_dtype);
+    if (!a->workspace || a->workspace_bytes < gneed) return set_error(PGCN_EWORKSPACE, "pgcn_layer_fwd: workspace too small");
+    if (p->n_inner == 0) return PGCN_OK;
+    GemmArgs m{};
+    m.M = (int32_t)p->n_inner;
+    m.N = a->f_out;
+    m.K = a->f_in;
+    m.dtype = a->gemm_dtype;
+    m.A = a->A;
+    m.lda = a->ld_in;
+    m.B = a->W;
+    m.ldb = a->f_out;
+    m.C = a->H_out;
+    m.ldc = a->ld_out;
+    m.workspace = (float *)a->workspace;
+    m.workspace_bytes = gneed;
+    return launch_gemm_nk(a->relu ? Gemm::NN_SRC32_RELU : Gemm::NN_SRC32_PLAIN, m, s);
+  }
   if (p->n_inner > 0) {
     PGCN_REQUIRE(a->H_in && a->W && a->H_out, "pgcn_layer_fwd: null H_in, W or H_out");
     PGCN_REQUIRE(aligned16(a->H_in) && aligned16(a->H_bd), "pgcn_layer_fwd: H_in/H_bd must be 16-byte aligned");
-    if (bf16) {
+    if (bf16 && !a->A) {
       PGCN_REQUIRE(a->A_bf16 && aligned16(a->A_bf16) && a->ld_in % 8 == 0,
-                   "pgcn_layer_fwd: bf16 path needs A_bf16 (16-byte aligned) and ld_in % 8 == 0");
+                   "pgcn_layer_fwd: bf16 path needs A_bf16 (16-byte aligned, ld_in % 8 == 0) or A");
     } else {
       PGCN_REQUIRE(a->A, "pgcn_layer_fwd: fp32 path needs A");
     }
     PGCN_REQUIRE(!a->A || aligned16(a->A), "pgcn_layer_fwd: A must be 16-byte aligned");
+    PGCN_REQUIRE(!a->A_bf16 || (aligned16(a->A_bf16) && a->ld_in % 8 == 0),
+                 "pgcn_layer_fwd: A_bf16 must be 16-byte aligned with ld_in % 8 == 0");
   }
   const size_t need = fwd_ws(p, a->f_in, a->f_out, a->gemm_dtype);
   if (need > 0 && (!a->workspace || a->workspace_bytes < need))
@@ -341,6 +369,8 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   m.ldc = a->ld_out;
   m.workspace = (float *)((char *)a->workspace + fwd_agg_bytes(p, a->f_in, a->gemm_dtype));
   m.workspace_bytes = gemm_nk_workspace(a->f_out, a->f_in, a->gemm_dtype);
+  if (bf16 && !a->A_bf16)           // bf16 path without the bf16 copy: A rounded while staged (same values)
+    return launch_gemm_nk(a->relu ? Gemm::NN_SRC32_RELU : Gemm::NN_SRC32_PLAIN, m, s);
   return launch_gemm_nk(a->relu ? Gemm::NN_RELU : Gemm::NN_PLAIN, m, s);
 }
 
@@ -367,9 +397,9 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
     PGCN_REQUIRE(a->J_out && a->W, "pgcn_layer_bwd: null J_out or W");
     PGCN_REQUIRE(!a->relu || a->H_out, "pgcn_layer_bwd: relu needs H_out as mask source");
     PGCN_REQUIRE(aligned16(a->J_out) && aligned16(a->H_out), "pgcn_layer_bwd: J_out/H_out must be 16-byte aligned");
-    if (bf16)
+    if (bf16 && !a->A)
       PGCN_REQUIRE(a->A_bf16 && aligned16(a->A_bf16) && a->ld_in % 8 == 0,
-                   "pgcn_layer_bwd: bf16 path needs A_bf16 (16-byte aligned) and ld_in % 8 == 0");
+                   "pgcn_layer_bwd: bf16 path needs A_bf16 (16-byte aligned, ld_in % 8 == 0) or A");
     else
       PGCN_REQUIRE(a->A && aligned16(a->A), "pgcn_layer_bwd: fp32 path needs A (16-byte aligned)");
   }
@@ -397,6 +427,7 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   uint16_t *M16 = p->n_inner > 0 ? m16_ptr(p, a->workspace, a->f_in, a->f_out, input_grad, a->gemm_dtype) : nullptr;
   g.M16 = M16;
   g.ldm16 = ld_m16(a->f_out);
+  if (bf16 && !a->A_bf16) g.k_split = p->n_inner;    // fp32 A rounded while staged (every row from A)
   rc = launch_gemm(Gemm::TN_MASK_SPLITK, g, s);
   if (rc) return rc;
   if (!input_grad || p->n_inner == 0) return PGCN_OK;

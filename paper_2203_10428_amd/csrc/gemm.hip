@@ -500,7 +500,7 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   p.partials = g.workspace;
   p.A_hi = a32 ? g.A_hi : nullptr;
   p.ksplit = a32 ? (int)g.k_split : g.K;
-  if (a32 && (!g.A || g.k_split > g.K || g.M16 || (g.lda % 4) != 0))
+  if (a32 && (!g.A || g.k_split > g.K || (g.lda % 4) != 0))
     return set_error(PGCN_EINVAL, "weight-gradient GEMM: bad split left operand");
   if (g.M16) {
     if (!bf16 || g.ldm16 < g.N || g.ldm16 % 4 != 0 || ((uintptr_t)g.M16 & 7u))

@@ -427,7 +427,8 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
     return set_error(PGCN_EWORKSPACE, "update GEMM: workspace too small for the packed weights");
   const int rows = (int)nk_rows(g.N), ldk = (int)nk_ldk(g.K);
   const bool fwd = kind == Gemm::NN_RELU || kind == Gemm::NN_PLAIN || kind == Gemm::NN_ACC_RELU ||
-                   kind == Gemm::NN_ACC_PLAIN || kind == Gemm::NN_SRC32_PLAIN || kind == Gemm::NN_SRC32_ROWSCALE;
+                   kind == Gemm::NN_ACC_PLAIN || kind == Gemm::NN_SRC32_PLAIN || kind == Gemm::NN_SRC32_ROWSCALE ||
+                   kind == Gemm::NN_SRC32_RELU;
   {
     TraceScope ts(PGCN_TK_GEMM_PACK, s);
     const unsigned blocks = (unsigned)(((int64_t)rows * ldk + 255) / 256);
@@ -462,6 +463,7 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
     case Gemm::NN_ACC_PLAIN: nk_launch_bn<NK_A_F32, NK_E_ACC_PLAIN>(p, bf16, s); break;
     case Gemm::NN_SRC32_PLAIN:                         // fp32 operand; on the bf16 path rounded while staged
     case Gemm::NN_SRC32_ROWSCALE:
+    case Gemm::NN_SRC32_RELU:
       if (!p.A) return set_error(PGCN_EINVAL, "launch_gemm_nk: NN_SRC32 needs the fp32 operand");
       if (kind == Gemm::NN_SRC32_ROWSCALE && !p.rowscale)
         return set_error(PGCN_EINVAL, "launch_gemm_nk: NN_SRC32_ROWSCALE needs the row scales");
@@ -469,6 +471,9 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
       if (kind == Gemm::NN_SRC32_PLAIN) {
         if (bf16) nk_launch_bn<NK_A_MASK, NK_E_PLAIN>(p, true, s);
         else nk_launch_bn<NK_A_F32, NK_E_PLAIN>(p, false, s);
+      } else if (kind == Gemm::NN_SRC32_RELU) {
+        if (bf16) nk_launch_bn<NK_A_MASK, NK_E_RELU>(p, true, s);
+        else nk_launch_bn<NK_A_F32, NK_E_RELU>(p, false, s);
       } else {
         if (bf16) nk_launch_bn<NK_A_MASK, NK_E_ROWSCALE>(p, true, s);
         else nk_launch_bn<NK_A_F32, NK_E_ROWSCALE>(p, false, s);

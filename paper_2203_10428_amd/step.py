@@ -32,6 +32,14 @@ counted by (layer, iteration).  ``optimizer``: Algorithm 1's SGD or Adam.
 ``order`` picks the association of each GCN layer's product P H W:
 ``"agg"`` (P H) W, ``"transform"`` P (H W), ``"auto"`` transform-first where
 the layer narrows (f_out < f_in), which aggregates fewer columns.
+
+``cache_layer1`` keeps layer 1's aggregate across iterations (GCN, no
+dropout): its input X never changes, so after the peers' rows have arrived
+once, A_full = P [X_in; X_bd] is fixed, and with feature smoothing the
+aggregate the layer uses is the moving average of A_full started at
+P [X_in; 0] (the smoothing is linear).  Layer 1 then runs aggregate-first
+without a gather, and its boundary rows are exchanged once.  It reuses
+outputs across iterations, so it is a variant, not the measured step.
 """
 from __future__ import annotations
 
@@ -67,6 +75,7 @@ class StepOptions:
     eps: float = 1e-8
     order: str = "agg"               # "agg" | "transform" | "auto" (GCN layers)
     norm: str = "mean"               # GCN propagation: "mean" D̃⁻¹Ã or "sym" D̃^{-1/2} Ã D̃^{-1/2}
+    cache_layer1: bool = False       # keep layer 1's aggregate across iterations (see the module notes)
 
 
 def layer_order(order: str, f_in: int, f_out: int) -> int:
@@ -131,10 +140,20 @@ class PartitionTrainer:
         self.G_peer = [None] * L
         self.order = {l: (B.PGCN_ORDER_AGG if self.sage else layer_order(opts.order, wd[l - 1], wd[l]))
                       for l in range(1, L + 1)}
+        self.cache1 = opts.cache_layer1
+        if self.cache1:
+            assert not self.sage and opts.dropout == 0.0, "layer-1 caching needs a constant layer input"
+            self.order[1] = B.PGCN_ORDER_AGG
         # activations, indexed by layer 1..L (a transform-first layer keeps no aggregate)
         agg = {l: self.order[l] == B.PGCN_ORDER_AGG for l in range(1, L + 1)}
         self.A = {l: (z(n, wd[l - 1]) if f32 and agg[l] else None) for l in range(1, L + 1)}
         self.A16 = {l: (None if f32 or not agg[l] else z(n, wd[l - 1], torch.bfloat16)) for l in range(1, L + 1)}
+        if self.cache1:   # fp32 aggregates of layer 1 on both paths: the running one and A_full
+            self.A[1], self.A16[1] = z(n, wd[0]), None
+            self.A1_full = z(n, wd[0])
+            self.H1_scratch = z(n, wd[1])
+            self.A1_ready = self.A1_started = False
+            self.A1_used = self.A[1]
         self.H = {l: z(n, wd[l]) for l in range(1, L + 1)}
         self.J_top = z(n, wd[L])
         self.J_in = {l: z(n, wd[l - 1]) for l in range(2, L + 1)}
@@ -193,6 +212,31 @@ class PartitionTrainer:
         B.pgcn_dropout(out, inp, rows, f, ld_of(f), row0, o.dropout, o.seed, self.self_part, l, self.t, out16,
                        ld_of(f) if out16 is not None else 0, st)
 
+    def _forward_layer1_cached(self, H_bd, st):
+        """Layer 1 from the kept aggregate: A_full once the peers' rows are in, then the moving
+        average of A_full (smoothing) or A_full itself; iteration 1 aggregates with zero
+        boundary rows straight into the running aggregate."""
+        o, wd, f = self.opts, self.widths, self.widths[0]
+        common = dict(f_in=f, f_out=wd[1], gemm_dtype=self.dtype, relu=self._relu(1), ld_in=ld_of(f),
+                      ld_out=ld_of(wd[1]), W=self.W[0], A_bf16=None, workspace=self.ws,
+                      workspace_bytes=self.ws_bytes, stream=st)
+        if not self.A1_ready:
+            if not self.A1_started:        # the running aggregate starts at P [X_in; 0]
+                B.pgcn_layer_fwd(self.part, H_in=self.X, H_bd=None, A=self.A[1], H_out=self.H[1], **common)
+                self.A1_started = True
+                if H_bd is None:
+                    self.A1_used = self.A[1]
+                    return
+            B.pgcn_layer_fwd(self.part, H_in=self.X, H_bd=H_bd, A=self.A1_full, H_out=self.H1_scratch, **common)
+            self.A1_ready = True
+        if o.smooth_f:
+            B.pgcn_smooth_ema(self.A[1], self.A1_full, self.n, f, ld_of(f), o.gamma, st)
+            A1 = self.A[1]
+        else:
+            A1 = self.A1_full
+        B.pgcn_layer_fwd(self.part, H_in=None, H_bd=None, A=A1, H_out=self.H[1], a_given=True, **common)
+        self.A1_used = A1
+
     def _forward_layer(self, l, H_in, H_bd, st):
         """Dropout of the layer input (after the receive), then the GCN or GraphSAGE layer."""
         wd, f = self.widths, self.widths[l - 1]
@@ -217,14 +261,16 @@ class PartitionTrainer:
     def _backward_layer(self, l, J_out, st):
         """Layer gradients; the input gradient then takes the forward's dropout mask."""
         wd, f = self.widths, self.widths[l - 1]
+        A = self.A1_used if (self.cache1 and l == 1) else self.A[l]
         common = dict(f_in=f, f_out=wd[l], gemm_dtype=self.dtype, relu=self._relu(l), ld_in=ld_of(f),
-                      ld_out=ld_of(wd[l]), J_out=J_out, H_out=self.H[l], A=self.A[l], A_bf16=self.A16[l],
+                      ld_out=ld_of(wd[l]), J_out=J_out, H_out=self.H[l], A=A, A_bf16=self.A16[l],
                       W=self.W[l - 1], dW=self.dW[l - 1], J_in=self.J_in.get(l), J_bd_out=self.J_bd_out.get(l),
                       workspace=self.ws, workspace_bytes=self.ws_bytes, stream=st)
         if self.sage:
             B.pgcn_sage_layer_bwd(self.part, X_in=self.X_used[l], X_in_bf16=self.Xd_16.get(l), **common)
         else:
-            B.pgcn_layer_bwd(self.part, order=self.order[l], H_in=self.X_used[l], H_bd=self.X_bd_used[l], **common)
+            B.pgcn_layer_bwd(self.part, order=self.order[l], H_in=self.X_used.get(l), H_bd=self.X_bd_used.get(l),
+                             **common)
         if l > 1 and self.opts.dropout > 0.0:
             self._dropout(self.J_in[l], self.J_in[l], self.n, l, 0, None, st)
             self._dropout(self.J_bd_out[l], self.J_bd_out[l], self.b, l, self.n, None, st)
@@ -245,6 +291,27 @@ class PartitionTrainer:
             f = wd[l - 1]
             H_in = self.X if l == 1 else self.H[l - 1]
             H_bd = None
+            if self.cache1 and l == 1:
+                # the constant layer input: its boundary rows are exchanged once (iteration 1's send,
+                # received in iteration 2) and the smoothing acts on the kept aggregate
+                if self.A1_ready:
+                    self._forward_layer1_cached(None, st)
+                    continue
+                if mode == "serial":
+                    self._refill(self.feat[1][cur], self.remote_f[1], st)
+                if t > 1 or mode == "serial":
+                    if mode == "pipe":
+                        st.wait_event(self.ev_feat[1])
+                    H_bd = self.feat[1][cur]
+                if t == 1:
+                    B.pgcn_pack_boundary(self.part, B.PGCN_PACK_FEAT, H_in, self.send_f[1], f, ld_of(f), st)
+                    if mode == "pipe":
+                        self.ev_pack[1].record(st)
+                        side.wait_event(self.ev_pack[1])
+                        self._refill(self.feat[1][nxt], self.remote_f[1], side)
+                        self.ev_feat[1].record(side)
+                self._forward_layer1_cached(H_bd, st)
+                continue
             if mode == "serial":
                 self._refill(self.feat[l][cur], self.remote_f[l], st)
             if t > 1 or mode == "serial":

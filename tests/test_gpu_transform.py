@@ -205,3 +205,50 @@ def test_tiny_autonomous_transform(order):
         tr.step()
         tr.synchronize()
         compare_step(tr, r0, "f32", L, w.widths, check_state=True)
+
+
+@pytest.mark.parametrize("sf,sg", [(False, False), (True, True)])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("mode", ["pipe", "serial"])
+def test_tiny_layer1_cached(sf, sg, dt, mode):
+    """Layer 1's aggregate kept across iterations (the input features are constant): the step
+    still reproduces the oracle's PipeGCN (or, with serial refills, its synchronous reading)."""
+    from oracle.pipegcn import Options as O
+    T = 5
+    w = configs.TINY
+    g = configs.make_graph(w)
+    d = configs.make_dense(w, g.n)
+    opts = O(mode="pipe" if mode == "pipe" else "vanilla", smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta,
+             loss=w.loss, loss_scale=w.loss_scale, gemm="bf16" if dt == "bf16" else "f64")
+    if mode == "serial":     # refilled before use: the oracle's vanilla mode without smoothing
+        if sf or sg:
+            pytest.skip("smoothing is defined on stale messages")
+    sim, recs = run(g.n, g.rowptr, g.col, g.owner, g.nparts, d.X, d.labels, d.W, T, opts)
+    L = w.layers
+    tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, dt,
+                          StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode=mode,
+                                      order="auto", cache_layer1=True))
+    assert tr.order[1] == B.PGCN_ORDER_AGG
+    tol = TOL[dt]
+    for t in range(1, T + 1):
+        r0, r1 = recs[t - 1][0], recs[t - 1][1]
+        src = r0["state_out"]       # pipe: consumed next iteration; vanilla: what this iteration used
+        torch.cuda.synchronize()
+        for l in range(1, L + 1):
+            put(tr.remote_f[l], src.feat_buf[l])
+        for l in range(2, L + 1):
+            put(tr.remote_g[l], src.grad_buf[l])
+        for l in range(L):
+            tr.G_peer[l] = torch.from_numpy(r1["G"][l + 1].astype(np.float32)).cuda()
+        torch.cuda.synchronize()
+        tr.step()
+        tr.synchronize()
+        errs = {"loss": abs(tr.loss.item() - r0["loss"]) / abs(r0["loss"])}
+        for l in range(1, L + 1):
+            errs[f"H{l}"] = rel_err(host(tr.H[l], w.widths[l]), r0["H"][l])
+            errs[f"G{l}"] = rel_err(tr.dW[l - 1].cpu().numpy(), r0["G"][l])
+        errs["A1"] = rel_err(host(tr.A1_used, w.widths[0]), r0["A"][1])
+        for l in range(L):
+            errs[f"W{l + 1}"] = rel_err(tr.W[l].cpu().numpy(), r0["W_out"][l])
+        bad = {k: v for k, v in errs.items() if not v <= (tol["grad"] if k.startswith("G") else tol["act"])}
+        assert not bad, (t, bad)
