@@ -16,9 +16,10 @@
 // bounds checks on the weights.
 //
 // Main loop for CDNA4: a 256-thread workgroup (4 wave64s, 2 x 2) computes a
-// 128 x BN tile; both tiles sit in LDS with k contiguous and are double
-// buffered, so one barrier per k-slab suffices while the next slab's global
-// loads are in flight.  Slabs are short (16 fp32 / 32 bf16 values of k) so
+// 128 x BN tile; both tiles sit in LDS with k contiguous (rows of four
+// 16-byte groups, XOR-swizzled by row so that staging writes and fragment
+// reads are free of bank conflicts) and are double buffered, so one barrier
+// per k-slab suffices while the next slab's global loads are in flight.  Slabs are short (16 fp32 / 32 bf16 values of k) so
 // that three workgroups fit per CU: the staging of one workgroup's next slab
 // (global load -> registers -> LDS) hides behind the others' MFMAs, which
 // measured faster than longer slabs at two workgroups per CU.  The MFMA k
@@ -166,13 +167,21 @@ __device__ __forceinline__ void nk_epilogue(const NKParams &p, const f32x16 (&ac
 
 // ------------------------------------------------------------------ fp32 ---
 
+// 16-byte group g of LDS row `row` (4 groups per row) is stored at group
+// g ^ ((row >> 2) & 3): the 16 lanes of one 16-byte access pass, whether 4
+// rows x 4 groups (staging writes) or 16 rows x 1 group (fragment reads), then
+// fall on 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int nk_sw(int row, int g) { return g ^ ((row >> 2) & 3); }
+
 template <int BM, int BN, int AK, int EK>
 __global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
-  constexpr int BK = 16, LK = BK + 4, KV = BK / 4;
+  constexpr int BK = 16, LK = BK, KV = BK / 4;        // rows of 4 16-byte groups, XOR-swizzled (nk_sw)
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
   constexpr int VA = BM * BK / 4 / 256, VB = BN * BK / 4 / 256;
-  __shared__ __attribute__((aligned(16))) float As[2][BM * LK];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LK];
+  constexpr int SM = 2 * (BM + BN) * LK > kNkStageFloats ? 2 * (BM + BN) * LK : kNkStageFloats;
+  __shared__ __attribute__((aligned(16))) float smem[SM];
+  float(*As)[BM * LK] = reinterpret_cast<float(*)[BM * LK]>(smem);
+  float(*Bs)[BN * LK] = reinterpret_cast<float(*)[BN * LK]>(smem + 2 * BM * LK);
 
   const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
   const int tile = nk_xcd_remap(blockIdx.x, gridDim.x);
@@ -213,12 +222,12 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
         if (e >= valid) x[e] = 0.f;
         if (AK == NK_A_MASK) x[e] = rh[v][e] > 0.f ? x[e] : 0.f;
       }
-      *reinterpret_cast<f32x4 *>(&As[b][(idx / KV) * LK + 4 * (idx % KV)]) = x;
+      *reinterpret_cast<f32x4 *>(&As[b][(idx / KV) * LK + 4 * nk_sw(idx / KV, idx % KV)]) = x;
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
       const int idx = t + 256 * v;
-      *reinterpret_cast<f32x4 *>(&Bs[b][(idx / KV) * LK + 4 * (idx % KV)]) = rb[v];
+      *reinterpret_cast<f32x4 *>(&Bs[b][(idx / KV) * LK + 4 * nk_sw(idx / KV, idx % KV)]) = rb[v];
     }
   };
 
@@ -244,10 +253,10 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
       f32x4 a[TM], b[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        a[i] = *reinterpret_cast<const f32x4 *>(&As[cur][(wm0 + i * 32 + r) * LK + (BK / 2) * h + 4 * q]);
+        a[i] = *reinterpret_cast<const f32x4 *>(&As[cur][(wm0 + i * 32 + r) * LK + 4 * nk_sw(wm0 + i * 32 + r, 2 * h + q)]);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        b[j] = *reinterpret_cast<const f32x4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + (BK / 2) * h + 4 * q]);
+        b[j] = *reinterpret_cast<const f32x4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + 4 * nk_sw(wn0 + j * 32 + r, 2 * h + q)]);
 #pragma unroll
       for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -260,20 +269,20 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
     __syncthreads();
   }
   // the last barrier of the loop ends every LDS read of the main loop
-  static_assert(sizeof(As) >= kNkStageFloats * sizeof(float), "epilogue staging does not fit");
-  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane,
-                          reinterpret_cast<float *>(&As[0][0]) + wave * 32 * kNkStageLd);
+  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane, smem + wave * 32 * kNkStageLd);
 }
 
 // ------------------------------------------------------------------ bf16 ---
 
 template <int BM, int BN, int AK, int EK>
 __global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
-  constexpr int BK = 32, LK = BK + 8, KV = BK / 8;     // bf16 elements; 80-byte rows
+  constexpr int BK = 32, LK = BK, KV = BK / 8;         // bf16 elements; 64-byte rows, XOR-swizzled (nk_sw)
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
   constexpr int VA = BM * BK / 8 / 256, VB = BN * BK / 8 / 256;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LK];
+  constexpr int SM = 2 * (BM + BN) * LK * 2 > kNkStageFloats * 4 ? 2 * (BM + BN) * LK * 2 : kNkStageFloats * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[SM];
+  uint16_t(*As)[BM * LK] = reinterpret_cast<uint16_t(*)[BM * LK]>(smem);
+  uint16_t(*Bs)[BN * LK] = reinterpret_cast<uint16_t(*)[BN * LK]>(smem + 2 * BM * LK * 2);
 
   const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
   const int tile = nk_xcd_remap(blockIdx.x, gridDim.x);
@@ -338,12 +347,12 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
         for (int w = 0; w < 4; ++w)
           o[w] = (uint32_t)nk_bf16(x[2 * w]) | ((uint32_t)nk_bf16(x[2 * w + 1]) << 16);
       }
-      *reinterpret_cast<u32x4 *>(&As[b][(idx / KV) * LK + 8 * (idx % KV)]) = o;
+      *reinterpret_cast<u32x4 *>(&As[b][(idx / KV) * LK + 8 * nk_sw(idx / KV, idx % KV)]) = o;
     }
 #pragma unroll
     for (int v = 0; v < VB; ++v) {
       const int idx = t + 256 * v;
-      *reinterpret_cast<u32x4 *>(&Bs[b][(idx / KV) * LK + 8 * (idx % KV)]) = rb[v];
+      *reinterpret_cast<u32x4 *>(&Bs[b][(idx / KV) * LK + 8 * nk_sw(idx / KV, idx % KV)]) = rb[v];
     }
   };
 
@@ -369,10 +378,12 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
       bf16x8 a[TM], b[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&As[cur][(wm0 + i * 32 + r) * LK + (BK / 2) * h + 8 * q]));
+        a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(
+                                              &As[cur][(wm0 + i * 32 + r) * LK + 8 * nk_sw(wm0 + i * 32 + r, 2 * h + q)]));
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(&Bs[cur][(wn0 + j * 32 + r) * LK + (BK / 2) * h + 8 * q]));
+        b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(
+                                              &Bs[cur][(wn0 + j * 32 + r) * LK + 8 * nk_sw(wn0 + j * 32 + r, 2 * h + q)]));
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -382,9 +393,7 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
     store(cur ^ 1);
     __syncthreads();
   }
-  static_assert(sizeof(As) >= kNkStageFloats * sizeof(float), "epilogue staging does not fit");
-  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane,
-                          reinterpret_cast<float *>(&As[0][0]) + wave * 32 * kNkStageLd);
+  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane, reinterpret_cast<float *>(smem) + wave * 32 * kNkStageLd);
 }
 
 // ---------------------------------------------------------------- launch ---
