@@ -19,10 +19,12 @@
 // 128 x BN tile; both tiles sit in LDS with k contiguous (rows of four
 // 16-byte groups, XOR-swizzled by row so that staging writes and fragment
 // reads are free of bank conflicts) and are double buffered, so one barrier
-// per k-slab suffices while the next slab's global loads are in flight.  Slabs are short (16 fp32 / 32 bf16 values of k) so
-// that three workgroups fit per CU: the staging of one workgroup's next slab
-// (global load -> registers -> LDS) hides behind the others' MFMAs, which
-// measured faster than longer slabs at two workgroups per CU.  The MFMA k
+// per k-slab suffices while the next slab's global loads are in flight.
+// Slabs are short (16 fp32 / 32 bf16 values of k) so that four workgroups fit
+// per CU (32 KB of LDS, at most 128 VGPRs; three for the bf16 kernel with an
+// fp32 masked operand): the staging of one workgroup's next slab (global load
+// -> registers -> LDS) hides behind the others' MFMAs, which measured faster
+// than longer slabs or deeper prefetch at two workgroups per CU.  The MFMA k
 // order is permuted so that each lane's fragments over a slab are contiguous
 // in LDS and load with 128-bit reads:
 //   fp32, v_mfma_f32_32x32x2f32, slab of 16: step s uses k = 8*h + s for
@@ -174,7 +176,7 @@ __device__ __forceinline__ void nk_epilogue(const NKParams &p, const f32x16 (&ac
 __device__ __forceinline__ int nk_sw(int row, int g) { return g ^ ((row >> 2) & 3); }
 
 template <int BM, int BN, int AK, int EK>
-__global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
+__global__ __launch_bounds__(256, 4) void gemm_nk_f32(NKParams p) {
   constexpr int BK = 16, LK = BK, KV = BK / 4;        // rows of 4 16-byte groups, XOR-swizzled (nk_sw)
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
   constexpr int VA = BM * BK / 4 / 256, VB = BN * BK / 4 / 256;
@@ -275,7 +277,7 @@ __global__ __launch_bounds__(256, 3) void gemm_nk_f32(NKParams p) {
 // ------------------------------------------------------------------ bf16 ---
 
 template <int BM, int BN, int AK, int EK>
-__global__ __launch_bounds__(256, 3) void gemm_nk_bf16(NKParams p) {
+__global__ __launch_bounds__(256, AK == NK_A_MASK ? 3 : 4) void gemm_nk_bf16(NKParams p) {
   constexpr int BK = 32, LK = BK, KV = BK / 8;         // bf16 elements; 64-byte rows, XOR-swizzled (nk_sw)
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
   constexpr int VA = BM * BK / 8 / 256, VB = BN * BK / 8 / 256;
