@@ -269,6 +269,9 @@ def main():
                 "frac": ach / HBM_PEAK_GBPS,
                 "traffic": None if tr_bytes is None else tr_bytes / per_step[dominant]["launches"],
                 "traffic_GBps": None if tr_bytes is None else tr_bytes / (per_step[dominant]["ms_per_step"] / 1e3) / 1e9,
+                # counter-measured HBM-side bytes over the same time, against the same peak
+                "traffic_frac": None if tr_bytes is None else
+                tr_bytes / (per_step[dominant]["ms_per_step"] / 1e3) / 1e9 / HBM_PEAK_GBPS,
                 "gather_model_GBps": util[dominant]["GBps_gather_model"],
                 "algorithmic_bytes_per_step": work[dominant],
                 "launches_per_step": per_step[dominant]["launches"],
