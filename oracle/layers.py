@@ -47,6 +47,10 @@ too, after communication, with one mask for the forward and the backward):
     J_full = Pᵀ dz, plus ds on the inner rows   (gradient of the dropped input;
                                                   the caller applies the mask)
 
+Transform-first (``order="transform"``): z W_top = P (X_full W_top), so
+Z = P (X_full W_top) + X_inner W_bot, and in the backward T = Pᵀ M gives the
+top half of G as X_fullᵀ T and the top part of J_full as T W_topᵀ.
+
 Adam (Kingma and Ba, ICLR 2015, Algorithm 1), the experiments' optimiser.
 
 Pinned by: dense brute force of P (tests), central finite differences of the
@@ -137,28 +141,46 @@ def sgd(W: np.ndarray, G: np.ndarray, eta: float) -> np.ndarray:
     return W - eta * G
 
 
-def sage_forward(P, X_full: np.ndarray, n_inner: int, W: np.ndarray, relu: bool, gemm: str = "f64"):
-    """Returns (z, Z, H); X_full = [X_inner; X_boundary] is the (dropped) layer input."""
+def sage_forward(P, X_full: np.ndarray, n_inner: int, W: np.ndarray, relu: bool, gemm: str = "f64",
+                 order: str = "agg"):
+    """Returns (z, Z, H); X_full = [X_inner; X_boundary] is the (dropped) layer input.
+    ``order="transform"``: Z = P (X_full W_top) + X_inner W_bot (z is still returned)."""
     z = P @ X_full
-    Xc = np.hstack([z, X_full[:n_inner]])
-    Z = _operand(Xc, gemm) @ _operand(W, gemm)
+    f = X_full.shape[1]
+    if order == "transform":
+        Z = P @ (_operand(X_full, gemm) @ _operand(W[:f], gemm)) + \
+            _operand(X_full[:n_inner], gemm) @ _operand(W[f:], gemm)
+    else:
+        Xc = np.hstack([z, X_full[:n_inner]])
+        Z = _operand(Xc, gemm) @ _operand(W, gemm)
     H = np.maximum(Z, 0.0) if relu else Z
     return z, Z, H
 
 
 def sage_backward(P, z: np.ndarray, X_inner: np.ndarray, Z: np.ndarray, J: np.ndarray, W: np.ndarray,
-                  relu: bool, input_grad: bool, gemm: str = "f64"):
-    """Returns (G, J_full): J_full is the gradient of the dropped input rows (inner, then boundary)."""
+                  relu: bool, input_grad: bool, gemm: str = "f64", order: str = "agg", X_full=None):
+    """Returns (G, J_full): J_full is the gradient of the dropped input rows (inner, then boundary).
+    ``order="transform"`` (needs X_full): T = Pᵀ M, G = [X_fullᵀ T ; X_innerᵀ M],
+    J_full = T W_topᵀ plus M W_botᵀ on the inner rows."""
     M = J * (Z > 0.0) if relu else J
     Mq = _operand(M, gemm)
+    f = X_inner.shape[1]
+    n = X_inner.shape[0]
+    if order == "transform":
+        Tq = _operand(P.T @ M, gemm)
+        G = np.vstack([_operand(X_full, gemm).T @ Tq, _operand(X_inner, gemm).T @ Mq])
+        if not input_grad:
+            return G, None
+        J_full = Tq @ _operand(W[:f], gemm).T
+        J_full[:n] += Mq @ _operand(W[f:], gemm).T
+        return G, J_full
     Xc = np.hstack([z, X_inner])
     G = _operand(Xc, gemm).T @ Mq
     if not input_grad:
         return G, None
-    f = z.shape[1]
     dX = Mq @ _operand(W, gemm).T
     J_full = P.T @ dX[:, :f]
-    J_full[: z.shape[0]] += dX[:, f:]
+    J_full[:n] += dX[:, f:]
     return G, J_full
 
 

@@ -79,10 +79,12 @@ class Options:
     eps: float = 1e-8
 
 
-def layer_order(o: Options, W: np.ndarray) -> str:
-    """The association a GCN layer with weights W [f_in, f_out] is evaluated in."""
+def layer_order(o: Options, W: np.ndarray, sage: bool = False) -> str:
+    """The association a layer is evaluated in; W is [f_in, f_out] (GCN) or [2 f_in, f_out] (GraphSAGE,
+    whose aggregated half is f_in wide)."""
     if o.order == "auto":
-        return "transform" if W.shape[1] < W.shape[0] else "agg"
+        f_in = W.shape[0] // 2 if sage else W.shape[0]
+        return "transform" if W.shape[1] < f_in else "agg"
     assert o.order in ("agg", "transform")
     return o.order
 
@@ -133,7 +135,7 @@ class Simulation:
         return l < self.L or self.opts.relu_last
 
     def _order(self, l):
-        return layer_order(self.opts, self.W[l - 1])
+        return layer_order(self.opts, self.W[l - 1], self.opts.model == "sage")
 
     def _use_features(self, i, l, t):
         """Boundary rows that layer l of partition i reads at iteration t."""
@@ -200,7 +202,8 @@ class Simulation:
                 X, mask = self._dropped_input(i, l, t, H_prev[i], Hbd)
                 rec[i]["X_in"][l], rec[i]["mask"][l] = X[: p.n_inner], mask
                 if o.model == "sage":
-                    A, Z, H = layers.sage_forward(self.P[i], X, p.n_inner, self.W[l - 1], self._relu(l), o.gemm)
+                    A, Z, H = layers.sage_forward(self.P[i], X, p.n_inner, self.W[l - 1], self._relu(l), o.gemm,
+                                                  self._order(l))
                 else:
                     A, Z, H = layers.layer_forward(self.P[i], X, self.W[l - 1], self._relu(l), o.gemm,
                                                    self._order(l))
@@ -226,7 +229,8 @@ class Simulation:
             for i, p in enumerate(self.parts):
                 if o.model == "sage":
                     G, Jf = layers.sage_backward(self.P[i], rec[i]["A"][l], rec[i]["X_in"][l], rec[i]["Z"][l], J[i],
-                                                 self.W[l - 1], self._relu(l), l > 1, o.gemm)
+                                                 self.W[l - 1], self._relu(l), l > 1, o.gemm, self._order(l),
+                                                 rec[i]["X_full"][l])
                 else:
                     G, Jf = layers.layer_backward(self.P[i], rec[i]["A"][l], rec[i]["Z"][l], J[i],
                                                   self.W[l - 1], self._relu(l), l > 1, o.gemm,
@@ -336,9 +340,9 @@ def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: di
         X = X * mask
         rec["X_in"][l], rec["mask"][l] = X[: p.n_inner], mask
         if sage:
-            A, Z, H = layers.sage_forward(P, X, p.n_inner, W[l - 1], relu, o.gemm)
+            A, Z, H = layers.sage_forward(P, X, p.n_inner, W[l - 1], relu, o.gemm, layer_order(o, W[l - 1], sage))
         else:
-            A, Z, H = layers.layer_forward(P, X, W[l - 1], relu, o.gemm, layer_order(o, W[l - 1]))
+            A, Z, H = layers.layer_forward(P, X, W[l - 1], relu, o.gemm, layer_order(o, W[l - 1], sage))
         rec["A"][l], rec["Z"][l], rec["H"][l] = A, Z, H
         rec["X_full"][l] = X
     f = layers.softmax_ce if o.loss == "softmax_ce" else layers.sigmoid_bce
@@ -347,10 +351,10 @@ def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: di
         relu = l < L or o.relu_last
         if sage:
             G, Jf = layers.sage_backward(P, rec["A"][l], rec["X_in"][l], rec["Z"][l], J, W[l - 1], relu, l > 1,
-                                         o.gemm)
+                                         o.gemm, layer_order(o, W[l - 1], sage), rec["X_full"][l])
         else:
             G, Jf = layers.layer_backward(P, rec["A"][l], rec["Z"][l], J, W[l - 1], relu, l > 1, o.gemm,
-                                          layer_order(o, W[l - 1]), rec["X_full"][l])
+                                          layer_order(o, W[l - 1], sage), rec["X_full"][l])
         rec["G"][l] = G
         if l == 1:
             break

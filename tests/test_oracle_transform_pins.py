@@ -13,6 +13,11 @@ Pinned against what fixes it independently of the oracle's own code:
   single elements recomputed term by term with torch's float32 -> bfloat16
   conversion, the standard error bound of a product of rounded operands
   against the fp64 result, and exactness when nothing needs rounding.
+
+The GraphSAGE layer in the same association (z W_top = P (X_full W_top)) is
+pinned by finite differences of its partition loss (with and without dropout
+masks), vanilla training equal to dense full-graph GraphSAGE, and bf16
+exactness when nothing needs rounding.
 """
 import numpy as np
 import pytest
@@ -220,3 +225,105 @@ def test_bf16_transform_exact_without_rounding():
         G, Jf = layers.layer_backward(P, A, Z, J, W, relu, True, order="transform", H_full=Hf)
         Gq, Jq = layers.layer_backward(P, A, Z, J, W, relu, True, gemm="bf16", order="transform", H_full=Hf)
         assert np.array_equal(G, Gq) and np.array_equal(Jf, Jq)
+
+
+# ---------------------------------------------------------------------------
+# GraphSAGE layer in the transform-first association
+# ---------------------------------------------------------------------------
+
+def sage_local_loss_tf(p, P, X_in, Hbd, masks, W, y, scale):
+    L = len(W)
+    H = X_in
+    cache = []
+    for l in range(L):
+        X = np.vstack([H, Hbd[l]]) * masks[l]
+        z, Z, Hn = layers.sage_forward(P, X, p.n_inner, W[l], l < L - 1, order="transform")
+        cache.append((z, X, Z))
+        H = Hn
+    val, J = layers.softmax_ce(H, y, scale)
+    G, Jbd = [None] * L, [None] * L
+    for l in range(L - 1, -1, -1):
+        z, X, Z = cache[l]
+        G[l], Jf = layers.sage_backward(P, z, X[: p.n_inner], Z, J, W[l], l < L - 1, True, order="transform",
+                                        X_full=X)
+        Jf = Jf * masks[l]
+        Jbd[l] = Jf[p.n_inner:]
+        J = Jf[: p.n_inner]
+    return val, G, Jbd
+
+
+@pytest.mark.parametrize("p_drop", [0.0, 0.35])
+def test_sage_transform_gradients_match_finite_differences(p_drop):
+    from oracle.philox import dropout_mask
+    n, rowptr, col, owner = SMALL_GRAPHS[0]
+    p = build_partition(n, rowptr, col, owner, 0, 3, self_loop=False)
+    P = propagation_matrix(p)
+    rng = np.random.default_rng(41)
+    widths = [7, 3, 5, 2]
+    X_in = rng.standard_normal((p.n_inner, widths[0]))
+    Hbd = [rng.standard_normal((p.n_bd, widths[l])) for l in range(3)]
+    W = [rng.standard_normal((2 * widths[l], widths[l + 1])) * 0.6 for l in range(3)]
+    masks = [dropout_mask(p.n_inner + p.n_bd, widths[l], p_drop, 3, 0, l + 1, 2) for l in range(3)]
+    y = rng.integers(0, widths[-1], p.n_inner)
+    _, G, Jbd = sage_local_loss_tf(p, P, X_in, Hbd, masks, W, y, 0.37)
+    eps = 1e-6
+
+    def f(W_, Hbd_):
+        return sage_local_loss_tf(p, P, X_in, Hbd_, masks, W_, y, 0.37)[0]
+
+    for l in range(3):
+        for (a, b) in [(0, 0), (2 * widths[l] - 1, widths[l + 1] - 1), (widths[l], 1), (1, 0)]:
+            Wp = [w.copy() for w in W]; Wm = [w.copy() for w in W]
+            Wp[l][a, b] += eps; Wm[l][a, b] -= eps
+            fd = (f(Wp, Hbd) - f(Wm, Hbd)) / (2 * eps)
+            assert abs(fd - G[l][a, b]) <= 1e-7 * max(1.0, abs(fd)), (l, a, b, fd, G[l][a, b])
+        for (r, c) in [(0, 0), (p.n_bd - 1, widths[l] - 1), (p.n_bd // 2, 1)]:
+            Hp = [h.copy() for h in Hbd]; Hm = [h.copy() for h in Hbd]
+            Hp[l][r, c] += eps; Hm[l][r, c] -= eps
+            fd = (f(W, Hp) - f(W, Hm)) / (2 * eps)
+            assert abs(fd - Jbd[l][r, c]) <= 1e-7 * max(1.0, abs(fd)), (l, r, c, fd, Jbd[l][r, c])
+
+
+@pytest.mark.parametrize("order", ["transform", "auto"])
+def test_sage_transform_vanilla_equals_dense_full_graph(order):
+    from test_oracle_sage_pins import dense_full_graph_sage, sage_problem
+    n, rowptr, col, owner = SMALL_GRAPHS[3]
+    nparts = int(owner.max()) + 1
+    widths = [6, 3, 5, 2]
+    X, W, y = sage_problem((n, rowptr, col, owner), widths)
+    opts = Options(mode="vanilla", model="sage", eta=0.3, loss_scale=1.0 / n, order=order)
+    sim, recs = run(n, rowptr, col, owner, nparts, X, y, W, 3, opts)
+    ref, W_ref = dense_full_graph_sage(n, rowptr, col, X, y, W, 3, 0.3, 1.0 / n)
+    for t in range(3):
+        assert np.isclose(sum(r["loss"] for r in recs[t]), ref[t]["loss"], rtol=1e-12)
+        for l in range(1, 4):
+            assert np.allclose(assemble(sim, recs[t], "H", l), ref[t]["H"][l - 1], atol=1e-12)
+            assert np.allclose(recs[t][0]["G_sum"][l - 1], ref[t]["G"][l - 1], atol=1e-12)
+    for w, wr in zip(sim.W, W_ref):
+        assert np.allclose(w, wr, atol=1e-12)
+
+
+def test_sage_layer_order_rule():
+    o = Options(order="auto")
+    assert layer_order(o, np.zeros((2 * 602, 256)), sage=True) == "transform"
+    assert layer_order(o, np.zeros((2 * 256, 256)), sage=True) == "agg"
+    assert layer_order(o, np.zeros((2 * 100, 128)), sage=True) == "agg"
+
+
+def test_sage_bf16_transform_exact_without_rounding():
+    """Isolated nodes (z = 0) and bf16-representable inputs: the bf16 reading equals fp64."""
+    n = 10
+    rowptr = np.zeros(n + 1, np.int64)
+    col = np.zeros(0, np.int32)
+    owner = np.zeros(n, np.int32)
+    p = build_partition(n, rowptr, col, owner, 0, 1, self_loop=False)
+    P = propagation_matrix(p)
+    rng = np.random.default_rng(3)
+    q = layers.round_bf16
+    X, W, J = q(rng.standard_normal((n, 4))), q(rng.standard_normal((8, 3))), q(rng.standard_normal((n, 3)))
+    z, Z, _ = layers.sage_forward(P, X, n, W, True, order="transform")
+    _, Zq, _ = layers.sage_forward(P, X, n, W, True, gemm="bf16", order="transform")
+    assert np.array_equal(Z, Zq)
+    G, Jf = layers.sage_backward(P, z, X, Z, J, W, True, True, order="transform", X_full=X)
+    Gq, Jq = layers.sage_backward(P, z, X, Z, J, W, True, True, gemm="bf16", order="transform", X_full=X)
+    assert np.array_equal(G, Gq) and np.array_equal(Jf, Jq)
