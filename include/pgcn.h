@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 150
+#define PGCN_VERSION 160
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -175,8 +175,9 @@ void pgcn_partition_destroy(pgcn_partition *part);
 /* Bytes of workspace that pgcn_layer_fwd / pgcn_layer_bwd / pgcn_loss_fwd_bwd need
  * for these widths (the maximum over the three), aggregate-first layers. */
 size_t pgcn_workspace_size(const pgcn_partition *part, int32_t f_in, int32_t f_out, int32_t gemm_dtype);
-/* The same for a layer evaluated in `order` (pgcn_layer_order); returns 0 for a
- * bad order.  PGCN_ORDER_AGG gives pgcn_workspace_size. */
+/* The same for a GCN or GraphSAGE layer evaluated in `order`
+ * (pgcn_layer_order); returns 0 for a bad order.  PGCN_ORDER_AGG gives
+ * pgcn_workspace_size. */
 size_t pgcn_layer_workspace_size(const pgcn_partition *part, int32_t f_in, int32_t f_out, int32_t gemm_dtype,
                                  int32_t order);
 
@@ -363,6 +364,11 @@ int pgcn_dropout(float *out, const float *in, int64_t rows, int32_t cols, int64_
  * and X_in_bf16 (the bf16 copy of X_in, e.g. from pgcn_dropout) is the
  * self operand; W is rounded to bf16; fp32 accumulation.
  * Workspace: pgcn_workspace_size(part, f_in, f_out, gemm_dtype).
+ * order == PGCN_ORDER_TRANSFORM evaluates z W_top as P_i (X W_top):
+ *     Y = [X_in ; X_bd] W_top        (n_inner + n_bd rows, in the workspace)
+ *     H_out = act(P_i Y + X_in W_bot)
+ * (bf16 path: X and W rounded to bf16 for the products); A and A_bf16 are
+ * unused.  Workspace: pgcn_layer_workspace_size with that order.
  */
 typedef struct {
   int32_t f_in, f_out;
@@ -378,6 +384,7 @@ typedef struct {
   float *H_out;                /* [n_inner, ld_out] out                          */
   void *workspace;
   size_t workspace_bytes;
+  int32_t order;               /* pgcn_layer_order (0: aggregate first)           */
 } pgcn_sage_fwd_args;
 int pgcn_sage_layer_fwd(const pgcn_partition *part, const pgcn_sage_fwd_args *args, hipStream_t stream);
 
@@ -391,6 +398,13 @@ int pgcn_sage_layer_fwd(const pgcn_partition *part, const pgcn_sage_fwd_args *ar
  * J_full is the gradient of the dropped input; apply the dropout mask to it
  * with pgcn_dropout (same arguments as in the forward) before it is sent or
  * accumulated.  J_in and J_bd_out are both NULL for the first layer.
+ * order == PGCN_ORDER_TRANSFORM (the forward used that order):
+ *     T = P_i^T M                    [n_inner + n_bd, f_out], in the workspace
+ *     dW rows [0, f_in) = [X_in ; X_bd]^T T,  rows [f_in, 2 f_in) = X_in^T M
+ *     J_full = T W_top^T, plus M W_bot^T on the inner rows
+ * X_bd is the (dropped) boundary input the forward used (NULL: zero rows); A
+ * and A_bf16 are unused.  bf16 path: X, T, M and W rounded to bf16 for the
+ * products.
  */
 typedef struct {
   int32_t f_in, f_out;
@@ -409,6 +423,8 @@ typedef struct {
   float *J_bd_out;             /* [n_bd, ld_in] out or NULL                      */
   void *workspace;
   size_t workspace_bytes;
+  int32_t order;               /* pgcn_layer_order (0: aggregate first)           */
+  const float *X_bd;           /* [n_bd, ld_in] or NULL        (PGCN_ORDER_TRANSFORM) */
 } pgcn_sage_bwd_args;
 int pgcn_sage_layer_bwd(const pgcn_partition *part, const pgcn_sage_bwd_args *args, hipStream_t stream);
 

@@ -70,14 +70,15 @@ class pgcn_bwd_args(C.Structure):
 class pgcn_sage_fwd_args(C.Structure):
     _fields_ = [("f_in", _i32), ("f_out", _i32), ("gemm_dtype", _i32), ("relu", _i32),
                 ("ld_in", _i64), ("ld_out", _i64), ("X_in", _vp), ("X_in_bf16", _vp), ("X_bd", _vp), ("W", _vp),
-                ("A", _vp), ("A_bf16", _vp), ("H_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz)]
+                ("A", _vp), ("A_bf16", _vp), ("H_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz),
+                ("order", _i32)]
 
 
 class pgcn_sage_bwd_args(C.Structure):
     _fields_ = [("f_in", _i32), ("f_out", _i32), ("gemm_dtype", _i32), ("relu", _i32),
                 ("ld_in", _i64), ("ld_out", _i64), ("J_out", _vp), ("H_out", _vp), ("A", _vp),
                 ("A_bf16", _vp), ("X_in", _vp), ("X_in_bf16", _vp), ("W", _vp), ("dW", _vp), ("J_in", _vp),
-                ("J_bd_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz)]
+                ("J_bd_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz), ("order", _i32), ("X_bd", _vp)]
 
 
 # every symbol include/pgcn.h declares, with its ctypes signature
@@ -269,18 +270,19 @@ def pgcn_dropout(out, inp, rows: int, cols: int, ld: int, row0: int, p: float, s
 
 
 def pgcn_sage_layer_fwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, X_in, X_in_bf16, X_bd, W,
-                        A, A_bf16, H_out, workspace, workspace_bytes, stream=None):
+                        A, A_bf16, H_out, workspace, workspace_bytes, order=PGCN_ORDER_AGG, stream=None):
     a = pgcn_sage_fwd_args(f_in, f_out, gemm_dtype, int(relu), ld_in, ld_out, _ptr(X_in), _ptr(X_in_bf16),
                            _ptr(X_bd), _ptr(W), _ptr(A), _ptr(A_bf16), _ptr(H_out), _ptr(workspace),
-                           workspace_bytes)
+                           workspace_bytes, order)
     _check(lib.pgcn_sage_layer_fwd(part.handle, C.byref(a), _stream(stream)), "pgcn_sage_layer_fwd")
 
 
 def pgcn_sage_layer_bwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, J_out, H_out, A, A_bf16,
-                        X_in, X_in_bf16, W, dW, J_in, J_bd_out, workspace, workspace_bytes, stream=None):
+                        X_in, X_in_bf16, W, dW, J_in, J_bd_out, workspace, workspace_bytes, order=PGCN_ORDER_AGG,
+                        X_bd=None, stream=None):
     a = pgcn_sage_bwd_args(f_in, f_out, gemm_dtype, int(relu), ld_in, ld_out, _ptr(J_out), _ptr(H_out), _ptr(A),
                            _ptr(A_bf16), _ptr(X_in), _ptr(X_in_bf16), _ptr(W), _ptr(dW), _ptr(J_in),
-                           _ptr(J_bd_out), _ptr(workspace), workspace_bytes)
+                           _ptr(J_bd_out), _ptr(workspace), workspace_bytes, order, _ptr(X_bd))
     _check(lib.pgcn_sage_layer_bwd(part.handle, C.byref(a), _stream(stream)), "pgcn_sage_layer_bwd")
 
 

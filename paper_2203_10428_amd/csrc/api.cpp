@@ -102,7 +102,7 @@ extern "C" size_t pgcn_layer_workspace_size(const pgcn_partition *p, int32_t f_i
   if (order == PGCN_ORDER_AGG) return pgcn_workspace_size(p, f_in, f_out, gemm_dtype);
   if (order != PGCN_ORDER_TRANSFORM || !p || f_in <= 0 || f_out <= 0) return 0;
   const size_t w = fwd_ws_tf(p, f_in, f_out, gemm_dtype);
-  const size_t b = bwd_ws_tf(p, f_in, f_out, true, gemm_dtype);
+  const size_t b = bwd_ws_tf(p, f_in, f_out, true, gemm_dtype) + m16_bytes(p, f_out, true, gemm_dtype);
   const size_t l = align_up(loss_workspace(p->n_inner), 256);
   const size_t m = w > b ? w : b;
   return m > l ? m : l;
@@ -483,6 +483,223 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
 
 // ---------------------------------------------------------------- GraphSAGE ---
 
+namespace {
+
+// GraphSAGE forward with z W_top evaluated as P_i (X W_top): Y = [X_in ; X_bd]
+// W_top, H_out = P_i Y, then H_out = act(H_out + X_in W_bot).
+int sage_fwd_transform(const pgcn_partition *p, const pgcn_sage_fwd_args *a, hipStream_t s) {
+  const bool bf16 = a->gemm_dtype == PGCN_BF16;
+  if (p->n_inner > 0) {
+    PGCN_REQUIRE(a->X_in && a->W && a->H_out, "pgcn_sage_layer_fwd: null X_in, W or H_out");
+    PGCN_REQUIRE(aligned16(a->X_in) && aligned16(a->X_bd) && aligned16(a->H_out),
+                 "pgcn_sage_layer_fwd: X_in/X_bd/H_out must be 16-byte aligned");
+    if (bf16)
+      PGCN_REQUIRE(a->X_in_bf16 && aligned16(a->X_in_bf16) && a->ld_in % 8 == 0,
+                   "pgcn_sage_layer_fwd: bf16 path needs X_in_bf16 (16-byte aligned) and ld_in % 8 == 0");
+  }
+  const size_t need = fwd_ws_tf(p, a->f_in, a->f_out, a->gemm_dtype);
+  if (!a->workspace || a->workspace_bytes < need)
+    return set_error(PGCN_EWORKSPACE, "pgcn_sage_layer_fwd: workspace too small");
+  if (p->n_inner == 0) return PGCN_OK;
+  const int64_t ldy = ld_y(a->f_out);
+  float *Y = (float *)a->workspace;
+  const bool bd = p->n_bd > 0 && a->X_bd != nullptr;
+  GemmArgs m{};
+  m.N = a->f_out;
+  m.K = a->f_in;
+  m.dtype = a->gemm_dtype;
+  m.lda = a->ld_in;
+  m.B = a->W;
+  m.ldb = a->f_out;
+  m.ldc = ldy;
+  m.workspace = (float *)((char *)a->workspace + fwd_tf_gemm_off(p, a->f_out));
+  m.workspace_bytes = gemm_nk_workspace(a->f_out, a->f_in, a->gemm_dtype);
+  for (int part = 0; part < (bd ? 2 : 1); ++part) {
+    m.M = (int32_t)(part ? p->n_bd : p->n_inner);
+    m.A = part ? a->X_bd : a->X_in;
+    m.C = part ? Y + p->n_inner * ldy : Y;
+    int rc = launch_gemm_nk(Gemm::NN_SRC32_PLAIN, m, s);
+    if (rc) return rc;
+  }
+  AggArgs g{};
+  g.plan = &p->plan;
+  g.col = p->d_col;
+  g.in_split = p->n_inner;
+  g.in_lo = Y;
+  g.in_hi = bd ? Y + p->n_inner * ldy : nullptr;
+  g.out_split = p->n_inner;
+  g.out_lo = a->H_out;
+  g.scale = p->d_inv_deg;
+  g.f = a->f_out;
+  g.ld_in = ldy;
+  g.ld_out = a->ld_out;
+  g.partials = (float *)((char *)a->workspace + fwd_tf_agg_off(p, a->f_out));
+  g.trace_kind = PGCN_TK_AGG_FWD;
+  int rc = launch_aggregate(g, s);
+  if (rc) return rc;
+  GemmArgs b{};                      // the self term, accumulated onto P_i Y, then the activation
+  b.M = (int32_t)p->n_inner;
+  b.N = a->f_out;
+  b.K = a->f_in;
+  b.dtype = a->gemm_dtype;
+  b.A = a->X_in;
+  b.A16 = a->X_in_bf16;
+  b.lda = a->ld_in;
+  b.B = a->W + (size_t)a->f_in * a->f_out;
+  b.ldb = a->f_out;
+  b.C = a->H_out;
+  b.ldc = a->ld_out;
+  b.workspace = m.workspace;
+  b.workspace_bytes = m.workspace_bytes;
+  return launch_gemm_nk(a->relu ? Gemm::NN_ACC_RELU : Gemm::NN_ACC_PLAIN, b, s);
+}
+
+// T = P_i^T M; dW = [[X_in ; X_bd]^T T ; X_in^T M]; J_full = T W_top^T (+ M W_bot^T on inner rows).
+int sage_bwd_transform(const pgcn_partition *p, const pgcn_sage_bwd_args *a, hipStream_t s) {
+  const bool bf16 = a->gemm_dtype == PGCN_BF16;
+  const bool input_grad = a->J_in != nullptr || a->J_bd_out != nullptr;
+  PGCN_REQUIRE(a->dW, "pgcn_sage_layer_bwd: null dW");
+  if (input_grad) {
+    PGCN_REQUIRE(a->J_in && (a->J_bd_out || p->n_bd == 0),
+                 "pgcn_sage_layer_bwd: J_in and J_bd_out must both be given (or both NULL)");
+    PGCN_REQUIRE(aligned16(a->J_in) && aligned16(a->J_bd_out),
+                 "pgcn_sage_layer_bwd: J_in/J_bd_out must be 16-byte aligned");
+  }
+  if (p->n_inner > 0) {
+    PGCN_REQUIRE(a->J_out && a->W && a->X_in, "pgcn_sage_layer_bwd: null J_out, W or X_in");
+    PGCN_REQUIRE(!a->relu || a->H_out, "pgcn_sage_layer_bwd: relu needs H_out as mask source");
+    PGCN_REQUIRE(aligned16(a->J_out) && aligned16(a->H_out) && aligned16(a->X_in) && aligned16(a->X_bd),
+                 "pgcn_sage_layer_bwd: J_out/H_out/X_in/X_bd must be 16-byte aligned");
+    if (bf16)
+      PGCN_REQUIRE(a->X_in_bf16 && aligned16(a->X_in_bf16) && a->ld_in % 8 == 0,
+                   "pgcn_sage_layer_bwd: bf16 path needs X_in_bf16 (16-byte aligned) and ld_in % 8 == 0");
+  }
+  const size_t need = bwd_ws_tf(p, a->f_in, a->f_out, input_grad, a->gemm_dtype) +
+                      m16_bytes(p, a->f_out, input_grad, a->gemm_dtype);
+  if (!a->workspace || a->workspace_bytes < need)
+    return set_error(PGCN_EWORKSPACE, "pgcn_sage_layer_bwd: workspace too small");
+  const size_t half = (size_t)a->f_in * a->f_out;
+  if (p->n_inner == 0) {             // no rows (so no boundary rows): both halves of dW are zero
+    GemmArgs z{};
+    z.M = 2 * a->f_in;
+    z.N = a->f_out;
+    z.dtype = a->gemm_dtype;
+    z.C = a->dW;
+    z.workspace = (float *)a->workspace;
+    z.workspace_bytes = a->workspace_bytes;
+    return launch_gemm(Gemm::TN_MASK_SPLITK, z, s);
+  }
+  const int64_t ldt = ld_y(a->f_out);
+  float *T = (float *)a->workspace;
+  char *R = (char *)a->workspace + y_bytes(p, a->f_out);
+  const size_t region = bwd_tf_region(p, a->f_in, a->f_out);
+  float *D = (float *)R;
+  float *partials = (float *)(R + align_up((size_t)p->n_inner * ldt * sizeof(float), 256));
+  int rc = launch_mask_scale(a->J_out, a->ld_out, a->relu ? a->H_out : nullptr, a->ld_out, p->d_inv_deg, p->n_inner,
+                             a->f_out, D, ldt, s);
+  if (rc) return rc;
+  AggArgs t{};
+  t.plan = &p->plan_t;
+  t.col = p->d_col_t;
+  t.in_split = p->n_inner;
+  t.in_lo = D;
+  t.out_split = p->n_inner;
+  t.out_lo = T;
+  t.out_hi = T + p->n_inner * ldt;
+  t.f = a->f_out;
+  t.ld_in = ldt;
+  t.ld_out = ldt;
+  t.partials = partials;
+  t.trace_kind = PGCN_TK_AGG_BWD;
+  rc = launch_aggregate(t, s);
+  if (rc) return rc;
+
+  GemmArgs g{};                      // top half: [X_in ; X_bd]^T T over n + b nodes
+  g.M = a->f_in;
+  g.N = a->f_out;
+  g.K = (int32_t)(p->n_inner + p->n_bd);
+  g.dtype = a->gemm_dtype;
+  g.A = a->X_in;
+  g.A_hi = p->n_bd > 0 ? a->X_bd : nullptr;
+  g.k_split = p->n_inner;
+  g.lda = a->ld_in;
+  g.B = T;
+  g.ldb = ldt;
+  g.C = a->dW;
+  g.ldc = a->f_out;
+  g.workspace = (float *)R;
+  g.workspace_bytes = region;
+  rc = launch_gemm(Gemm::TN_MASK_SPLITK, g, s);
+  if (rc) return rc;
+  uint16_t *M16 = (bf16 && input_grad)
+                      ? (uint16_t *)(R + region + gemm_nk_workspace(a->f_in, a->f_out, a->gemm_dtype)) : nullptr;
+  GemmArgs h{};                      // bottom half: X_in^T (J ∘ 1[H > 0]); bf16: also writes the rounded M
+  h.M = a->f_in;
+  h.N = a->f_out;
+  h.K = (int32_t)p->n_inner;
+  h.dtype = a->gemm_dtype;
+  h.A = a->X_in;
+  h.A16 = a->X_in_bf16;
+  h.lda = a->ld_in;
+  h.B = a->J_out;
+  h.ldb = a->ld_out;
+  h.Hmask = a->relu ? a->H_out : nullptr;
+  h.ldm = a->ld_out;
+  h.C = a->dW + half;
+  h.ldc = a->f_out;
+  h.workspace = (float *)R;
+  h.workspace_bytes = region;
+  h.M16 = M16;
+  h.ldm16 = ld_m16(a->f_out);
+  rc = launch_gemm(Gemm::TN_MASK_SPLITK, h, s);
+  if (rc || !input_grad) return rc;
+
+  GemmArgs d{};                      // J_in = M W_bot^T, then J_in += T_in W_top^T; J_bd_out = T_bd W_top^T
+  d.M = (int32_t)p->n_inner;
+  d.N = a->f_in;
+  d.K = a->f_out;
+  d.dtype = a->gemm_dtype;
+  d.A = a->J_out;
+  d.lda = a->ld_out;
+  d.Hmask = a->relu ? a->H_out : nullptr;
+  d.ldm = a->ld_out;
+  d.B = a->W + half;
+  d.ldb = a->f_out;
+  d.C = a->J_in;
+  d.ldc = a->ld_in;
+  d.workspace = (float *)(R + region);
+  d.workspace_bytes = gemm_nk_workspace(a->f_in, a->f_out, a->gemm_dtype);
+  if (M16) {
+    d.A = nullptr;
+    d.A16 = M16;
+    d.lda = ld_m16(a->f_out);
+    d.Hmask = nullptr;
+  }
+  rc = launch_gemm_nk(M16 ? Gemm::NT16_PLAIN : Gemm::MASK_NT_PLAIN, d, s);
+  if (rc) return rc;
+  GemmArgs e{};
+  e.N = a->f_in;
+  e.K = a->f_out;
+  e.dtype = a->gemm_dtype;
+  e.lda = ldt;
+  e.B = a->W;
+  e.ldb = a->f_out;
+  e.ldc = a->ld_in;
+  e.workspace = d.workspace;
+  e.workspace_bytes = d.workspace_bytes;
+  e.M = (int32_t)p->n_inner;
+  e.A = T;
+  e.C = a->J_in;
+  rc = launch_gemm_nk(Gemm::NT_SRC32_ACC_PLAIN, e, s);
+  if (rc || p->n_bd == 0) return rc;
+  e.M = (int32_t)p->n_bd;
+  e.A = T + p->n_inner * ldt;
+  e.C = a->J_bd_out;
+  return launch_gemm_nk(Gemm::MASK_NT_PLAIN, e, s);
+}
+
+}  // namespace
+
 extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_args *a, hipStream_t s) {
   int rc = check_part(p, "pgcn_sage_layer_fwd");
   if (rc) return rc;
@@ -493,6 +710,8 @@ extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_sage_layer_fwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0,
                "pgcn_sage_layer_fwd: ld_out must be >= f_out and a multiple of 4");
+  PGCN_REQUIRE(a->order == PGCN_ORDER_AGG || a->order == PGCN_ORDER_TRANSFORM, "pgcn_sage_layer_fwd: bad order");
+  if (a->order == PGCN_ORDER_TRANSFORM) return sage_fwd_transform(p, a, s);
   const bool bf16 = a->gemm_dtype == PGCN_BF16;
   if (p->n_inner > 0) {
     PGCN_REQUIRE(a->X_in && a->W && a->H_out, "pgcn_sage_layer_fwd: null X_in, W or H_out");
@@ -567,6 +786,8 @@ extern "C" int pgcn_sage_layer_bwd(const pgcn_partition *p, const pgcn_sage_bwd_
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_sage_layer_bwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0,
                "pgcn_sage_layer_bwd: ld_out must be >= f_out and a multiple of 4");
+  PGCN_REQUIRE(a->order == PGCN_ORDER_AGG || a->order == PGCN_ORDER_TRANSFORM, "pgcn_sage_layer_bwd: bad order");
+  if (a->order == PGCN_ORDER_TRANSFORM) return sage_bwd_transform(p, a, s);
   const bool bf16 = a->gemm_dtype == PGCN_BF16;
   const bool input_grad = a->J_in != nullptr || a->J_bd_out != nullptr;
   PGCN_REQUIRE(a->dW, "pgcn_sage_layer_bwd: null dW");

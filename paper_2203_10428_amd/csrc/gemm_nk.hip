@@ -492,6 +492,12 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
       break;
     case Gemm::MASK_NT_ROWSCALE: nk_launch_bn<NK_A_MASK, NK_E_ROWSCALE>(p, bf16, s); break;
     case Gemm::MASK_NT_PLAIN: nk_launch_bn<NK_A_MASK, NK_E_PLAIN>(p, bf16, s); break;
+    case Gemm::NT_SRC32_ACC_PLAIN:                     // C += A W^T, fp32 A rounded while staged on bf16
+      if (!p.A) return set_error(PGCN_EINVAL, "launch_gemm_nk: NT_SRC32 needs the fp32 operand");
+      p.Am = nullptr;
+      if (bf16) nk_launch_bn<NK_A_MASK, NK_E_ACC_PLAIN>(p, true, s);
+      else nk_launch_bn<NK_A_F32, NK_E_ACC_PLAIN>(p, false, s);
+      break;
     case Gemm::NT16_ROWSCALE:
     case Gemm::NT16_PLAIN:
       if (!bf16 || !p.A16) return set_error(PGCN_EINVAL, "launch_gemm_nk: NT16 needs the bf16 path and A16");

@@ -130,11 +130,12 @@ size_t aggregate_workspace(const Plan &plan, int64_t f);
 // NN_*: C (=|+=) A W, with ReLU for *_RELU (ACC: C = act(C + A W));
 // MASK_NT_*: C = (J ∘ mask) W^T, row-scaled or plain (fp32 J and mask; rounded to bf16 on the
 // bf16 path); NT16_*: the same with the masked operand already bf16 in A16;
+// NT_SRC32_ACC_PLAIN: C += A W^T from the fp32 operand on both paths;
 // NN_SRC32_PLAIN / _ROWSCALE / _RELU: C = act((diag(rowscale)) A W) from the fp32 operand on both paths
 // (rounded to bf16 while staged on the bf16 path); TN_MASK_SPLITK: C = A^T (J ∘ mask)
 enum class Gemm {
   NN_RELU, NN_PLAIN, NN_ACC_RELU, NN_ACC_PLAIN, MASK_NT_ROWSCALE, MASK_NT_PLAIN, NT16_ROWSCALE, NT16_PLAIN,
-  NN_SRC32_PLAIN, NN_SRC32_ROWSCALE, NN_SRC32_RELU, TN_MASK_SPLITK
+  NN_SRC32_PLAIN, NN_SRC32_ROWSCALE, NN_SRC32_RELU, NT_SRC32_ACC_PLAIN, TN_MASK_SPLITK
 };
 struct GemmArgs {
   int32_t M, N, K;

@@ -138,8 +138,7 @@ class PartitionTrainer:
         self.Xd_16 = {l: z(n, wd[l - 1], torch.bfloat16) for l in range(1, L + 1)} \
             if (self.sage and not f32) else {}
         self.G_peer = [None] * L
-        self.order = {l: (B.PGCN_ORDER_AGG if self.sage else layer_order(opts.order, wd[l - 1], wd[l]))
-                      for l in range(1, L + 1)}
+        self.order = {l: layer_order(opts.order, wd[l - 1], wd[l]) for l in range(1, L + 1)}
         self.cache1 = opts.cache_layer1
         if self.cache1:
             assert not self.sage and opts.dropout == 0.0, "layer-1 caching needs a constant layer input"
@@ -252,7 +251,7 @@ class PartitionTrainer:
                       ld_out=ld_of(wd[l]), W=self.W[l - 1], A=self.A[l], A_bf16=self.A16[l], H_out=self.H[l],
                       workspace=self.ws, workspace_bytes=self.ws_bytes, stream=st)
         if self.sage:
-            B.pgcn_sage_layer_fwd(self.part, X_in=X_in, X_in_bf16=X16, X_bd=X_bd, **common)
+            B.pgcn_sage_layer_fwd(self.part, X_in=X_in, X_in_bf16=X16, X_bd=X_bd, order=self.order[l], **common)
         else:
             B.pgcn_layer_fwd(self.part, H_in=X_in, H_bd=X_bd, order=self.order[l], **common)
         self.X_used[l] = X_in
@@ -267,7 +266,8 @@ class PartitionTrainer:
                       W=self.W[l - 1], dW=self.dW[l - 1], J_in=self.J_in.get(l), J_bd_out=self.J_bd_out.get(l),
                       workspace=self.ws, workspace_bytes=self.ws_bytes, stream=st)
         if self.sage:
-            B.pgcn_sage_layer_bwd(self.part, X_in=self.X_used[l], X_in_bf16=self.Xd_16.get(l), **common)
+            B.pgcn_sage_layer_bwd(self.part, X_in=self.X_used[l], X_in_bf16=self.Xd_16.get(l), order=self.order[l],
+                                  X_bd=self.X_bd_used.get(l), **common)
         else:
             B.pgcn_layer_bwd(self.part, order=self.order[l], H_in=self.X_used.get(l), H_bd=self.X_bd_used.get(l),
                              **common)

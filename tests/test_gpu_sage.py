@@ -184,6 +184,50 @@ def test_sage_layer_backward(graphs, gname, dt, f_in, f_out, input_grad):
         assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
 
 
+@pytest.mark.parametrize("gname", ["plain", "sparse", "chunked"])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("f_in,f_out", [(5, 3), (47, 41), (602, 256), (128, 100), (100, 128)])
+@pytest.mark.parametrize("with_bd", [True, False])
+def test_sage_layer_transform(graphs, gname, dt, f_in, f_out, with_bd):
+    """Forward and backward in the transform-first association against the oracle's reading of it."""
+    g = graphs[gname]
+    rng = np.random.default_rng(f_in * 31 + f_out)
+    n, b = g.ref.n_inner, g.ref.n_bd
+    X_in = rng.standard_normal((n, f_in))
+    X_bd = rng.standard_normal((b, f_in)) if with_bd else np.zeros((b, f_in))
+    X_full = np.vstack([X_in, X_bd])
+    W = rng.uniform(-0.2, 0.2, (2 * f_in, f_out)).astype(np.float32)
+    relu = f_out != 3
+    bf16 = dt == "bf16"
+    gm = "bf16" if bf16 else "f64"
+    dtype = B.PGCN_BF16 if bf16 else B.PGCN_F32
+    z_ref, Z_ref, H_ref = layers.sage_forward(g.P, X_full, n, W.astype(np.float64), relu, gm, order="transform")
+    dX, dXbd = dev(X_in), (dev(X_bd) if with_bd else None)
+    dX16 = dev(X_in, dtype=torch.bfloat16) if bf16 else None
+    H = dev(np.zeros((n, f_out)))
+    nb = B.pgcn_layer_workspace_size(g.part, f_in, f_out, dtype, B.PGCN_ORDER_TRANSFORM)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    common = dict(f_in=f_in, f_out=f_out, gemm_dtype=dtype, relu=relu, ld_in=ld_of(f_in), ld_out=ld_of(f_out),
+                  W=torch.from_numpy(W).cuda(), A=None, A_bf16=None, workspace=ws, workspace_bytes=nb,
+                  order=B.PGCN_ORDER_TRANSFORM)
+    B.pgcn_sage_layer_fwd(g.part, X_in=dX, X_in_bf16=dX16, X_bd=dXbd, H_out=H, **common)
+    assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"]
+    # backward from a fixed Z (mask) and J
+    Z = rng.standard_normal((n, f_out))
+    J = rng.standard_normal((n, f_out)) * 1e-2
+    G_ref, Jf_ref = layers.sage_backward(g.P, None, X_in, Z, J, W.astype(np.float64), relu, True, gm,
+                                         order="transform", X_full=X_full)
+    dG = torch.zeros((2 * f_in, f_out), device="cuda")
+    J_in, J_bd = dev(np.zeros((n, f_in))), dev(np.zeros((b, f_in)))
+    B.pgcn_sage_layer_bwd(g.part, J_out=dev(J), H_out=dev(np.maximum(Z, 0) if relu else Z), X_in=dX, X_in_bf16=dX16,
+                          X_bd=dXbd, dW=dG, J_in=J_in, J_bd_out=J_bd, **common)
+    tol = TOL[dt]["grad"]
+    torch.cuda.synchronize()
+    assert rel_err(dG.cpu().numpy(), G_ref) < tol
+    assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol
+    assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
+
+
 def test_layer_entry_points_check_the_partition_kind(graphs):
     g = graphs["plain"]
     n = g.ref.n_inner
