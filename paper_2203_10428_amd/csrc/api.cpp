@@ -581,13 +581,17 @@ int sage_bwd_transform(const pgcn_partition *p, const pgcn_sage_bwd_args *a, hip
   const size_t half = (size_t)a->f_in * a->f_out;
   if (p->n_inner == 0) {             // no rows (so no boundary rows): both halves of dW are zero
     GemmArgs z{};
-    z.M = 2 * a->f_in;
+    z.M = a->f_in;
     z.N = a->f_out;
     z.dtype = a->gemm_dtype;
-    z.C = a->dW;
     z.workspace = (float *)a->workspace;
     z.workspace_bytes = a->workspace_bytes;
-    return launch_gemm(Gemm::TN_MASK_SPLITK, z, s);
+    for (int hlf = 0; hlf < 2; ++hlf) {
+      z.C = a->dW + hlf * half;
+      int rc = launch_gemm(Gemm::TN_MASK_SPLITK, z, s);
+      if (rc) return rc;
+    }
+    return PGCN_OK;
   }
   const int64_t ldt = ld_y(a->f_out);
   float *T = (float *)a->workspace;

@@ -1,0 +1,107 @@
+"""Degenerate partitions through the C ABI, for every layer form the library
+offers (aggregate-first and transform-first GCN, mean and symmetric
+normalisation, GraphSAGE in both associations), against the oracle:
+
+* one partition: no boundary rows and no send list (n_bd = 0), so the split
+  weight-gradient GEMM has no second matrix and the transposed aggregation no
+  outgoing rows;
+* an empty partition (owns no node): every call succeeds, dW = 0;
+* a partition whose inner nodes have no edges (P = I with self loops, zero
+  rows of the GraphSAGE mean).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import TOL, dev, host, random_partition_graph, rel_err
+from oracle import layers
+from oracle.partition import build_partition, propagation_matrix
+from paper_2203_10428_amd import binding as B
+from paper_2203_10428_amd.step import ld_of
+
+pytestmark = pytest.mark.gpu
+
+FORMS = [("gcn", "mean", "agg"), ("gcn", "mean", "transform"), ("gcn", "sym", "agg"), ("gcn", "sym", "transform"),
+         ("sage", "mean", "agg"), ("sage", "mean", "transform")]
+ORDER = {"agg": B.PGCN_ORDER_AGG, "transform": B.PGCN_ORDER_TRANSFORM}
+
+
+def graph(kind):
+    if kind == "one_partition":
+        n, rowptr, col, _ = random_partition_graph(900, 300, 2, 10, 4)
+        return n, rowptr, col, np.zeros(n, np.int32), 1
+    if kind == "empty":
+        n, rowptr, col, owner = random_partition_graph(600, 300, 3, 8, 5)
+        owner = np.where(owner == 0, 1, owner).astype(np.int32)      # partition 0 owns nothing
+        return n, rowptr, col, owner, 3
+    n = 700                                                          # no edges at all
+    return n, np.zeros(n + 1, np.int64), np.zeros(0, np.int32), (np.arange(n) % 2).astype(np.int32), 2
+
+
+def run_layer(kind, model, norm, order, dt, f_in=37, f_out=21):
+    n_g, rowptr, col, owner, nparts = graph(kind)
+    sage = model == "sage"
+    ref = build_partition(n_g, rowptr, col, owner, 0, nparts, self_loop=not sage)
+    P = propagation_matrix(ref, norm)
+    part = B.pgcn_partition_setup(n_g, rowptr, col, owner, nparts, 0, self_loop=not sage, symmetric=norm == "sym")
+    n, b = ref.n_inner, ref.n_bd
+    rng = np.random.default_rng(n + b + f_in)
+    X = rng.standard_normal((n + b, f_in))
+    k = 2 if sage else 1
+    W = rng.uniform(-0.3, 0.3, (k * f_in, f_out)).astype(np.float32)
+    J = rng.standard_normal((n, f_out)) * 1e-2
+    gm = "bf16" if dt == "bf16" else "f64"
+    dtype = B.PGCN_BF16 if dt == "bf16" else B.PGCN_F32
+    nb = max(B.pgcn_layer_workspace_size(part, f_in, f_out, dtype, ORDER[order]), 256)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    dX, dXbd = dev(X[:n]), dev(X[n:])
+    dX16 = dev(X[:n], dtype=torch.bfloat16) if dt == "bf16" else None
+    agg = order == "agg"
+    A = dev(np.zeros((n, f_in))) if agg else None
+    A16 = torch.zeros((n, ld_of(f_in)), dtype=torch.bfloat16, device="cuda") if agg and dt == "bf16" else None
+    H = dev(np.zeros((n, f_out)))
+    common = dict(f_in=f_in, f_out=f_out, gemm_dtype=dtype, relu=True, ld_in=ld_of(f_in), ld_out=ld_of(f_out),
+                  W=torch.from_numpy(W).cuda(), workspace=ws, workspace_bytes=nb, order=ORDER[order])
+    if sage:
+        B.pgcn_sage_layer_fwd(part, X_in=dX, X_in_bf16=dX16, X_bd=dXbd if b else None, A=A, A_bf16=A16, H_out=H,
+                              **common)
+        z_ref, Z, H_ref = layers.sage_forward(P, X, n, W.astype(np.float64), True, gm, order=order)
+    else:
+        B.pgcn_layer_fwd(part, H_in=dX, H_bd=dXbd if b else None, A=A, A_bf16=A16, H_out=H, **common)
+        A_ref, Z, H_ref = layers.layer_forward(P, X, W.astype(np.float64), True, gm, order=order)
+    dG = torch.full((k * f_in, f_out), 3.0, device="cuda")
+    J_in, J_bd = dev(np.zeros((n, f_in))), (dev(np.zeros((b, f_in))) if b else None)
+    if sage:
+        B.pgcn_sage_layer_bwd(part, J_out=dev(J), H_out=H, A=A, A_bf16=A16, X_in=dX, X_in_bf16=dX16,
+                              X_bd=dXbd if b else None, dW=dG, J_in=J_in, J_bd_out=J_bd, **common)
+        G_ref, Jf_ref = layers.sage_backward(P, z_ref, X[:n], Z, J, W.astype(np.float64), True, True, gm,
+                                             order=order, X_full=X)
+    else:
+        B.pgcn_layer_bwd(part, J_out=dev(J), H_out=H, A=A, A_bf16=A16, dW=dG, J_in=J_in, J_bd_out=J_bd,
+                         H_in=dX, H_bd=dXbd if b else None, **common)
+        G_ref, Jf_ref = layers.layer_backward(P, A_ref, Z, J, W.astype(np.float64), True, True, gm, order=order,
+                                              H_full=X)
+    torch.cuda.synchronize()
+    return dict(n=n, b=b, H=host(H, f_out), H_ref=H_ref, G=dG.cpu().numpy(), G_ref=G_ref,
+                J_in=host(J_in, f_in), J_bd=host(J_bd, f_in) if b else np.zeros((0, f_in)), Jf_ref=Jf_ref)
+
+
+@pytest.mark.parametrize("model,norm,order", FORMS)
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", ["one_partition", "no_edges"])
+def test_degenerate_partitions(kind, model, norm, order, dt):
+    r = run_layer(kind, model, norm, order, dt)
+    if kind == "one_partition":
+        assert r["b"] == 0
+    tol = TOL[dt]
+    assert rel_err(r["H"], r["H_ref"]) < tol["act"]
+    assert rel_err(r["G"], r["G_ref"]) < tol["grad"]
+    assert rel_err(r["J_in"], r["Jf_ref"][: r["n"]]) < tol["grad"]
+    assert rel_err(r["J_bd"], r["Jf_ref"][r["n"]:]) < tol["grad"]
+
+
+@pytest.mark.parametrize("model,norm,order", FORMS)
+def test_empty_partition(model, norm, order):
+    r = run_layer("empty", model, norm, order, "f32")
+    assert r["n"] == 0 and r["b"] == 0
+    assert np.all(r["G"] == 0)
