@@ -158,7 +158,7 @@ def main():
                     help="variant: keep layer 1's aggregate across steps (constant input features); it reuses "
                          "outputs across steps, so its line is a variant, not the step's measurement")
     ap.add_argument("--no-copy-modes", action="store_true", help="skip the serial / no-refill comparison")
-    ap.add_argument("--refill", default="dma", choices=["dma", "blit"], help="engine of the stale-buffer refills")
+    ap.add_argument("--refill", default="blit", choices=["dma", "blit"], help="engine of the stale-buffer refills")
     ap.add_argument("--remote", default="device", choices=["device", "host"],
                     help="where the emulated peers' data lives: device memory, or pinned host memory (refills "
                          "cross the host link, as in the paper's CPU-staged exchange)")

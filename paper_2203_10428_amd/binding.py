@@ -168,7 +168,7 @@ class Partition:
 
     def __del__(self):
         h = getattr(self, "handle", None)
-        if h:
+        if h and lib is not None:                  # at interpreter exit the module may be torn down first
             lib.pgcn_partition_destroy(h)
             self.handle = None
 
