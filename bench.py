@@ -225,9 +225,9 @@ def main():
 
     def summarise(records, k):
         kinds = {}
-        for name, ms in records:
+        for name, ms, launches in records:     # an aggregation record spans its back-to-back chunk launches
             c = kinds.setdefault(name, [0, 0.0])
-            c[0] += 1
+            c[0] += launches
             c[1] += ms
         return {n: {"launches": c[0] / k, "ms_per_step": c[1] / k, "avg_launch_ms": c[1] / c[0]}
                 for n, c in kinds.items()}
@@ -242,7 +242,8 @@ def main():
     dominant = max((k for k in compute_kinds if k in breakdown), key=lambda k: breakdown[k]["ms_per_step"])
 
     # timed region: exactly --steps steps; the dominant kernel's launches are
-    # bracketed by HIP events on their launch stream (the roofline's durations)
+    # bracketed by HIP events on their launch stream (the roofline's durations;
+    # aggregation chunk launches of one column range share one pair)
     B.pgcn_trace_enable(max(1024, args.steps * 256))
     B.pgcn_trace_filter([dominant])
     ms_per_step = timed(args.steps, "pipe")

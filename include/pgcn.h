@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 160
+#define PGCN_VERSION 161
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -442,9 +442,14 @@ int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, 
 /*
  * Kernel tracing (measurement support).  While enabled, every kernel launch
  * (and every refill copy) of the library is bracketed by a HIP event pair
- * recorded on the launch stream; pgcn_trace_collect waits for the recorded
- * pairs and returns each launch's kind (pgcn_trace_kind) and duration in ms,
- * then clears the record.  pgcn_trace_enable creates `capacity` event pairs
+ * recorded on the launch stream, except that the chunk launches of one
+ * aggregation column range (PGCN_TK_AGG_FWD / _BWD), which run back to back,
+ * share one pair: each event record costs the stream several microseconds.
+ * pgcn_trace_collect waits for the recorded pairs and returns each record's
+ * kind (pgcn_trace_kind), duration in ms and the number of launches it spans
+ * (`launches`, may be NULL; 1 except for the shared aggregation records,
+ * which may span 0 launches when every chunk is empty), then clears the
+ * record.  pgcn_trace_enable creates `capacity` event pairs
  * up front (timing-only events without the system-scope cache flush a
  * default event record performs, so tracing does not disturb the caches of
  * the kernels it brackets) and resets the kind filter to "all kinds";
@@ -461,7 +466,7 @@ enum pgcn_trace_kind {
 };
 int pgcn_trace_enable(int32_t capacity);
 int pgcn_trace_filter(uint32_t kind_mask);
-int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t max_records, int32_t *count);
+int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t *launches, int32_t max_records, int32_t *count);
 int pgcn_trace_disable(void);
 
 const char *pgcn_last_error(void);

@@ -105,7 +105,7 @@ SIGNATURES = {
     "pgcn_refill_async": (_i32, [_vp, _vp, _sz, _u32, _vp]),
     "pgcn_trace_enable": (_i32, [_i32]),
     "pgcn_trace_filter": (_i32, [C.c_uint32]),
-    "pgcn_trace_collect": (_i32, [_vp, _vp, _i32, C.POINTER(_i32)]),
+    "pgcn_trace_collect": (_i32, [_vp, _vp, _vp, _i32, C.POINTER(_i32)]),
     "pgcn_trace_disable": (_i32, []),
     "pgcn_last_error": (C.c_char_p, []),
     "pgcn_version": (_i32, []),
@@ -311,12 +311,16 @@ def pgcn_trace_filter(kinds=None):
 
 
 def pgcn_trace_collect(max_records: int = 1 << 16):
-    """[(kind name, ms)] of the launches recorded since the last collect."""
+    """[(kind name, ms, launches)] of the records since the last collect (a record spans
+    one launch, or the back-to-back chunk launches of one aggregation column range)."""
     kinds = np.zeros(max_records, np.int32)
     ms = np.zeros(max_records, np.float32)
+    nl = np.zeros(max_records, np.int32)
     cnt = C.c_int32(0)
-    _check(lib.pgcn_trace_collect(kinds.ctypes.data, ms.ctypes.data, max_records, C.byref(cnt)), "pgcn_trace_collect")
-    return [(TRACE_KINDS[k], float(v)) for k, v in zip(kinds[: cnt.value], ms[: cnt.value])]
+    _check(lib.pgcn_trace_collect(kinds.ctypes.data, ms.ctypes.data, nl.ctypes.data, max_records, C.byref(cnt)),
+           "pgcn_trace_collect")
+    n = cnt.value
+    return [(TRACE_KINDS[k], float(v), int(c)) for k, v, c in zip(kinds[:n], ms[:n], nl[:n])]
 
 
 def pgcn_trace_disable():

@@ -380,16 +380,21 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
     p.slices = S;
     const int U = 8;
     const int threshold = (64 / SL) * U;
-    for (int c = 0; c < C; ++c) {
-      p.mode = (c == 0 ? AGG_FIRST : 0) | (c == C - 1 ? AGG_LAST : 0);
-      const int64_t b = plan.chunk_items[c], e = plan.chunk_items[c + 1];
-      if (e == b) continue;
-      p.items = plan.d_items + b;
-      p.n_items = e - b;
-      p.n_long = first_short(plan, c, threshold) - b;
-      TraceScope ts(a.trace_kind, s);
-      launch_dispatch(p, SL, s);
-      PGCN_HIP(hipGetLastError());
+    {
+      TraceScope ts(a.trace_kind, s);      // one record for the chunk launches, which run back to back
+      int32_t launched = 0;
+      for (int c = 0; c < C; ++c) {
+        p.mode = (c == 0 ? AGG_FIRST : 0) | (c == C - 1 ? AGG_LAST : 0);
+        const int64_t b = plan.chunk_items[c], e = plan.chunk_items[c + 1];
+        if (e == b) continue;
+        p.items = plan.d_items + b;
+        p.n_items = e - b;
+        p.n_long = first_short(plan, c, threshold) - b;
+        launch_dispatch(p, SL, s);
+        ++launched;
+        PGCN_HIP(hipGetLastError());
+      }
+      ts.set_launches(launched);
     }
     if (!plan.splits.empty()) {       // split rows: all their slots, in (chunk, segment) order
       p.mode = AGG_FIRST | AGG_LAST;

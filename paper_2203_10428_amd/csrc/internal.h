@@ -75,11 +75,13 @@ namespace pgcn {
 int set_error(int code, const std::string &msg);
 
 // Records a HIP event pair around a kernel launch on stream `s` while tracing
-// is enabled (pgcn_trace_enable); does nothing otherwise.
+// is enabled (pgcn_trace_enable); does nothing otherwise.  A scope around
+// several back-to-back launches says how many with set_launches.
 class TraceScope {
  public:
   TraceScope(int32_t kind, hipStream_t s);
   ~TraceScope();
+  void set_launches(int32_t n);
   TraceScope(const TraceScope &) = delete;
   TraceScope &operator=(const TraceScope &) = delete;
 

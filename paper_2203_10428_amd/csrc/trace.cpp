@@ -1,7 +1,9 @@
 // Kernel tracing: when enabled, every kernel launch of the library (of the
 // kinds selected by the filter) is bracketed by a pair of HIP events recorded
 // on the launch stream, so the caller can read per-kernel durations measured
-// on the stream the kernel ran on.  Event pairs are created once by
+// on the stream the kernel ran on.  The chunk launches of one aggregation
+// column range share a pair (one record spanning several launches): an
+// event record between back-to-back kernels costs several microseconds.  Event pairs are created once by
 // pgcn_trace_enable (no allocation while tracing) without the system-scope
 // fence of a default event: a fenced record writes back and invalidates the
 // caches, which would slow the traced kernels themselves.  Launches beyond
@@ -18,7 +20,7 @@ struct TraceState {
   bool on = false;
   uint32_t mask = 0xffffffffu;
   std::vector<hipEvent_t> start, stop;
-  std::vector<int32_t> kind;
+  std::vector<int32_t> kind, launches;
   size_t used = 0;
 };
 TraceState &state() {
@@ -34,7 +36,12 @@ TraceScope::TraceScope(int32_t kind, hipStream_t s) : s_(s) {
   if (!t.on || t.used >= t.start.size() || kind < 0 || kind > 31 || !((t.mask >> kind) & 1u)) return;
   slot_ = (int64_t)t.used++;
   t.kind[slot_] = kind;
+  t.launches[slot_] = 1;
   (void)hipEventRecord(t.start[slot_], s_);
+}
+
+void TraceScope::set_launches(int32_t n) {
+  if (slot_ >= 0) state().launches[slot_] = n;
 }
 
 TraceScope::~TraceScope() {
@@ -56,6 +63,7 @@ extern "C" int pgcn_trace_enable(int32_t capacity) {
   t.start.assign(capacity, nullptr);
   t.stop.assign(capacity, nullptr);
   t.kind.assign(capacity, -1);
+  t.launches.assign(capacity, 0);
   for (int32_t i = 0; i < capacity; ++i) {
     PGCN_HIP(hipEventCreateWithFlags(&t.start[i], hipEventDisableSystemFence));
     PGCN_HIP(hipEventCreateWithFlags(&t.stop[i], hipEventDisableSystemFence));
@@ -73,7 +81,8 @@ extern "C" int pgcn_trace_filter(uint32_t kind_mask) {
   return PGCN_OK;
 }
 
-extern "C" int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t max_records, int32_t *count) {
+extern "C" int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t *launches, int32_t max_records,
+                                  int32_t *count) {
   PGCN_REQUIRE(count && max_records >= 0 && (max_records == 0 || (kinds && ms)), "pgcn_trace_collect: bad arguments");
   TraceState &t = state();
   std::lock_guard<std::mutex> g(t.mu);
@@ -84,6 +93,7 @@ extern "C" int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t max_records
     PGCN_HIP(hipEventElapsedTime(&v, t.start[i], t.stop[i]));
     kinds[i] = t.kind[i];
     ms[i] = v;
+    if (launches) launches[i] = t.launches[i];
   }
   *count = n;
   t.used = 0;
