@@ -31,6 +31,7 @@
 // of the left operand come from a second matrix (A_hi), and on the bf16 path
 // that operand is fp32 in memory and rounded while staged (template A32).
 #include <algorithm>
+#include <cstdlib>
 
 #include "internal.h"
 
@@ -106,9 +107,9 @@ __device__ __forceinline__ void tn_store_partial(const TNParams &p, const f32x16
 // H alike, coalesced over the row), and the next-but-one slab is loaded into a
 // second register set, so each load has two slabs of MFMAs to arrive.
 
-template <int BN>
+template <int BM, int BN>
 __global__ __launch_bounds__(256, BN == 128 ? 2 : 3) void gemm_tn_f32(TNParams p) {
-  constexpr int BM = 128, BK = 16;                     // BK nodes per slab
+  constexpr int BK = 16;                               // BK nodes per slab
   constexpr int LDA = BM + 32, LDB = BN + 32;
   constexpr int VA = BK * BM / 4 / 256, VB = BK * BN / 4 / 256;
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
@@ -193,7 +194,7 @@ __global__ __launch_bounds__(256, BN == 128 ? 2 : 3) void gemm_tn_f32(TNParams p
   };
 
   const int ns = (kend - kbeg + BK - 1) / BK;          // slabs of this split (<= 0: none)
-  if (ns > 0) {
+  if (ns > 0 && BM == 128) {
     Regs R0, R1;
     load(R0, kbeg);
     load(R1, kbeg + BK);                               // past kend: zero vectors, no loads
@@ -208,6 +209,20 @@ __global__ __launch_bounds__(256, BN == 128 ? 2 : 3) void gemm_tn_f32(TNParams p
       load(R1, kbeg + (sl + 3) * BK);
       compute(1);
       store(R0, 0);
+      __syncthreads();
+    }
+  } else if (ns > 0) {
+    // 256-row tiles: a slab's MFMAs take twice as long, so loads one slab
+    // ahead have time to arrive, and one register set leaves room for the
+    // 128 accumulators
+    Regs R0;
+    load(R0, kbeg);
+    store(R0, 0);
+    __syncthreads();
+    for (int sl = 0; sl < ns; ++sl) {
+      load(R0, kbeg + (sl + 1) * BK);
+      compute(sl & 1);
+      store(R0, (sl + 1) & 1);
       __syncthreads();
     }
   }
@@ -428,9 +443,24 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *ws, int
 
 // ---------------------------------------------------------------- launch ---
 
-static int tn_tiles(int M, int N) {
+// Tile height of the fp32 kernel: 256 (each wave 128 x 64: the same staged
+// bytes feed twice the MFMAs, and staging, not the matrix cores, bounds the
+// 128-row tile) for 128-wide tiles when f_in >= 384 and 256-row tiles pad it
+// no further than 128-row tiles would; 128 otherwise and on bf16 (at f_in =
+// 256 the two tiles leave the grid short of one round of resident
+// workgroups: measured slower).  PGCN_TN_BM=128 (environment) keeps 128.
+static int tn_bm(int M, int N, bool bf16) {
+  static const bool only128 = [] {
+    const char *e = std::getenv("PGCN_TN_BM");
+    return e && std::atoi(e) == 128;
+  }();
+  if (bf16 || N <= 64 || only128 || M < 384) return 128;
+  return (M + 255) / 256 * 256 <= (M + 127) / 128 * 128 ? 256 : 128;
+}
+
+static int tn_tiles(int M, int N, int bm) {
   const int BN = N <= 64 ? 64 : 128;
-  return ((M + 127) / 128) * ((N + BN - 1) / BN);
+  return ((M + bm - 1) / bm) * ((N + BN - 1) / BN);
 }
 
 // Resident workgroups of a variant on 256 CUs: three per CU, two for the
@@ -443,8 +473,8 @@ static int tn_slots(int N, bool bf16, bool a32) {
 // Splits over the nodes: tiles x splits about one round of resident
 // workgroups, at least 256 nodes per split, and tiles x splits a multiple of 8
 // when possible (XCD mapping).
-static int splitk_count(int M, int N, int K, int slots) {
-  const int tiles = tn_tiles(M, N);
+static int splitk_count(int M, int N, int K, int slots, int bm) {
+  const int tiles = tn_tiles(M, N, bm);
   int s = slots / tiles;
   const int max_s = (K + 255) / 256;
   if (s > max_s) s = max_s;
@@ -457,13 +487,13 @@ static int splitk_count(int M, int N, int K, int slots) {
 
 size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K) {
   if (kind != Gemm::TN_MASK_SPLITK) return 0;
-  const int s = std::max(splitk_count(M, N, K, 512), splitk_count(M, N, K, 768));   // any variant
+  const int s = std::max({splitk_count(M, N, K, 512, 128), splitk_count(M, N, K, 768, 128),
+                           splitk_count(M, N, K, 512, 256)});                     // any variant
   return (size_t)s * (size_t)M * (size_t)N * sizeof(float);
 }
 
-template <int BN>
+template <int BM, int BN>
 static void tn_launch(TNParams p, bool bf16, bool a32, int splits, hipStream_t s) {
-  constexpr int BM = 128;
   p.tiles_n = (p.N + BN - 1) / BN;
   p.tiles = ((p.M + BM - 1) / BM) * p.tiles_n;
   const int slab = bf16 ? 32 : 16;
@@ -474,7 +504,7 @@ static void tn_launch(TNParams p, bool bf16, bool a32, int splits, hipStream_t s
   const dim3 grid((unsigned)(p.tiles * splits));
   if (bf16 && a32) hipLaunchKernelGGL((gemm_tn_bf16<BN, true>), grid, dim3(256), 0, s, p);
   else if (bf16) hipLaunchKernelGGL((gemm_tn_bf16<BN, false>), grid, dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((gemm_tn_f32<BN>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((gemm_tn_f32<BM, BN>), grid, dim3(256), 0, s, p);
 }
 
 int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
@@ -482,7 +512,8 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return PGCN_OK;
   const bool bf16 = g.dtype == PGCN_BF16;
   const bool a32 = g.k_split > 0;                      // second left matrix; fp32 left operand on both paths
-  const int splits = splitk_count(g.M, g.N, g.K, tn_slots(g.N, bf16, a32));
+  const int bm = tn_bm(g.M, g.N, bf16);
+  const int splits = splitk_count(g.M, g.N, g.K, tn_slots(g.N, bf16, a32), bm);
   const size_t need = (size_t)splits * (size_t)g.M * (size_t)g.N * sizeof(float);
   if (!g.workspace || g.workspace_bytes < need)
     return set_error(PGCN_EWORKSPACE, "weight-gradient GEMM: workspace too small");
@@ -510,8 +541,9 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   }
   {
     TraceScope ts(PGCN_TK_GEMM_WGRAD, s);
-    if (g.N <= 64) tn_launch<64>(p, bf16, a32, splits, s);
-    else tn_launch<128>(p, bf16, a32, splits, s);
+    if (g.N <= 64) tn_launch<128, 64>(p, bf16, a32, splits, s);
+    else if (bm == 256) tn_launch<256, 128>(p, bf16, a32, splits, s);
+    else tn_launch<128, 128>(p, bf16, a32, splits, s);
     PGCN_HIP(hipGetLastError());
   }
   const int64_t mn = (int64_t)g.M * g.N;

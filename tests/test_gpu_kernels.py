@@ -99,7 +99,9 @@ def test_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
 
 @pytest.mark.parametrize("gname", ["plain", "hub", "chunked"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
-@pytest.mark.parametrize("f_in,f_out", [(3, 1), (47, 41), (128, 100), (256, 256), (300, 512), (602, 256), (1100, 16)])
+# (500, 130), (512, 300) and (1000, 200) run the fp32 weight gradient in 256-row tiles (ragged and whole)
+@pytest.mark.parametrize("f_in,f_out", [(3, 1), (47, 41), (128, 100), (256, 256), (300, 512), (500, 130), (512, 300),
+                                        (602, 256), (1000, 200), (1100, 16)])
 @pytest.mark.parametrize("input_grad", [True, False])
 def test_layer_backward(graphs, gname, dt, f_in, f_out, input_grad):
     g = graphs[gname]
