@@ -41,11 +41,13 @@ def log(msg):
 
 
 def algorithmic_work(tr, w, model="gcn"):
-    """Per-step algorithmic bytes / flops of each kernel kind (see DESIGN.md).
+    """Per-step algorithmic bytes / flops of each kernel kind.
 
     Aggregation, compulsory model: every index once, every input feature row
     once, every output row once.  Gather model: every non-zero gathers one
-    full input row.  GEMMs: 2*M*N*K flops.
+    full input row.  GEMMs: 2*M*N*K flops of the products the layer forms
+    (a transform-first GraphSAGE layer adds its self term X_in W_bot over the
+    inner rows to P (X W_top) over inner and boundary rows).
     """
     from paper_2203_10428_amd import binding as B
     i = tr.info
@@ -67,10 +69,11 @@ def algorithmic_work(tr, w, model="gcn"):
             out["agg_fwd_gather"] += idx + e * f4(fo) * 4 + n * f4(fo) * 4
             out["agg_bwd"] += idx_t + n * f4(fo) * 4 + (n + b) * f4(fo) * 4
             out["agg_bwd_gather"] += idx_t + e * f4(fo) * 4 + (n + b) * f4(fo) * 4
-            out["gemm_fwd"] += 2.0 * (n + b) * f * fo
-            out["gemm_wgrad"] += 2.0 * (n + b) * f * fo
+            self_term = 2.0 * n * f * fo if model == "sage" else 0.0
+            out["gemm_fwd"] += 2.0 * (n + b) * f * fo + self_term
+            out["gemm_wgrad"] += 2.0 * (n + b) * f * fo + self_term
             if l > 1:
-                out["gemm_dgrad"] += 2.0 * (n + b) * f * fo
+                out["gemm_dgrad"] += 2.0 * (n + b) * f * fo + self_term
             continue
         out["agg_fwd"] += idx + (n + b) * f * 4 + n * f4(f) * (6 if bf16 else 4)
         out["agg_fwd_gather"] += idx + e * f4(f) * 4 + n * f4(f) * (6 if bf16 else 4)
@@ -182,8 +185,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one partition on one GPU; runs on more than one GPU are not part of this "
-              "build (the multi-GPU exchange is a design, see DESIGN.md).", file=sys.stderr)
+        print("bench.py measures one partition on one GPU: runs on more than one GPU are not supported "
+              "(the multi-partition exchange over xGMI is a design only).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
