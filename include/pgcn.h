@@ -111,6 +111,11 @@ typedef struct {
 
 typedef struct pgcn_partition pgcn_partition;
 
+/* Largest layer width (f_in, f_out) the layer entry points accept: the
+ * aggregation covers a row in at most 32 launches of up to 512 float4
+ * columns.  Wider layers are rejected with PGCN_EINVAL before any launch. */
+#define PGCN_MAX_WIDTH 63740
+
 /* Sizes of a built partition. */
 typedef struct {
   int64_t n_inner;         /* |V_i|                                           */
@@ -205,7 +210,7 @@ size_t pgcn_layer_workspace_size(const pgcn_partition *part, int32_t f_in, int32
  * (the input features are constant); H_in / H_bd are then not read.
  */
 typedef struct {
-  int32_t f_in, f_out;
+  int32_t f_in, f_out;         /* 1 .. PGCN_MAX_WIDTH                            */
   int32_t gemm_dtype;          /* pgcn_dtype                                    */
   int32_t relu;                /* 1: H_out = relu(Z); 0: H_out = Z (last layer)  */
   int64_t ld_in;               /* stride of H_in, H_bd, A, A_bf16 (elements)     */

@@ -24,6 +24,7 @@ PGCN_OK, PGCN_EINVAL, PGCN_ENOMEM, PGCN_EHIP, PGCN_EUNSUPPORTED, PGCN_EWORKSPACE
 PGCN_F32, PGCN_BF16 = 0, 1
 PGCN_SETUP_HOST_ONLY, PGCN_SETUP_NO_SELF_LOOP, PGCN_SETUP_SYMMETRIC = 1, 2, 4
 PGCN_PACK_FEAT, PGCN_ACCUM_GRAD = 0, 1
+PGCN_MAX_WIDTH = 63740
 PGCN_SOFTMAX_CE, PGCN_SIGMOID_BCE = 0, 1
 PGCN_REFILL_DMA, PGCN_REFILL_FROM_HOST = 1, 2
 PGCN_ORDER_AGG, PGCN_ORDER_TRANSFORM = 0, 1

@@ -306,6 +306,7 @@ struct ColLaunch {
   int off, cnt, S, SL;
 };
 constexpr int kMaxAggF4 = 31 * 512 + 63;                 // 32 launches at most
+static_assert(4 * kMaxAggF4 == PGCN_MAX_WIDTH, "the entry points' width limit is the aggregation's");
 
 static int slice_width() {
   const char *env = std::getenv("PGCN_AGG_SLICE_F4");    // tuning override: 16, 32 or 64

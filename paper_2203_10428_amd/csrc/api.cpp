@@ -267,6 +267,7 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   PGCN_REQUIRE(p->self_loop, "pgcn_layer_fwd: the GCN layer needs a partition built with self loops");
   PGCN_REQUIRE(a, "pgcn_layer_fwd: null args");
   PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_layer_fwd: widths must be >= 1");
+  PGCN_REQUIRE(a->f_in <= PGCN_MAX_WIDTH && a->f_out <= PGCN_MAX_WIDTH, "pgcn_layer_fwd: widths above PGCN_MAX_WIDTH");
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_layer_fwd: bad gemm_dtype");
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_layer_fwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0, "pgcn_layer_fwd: ld_out must be >= f_out and a multiple of 4");
@@ -380,6 +381,7 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   PGCN_REQUIRE(p->self_loop, "pgcn_layer_bwd: the GCN layer needs a partition built with self loops");
   PGCN_REQUIRE(a, "pgcn_layer_bwd: null args");
   PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_layer_bwd: widths must be >= 1");
+  PGCN_REQUIRE(a->f_in <= PGCN_MAX_WIDTH && a->f_out <= PGCN_MAX_WIDTH, "pgcn_layer_bwd: widths above PGCN_MAX_WIDTH");
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_layer_bwd: bad gemm_dtype");
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_layer_bwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0, "pgcn_layer_bwd: ld_out must be >= f_out and a multiple of 4");
@@ -710,6 +712,7 @@ extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_
   PGCN_REQUIRE(!p->self_loop, "pgcn_sage_layer_fwd: the partition must be built with PGCN_SETUP_NO_SELF_LOOP");
   PGCN_REQUIRE(a, "pgcn_sage_layer_fwd: null args");
   PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_sage_layer_fwd: widths must be >= 1");
+  PGCN_REQUIRE(a->f_in <= PGCN_MAX_WIDTH && a->f_out <= PGCN_MAX_WIDTH, "pgcn_sage_layer_fwd: widths above PGCN_MAX_WIDTH");
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_sage_layer_fwd: bad gemm_dtype");
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_sage_layer_fwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0,
@@ -786,6 +789,7 @@ extern "C" int pgcn_sage_layer_bwd(const pgcn_partition *p, const pgcn_sage_bwd_
   PGCN_REQUIRE(!p->self_loop, "pgcn_sage_layer_bwd: the partition must be built with PGCN_SETUP_NO_SELF_LOOP");
   PGCN_REQUIRE(a, "pgcn_sage_layer_bwd: null args");
   PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_sage_layer_bwd: widths must be >= 1");
+  PGCN_REQUIRE(a->f_in <= PGCN_MAX_WIDTH && a->f_out <= PGCN_MAX_WIDTH, "pgcn_sage_layer_bwd: widths above PGCN_MAX_WIDTH");
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_sage_layer_bwd: bad gemm_dtype");
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_sage_layer_bwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0,

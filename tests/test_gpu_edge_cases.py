@@ -7,7 +7,10 @@ normalisation, GraphSAGE in both associations), against the oracle:
   outgoing rows;
 * an empty partition (owns no node): every call succeeds, dW = 0;
 * a partition whose inner nodes have no edges (P = I with self loops, zero
-  rows of the GraphSAGE mean).
+  rows of the GraphSAGE mean);
+* the widest layers the entry points accept (PGCN_MAX_WIDTH columns in or
+  out: 32 aggregation launches per row), and one column more, which every
+  layer entry point rejects before launching anything.
 """
 import numpy as np
 import pytest
@@ -27,6 +30,9 @@ ORDER = {"agg": B.PGCN_ORDER_AGG, "transform": B.PGCN_ORDER_TRANSFORM}
 
 
 def graph(kind):
+    if kind == "small":
+        n, rowptr, col, owner = random_partition_graph(300, 150, 3, 8, 7)
+        return n, rowptr, col, owner, 3
     if kind == "one_partition":
         n, rowptr, col, _ = random_partition_graph(900, 300, 2, 10, 4)
         return n, rowptr, col, np.zeros(n, np.int32), 1
@@ -71,15 +77,18 @@ def run_layer(kind, model, norm, order, dt, f_in=37, f_out=21):
         A_ref, Z, H_ref = layers.layer_forward(P, X, W.astype(np.float64), True, gm, order=order)
     dG = torch.full((k * f_in, f_out), 3.0, device="cuda")
     J_in, J_bd = dev(np.zeros((n, f_in))), (dev(np.zeros((b, f_in))) if b else None)
+    # the ReLU mask is a decision taken by floating point: the oracle's backward takes the kernel's
+    # (H > 0 from the GPU forward), since with millions of outputs some Z lie within rounding of zero
+    Zm = np.where(host(H, f_out) > 0, np.abs(Z) + 1.0, -1.0)
     if sage:
         B.pgcn_sage_layer_bwd(part, J_out=dev(J), H_out=H, A=A, A_bf16=A16, X_in=dX, X_in_bf16=dX16,
                               X_bd=dXbd if b else None, dW=dG, J_in=J_in, J_bd_out=J_bd, **common)
-        G_ref, Jf_ref = layers.sage_backward(P, z_ref, X[:n], Z, J, W.astype(np.float64), True, True, gm,
+        G_ref, Jf_ref = layers.sage_backward(P, z_ref, X[:n], Zm, J, W.astype(np.float64), True, True, gm,
                                              order=order, X_full=X)
     else:
         B.pgcn_layer_bwd(part, J_out=dev(J), H_out=H, A=A, A_bf16=A16, dW=dG, J_in=J_in, J_bd_out=J_bd,
                          H_in=dX, H_bd=dXbd if b else None, **common)
-        G_ref, Jf_ref = layers.layer_backward(P, A_ref, Z, J, W.astype(np.float64), True, True, gm, order=order,
+        G_ref, Jf_ref = layers.layer_backward(P, A_ref, Zm, J, W.astype(np.float64), True, True, gm, order=order,
                                               H_full=X)
     torch.cuda.synchronize()
     return dict(n=n, b=b, H=host(H, f_out), H_ref=H_ref, G=dG.cpu().numpy(), G_ref=G_ref,
@@ -105,3 +114,48 @@ def test_empty_partition(model, norm, order):
     r = run_layer("empty", model, norm, order, "f32")
     assert r["n"] == 0 and r["b"] == 0
     assert np.all(r["G"] == 0)
+
+
+@pytest.mark.parametrize("model,norm,order", [("gcn", "mean", "agg"), ("gcn", "mean", "transform"),
+                                              ("sage", "mean", "agg"), ("sage", "mean", "transform")])
+@pytest.mark.parametrize("f_in,f_out", [(B.PGCN_MAX_WIDTH, 8), (8, B.PGCN_MAX_WIDTH)])
+def test_maximum_width(model, norm, order, f_in, f_out):
+    r = run_layer("small", model, norm, order, "f32", f_in=f_in, f_out=f_out)
+    tol = TOL["f32"]
+    assert rel_err(r["H"], r["H_ref"]) < tol["act"]
+    assert rel_err(r["G"], r["G_ref"]) < tol["grad"]
+    assert rel_err(r["J_in"], r["Jf_ref"][: r["n"]]) < tol["grad"]
+    assert rel_err(r["J_bd"], r["Jf_ref"][r["n"]:]) < tol["grad"]
+
+
+@pytest.mark.parametrize("entry", ["fwd", "bwd", "sage_fwd", "sage_bwd"])
+@pytest.mark.parametrize("wide", ["in", "out"])
+def test_width_above_maximum_is_rejected(entry, wide):
+    n_g, rowptr, col, owner, nparts = graph("small")
+    sage = entry.startswith("sage")
+    part = B.pgcn_partition_setup(n_g, rowptr, col, owner, nparts, 0, self_loop=not sage)
+    info = B.pgcn_partition_info(part)
+    n, b = info["n_inner"], info["n_bd"]
+    f_in, f_out = (B.PGCN_MAX_WIDTH + 1, 8) if wide == "in" else (8, B.PGCN_MAX_WIDTH + 1)
+    li, lo = ld_of(f_in), ld_of(f_out)
+    k = 2 if sage else 1
+    # buffers of the full sizes the call would use, so nothing could go out of bounds
+    z = lambda r, c: torch.zeros((max(r, 1), c), device="cuda")
+    nb = max(B.pgcn_workspace_size(part, f_in, f_out, B.PGCN_F32), 256)
+    common = dict(f_in=f_in, f_out=f_out, gemm_dtype=B.PGCN_F32, relu=True, ld_in=li, ld_out=lo,
+                  W=z(k * f_in, f_out), workspace=torch.zeros(nb, dtype=torch.uint8, device="cuda"), workspace_bytes=nb)
+    with pytest.raises(B.PgcnError) as e:
+        if entry == "fwd":
+            B.pgcn_layer_fwd(part, H_in=z(n, li), H_bd=z(b, li), A=z(n, li), A_bf16=None, H_out=z(n, lo), **common)
+        elif entry == "bwd":
+            B.pgcn_layer_bwd(part, J_out=z(n, lo), H_out=z(n, lo), A=z(n, li), A_bf16=None, dW=z(f_in, f_out),
+                             J_in=z(n, li), J_bd_out=z(b, li), **common)
+        elif entry == "sage_fwd":
+            B.pgcn_sage_layer_fwd(part, X_in=z(n, li), X_in_bf16=None, X_bd=z(b, li), A=z(n, li), A_bf16=None,
+                                  H_out=z(n, lo), **common)
+        else:
+            B.pgcn_sage_layer_bwd(part, J_out=z(n, lo), H_out=z(n, lo), A=z(n, li), A_bf16=None, X_in=z(n, li),
+                                  X_in_bf16=None, X_bd=z(b, li), dW=z(2 * f_in, f_out), J_in=z(n, li),
+                                  J_bd_out=z(b, li), **common)
+    assert e.value.code == B.PGCN_EINVAL
+    assert "PGCN_MAX_WIDTH" in str(e.value)
