@@ -111,6 +111,19 @@ typedef struct {
 
 typedef struct pgcn_partition pgcn_partition;
 
+/* Tuning overrides (environment variables; none is needed for correct use):
+ *   PGCN_AGG_CHUNKS    column chunks of the aggregation plans, 1..64 (read by
+ *                      pgcn_partition_setup; default: about 11,000 gathered rows
+ *                      per chunk while rows keep >= 32 non-zeros per chunk);
+ *   PGCN_SEGMENT       length at which long rows are split into segments,
+ *                      16..1048576 (read by pgcn_partition_setup; default 512);
+ *   PGCN_AGG_SLICE_F4  float4 columns per aggregation lane slice: 16, 32 or 64
+ *                      (read per call; default 64);
+ *   PGCN_TN_BM=128     keeps the fp32 weight-gradient GEMM in 128-row tiles
+ *                      (read once; default: 256-row tiles for f_in >= 384).
+ * Chunks and segments set the order in which a row's terms are added (results
+ * stay deterministic for a given setting); the other two change only speed. */
+
 /* Largest layer width (f_in, f_out) the layer entry points accept: the
  * aggregation covers a row in at most 32 launches of up to 512 float4
  * columns.  Wider layers are rejected with PGCN_EINVAL before any launch. */
