@@ -41,7 +41,9 @@ def graphs():
     return {"plain": Graph(), "hub": Graph(n_inner=2500, n_pool=900, seed=1, hub_deg=3000),
             # cache-blocked plan: 3 column chunks, runs split every 16 non-zeros (partials in every chunk)
             "chunked": Graph(n_inner=2000, n_pool=1200, seed=2, mean_deg=60, hub_deg=2000,
-                             env={"PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "16"})}
+                             env={"PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "16"}),
+            # 5,000 inner rows: 40 row tiles of the node-major GEMMs, the last one ragged
+            "tall": Graph(n_inner=5000, n_pool=1500, seed=3, mean_deg=10)}
 
 
 def ws_for(g, f_in, f_out, dt):
@@ -58,7 +60,7 @@ def test_partition_device_build_matches_oracle(graphs):
     assert graphs["chunked"].info["spmm_chunks"] == 3 and graphs["chunked"].info["spmmt_chunks"] == 3
 
 
-@pytest.mark.parametrize("gname", ["plain", "hub", "chunked"])
+@pytest.mark.parametrize("gname", ["plain", "hub", "chunked", "tall"])
 @pytest.mark.parametrize("dt", ["f32", "bf16", "bf16-noA"])
 @pytest.mark.parametrize("f_in,f_out", [(1, 3), (41, 47), (100, 128), (128, 64), (300, 512), (602, 256), (1100, 16),
                                         (2100, 8)])
@@ -97,7 +99,7 @@ def test_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
     assert rel_err(host(H, f_out), H_ref) < tol
 
 
-@pytest.mark.parametrize("gname", ["plain", "hub", "chunked"])
+@pytest.mark.parametrize("gname", ["plain", "hub", "chunked", "tall"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 # (500, 130), (512, 300) and (1000, 200) run the fp32 weight gradient in 256-row tiles (ragged and whole)
 @pytest.mark.parametrize("f_in,f_out", [(3, 1), (47, 41), (128, 100), (256, 256), (300, 512), (500, 130), (512, 300),
@@ -135,7 +137,7 @@ def test_layer_backward(graphs, gname, dt, f_in, f_out, input_grad):
         assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
 
 
-@pytest.mark.parametrize("gname", ["hub", "chunked"])
+@pytest.mark.parametrize("gname", ["hub", "chunked", "tall"])
 def test_backward_is_deterministic(graphs, gname):
     g = graphs[gname]
     rng = np.random.default_rng(3)

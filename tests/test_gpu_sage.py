@@ -42,7 +42,9 @@ def graphs():
     # mean_deg 3 leaves inner rows without neighbours (zero rows of the mean)
     return {"plain": SageGraph(), "sparse": SageGraph(n_inner=2000, n_pool=800, seed=3, mean_deg=1.5),
             "chunked": SageGraph(n_inner=2000, n_pool=1200, seed=2, mean_deg=60, hub_deg=2000,
-                                 env={"PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "16"})}
+                                 env={"PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "16"}),
+            # 5,000 inner rows: 40 row tiles of the node-major GEMMs, the last one ragged
+            "tall": SageGraph(n_inner=5000, n_pool=1500, seed=4, mean_deg=8)}
 
 
 def ws_for(g, f_in, f_out, dt):
@@ -109,7 +111,7 @@ def test_adam_update(t, peer):
     assert abs(step_gpu - step_ref) < 1e-3 * step_ref           # the update is applied
 
 
-@pytest.mark.parametrize("gname", ["plain", "sparse", "chunked"])
+@pytest.mark.parametrize("gname", ["plain", "sparse", "chunked", "tall"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("f_in,f_out", [(3, 5), (41, 47), (100, 128), (300, 512), (602, 256)])
 @pytest.mark.parametrize("with_bd", [True, False])
@@ -142,7 +144,7 @@ def test_sage_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
     assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"]
 
 
-@pytest.mark.parametrize("gname", ["plain", "sparse", "chunked"])
+@pytest.mark.parametrize("gname", ["plain", "sparse", "chunked", "tall"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("f_in,f_out", [(5, 3), (47, 41), (128, 100), (256, 256), (602, 256)])
 @pytest.mark.parametrize("input_grad", [True, False])
@@ -184,7 +186,7 @@ def test_sage_layer_backward(graphs, gname, dt, f_in, f_out, input_grad):
         assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
 
 
-@pytest.mark.parametrize("gname", ["plain", "sparse", "chunked"])
+@pytest.mark.parametrize("gname", ["plain", "sparse", "chunked", "tall"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("f_in,f_out", [(5, 3), (47, 41), (602, 256), (128, 100), (100, 128)])
 @pytest.mark.parametrize("with_bd", [True, False])

@@ -27,7 +27,9 @@ TF = B.PGCN_ORDER_TRANSFORM
 def graphs():
     return {"plain": Graph(), "hub": Graph(n_inner=2500, n_pool=900, seed=1, hub_deg=3000),
             "chunked": Graph(n_inner=2000, n_pool=1200, seed=2, mean_deg=60, hub_deg=2000,
-                             env={"PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "16"})}
+                             env={"PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "16"}),
+            # 5,000 inner and several thousand boundary rows: many row tiles in both GEMM halves
+            "tall": Graph(n_inner=5000, n_pool=6000, nparts=2, seed=3, mean_deg=10)}
 
 
 def ws_tf(g, f_in, f_out, dt):
@@ -36,7 +38,7 @@ def ws_tf(g, f_in, f_out, dt):
     return torch.empty(nbytes, dtype=torch.uint8, device="cuda"), nbytes
 
 
-@pytest.mark.parametrize("gname", ["plain", "hub", "chunked"])
+@pytest.mark.parametrize("gname", ["plain", "hub", "chunked", "tall"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("f_in,f_out", [(3, 1), (47, 41), (128, 47), (602, 256), (256, 41), (512, 100), (1100, 16),
                                         (100, 128)])
@@ -63,7 +65,7 @@ def test_transform_forward(graphs, gname, dt, f_in, f_out, with_bd):
     assert np.all(pad == 0)
 
 
-@pytest.mark.parametrize("gname", ["plain", "hub", "chunked"])
+@pytest.mark.parametrize("gname", ["plain", "hub", "chunked", "tall"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("f_in,f_out", [(3, 1), (47, 41), (602, 256), (256, 41), (512, 100), (1100, 16), (100, 128)])
 @pytest.mark.parametrize("input_grad", [True, False])
