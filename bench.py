@@ -157,6 +157,8 @@ def main():
                     help="GCN layer association: (P H) W, P (H W), or P (H W) where the layer narrows")
     ap.add_argument("--norm", default="mean", choices=["mean", "sym"],
                     help="GCN propagation matrix: mean D^-1 (A+I) or symmetric D^-1/2 (A+I) D^-1/2")
+    ap.add_argument("--no-fuse-pack", action="store_true",
+                    help="pack the sent rows in a pass of their own instead of in the kernel writing the layer output")
     ap.add_argument("--cache-layer1", action="store_true",
                     help="variant: keep layer 1's aggregate across steps (constant input features); it reuses "
                          "outputs across steps, so its line is a variant, not the step's measurement")
@@ -204,7 +206,7 @@ def main():
     sf, sg = VARIANTS[args.variant]
     so = StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="pipe",
                      refill_dma=args.refill == "dma", remote=args.remote, order=args.order, norm=args.norm,
-                     cache_layer1=args.cache_layer1)
+                     cache_layer1=args.cache_layer1, fuse_pack=not args.no_fuse_pack)
     if args.model == "sage":
         so = StepOptions(**{**so.__dict__, "model": "sage", "dropout": w.sage_dropout, "optimizer": "adam",
                             "eta": w.sage_lr})
@@ -333,7 +335,7 @@ def main():
         "config": {"workload": w.name, "variant": args.variant,
                    "layer": "graphsage-concat" if args.model == "sage" else "gcn", "remote": args.remote,
                    "optimizer": so.optimizer, "dropout": so.dropout, "copy_mode": "pipe", "refill": args.refill,
-                   "order": args.order, "norm": args.norm, "layer1_cached": args.cache_layer1,
+                   "order": args.order, "norm": args.norm, "layer1_cached": args.cache_layer1, "pack_fused": not args.no_fuse_pack,
                    "transform_first_layers": [l for l in range(1, tr.L + 1) if tr.order[l] == B.PGCN_ORDER_TRANSFORM],
                    "widths": list(w.widths),
                    "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",

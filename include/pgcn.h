@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 161
+#define PGCN_VERSION 162
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -240,6 +240,12 @@ typedef struct {
   int32_t a_given;             /* 1: A (fp32) already holds P_i [H_in ; H_bd]; only
                                   the update runs (aggregate first; on the bf16
                                   path A is rounded while staged, A_bf16 unused) */
+  float *send_out;             /* [n_send, ld_out] or NULL: also writes the rows of
+                                  H_out that this partition sends (Algorithm 1's
+                                  forward send of the next layer's input), row k =
+                                  H_out[send_idx[k]], columns [0, f_out); the kernel
+                                  that writes H_out writes them (no second pass over
+                                  H_out). 16-byte aligned. */
 } pgcn_fwd_args;
 int pgcn_layer_fwd(const pgcn_partition *part, const pgcn_fwd_args *args, hipStream_t stream);
 
@@ -403,6 +409,8 @@ typedef struct {
   void *workspace;
   size_t workspace_bytes;
   int32_t order;               /* pgcn_layer_order (0: aggregate first)           */
+  float *send_out;             /* [n_send, ld_out] or NULL: the sent rows of H_out,
+                                  as in pgcn_fwd_args                            */
 } pgcn_sage_fwd_args;
 int pgcn_sage_layer_fwd(const pgcn_partition *part, const pgcn_sage_fwd_args *args, hipStream_t stream);
 

@@ -58,7 +58,7 @@ class pgcn_fwd_args(C.Structure):
     _fields_ = [("f_in", _i32), ("f_out", _i32), ("gemm_dtype", _i32), ("relu", _i32),
                 ("ld_in", _i64), ("ld_out", _i64), ("H_in", _vp), ("H_bd", _vp), ("W", _vp),
                 ("A", _vp), ("A_bf16", _vp), ("H_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz),
-                ("order", _i32), ("a_given", _i32)]
+                ("order", _i32), ("a_given", _i32), ("send_out", _vp)]
 
 
 class pgcn_bwd_args(C.Structure):
@@ -72,7 +72,7 @@ class pgcn_sage_fwd_args(C.Structure):
     _fields_ = [("f_in", _i32), ("f_out", _i32), ("gemm_dtype", _i32), ("relu", _i32),
                 ("ld_in", _i64), ("ld_out", _i64), ("X_in", _vp), ("X_in_bf16", _vp), ("X_bd", _vp), ("W", _vp),
                 ("A", _vp), ("A_bf16", _vp), ("H_out", _vp), ("workspace", _vp), ("workspace_bytes", _sz),
-                ("order", _i32)]
+                ("order", _i32), ("send_out", _vp)]
 
 
 class pgcn_sage_bwd_args(C.Structure):
@@ -222,9 +222,11 @@ def pgcn_layer_workspace_size(part: Partition, f_in: int, f_out: int, gemm_dtype
 
 
 def pgcn_layer_fwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, H_in, H_bd, W, A, A_bf16,
-                   H_out, workspace, workspace_bytes, order=PGCN_ORDER_AGG, a_given=False, stream=None):
+                   H_out, workspace, workspace_bytes, order=PGCN_ORDER_AGG, a_given=False, send_out=None,
+                   stream=None):
     a = pgcn_fwd_args(f_in, f_out, gemm_dtype, int(relu), ld_in, ld_out, _ptr(H_in), _ptr(H_bd), _ptr(W),
-                      _ptr(A), _ptr(A_bf16), _ptr(H_out), _ptr(workspace), workspace_bytes, order, int(a_given))
+                      _ptr(A), _ptr(A_bf16), _ptr(H_out), _ptr(workspace), workspace_bytes, order, int(a_given),
+                      _ptr(send_out))
     _check(lib.pgcn_layer_fwd(part.handle, C.byref(a), _stream(stream)), "pgcn_layer_fwd")
 
 
@@ -271,10 +273,11 @@ def pgcn_dropout(out, inp, rows: int, cols: int, ld: int, row0: int, p: float, s
 
 
 def pgcn_sage_layer_fwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, X_in, X_in_bf16, X_bd, W,
-                        A, A_bf16, H_out, workspace, workspace_bytes, order=PGCN_ORDER_AGG, stream=None):
+                        A, A_bf16, H_out, workspace, workspace_bytes, order=PGCN_ORDER_AGG, send_out=None,
+                        stream=None):
     a = pgcn_sage_fwd_args(f_in, f_out, gemm_dtype, int(relu), ld_in, ld_out, _ptr(X_in), _ptr(X_in_bf16),
                            _ptr(X_bd), _ptr(W), _ptr(A), _ptr(A_bf16), _ptr(H_out), _ptr(workspace),
-                           workspace_bytes, order)
+                           workspace_bytes, order, _ptr(send_out))
     _check(lib.pgcn_sage_layer_fwd(part.handle, C.byref(a), _stream(stream)), "pgcn_sage_layer_fwd")
 
 

@@ -67,6 +67,9 @@ struct AggParams {
   int32_t relu;           // final rows are max(x, 0)
   int64_t ld_in, ld_out, ld_bf16, ld_part;
   float *partials;
+  float *send;            // or null: final rows [0, out_split) also to their send rows (stride ld_out)
+  const int64_t *send_ptr;
+  const int32_t *send_pos;
 };
 
 enum { AGG_FIRST = 1, AGG_LAST = 2 };
@@ -112,6 +115,17 @@ __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, fl
     q.w = q.w > 0.f ? q.w : 0.f;
   }
   if (o) *reinterpret_cast<float4 *>(o + c) = q;
+  if (p.send && r < p.out_split) {                     // four send slots per round, positions loaded together
+    const int64_t kb = p.send_ptr[r], ke = p.send_ptr[r + 1];
+    for (int64_t k = kb; k < ke; k += 4) {
+      int32_t pos[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pos[e] = k + e < ke ? p.send_pos[k + e] : -1;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (pos[e] >= 0) *reinterpret_cast<float4 *>(p.send + (int64_t)pos[e] * p.ld_out + c) = q;
+    }
+  }
   if (p.out_bf16 && r < p.out_split) {
     uint2 w;
     w.x = (uint32_t)f32_to_bf16_rne(q.x) | ((uint32_t)f32_to_bf16_rne(q.y) << 16);
@@ -368,6 +382,11 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
   p.partials = a.partials;
   p.accum_lo = a.accum_lo;
   p.relu = a.relu;
+  p.send = a.send;
+  p.send_ptr = a.send_ptr;
+  p.send_pos = a.send_pos;
+  if (a.send && (!a.send_ptr || !a.send_pos || (reinterpret_cast<uintptr_t>(a.send) & 15) || a.ld_out % 4))
+    return set_error(PGCN_EINVAL, "aggregation: send rows need the send map, 16-byte alignment and ld % 4 == 0");
   const int f4 = (a.f + 3) / 4;
   const int C = plan.chunks;
   if (f4 > kMaxAggF4) return set_error(PGCN_EINVAL, "aggregation: feature widths above 63,740 are not supported");

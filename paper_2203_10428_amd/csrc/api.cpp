@@ -121,6 +121,16 @@ namespace {
 
 // Y = [H_in ; H_bd] W, then H_out = act(P_i Y): the layer function of
 // Appendix A.1 in the association P (H W).
+// Rows of the layer output that this partition sends, written by the kernel
+// that produces them (send_idx order, via the inverse send map).
+template <class Args>
+void set_send(Args &x, const pgcn_partition *p, float *send_out) {
+  if (!send_out || p->n_send == 0) return;
+  x.send = send_out;
+  x.send_ptr = p->d_inv_ptr;
+  x.send_pos = p->d_inv_k;
+}
+
 int layer_fwd_transform(const pgcn_partition *p, const pgcn_fwd_args *a, hipStream_t s) {
   if (p->n_inner > 0) {
     PGCN_REQUIRE(a->H_in && a->W && a->H_out, "pgcn_layer_fwd: null H_in, W or H_out");
@@ -166,6 +176,7 @@ int layer_fwd_transform(const pgcn_partition *p, const pgcn_fwd_args *a, hipStre
   g.partials = (float *)((char *)a->workspace + fwd_tf_agg_off(p, a->f_out));
   g.relu = a->relu ? 1 : 0;
   g.trace_kind = PGCN_TK_AGG_FWD;
+  set_send(g, p, a->send_out);
   return launch_aggregate(g, s);
 }
 
@@ -268,6 +279,7 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   PGCN_REQUIRE(a, "pgcn_layer_fwd: null args");
   PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_layer_fwd: widths must be >= 1");
   PGCN_REQUIRE(a->f_in <= PGCN_MAX_WIDTH && a->f_out <= PGCN_MAX_WIDTH, "pgcn_layer_fwd: widths above PGCN_MAX_WIDTH");
+  PGCN_REQUIRE(aligned16(a->send_out), "pgcn_layer_fwd: send_out must be 16-byte aligned");
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_layer_fwd: bad gemm_dtype");
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_layer_fwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0, "pgcn_layer_fwd: ld_out must be >= f_out and a multiple of 4");
@@ -298,6 +310,7 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
     m.ldc = a->ld_out;
     m.workspace = (float *)a->workspace;
     m.workspace_bytes = gneed;
+    set_send(m, p, a->send_out);
     return launch_gemm_nk(a->relu ? Gemm::NN_SRC32_RELU : Gemm::NN_SRC32_PLAIN, m, s);
   }
   if (p->n_inner > 0) {
@@ -370,6 +383,7 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   m.ldc = a->ld_out;
   m.workspace = (float *)((char *)a->workspace + fwd_agg_bytes(p, a->f_in, a->gemm_dtype));
   m.workspace_bytes = gemm_nk_workspace(a->f_out, a->f_in, a->gemm_dtype);
+  set_send(m, p, a->send_out);
   if (bf16 && !a->A_bf16)           // bf16 path without the bf16 copy: A rounded while staged (same values)
     return launch_gemm_nk(a->relu ? Gemm::NN_SRC32_RELU : Gemm::NN_SRC32_PLAIN, m, s);
   return launch_gemm_nk(a->relu ? Gemm::NN_RELU : Gemm::NN_PLAIN, m, s);
@@ -553,6 +567,7 @@ int sage_fwd_transform(const pgcn_partition *p, const pgcn_sage_fwd_args *a, hip
   b.ldc = a->ld_out;
   b.workspace = m.workspace;
   b.workspace_bytes = m.workspace_bytes;
+  set_send(b, p, a->send_out);
   return launch_gemm_nk(a->relu ? Gemm::NN_ACC_RELU : Gemm::NN_ACC_PLAIN, b, s);
 }
 
@@ -713,6 +728,7 @@ extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_
   PGCN_REQUIRE(a, "pgcn_sage_layer_fwd: null args");
   PGCN_REQUIRE(a->f_in >= 1 && a->f_out >= 1, "pgcn_sage_layer_fwd: widths must be >= 1");
   PGCN_REQUIRE(a->f_in <= PGCN_MAX_WIDTH && a->f_out <= PGCN_MAX_WIDTH, "pgcn_sage_layer_fwd: widths above PGCN_MAX_WIDTH");
+  PGCN_REQUIRE(aligned16(a->send_out), "pgcn_sage_layer_fwd: send_out must be 16-byte aligned");
   PGCN_REQUIRE(a->gemm_dtype == PGCN_F32 || a->gemm_dtype == PGCN_BF16, "pgcn_sage_layer_fwd: bad gemm_dtype");
   PGCN_REQUIRE(a->ld_in >= a->f_in && a->ld_in % 4 == 0, "pgcn_sage_layer_fwd: ld_in must be >= f_in and a multiple of 4");
   PGCN_REQUIRE(a->ld_out >= a->f_out && a->ld_out % 4 == 0,
@@ -780,6 +796,7 @@ extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_
   m.A = a->X_in;
   m.A16 = a->X_in_bf16;
   m.B = a->W + (size_t)a->f_in * a->f_out;
+  set_send(m, p, a->send_out);
   return launch_gemm_nk(a->relu ? Gemm::NN_ACC_RELU : Gemm::NN_ACC_PLAIN, m, s);
 }
 

@@ -55,6 +55,9 @@ struct NKParams {
   int64_t ldc;
   const float *rowscale;
   int vec;                 // C rows 16-byte aligned: ldc % 4 == 0 and C 16-byte aligned
+  float *send;             // or null: final rows of C also written to send rows (stride ldc)
+  const int64_t *send_ptr; // send rows of output row r: send_pos[send_ptr[r] .. send_ptr[r + 1])
+  const int32_t *send_pos;
 };
 
 enum NKA { NK_A_F32, NK_A_BF16, NK_A_MASK };
@@ -153,14 +156,47 @@ __device__ __forceinline__ void nk_epilogue(const NKParams &p, const f32x16 (&ac
         }
 #pragma unroll
         for (int s = 0; s < 4; ++s) *reinterpret_cast<f32x4 *>(c0 + (int64_t)(8 * s) * p.ldc) = v[s];
+        if (p.send) {                                  // the same rows to their send slots
+          int64_t kb[4], ke[4];
+#pragma unroll
+          for (int s = 0; s < 4; ++s) {
+            kb[s] = p.send_ptr[mb + rr + 8 * s];
+            ke[s] = p.send_ptr[mb + rr + 8 * s + 1];
+          }
+          // one slot of each of the four rows per round: their position loads are issued together
+          for (int i = 0;; ++i) {
+            int32_t pos[4];
+            bool any = false;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+              pos[s] = kb[s] + i < ke[s] ? p.send_pos[kb[s] + i] : -1;
+              any |= pos[s] >= 0;
+            }
+            if (!any) break;
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+              if (pos[s] >= 0) *reinterpret_cast<f32x4 *>(p.send + (int64_t)pos[s] * p.ldc + cb) = v[s];
+          }
+        }
       } else {
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
-          if (mb + rr + 8 * s >= p.M) continue;
+          const int row = mb + rr + 8 * s;
+          if (row >= p.M) continue;
           float *c = c0 + (int64_t)(8 * s) * p.ldc;
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (cb + e < p.N) c[e] = ACC ? nk_out<EK>(v[s][e], 0.f, c[e]) : v[s][e];
+            if (cb + e < p.N) {
+              v[s][e] = ACC ? nk_out<EK>(v[s][e], 0.f, c[e]) : v[s][e];
+              c[e] = v[s][e];
+            }
+          if (p.send)
+            for (int64_t k = p.send_ptr[row]; k < p.send_ptr[row + 1]; ++k) {
+              float *d = p.send + (int64_t)p.send_pos[k] * p.ldc + cb;
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (cb + e < p.N) d[e] = v[s][e];
+            }
         }
       }
     }
@@ -466,6 +502,13 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
   p.ldc = g.ldc;
   p.rowscale = g.rowscale;
   p.vec = (g.ldc % 4 == 0 && (reinterpret_cast<uintptr_t>(g.C) & 15) == 0) ? 1 : 0;
+  if (g.send) {
+    if (!fwd || !g.send_ptr || !g.send_pos || ((reinterpret_cast<uintptr_t>(g.send) & 15) && p.vec))
+      return set_error(PGCN_EINVAL, "update GEMM: send rows need a forward kind, the send map and 16-byte alignment");
+    p.send = g.send;
+    p.send_ptr = g.send_ptr;
+    p.send_pos = g.send_pos;
+  }
   TraceScope ts(fwd ? PGCN_TK_GEMM_FWD : PGCN_TK_GEMM_DGRAD, s);
   switch (kind) {
     case Gemm::NN_RELU: nk_launch_bn<NK_A_F32, NK_E_RELU>(p, bf16, s); break;

@@ -125,6 +125,11 @@ struct AggArgs {
   int32_t trace_kind;      // PGCN_TK_AGG_FWD or PGCN_TK_AGG_BWD
   int32_t accum_lo;        // 1: rows [0, out_split) add to what out_lo holds (GraphSAGE self term)
   int32_t relu;            // 1: the final rows are max(x, 0) (transform-first forward)
+  // optional: the final rows [0, out_split) also go to the send rows that carry them:
+  // send[k] for k in send_pos[send_ptr[r] .. send_ptr[r + 1]) (stride ld_out)
+  float *send;
+  const int64_t *send_ptr;
+  const int32_t *send_pos;
 };
 int launch_aggregate(const AggArgs &a, hipStream_t s);
 size_t aggregate_workspace(const Plan &plan, int64_t f);
@@ -161,6 +166,11 @@ struct GemmArgs {
   // while staged instead of reading A16
   const float *A_hi;
   int64_t k_split;
+  // NN_* (launch_gemm_nk): the final rows of C also go to the send rows that carry them,
+  // send[k] for k in send_pos[send_ptr[r] .. send_ptr[r + 1]) (stride ldc); null: not written
+  float *send;
+  const int64_t *send_ptr;
+  const int32_t *send_pos;
 };
 int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s);
 size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K);

@@ -65,6 +65,7 @@ class StepOptions:
     relu_last: bool = False
     copy_mode: str = "pipe"          # "pipe" | "serial" | "none"
     refill_dma: bool = False         # refills by the DMA engines instead of a blit kernel
+    fuse_pack: bool = True           # a layer's output kernel also writes the next layer's send rows
     remote: str = "device"           # emulated peers' data in "device" memory or pinned "host" memory
     model: str = "gcn"               # "gcn" | "sage"
     dropout: float = 0.0
@@ -219,9 +220,11 @@ class PartitionTrainer:
         common = dict(f_in=f, f_out=wd[1], gemm_dtype=self.dtype, relu=self._relu(1), ld_in=ld_of(f),
                       ld_out=ld_of(wd[1]), W=self.W[0], A_bf16=None, workspace=self.ws,
                       workspace_bytes=self.ws_bytes, stream=st)
+        send = self._send_out(1)
         if not self.A1_ready:
             if not self.A1_started:        # the running aggregate starts at P [X_in; 0]
-                B.pgcn_layer_fwd(self.part, H_in=self.X, H_bd=None, A=self.A[1], H_out=self.H[1], **common)
+                B.pgcn_layer_fwd(self.part, H_in=self.X, H_bd=None, A=self.A[1], H_out=self.H[1], send_out=send,
+                                 **common)
                 self.A1_started = True
                 if H_bd is None:
                     self.A1_used = self.A[1]
@@ -233,8 +236,14 @@ class PartitionTrainer:
             A1 = self.A[1]
         else:
             A1 = self.A1_full
-        B.pgcn_layer_fwd(self.part, H_in=None, H_bd=None, A=A1, H_out=self.H[1], a_given=True, **common)
+        B.pgcn_layer_fwd(self.part, H_in=None, H_bd=None, A=A1, H_out=self.H[1], a_given=True, send_out=send,
+                         **common)
         self.A1_used = A1
+
+    def _send_out(self, l):
+        """Send rows of layer l's output (the next layer's input), written by the layer's own output
+        kernel when packs are fused; None for the last layer or without fusion."""
+        return self.send_f[l + 1] if self.opts.fuse_pack and l < self.L else None
 
     def _forward_layer(self, l, H_in, H_bd, st):
         """Dropout of the layer input (after the receive), then the GCN or GraphSAGE layer."""
@@ -250,10 +259,12 @@ class PartitionTrainer:
         common = dict(f_in=f, f_out=wd[l], gemm_dtype=self.dtype, relu=self._relu(l), ld_in=ld_of(f),
                       ld_out=ld_of(wd[l]), W=self.W[l - 1], A=self.A[l], A_bf16=self.A16[l], H_out=self.H[l],
                       workspace=self.ws, workspace_bytes=self.ws_bytes, stream=st)
+        send = self._send_out(l)
         if self.sage:
-            B.pgcn_sage_layer_fwd(self.part, X_in=X_in, X_in_bf16=X16, X_bd=X_bd, order=self.order[l], **common)
+            B.pgcn_sage_layer_fwd(self.part, X_in=X_in, X_in_bf16=X16, X_bd=X_bd, order=self.order[l], send_out=send,
+                                  **common)
         else:
-            B.pgcn_layer_fwd(self.part, H_in=X_in, H_bd=X_bd, order=self.order[l], **common)
+            B.pgcn_layer_fwd(self.part, H_in=X_in, H_bd=X_bd, order=self.order[l], send_out=send, **common)
         self.X_used[l] = X_in
         self.X_bd_used[l] = X_bd
 
@@ -321,7 +332,8 @@ class PartitionTrainer:
                 if o.smooth_f:
                     B.pgcn_smooth_ema(self.ema_f[l], H_bd, b, f, ld_of(f), o.gamma, st)
                     H_bd = self.ema_f[l]
-            B.pgcn_pack_boundary(self.part, B.PGCN_PACK_FEAT, H_in, self.send_f[l], f, ld_of(f), st)
+            if l == 1 or not o.fuse_pack:      # fused: layer l - 1's output kernel wrote these rows
+                B.pgcn_pack_boundary(self.part, B.PGCN_PACK_FEAT, H_in, self.send_f[l], f, ld_of(f), st)
             if mode == "pipe":
                 self.ev_pack[l].record(st)
                 side.wait_event(self.ev_pack[l])

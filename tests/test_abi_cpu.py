@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
     assert set(syms) == set(B.SIGNATURES), "binding signatures must cover exactly the header"
     for s in syms:
         assert getattr(B.lib, s) is not None
-    assert B.pgcn_version() == 161
+    assert B.pgcn_version() == 162
 
 
 def compare(g_n, rowptr, col, owner, nparts, part, self_loop=True):
