@@ -113,8 +113,9 @@ typedef struct pgcn_partition pgcn_partition;
 
 /* Tuning overrides (environment variables; none is needed for correct use):
  *   PGCN_AGG_CHUNKS    column chunks of the aggregation plans, 1..64 (read by
- *                      pgcn_partition_setup; default: about 11,000 gathered rows
+ *                      pgcn_partition_setup; default: about 8,000 gathered rows
  *                      per chunk while rows keep >= 32 non-zeros per chunk);
+ *   PGCN_AGG_CHUNKS_T  the same for the plan of P_i^T alone (takes precedence);
  *   PGCN_SEGMENT       length at which long rows are split into segments,
  *                      16..1048576 (read by pgcn_partition_setup; default 512);
  *   PGCN_AGG_SLICE_F4  float4 columns per aggregation lane slice: 16, 32 or 64

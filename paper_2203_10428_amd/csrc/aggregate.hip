@@ -19,7 +19,7 @@
 //    Workgroup b works on slice b % S; the hardware deals workgroups to the
 //    8 XCDs round robin, so an XCD only ever touches one slice of every row.
 //  * The columns of the sparse matrix (the gathered rows) are cut into C
-//    chunks of about 11,000 rows, one launch per chunk, so that the rows one
+//    chunks of about 8,000 rows, one launch per chunk, so that the rows one
 //    launch gathers from stay in the caches while they are reused (cache
 //    blocking; C = 1 for short rows, where each gathered row is used only a
 //    few times anyway).  Chunk c adds its partial sum to the output in chunk

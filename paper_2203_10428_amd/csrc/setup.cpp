@@ -24,16 +24,20 @@ int check_hip(hipError_t e, const char *what) {
 }
 
 // Number of column chunks of a CSR matrix for cache blocking: chunks of about
-// 11,000 gathered rows (the measured optimum for 1 KB rows on MI355X), but
-// only while a row keeps >= 32 non-zeros per chunk on average.
-static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz) {
-  const char *env = std::getenv("PGCN_AGG_CHUNKS");
-  if (env) {
+// 8,000 gathered rows (measured on MI355X with 1 KB rows: the Reddit-like
+// forward is fastest at 10-11 chunks of its 88,000 columns, the transposed
+// aggregation at 7-8 of its 58,000), but only while a row keeps >= 32
+// non-zeros per chunk on average.  PGCN_AGG_CHUNKS overrides both plans,
+// PGCN_AGG_CHUNKS_T the transposed one.
+static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz, bool transposed) {
+  for (const char *name : {transposed ? "PGCN_AGG_CHUNKS_T" : "", "PGCN_AGG_CHUNKS"}) {
+    const char *env = *name ? std::getenv(name) : nullptr;
+    if (!env) continue;
     int v = std::atoi(env);
     if (v >= 1 && v <= 64) return v;
   }
   if (nrows == 0 || ncols == 0) return 1;
-  const int64_t by_cache = (ncols + 10999) / 11000;
+  const int64_t by_cache = (ncols + 7999) / 8000;
   const int64_t by_len = (nnz / nrows) / 32;
   int64_t c = std::min(by_cache, by_len);
   return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, 16));
@@ -48,12 +52,12 @@ static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz) {
 // (empty runs are skipped except in the first and last chunk, which write
 // and finish the row).  Whole runs are scheduled longest first.
 static void build_plan(const std::vector<int64_t> &rowptr, const std::vector<int32_t> &col, int64_t nrows,
-                       int64_t ncols, int32_t segment, Plan &p) {
+                       int64_t ncols, int32_t segment, bool transposed, Plan &p) {
   p.items.clear();
   p.splits.clear();
   p.slots = 0;
   const int64_t nnz = nrows ? rowptr[nrows] : 0;
-  p.chunks = choose_chunks(nrows, ncols, nnz);
+  p.chunks = choose_chunks(nrows, ncols, nnz, transposed);
   const int32_t C = p.chunks;
   p.chunk_items.assign(C + 1, 0);
   p.chunk_whole.assign(C, 0);
@@ -328,8 +332,8 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
     for (int64_t k = 0; k < p->n_send; ++k) p->inv_k[fill[p->send_idx[k]]++] = (int32_t)k;
   }
 
-  build_plan(p->rowptr, p->col, n_in, n_all, p->segment, p->plan);
-  build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, p->plan_t);
+  build_plan(p->rowptr, p->col, n_in, n_all, p->segment, false, p->plan);
+  build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, true, p->plan_t);
 
   if (!p->host_only) {
     PGCN_HIP(hipGetDevice(&p->device));
