@@ -2,6 +2,7 @@
 (bit-exact against the oracle's builder) and argument errors.  No kernel is
 launched here; the partition is built with PGCN_SETUP_HOST_ONLY.
 """
+import ctypes as C
 import os
 import re
 import subprocess
@@ -165,3 +166,31 @@ def test_setup_bit_exact_full_size(name):
     w = configs.WORKLOADS[name]
     g = configs.make_graph(w)
     compare(g.n, g.rowptr, g.col, g.owner, g.nparts, 0)
+
+
+def test_binding_structs_match_the_header(tmp_path):
+    """Every ctypes structure of the binding has the header's size and, field
+    by field, its offsets (a C program compiled against include/pgcn.h prints
+    them), so no argument can land in the wrong slot."""
+    structs = [B.pgcn_csr, B.pgcn_boundary_map, B.pgcn_info, B.pgcn_arrays, B.pgcn_fwd_args, B.pgcn_bwd_args,
+               B.pgcn_sage_fwd_args, B.pgcn_sage_bwd_args]
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "pgcn.h"', "int main(void) {"]
+    for cls in structs:
+        name = cls.__name__
+        lines.append(f'  printf("{name} %zu\\n", sizeof({name}));')
+        for field, _ in cls._fields_:
+            lines.append(f'  printf("{name}.{field} %zu\\n", offsetof({name}, {field}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    r = subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+                        str(src), "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    c_side = dict(line.split() for line in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                          check=True).stdout.splitlines())
+    for cls in structs:
+        name = cls.__name__
+        assert int(c_side[name]) == C.sizeof(cls), name
+        for field, _ in cls._fields_:
+            assert int(c_side[f"{name}.{field}"]) == getattr(cls, field).offset, f"{name}.{field}"
