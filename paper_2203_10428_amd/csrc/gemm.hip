@@ -397,18 +397,19 @@ __global__ __launch_bounds__(256, (BN == 128 && A32) ? 2 : 3) void gemm_tn_bf16(
   tn_store_partial<TM, TN, UA, 8, UB>(p, acc, split, m0, n0, wm0, wn0, lane);
 }
 
-// Fixed-order sum of split partials.  A block owns 64 consecutive outputs and
-// G ranges of the split index: thread (g, c) adds the splits of range g in
-// ascending order for outputs V c .. V c + V - 1 (16-byte loads when
-// mn % 4 == 0, V = 4, G = 16), then the G range sums of each output are added
-// in order g = 0 .. G - 1.  Many short independent sums keep enough loads in
-// flight for partials that number in the hundreds per output.
-template <int V>
+// Fixed-order sum of split partials.  A block owns OUT consecutive outputs
+// (64, or 16 for small outputs) and G = 256 V / OUT ranges of the split
+// index: thread (g, c) adds the splits of range g in ascending order for
+// outputs V c .. V c + V - 1 (16-byte loads when mn % 4 == 0, V = 4), then
+// the G range sums of each output are added in order g = 0 .. G - 1.  Many
+// short independent sums keep enough loads in flight for partials that
+// number in the hundreds per output.
+template <int V, int OUT>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *ws, int splits, int64_t mn, float *out) {
-  constexpr int C = 64 / V, G = 256 / C;
-  __shared__ float part[G][64];
+  constexpr int C = OUT / V, G = 256 / C;
+  __shared__ float part[G][OUT];
   const int c = threadIdx.x % C, g = threadIdx.x / C;
-  const int64_t i0 = (int64_t)blockIdx.x * 64 + V * c;
+  const int64_t i0 = (int64_t)blockIdx.x * OUT + V * c;
   const int per = (splits + G - 1) / G;
   const int z0 = g * per, z1 = min(splits, z0 + per);
   float s[V];
@@ -432,8 +433,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *ws, int
   for (int e = 0; e < V; ++e) part[g][V * c + e] = s[e];
   __syncthreads();
   const int o = threadIdx.x;
-  const int64_t i = (int64_t)blockIdx.x * 64 + o;
-  if (o < 64 && i < mn) {
+  const int64_t i = (int64_t)blockIdx.x * OUT + o;
+  if (o < OUT && i < mn) {
     float t = 0.f;
 #pragma unroll
     for (int k = 0; k < G; ++k) t += part[k][o];
@@ -548,11 +549,18 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   }
   const int64_t mn = (int64_t)g.M * g.N;
   TraceScope ts(PGCN_TK_WGRAD_REDUCE, s);
-  const dim3 rgrid((unsigned)((mn + 63) / 64));
-  if (mn % 4 == 0 && ((uintptr_t)g.workspace & 15u) == 0)   // every partial [M x N] starts 16-byte aligned
-    hipLaunchKernelGGL(splitk_reduce_kernel<4>, rgrid, dim3(256), 0, s, (const float *)g.workspace, splits, mn, g.C);
-  else
-    hipLaunchKernelGGL(splitk_reduce_kernel<1>, rgrid, dim3(256), 0, s, (const float *)g.workspace, splits, mn, g.C);
+  // 64 outputs per workgroup, or 16 (64 split ranges each) when that would
+  // leave fewer than four workgroups per CU: the sums stay short and many
+  const bool narrow = (mn + 63) / 64 < 1024;
+  const dim3 rgrid((unsigned)(narrow ? (mn + 15) / 16 : (mn + 63) / 64));
+  const float *ws = (const float *)g.workspace;
+  if (mn % 4 == 0 && ((uintptr_t)g.workspace & 15u) == 0) {   // every partial [M x N] starts 16-byte aligned
+    if (narrow) hipLaunchKernelGGL((splitk_reduce_kernel<4, 16>), rgrid, dim3(256), 0, s, ws, splits, mn, g.C);
+    else hipLaunchKernelGGL((splitk_reduce_kernel<4, 64>), rgrid, dim3(256), 0, s, ws, splits, mn, g.C);
+  } else {
+    if (narrow) hipLaunchKernelGGL((splitk_reduce_kernel<1, 16>), rgrid, dim3(256), 0, s, ws, splits, mn, g.C);
+    else hipLaunchKernelGGL((splitk_reduce_kernel<1, 64>), rgrid, dim3(256), 0, s, ws, splits, mn, g.C);
+  }
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;
 }
