@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 162
+#define PGCN_VERSION 163
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -114,8 +114,9 @@ typedef struct pgcn_partition pgcn_partition;
 /* Tuning overrides (environment variables; none is needed for correct use):
  *   PGCN_AGG_CHUNKS    column chunks of the aggregation plans, 1..64 (read by
  *                      pgcn_partition_setup; default: about 8,000 gathered rows
- *                      per chunk while rows keep >= 32 non-zeros per chunk);
- *   PGCN_AGG_CHUNKS_T  the same for the plan of P_i^T alone (takes precedence);
+ *                      per chunk, 32,000 for rows of at most 64 floats, while
+ *                      rows keep >= 32 non-zeros per chunk);
+ *   PGCN_AGG_CHUNKS_T  the same for the plans of P_i^T alone (takes precedence);
  *   PGCN_SEGMENT       length at which long rows are split into segments,
  *                      16..1048576 (read by pgcn_partition_setup; default 512);
  *   PGCN_AGG_SLICE_F4  float4 columns per aggregation lane slice: 16, 32 or 64
@@ -123,7 +124,8 @@ typedef struct pgcn_partition pgcn_partition;
  *   PGCN_TN_BM=128     keeps the fp32 weight-gradient GEMM in 128-row tiles
  *                      (read once; default: 256-row tiles for f_in >= 384).
  * Chunks and segments set the order in which a row's terms are added (results
- * stay deterministic for a given setting); the other two change only speed. */
+ * stay deterministic for a given setting and row width); the other two change
+ * only speed. */
 
 /* Largest layer width (f_in, f_out) the layer entry points accept: the
  * aggregation covers a row in at most 32 launches of up to 512 float4
@@ -151,6 +153,9 @@ typedef struct {
   int32_t spmmt_chunks;    /* column chunks of P_i^T                          */
   int32_t symmetric;       /* 1 if built with PGCN_SETUP_SYMMETRIC            */
   int32_t self_loop;       /* 0 if built with PGCN_SETUP_NO_SELF_LOOP         */
+  int32_t spmm_chunks_narrow;  /* column chunks of P_i when the aggregated rows
+                                  have at most 64 floats                      */
+  int32_t spmmt_chunks_narrow; /* the same for P_i^T                          */
 } pgcn_info;
 
 /* Caller-allocated host buffers for pgcn_partition_export, sized from pgcn_info.

@@ -46,7 +46,8 @@ class pgcn_info(C.Structure):
                 ("max_row_len", _i64), ("max_row_len_t", _i64), ("nparts", _i32), ("self", _i32),
                 ("host_only", _i32), ("spmm_segment", _i32), ("spmm_items", _i64),
                 ("spmm_split_slots", _i64), ("spmmt_items", _i64), ("spmmt_split_slots", _i64),
-                ("spmm_chunks", _i32), ("spmmt_chunks", _i32), ("symmetric", _i32), ("self_loop", _i32)]
+                ("spmm_chunks", _i32), ("spmmt_chunks", _i32), ("symmetric", _i32), ("self_loop", _i32),
+                ("spmm_chunks_narrow", _i32), ("spmmt_chunks_narrow", _i32)]
 
 
 class pgcn_arrays(C.Structure):

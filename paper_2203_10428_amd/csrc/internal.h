@@ -59,6 +59,9 @@ struct pgcn_partition {
   std::vector<int64_t> deg;        // whole-graph degree + 1 of the n_inner + n_bd local nodes
   std::vector<float> sym_scale;    // d̃^{-1/2} of the local nodes (symmetric partitions)
   pgcn::Plan plan, plan_t;
+  // plans for gathered rows of at most kNarrowRow floats, whose chunks hold
+  // more rows for the same bytes; chunks == 0: not built (same as plan, plan_t)
+  pgcn::Plan plan_n, plan_tn;
   // device copies
   int32_t *d_col = nullptr, *d_col_t = nullptr, *d_send_idx = nullptr, *d_inv_k = nullptr;
   int64_t *d_inv_ptr = nullptr;
@@ -71,6 +74,16 @@ struct pgcn_partition {
 };
 
 namespace pgcn {
+
+// Aggregations of rows of at most this many floats use the narrow plans.
+constexpr int64_t kNarrowRow = 64;
+
+// The work plan for an aggregation of P_i (transposed: P_i^T) over rows of f floats.
+inline const Plan &agg_plan(const pgcn_partition *p, bool transposed, int64_t f) {
+  const Plan &narrow = transposed ? p->plan_tn : p->plan_n;
+  if (f <= kNarrowRow && narrow.chunks > 0) return narrow;
+  return transposed ? p->plan_t : p->plan;
+}
 
 int set_error(int code, const std::string &msg);
 

@@ -24,12 +24,13 @@ int check_hip(hipError_t e, const char *what) {
 }
 
 // Number of column chunks of a CSR matrix for cache blocking: chunks of about
-// 8,000 gathered rows (measured on MI355X with 1 KB rows: the Reddit-like
-// forward is fastest at 10-11 chunks of its 88,000 columns, the transposed
-// aggregation at 7-8 of its 58,000), but only while a row keeps >= 32
-// non-zeros per chunk on average.  PGCN_AGG_CHUNKS overrides both plans,
-// PGCN_AGG_CHUNKS_T the transposed one.
-static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz, bool transposed) {
+// 8,000 gathered rows of 1 KB (measured on MI355X: the Reddit-like forward is
+// fastest at 10-11 chunks of its 88,000 columns, the transposed aggregation at
+// 7-8 of its 58,000), or 32,000 rows for the narrow plans (rows of at most 256
+// bytes: the Reddit-like 41-wide output layer is fastest at 2-4 chunks), but
+// only while a row keeps >= 32 non-zeros per chunk on average.
+// PGCN_AGG_CHUNKS overrides every plan, PGCN_AGG_CHUNKS_T the transposed ones.
+static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz, bool transposed, int64_t rows_per_chunk) {
   for (const char *name : {transposed ? "PGCN_AGG_CHUNKS_T" : "", "PGCN_AGG_CHUNKS"}) {
     const char *env = *name ? std::getenv(name) : nullptr;
     if (!env) continue;
@@ -37,7 +38,7 @@ static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz, bool tra
     if (v >= 1 && v <= 64) return v;
   }
   if (nrows == 0 || ncols == 0) return 1;
-  const int64_t by_cache = (ncols + 7999) / 8000;
+  const int64_t by_cache = (ncols + rows_per_chunk - 1) / rows_per_chunk;
   const int64_t by_len = (nnz / nrows) / 32;
   int64_t c = std::min(by_cache, by_len);
   return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, 16));
@@ -52,12 +53,11 @@ static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz, bool tra
 // (empty runs are skipped except in the first and last chunk, which write
 // and finish the row).  Whole runs are scheduled longest first.
 static void build_plan(const std::vector<int64_t> &rowptr, const std::vector<int32_t> &col, int64_t nrows,
-                       int64_t ncols, int32_t segment, bool transposed, Plan &p) {
+                       int64_t ncols, int32_t segment, int32_t chunks, Plan &p) {
   p.items.clear();
   p.splits.clear();
   p.slots = 0;
-  const int64_t nnz = nrows ? rowptr[nrows] : 0;
-  p.chunks = choose_chunks(nrows, ncols, nnz, transposed);
+  p.chunks = chunks;
   const int32_t C = p.chunks;
   p.chunk_items.assign(C + 1, 0);
   p.chunk_whole.assign(C, 0);
@@ -129,15 +129,16 @@ static int upload(T **dptr, const std::vector<T> &h) {
 
 static void free_device(pgcn_partition *p) {
   void *ptrs[] = {p->d_col, p->d_col_t, p->d_send_idx, p->d_inv_k, p->d_inv_ptr, p->d_inv_deg, p->d_sym_scale,
-                  p->plan.d_items, p->plan.d_splits, p->plan_t.d_items, p->plan_t.d_splits};
+                  p->plan.d_items, p->plan.d_splits, p->plan_t.d_items, p->plan_t.d_splits,
+                  p->plan_n.d_items, p->plan_n.d_splits, p->plan_tn.d_items, p->plan_tn.d_splits};
   for (void *q : ptrs)
     if (q) (void)hipFree(q);
   p->d_col = p->d_col_t = p->d_send_idx = p->d_inv_k = nullptr;
   p->d_inv_ptr = nullptr;
   p->d_inv_deg = p->d_sym_scale = nullptr;
   p->d_row_scale = p->d_col_scale = nullptr;
-  p->plan.d_items = p->plan_t.d_items = nullptr;
-  p->plan.d_splits = p->plan_t.d_splits = nullptr;
+  p->plan.d_items = p->plan_t.d_items = p->plan_n.d_items = p->plan_tn.d_items = nullptr;
+  p->plan.d_splits = p->plan_t.d_splits = p->plan_n.d_splits = p->plan_tn.d_splits = nullptr;
 }
 
 static int check_device() {
@@ -332,8 +333,17 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
     for (int64_t k = 0; k < p->n_send; ++k) p->inv_k[fill[p->send_idx[k]]++] = (int32_t)k;
   }
 
-  build_plan(p->rowptr, p->col, n_in, n_all, p->segment, false, p->plan);
-  build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, true, p->plan_t);
+  {
+    const int64_t nnz = p->nnz, wide = 8000, narrow = 32000;
+    const int32_t c = choose_chunks(n_in, n_all, nnz, false, wide), ct = choose_chunks(n_all, n_in, nnz, true, wide);
+    const int32_t cn = choose_chunks(n_in, n_all, nnz, false, narrow);
+    const int32_t ctn = choose_chunks(n_all, n_in, nnz, true, narrow);
+    build_plan(p->rowptr, p->col, n_in, n_all, p->segment, c, p->plan);
+    build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, ct, p->plan_t);
+    p->plan_n.chunks = p->plan_tn.chunks = 0;
+    if (cn != c) build_plan(p->rowptr, p->col, n_in, n_all, p->segment, cn, p->plan_n);
+    if (ctn != ct) build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, ctn, p->plan_tn);
+  }
 
   if (!p->host_only) {
     PGCN_HIP(hipGetDevice(&p->device));
@@ -349,6 +359,10 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
     if (!rc) rc = upload(&p->plan.d_splits, p->plan.splits);
     if (!rc) rc = upload(&p->plan_t.d_items, p->plan_t.items);
     if (!rc) rc = upload(&p->plan_t.d_splits, p->plan_t.splits);
+    if (!rc) rc = upload(&p->plan_n.d_items, p->plan_n.items);
+    if (!rc) rc = upload(&p->plan_n.d_splits, p->plan_n.splits);
+    if (!rc) rc = upload(&p->plan_tn.d_items, p->plan_tn.items);
+    if (!rc) rc = upload(&p->plan_tn.d_splits, p->plan_tn.splits);
     if (rc) {
       free_device(p);
       delete p;
@@ -379,6 +393,8 @@ extern "C" int pgcn_partition_info(const pgcn_partition *p, pgcn_info *o) {
   o->spmmt_split_slots = p->plan_t.slots;
   o->spmm_chunks = p->plan.chunks;
   o->spmmt_chunks = p->plan_t.chunks;
+  o->spmm_chunks_narrow = p->plan_n.chunks ? p->plan_n.chunks : p->plan.chunks;
+  o->spmmt_chunks_narrow = p->plan_tn.chunks ? p->plan_tn.chunks : p->plan_t.chunks;
   o->symmetric = p->symmetric;
   o->self_loop = p->self_loop;
   return PGCN_OK;

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
     assert set(syms) == set(B.SIGNATURES), "binding signatures must cover exactly the header"
     for s in syms:
         assert getattr(B.lib, s) is not None
-    assert B.pgcn_version() == 162
+    assert B.pgcn_version() == 163
 
 
 def compare(g_n, rowptr, col, owner, nparts, part, self_loop=True):
@@ -89,6 +89,31 @@ def test_setup_empty_partition_and_isolated_nodes():
         info = compare(n, rowptr, col, owner, 3, part)
         if part == 2:
             assert info["n_inner"] == 0 and info["nnz"] == 0
+
+
+def test_setup_chunk_counts_by_row_width(monkeypatch):
+    # column chunks: about 8,000 gathered rows each (32,000 for rows of at most
+    # 64 floats), while rows keep >= 32 non-zeros per chunk; the overrides set
+    # every plan (PGCN_AGG_CHUNKS) or those of P_i^T (PGCN_AGG_CHUNKS_T)
+    from gpu_helpers import random_partition_graph
+    n, rowptr, col, owner = random_partition_graph(9000, 3000, 2, 120, 13)
+    for k in ("PGCN_AGG_CHUNKS", "PGCN_AGG_CHUNKS_T"):
+        monkeypatch.delenv(k, raising=False)
+
+    def counts():
+        info = B.pgcn_partition_info(B.pgcn_partition_setup(n, rowptr, col, owner, 2, 0, host_only=True))
+        return info, (info["spmm_chunks"], info["spmm_chunks_narrow"], info["spmmt_chunks"],
+                      info["spmmt_chunks_narrow"])
+
+    info, got = counts()
+    rows, cols, nnz = info["n_inner"], info["n_inner"] + info["n_bd"], info["nnz"]
+    rule = lambda nr, nc, per: max(1, min(-(-nc // per), nnz // nr // 32, 16))
+    assert got == (rule(rows, cols, 8000), rule(rows, cols, 32000), rule(cols, rows, 8000), rule(cols, rows, 32000))
+    assert got == (2, 1, 2, 1)
+    monkeypatch.setenv("PGCN_AGG_CHUNKS", "3")
+    assert counts()[1] == (3, 3, 3, 3)
+    monkeypatch.setenv("PGCN_AGG_CHUNKS_T", "5")
+    assert counts()[1] == (3, 3, 5, 5)
 
 
 def test_setup_heavy_rows_are_split_into_fixed_segments():

@@ -10,7 +10,10 @@ normalisation, GraphSAGE in both associations), against the oracle:
   rows of the GraphSAGE mean);
 * the widest layers the entry points accept (PGCN_MAX_WIDTH columns in or
   out: 32 aggregation launches per row), and one column more, which every
-  layer entry point rejects before launching anything.
+  layer entry point rejects before launching anything;
+* a partition whose aggregation plans differ by row width (2 column chunks
+  for wide rows, 1 for rows of at most 64 floats), with one narrow and one
+  wide width per layer, so that each order runs each plan in each direction.
 """
 import numpy as np
 import pytest
@@ -36,6 +39,9 @@ def graph(kind):
     if kind == "one_partition":
         n, rowptr, col, _ = random_partition_graph(900, 300, 2, 10, 4)
         return n, rowptr, col, np.zeros(n, np.int32), 1
+    if kind == "two_plans":       # 12,000 columns, ~100 non-zeros per row: wide plans 2 chunks, narrow 1
+        n, rowptr, col, owner = random_partition_graph(9000, 3000, 2, 120, 13)
+        return n, rowptr, col, owner, 2
     if kind == "empty":
         n, rowptr, col, owner = random_partition_graph(600, 300, 3, 8, 5)
         owner = np.where(owner == 0, 1, owner).astype(np.int32)      # partition 0 owns nothing
@@ -91,7 +97,7 @@ def run_layer(kind, model, norm, order, dt, f_in=37, f_out=21):
         G_ref, Jf_ref = layers.layer_backward(P, A_ref, Zm, J, W.astype(np.float64), True, True, gm, order=order,
                                               H_full=X)
     torch.cuda.synchronize()
-    return dict(n=n, b=b, H=host(H, f_out), H_ref=H_ref, G=dG.cpu().numpy(), G_ref=G_ref,
+    return dict(info=B.pgcn_partition_info(part), n=n, b=b, H=host(H, f_out), H_ref=H_ref, G=dG.cpu().numpy(), G_ref=G_ref,
                 J_in=host(J_in, f_in), J_bd=host(J_bd, f_in) if b else np.zeros((0, f_in)), Jf_ref=Jf_ref)
 
 
@@ -159,3 +165,18 @@ def test_width_above_maximum_is_rejected(entry, wide):
                                   J_bd_out=z(b, li), **common)
     assert e.value.code == B.PGCN_EINVAL
     assert "PGCN_MAX_WIDTH" in str(e.value)
+
+
+@pytest.mark.parametrize("model,norm,order", FORMS)
+@pytest.mark.parametrize("f_in,f_out", [(41, 72), (72, 41)])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_narrow_and_wide_plans(model, norm, order, f_in, f_out, dt):
+    r = run_layer("two_plans", model, norm, order, dt, f_in=f_in, f_out=f_out)
+    info = r["info"]
+    assert (info["spmm_chunks"], info["spmm_chunks_narrow"]) == (2, 1)
+    assert (info["spmmt_chunks"], info["spmmt_chunks_narrow"]) == (2, 1)
+    tol = TOL[dt]
+    assert rel_err(r["H"], r["H_ref"]) < tol["act"]
+    assert rel_err(r["G"], r["G_ref"]) < tol["grad"]
+    assert rel_err(r["J_in"], r["Jf_ref"][: r["n"]]) < tol["grad"]
+    assert rel_err(r["J_bd"], r["Jf_ref"][r["n"]:]) < tol["grad"]
