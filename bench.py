@@ -91,7 +91,7 @@ def measured_traffic(workload: str, kernel: str):
 
     profiles/traffic_<workload>.json holds FETCH_SIZE and WRITE_SIZE summed over
     the kernel's dispatches of one step, scaled by the same counters on a plain
-    copy of known size, and the SHA-256 of the kernel and work-plan sources
+    copy of known size, and the SHA-256 of the kernel, work-plan and stride sources
     they were taken with.  If a source has changed since, the figure no longer
     applies (None).
     """
