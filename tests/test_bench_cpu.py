@@ -3,7 +3,9 @@ per-step algorithmic work (the roofline's numerator) counts exactly the
 matrix products each layer forms.  The expected flops are listed product by
 product from the layer algebra (GCN: Z = (P H) W or P (H W); GraphSAGE:
 CONCAT(P X, X) W, or P (X W_top) + X_in W_bot; backward: the weight gradient
-and, above layer 1, the feature gradient of each product)."""
+and, above layer 1, the feature gradient of each product).  The counter-based
+traffic figure is reported only while the sources it was measured with are
+unchanged."""
 import importlib.util
 import os
 import subprocess
@@ -70,3 +72,34 @@ def test_gemm_flops_match_layer_products(model, orders):
         assert got[key] == v, key
     # every aggregation model moves at least the compulsory bytes
     assert got["agg_fwd_gather"] >= got["agg_fwd"] > 0 and got["agg_bwd_gather"] >= got["agg_bwd"] > 0
+
+
+def test_measured_traffic_is_void_once_a_source_changes(tmp_path, monkeypatch):
+    # roofline.traffic comes from committed counter runs only while the sources
+    # they were taken with hash the same
+    import hashlib
+    import json
+    bench = load_bench()
+    csrc = tmp_path / "paper_2203_10428_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    (csrc / "aggregate.hip").write_text("kernel, first version")
+    (tmp_path / "profiles").mkdir()
+    digest = hashlib.sha256(b"kernel, first version").hexdigest()
+    rec = {"sources": {"aggregate.hip": digest}, "kernels": {"agg_fwd": 123.0}}
+    (tmp_path / "profiles" / "traffic_w.json").write_text(json.dumps(rec))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.measured_traffic("w", "agg_fwd") == 123.0
+    assert bench.measured_traffic("w", "agg_bwd") is None
+    assert bench.measured_traffic("other", "agg_fwd") is None
+    (csrc / "aggregate.hip").write_text("kernel, second version")
+    assert bench.measured_traffic("w", "agg_fwd") is None
+
+
+def test_committed_traffic_records_name_existing_sources():
+    import json
+    for wl in ("reddit-like-1of4", "yelp-like-1of3"):
+        rec = json.load(open(os.path.join(ROOT, "profiles", f"traffic_{wl}.json")))
+        assert {"aggregate.hip", "setup.cpp", "api.cpp"} <= set(rec["sources"])
+        for name in rec["sources"]:
+            assert os.path.exists(os.path.join(ROOT, "paper_2203_10428_amd", "csrc", name))
+        assert rec["kernels"]["agg_fwd"] > 0 and rec["kernels"]["agg_bwd"] > 0
