@@ -13,7 +13,8 @@ normalisation, GraphSAGE in both associations), against the oracle:
   layer entry point rejects before launching anything;
 * a partition whose aggregation plans differ by row width (2 column chunks
   for wide rows, 1 for rows of at most 64 floats), with one narrow and one
-  wide width per layer, so that each order runs each plan in each direction.
+  wide width per layer (also 64 against 65, either side of the threshold), so
+  that each order runs each plan in each direction.
 """
 import numpy as np
 import pytest
@@ -168,7 +169,7 @@ def test_width_above_maximum_is_rejected(entry, wide):
 
 
 @pytest.mark.parametrize("model,norm,order", FORMS)
-@pytest.mark.parametrize("f_in,f_out", [(41, 72), (72, 41)])
+@pytest.mark.parametrize("f_in,f_out", [(41, 72), (72, 41), (64, 65), (65, 64)])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_narrow_and_wide_plans(model, norm, order, f_in, f_out, dt):
     r = run_layer("two_plans", model, norm, order, dt, f_in=f_in, f_out=f_out)
