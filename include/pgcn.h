@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 163
+#define PGCN_VERSION 164
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -254,6 +254,30 @@ typedef struct {
                                   H_out). 16-byte aligned. */
 } pgcn_fwd_args;
 int pgcn_layer_fwd(const pgcn_partition *part, const pgcn_fwd_args *args, hipStream_t stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * layer forward as pgcn_layer_fwd (same kernels, same results bit for bit),
+ * with its workspace taken from a fixed array inside this library instead of
+ * args->workspace.  Nothing is allocated by the call.
+ *
+ * args->workspace must be NULL and args->workspace_bytes 0 (else
+ * PGCN_EINVAL); every other argument is as for pgcn_layer_fwd, and the
+ * caller still owns and passes every input and output.  A layer whose
+ * workspace (pgcn_layer_workspace_size's forward share) exceeds
+ * PGCN_NOALLOC_SCRATCH_BYTES is rejected with PGCN_EWORKSPACE before any
+ * launch.  The array holds PGCN_NOALLOC_SCRATCH_BYTES on every GPU the
+ * library runs on, until the process ends; its address on a device is
+ * resolved when a partition is set up there.
+ *
+ * All calls on one GPU share that GPU's array and it keeps the last call's
+ * contents (nothing in it needs to start at zero): calls that overlap on one
+ * GPU (two streams, two threads, two graphs replayed concurrently) race and
+ * must be serialised by the caller.
+ */
+#define PGCN_NOALLOC_SCRATCH_BYTES (32u << 20)
+int pgcn_layer_fwd_noalloc(const pgcn_partition *part, const pgcn_fwd_args *args, hipStream_t stream);
 
 /*
  * One layer backward (Algorithm 1's weight- and feature-gradient lines;

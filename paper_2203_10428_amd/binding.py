@@ -28,6 +28,7 @@ PGCN_MAX_WIDTH = 63740
 PGCN_SOFTMAX_CE, PGCN_SIGMOID_BCE = 0, 1
 PGCN_REFILL_DMA, PGCN_REFILL_FROM_HOST = 1, 2
 PGCN_ORDER_AGG, PGCN_ORDER_TRANSFORM = 0, 1
+PGCN_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 _vp = C.c_void_p
 _i32, _i64, _u32, _f32, _sz = C.c_int32, C.c_int64, C.c_uint32, C.c_float, C.c_size_t
@@ -92,6 +93,7 @@ SIGNATURES = {
     "pgcn_workspace_size": (_sz, [_vp, _i32, _i32, _i32]),
     "pgcn_layer_workspace_size": (_sz, [_vp, _i32, _i32, _i32, _i32]),
     "pgcn_layer_fwd": (_i32, [_vp, C.POINTER(pgcn_fwd_args), _vp]),
+    "pgcn_layer_fwd_noalloc": (_i32, [_vp, C.POINTER(pgcn_fwd_args), _vp]),
     "pgcn_layer_bwd": (_i32, [_vp, C.POINTER(pgcn_bwd_args), _vp]),
     "pgcn_smooth_ema": (_i32, [_vp, _vp, _i64, _i32, _i64, _f32, _vp]),
     "pgcn_pack_boundary": (_i32, [_vp, _i32, _vp, _vp, _i32, _i64, _vp]),
@@ -229,6 +231,15 @@ def pgcn_layer_fwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_
                       _ptr(A), _ptr(A_bf16), _ptr(H_out), _ptr(workspace), workspace_bytes, order, int(a_given),
                       _ptr(send_out))
     _check(lib.pgcn_layer_fwd(part.handle, C.byref(a), _stream(stream)), "pgcn_layer_fwd")
+
+
+def pgcn_layer_fwd_noalloc(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, H_in, H_bd, W, A,
+                           A_bf16, H_out, order=PGCN_ORDER_AGG, a_given=False, send_out=None, stream=None,
+                           workspace=None, workspace_bytes=0):
+    a = pgcn_fwd_args(f_in, f_out, gemm_dtype, int(relu), ld_in, ld_out, _ptr(H_in), _ptr(H_bd), _ptr(W),
+                      _ptr(A), _ptr(A_bf16), _ptr(H_out), _ptr(workspace), workspace_bytes, order, int(a_given),
+                      _ptr(send_out))
+    _check(lib.pgcn_layer_fwd_noalloc(part.handle, C.byref(a), _stream(stream)), "pgcn_layer_fwd_noalloc")
 
 
 def pgcn_layer_bwd(part: Partition, *, f_in, f_out, gemm_dtype, relu, ld_in, ld_out, J_out, H_out, A, A_bf16,

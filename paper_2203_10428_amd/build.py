@@ -18,7 +18,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpgcn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["setup.cpp", "api.cpp", "trace.cpp", "aggregate.hip", "gemm.hip", "gemm_nk.hip", "elementwise.hip"]
+SOURCES = ["setup.cpp", "api.cpp", "trace.cpp", "aggregate.hip", "gemm.hip", "gemm_nk.hip", "elementwise.hip", "noalloc.hip"]
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", "--offload-arch=gfx950",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -102,6 +102,16 @@ size_t bwd_ws_tf(const pgcn_partition *p, int32_t f_in, int32_t f_out, bool inpu
 
 }  // namespace
 
+// Workspace bytes one pgcn_layer_fwd call needs (0 for arguments it rejects).
+size_t pgcn::layer_fwd_workspace(const pgcn_partition *p, const pgcn_fwd_args *a) {
+  if (!p || !a || a->f_in < 1 || a->f_out < 1 || a->f_in > PGCN_MAX_WIDTH || a->f_out > PGCN_MAX_WIDTH) return 0;
+  if (a->gemm_dtype != PGCN_F32 && a->gemm_dtype != PGCN_BF16) return 0;
+  if (a->order == PGCN_ORDER_TRANSFORM) return fwd_ws_tf(p, a->f_in, a->f_out, a->gemm_dtype);
+  if (a->order != PGCN_ORDER_AGG) return 0;
+  if (a->a_given) return gemm_nk_workspace(a->f_out, a->f_in, a->gemm_dtype);
+  return fwd_ws(p, a->f_in, a->f_out, a->gemm_dtype);
+}
+
 extern "C" size_t pgcn_layer_workspace_size(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype,
                                             int32_t order) {
   if (order == PGCN_ORDER_AGG) return pgcn_workspace_size(p, f_in, f_out, gemm_dtype);

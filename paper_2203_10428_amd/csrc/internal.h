@@ -87,6 +87,12 @@ inline const Plan &agg_plan(const pgcn_partition *p, bool transposed, int64_t f)
 
 int set_error(int code, const std::string &msg);
 
+// Workspace bytes one pgcn_layer_fwd call needs (0 for arguments it rejects).
+size_t layer_fwd_workspace(const pgcn_partition *p, const pgcn_fwd_args *a);
+// Resolves this library's fixed scratch array on device `dev` (which must be
+// current) once; pgcn_partition_setup calls it for the device it builds on.
+int noalloc_scratch_init(int dev);
+
 // Records a HIP event pair around a kernel launch on stream `s` while tracing
 // is enabled (pgcn_trace_enable); does nothing otherwise.  A scope around
 // several back-to-back launches says how many with set_launches.

@@ -347,7 +347,7 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
 
   if (!p->host_only) {
     PGCN_HIP(hipGetDevice(&p->device));
-    int rc = PGCN_OK;
+    int rc = noalloc_scratch_init(p->device);
     if (!rc) rc = upload(&p->d_col, p->col);
     if (!rc) rc = upload(&p->d_col_t, p->col_t);
     if (!rc) rc = upload(&p->d_send_idx, p->send_idx);

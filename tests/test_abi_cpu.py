@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     for s in syms:
         assert getattr(B.lib, s) is not None
     header = open(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "pgcn.h")).read()
-    assert B.pgcn_version() == int(re.search(r"#define PGCN_VERSION (\d+)", header).group(1)) == 163
+    assert B.pgcn_version() == int(re.search(r"#define PGCN_VERSION (\d+)", header).group(1)) == 164
 
 
 def compare(g_n, rowptr, col, owner, nparts, part, self_loop=True):
@@ -184,6 +184,18 @@ def test_compute_calls_reject_host_only_handle():
         B.pgcn_smooth_ema(0, 0, 10, 8, 6, 0.9)          # ld < cols
     with pytest.raises(B.PgcnError):
         B.pgcn_loss_fwd_bwd(7, 0, 1, 1, 1, None, None, 1, 1.0, 0, 0, 0, 0)
+    # the forward that allocates nothing checks its handle and workspace arguments before any device call
+    fwd = dict(f_in=8, f_out=4, gemm_dtype=B.PGCN_F32, relu=True, ld_in=8, ld_out=4, H_in=None, H_bd=None, W=None,
+               A=None, A_bf16=None, H_out=None)
+    with pytest.raises(B.PgcnError, match="host-only") as e:
+        B.pgcn_layer_fwd_noalloc(h, **fwd)
+    assert e.value.code == B.PGCN_EINVAL
+
+
+def test_noalloc_scratch_limit_matches_the_header():
+    header = open(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "pgcn.h")).read()
+    m = re.search(r"#define PGCN_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", header)
+    assert m and int(m.group(1)) << int(m.group(2)) == B.PGCN_NOALLOC_SCRATCH_BYTES
 
 
 @pytest.mark.slow
