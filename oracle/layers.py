@@ -96,10 +96,21 @@ def layer_forward(P, H_full: np.ndarray, W: np.ndarray, relu: bool, gemm: str = 
     return A, Z, H
 
 
+def relu_mask(Z: np.ndarray, mask=None) -> np.ndarray:
+    """The ReLU derivative 1[Z > 0] (reading: 0 at Z = 0), or a given decision.
+
+    The decision is an integer taken from a floating-point value; where the
+    value lies within rounding of zero, either side is a correct result, and a
+    caller comparing two computations passes the decision it has certified
+    (as it passes the received messages) instead of re-deciding here."""
+    return (Z > 0.0) if mask is None else np.asarray(mask, dtype=bool)
+
+
 def layer_backward(P, A: np.ndarray, Z: np.ndarray, J: np.ndarray, W: np.ndarray,
-                   relu: bool, input_grad: bool, gemm: str = "f64", order: str = "agg", H_full=None):
-    """``order="transform"`` needs the layer input H_full (inner and boundary rows) instead of A."""
-    M = J * (Z > 0.0) if relu else J
+                   relu: bool, input_grad: bool, gemm: str = "f64", order: str = "agg", H_full=None, mask=None):
+    """``order="transform"`` needs the layer input H_full (inner and boundary rows) instead of A.
+    ``mask`` (bool, Z's shape) replaces the decision Z > 0 when given."""
+    M = J * relu_mask(Z, mask) if relu else J
     if order == "transform":
         Tq = _operand(P.T @ M, gemm)
         G = _operand(H_full, gemm).T @ Tq
@@ -158,11 +169,11 @@ def sage_forward(P, X_full: np.ndarray, n_inner: int, W: np.ndarray, relu: bool,
 
 
 def sage_backward(P, z: np.ndarray, X_inner: np.ndarray, Z: np.ndarray, J: np.ndarray, W: np.ndarray,
-                  relu: bool, input_grad: bool, gemm: str = "f64", order: str = "agg", X_full=None):
+                  relu: bool, input_grad: bool, gemm: str = "f64", order: str = "agg", X_full=None, mask=None):
     """Returns (G, J_full): J_full is the gradient of the dropped input rows (inner, then boundary).
     ``order="transform"`` (needs X_full): T = Pᵀ M, G = [X_fullᵀ T ; X_innerᵀ M],
-    J_full = T W_topᵀ plus M W_botᵀ on the inner rows."""
-    M = J * (Z > 0.0) if relu else J
+    J_full = T W_topᵀ plus M W_botᵀ on the inner rows.  ``mask`` as in ``layer_backward``."""
+    M = J * relu_mask(Z, mask) if relu else J
     Mq = _operand(M, gemm)
     f = X_inner.shape[1]
     n = X_inner.shape[0]

@@ -309,7 +309,7 @@ def run(n, rowptr, col, owner, nparts, X, labels, W0, T, opts: Options):
 
 
 def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: dict, ema_f: dict, ema_g: dict,
-                   t: int, opts: Options):
+                   t: int, opts: Options, relu_masks: dict = None):
     """One iteration of Algorithm 1 for one partition, given what it received.
 
     ``received_f[l]`` ([b, f_{l-1}]) and ``received_g[l]`` ([s, f_{l-1}], l >= 2)
@@ -319,7 +319,10 @@ def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: di
     J_full, G, send_f, X_in, mask) and the partition's weight gradients,
     without applying the update.  Pipelined mode; ``ema_init`` "zero"; no
     boundary preload.  ``P`` must match ``opts.model`` (self loops for GCN).
+    ``relu_masks[l]`` (bool [n, f_l]), where given, is layer l's ReLU
+    decision in the backward instead of Z > 0 (``layers.relu_mask``).
     """
+    relu_masks = relu_masks or {}
     o = opts
     L = len(W)
     sage = o.model == "sage"
@@ -351,10 +354,12 @@ def partition_step(p: Partition, P, X_in, y, W, received_f: dict, received_g: di
         relu = l < L or o.relu_last
         if sage:
             G, Jf = layers.sage_backward(P, rec["A"][l], rec["X_in"][l], rec["Z"][l], J, W[l - 1], relu, l > 1,
-                                         o.gemm, layer_order(o, W[l - 1], sage), rec["X_full"][l])
+                                         o.gemm, layer_order(o, W[l - 1], sage), rec["X_full"][l],
+                                         mask=relu_masks.get(l))
         else:
             G, Jf = layers.layer_backward(P, rec["A"][l], rec["Z"][l], J, W[l - 1], relu, l > 1, o.gemm,
-                                          layer_order(o, W[l - 1], sage), rec["X_full"][l])
+                                          layer_order(o, W[l - 1], sage), rec["X_full"][l],
+                                          mask=relu_masks.get(l))
         rec["G"][l] = G
         if l == 1:
             break
