@@ -113,7 +113,7 @@ size_t pgcn::layer_fwd_workspace(const pgcn_partition *p, const pgcn_fwd_args *a
 }
 
 extern "C" size_t pgcn_layer_workspace_size(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype,
-                                            int32_t order) {
+                                            int32_t order) try {
   if (order == PGCN_ORDER_AGG) return pgcn_workspace_size(p, f_in, f_out, gemm_dtype);
   if (order != PGCN_ORDER_TRANSFORM || !p || f_in <= 0 || f_out <= 0) return 0;
   const size_t w = fwd_ws_tf(p, f_in, f_out, gemm_dtype);
@@ -121,15 +121,21 @@ extern "C" size_t pgcn_layer_workspace_size(const pgcn_partition *p, int32_t f_i
   const size_t l = align_up(loss_workspace(p->n_inner), 256);
   const size_t m = w > b ? w : b;
   return m > l ? m : l;
+} catch (...) {
+  (void)exception_status("pgcn_layer_workspace_size");
+  return 0;
 }
 
-extern "C" size_t pgcn_workspace_size(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) {
+extern "C" size_t pgcn_workspace_size(const pgcn_partition *p, int32_t f_in, int32_t f_out, int32_t gemm_dtype) try {
   if (!p || f_in <= 0 || f_out <= 0) return 0;
   size_t w = fwd_ws(p, f_in, f_out, gemm_dtype);
   size_t b = bwd_ws(p, f_in, f_out, true, gemm_dtype);
   size_t l = align_up(loss_workspace(p->n_inner), 256);
   size_t m = w > b ? w : b;
   return m > l ? m : l;
+} catch (...) {
+  (void)exception_status("pgcn_workspace_size");
+  return 0;
 }
 
 namespace {
@@ -287,7 +293,7 @@ int layer_bwd_transform(const pgcn_partition *p, const pgcn_bwd_args *a, hipStre
 
 }  // namespace
 
-extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, hipStream_t s) {
+extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, hipStream_t s) try {
   int rc = check_part(p, "pgcn_layer_fwd");
   if (rc) return rc;
   PGCN_REQUIRE(p->self_loop, "pgcn_layer_fwd: the GCN layer needs a partition built with self loops");
@@ -402,9 +408,11 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   if (bf16 && !a->A_bf16)           // bf16 path without the bf16 copy: A rounded while staged (same values)
     return launch_gemm_nk(a->relu ? Gemm::NN_SRC32_RELU : Gemm::NN_SRC32_PLAIN, m, s);
   return launch_gemm_nk(a->relu ? Gemm::NN_RELU : Gemm::NN_PLAIN, m, s);
+} catch (...) {
+  return exception_status("pgcn_layer_fwd");
 }
 
-extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, hipStream_t s) {
+extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, hipStream_t s) try {
   int rc = check_part(p, "pgcn_layer_bwd");
   if (rc) return rc;
   PGCN_REQUIRE(p->self_loop, "pgcn_layer_bwd: the GCN layer needs a partition built with self loops");
@@ -510,6 +518,8 @@ extern "C" int pgcn_layer_bwd(const pgcn_partition *p, const pgcn_bwd_args *a, h
   t.partials = partials;
   t.trace_kind = PGCN_TK_AGG_BWD;
   return launch_aggregate(t, s);
+} catch (...) {
+  return exception_status("pgcn_layer_bwd");
 }
 
 // ---------------------------------------------------------------- GraphSAGE ---
@@ -736,7 +746,7 @@ int sage_bwd_transform(const pgcn_partition *p, const pgcn_sage_bwd_args *a, hip
 
 }  // namespace
 
-extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_args *a, hipStream_t s) {
+extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_args *a, hipStream_t s) try {
   int rc = check_part(p, "pgcn_sage_layer_fwd");
   if (rc) return rc;
   PGCN_REQUIRE(!p->self_loop, "pgcn_sage_layer_fwd: the partition must be built with PGCN_SETUP_NO_SELF_LOOP");
@@ -813,9 +823,11 @@ extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_
   m.B = a->W + (size_t)a->f_in * a->f_out;
   set_send(m, p, a->send_out);
   return launch_gemm_nk(a->relu ? Gemm::NN_ACC_RELU : Gemm::NN_ACC_PLAIN, m, s);
+} catch (...) {
+  return exception_status("pgcn_sage_layer_fwd");
 }
 
-extern "C" int pgcn_sage_layer_bwd(const pgcn_partition *p, const pgcn_sage_bwd_args *a, hipStream_t s) {
+extern "C" int pgcn_sage_layer_bwd(const pgcn_partition *p, const pgcn_sage_bwd_args *a, hipStream_t s) try {
   int rc = check_part(p, "pgcn_sage_layer_bwd");
   if (rc) return rc;
   PGCN_REQUIRE(!p->self_loop, "pgcn_sage_layer_bwd: the partition must be built with PGCN_SETUP_NO_SELF_LOOP");
@@ -933,11 +945,13 @@ extern "C" int pgcn_sage_layer_bwd(const pgcn_partition *p, const pgcn_sage_bwd_
   t.trace_kind = PGCN_TK_AGG_BWD;
   t.accum_lo = 1;
   return launch_aggregate(t, s);
+} catch (...) {
+  return exception_status("pgcn_sage_layer_bwd");
 }
 
 extern "C" int pgcn_dropout(float *out, const float *in, int64_t rows, int32_t cols, int64_t ld, int64_t row0,
                             double p, uint32_t seed, uint32_t part, uint32_t layer, uint32_t iteration,
-                            uint16_t *out_bf16, int64_t ld_bf16, hipStream_t s) {
+                            uint16_t *out_bf16, int64_t ld_bf16, hipStream_t s) try {
   PGCN_REQUIRE(rows >= 0 && cols >= 0 && ld >= cols && ld % 4 == 0 && row0 >= 0, "pgcn_dropout: bad shape or stride");
   PGCN_REQUIRE(p >= 0.0 && p < 1.0, "pgcn_dropout: p must be in [0, 1)");
   if (rows == 0 || cols == 0) return PGCN_OK;
@@ -948,10 +962,12 @@ extern "C" int pgcn_dropout(float *out, const float *in, int64_t rows, int32_t c
   const uint32_t thr = t >= 4294967295.0 ? 0xffffffffu : (uint32_t)t;
   const float scale = (float)(1.0 / (1.0 - p));
   return launch_dropout(out, in, rows, cols, ld, row0, thr, scale, seed, part, layer, iteration, out_bf16, ld_bf16, s);
+} catch (...) {
+  return exception_status("pgcn_dropout");
 }
 
 extern "C" int pgcn_adam_update(float *W, const float *G, const float *G_peer, float *m, float *v, int64_t count,
-                                double lr, double beta1, double beta2, double eps, int32_t t, hipStream_t s) {
+                                double lr, double beta1, double beta2, double eps, int32_t t, hipStream_t s) try {
   PGCN_REQUIRE(count >= 0 && t >= 1, "pgcn_adam_update: count must be >= 0 and t >= 1");
   PGCN_REQUIRE(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0, "pgcn_adam_update: betas must be in [0, 1)");
   if (count == 0) return PGCN_OK;
@@ -966,19 +982,23 @@ extern "C" int pgcn_adam_update(float *W, const float *G, const float *G_peer, f
   c.c1 = (float)(1.0 / (1.0 - std::pow(beta1, (double)t)));
   c.c2 = (float)(1.0 / (1.0 - std::pow(beta2, (double)t)));
   return launch_adam(W, G, G_peer, m, v, count, c, s);
+} catch (...) {
+  return exception_status("pgcn_adam_update");
 }
 
 extern "C" int pgcn_smooth_ema(float *state, const float *incoming, int64_t rows, int32_t cols, int64_t ld,
-                               float gamma, hipStream_t s) {
+                               float gamma, hipStream_t s) try {
   PGCN_REQUIRE(rows >= 0 && cols >= 0 && ld >= cols && ld % 4 == 0, "pgcn_smooth_ema: bad shape or stride");
   if (rows == 0 || cols == 0) return PGCN_OK;
   PGCN_REQUIRE(state && incoming && aligned16(state) && aligned16(incoming),
                "pgcn_smooth_ema: null or unaligned buffer");
   return launch_ema(state, incoming, rows, cols, ld, gamma, s);
+} catch (...) {
+  return exception_status("pgcn_smooth_ema");
 }
 
 extern "C" int pgcn_pack_boundary(const pgcn_partition *p, int32_t kind, const float *src, float *dst, int32_t cols,
-                                  int64_t ld, hipStream_t s) {
+                                  int64_t ld, hipStream_t s) try {
   int rc = check_part(p, "pgcn_pack_boundary");
   if (rc) return rc;
   PGCN_REQUIRE(kind == PGCN_PACK_FEAT || kind == PGCN_ACCUM_GRAD, "pgcn_pack_boundary: bad kind");
@@ -987,10 +1007,12 @@ extern "C" int pgcn_pack_boundary(const pgcn_partition *p, int32_t kind, const f
   PGCN_REQUIRE(src && dst && aligned16(src) && aligned16(dst), "pgcn_pack_boundary: null or unaligned buffer");
   if (kind == PGCN_PACK_FEAT) return launch_pack(p->d_send_idx, p->n_send, src, dst, cols, ld, s);
   return launch_accum(p->d_inv_ptr, p->d_inv_k, p->n_inner, src, dst, cols, ld, s);
+} catch (...) {
+  return exception_status("pgcn_pack_boundary");
 }
 
 extern "C" int pgcn_accum_smoothed(const pgcn_partition *p, const float *incoming, float *state, float gamma,
-                                   float *dst, int32_t cols, int64_t ld, hipStream_t s) {
+                                   float *dst, int32_t cols, int64_t ld, hipStream_t s) try {
   int rc = check_part(p, "pgcn_accum_smoothed");
   if (rc) return rc;
   PGCN_REQUIRE(cols >= 0 && ld >= cols && ld % 4 == 0, "pgcn_accum_smoothed: bad shape or stride");
@@ -1000,11 +1022,13 @@ extern "C" int pgcn_accum_smoothed(const pgcn_partition *p, const float *incomin
                "pgcn_accum_smoothed: null or unaligned buffer");
   PGCN_REQUIRE(state != incoming && state != dst, "pgcn_accum_smoothed: state aliases another buffer");
   return launch_accum_ema(p->d_inv_ptr, p->d_inv_k, p->n_inner, incoming, state, gamma, dst, cols, ld, s);
+} catch (...) {
+  return exception_status("pgcn_accum_smoothed");
 }
 
 extern "C" int pgcn_loss_fwd_bwd(int32_t kind, const float *Z, int64_t rows, int32_t classes, int64_t ld,
                                  const int32_t *labels, const float *targets, int64_t ld_t, float scale, float *J,
-                                 float *loss_out, void *workspace, size_t workspace_bytes, hipStream_t s) {
+                                 float *loss_out, void *workspace, size_t workspace_bytes, hipStream_t s) try {
   PGCN_REQUIRE(kind == PGCN_SOFTMAX_CE || kind == PGCN_SIGMOID_BCE, "pgcn_loss_fwd_bwd: bad kind");
   PGCN_REQUIRE(rows >= 0 && classes >= 1 && ld >= classes, "pgcn_loss_fwd_bwd: bad shape or stride");
   PGCN_REQUIRE(loss_out, "pgcn_loss_fwd_bwd: null loss_out");
@@ -1016,17 +1040,21 @@ extern "C" int pgcn_loss_fwd_bwd(int32_t kind, const float *Z, int64_t rows, int
   if (!workspace || workspace_bytes < loss_workspace(rows))
     return set_error(PGCN_EWORKSPACE, "pgcn_loss_fwd_bwd: workspace too small");
   return launch_loss(kind, Z, rows, classes, ld, labels, targets, ld_t, scale, J, loss_out, (float *)workspace, s);
+} catch (...) {
+  return exception_status("pgcn_loss_fwd_bwd");
 }
 
 extern "C" int pgcn_sgd_update(float *W, const float *G, const float *G_peer, int64_t count, float eta,
-                               hipStream_t s) {
+                               hipStream_t s) try {
   PGCN_REQUIRE(count >= 0, "pgcn_sgd_update: negative count");
   if (count == 0) return PGCN_OK;
   PGCN_REQUIRE(W && G, "pgcn_sgd_update: null W or G");
   return launch_sgd(W, G, G_peer, count, eta, s);
+} catch (...) {
+  return exception_status("pgcn_sgd_update");
 }
 
-extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, hipStream_t s) {
+extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, hipStream_t s) try {
   if (bytes == 0) return PGCN_OK;
   PGCN_REQUIRE(dst && src, "pgcn_refill_async: null buffer");
   PGCN_REQUIRE((flags & ~(uint32_t)(PGCN_REFILL_DMA | PGCN_REFILL_FROM_HOST)) == 0, "pgcn_refill_async: unknown flags");
@@ -1043,4 +1071,6 @@ extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint3
   TraceScope ts(PGCN_TK_REFILL, s);
   PGCN_HIP(hipMemcpyAsync(dst, src, bytes, (flags & PGCN_REFILL_DMA) ? hipMemcpyDeviceToDeviceNoCU : hipMemcpyDeviceToDevice, s));
   return PGCN_OK;
+} catch (...) {
+  return exception_status("pgcn_refill_async");
 }

@@ -85,7 +85,10 @@ inline const Plan &agg_plan(const pgcn_partition *p, bool transposed, int64_t f)
   return transposed ? p->plan_t : p->plan;
 }
 
-int set_error(int code, const std::string &msg);
+int set_error(int code, const std::string &msg) noexcept;
+// The status of an exception caught at an entry point (call from a catch handler): no C++
+// exception crosses the C interface; std::bad_alloc is PGCN_ENOMEM, anything else PGCN_EINVAL.
+int exception_status(const char *fn) noexcept;
 
 // Workspace bytes one pgcn_layer_fwd call needs (0 for arguments it rejects).
 size_t layer_fwd_workspace(const pgcn_partition *p, const pgcn_fwd_args *a);

@@ -46,7 +46,7 @@ int noalloc_scratch_init(int dev) {
 
 using namespace pgcn;
 
-extern "C" int pgcn_layer_fwd_noalloc(const pgcn_partition *p, const pgcn_fwd_args *a, hipStream_t s) {
+extern "C" int pgcn_layer_fwd_noalloc(const pgcn_partition *p, const pgcn_fwd_args *a, hipStream_t s) try {
   PGCN_REQUIRE(p && a, "pgcn_layer_fwd_noalloc: null partition or args");
   PGCN_REQUIRE(!p->host_only, "pgcn_layer_fwd_noalloc: partition was built host-only");
   PGCN_REQUIRE(!a->workspace && a->workspace_bytes == 0,
@@ -70,4 +70,6 @@ extern "C" int pgcn_layer_fwd_noalloc(const pgcn_partition *p, const pgcn_fwd_ar
   b.workspace = ptr;
   b.workspace_bytes = (size_t)PGCN_NOALLOC_SCRATCH_BYTES;
   return pgcn_layer_fwd(p, &b, s);
+} catch (...) {
+  return exception_status("pgcn_layer_fwd_noalloc");
 }

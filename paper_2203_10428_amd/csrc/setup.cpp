@@ -6,16 +6,50 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <memory>
+#include <new>
 #include <numeric>
+#include <utility>
 
 #include "internal.h"
 
 namespace pgcn {
 
 static thread_local std::string g_error;
+// Set when the message itself could not be stored (out of host memory).
+static thread_local const char *g_error_static = nullptr;
 
-int set_error(int code, const std::string &msg) {
-  g_error = msg;
+int set_error(int code, const std::string &msg) noexcept {
+  try {
+    g_error = msg;
+    g_error_static = nullptr;
+  } catch (...) {
+    g_error_static = "libpgcn: out of host memory while reporting an error";
+  }
+  return code;
+}
+
+static void set_message(const char *fn, const char *what) noexcept {
+  try {
+    g_error = std::string(fn) + ": " + what;
+    g_error_static = nullptr;
+  } catch (...) {
+    g_error_static = "libpgcn: out of host memory while reporting an error";
+  }
+}
+
+int exception_status(const char *fn) noexcept {
+  int code = PGCN_EINVAL;
+  try {
+    throw;
+  } catch (const std::bad_alloc &) {
+    code = PGCN_ENOMEM;
+    set_message(fn, "out of host memory");
+  } catch (const std::exception &e) {
+    set_message(fn, e.what());
+  } catch (...) {
+    set_message(fn, "unexpected C++ exception");
+  }
   return code;
 }
 
@@ -141,6 +175,36 @@ static void free_device(pgcn_partition *p) {
   p->plan.d_splits = p->plan_t.d_splits = p->plan_n.d_splits = p->plan_tn.d_splits = nullptr;
 }
 
+// The graph must be undirected: v lists u exactly when u lists v (self loops
+// and repeated entries ignored).  Compares every row with the same row of the
+// transpose, both sorted and deduplicated.
+static bool graph_is_symmetric(int64_t n, const int64_t *rp, const int32_t *cl) {
+  std::vector<int64_t> tp(n + 1, 0);
+  for (int64_t v = 0; v < n; ++v)
+    for (int64_t k = rp[v]; k < rp[v + 1]; ++k)
+      if (cl[k] != v) tp[cl[k] + 1]++;
+  for (int64_t v = 0; v < n; ++v) tp[v + 1] += tp[v];
+  std::vector<int32_t> tc(tp[n]);
+  {
+    std::vector<int64_t> fill(tp.begin(), tp.end() - 1);
+    for (int64_t v = 0; v < n; ++v)           // rows visited in ascending v: transposed rows come out sorted
+      for (int64_t k = rp[v]; k < rp[v + 1]; ++k)
+        if (cl[k] != v) tc[fill[cl[k]]++] = (int32_t)v;
+  }
+  std::vector<int32_t> row;
+  for (int64_t v = 0; v < n; ++v) {
+    row.clear();
+    for (int64_t k = rp[v]; k < rp[v + 1]; ++k)
+      if (cl[k] != v) row.push_back(cl[k]);
+    std::sort(row.begin(), row.end());
+    row.erase(std::unique(row.begin(), row.end()), row.end());
+    auto tb = tc.begin() + tp[v], te = tc.begin() + tp[v + 1];
+    te = std::unique(tb, te);
+    if ((int64_t)row.size() != (int64_t)(te - tb) || !std::equal(row.begin(), row.end(), tb)) return false;
+  }
+  return true;
+}
+
 static int check_device() {
   int dev = 0;
   PGCN_HIP(hipGetDevice(&dev));
@@ -165,7 +229,7 @@ static int default_segment() {
 using namespace pgcn;
 
 extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map *bmap, uint32_t flags,
-                                    pgcn_partition **out) {
+                                    pgcn_partition **out) try {
   PGCN_REQUIRE(csr && bmap && out, "pgcn_partition_setup: null argument");
   *out = nullptr;
   const int64_t n = csr->n;
@@ -189,12 +253,22 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
     PGCN_REQUIRE(cl[k] >= 0 && cl[k] < n, "pgcn_partition_setup: column out of range");
   for (int64_t v = 0; v < n; ++v)
     PGCN_REQUIRE(owner[v] >= 0 && owner[v] < nparts, "pgcn_partition_setup: owner out of range");
+  PGCN_REQUIRE(graph_is_symmetric(n, rp, cl),
+               "pgcn_partition_setup: the graph is not symmetric (some v lists u but u does not list v)");
   if (!(flags & PGCN_SETUP_HOST_ONLY)) {
     int rc = check_device();
     if (rc) return rc;
   }
 
-  pgcn_partition *p = new (std::nothrow) pgcn_partition();
+  // owned here until it is handed out: every early return frees it (device arrays included)
+  struct Release {
+    void operator()(pgcn_partition *q) const noexcept {
+      if (!q->host_only) free_device(q);
+      delete q;
+    }
+  };
+  std::unique_ptr<pgcn_partition, Release> holder(new (std::nothrow) pgcn_partition());
+  pgcn_partition *p = holder.get();
   if (!p) return set_error(PGCN_ENOMEM, "pgcn_partition_setup: out of host memory");
   p->nparts = nparts;
   p->self = self;
@@ -305,21 +379,25 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
   // S_{i,j} = B_j ∩ V_i: inner u adjacent to some w owned by j (w's row lists u)
   p->send_ptr.assign(nparts + 1, 0);
   {
-    std::vector<uint8_t> mark((size_t)nparts * (size_t)n_in, 0);
+    // (j, local u) for every edge from a node w owned by j != self to an inner u; sorted and
+    // deduplicated, this is S_{i,j} for ascending j, each by ascending local (= global) id
+    std::vector<std::pair<int32_t, int32_t>> su;
     for (int64_t w = 0; w < n; ++w) {
       int32_t j = owner[w];
       if (j == self) continue;
       for (int64_t k = rp[w]; k < rp[w + 1]; ++k) {
         int32_t u = cl[k];
-        if (u != w && owner[u] == self) mark[(size_t)j * n_in + local_of[u]] = 1;
+        if (u != w && owner[u] == self) su.emplace_back(j, (int32_t)local_of[u]);
       }
     }
-    for (int32_t j = 0; j < nparts; ++j) {
-      if (j != self)
-        for (int64_t u = 0; u < n_in; ++u)
-          if (mark[(size_t)j * n_in + u]) p->send_idx.push_back((int32_t)u);
-      p->send_ptr[j + 1] = (int64_t)p->send_idx.size();
+    std::sort(su.begin(), su.end());
+    su.erase(std::unique(su.begin(), su.end()), su.end());
+    p->send_idx.reserve(su.size());
+    for (const auto &e : su) {
+      p->send_idx.push_back(e.second);
+      p->send_ptr[e.first + 1]++;
     }
+    for (int32_t j = 0; j < nparts; ++j) p->send_ptr[j + 1] += p->send_ptr[j];
   }
   p->n_send = (int64_t)p->send_idx.size();
 
@@ -363,19 +441,17 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
     if (!rc) rc = upload(&p->plan_n.d_splits, p->plan_n.splits);
     if (!rc) rc = upload(&p->plan_tn.d_items, p->plan_tn.items);
     if (!rc) rc = upload(&p->plan_tn.d_splits, p->plan_tn.splits);
-    if (rc) {
-      free_device(p);
-      delete p;
-      return rc;
-    }
+    if (rc) return rc;
     p->d_row_scale = p->symmetric ? p->d_sym_scale : p->d_inv_deg;
     p->d_col_scale = p->symmetric ? p->d_sym_scale : nullptr;
   }
-  *out = p;
+  *out = holder.release();
   return PGCN_OK;
+} catch (...) {
+  return exception_status("pgcn_partition_setup");
 }
 
-extern "C" int pgcn_partition_info(const pgcn_partition *p, pgcn_info *o) {
+extern "C" int pgcn_partition_info(const pgcn_partition *p, pgcn_info *o) try {
   PGCN_REQUIRE(p && o, "pgcn_partition_info: null argument");
   o->n_inner = p->n_inner;
   o->n_bd = p->n_bd;
@@ -398,6 +474,8 @@ extern "C" int pgcn_partition_info(const pgcn_partition *p, pgcn_info *o) {
   o->symmetric = p->symmetric;
   o->self_loop = p->self_loop;
   return PGCN_OK;
+} catch (...) {
+  return exception_status("pgcn_partition_info");
 }
 
 template <class T>
@@ -405,7 +483,7 @@ static void copy_out(T *dst, const std::vector<T> &src) {
   if (dst && !src.empty()) std::memcpy(dst, src.data(), src.size() * sizeof(T));
 }
 
-extern "C" int pgcn_partition_export(const pgcn_partition *p, const pgcn_arrays *h) {
+extern "C" int pgcn_partition_export(const pgcn_partition *p, const pgcn_arrays *h) try {
   PGCN_REQUIRE(p && h, "pgcn_partition_export: null argument");
   copy_out(h->inner_gid, p->inner_gid);
   copy_out(h->bd_gid, p->bd_gid);
@@ -420,14 +498,18 @@ extern "C" int pgcn_partition_export(const pgcn_partition *p, const pgcn_arrays 
   copy_out(h->inv_k, p->inv_k);
   copy_out(h->deg, p->deg);
   return PGCN_OK;
+} catch (...) {
+  return exception_status("pgcn_partition_export");
 }
 
-extern "C" void pgcn_partition_destroy(pgcn_partition *p) {
+extern "C" void pgcn_partition_destroy(pgcn_partition *p) try {
   if (!p) return;
   if (!p->host_only) free_device(p);
   delete p;
+} catch (...) {
+  (void)exception_status("pgcn_partition_destroy");
 }
 
-extern "C" const char *pgcn_last_error(void) { return g_error.c_str(); }
+extern "C" const char *pgcn_last_error(void) { return g_error_static ? g_error_static : g_error.c_str(); }
 
 extern "C" int pgcn_version(void) { return PGCN_VERSION; }

@@ -54,7 +54,7 @@ TraceScope::~TraceScope() {
 
 using namespace pgcn;
 
-extern "C" int pgcn_trace_enable(int32_t capacity) {
+extern "C" int pgcn_trace_enable(int32_t capacity) try {
   PGCN_REQUIRE(capacity > 0 && capacity <= (1 << 20), "pgcn_trace_enable: capacity out of range");
   TraceState &t = state();
   std::lock_guard<std::mutex> g(t.mu);
@@ -72,17 +72,21 @@ extern "C" int pgcn_trace_enable(int32_t capacity) {
   t.mask = 0xffffffffu;
   t.on = true;
   return PGCN_OK;
+} catch (...) {
+  return exception_status("pgcn_trace_enable");
 }
 
-extern "C" int pgcn_trace_filter(uint32_t kind_mask) {
+extern "C" int pgcn_trace_filter(uint32_t kind_mask) try {
   TraceState &t = state();
   std::lock_guard<std::mutex> g(t.mu);
   t.mask = kind_mask;
   return PGCN_OK;
+} catch (...) {
+  return exception_status("pgcn_trace_filter");
 }
 
 extern "C" int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t *launches, int32_t max_records,
-                                  int32_t *count) {
+                                  int32_t *count) try {
   PGCN_REQUIRE(count && max_records >= 0 && (max_records == 0 || (kinds && ms)), "pgcn_trace_collect: bad arguments");
   TraceState &t = state();
   std::lock_guard<std::mutex> g(t.mu);
@@ -98,12 +102,16 @@ extern "C" int pgcn_trace_collect(int32_t *kinds, float *ms, int32_t *launches, 
   *count = n;
   t.used = 0;
   return PGCN_OK;
+} catch (...) {
+  return exception_status("pgcn_trace_collect");
 }
 
-extern "C" int pgcn_trace_disable(void) {
+extern "C" int pgcn_trace_disable(void) try {
   TraceState &t = state();
   std::lock_guard<std::mutex> g(t.mu);
   t.on = false;
   t.used = 0;
   return PGCN_OK;
+} catch (...) {
+  return exception_status("pgcn_trace_disable");
 }

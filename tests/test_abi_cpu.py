@@ -6,6 +6,7 @@ import ctypes as C
 import os
 import re
 import subprocess
+import sys
 
 import numpy as np
 import pytest
@@ -130,7 +131,8 @@ def test_setup_heavy_rows_are_split_into_fixed_segments():
     assert info["spmm_split_slots"] >= 2
 
 
-@pytest.mark.parametrize("bad", ["rowptr0", "decreasing", "col_range", "owner_range", "self_range"])
+@pytest.mark.parametrize("bad", ["rowptr0", "decreasing", "col_range", "owner_range", "self_range", "asymmetric",
+                                 "asymmetric_duplicate"])
 def test_setup_rejects_bad_input(bad):
     n = 4
     rowptr = np.array([0, 1, 2, 3, 4], np.int64)
@@ -145,12 +147,56 @@ def test_setup_rejects_bad_input(bad):
         col = np.array([1, 0, 7, 2], np.int32)
     elif bad == "owner_range":
         owner = np.array([0, 0, 2, 1], np.int32)
+    elif bad == "asymmetric":                   # 2 lists 1, 1 does not list 2
+        rowptr = np.array([0, 1, 2, 4, 5], np.int64)
+        col = np.array([1, 0, 3, 1, 2], np.int32)
+    elif bad == "asymmetric_duplicate":         # a repeated entry does not stand in for the reverse edge
+        rowptr = np.array([0, 2, 3, 4, 5], np.int64)
+        col = np.array([1, 2, 0, 3, 2], np.int32)
     else:
         part = 2
     with pytest.raises(B.PgcnError) as e:
         B.pgcn_partition_setup(n, rowptr, col, owner, nparts, part, host_only=True)
     assert e.value.code == B.PGCN_EINVAL
     assert B.pgcn_last_error()
+    if bad.startswith("asymmetric"):
+        assert "not symmetric" in B.pgcn_last_error()
+
+
+def test_setup_accepts_duplicates_and_self_loops():
+    # a symmetric graph listed with repeated entries and self loops (both are canonicalised)
+    rowptr = np.array([0, 3, 5, 7, 8], np.int64)
+    col = np.array([1, 1, 0, 0, 1, 3, 2, 2], np.int32)
+    owner = np.array([0, 0, 1, 1], np.int32)
+    h = B.pgcn_partition_setup(4, rowptr, col, owner, 2, 0, host_only=True)
+    assert B.pgcn_partition_info(h)["nnz"] == 4          # rows {0, 1} and {0, 1} with their self loops
+
+
+def test_out_of_host_memory_is_a_status_not_an_abort():
+    """A host allocation that fails inside set-up comes back as PGCN_ENOMEM (no C++ exception
+    crosses the C interface).  Run in a child process whose address space is capped just above
+    what it holds, on a graph whose set-up needs a few hundred MB more."""
+    import textwrap
+    code = textwrap.dedent("""
+        import resource, sys
+        import numpy as np
+        sys.path.insert(0, %r)
+        from paper_2203_10428_amd import binding as B
+        n = 50_000_000
+        rowptr = np.zeros(n + 1, np.int64)
+        owner = np.zeros(n, np.int32)
+        col = np.zeros(1, np.int32)
+        vm = [int(l.split()[1]) for l in open("/proc/self/status") if l.startswith("VmSize:")][0] * 1024
+        resource.setrlimit(resource.RLIMIT_AS, (vm + (128 << 20), vm + (128 << 20)))
+        try:
+            B.pgcn_partition_setup(n, rowptr, col, owner, 1, 0, host_only=True)
+            print("no error")
+        except B.PgcnError as e:
+            print("status", e.code, B.pgcn_last_error())
+    """ % os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert f"status {B.PGCN_ENOMEM} pgcn_partition_setup: out of host memory" in r.stdout, r.stdout + r.stderr[-2000:]
 
 
 def test_setup_symmetric_flag():
@@ -199,7 +245,7 @@ def test_noalloc_scratch_limit_matches_the_header():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["reddit-like-1of4", "yelp-like-1of3"])
+@pytest.mark.parametrize("name", ["reddit-like-1of4", "products-like-1of8", "yelp-like-1of3", "stress-rmat-2M"])
 def test_setup_bit_exact_full_size(name):
     w = configs.WORKLOADS[name]
     g = configs.make_graph(w)
