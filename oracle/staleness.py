@@ -34,17 +34,21 @@ def _rel(pairs):
     return np.sqrt(num / den) if den > 0 else np.sqrt(num)
 
 
-def staleness_errors(n, rowptr, col, owner, nparts, X, labels, W0, T, opts: Options, vanilla_g: bool = True):
-    """Per iteration t >= 2: {"feat": {l: err}, "grad": {l: err}, "G": err} (G only with vanilla_g)."""
+def staleness_errors(n, rowptr, col, owner, nparts, X, labels, W0, T, opts: Options, vanilla_g: bool = True,
+                     parts=None):
+    """Per iteration t >= 2: {"feat": {l: err}, "grad": {l: err}, "G": err} (G only with vanilla_g).
+    ``parts``: the partitions whose received rows enter the feature and gradient errors (all by
+    default; one partition gives that partition's share, e.g. to check one device's buffers)."""
     assert opts.mode == "pipe"
     sim, recs = run(n, rowptr, col, owner, nparts, X, labels, W0, T, opts)
     L = sim.L
+    parts = range(nparts) if parts is None else parts
     out = []
     for t in range(2, T + 1):
         rec = recs[t - 1]
-        feat = {l: _rel([(rec[i]["H_bd_used"][l], rec[i]["state_out"].feat_buf[l]) for i in range(nparts)])
+        feat = {l: _rel([(rec[i]["H_bd_used"][l], rec[i]["state_out"].feat_buf[l]) for i in parts])
                 for l in range(1, L + 1)}
-        grad = {l: _rel([(rec[i]["C_used"][l], rec[i]["state_out"].grad_buf[l]) for i in range(nparts)])
+        grad = {l: _rel([(rec[i]["C_used"][l], rec[i]["state_out"].grad_buf[l]) for i in parts])
                 for l in range(2, L + 1)}
         row = {"t": t, "feat": feat, "grad": grad}
         if vanilla_g:

@@ -59,3 +59,22 @@ def test_weight_gradient_error_scales_with_the_learning_rate(model):
         errs.append(np.mean([r["G"] for r in rows if r["t"] >= 4]))
     assert 5.0 < errs[1] / errs[0] < 20.0, errs
     assert 5.0 < errs[2] / errs[1] < 20.0, errs
+
+
+def test_per_partition_errors_combine_into_the_total():
+    """The error over all partitions is the root of the den-weighted mean of the per-partition squared
+    errors, so it lies between them; both partitions together give the default."""
+    graph = tiny()
+    w = configs.TINY
+    d = configs.make_dense(w, graph[0])
+    o = Options(smooth_f=True, smooth_g=True, gamma=0.5, eta=0.2, loss_scale=1.0 / graph[0])
+    all_ = staleness_errors(*graph, d.X, d.labels, d.W, 4, o, vanilla_g=False)
+    both = staleness_errors(*graph, d.X, d.labels, d.W, 4, o, vanilla_g=False, parts=(0, 1))
+    p0 = staleness_errors(*graph, d.X, d.labels, d.W, 4, o, vanilla_g=False, parts=(0,))
+    p1 = staleness_errors(*graph, d.X, d.labels, d.W, 4, o, vanilla_g=False, parts=(1,))
+    for ra, rb, r0, r1 in zip(all_, both, p0, p1):
+        assert ra["feat"] == rb["feat"] and ra["grad"] == rb["grad"]
+        for kind in ("feat", "grad"):
+            for l, e in ra[kind].items():
+                lo, hi = sorted((r0[kind][l], r1[kind][l]))
+                assert lo - 1e-15 <= e <= hi + 1e-15, (kind, l, lo, e, hi)
