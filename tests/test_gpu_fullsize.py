@@ -144,6 +144,8 @@ def test_forward_layers_full_size(name):
             Z_ref = A_ref @ Wd
             assert rel(A_gpu, A_ref) < 1e-5
         assert rel(H_gpu, np.maximum(Z_ref, 0)) < tol, (name, layer)
+        if dt == B.PGCN_BF16:                            # and the plain fp64 oracle, same tolerance
+            assert rel(H_gpu, np.maximum(A_ref @ Wd, 0)) < tol, (name, layer, "fp64")
         del dH_in, dH_bd, A, A16, H, ws
 
 
@@ -173,37 +175,38 @@ def test_backward_layer_full_size(name):
                      W=torch.from_numpy(W).cuda(), dW=dG, J_in=J_in, J_bd_out=J_bd, workspace=ws,
                      workspace_bytes=nb)
     torch.cuda.synchronize()
-    M = J.astype(np.float64) * (Hout > 0)
-    Wd = W.astype(np.float64)
+    M0 = J.astype(np.float64) * (Hout > 0)
+    W0 = W.astype(np.float64)
     Ad = A.astype(np.float64)
-    if dt == B.PGCN_BF16:
-        M, Wd = round_bf16(M), round_bf16(Wd)
     cols = rng.choice(f_out, 6, replace=False)
-    G_ref = Ad.T @ M[:, cols]
-    assert rel(dG.cpu().numpy()[:, cols], G_ref) < tol, name
-    # transposed aggregation on sampled inner and boundary rows
     d_inner = F.deg[F.inner] + 1
-
-    def D_rows(local):                                   # (M W^T)[v] / d_v for inner local rows
-        return (M[local] @ Wd.T) / d_inner[local][:, None]
-
     rows_in = F.sample_inner(24, 5)
-    ref_in = np.zeros((len(rows_in), f_in))
-    for k, r in enumerate(rows_in):
-        gid = F.inner[r]
-        vs = F.local_inner[F.neighbours(gid)]
-        vs = np.concatenate([vs[vs >= 0], [r]])
-        ref_in[k] = D_rows(vs).sum(0)
-    got_in = J_in[torch.from_numpy(rows_in).cuda(), :f_in].cpu().numpy()
-    assert rel(got_in, ref_in) < tol, name
     rows_bd = np.unique(np.concatenate([rng.choice(F.b, 24, replace=False),
                                         np.argsort(-F.deg[F.bd])[:2]]))
-    ref_bd = np.zeros((len(rows_bd), f_in))
-    for k, r in enumerate(rows_bd):
-        vs = F.local_inner[F.neighbours(F.bd[r])]
-        ref_bd[k] = D_rows(vs[vs >= 0]).sum(0)
+    got_G = dG.cpu().numpy()[:, cols]
+    got_in = J_in[torch.from_numpy(rows_in).cuda(), :f_in].cpu().numpy()
     got_bd = J_bd[torch.from_numpy(rows_bd).cuda(), :f_in].cpu().numpy()
-    assert rel(got_bd, ref_bd) < tol, name
+    # bf16: the bf16-operand reading (M and W rounded) and the plain fp64 oracle, same tolerance
+    for rounded in ((True, False) if dt == B.PGCN_BF16 else (False,)):
+        M, Wd = (round_bf16(M0), round_bf16(W0)) if rounded else (M0, W0)
+        assert rel(got_G, Ad.T @ M[:, cols]) < tol, (name, rounded)
+
+        def D_rows(local):                               # (M W^T)[v] / d_v for inner local rows
+            return (M[local] @ Wd.T) / d_inner[local][:, None]
+
+        # transposed aggregation on sampled inner and boundary rows
+        ref_in = np.zeros((len(rows_in), f_in))
+        for k, r in enumerate(rows_in):
+            gid = F.inner[r]
+            vs = F.local_inner[F.neighbours(gid)]
+            vs = np.concatenate([vs[vs >= 0], [r]])
+            ref_in[k] = D_rows(vs).sum(0)
+        assert rel(got_in, ref_in) < tol, (name, rounded)
+        ref_bd = np.zeros((len(rows_bd), f_in))
+        for k, r in enumerate(rows_bd):
+            vs = F.local_inner[F.neighbours(F.bd[r])]
+            ref_bd[k] = D_rows(vs[vs >= 0]).sum(0)
+        assert rel(got_bd, ref_bd) < tol, (name, rounded)
 
 
 @pytest.mark.parametrize("order", ["agg", "auto"])
@@ -260,15 +263,17 @@ def test_transform_forward_full_size(name):
         torch.cuda.synchronize()
         rows = F.sample_inner(48, layer + 7)
         H_gpu = H[torch.from_numpy(rows).cuda(), :f_out].cpu().numpy()
-        Hd = round_bf16(Hg) if dt == B.PGCN_BF16 else Hg.astype(np.float64)
-        Wd = round_bf16(W) if dt == B.PGCN_BF16 else W.astype(np.float64)
-        Z_ref = np.zeros((len(rows), f_out))
-        for k, r in enumerate(rows):
-            gid = F.inner[r]
-            nbrs = F.neighbours(gid)
-            Z_ref[k] = ((Hd[gid] + Hd[nbrs].sum(0)) @ Wd) / (len(nbrs) + 1)
-        ref = np.maximum(Z_ref, 0) if relu else Z_ref
-        assert rel(H_gpu, ref) < tol, (name, layer)
+        # bf16: the bf16-operand reading (H and W rounded) and the plain fp64 oracle, same tolerance
+        for rounded in ((True, False) if dt == B.PGCN_BF16 else (False,)):
+            Hd = round_bf16(Hg) if rounded else Hg.astype(np.float64)
+            Wd = round_bf16(W) if rounded else W.astype(np.float64)
+            Z_ref = np.zeros((len(rows), f_out))
+            for k, r in enumerate(rows):
+                gid = F.inner[r]
+                nbrs = F.neighbours(gid)
+                Z_ref[k] = ((Hd[gid] + Hd[nbrs].sum(0)) @ Wd) / (len(nbrs) + 1)
+            ref = np.maximum(Z_ref, 0) if relu else Z_ref
+            assert rel(H_gpu, ref) < tol, (name, layer, rounded)
         del H, ws
 
 
@@ -295,15 +300,18 @@ def test_transform_backward_full_size(name):
                      workspace_bytes=nb, order=B.PGCN_ORDER_TRANSFORM, H_in=upload(H_full[:F.n]),
                      H_bd=upload(H_full[F.n:]))
     torch.cuda.synchronize()
-    T = F.propagation_t() @ J.astype(np.float64)          # no ReLU on the last layer: M = J
-    Hd, Wd = H_full.astype(np.float64), W.astype(np.float64)
-    if dt == B.PGCN_BF16:
-        T, Hd, Wd = round_bf16(T), round_bf16(Hd), round_bf16(Wd)
+    T0 = F.propagation_t() @ J.astype(np.float64)         # no ReLU on the last layer: M = J
     cols = rng.choice(f_out, 6, replace=False)
-    assert rel(dG.cpu().numpy()[:, cols], Hd.T @ T[:, cols]) < tol, name
     rows_in = F.sample_inner(24, 13)
-    got_in = J_in[torch.from_numpy(rows_in).cuda(), :f_in].cpu().numpy()
-    assert rel(got_in, T[rows_in] @ Wd.T) < tol, name
     rows_bd = np.unique(np.concatenate([rng.choice(F.b, 24, replace=False), np.argsort(-F.deg[F.bd])[:2]]))
+    got_G = dG.cpu().numpy()[:, cols]
+    got_in = J_in[torch.from_numpy(rows_in).cuda(), :f_in].cpu().numpy()
     got_bd = J_bd[torch.from_numpy(rows_bd).cuda(), :f_in].cpu().numpy()
-    assert rel(got_bd, T[F.n + rows_bd] @ Wd.T) < tol, name
+    # bf16: the bf16-operand reading (T, H, W rounded) and the plain fp64 oracle, same tolerance
+    for rounded in ((True, False) if dt == B.PGCN_BF16 else (False,)):
+        T, Hd, Wd = T0, H_full.astype(np.float64), W.astype(np.float64)
+        if rounded:
+            T, Hd, Wd = round_bf16(T), round_bf16(Hd), round_bf16(Wd)
+        assert rel(got_G, Hd.T @ T[:, cols]) < tol, (name, rounded)
+        assert rel(got_in, T[rows_in] @ Wd.T) < tol, (name, rounded)
+        assert rel(got_bd, T[F.n + rows_bd] @ Wd.T) < tol, (name, rounded)

@@ -117,6 +117,8 @@ def test_sage_forward_full_size(name):
         Z_ref = Xc @ Wd
         assert rel(z_gpu, z_ref) < 1e-5
     assert rel(H_gpu, np.maximum(Z_ref, 0)) < TOL["bf16" if bf16 else "f32"]["act"], name
+    if bf16:                                             # and the plain fp64 oracle, same tolerance
+        assert rel(H_gpu, np.maximum(Xc @ Wd, 0)) < TOL["bf16"]["act"], (name, "fp64")
 
 
 @pytest.mark.parametrize("name", WORKLOADS)
@@ -147,33 +149,35 @@ def test_sage_backward_full_size(name):
                           W=torch.from_numpy(W).cuda(), dW=dG, J_in=J_in, J_bd_out=J_bd, workspace=ws,
                           workspace_bytes=nb)
     torch.cuda.synchronize()
-    M = J.astype(np.float64) * (Hout > 0)
-    Wd = W.astype(np.float64)
-    if bf16:
-        M, Wd = round_bf16(M), round_bf16(Wd)
+    M0 = J.astype(np.float64) * (Hout > 0)
+    W0 = W.astype(np.float64)
     cols = rng.choice(f_out, 6, replace=False)
     Xc = np.hstack([z.astype(np.float64), X.astype(np.float64)])
-    assert rel(dG.cpu().numpy()[:, cols], Xc.T @ M[:, cols]) < tol, name
     d_inner = F.deg[F.inner]
-
-    def top(local):                                      # (M W_top^T)[v] / |N(v)|
-        return (M[local] @ Wd[:f_in].T) / d_inner[local][:, None]
-
     rows_in = F.sample_inner(24, 5)
-    ref_in = np.zeros((len(rows_in), f_in))
-    for k, r in enumerate(rows_in):
-        vs = F.local_inner[F.neighbours(F.inner[r])]
-        vs = vs[vs >= 0]
-        ref_in[k] = (top(vs).sum(0) if len(vs) else 0.0) + M[r] @ Wd[f_in:].T
-    got_in = J_in[torch.from_numpy(rows_in).cuda(), :f_in].cpu().numpy()
-    assert rel(got_in, ref_in) < tol, name
     rows_bd = np.unique(np.concatenate([rng.choice(F.b, 24, replace=False), np.argsort(-F.deg[F.bd])[:2]]))
-    ref_bd = np.zeros((len(rows_bd), f_in))
-    for k, r in enumerate(rows_bd):
-        vs = F.local_inner[F.neighbours(F.bd[r])]
-        ref_bd[k] = top(vs[vs >= 0]).sum(0)
+    got_G = dG.cpu().numpy()[:, cols]
+    got_in = J_in[torch.from_numpy(rows_in).cuda(), :f_in].cpu().numpy()
     got_bd = J_bd[torch.from_numpy(rows_bd).cuda(), :f_in].cpu().numpy()
-    assert rel(got_bd, ref_bd) < tol, name
+    # bf16: the bf16-operand reading (M and W rounded) and the plain fp64 oracle, same tolerance
+    for rounded in ((True, False) if bf16 else (False,)):
+        M, Wd = (round_bf16(M0), round_bf16(W0)) if rounded else (M0, W0)
+        assert rel(got_G, Xc.T @ M[:, cols]) < tol, (name, rounded)
+
+        def top(local):                                  # (M W_top^T)[v] / |N(v)|
+            return (M[local] @ Wd[:f_in].T) / d_inner[local][:, None]
+
+        ref_in = np.zeros((len(rows_in), f_in))
+        for k, r in enumerate(rows_in):
+            vs = F.local_inner[F.neighbours(F.inner[r])]
+            vs = vs[vs >= 0]
+            ref_in[k] = (top(vs).sum(0) if len(vs) else 0.0) + M[r] @ Wd[f_in:].T
+        assert rel(got_in, ref_in) < tol, (name, rounded)
+        ref_bd = np.zeros((len(rows_bd), f_in))
+        for k, r in enumerate(rows_bd):
+            vs = F.local_inner[F.neighbours(F.bd[r])]
+            ref_bd[k] = top(vs[vs >= 0]).sum(0)
+        assert rel(got_bd, ref_bd) < tol, (name, rounded)
 
 
 @pytest.mark.parametrize("name", WORKLOADS)

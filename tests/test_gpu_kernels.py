@@ -7,6 +7,7 @@ import numpy as np
 import pytest
 import torch
 
+from certify import readings
 from gpu_helpers import TOL, dev, host, random_partition_graph, rel_err
 from oracle import layers
 from oracle.partition import build_partition, propagation_matrix
@@ -75,8 +76,7 @@ def test_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
     relu = f_out != 3
     no_A = dt == "bf16-noA"                  # bf16 path without an fp32 copy of A
     dt = "bf16" if no_A else dt
-    A_ref, Z_ref, H_ref = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), relu,
-                                               "bf16" if dt == "bf16" else "f64")
+    A_ref, _, _ = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), relu)
     dtype = B.PGCN_BF16 if dt == "bf16" else B.PGCN_F32
     dH_in = dev(H_in)
     dH_bd = dev(H_bd) if with_bd else None
@@ -96,7 +96,9 @@ def test_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
         assert np.all(pad == 0)
     if dt == "bf16":
         assert rel_err(host(A16, f_in), A_ref) < 1e-2    # one bf16 rounding
-    assert rel_err(host(H, f_out), H_ref) < tol
+    for gm in readings(dt):                              # bf16: the fp64 oracle and its bf16-operand reading
+        _, _, H_ref = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), relu, gm)
+        assert rel_err(host(H, f_out), H_ref) < tol, gm
 
 
 @pytest.mark.parametrize("gname", ["plain", "hub", "chunked", "tall"])

@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 import torch
 
+from certify import readings
 from gpu_helpers import TOL, dev, host, random_partition_graph, rel_err
 from oracle import layers
 from oracle.partition import build_partition, propagation_matrix
@@ -124,8 +125,7 @@ def test_sage_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
     W = rng.uniform(-0.2, 0.2, (2 * f_in, f_out)).astype(np.float32)
     relu = f_out != 5
     bf16 = dt == "bf16"
-    z_ref, Z_ref, H_ref = layers.sage_forward(g.P, np.vstack([X_in, X_bd]), n, W.astype(np.float64), relu,
-                                              "bf16" if bf16 else "f64")
+    z_ref, _, _ = layers.sage_forward(g.P, np.vstack([X_in, X_bd]), n, W.astype(np.float64), relu)
     dtype = B.PGCN_BF16 if bf16 else B.PGCN_F32
     dX = dev(X_in)
     dX16 = dev(X_in, dtype=torch.bfloat16) if bf16 else None
@@ -141,7 +141,9 @@ def test_sage_layer_forward(graphs, gname, dt, f_in, f_out, with_bd):
         assert rel_err(host(A, f_in), z_ref) < 1e-5
     else:
         assert rel_err(host(A16, f_in), z_ref) < 1e-2
-    assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"]
+    for gm in readings(dt):             # bf16: the fp64 oracle and its bf16-operand reading
+        _, _, H_ref = layers.sage_forward(g.P, np.vstack([X_in, X_bd]), n, W.astype(np.float64), relu, gm)
+        assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"], gm
 
 
 @pytest.mark.parametrize("gname", ["plain", "sparse", "chunked", "tall"])
@@ -163,8 +165,6 @@ def test_sage_layer_backward(graphs, gname, dt, f_in, f_out, input_grad):
     if bf16:   # the bf16 path reads z and X_in as bf16: give the oracle the same rounded operands
         z = torch.from_numpy(z).to(torch.bfloat16).double().numpy()
         X_in = torch.from_numpy(X_in).to(torch.bfloat16).double().numpy()
-    G_ref, Jf_ref = layers.sage_backward(g.P, z, X_in, Z, J, W.astype(np.float64), relu, input_grad,
-                                         "bf16" if bf16 else "f64")
     H_out = np.maximum(Z, 0) if relu else Z
     dz = None if bf16 else dev(z)
     dz16 = dev(z, dtype=torch.bfloat16) if bf16 else None
@@ -180,10 +180,12 @@ def test_sage_layer_backward(graphs, gname, dt, f_in, f_out, input_grad):
                           workspace=ws, workspace_bytes=nb)
     tol = TOL[dt]["grad"]
     torch.cuda.synchronize()
-    assert rel_err(dG.cpu().numpy(), G_ref) < tol
-    if input_grad:
-        assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol
-        assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
+    for gm in readings(dt):             # bf16: the fp64 oracle and its bf16-operand reading
+        G_ref, Jf_ref = layers.sage_backward(g.P, z, X_in, Z, J, W.astype(np.float64), relu, input_grad, gm)
+        assert rel_err(dG.cpu().numpy(), G_ref) < tol, gm
+        if input_grad:
+            assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol, gm
+            assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol, gm
 
 
 @pytest.mark.parametrize("gname", ["plain", "sparse", "chunked", "tall"])
@@ -201,9 +203,7 @@ def test_sage_layer_transform(graphs, gname, dt, f_in, f_out, with_bd):
     W = rng.uniform(-0.2, 0.2, (2 * f_in, f_out)).astype(np.float32)
     relu = f_out != 3
     bf16 = dt == "bf16"
-    gm = "bf16" if bf16 else "f64"
     dtype = B.PGCN_BF16 if bf16 else B.PGCN_F32
-    z_ref, Z_ref, H_ref = layers.sage_forward(g.P, X_full, n, W.astype(np.float64), relu, gm, order="transform")
     dX, dXbd = dev(X_in), (dev(X_bd) if with_bd else None)
     dX16 = dev(X_in, dtype=torch.bfloat16) if bf16 else None
     H = dev(np.zeros((n, f_out)))
@@ -213,21 +213,24 @@ def test_sage_layer_transform(graphs, gname, dt, f_in, f_out, with_bd):
                   W=torch.from_numpy(W).cuda(), A=None, A_bf16=None, workspace=ws, workspace_bytes=nb,
                   order=B.PGCN_ORDER_TRANSFORM)
     B.pgcn_sage_layer_fwd(g.part, X_in=dX, X_in_bf16=dX16, X_bd=dXbd, H_out=H, **common)
-    assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"]
+    for gm in readings(dt):             # bf16: the fp64 oracle and its bf16-operand reading
+        _, _, H_ref = layers.sage_forward(g.P, X_full, n, W.astype(np.float64), relu, gm, order="transform")
+        assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"], gm
     # backward from a fixed Z (mask) and J
     Z = rng.standard_normal((n, f_out))
     J = rng.standard_normal((n, f_out)) * 1e-2
-    G_ref, Jf_ref = layers.sage_backward(g.P, None, X_in, Z, J, W.astype(np.float64), relu, True, gm,
-                                         order="transform", X_full=X_full)
     dG = torch.zeros((2 * f_in, f_out), device="cuda")
     J_in, J_bd = dev(np.zeros((n, f_in))), dev(np.zeros((b, f_in)))
     B.pgcn_sage_layer_bwd(g.part, J_out=dev(J), H_out=dev(np.maximum(Z, 0) if relu else Z), X_in=dX, X_in_bf16=dX16,
                           X_bd=dXbd, dW=dG, J_in=J_in, J_bd_out=J_bd, **common)
     tol = TOL[dt]["grad"]
     torch.cuda.synchronize()
-    assert rel_err(dG.cpu().numpy(), G_ref) < tol
-    assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol
-    assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
+    for gm in readings(dt):
+        G_ref, Jf_ref = layers.sage_backward(g.P, None, X_in, Z, J, W.astype(np.float64), relu, True, gm,
+                                             order="transform", X_full=X_full)
+        assert rel_err(dG.cpu().numpy(), G_ref) < tol, gm
+        assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol, gm
+        assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol, gm
 
 
 def test_layer_entry_points_check_the_partition_kind(graphs):

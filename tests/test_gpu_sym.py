@@ -17,7 +17,10 @@ from oracle.pipegcn import Options, run
 from paper_2203_10428_amd import binding as B
 from paper_2203_10428_amd import configs
 from paper_2203_10428_amd.step import PartitionTrainer, StepOptions, ld_of
-from test_gpu_pipegcn import compare_step, put
+from dataclasses import replace
+
+from certify import certified_reference, readings
+from test_gpu_pipegcn import compare_step, exact_decisions, inject, put, sim_reference
 
 pytestmark = pytest.mark.gpu
 
@@ -69,8 +72,7 @@ def test_sym_forward(graphs, gname, order, dt, f_in, f_out, with_bd):
     H_in = rng.standard_normal((n, f_in))
     H_bd = rng.standard_normal((b, f_in)) if with_bd else np.zeros((b, f_in))
     W = rng.uniform(-0.2, 0.2, (f_in, f_out)).astype(np.float32)
-    A_ref, _, H_ref = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), True,
-                                           "bf16" if dt == "bf16" else "f64", order=order)
+    A_ref, _, _ = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), True, order=order)
     dtype = B.PGCN_BF16 if dt == "bf16" else B.PGCN_F32
     agg = order == "agg"
     A = dev(np.zeros((n, f_in))) if agg and dt == "f32" else None
@@ -84,7 +86,9 @@ def test_sym_forward(graphs, gname, order, dt, f_in, f_out, with_bd):
                      order=ORDERS[order])
     if A is not None:
         assert rel_err(host(A, f_in), A_ref) < 1e-5
-    assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"]
+    for gm in readings(dt):             # bf16: the fp64 oracle and its bf16-operand reading
+        _, _, H_ref = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), True, gm, order=order)
+        assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"], gm
 
 
 @pytest.mark.parametrize("gname", ["plain", "hub", "chunked"])
@@ -103,8 +107,6 @@ def test_sym_backward(graphs, gname, order, dt, f_in, f_out):
     dtype = B.PGCN_BF16 if dt == "bf16" else B.PGCN_F32
     if dt == "bf16" and order == "agg":      # the bf16 path reads A as bf16: the oracle gets the same rounded A
         A = torch.from_numpy(A).to(torch.bfloat16).double().numpy()
-    G_ref, Jf_ref = layers.layer_backward(g.P, A, Z, J, W.astype(np.float64), True, True,
-                                          "bf16" if dt == "bf16" else "f64", order=order, H_full=H_full)
     agg = order == "agg"
     dA = dev(A) if agg and dt == "f32" else None
     dA16 = dev(A, dtype=torch.bfloat16) if agg and dt == "bf16" else None
@@ -118,9 +120,12 @@ def test_sym_backward(graphs, gname, order, dt, f_in, f_out):
                      order=ORDERS[order], H_in=dev(H_full[:n]), H_bd=dev(H_full[n:]))
     tol = TOL[dt]["grad"]
     torch.cuda.synchronize()
-    assert rel_err(dG.cpu().numpy(), G_ref) < tol
-    assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol
-    assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
+    for gm in readings(dt):             # bf16: the fp64 oracle and its bf16-operand reading
+        G_ref, Jf_ref = layers.layer_backward(g.P, A, Z, J, W.astype(np.float64), True, True, gm, order=order,
+                                              H_full=H_full)
+        assert rel_err(dG.cpu().numpy(), G_ref) < tol, gm
+        assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol, gm
+        assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol, gm
 
 
 def tiny_setup(T, gemm, order):
@@ -137,28 +142,21 @@ def tiny_setup(T, gemm, order):
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_tiny_injected_sym(order, dt):
     T = 3
-    w, g, d, sim, recs = tiny_setup(T, "bf16" if dt == "bf16" else "f64", order)
+    w, g, d, sim, recs = tiny_setup(T, "f64", order)
     L = w.layers
     tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, dt,
                           StepOptions(gamma=w.gamma, eta=w.eta, copy_mode="none", order=order, norm="sym"))
     assert tr.info["symmetric"] == 1
     for t in range(1, T + 1):
         r0, r1 = recs[t - 1][0], recs[t - 1][1]
-        si = r0["state_in"]
-        for l in range(L):
-            tr.W[l].copy_(torch.from_numpy(r0["W_in"][l].astype(np.float32)))
-            tr.G_peer[l] = torch.from_numpy(r1["G"][l + 1].astype(np.float32)).cuda()
-        for l in range(1, L + 1):
-            put(tr.feat[l][tr.cur], si.feat_buf[l])
-            put(tr.ema_f[l], si.ema_f[l])
-        for l in range(2, L + 1):
-            put(tr.grad[l][tr.cur], si.grad_buf[l])
-            put(tr.ema_g[l], si.ema_g[l])
-        tr.t = t - 1
+        inject(tr, r0, r1, L)
         torch.cuda.synchronize()
         tr.step()
         tr.synchronize()
-        compare_step(tr, r0, dt, L, w.widths)
+        H_gpu = {l: host(tr.H[l], w.widths[l]) for l in range(1, L + 1)}
+        for gm in readings(dt):
+            ref = certified_reference(sim, r0, r1, replace(sim.opts, gemm=gm), H_gpu, dt)
+            compare_step(tr, ref, dt, L, w.widths, f"sym {order} {dt} t={t} vs {gm}")
 
 
 def test_tiny_autonomous_sym():
@@ -180,4 +178,5 @@ def test_tiny_autonomous_sym():
         torch.cuda.synchronize()
         tr.step()
         tr.synchronize()
-        compare_step(tr, r0, "f32", L, w.widths, check_state=True)
+        exact_decisions(tr, r0, L, w.widths, f"autonomous sym t={t}")
+        compare_step(tr, sim_reference(r0), "f32", L, w.widths, f"autonomous sym t={t}")

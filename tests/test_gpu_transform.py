@@ -16,7 +16,10 @@ from paper_2203_10428_amd import binding as B
 from paper_2203_10428_amd import configs
 from paper_2203_10428_amd.step import PartitionTrainer, StepOptions, ld_of
 from test_gpu_kernels import Graph
-from test_gpu_pipegcn import compare_step, put
+from dataclasses import replace
+
+from certify import certified_reference, readings
+from test_gpu_pipegcn import compare_step, exact_decisions, inject, put, sim_reference
 
 pytestmark = pytest.mark.gpu
 
@@ -51,8 +54,6 @@ def test_transform_forward(graphs, gname, dt, f_in, f_out, with_bd):
     H_bd = rng.standard_normal((b, f_in)) if with_bd else np.zeros((b, f_in))
     W = rng.uniform(-0.2, 0.2, (f_in, f_out)).astype(np.float32)
     relu = f_out not in (1, 41)
-    _, _, H_ref = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), relu,
-                                       "bf16" if dt == "bf16" else "f64", order="transform")
     dtype = B.PGCN_BF16 if dt == "bf16" else B.PGCN_F32
     H = dev(np.full((n, f_out), 7.0))
     ws, nb = ws_tf(g, f_in, f_out, dtype)
@@ -60,7 +61,10 @@ def test_transform_forward(graphs, gname, dt, f_in, f_out, with_bd):
                      ld_out=ld_of(f_out), H_in=dev(H_in), H_bd=dev(H_bd) if with_bd else None,
                      W=torch.from_numpy(W).cuda(), A=None, A_bf16=None, H_out=H, workspace=ws, workspace_bytes=nb,
                      order=TF)
-    assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"]
+    for gm in readings(dt):             # bf16: the fp64 oracle and its bf16-operand reading
+        _, _, H_ref = layers.layer_forward(g.P, np.vstack([H_in, H_bd]), W.astype(np.float64), relu, gm,
+                                           order="transform")
+        assert rel_err(host(H, f_out), H_ref) < TOL[dt]["act"], gm
     pad = host(H, ld_of(f_out))[:, f_out:(f_out + 3) // 4 * 4]       # padding columns written as zeros
     assert np.all(pad == 0)
 
@@ -80,9 +84,6 @@ def test_transform_backward(graphs, gname, dt, f_in, f_out, input_grad, with_bd)
     J = rng.standard_normal((n, f_out)) * 1e-2
     W = rng.uniform(-0.2, 0.2, (f_in, f_out)).astype(np.float32)
     relu = f_out not in (1, 41)
-    G_ref, Jf_ref = layers.layer_backward(g.P, None, Z, J, W.astype(np.float64), relu, input_grad,
-                                          "bf16" if dt == "bf16" else "f64", order="transform",
-                                          H_full=np.vstack([H_in, H_bd]))
     H_out = np.maximum(Z, 0) if relu else Z                          # mask source: H > 0 <=> Z > 0
     dtype = B.PGCN_BF16 if dt == "bf16" else B.PGCN_F32
     dG = torch.full((f_in, f_out), 5.0, device="cuda")
@@ -95,10 +96,13 @@ def test_transform_backward(graphs, gname, dt, f_in, f_out, input_grad, with_bd)
                      order=TF, H_in=dev(H_in), H_bd=dev(H_bd) if with_bd else None)
     tol = TOL[dt]["grad"]
     torch.cuda.synchronize()
-    assert rel_err(dG.cpu().numpy(), G_ref) < tol
-    if input_grad:
-        assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol
-        assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol
+    for gm in readings(dt):             # bf16: the fp64 oracle and its bf16-operand reading
+        G_ref, Jf_ref = layers.layer_backward(g.P, None, Z, J, W.astype(np.float64), relu, input_grad, gm,
+                                              order="transform", H_full=np.vstack([H_in, H_bd]))
+        assert rel_err(dG.cpu().numpy(), G_ref) < tol, gm
+        if input_grad:
+            assert rel_err(host(J_in, f_in), Jf_ref[:n]) < tol, gm
+            assert rel_err(host(J_bd, f_in), Jf_ref[n:]) < tol, gm
 
 
 @pytest.mark.parametrize("gname", ["hub", "chunked"])
@@ -160,7 +164,7 @@ def tiny_setup(T, sf, sg, gemm, order):
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_tiny_injected_transform(sf, sg, dt):
     T = 3
-    w, g, d, sim, recs = tiny_setup(T, sf, sg, "bf16" if dt == "bf16" else "f64", "transform")
+    w, g, d, sim, recs = tiny_setup(T, sf, sg, "f64", "transform")
     L = w.layers
     tr = PartitionTrainer(g, d.X, d.labels, d.W, w.widths, w.loss, w.loss_scale, dt,
                           StepOptions(smooth_f=sf, smooth_g=sg, gamma=w.gamma, eta=w.eta, copy_mode="none",
@@ -168,21 +172,14 @@ def test_tiny_injected_transform(sf, sg, dt):
     assert all(tr.order[l] == TF and tr.A[l] is None for l in range(1, L + 1))
     for t in range(1, T + 1):
         r0, r1 = recs[t - 1][0], recs[t - 1][1]
-        si = r0["state_in"]
-        for l in range(L):
-            tr.W[l].copy_(torch.from_numpy(r0["W_in"][l].astype(np.float32)))
-            tr.G_peer[l] = torch.from_numpy(r1["G"][l + 1].astype(np.float32)).cuda()
-        for l in range(1, L + 1):
-            put(tr.feat[l][tr.cur], si.feat_buf[l])
-            put(tr.ema_f[l], si.ema_f[l])
-        for l in range(2, L + 1):
-            put(tr.grad[l][tr.cur], si.grad_buf[l])
-            put(tr.ema_g[l], si.ema_g[l])
-        tr.t = t - 1
+        inject(tr, r0, r1, L)
         torch.cuda.synchronize()
         tr.step()
         tr.synchronize()
-        compare_step(tr, r0, dt, L, w.widths)
+        H_gpu = {l: host(tr.H[l], w.widths[l]) for l in range(1, L + 1)}
+        for gm in readings(dt):
+            ref = certified_reference(sim, r0, r1, replace(sim.opts, gemm=gm), H_gpu, dt)
+            compare_step(tr, ref, dt, L, w.widths, f"transform {dt} t={t} vs {gm}")
 
 
 @pytest.mark.parametrize("order", ["transform", "auto"])
@@ -206,7 +203,8 @@ def test_tiny_autonomous_transform(order):
         torch.cuda.synchronize()
         tr.step()
         tr.synchronize()
-        compare_step(tr, r0, "f32", L, w.widths, check_state=True)
+        exact_decisions(tr, r0, L, w.widths, f"autonomous {order} t={t}")
+        compare_step(tr, sim_reference(r0), "f32", L, w.widths, f"autonomous {order} t={t}")
 
 
 @pytest.mark.parametrize("sf,sg", [(False, False), (True, True)])
@@ -245,6 +243,9 @@ def test_tiny_layer1_cached(sf, sg, dt, mode):
         torch.cuda.synchronize()
         tr.step()
         tr.synchronize()
+        # an autonomous run: decisions must agree with the reading exactly (the injected tests certify
+        # differing ones); on the bf16 path this run follows the oracle's bf16-operand reading
+        exact_decisions(tr, r0, L, w.widths, f"layer-1 cached {dt} {mode} t={t}")
         errs = {"loss": abs(tr.loss.item() - r0["loss"]) / abs(r0["loss"])}
         for l in range(1, L + 1):
             errs[f"H{l}"] = rel_err(host(tr.H[l], w.widths[l]), r0["H"][l])
