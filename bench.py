@@ -58,10 +58,14 @@ def algorithmic_work(tr, w, model="gcn"):
     k = 2 if model == "sage" else 1          # GraphSAGE's update takes CONCAT(z, h): K = 2 f
     f4 = lambda f: (f + 3) // 4 * 4
     out = {k: 0.0 for k in ("agg_fwd", "agg_bwd", "agg_fwd_gather", "agg_bwd_gather", "gemm_fwd", "gemm_dgrad",
-                            "gemm_wgrad")}
+                            "gemm_wgrad", "gemm_fwd_bytes", "gemm_dgrad_bytes", "gemm_wgrad_bytes")}
     idx, idx_t = e * 4 + items * 16, e * 4 + items_t * 16
+    s = i["n_send"]
+    ea = 2 if bf16 else 4                    # bytes per activation element the GEMM reads where a bf16 copy exists
+    ew = 2 if bf16 else 4                    # packed weights
     for l in range(1, L + 1):
         f, fo = wd[l - 1], wd[l]
+        send = s * fo * 4 if l < L else 0    # the forward GEMM's epilogue also writes the next layer's sent rows
         if tr.order[l] == B.PGCN_ORDER_TRANSFORM:
             # P (H W): the aggregations move f_out-wide rows (Y forward, T = P^T M backward, at every
             # layer), and the GEMMs run over the n + b inner and boundary rows
@@ -72,17 +76,27 @@ def algorithmic_work(tr, w, model="gcn"):
             self_term = 2.0 * n * f * fo if model == "sage" else 0.0
             out["gemm_fwd"] += 2.0 * (n + b) * f * fo + self_term
             out["gemm_wgrad"] += 2.0 * (n + b) * f * fo + self_term
+            # compulsory bytes: fp32 operands read once (rounded while staged on the bf16 path), output once
+            out["gemm_fwd_bytes"] += (n + b) * f * 4 + k * f * fo * ew + (n + b) * fo * 4
+            out["gemm_wgrad_bytes"] += (n + b) * (f + fo) * 4 + f * fo * 4
             if l > 1:
                 out["gemm_dgrad"] += 2.0 * (n + b) * f * fo + self_term
+                out["gemm_dgrad_bytes"] += (n + b) * (fo + f) * 4 + k * f * fo * ew
             continue
         out["agg_fwd"] += idx + (n + b) * f * 4 + n * f4(f) * (6 if bf16 else 4)
         out["agg_fwd_gather"] += idx + e * f4(f) * 4 + n * f4(f) * (6 if bf16 else 4)
         out["gemm_fwd"] += 2.0 * n * k * f * fo
         out["gemm_wgrad"] += 2.0 * n * k * f * fo
+        out["gemm_fwd_bytes"] += n * k * f * ea + k * f * fo * ew + n * fo * 4 + send
+        # A, J and the mask source H read once; dW written once; bf16 path with an input gradient
+        # also writes the masked operand as bf16
+        out["gemm_wgrad_bytes"] += n * k * f * ea + 2 * n * fo * 4 + k * f * fo * 4 + \
+            (n * fo * 2 if bf16 and l > 1 else 0)
         if l > 1:
             out["agg_bwd"] += idx_t + n * f * 4 + (n + b) * f4(f) * 4
             out["agg_bwd_gather"] += idx_t + e * f4(f) * 4 + (n + b) * f4(f) * 4
             out["gemm_dgrad"] += 2.0 * n * k * f * fo
+            out["gemm_dgrad_bytes"] += n * fo * (2 if bf16 else 8) + k * f * fo * ew + n * k * f * 4
     return out
 
 
@@ -108,8 +122,8 @@ def measured_traffic(workload: str, kernel: str):
 
 
 def cpu_baseline(w, scale: float, model: str = "gcn", order: str = "agg", norm: str = "mean"):
-    """Time the fp64 oracle's per-partition step on a sample of the workload (same layer
-    association and normalisation as the GPU run)."""
+    """Time the fp64 oracle's per-partition step (same layer association and normalisation as the
+    GPU run) on the whole partition (scale 1) or on a sample of the same graph law."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -117,7 +131,7 @@ def cpu_baseline(w, scale: float, model: str = "gcn", order: str = "agg", norm: 
     from oracle.pipegcn import Options, partition_step
     from paper_2203_10428_amd import configs
 
-    ws = configs.with_inner_scale(w, scale)
+    ws = w if scale == 1.0 else configs.with_inner_scale(w, scale)
     g = configs.make_graph(ws)
     d = configs.make_dense(ws, g.n, model=model)
     p = build_partition(g.n, g.rowptr, g.col, g.owner, 0, g.nparts, self_loop=model == "gcn")
@@ -169,8 +183,10 @@ def main():
                          "cross the host link, as in the paper's CPU-staged exchange)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=None,
-                    help="inner-node fraction timed on the CPU (default 0.4; 0.15 for the GraphSAGE model, whose "
-                         "oracle also draws the dropout masks)")
+                    help="inner-node fraction timed on the CPU (default 1: one step of the whole partition; "
+                         "0.1 for the 2M-row stress partition, whose fp64 step needs ~115 GB; 0.15 for the "
+                         "GraphSAGE model, whose oracle also draws the dropout masks)")
+    ap.add_argument("--out", default=None, help="also write the JSON line to this file")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 5 plain device copies of BYTES bytes (counter calibration) and exit")
     args = ap.parse_args()
@@ -214,14 +230,26 @@ def main():
     del d
     log(f"partition set up: {tr.info}")
 
-    def timed(k, mode):
+    def timed(k, mode, per_step_ms=None):
+        """Mean wall-clock ms per step over k steps bracketed by device synchronisations; with
+        per_step_ms, also each step's time between events recorded on the compute stream."""
         tr.opts.copy_mode = mode
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(k)] if per_step_ms is not None else None
         torch.cuda.synchronize()
         s = time.perf_counter()
-        for _ in range(k):
+        for i in range(k):
+            if evs:
+                tr.stream.wait_stream(torch.cuda.current_stream())
+                evs[i][0].record(tr.stream)
             tr.step()
+            if evs:
+                evs[i][1].record(tr.stream)
         torch.cuda.synchronize()
-        return (time.perf_counter() - s) / k * 1e3
+        mean = (time.perf_counter() - s) / k * 1e3
+        if evs:
+            per_step_ms.extend(a.elapsed_time(b) for a, b in evs)
+        return mean
 
     for _ in range(args.warmup):
         tr.step()
@@ -251,11 +279,14 @@ def main():
     # aggregation chunk launches of one column range share one pair)
     B.pgcn_trace_enable(max(1024, args.steps * 256))
     B.pgcn_trace_filter([dominant])
-    ms_per_step = timed(args.steps, "pipe")
+    step_events = []
+    ms_per_step = timed(args.steps, "pipe", step_events)
     per_step = summarise(B.pgcn_trace_collect(args.steps * 256), args.steps)
     B.pgcn_trace_disable()
     loss = tr.loss.item()
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, loss {loss:.6f}")
+    step_median = float(np.median(step_events))
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall clock), median {step_median:.3f} ms "
+        f"(compute-stream events), loss {loss:.6f}")
 
     work = algorithmic_work(tr, w, args.model)
     dt = "bf16" if w.gemm_dtype == "bf16" else "f32"
@@ -267,7 +298,13 @@ def main():
         if k.startswith("agg"):
             util[k] = {"GBps_compulsory": work[k] / sec / 1e9, "GBps_gather_model": work[k + "_gather"] / sec / 1e9}
         else:
-            util[k] = {"TFLOPs": work[k] / sec / 1e12, "mfma_frac": work[k] / sec / 1e12 / MFMA_PEAK_TFLOPS[dt]}
+            # the attainable rate is the lower of the matrix-core peak and the product's arithmetic
+            # intensity (flops per compulsory byte) times the HBM peak
+            ai = work[k] / max(work[k + "_bytes"], 1.0)
+            attain = min(MFMA_PEAK_TFLOPS[dt], ai * HBM_PEAK_GBPS / 1e3)
+            util[k] = {"TFLOPs": work[k] / sec / 1e12, "mfma_frac": work[k] / sec / 1e12 / MFMA_PEAK_TFLOPS[dt],
+                       "flop_per_byte": ai, "attainable_TFLOPs": attain,
+                       "frac_attainable": work[k] / sec / 1e12 / attain}
     if dominant.startswith("agg"):
         ach = util[dominant]["GBps_compulsory"]
         tr_bytes = measured_traffic(w.name, dominant)
@@ -305,14 +342,20 @@ def main():
     if not args.no_cpu_baseline:
         try:
             if args.cpu_sample is None:
-                args.cpu_sample = 0.4 if args.model == "gcn" else 0.15
+                args.cpu_sample = 0.15 if args.model == "sage" else (0.1 if w.graph_kind == "rmat" else 1.0)
             sec, n_s, nnz_s, threads = cpu_baseline(w, args.cpu_sample, args.model, args.order, args.norm)
             scale = tr.info["nnz"] / nnz_s
+            what = (f"fp64 oracle per-partition step ({args.model}, PipeGCN-GF, t=2)")
+            if args.cpu_sample == 1.0:
+                what += (f" on the whole partition ({n_s} inner rows, {nnz_s} nnz): {sec:.2f}s for one step, "
+                         f"not extrapolated")
+            else:
+                what += (f" on the same graph law at {args.cpu_sample:g} of the inner/pool nodes ({n_s} inner rows, "
+                         f"{nnz_s} nnz) took {sec:.2f}s; scaled by the nnz ratio {scale:.2f} to the full partition")
             cpu = {"value": 1.0 / (sec * scale), "unit": "steps/s", "cores": threads, "kind": "oracle",
-                   "sample": (f"fp64 oracle per-partition step ({args.model}, PipeGCN-GF, t=2) on the same graph law at "
-                              f"{args.cpu_sample:g} of the inner/pool nodes ({n_s} inner rows, {nnz_s} nnz) took "
-                              f"{sec:.2f}s; scaled by the nnz ratio {scale:.2f} to the full partition; SciPy's "
-                              f"sparse products run single-threaded, dense products use {threads} BLAS threads")}
+                   "host_cpus": os.cpu_count(), "blas_threads": threads, "sparse_threads": 1,
+                   "sample": what + (f"; SciPy's sparse products run single-threaded, the dense products on "
+                                     f"{threads} BLAS threads of the host's {os.cpu_count()} CPUs")}
             log(f"cpu baseline: {cpu}")
         except Exception as exc:  # the baseline must never hide the GPU result
             cpu = {"value": None, "unit": "steps/s", "cores": os.cpu_count(), "kind": "oracle",
@@ -327,6 +370,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        # per-step time between events recorded on the compute stream around each timed step
+        "ms_per_step_median_events": step_median,
+        "ms_per_step_events_min_max": [float(np.min(step_events)), float(np.max(step_events))],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -353,6 +399,10 @@ def main():
         "loss": loss,
     }
     print(json.dumps(line), flush=True)
+    if args.out:
+        os.makedirs(os.path.dirname(os.path.abspath(args.out)), exist_ok=True)
+        with open(args.out, "w") as f:
+            f.write(json.dumps(line) + "\n")
 
 
 if __name__ == "__main__":

@@ -59,7 +59,7 @@ def test_gemm_flops_match_layer_products(model, orders):
     n, b, e = 1000, 300, 12000
     widths = [40, 24, 24, 7]
     order = {l + 1: (B.PGCN_ORDER_TRANSFORM if o == "transform" else B.PGCN_ORDER_AGG) for l, o in enumerate(orders)}
-    tr = SimpleNamespace(info=dict(n_inner=n, n_bd=b, nnz=e, spmm_items=1100, spmmt_items=1400), L=3,
+    tr = SimpleNamespace(info=dict(n_inner=n, n_bd=b, nnz=e, n_send=280, spmm_items=1100, spmmt_items=1400), L=3,
                          widths=widths, order=order)
     w = SimpleNamespace(gemm_dtype="f32")
     got = bench.algorithmic_work(tr, w, model)
@@ -72,6 +72,9 @@ def test_gemm_flops_match_layer_products(model, orders):
         assert got[key] == v, key
     # every aggregation model moves at least the compulsory bytes
     assert got["agg_fwd_gather"] >= got["agg_fwd"] > 0 and got["agg_bwd_gather"] >= got["agg_bwd"] > 0
+    # a GEMM's compulsory bytes cover at least its operands' and output's fp32-or-bf16 elements once
+    for key in ("gemm_fwd", "gemm_wgrad", "gemm_dgrad"):
+        assert got[key + "_bytes"] > 0 and got[key] / got[key + "_bytes"] < 64
 
 
 def test_measured_traffic_is_void_once_a_source_changes(tmp_path, monkeypatch):
