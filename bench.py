@@ -386,7 +386,11 @@ def main():
                    "widths": list(w.widths),
                    "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",
                    "n_inner": i["n_inner"], "n_bd": i["n_bd"], "n_send": i["n_send"], "nnz": i["nnz"],
-                   "max_row_len": i["max_row_len"], "parallelism": "1 partition / 1 GPU"},
+                   "max_row_len": i["max_row_len"],
+                   # the block of P_i (and of P_i^T) aggregated on the matrix cores: rows, columns, non-zeros
+                   "dense_block": [i["spmm_hub_rows"], i["spmm_hub_cols"], i["spmm_hub_nnz"]],
+                   "dense_block_t": [i["spmmt_hub_rows"], i["spmmt_hub_cols"], i["spmmt_hub_nnz"]],
+                   "parallelism": "1 partition / 1 GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": breakdown,

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define PGCN_VERSION 164
+#define PGCN_VERSION 165
 
 enum pgcn_status {
   PGCN_OK = 0,
@@ -122,10 +122,16 @@ typedef struct pgcn_partition pgcn_partition;
  *   PGCN_AGG_SLICE_F4  float4 columns per aggregation lane slice: 16, 32 or 64
  *                      (read per call; default 64);
  *   PGCN_TN_BM=128     keeps the fp32 weight-gradient GEMM in 128-row tiles
- *                      (read once; default: 256-row tiles for f_in >= 384).
- * Chunks and segments set the order in which a row's terms are added (results
- * stay deterministic for a given setting and row width); the other two change
- * only speed. */
+ *                      (read once; default: 256-row tiles for f_in >= 384);
+ *   PGCN_HUB=0         no dense block on the matrix cores (read by
+ *                      pgcn_partition_setup; default: a block of the rows with
+ *                      the most non-zeros x the most referenced columns where it
+ *                      saves >= 5% of the gathers, reported by pgcn_info);
+ *   PGCN_HUB_ROWS, PGCN_HUB_COLS  both > 0: force the block to that many rows
+ *                      and columns (clamped to the matrix).
+ * Chunks, segments and the dense block set the order in which a row's terms are
+ * added (results stay deterministic for a given setting and row width); the
+ * slice width and PGCN_TN_BM change only speed. */
 
 /* Largest layer width (f_in, f_out) the layer entry points accept: the
  * aggregation covers a row in at most 32 launches of up to 512 float4
@@ -156,6 +162,12 @@ typedef struct {
   int32_t spmm_chunks_narrow;  /* column chunks of P_i when the aggregated rows
                                   have at most 64 floats                      */
   int32_t spmmt_chunks_narrow; /* the same for P_i^T                          */
+  int32_t spmm_hub_rows;   /* rows x columns of the dense block of P_i taken  */
+  int32_t spmm_hub_cols;   /* by the matrix cores (0: none)                   */
+  int64_t spmm_hub_nnz;    /* its non-zeros                                   */
+  int32_t spmmt_hub_rows;  /* the same for P_i^T                              */
+  int32_t spmmt_hub_cols;
+  int64_t spmmt_hub_nnz;
 } pgcn_info;
 
 /* Caller-allocated host buffers for pgcn_partition_export, sized from pgcn_info.

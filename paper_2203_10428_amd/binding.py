@@ -48,7 +48,9 @@ class pgcn_info(C.Structure):
                 ("host_only", _i32), ("spmm_segment", _i32), ("spmm_items", _i64),
                 ("spmm_split_slots", _i64), ("spmmt_items", _i64), ("spmmt_split_slots", _i64),
                 ("spmm_chunks", _i32), ("spmmt_chunks", _i32), ("symmetric", _i32), ("self_loop", _i32),
-                ("spmm_chunks_narrow", _i32), ("spmmt_chunks_narrow", _i32)]
+                ("spmm_chunks_narrow", _i32), ("spmmt_chunks_narrow", _i32),
+                ("spmm_hub_rows", _i32), ("spmm_hub_cols", _i32), ("spmm_hub_nnz", _i64),
+                ("spmmt_hub_rows", _i32), ("spmmt_hub_cols", _i32), ("spmmt_hub_nnz", _i64)]
 
 
 class pgcn_arrays(C.Structure):

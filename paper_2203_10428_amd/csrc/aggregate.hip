@@ -70,6 +70,7 @@ struct AggParams {
   float *send;            // or null: final rows [0, out_split) also to their send rows (stride ld_out)
   const int64_t *send_ptr;
   const int32_t *send_pos;
+  const uint32_t *hub_init;  // or null: rows whose bit is set start from their dense-block sum
 };
 
 enum { AGG_FIRST = 1, AGG_LAST = 2 };
@@ -97,7 +98,8 @@ __device__ __forceinline__ float *out_row(const AggParams &p, int64_t r) {
 __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, float4 v) {
   const int c = 4 * c4;
   float *o = out_row(p, r);
-  if (!(p.mode & AGG_FIRST) || (p.accum_lo && r < p.out_split)) v = add4(v, *reinterpret_cast<const float4 *>(o + c));
+  if (!(p.mode & AGG_FIRST) || (p.accum_lo && r < p.out_split) || (p.hub_init && ((p.hub_init[r >> 5] >> (r & 31)) & 1u)))
+    v = add4(v, *reinterpret_cast<const float4 *>(o + c));
   if (!(p.mode & AGG_LAST)) {
     *reinterpret_cast<float4 *>(o + c) = v;
     return;
@@ -277,6 +279,198 @@ __global__ __launch_bounds__(256) void agg_fixup_kernel(AggParams p, const Split
   }
 }
 
+// ------------------------------------------------------------ dense block ---
+//
+// Block sums on the matrix cores: S[r] = sum over hub columns c of bit(r, c) H[c]
+// for the hub rows r.  First hub_split_kernel writes, per tile of kHubColTile =
+// 32 hub columns, the tile's gathered rows (this launch's float4 slice) as
+// three bf16 parts (hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi - mid):
+// x = hi + mid + lo exactly for normal fp32 x), feature-major with the 32
+// columns contiguous, in exactly the layout the MFMA loop reads from LDS (a
+// tile image).  hub_kernel: a workgroup (4 waves) owns kHubRowTile = 256 hub
+// rows (64 per wave) and a range of column tiles; it copies the next tile
+// image to registers while multiplying the current one from LDS (double
+// buffered): v_mfma_f32_32x32x16_bf16 multiplies the 0/1 bits (bf16 1.0 or 0,
+// exact) by each part with fp32 accumulation, so the products are exact and
+// only the fp32 sums round, as in the gather.  Each fragment of a part feeds
+// the wave's two 32-row halves.  The bits of a row for a tile are one 32-bit
+// word.  Operand layout as in the update GEMMs: the feature side is the
+// MFMA's first operand, so lane l holds hub row l % 32 (of its half) and
+// registers 4q .. 4q+3 of block j hold features 32 j + 8 q + 4 (l / 32) .. +3;
+// lane half h supplies columns 16 s + 8 h .. +7 of k-step s on both sides.
+
+typedef float hub_f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 hub_bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int hub_u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kHubLds = 40;                                  // bf16 per feature row: 32 columns + 8 pad
+constexpr int kHubImage = 3 * 256 * kHubLds * 2;             // bytes of one tile image (61,440)
+constexpr int kHubImageVec = kHubImage / 16 / 256;           // 16-byte vectors per thread (15)
+
+struct HubParams {
+  const int32_t *row_ids;          // [rows]  output row of each hub row (-1: padding)
+  const int32_t *col_ids;          // [cols]  gathered row of each hub column (-1: padding)
+  const uint32_t *bits;            // [rows][ntiles]
+  int32_t rows, ntiles, tiles_per_group, groups;
+  int64_t in_split;
+  const float *in_lo, *in_hi;
+  int64_t ld_in;
+  int32_t c4_off, c4_cnt;          // float4 columns of this pass (at most 64)
+  uint16_t *img;                   // [ntiles] tile images of this pass
+  float *part;                     // [groups][rows][ld_part] block sums of each group
+  int64_t ld_part;
+};
+
+__device__ __forceinline__ uint16_t hub_bf16(float x) {
+  uint32_t b = __float_as_uint(x);
+  b += 0x7fffu + ((b >> 16) & 1u);
+  return (uint16_t)(b >> 16);
+}
+__device__ __forceinline__ float hub_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// One workgroup per tile: thread (w, l) splits columns 8 w .. 8 w + 7 of features 4 l .. 4 l + 3.
+__global__ __launch_bounds__(256) void hub_split_kernel(HubParams p) {
+  const int ct = blockIdx.x, t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const bool f4_ok = lane < p.c4_cnt;
+  const int cb = 4 * (p.c4_off + lane);
+  float4 x8[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int c = p.col_ids[ct * kHubColTile + 8 * wave + e];
+    const float *src = nullptr;
+    if (c >= 0) {
+      if (c < p.in_split) src = p.in_lo + (int64_t)c * p.ld_in;
+      else if (p.in_hi) src = p.in_hi + (int64_t)(c - p.in_split) * p.ld_in;
+    }
+    x8[e] = (f4_ok && src) ? *reinterpret_cast<const float4 *>(src + cb) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  uint16_t *img = p.img + (int64_t)ct * (kHubImage / 2);
+#pragma unroll
+  for (int fe = 0; fe < 4; ++fe) {
+    uint16_t hi[8], mi[8], lo[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float x = fe == 0 ? x8[e].x : fe == 1 ? x8[e].y : fe == 2 ? x8[e].z : x8[e].w;
+      hi[e] = hub_bf16(x);
+      const float r1 = x - hub_f32(hi[e]);
+      mi[e] = hub_bf16(r1);
+      lo[e] = hub_bf16(r1 - hub_f32(mi[e]));
+    }
+    hub_u32x4 vh, vm, vl;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      vh[w] = (uint32_t)hi[2 * w] | ((uint32_t)hi[2 * w + 1] << 16);
+      vm[w] = (uint32_t)mi[2 * w] | ((uint32_t)mi[2 * w + 1] << 16);
+      vl[w] = (uint32_t)lo[2 * w] | ((uint32_t)lo[2 * w + 1] << 16);
+    }
+    const int f = 4 * lane + fe;
+    *reinterpret_cast<hub_u32x4 *>(img + (0 * 256 + f) * kHubLds + 8 * wave) = vh;
+    *reinterpret_cast<hub_u32x4 *>(img + (1 * 256 + f) * kHubLds + 8 * wave) = vm;
+    *reinterpret_cast<hub_u32x4 *>(img + (2 * 256 + f) * kHubLds + 8 * wave) = vl;
+  }
+}
+
+__global__ __launch_bounds__(256) void hub_kernel(HubParams p) {
+  __shared__ __attribute__((aligned(16))) uint16_t hs[2][kHubImage / 2];       // 122,880 bytes
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int rt = blockIdx.x / p.groups, g = blockIdx.x % p.groups;
+  const int ct0 = g * p.tiles_per_group;
+  const int ct1 = ct0 + p.tiles_per_group < p.ntiles ? ct0 + p.tiles_per_group : p.ntiles;
+  const int h = lane >> 5, r32 = lane & 31;
+  const int hrow0 = rt * kHubRowTile + wave * 64 + r32;          // this lane's rows: hrow0, hrow0 + 32
+
+  hub_u32x4 stg[kHubImageVec];
+  uint32_t pat0 = 0, pat1 = 0;
+  auto load = [&](int ct) __attribute__((always_inline)) {
+    const hub_u32x4 *src = reinterpret_cast<const hub_u32x4 *>(p.img + (int64_t)ct * (kHubImage / 2));
+#pragma unroll
+    for (int v = 0; v < kHubImageVec; ++v) stg[v] = src[t + 256 * v];
+    pat0 = p.bits[(int64_t)hrow0 * p.ntiles + ct];
+    pat1 = p.bits[(int64_t)(hrow0 + 32) * p.ntiles + ct];
+  };
+  auto store = [&](int buf) __attribute__((always_inline)) {
+    hub_u32x4 *dst = reinterpret_cast<hub_u32x4 *>(hs[buf]);
+#pragma unroll
+    for (int v = 0; v < kHubImageVec; ++v) dst[t + 256 * v] = stg[v];
+  };
+  auto expand = [](uint32_t byte) __attribute__((always_inline)) {
+    hub_u32x4 aw;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      aw[w] = (((byte >> (2 * w)) & 1u) ? 0x3f80u : 0u) | (((byte >> (2 * w + 1)) & 1u) ? 0x3f800000u : 0u);
+    return __builtin_bit_cast(hub_bf16x8, aw);
+  };
+
+  hub_f32x16 acc[2][8];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = (hub_f32x16){};
+  const int nb = (4 * p.c4_cnt + 31) / 32;                       // 32-feature blocks of this pass
+  if (ct0 < ct1) {
+    load(ct0);
+    store(0);
+  }
+  __syncthreads();
+  for (int ct = ct0; ct < ct1; ++ct) {
+    const int cur = (ct - ct0) & 1;
+    const uint32_t pc0 = pat0, pc1 = pat1;
+    if (ct + 1 < ct1) load(ct + 1);
+    const uint16_t *tile = hs[cur];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const int sh = 16 * st + 8 * h;
+      const hub_bf16x8 a0 = expand((pc0 >> sh) & 0xffu), a1 = expand((pc1 >> sh) & 0xffu);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (j < nb) {
+#pragma unroll
+          for (int part = 0; part < 3; ++part) {
+            const hub_bf16x8 b = __builtin_bit_cast(
+                hub_bf16x8, *reinterpret_cast<const hub_u32x4 *>(tile + (part * 256 + 32 * j + r32) * kHubLds + 16 * st + 8 * h));
+            acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a0, acc[0][j], 0, 0, 0);
+            acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a1, acc[1][j], 0, 0, 0);
+          }
+        }
+      }
+    }
+    if (ct + 1 < ct1) store(cur ^ 1);
+    __syncthreads();
+  }
+  // partial sums of this group: rows hrow0 (+32), features 32 j + 8 q + 4 h .. +3
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    float *dst = p.part + ((int64_t)g * p.rows + hrow0 + 32 * i) * p.ld_part + 4 * p.c4_off;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int f = 32 * j + 8 * q + 4 * h;
+        if (f < 4 * p.c4_cnt)
+          *reinterpret_cast<float4 *>(dst + f) =
+              make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+      }
+  }
+}
+
+// Start value of every hub row: its block sum (groups added in group order),
+// plus, with accum_lo, what an inner row held before.  One wave per hub row.
+__global__ __launch_bounds__(256) void hub_combine_kernel(AggParams p, HubParams hp) {
+  const int i = blockIdx.x * 4 + threadIdx.x / 64, lane = threadIdx.x % 64;
+  if (i >= hp.rows || lane >= p.c4_cnt) return;
+  const int r = hp.row_ids[i];
+  if (r < 0) return;
+  const int c = 4 * (p.c4_off + lane);
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int g = 0; g < hp.groups; ++g)
+    v = add4(v, *reinterpret_cast<const float4 *>(hp.part + ((int64_t)g * hp.rows + i) * hp.ld_part + c));
+  float *o = out_row(p, r);
+  if (p.accum_lo && r < p.out_split) v = add4(*reinterpret_cast<const float4 *>(o + c), v);
+  *reinterpret_cast<float4 *>(o + c) = v;
+}
+
 template <int SL>
 static void launch_sl(AggParams p, hipStream_t s) {
   constexpr int U = 8;
@@ -356,16 +550,20 @@ static int col_launches(int f4, ColLaunch *out, int max_out) {
   return n;
 }
 
+// [split-row partial slots | dense-block sums of every group | tile images of the block's columns]
 size_t aggregate_workspace(const Plan &plan, int64_t f) {
   const int64_t ld_part = (f + 3) / 4 * 4;
-  return (size_t)plan.slots * (size_t)ld_part * sizeof(float);
+  const size_t sums = ((size_t)plan.slots + (size_t)plan.hub.groups * (size_t)plan.hub.rows) * (size_t)ld_part * 4;
+  return sums + (size_t)(plan.hub.cols / kHubColTile) * (size_t)kHubImage;
 }
 
 int launch_aggregate(const AggArgs &a, hipStream_t s) {
   const Plan &plan = *a.plan;
   if (plan.items.empty()) return PGCN_OK;
   AggParams p{};
-  p.col = a.col;
+  const Hub &hub = plan.hub;
+  p.col = hub.rows > 0 ? plan.d_col_rest : a.col;     // with a dense block the items index the rest
+  p.hub_init = hub.rows > 0 ? hub.d_init : nullptr;
   p.in_split = a.in_split;
   p.in_lo = a.in_lo;
   p.in_hi = a.in_hi;
@@ -403,6 +601,39 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
     {
       TraceScope ts(a.trace_kind, s);      // one record for the chunk launches, which run back to back
       int32_t launched = 0;
+      if (hub.rows > 0) {                  // block sums first: the rows' items add onto them
+        HubParams hp{};
+        hp.row_ids = hub.d_row_ids;
+        hp.col_ids = hub.d_col_ids;
+        hp.bits = hub.d_bits;
+        hp.rows = hub.rows;
+        hp.ntiles = hub.cols / kHubColTile;
+        hp.groups = hub.groups;
+        hp.tiles_per_group = (hp.ntiles + hub.groups - 1) / hub.groups;
+        hp.in_split = a.in_split;
+        hp.in_lo = a.in_lo;
+        hp.in_hi = a.in_hi;
+        hp.ld_in = a.ld_in;
+        hp.c4_off = cl[li].off;
+        hp.c4_cnt = cl[li].cnt < 64 ? cl[li].cnt : 64;
+        hp.ld_part = p.ld_part;
+        hp.part = a.partials + (size_t)plan.slots * (size_t)p.ld_part;
+        hp.img = reinterpret_cast<uint16_t *>(hp.part + (size_t)hub.groups * (size_t)hub.rows * (size_t)p.ld_part);
+        for (int c0 = cl[li].off; c0 < cl[li].off + cl[li].cnt; c0 += 64) {   // at most 64 float4 per pass
+          hp.c4_off = c0;
+          hp.c4_cnt = cl[li].off + cl[li].cnt - c0 < 64 ? cl[li].off + cl[li].cnt - c0 : 64;
+          hipLaunchKernelGGL(hub_split_kernel, dim3((unsigned)hp.ntiles), dim3(256), 0, s, hp);
+          PGCN_HIP(hipGetLastError());
+          hipLaunchKernelGGL(hub_kernel, dim3((unsigned)(hub.rows / kHubRowTile * hub.groups)), dim3(256), 0, s, hp);
+          PGCN_HIP(hipGetLastError());
+          AggParams pc = p;
+          pc.c4_off = hp.c4_off;
+          pc.c4_cnt = hp.c4_cnt;
+          hipLaunchKernelGGL(hub_combine_kernel, dim3((unsigned)((hub.rows + 3) / 4)), dim3(256), 0, s, pc, hp);
+          PGCN_HIP(hipGetLastError());
+          launched += 3;
+        }
+      }
       for (int c = 0; c < C; ++c) {
         p.mode = (c == 0 ? AGG_FIRST : 0) | (c == C - 1 ? AGG_LAST : 0);
         const int64_t b = plan.chunk_items[c], e = plan.chunk_items[c + 1];

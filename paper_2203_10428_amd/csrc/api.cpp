@@ -29,7 +29,8 @@ int64_t ldw(int64_t f) { return (f + 7) / 8 * 8; }
 // forward: split-row partials, plus an fp32 running sum over the column chunks
 // when the caller keeps no fp32 A (bf16 path)
 size_t fwd_acc_bytes(const pgcn_partition *p, int32_t f_in, int32_t gemm_dtype) {
-  if (agg_plan(p, false, f_in).chunks <= 1 || gemm_dtype != PGCN_BF16) return 0;
+  const Plan &pl = agg_plan(p, false, f_in);
+  if ((pl.chunks <= 1 && pl.hub.rows == 0) || gemm_dtype != PGCN_BF16) return 0;
   return align_up((size_t)p->n_inner * (size_t)ld4(f_in) * sizeof(float), 256);
 }
 // forward workspace: [aggregation partials | running sum | packed weights]
@@ -382,7 +383,7 @@ extern "C" int pgcn_layer_fwd(const pgcn_partition *p, const pgcn_fwd_args *a, h
   g.ld_out = a->ld_in;
   g.ld_bf16 = a->ld_in;
   g.partials = (float *)a->workspace;
-  if (!a->A && g.plan->chunks > 1) {   // running sum over chunks in the workspace
+  if (!a->A && (g.plan->chunks > 1 || g.plan->hub.rows > 0)) {   // running sum over chunks (and the block sum)
     g.out_lo = (float *)((char *)a->workspace + align_up(aggregate_workspace(*g.plan, a->f_in), 256));
     g.ld_out = ld4(a->f_in);
   }
@@ -793,7 +794,7 @@ extern "C" int pgcn_sage_layer_fwd(const pgcn_partition *p, const pgcn_sage_fwd_
   g.ld_out = a->ld_in;
   g.ld_bf16 = a->ld_in;
   g.partials = (float *)a->workspace;
-  if (!a->A && g.plan->chunks > 1) {
+  if (!a->A && (g.plan->chunks > 1 || g.plan->hub.rows > 0)) {
     g.out_lo = (float *)((char *)a->workspace + align_up(aggregate_workspace(*g.plan, a->f_in), 256));
     g.ld_out = ld4(a->f_in);
   }

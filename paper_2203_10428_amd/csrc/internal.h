@@ -35,6 +35,28 @@ struct SplitRow {
 // (items[.. chunk_whole[c])), then one item per other row's run, longest
 // first.  Split rows own `slots` partial slots in total, contiguous per row in
 // (chunk, segment) order; `splits` lists them for the fix-up pass.
+// Dense block of the matrix taken by the matrix cores instead of the gather:
+// the hub rows (most non-zeros) x the hub columns (most referenced), as one
+// bit per (row, column).  The block's sum of each hub row is formed first
+// (workgroups of kHubRowTile rows, column tiles of kHubColTile staged in LDS,
+// the gathered rows split exactly into three bf16 parts, fp32 accumulation;
+// `groups` workgroups share a row tile, each over its own range of column
+// tiles, and their partial sums are added in group order), and the plan's
+// items then add the rest of the row onto it.
+constexpr int kHubRowTile = 256;
+constexpr int kHubColTile = 32;
+struct Hub {
+  int32_t rows = 0, rows_real = 0;      // hub rows, padded to kHubRowTile (padding: row id -1)
+  int32_t cols = 0, cols_real = 0;      // hub columns, padded to kHubColTile (padding: column id -1)
+  int32_t groups = 1;
+  int64_t nnz = 0;                      // non-zeros inside the block
+  std::vector<int32_t> row_ids, col_ids;
+  std::vector<uint32_t> bits;           // [rows][cols / kHubColTile]: bit k = column tile*32 + k
+  std::vector<uint32_t> init;           // over all output rows: the row starts from its block sum
+  int32_t *d_row_ids = nullptr, *d_col_ids = nullptr;
+  uint32_t *d_bits = nullptr, *d_init = nullptr;
+};
+
 struct Plan {
   int32_t chunks = 1;
   std::vector<WorkItem> items;
@@ -43,6 +65,11 @@ struct Plan {
   int64_t slots = 0;            // partial slots of all split rows
   WorkItem *d_items = nullptr;
   SplitRow *d_splits = nullptr;
+  Hub hub;                      // hub.rows == 0: no dense block
+  // with a dense block the items index the matrix without it (col_rest); otherwise the
+  // partition's column array
+  std::vector<int32_t> col_rest;
+  int32_t *d_col_rest = nullptr;
 };
 
 }  // namespace pgcn

@@ -78,6 +78,126 @@ static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz, bool tra
   return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, 16));
 }
 
+// Cost of one (row, column) pair of a dense block on the matrix cores, in
+// units of one gathered non-zero of the same width, measured on MI355X for
+// 1 KB rows: the block (split, products, combine) takes 1.6 ps per pair, and
+// each non-zero it takes off the gather saves 28.5 ps there (the block's
+// columns are the most referenced rows, mostly served by the L2, so they cost
+// the gather less than its average non-zero).
+constexpr double kHubPairCost = 0.057;
+
+static int64_t env_int(const char *name, int64_t dflt) {
+  const char *v = std::getenv(name);
+  return v ? std::atoll(v) : dflt;
+}
+
+// The dense block of a CSR matrix for the matrix cores: the rows with the
+// most non-zeros x the most referenced columns, sizes on a grid of
+// 512 x 2^i (and the full extent), chosen to maximise the non-zeros moved off
+// the gather minus kHubPairCost x the block's area; no block when that saving
+// is under 5% of the non-zeros or the matrix is small.  PGCN_HUB=0 disables
+// it; PGCN_HUB_ROWS / PGCN_HUB_COLS force its size (tests).  Fills the block's
+// rows, columns and bits, and the matrix without the block (rowptr_rest,
+// col_rest; columns stay ascending).
+static void choose_hub(const std::vector<int64_t> &rowptr, const std::vector<int32_t> &col, int64_t nrows,
+                       int64_t ncols, Hub &h, std::vector<int64_t> &rowptr_rest, std::vector<int32_t> &col_rest) {
+  h = Hub();
+  rowptr_rest.clear();
+  col_rest.clear();
+  const int64_t nnz = (int64_t)col.size();
+  if (env_int("PGCN_HUB", 1) == 0 || nrows == 0 || ncols == 0 || nnz == 0) return;
+  const int64_t force_r = env_int("PGCN_HUB_ROWS", 0), force_c = env_int("PGCN_HUB_COLS", 0);
+  // ranks: rows by decreasing length, columns by decreasing reference count (ties by id)
+  std::vector<int64_t> ccount(ncols, 0);
+  for (int32_t c : col) ccount[c]++;
+  std::vector<int64_t> rord(nrows), cord(ncols);
+  std::iota(rord.begin(), rord.end(), 0);
+  std::iota(cord.begin(), cord.end(), 0);
+  std::stable_sort(rord.begin(), rord.end(),
+                   [&](int64_t a, int64_t b) { return rowptr[a + 1] - rowptr[a] > rowptr[b + 1] - rowptr[b]; });
+  std::stable_sort(cord.begin(), cord.end(), [&](int64_t a, int64_t b) { return ccount[a] > ccount[b]; });
+  std::vector<int64_t> rrank(nrows), crank(ncols);
+  for (int64_t i = 0; i < nrows; ++i) rrank[rord[i]] = i;
+  for (int64_t i = 0; i < ncols; ++i) crank[cord[i]] = i;
+  int64_t R = 0, C = 0;
+  if (force_r > 0 && force_c > 0) {
+    R = std::min(force_r, nrows);
+    C = std::min(force_c, ncols);
+  } else {
+    if (force_r < 0 || force_c < 0 || nnz < (int64_t)1 << 20) return;
+    // grid sizes and a 2D histogram of the non-zeros by (row size class, column size class)
+    std::vector<int64_t> gr, gc;
+    for (int64_t v = 512; v < nrows; v *= 2) gr.push_back(v);
+    gr.push_back(nrows);
+    for (int64_t v = 512; v < ncols; v *= 2) gc.push_back(v);
+    gc.push_back(ncols);
+    auto cls = [](const std::vector<int64_t> &g, int64_t rank) {
+      return (int64_t)(std::upper_bound(g.begin(), g.end(), rank) - g.begin());
+    };
+    const int64_t nr = (int64_t)gr.size(), nc = (int64_t)gc.size();
+    std::vector<int64_t> hist((size_t)nr * nc, 0);
+    for (int64_t r = 0; r < nrows; ++r) {
+      const int64_t a = cls(gr, rrank[r]);
+      for (int64_t k = rowptr[r]; k < rowptr[r + 1]; ++k) hist[(size_t)a * nc + cls(gc, crank[col[k]])]++;
+    }
+    double best = 0.05 * (double)nnz;
+    for (int64_t i = 0; i < nr; ++i)
+      for (int64_t j = 0; j < nc; ++j) {
+        int64_t in = 0;
+        for (int64_t a = 0; a <= i; ++a)
+          for (int64_t b = 0; b <= j; ++b) in += hist[(size_t)a * nc + b];
+        const double net = (double)in - kHubPairCost * (double)gr[i] * (double)gc[j];
+        if (net > best) {
+          best = net;
+          R = gr[i];
+          C = gc[j];
+        }
+      }
+    if (R == 0) return;
+  }
+  // hub rows and columns in ascending id; positions of the columns
+  std::vector<int32_t> rows, cols;
+  for (int64_t r = 0; r < nrows; ++r)
+    if (rrank[r] < R) rows.push_back((int32_t)r);
+  for (int64_t c = 0; c < ncols; ++c)
+    if (crank[c] < C) cols.push_back((int32_t)c);
+  std::vector<int32_t> cpos(ncols, -1);
+  for (size_t i = 0; i < cols.size(); ++i) cpos[cols[i]] = (int32_t)i;
+  h.rows_real = (int32_t)rows.size();
+  h.cols_real = (int32_t)cols.size();
+  h.rows = (h.rows_real + kHubRowTile - 1) / kHubRowTile * kHubRowTile;
+  h.cols = (h.cols_real + kHubColTile - 1) / kHubColTile * kHubColTile;
+  h.row_ids.assign(h.rows, -1);
+  std::copy(rows.begin(), rows.end(), h.row_ids.begin());
+  h.col_ids.assign(h.cols, -1);
+  std::copy(cols.begin(), cols.end(), h.col_ids.begin());
+  const int64_t ntiles = h.cols / kHubColTile;
+  h.bits.assign((size_t)h.rows * ntiles, 0u);
+  h.init.assign((size_t)(nrows + 31) / 32, 0u);
+  std::vector<int32_t> rpos(nrows, -1);
+  for (size_t i = 0; i < rows.size(); ++i) {
+    rpos[rows[i]] = (int32_t)i;
+    h.init[rows[i] >> 5] |= 1u << (rows[i] & 31);
+  }
+  rowptr_rest.assign(nrows + 1, 0);
+  col_rest.reserve(nnz);
+  for (int64_t r = 0; r < nrows; ++r) {
+    for (int64_t k = rowptr[r]; k < rowptr[r + 1]; ++k) {
+      const int32_t c = col[k];
+      if (rpos[r] >= 0 && cpos[c] >= 0) {
+        h.bits[(size_t)rpos[r] * ntiles + cpos[c] / kHubColTile] |= 1u << (cpos[c] % kHubColTile);
+        h.nnz++;
+      } else {
+        col_rest.push_back(c);
+      }
+    }
+    rowptr_rest[r + 1] = (int64_t)col_rest.size();
+  }
+  // workgroups sharing a row tile, each over its own range of column tiles: about one per CU
+  const int64_t row_tiles = h.rows / kHubRowTile;
+  h.groups = (int32_t)std::max<int64_t>(1, std::min<int64_t>(ntiles, (256 + row_tiles / 2) / row_tiles));
+}
+
 // Work plan of one aggregation.  A row whose run inside some chunk is longer
 // than `segment` is a split row: every run of it, in every chunk, is cut into
 // segments of at most `segment` non-zeros that write partial slots; the row's
@@ -167,6 +287,14 @@ static void free_device(pgcn_partition *p) {
                   p->plan_n.d_items, p->plan_n.d_splits, p->plan_tn.d_items, p->plan_tn.d_splits};
   for (void *q : ptrs)
     if (q) (void)hipFree(q);
+  for (Plan *q : {&p->plan, &p->plan_t}) {
+    void *hp[] = {q->d_col_rest, q->hub.d_row_ids, q->hub.d_col_ids, q->hub.d_bits, q->hub.d_init};
+    for (void *x : hp)
+      if (x) (void)hipFree(x);
+    q->d_col_rest = nullptr;
+    q->hub.d_row_ids = q->hub.d_col_ids = nullptr;
+    q->hub.d_bits = q->hub.d_init = nullptr;
+  }
   p->d_col = p->d_col_t = p->d_send_idx = p->d_inv_k = nullptr;
   p->d_inv_ptr = nullptr;
   p->d_inv_deg = p->d_sym_scale = nullptr;
@@ -416,8 +544,14 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
     const int32_t c = choose_chunks(n_in, n_all, nnz, false, wide), ct = choose_chunks(n_all, n_in, nnz, true, wide);
     const int32_t cn = choose_chunks(n_in, n_all, nnz, false, narrow);
     const int32_t ctn = choose_chunks(n_all, n_in, nnz, true, narrow);
-    build_plan(p->rowptr, p->col, n_in, n_all, p->segment, c, p->plan);
-    build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, ct, p->plan_t);
+    // the wide plans may take a dense block on the matrix cores; their items then index the rest
+    std::vector<int64_t> rp_rest;
+    choose_hub(p->rowptr, p->col, n_in, n_all, p->plan.hub, rp_rest, p->plan.col_rest);
+    if (p->plan.hub.rows > 0) build_plan(rp_rest, p->plan.col_rest, n_in, n_all, p->segment, c, p->plan);
+    else build_plan(p->rowptr, p->col, n_in, n_all, p->segment, c, p->plan);
+    choose_hub(p->rowptr_t, p->col_t, n_all, n_in, p->plan_t.hub, rp_rest, p->plan_t.col_rest);
+    if (p->plan_t.hub.rows > 0) build_plan(rp_rest, p->plan_t.col_rest, n_all, n_in, p->segment, ct, p->plan_t);
+    else build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, ct, p->plan_t);
     p->plan_n.chunks = p->plan_tn.chunks = 0;
     if (cn != c) build_plan(p->rowptr, p->col, n_in, n_all, p->segment, cn, p->plan_n);
     if (ctn != ct) build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, ctn, p->plan_tn);
@@ -441,6 +575,13 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
     if (!rc) rc = upload(&p->plan_n.d_splits, p->plan_n.splits);
     if (!rc) rc = upload(&p->plan_tn.d_items, p->plan_tn.items);
     if (!rc) rc = upload(&p->plan_tn.d_splits, p->plan_tn.splits);
+    for (Plan *q : {&p->plan, &p->plan_t}) {
+      if (!rc) rc = upload(&q->d_col_rest, q->col_rest);
+      if (!rc) rc = upload(&q->hub.d_row_ids, q->hub.row_ids);
+      if (!rc) rc = upload(&q->hub.d_col_ids, q->hub.col_ids);
+      if (!rc) rc = upload(&q->hub.d_bits, q->hub.bits);
+      if (!rc) rc = upload(&q->hub.d_init, q->hub.init);
+    }
     if (rc) return rc;
     p->d_row_scale = p->symmetric ? p->d_sym_scale : p->d_inv_deg;
     p->d_col_scale = p->symmetric ? p->d_sym_scale : nullptr;
@@ -471,6 +612,12 @@ extern "C" int pgcn_partition_info(const pgcn_partition *p, pgcn_info *o) try {
   o->spmmt_chunks = p->plan_t.chunks;
   o->spmm_chunks_narrow = p->plan_n.chunks ? p->plan_n.chunks : p->plan.chunks;
   o->spmmt_chunks_narrow = p->plan_tn.chunks ? p->plan_tn.chunks : p->plan_t.chunks;
+  o->spmm_hub_rows = p->plan.hub.rows_real;
+  o->spmm_hub_cols = p->plan.hub.cols_real;
+  o->spmm_hub_nnz = p->plan.hub.nnz;
+  o->spmmt_hub_rows = p->plan_t.hub.rows_real;
+  o->spmmt_hub_cols = p->plan_t.hub.cols_real;
+  o->spmmt_hub_nnz = p->plan_t.hub.nnz;
   o->symmetric = p->symmetric;
   o->self_loop = p->self_loop;
   return PGCN_OK;

@@ -13,13 +13,14 @@ Error model (standard forward error analysis of sums of products, Higham,
 "Accuracy and Stability of Numerical Algorithms", 2nd ed., Sec. 3.1):
 |fl(sum_k x_k y_k) - sum_k x_k y_k| <= gamma_n sum_k |x_k y_k|, with
 gamma_n = n u / (1 - n u) for n terms in any order.  One GCN output is
-Z_vc = sum_u P_vu sum_k X_uk W_kc.  The GPU sums the d_v rows of P (plus up to
-four roundings for the 1/d or d^-1/2 scales and their products) and K
-products, in fp32; on the bf16 path both product operands are first rounded
-once to bf16 (nearest even).  So
+Z_vc = sum_u P_vu sum_k X_uk W_kc.  The GPU sums the d_v rows of P (each as
+one term, or as three exact bf16 parts in the dense block the matrix cores
+take, plus up to four roundings for the 1/d or d^-1/2 scales and their
+products) and K products, in fp32; on the bf16 path both product operands are
+first rounded once to bf16 (nearest even).  So
 
     |Z_gpu - Z| <= c_v (P|X|)|W| + (1 + c_v) (P E_X)|W|,
-    c_v = (1 + b)^2 (1 + 2^-24) (1 + gamma_K) (1 + gamma_{d_v + 4}) - 1,
+    c_v = (1 + b)^2 (1 + 2^-24) (1 + gamma_K) (1 + gamma_{3 d_v + 4}) - 1,
 
 with b = 2^-8 on the bf16 path and 0 on the fp32 path, 2^-24 for the weights
 handed over in fp32, and E_X a bound on the
@@ -50,7 +51,9 @@ def product_factor(dt: str, K: int, row_terms: np.ndarray) -> np.ndarray:
     """c_v per output row (column vector) for K products and row_terms aggregated rows."""
     b = UBF16 if dt == "bf16" else 0.0
     w = 2.0 ** -24                     # the weights are handed to the GPU rounded to fp32
-    return ((1.0 + b) ** 2 * (1.0 + w) * (1.0 + gamma(K)) * (1.0 + gamma(np.asarray(row_terms) + 4)) - 1.0)[:, None]
+    # each aggregated row may enter as three exact bf16 parts (the dense block on the matrix cores)
+    return ((1.0 + b) ** 2 * (1.0 + w) * (1.0 + gamma(K)) * (1.0 + gamma(3 * np.asarray(row_terms) + 4))
+            - 1.0)[:, None]
 
 
 def row_lengths(P) -> np.ndarray:

@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
     for s in syms:
         assert getattr(B.lib, s) is not None
     header = open(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "pgcn.h")).read()
-    assert B.pgcn_version() == int(re.search(r"#define PGCN_VERSION (\d+)", header).group(1)) == 164
+    assert B.pgcn_version() == int(re.search(r"#define PGCN_VERSION (\d+)", header).group(1)) == 165
 
 
 def compare(g_n, rowptr, col, owner, nparts, part, self_loop=True):
@@ -278,3 +278,33 @@ def test_binding_structs_match_the_header(tmp_path):
         assert int(c_side[name]) == C.sizeof(cls), name
         for field, _ in cls._fields_:
             assert int(c_side[f"{name}.{field}"]) == getattr(cls, field).offset, f"{name}.{field}"
+
+
+def test_dense_block_selection(monkeypatch):
+    """PGCN_HUB_ROWS / _COLS force a dense block: the rows with the most non-zeros and the most
+    referenced columns (ties by id); its non-zeros counted as set-up counts them, both directions."""
+    from gpu_helpers import random_partition_graph
+    n, rowptr, col, owner = random_partition_graph(1500, 900, 3, 30, 4, hub_deg=800)
+    ref = build_partition(n, rowptr, col, owner, 0, 3)
+    monkeypatch.setenv("PGCN_HUB_ROWS", "300")
+    monkeypatch.setenv("PGCN_HUB_COLS", "700")
+    info = B.pgcn_partition_info(B.pgcn_partition_setup(n, rowptr, col, owner, 3, 0, host_only=True))
+
+    def block_nnz(rp, cl, nrows, ncols, R, C):
+        lens = np.diff(rp)
+        top_r = np.argsort(-lens, kind="stable")[:R]
+        cnt = np.bincount(cl, minlength=ncols)
+        top_c = np.zeros(ncols, bool)
+        top_c[np.argsort(-cnt, kind="stable")[:C]] = True
+        return int(sum(top_c[cl[rp[r]:rp[r + 1]]].sum() for r in top_r))
+
+    nr, nc = ref.n_inner, ref.n_inner + ref.n_bd
+    assert (info["spmm_hub_rows"], info["spmm_hub_cols"]) == (300, 700)
+    assert info["spmm_hub_nnz"] == block_nnz(ref.rowptr, ref.col, nr, nc, 300, 700) > 0
+    assert (info["spmmt_hub_rows"], info["spmmt_hub_cols"]) == (300, 700)
+    assert info["spmmt_hub_nnz"] == block_nnz(ref.rowptr_t, ref.col_t, nc, nr, 300, 700) > 0
+    # the set-up arrays themselves do not change
+    compare(n, rowptr, col, owner, 3, 0)
+    monkeypatch.setenv("PGCN_HUB", "0")
+    info = B.pgcn_partition_info(B.pgcn_partition_setup(n, rowptr, col, owner, 3, 0, host_only=True))
+    assert info["spmm_hub_rows"] == 0 and info["spmmt_hub_rows"] == 0
