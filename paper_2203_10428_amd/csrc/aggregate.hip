@@ -282,44 +282,57 @@ __global__ __launch_bounds__(256) void agg_fixup_kernel(AggParams p, const Split
 // ------------------------------------------------------------ dense block ---
 //
 // Block sums on the matrix cores: S[r] = sum over hub columns c of bit(r, c) H[c]
-// for the hub rows r.  First hub_split_kernel writes, per tile of kHubColTile =
-// 32 hub columns, the tile's gathered rows (this launch's float4 slice) as
-// three bf16 parts (hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi - mid):
-// x = hi + mid + lo exactly for normal fp32 x), feature-major with the 32
-// columns contiguous, in exactly the layout the MFMA loop reads from LDS (a
-// tile image).  hub_kernel: a workgroup (4 waves) owns kHubRowTile = 256 hub
-// rows (64 per wave) and a range of column tiles; it copies the next tile
-// image to registers while multiplying the current one from LDS (double
-// buffered): v_mfma_f32_32x32x16_bf16 multiplies the 0/1 bits (bf16 1.0 or 0,
-// exact) by each part with fp32 accumulation, so the products are exact and
-// only the fp32 sums round, as in the gather.  Each fragment of a part feeds
-// the wave's two 32-row halves.  The bits of a row for a tile are one 32-bit
-// word.  Operand layout as in the update GEMMs: the feature side is the
-// MFMA's first operand, so lane l holds hub row l % 32 (of its half) and
-// registers 4q .. 4q+3 of block j hold features 32 j + 8 q + 4 (l / 32) .. +3;
-// lane half h supplies columns 16 s + 8 h .. +7 of k-step s on both sides.
+// for the hub rows r.  First hub_split_kernel (four workgroups per tile, two
+// columns per thread) writes, per tile of kHubColTile =
+// 32 hub columns and per block of 32 features of this launch's float4 slice,
+// the tile's gathered rows as three bf16 parts (hi = bf16(x), mid = bf16(x -
+// hi), lo = bf16(x - hi - mid): x = hi + mid + lo exactly for normal fp32 x),
+// feature-major with the 32 columns contiguous, in exactly the layout the
+// MFMA loop reads from LDS (an image of kHubImage bytes).  hub_kernel: a
+// workgroup (4 waves) owns kHubRowTile = 512 hub rows (128 per wave), one
+// feature block and a range of column tiles; it copies the next image into
+// LDS while multiplying the current one (double buffered), several
+// workgroups per CU.  v_mfma_f32_32x32x16_bf16 multiplies each part by the
+// 0/1 bits (bf16 1.0 or 0, exact) with fp32 accumulation, so the products
+// are exact and only the fp32 sums round, as in the gather.  Each fragment of
+// a part read from LDS feeds the wave's four 32-row quarters.  The bits of a
+// row for a tile are one 32-bit word, stored tile-major so that a wave's 32
+// rows load as one contiguous 128-byte access.  Operand layout as in the update GEMMs:
+// the feature side is the MFMA's first operand, so lane l holds hub row
+// l % 32 (of its quarter) and registers 4q .. 4q+3 hold features
+// 8q + 4(l / 32) .. +3 of the block; lane half h supplies columns
+// 16 s + 8 h .. +7 of k-step s on both sides.  Column ranges ("groups") write
+// partial sums that hub_combine_kernel adds in range order.
 
 typedef float hub_f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 hub_bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int hub_u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kHubLds = 40;                                  // bf16 per feature row: 32 columns + 8 pad
-constexpr int kHubImage = 3 * 256 * kHubLds * 2;             // bytes of one tile image (61,440)
-constexpr int kHubImageVec = kHubImage / 16 / 256;           // 16-byte vectors per thread (15)
+constexpr int kHubLds = 40;                  // bf16 per feature row of an image: 32 columns + 8 pad
+constexpr int kHubImage = 8192;              // bytes per (tile, feature block): 3 x 32 x 40 bf16 = 7,680, padded
+constexpr int kHubFeatBlocks = 8;            // feature blocks of a 64-float4 slice
+constexpr int kHubTargetWgs = 512;           // workgroups per launch the column ranges aim at
 
 struct HubParams {
   const int32_t *row_ids;          // [rows]  output row of each hub row (-1: padding)
   const int32_t *col_ids;          // [cols]  gathered row of each hub column (-1: padding)
-  const uint32_t *bits;            // [rows][ntiles]
-  int32_t rows, ntiles, tiles_per_group, groups;
+  const uint32_t *bits;            // [ntiles][rows]
+  int32_t rows, ntiles, tiles_per_group, groups, nfb;
   int64_t in_split;
   const float *in_lo, *in_hi;
   int64_t ld_in;
   int32_t c4_off, c4_cnt;          // float4 columns of this pass (at most 64)
-  uint16_t *img;                   // [ntiles] tile images of this pass
-  float *part;                     // [groups][rows][ld_part] block sums of each group
+  uint16_t *img;                   // [kHubFeatBlocks][ntiles] images of this pass
+  float *part;                     // [groups][rows][ld_part] block sums of each column range
   int64_t ld_part;
 };
+
+// Column ranges of a pass over nfb feature blocks: about kHubTargetWgs workgroups.
+static int hub_groups(const Hub &h, int nfb) {
+  const int64_t per = (int64_t)(h.rows / kHubRowTile) * nfb;
+  const int64_t g = (kHubTargetWgs + per / 2) / per;
+  return (int)std::max<int64_t>(1, std::min<int64_t>(g, h.cols / kHubColTile));
+}
 
 __device__ __forceinline__ uint16_t hub_bf16(float x) {
   uint32_t b = __float_as_uint(x);
@@ -328,72 +341,73 @@ __device__ __forceinline__ uint16_t hub_bf16(float x) {
 }
 __device__ __forceinline__ float hub_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-// One workgroup per tile: thread (w, l) splits columns 8 w .. 8 w + 7 of features 4 l .. 4 l + 3.
+// Four workgroups per tile (b = 4 tile + quarter): thread (w, l) splits columns
+// 8 quarter + 2 w and + 1 of features 4 l .. 4 l + 3.
 __global__ __launch_bounds__(256) void hub_split_kernel(HubParams p) {
-  const int ct = blockIdx.x, t = threadIdx.x, lane = t & 63;
+  const int ct = blockIdx.x >> 2, t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int c0 = 8 * (blockIdx.x & 3) + 2 * wave;
   const bool f4_ok = lane < p.c4_cnt;
   const int cb = 4 * (p.c4_off + lane);
-  float4 x8[8];
+  float4 x2[2];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int c = p.col_ids[ct * kHubColTile + 8 * wave + e];
+  for (int e = 0; e < 2; ++e) {
+    const int c = p.col_ids[ct * kHubColTile + c0 + e];
     const float *src = nullptr;
     if (c >= 0) {
       if (c < p.in_split) src = p.in_lo + (int64_t)c * p.ld_in;
       else if (p.in_hi) src = p.in_hi + (int64_t)(c - p.in_split) * p.ld_in;
     }
-    x8[e] = (f4_ok && src) ? *reinterpret_cast<const float4 *>(src + cb) : make_float4(0.f, 0.f, 0.f, 0.f);
+    x2[e] = (f4_ok && src) ? *reinterpret_cast<const float4 *>(src + cb) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  uint16_t *img = p.img + (int64_t)ct * (kHubImage / 2);
+  // features 4 lane .. 4 lane + 3 all sit in feature block lane / 8, rows 4 (lane % 8) .. +3
+  uint16_t *img = p.img + ((int64_t)(lane >> 3) * p.ntiles + ct) * (kHubImage / 2);
 #pragma unroll
   for (int fe = 0; fe < 4; ++fe) {
-    uint16_t hi[8], mi[8], lo[8];
+    uint32_t v[3] = {0u, 0u, 0u};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float x = fe == 0 ? x8[e].x : fe == 1 ? x8[e].y : fe == 2 ? x8[e].z : x8[e].w;
-      hi[e] = hub_bf16(x);
-      const float r1 = x - hub_f32(hi[e]);
-      mi[e] = hub_bf16(r1);
-      lo[e] = hub_bf16(r1 - hub_f32(mi[e]));
+    for (int e = 0; e < 2; ++e) {
+      const float x = fe == 0 ? x2[e].x : fe == 1 ? x2[e].y : fe == 2 ? x2[e].z : x2[e].w;
+      const uint16_t hi = hub_bf16(x);
+      const float r1 = x - hub_f32(hi);
+      const uint16_t mi = hub_bf16(r1);
+      const uint16_t lo = hub_bf16(r1 - hub_f32(mi));
+      v[0] |= (uint32_t)hi << (16 * e);
+      v[1] |= (uint32_t)mi << (16 * e);
+      v[2] |= (uint32_t)lo << (16 * e);
     }
-    hub_u32x4 vh, vm, vl;
+    const int fl = 4 * (lane & 7) + fe;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      vh[w] = (uint32_t)hi[2 * w] | ((uint32_t)hi[2 * w + 1] << 16);
-      vm[w] = (uint32_t)mi[2 * w] | ((uint32_t)mi[2 * w + 1] << 16);
-      vl[w] = (uint32_t)lo[2 * w] | ((uint32_t)lo[2 * w + 1] << 16);
-    }
-    const int f = 4 * lane + fe;
-    *reinterpret_cast<hub_u32x4 *>(img + (0 * 256 + f) * kHubLds + 8 * wave) = vh;
-    *reinterpret_cast<hub_u32x4 *>(img + (1 * 256 + f) * kHubLds + 8 * wave) = vm;
-    *reinterpret_cast<hub_u32x4 *>(img + (2 * 256 + f) * kHubLds + 8 * wave) = vl;
+    for (int part = 0; part < 3; ++part)
+      *reinterpret_cast<uint32_t *>(img + (part * 32 + fl) * kHubLds + c0) = v[part];
   }
 }
 
+// Workgroup b: row tile b / (groups nfb), column range (b / nfb) % groups, feature block b % nfb.
 __global__ __launch_bounds__(256) void hub_kernel(HubParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t hs[2][kHubImage / 2];       // 122,880 bytes
+  __shared__ __attribute__((aligned(16))) uint16_t hs[2][kHubImage / 2];       // 16,384 bytes
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int rt = blockIdx.x / p.groups, g = blockIdx.x % p.groups;
+  const int fb = blockIdx.x % p.nfb, g = (blockIdx.x / p.nfb) % p.groups, rt = blockIdx.x / (p.nfb * p.groups);
   const int ct0 = g * p.tiles_per_group;
   const int ct1 = ct0 + p.tiles_per_group < p.ntiles ? ct0 + p.tiles_per_group : p.ntiles;
   const int h = lane >> 5, r32 = lane & 31;
-  const int hrow0 = rt * kHubRowTile + wave * 64 + r32;          // this lane's rows: hrow0, hrow0 + 32
+  const int hrow0 = rt * kHubRowTile + wave * 128 + r32;         // this lane's rows: hrow0 + 32 i, i < 4
+  const uint16_t *img = p.img + (int64_t)fb * p.ntiles * (kHubImage / 2);
 
-  hub_u32x4 stg[kHubImageVec];
-  uint32_t pat0 = 0, pat1 = 0;
+  hub_u32x4 stg[2];
+  uint32_t pat[4];
   auto load = [&](int ct) __attribute__((always_inline)) {
-    const hub_u32x4 *src = reinterpret_cast<const hub_u32x4 *>(p.img + (int64_t)ct * (kHubImage / 2));
+    const hub_u32x4 *src = reinterpret_cast<const hub_u32x4 *>(img + (int64_t)ct * (kHubImage / 2));
+    stg[0] = src[t];
+    stg[1] = src[t + 256];
 #pragma unroll
-    for (int v = 0; v < kHubImageVec; ++v) stg[v] = src[t + 256 * v];
-    pat0 = p.bits[(int64_t)hrow0 * p.ntiles + ct];
-    pat1 = p.bits[(int64_t)(hrow0 + 32) * p.ntiles + ct];
+    for (int i = 0; i < 4; ++i) pat[i] = p.bits[(int64_t)ct * p.rows + hrow0 + 32 * i];
   };
   auto store = [&](int buf) __attribute__((always_inline)) {
     hub_u32x4 *dst = reinterpret_cast<hub_u32x4 *>(hs[buf]);
-#pragma unroll
-    for (int v = 0; v < kHubImageVec; ++v) dst[t + 256 * v] = stg[v];
+    dst[t] = stg[0];
+    dst[t + 256] = stg[1];
   };
   auto expand = [](uint32_t byte) __attribute__((always_inline)) {
     hub_u32x4 aw;
@@ -403,12 +417,9 @@ __global__ __launch_bounds__(256) void hub_kernel(HubParams p) {
     return __builtin_bit_cast(hub_bf16x8, aw);
   };
 
-  hub_f32x16 acc[2][8];
+  hub_f32x16 acc[4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = (hub_f32x16){};
-  const int nb = (4 * p.c4_cnt + 31) / 32;                       // 32-feature blocks of this pass
+  for (int i = 0; i < 4; ++i) acc[i] = (hub_f32x16){};
   if (ct0 < ct1) {
     load(ct0);
     store(0);
@@ -416,42 +427,39 @@ __global__ __launch_bounds__(256) void hub_kernel(HubParams p) {
   __syncthreads();
   for (int ct = ct0; ct < ct1; ++ct) {
     const int cur = (ct - ct0) & 1;
-    const uint32_t pc0 = pat0, pc1 = pat1;
+    uint32_t pc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pc[i] = pat[i];
     if (ct + 1 < ct1) load(ct + 1);
     const uint16_t *tile = hs[cur];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
       const int sh = 16 * st + 8 * h;
-      const hub_bf16x8 a0 = expand((pc0 >> sh) & 0xffu), a1 = expand((pc1 >> sh) & 0xffu);
+      hub_bf16x8 a[4];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (j < nb) {
+      for (int i = 0; i < 4; ++i) a[i] = expand((pc[i] >> sh) & 0xffu);
 #pragma unroll
-          for (int part = 0; part < 3; ++part) {
-            const hub_bf16x8 b = __builtin_bit_cast(
-                hub_bf16x8, *reinterpret_cast<const hub_u32x4 *>(tile + (part * 256 + 32 * j + r32) * kHubLds + 16 * st + 8 * h));
-            acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a0, acc[0][j], 0, 0, 0);
-            acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a1, acc[1][j], 0, 0, 0);
-          }
-        }
+      for (int part = 0; part < 3; ++part) {
+        const hub_bf16x8 b = __builtin_bit_cast(
+            hub_bf16x8, *reinterpret_cast<const hub_u32x4 *>(tile + (part * 32 + r32) * kHubLds + 16 * st + 8 * h));
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a[i], acc[i], 0, 0, 0);
       }
     }
     if (ct + 1 < ct1) store(cur ^ 1);
     __syncthreads();
   }
-  // partial sums of this group: rows hrow0 (+32), features 32 j + 8 q + 4 h .. +3
+  // partial sums of this column range: rows hrow0 + 32 i, features 32 fb + 8 q + 4 h .. +3
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    float *dst = p.part + ((int64_t)g * p.rows + hrow0 + 32 * i) * p.ld_part + 4 * p.c4_off;
+  for (int i = 0; i < 4; ++i) {
+    float *dst = p.part + ((int64_t)g * p.rows + hrow0 + 32 * i) * p.ld_part + 4 * p.c4_off + 32 * fb;
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int f = 32 * j + 8 * q + 4 * h;
-        if (f < 4 * p.c4_cnt)
-          *reinterpret_cast<float4 *>(dst + f) =
-              make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-      }
+    for (int q = 0; q < 4; ++q) {
+      const int f = 32 * fb + 8 * q + 4 * h;
+      if (f < 4 * p.c4_cnt)
+        *reinterpret_cast<float4 *>(dst + 8 * q + 4 * h) =
+            make_float4(acc[i][4 * q], acc[i][4 * q + 1], acc[i][4 * q + 2], acc[i][4 * q + 3]);
+    }
   }
 }
 
@@ -550,11 +558,29 @@ static int col_launches(int f4, ColLaunch *out, int max_out) {
   return n;
 }
 
-// [split-row partial slots | dense-block sums of every group | tile images of the block's columns]
+// Feature blocks of a dense-block pass over cnt float4 columns.
+static int hub_nfb(int cnt) { return (4 * cnt + 31) / 32; }
+
+// Rows of dense-block partial sums an aggregation over rows of f floats needs: the most
+// that any of its passes uses.
+static int64_t hub_sum_rows(const Plan &plan, int64_t f) {
+  int64_t n = 0;
+  if (plan.hub.rows == 0) return 0;
+  ColLaunch cl[128];
+  const int ncl = col_launches((int)((f + 3) / 4), cl, 128);
+  for (int li = 0; li < ncl; ++li)
+    for (int c0 = cl[li].off; c0 < cl[li].off + cl[li].cnt; c0 += 64) {
+      const int cnt = std::min(64, cl[li].off + cl[li].cnt - c0);
+      n = std::max<int64_t>(n, (int64_t)hub_groups(plan.hub, hub_nfb(cnt)) * plan.hub.rows);
+    }
+  return n;
+}
+
+// [split-row partial slots | dense-block sums of every column range | images of the block's columns]
 size_t aggregate_workspace(const Plan &plan, int64_t f) {
   const int64_t ld_part = (f + 3) / 4 * 4;
-  const size_t sums = ((size_t)plan.slots + (size_t)plan.hub.groups * (size_t)plan.hub.rows) * (size_t)ld_part * 4;
-  return sums + (size_t)(plan.hub.cols / kHubColTile) * (size_t)kHubImage;
+  const size_t sums = ((size_t)plan.slots + (size_t)hub_sum_rows(plan, f)) * (size_t)ld_part * 4;
+  return sums + (size_t)(plan.hub.cols / kHubColTile) * kHubFeatBlocks * (size_t)kHubImage;
 }
 
 int launch_aggregate(const AggArgs &a, hipStream_t s) {
@@ -608,8 +634,6 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
         hp.bits = hub.d_bits;
         hp.rows = hub.rows;
         hp.ntiles = hub.cols / kHubColTile;
-        hp.groups = hub.groups;
-        hp.tiles_per_group = (hp.ntiles + hub.groups - 1) / hub.groups;
         hp.in_split = a.in_split;
         hp.in_lo = a.in_lo;
         hp.in_hi = a.in_hi;
@@ -618,13 +642,17 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
         hp.c4_cnt = cl[li].cnt < 64 ? cl[li].cnt : 64;
         hp.ld_part = p.ld_part;
         hp.part = a.partials + (size_t)plan.slots * (size_t)p.ld_part;
-        hp.img = reinterpret_cast<uint16_t *>(hp.part + (size_t)hub.groups * (size_t)hub.rows * (size_t)p.ld_part);
+        hp.img = reinterpret_cast<uint16_t *>(hp.part + (size_t)hub_sum_rows(plan, a.f) * (size_t)p.ld_part);
         for (int c0 = cl[li].off; c0 < cl[li].off + cl[li].cnt; c0 += 64) {   // at most 64 float4 per pass
           hp.c4_off = c0;
           hp.c4_cnt = cl[li].off + cl[li].cnt - c0 < 64 ? cl[li].off + cl[li].cnt - c0 : 64;
-          hipLaunchKernelGGL(hub_split_kernel, dim3((unsigned)hp.ntiles), dim3(256), 0, s, hp);
+          hp.nfb = hub_nfb(hp.c4_cnt);
+          hp.groups = hub_groups(hub, hp.nfb);
+          hp.tiles_per_group = (hp.ntiles + hp.groups - 1) / hp.groups;
+          hipLaunchKernelGGL(hub_split_kernel, dim3((unsigned)(4 * hp.ntiles)), dim3(256), 0, s, hp);
           PGCN_HIP(hipGetLastError());
-          hipLaunchKernelGGL(hub_kernel, dim3((unsigned)(hub.rows / kHubRowTile * hub.groups)), dim3(256), 0, s, hp);
+          hipLaunchKernelGGL(hub_kernel, dim3((unsigned)(hub.rows / kHubRowTile * hp.groups * hp.nfb)), dim3(256), 0,
+                             s, hp);
           PGCN_HIP(hipGetLastError());
           AggParams pc = p;
           pc.c4_off = hp.c4_off;

@@ -40,18 +40,17 @@ struct SplitRow {
 // bit per (row, column).  The block's sum of each hub row is formed first
 // (workgroups of kHubRowTile rows, column tiles of kHubColTile staged in LDS,
 // the gathered rows split exactly into three bf16 parts, fp32 accumulation;
-// `groups` workgroups share a row tile, each over its own range of column
-// tiles, and their partial sums are added in group order), and the plan's
+// several workgroups share a row tile, each over its own range of column
+// tiles, and their partial sums are added in range order), and the plan's
 // items then add the rest of the row onto it.
-constexpr int kHubRowTile = 256;
+constexpr int kHubRowTile = 512;
 constexpr int kHubColTile = 32;
 struct Hub {
   int32_t rows = 0, rows_real = 0;      // hub rows, padded to kHubRowTile (padding: row id -1)
   int32_t cols = 0, cols_real = 0;      // hub columns, padded to kHubColTile (padding: column id -1)
-  int32_t groups = 1;
   int64_t nnz = 0;                      // non-zeros inside the block
   std::vector<int32_t> row_ids, col_ids;
-  std::vector<uint32_t> bits;           // [rows][cols / kHubColTile]: bit k = column tile*32 + k
+  std::vector<uint32_t> bits;           // [cols / kHubColTile][rows]: bit k = column tile*32 + k
   std::vector<uint32_t> init;           // over all output rows: the row starts from its block sum
   int32_t *d_row_ids = nullptr, *d_col_ids = nullptr;
   uint32_t *d_bits = nullptr, *d_init = nullptr;

@@ -80,10 +80,11 @@ static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz, bool tra
 
 // Cost of one (row, column) pair of a dense block on the matrix cores, in
 // units of one gathered non-zero of the same width, measured on MI355X for
-// 1 KB rows: the block (split, products, combine) takes 1.6 ps per pair, and
-// each non-zero it takes off the gather saves 28.5 ps there (the block's
-// columns are the most referenced rows, mostly served by the L2, so they cost
-// the gather less than its average non-zero).
+// 1 KB rows: each non-zero the block takes off the gather saves about 28.5 ps
+// there (the block's columns are the most referenced rows, mostly served by
+// the L2, so they cost the gather less than its average non-zero), and the
+// block costs 1.6-2.4 ps per pair.  A sweep of this constant on the
+// Reddit-like partition (0.02 to 0.08) put the best step at 0.057.
 constexpr double kHubPairCost = 0.057;
 
 static int64_t env_int(const char *name, int64_t dflt) {
@@ -185,7 +186,7 @@ static void choose_hub(const std::vector<int64_t> &rowptr, const std::vector<int
     for (int64_t k = rowptr[r]; k < rowptr[r + 1]; ++k) {
       const int32_t c = col[k];
       if (rpos[r] >= 0 && cpos[c] >= 0) {
-        h.bits[(size_t)rpos[r] * ntiles + cpos[c] / kHubColTile] |= 1u << (cpos[c] % kHubColTile);
+        h.bits[(size_t)(cpos[c] / kHubColTile) * h.rows + rpos[r]] |= 1u << (cpos[c] % kHubColTile);
         h.nnz++;
       } else {
         col_rest.push_back(c);
@@ -193,9 +194,6 @@ static void choose_hub(const std::vector<int64_t> &rowptr, const std::vector<int
     }
     rowptr_rest[r + 1] = (int64_t)col_rest.size();
   }
-  // workgroups sharing a row tile, each over its own range of column tiles: about one per CU
-  const int64_t row_tiles = h.rows / kHubRowTile;
-  h.groups = (int32_t)std::max<int64_t>(1, std::min<int64_t>(ntiles, (256 + row_tiles / 2) / row_tiles));
 }
 
 // Work plan of one aggregation.  A row whose run inside some chunk is longer

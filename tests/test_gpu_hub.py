@@ -2,7 +2,7 @@
 size on small graphs; the Reddit-like partition selects one by itself):
 layer forward and backward of every form through the C ABI against the
 oracle, element by element, with the block's rows and columns padded
-(sizes not multiples of the 256-row and 32-column tiles), column chunks and
+(sizes not multiples of the 512-row and 32-column tiles), column chunks and
 split rows in the rest of the plan, widths of one, several and a partial
 64-float4 pass, and both GEMM precisions (bf16 against both oracle
 readings).  ReLU decisions that differ from the oracle's are certified
