@@ -119,8 +119,10 @@ int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst,
   return PGCN_OK;
 }
 
-__global__ __launch_bounds__(256) void accum_kernel(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows,
-                                                    const float *src, float *dst, int f4, int64_t ld, int sh) {
+__global__ __launch_bounds__(256) void accum_kernel(const int64_t *__restrict__ inv_ptr,
+                                                    const int32_t *__restrict__ inv_k, int64_t rows,
+                                                    const float *__restrict__ src, float *__restrict__ dst, int f4,
+                                                    int64_t ld, int sh) {
   const int64_t u = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
   if (u >= rows) return;
   const int64_t b = inv_ptr[u], e = inv_ptr[u + 1];
@@ -128,7 +130,8 @@ __global__ __launch_bounds__(256) void accum_kernel(const int64_t *inv_ptr, cons
   float4 *d = reinterpret_cast<float4 *>(dst + u * ld);
   for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) {
     float4 v = d[c4];
-    for (int64_t q = b; q < e; ++q) {   // ascending send-list position: ascending peer
+#pragma unroll 4
+    for (int64_t q = b; q < e; ++q) {   // ascending send-list position: ascending peer (loads are independent)
       const float4 x = reinterpret_cast<const float4 *>(src + (int64_t)inv_k[q] * ld)[c4];
       v.x += x.x;
       v.y += x.y;
@@ -144,9 +147,14 @@ __global__ __launch_bounds__(256) void accum_kernel(const int64_t *inv_ptr, cons
 // thread that adds row k into u also updates its moving average, once:
 //     state[k] = gamma state[k] + (1 - gamma) src[k];  dst[u] += state[k]
 // (the moving average is read once instead of twice).
-__global__ __launch_bounds__(256) void accum_ema_kernel(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows,
-                                                        const float *src, float *state, float gamma, float *dst,
-                                                        int f4, int64_t ld, int sh) {
+// The three buffers are distinct allocations and the send rows k of one inner
+// row are distinct, so the loads of later send rows may be issued ahead of the
+// state stores of earlier ones (restrict); the sums keep ascending order.
+__global__ __launch_bounds__(256) void accum_ema_kernel(const int64_t *__restrict__ inv_ptr,
+                                                        const int32_t *__restrict__ inv_k, int64_t rows,
+                                                        const float *__restrict__ src, float *__restrict__ state,
+                                                        float gamma, float *__restrict__ dst, int f4, int64_t ld,
+                                                        int sh) {
   const int64_t u = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
   if (u >= rows) return;
   const int64_t b = inv_ptr[u], e = inv_ptr[u + 1];
@@ -155,20 +163,32 @@ __global__ __launch_bounds__(256) void accum_ema_kernel(const int64_t *inv_ptr, 
   float4 *d = reinterpret_cast<float4 *>(dst + u * ld);
   for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) {
     float4 v = d[c4];
-    for (int64_t q = b; q < e; ++q) {   // ascending send-list position: ascending peer
-      const int64_t k = inv_k[q];
-      const float4 x = reinterpret_cast<const float4 *>(src + k * ld)[c4];
-      float4 *sp = reinterpret_cast<float4 *>(state + k * ld) + c4;
-      float4 m = *sp;
-      m.x = gamma * m.x + g1 * x.x;
-      m.y = gamma * m.y + g1 * x.y;
-      m.z = gamma * m.z + g1 * x.z;
-      m.w = gamma * m.w + g1 * x.w;
-      *sp = m;
-      v.x += m.x;
-      v.y += m.y;
-      v.z += m.z;
-      v.w += m.w;
+    for (int64_t q0 = b; q0 < e; q0 += 4) {   // ascending send-list position: ascending peer
+      // four send rows per round, their loads issued together; past the row's last slot the
+      // round repeats that slot and neither stores nor adds it
+      const int n = e - q0 < 4 ? (int)(e - q0) : 4;
+      int64_t k[4];
+      float4 x[4], m[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) k[j] = inv_k[q0 + (j < n ? j : n - 1)];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[j] = reinterpret_cast<const float4 *>(src + k[j] * ld)[c4];
+        m[j] = reinterpret_cast<const float4 *>(state + k[j] * ld)[c4];
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        m[j].x = gamma * m[j].x + g1 * x[j].x;
+        m[j].y = gamma * m[j].y + g1 * x[j].y;
+        m[j].z = gamma * m[j].z + g1 * x[j].z;
+        m[j].w = gamma * m[j].w + g1 * x[j].w;
+        if (j < n) reinterpret_cast<float4 *>(state + k[j] * ld)[c4] = m[j];
+        const bool in = j < n;
+        v.x = in ? v.x + m[j].x : v.x;
+        v.y = in ? v.y + m[j].y : v.y;
+        v.z = in ? v.z + m[j].z : v.z;
+        v.w = in ? v.w + m[j].w : v.w;
+      }
     }
     d[c4] = v;
   }
