@@ -3,8 +3,9 @@ callers that cannot allocate: graph capture, serving loops) against
 pgcn_layer_fwd with a caller-owned workspace.  Both run the same kernels, so
 every output must agree bit for bit; the outputs are also held to the fp64
 oracle at the path's tolerance.  Two calls in a row share the library's fixed
-scratch array: the first on a partition with column chunks and split rows
-(partial sums in the scratch), the second on a smaller partition with
+scratch array: the first on a partition with column chunks, split rows and a
+dense block (partial sums, block sums and block images in the scratch), the
+second on a smaller partition with
 narrower layers, in both associations and both GEMM precisions.  Arguments the
 entry point must refuse (a workspace given, a layer whose workspace exceeds
 the fixed array) are refused before any launch."""
@@ -47,10 +48,14 @@ class Part:
 
 @pytest.fixture(scope="module")
 def parts():
-    # 3 column chunks and rows split every 64 non-zeros: the forward keeps partial sums in its workspace
-    big = Part(3000, 1500, 12, 0, hub_deg=3000, env={"PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "64"})
+    # 3 column chunks, rows split every 64 non-zeros and a 600 x 1000 dense block on the matrix cores:
+    # the forward keeps partial sums, block sums and block images in its workspace
+    big = Part(3000, 1500, 12, 0, hub_deg=3000, env={"PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "64",
+                                                     "PGCN_HUB_ROWS": "600", "PGCN_HUB_COLS": "1000"})
     small = Part(1000, 400, 8, 1)
     assert big.info["spmm_chunks"] == 3 and big.info["spmm_split_slots"] > 0
+    assert (big.info["spmm_hub_rows"], big.info["spmm_hub_cols"]) == (600, 1000) and big.info["spmm_hub_nnz"] > 0
+    assert small.info["spmm_hub_rows"] == 0
     return big, small
 
 
