@@ -2,8 +2,8 @@
 size on small graphs; the Reddit-like partition selects one by itself):
 layer forward and backward of every form through the C ABI against the
 oracle, element by element, with the block's rows and columns padded
-(sizes not multiples of the 512-row and 32-column tiles), column chunks and
-split rows in the rest of the plan, widths of one, several and a partial
+(sizes not multiples of the 512-row and 32-column tiles), three column
+chunks or one, split rows in the rest of the plan, widths of one, several and a partial
 64-float4 pass, and both GEMM precisions (bf16 against both oracle
 readings).  ReLU decisions that differ from the oracle's are certified
 (tests/certify.py)."""
@@ -24,17 +24,20 @@ pytestmark = pytest.mark.gpu
 
 ORDER = {"agg": B.PGCN_ORDER_AGG, "transform": B.PGCN_ORDER_TRANSFORM}
 ENV = {"PGCN_HUB_ROWS": "600", "PGCN_HUB_COLS": "1000", "PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "64"}
+# one column chunk: the block sums are the rows' only other contribution
+ENV_ONE = {"PGCN_HUB_ROWS": "600", "PGCN_HUB_COLS": "1000", "PGCN_AGG_CHUNKS": "1"}
 _PARTS = {}
 
 
-def part(model, norm):
-    key = (model, norm)
+def part(model, norm, env=None):
+    env = env or ENV
+    key = (model, norm, tuple(sorted(env.items())))
     if key not in _PARTS:
         n_g, rowptr, col, owner = random_partition_graph(3000, 2000, 3, 40, 21, hub_deg=2500)
         sage = model == "sage"
         ref = build_partition(n_g, rowptr, col, owner, 0, 3, self_loop=not sage)
-        old = {k: os.environ.get(k) for k in ENV}
-        os.environ.update(ENV)
+        old = {k: os.environ.get(k) for k in env}
+        os.environ.update(env)
         try:
             h = B.pgcn_partition_setup(n_g, rowptr, col, owner, 3, 0, self_loop=not sage, symmetric=norm == "sym")
         finally:
@@ -46,7 +49,8 @@ def part(model, norm):
         info = B.pgcn_partition_info(h)
         assert (info["spmm_hub_rows"], info["spmm_hub_cols"]) == (600, 1000)
         assert (info["spmmt_hub_rows"], info["spmmt_hub_cols"]) == (600, 1000)
-        assert info["spmm_hub_nnz"] > 0 and info["spmmt_hub_nnz"] > 0 and info["spmm_chunks"] == 3
+        assert info["spmm_hub_nnz"] > 0 and info["spmmt_hub_nnz"] > 0
+        assert info["spmm_chunks"] == int(env["PGCN_AGG_CHUNKS"])
         _PARTS[key] = (ref, propagation_matrix(ref, norm), h)
     return _PARTS[key]
 
@@ -59,7 +63,19 @@ FORMS = [("gcn", "mean", "agg"), ("gcn", "mean", "transform"), ("gcn", "sym", "a
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("f_in,f_out", [(256, 256), (41, 47), (300, 72), (602, 256), (64, 300)])
 def test_layer_with_dense_block(model, norm, order, dt, f_in, f_out):
-    ref, P, part_h = part(model, norm)
+    check_layer(model, norm, order, dt, f_in, f_out, ENV)
+
+
+@pytest.mark.parametrize("model,norm,order", [("gcn", "mean", "agg"), ("gcn", "sym", "transform"),
+                                              ("sage", "mean", "agg")])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("f_in,f_out", [(256, 256), (41, 47)])
+def test_layer_with_dense_block_one_chunk(model, norm, order, dt, f_in, f_out):
+    check_layer(model, norm, order, dt, f_in, f_out, ENV_ONE)
+
+
+def check_layer(model, norm, order, dt, f_in, f_out, env):
+    ref, P, part_h = part(model, norm, env)
     sage = model == "sage"
     n, b = ref.n_inner, ref.n_bd
     rng = np.random.default_rng(f_in * 131 + f_out)
