@@ -231,7 +231,44 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// One wave64 per row.
+// Softmax cross-entropy, every row read once into registers where it fits:
+// rows of at most 64 classes four to a wave (one class per lane, the four
+// rows' loads in flight together), rows of at most 256 classes one to a wave
+// (four classes per lane), wider rows one to a wave and read three times.
+constexpr int kCeRegs = 4;
+
+__device__ __forceinline__ float ce_row_loss(float m, float s, float zy, bool y_ok, float scale) {
+  return y_ok ? scale * (m + __logf(s) - zy) : __builtin_nanf("");  // an out-of-range label poisons the loss
+}
+
+// Four rows per wave (C <= 64): slot i holds class `lane` of row r0 + i.
+__global__ __launch_bounds__(256) void softmax_ce4_kernel(const float *Z, int64_t rows, int C, int64_t ld,
+                                                          const int32_t *labels, float scale, float *J,
+                                                          float *row_loss) {
+  const int lane = threadIdx.x % 64;
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + threadIdx.x / 64) * kCeRegs;
+  if (r0 >= rows) return;
+  float zr[kCeRegs], m[kCeRegs], s[kCeRegs];
+#pragma unroll
+  for (int i = 0; i < kCeRegs; ++i) zr[i] = (r0 + i < rows && lane < C) ? Z[(r0 + i) * ld + lane] : -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kCeRegs; ++i) m[i] = wave_max(zr[i]);
+#pragma unroll
+  for (int i = 0; i < kCeRegs; ++i) s[i] = wave_sum(lane < C ? __expf(zr[i] - m[i]) : 0.f);
+#pragma unroll
+  for (int i = 0; i < kCeRegs; ++i) {
+    const int64_t r = r0 + i;
+    if (r >= rows) break;
+    const int y = labels[r];
+    const float inv_s = 1.0f / s[i];
+    if (lane < C) J[r * ld + lane] = scale * (__expf(zr[i] - m[i]) * inv_s - (lane == y ? 1.0f : 0.0f));
+    const bool y_ok = y >= 0 && y < C;
+    const float zy = __shfl(zr[i], y_ok ? y : 0, 64);
+    if (lane == 0) row_loss[r] = ce_row_loss(m[i], s[i], zy, y_ok, scale);
+  }
+}
+
+// One row per wave.
 __global__ __launch_bounds__(256) void softmax_ce_kernel(const float *Z, int64_t rows, int C, int64_t ld,
                                                          const int32_t *labels, float scale, float *J,
                                                          float *row_loss) {
@@ -239,21 +276,39 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(const float *Z, int64_t
   const int64_t r = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
   if (r >= rows) return;
   const float *z = Z + r * ld;
-  float m = -INFINITY;
-  for (int c = lane; c < C; c += 64) m = fmaxf(m, z[c]);
-  m = wave_max(m);
-  float s = 0.f;
-  for (int c = lane; c < C; c += 64) s += __expf(z[c] - m);
-  s = wave_sum(s);
   const int y = labels[r];
-  const bool y_ok = y >= 0 && y < C;          // an out-of-range label poisons the loss instead of reading out of the row
-  const float inv_s = 1.0f / s;
+  const bool y_ok = y >= 0 && y < C;
   float *j = J + r * ld;
-  for (int c = lane; c < C; c += 64) {
-    const float p = __expf(z[c] - m) * inv_s;
-    j[c] = scale * (p - (c == y ? 1.0f : 0.0f));
+  float m = -INFINITY, s = 0.f;
+  if (C <= 64 * kCeRegs) {
+    float zr[kCeRegs];
+#pragma unroll
+    for (int i = 0; i < kCeRegs; ++i) zr[i] = lane + 64 * i < C ? z[lane + 64 * i] : -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kCeRegs; ++i) m = fmaxf(m, zr[i]);
+    m = wave_max(m);
+#pragma unroll
+    for (int i = 0; i < kCeRegs; ++i)
+      if (lane + 64 * i < C) s += __expf(zr[i] - m);
+    s = wave_sum(s);
+    const float inv_s = 1.0f / s;
+#pragma unroll
+    for (int i = 0; i < kCeRegs; ++i) {
+      const int c = lane + 64 * i;
+      if (c < C) j[c] = scale * (__expf(zr[i] - m) * inv_s - (c == y ? 1.0f : 0.0f));
+    }
+  } else {
+    for (int c = lane; c < C; c += 64) m = fmaxf(m, z[c]);
+    m = wave_max(m);
+    for (int c = lane; c < C; c += 64) s += __expf(z[c] - m);
+    s = wave_sum(s);
+    const float inv_s = 1.0f / s;
+    for (int c = lane; c < C; c += 64) {
+      const float p = __expf(z[c] - m) * inv_s;
+      j[c] = scale * (p - (c == y ? 1.0f : 0.0f));
+    }
   }
-  if (lane == 0) row_loss[r] = y_ok ? scale * (m + __logf(s) - z[y]) : __builtin_nanf("");
+  if (lane == 0) row_loss[r] = ce_row_loss(m, s, y_ok ? z[y] : 0.f, y_ok, scale);
 }
 
 __global__ __launch_bounds__(256) void sigmoid_bce_kernel(const float *Z, int64_t rows, int C, int64_t ld,
@@ -276,18 +331,38 @@ __global__ __launch_bounds__(256) void sigmoid_bce_kernel(const float *Z, int64_
   if (lane == 0) row_loss[r] = scale * l;
 }
 
-// Fixed-order reduction of the per-row losses (one block, fp64 partials).
-__global__ __launch_bounds__(1024) void loss_reduce_kernel(const float *row_loss, int64_t rows, float *out) {
-  __shared__ double part[1024];
-  double s = 0.0;
-  for (int64_t r = threadIdx.x; r < rows; r += 1024) s += (double)row_loss[r];
+// Fixed-order reduction of the per-row losses in two passes, fp64 sums: block b
+// of the first adds rows [b per, (b + 1) per) (a fixed tree over its threads'
+// strided sums) and leaves the result, rounded to fp32, in the range's first
+// element; one block then adds those kLossBlocks values the same way.
+constexpr int kLossBlocks = 256;
+
+__device__ __forceinline__ double block_sum_1024(double s, double *part) {
   part[threadIdx.x] = s;
   __syncthreads();
   for (int w = 512; w > 0; w >>= 1) {
     if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
     __syncthreads();
   }
-  if (threadIdx.x == 0) *out = (float)part[0];
+  return part[0];
+}
+
+__global__ __launch_bounds__(1024) void loss_partial_kernel(float *row_loss, int64_t rows, int64_t per) {
+  __shared__ double part[1024];
+  const int64_t r0 = (int64_t)blockIdx.x * per, r1 = r0 + per < rows ? r0 + per : rows;
+  double s = 0.0;
+  for (int64_t r = r0 + threadIdx.x; r < r1; r += 1024) s += (double)row_loss[r];
+  s = block_sum_1024(s, part);             // every read of the range is done before this point
+  if (threadIdx.x == 0 && r0 < r1) row_loss[r0] = (float)s;
+}
+
+__global__ __launch_bounds__(1024) void loss_reduce_kernel(const float *row_loss, int64_t rows, int64_t per,
+                                                           float *out) {
+  __shared__ double part[1024];
+  double s = 0.0;
+  for (int64_t r = (int64_t)threadIdx.x * per; r < rows; r += (int64_t)1024 * per) s += (double)row_loss[r];
+  s = block_sum_1024(s, part);
+  if (threadIdx.x == 0) *out = (float)s;
 }
 
 size_t loss_workspace(int64_t rows) { return (size_t)rows * sizeof(float); }
@@ -298,14 +373,22 @@ int launch_loss(int32_t kind, const float *Z, int64_t rows, int32_t C, int64_t l
   TraceScope ts(PGCN_TK_LOSS, s);
   if (rows > 0) {
     const unsigned blocks = (unsigned)((rows + 3) / 4);
-    if (kind == PGCN_SOFTMAX_CE)
+    if (kind == PGCN_SOFTMAX_CE && C <= 64)
+      hipLaunchKernelGGL(softmax_ce4_kernel, dim3((unsigned)((rows + 4 * kCeRegs - 1) / (4 * kCeRegs))), dim3(256), 0,
+                         s, Z, rows, C, ld, labels, scale, J, ws);
+    else if (kind == PGCN_SOFTMAX_CE)
       hipLaunchKernelGGL(softmax_ce_kernel, dim3(blocks), dim3(256), 0, s, Z, rows, C, ld, labels, scale, J, ws);
     else
       hipLaunchKernelGGL(sigmoid_bce_kernel, dim3(blocks), dim3(256), 0, s, Z, rows, C, ld, targets, ld_t, scale,
                          J, ws);
     PGCN_HIP(hipGetLastError());
   }
-  hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(1024), 0, s, (const float *)ws, rows, loss_out);
+  const int64_t per = rows > 0 ? (rows + kLossBlocks - 1) / kLossBlocks : 1;
+  if (rows > 0) {
+    hipLaunchKernelGGL(loss_partial_kernel, dim3((unsigned)((rows + per - 1) / per)), dim3(1024), 0, s, ws, rows, per);
+    PGCN_HIP(hipGetLastError());
+  }
+  hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(1024), 0, s, (const float *)ws, rows, per, loss_out);
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;
 }
