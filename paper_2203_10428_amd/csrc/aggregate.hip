@@ -75,6 +75,8 @@ struct AggParams {
 
 enum { AGG_FIRST = 1, AGG_LAST = 2 };
 
+typedef float agg_f32x4 __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
   uint32_t b = __float_as_uint(x);
   if ((b & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((b >> 16) | 0x40u);  // quiet NaN
@@ -118,6 +120,7 @@ __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, fl
   }
   if (o) *reinterpret_cast<float4 *>(o + c) = q;
   if (p.send && r < p.out_split) {                     // four send slots per round, positions loaded together
+    const agg_f32x4 qv = {q.x, q.y, q.z, q.w};
     const int64_t kb = p.send_ptr[r], ke = p.send_ptr[r + 1];
     for (int64_t k = kb; k < ke; k += 4) {
       int32_t pos[4];
@@ -125,7 +128,8 @@ __device__ __forceinline__ void finish(const AggParams &p, int64_t r, int c4, fl
       for (int e = 0; e < 4; ++e) pos[e] = k + e < ke ? p.send_pos[k + e] : -1;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (pos[e] >= 0) *reinterpret_cast<float4 *>(p.send + (int64_t)pos[e] * p.ld_out + c) = q;
+        if (pos[e] >= 0)   // read by no kernel of this step: kept out of the caches
+          __builtin_nontemporal_store(qv, reinterpret_cast<agg_f32x4 *>(p.send + (int64_t)pos[e] * p.ld_out + c));
     }
   }
   if (p.out_bf16 && r < p.out_split) {

@@ -99,13 +99,19 @@ int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_
   return PGCN_OK;
 }
 
+typedef float ew_f32x4 __attribute__((ext_vector_type(4)));
+
 __global__ __launch_bounds__(256) void pack_kernel(const int32_t *idx, int64_t count, const float *src,
                                                    float *dst, int f4, int64_t ld, int sh) {
   const int64_t k = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
   if (k >= count) return;
   const float4 *from = reinterpret_cast<const float4 *>(src + (int64_t)idx[k] * ld);
   float4 *to = reinterpret_cast<float4 *>(dst + k * ld);
-  for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) to[c4] = from[c4];
+  // the sent rows are read by no kernel of this step: kept out of the caches
+  for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) {
+    const float4 x = from[c4];
+    __builtin_nontemporal_store((ew_f32x4){x.x, x.y, x.z, x.w}, reinterpret_cast<ew_f32x4 *>(to + c4));
+  }
 }
 
 int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst, int32_t cols, int64_t ld,

@@ -175,7 +175,8 @@ __device__ __forceinline__ void nk_epilogue(const NKParams &p, const f32x16 (&ac
             if (!any) break;
 #pragma unroll
             for (int s = 0; s < 4; ++s)
-              if (pos[s] >= 0) *reinterpret_cast<f32x4 *>(p.send + (int64_t)pos[s] * p.ldc + cb) = v[s];
+              if (pos[s] >= 0)   // read by no kernel of this step: kept out of the caches
+                __builtin_nontemporal_store(v[s], reinterpret_cast<f32x4 *>(p.send + (int64_t)pos[s] * p.ldc + cb));
           }
         }
       } else {
