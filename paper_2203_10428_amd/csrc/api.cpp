@@ -1055,6 +1055,19 @@ extern "C" int pgcn_sgd_update(float *W, const float *G, const float *G_peer, in
   return exception_status("pgcn_sgd_update");
 }
 
+namespace {
+// True when `p` is device memory of this process (not host memory, pinned or not).
+bool is_device_memory(const void *p) {
+  hipPointerAttribute_t attr{};
+  const hipError_t e = hipPointerGetAttributes(&attr, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();        // unregistered host memory: clear the sticky error
+    return false;
+  }
+  return attr.type == hipMemoryTypeDevice;
+}
+}  // namespace
+
 extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint32_t flags, hipStream_t s) try {
   if (bytes == 0) return PGCN_OK;
   PGCN_REQUIRE(dst && src, "pgcn_refill_async: null buffer");
@@ -1070,6 +1083,11 @@ extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint3
     return PGCN_OK;
   }
   TraceScope ts(PGCN_TK_REFILL, s);
+  // flags = 0 on 16-byte-aligned device buffers: the library's non-temporal copy kernel;
+  // anything else goes to the runtime's copy, which validates host pointers itself.
+  const bool vec = (bytes % 16) == 0 && ((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src)) & 15) == 0;
+  if (!(flags & PGCN_REFILL_DMA) && vec && is_device_memory(dst) && is_device_memory(src))
+    return launch_refill_copy(dst, src, bytes, s);
   PGCN_HIP(hipMemcpyAsync(dst, src, bytes, (flags & PGCN_REFILL_DMA) ? hipMemcpyDeviceToDeviceNoCU : hipMemcpyDeviceToDevice, s));
   return PGCN_OK;
 } catch (...) {

@@ -14,6 +14,8 @@
 //     transform-first layer aggregates in its backward (Appendix A.1's
 //     gradients in the other association).
 // All are float4-vectorised over the feature dimension; no float atomics.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace pgcn {
@@ -112,6 +114,23 @@ __global__ __launch_bounds__(256) void pack_kernel(const int32_t *idx, int64_t c
     const float4 x = from[c4];
     __builtin_nontemporal_store((ew_f32x4){x.x, x.y, x.z, x.w}, reinterpret_cast<ew_f32x4 *>(to + c4));
   }
+}
+
+// Device-to-device refill: 16-byte vectors with non-temporal loads and stores
+// (the copied rows are read in the next iteration, not in this one, so they
+// stay out of the caches the gathers use).
+__global__ __launch_bounds__(256) void refill_copy_kernel(const ew_f32x4 *src, ew_f32x4 *dst, int64_t n16) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (int64_t)gridDim.x * 256)
+    __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+}
+
+int launch_refill_copy(void *dst, const void *src, size_t bytes, hipStream_t s) {
+  const int64_t n16 = (int64_t)(bytes / 16);
+  const unsigned blocks = (unsigned)std::min<int64_t>((n16 + 255) / 256, 2048);
+  hipLaunchKernelGGL(refill_copy_kernel, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const ew_f32x4 *>(src),
+                     reinterpret_cast<ew_f32x4 *>(dst), n16);
+  PGCN_HIP(hipGetLastError());
+  return PGCN_OK;
 }
 
 int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst, int32_t cols, int64_t ld,

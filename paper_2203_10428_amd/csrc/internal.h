@@ -240,6 +240,9 @@ struct AdamCoef {
 };
 int launch_adam(float *W, const float *G, const float *Gp, float *m, float *v, int64_t count, const AdamCoef &c,
                 hipStream_t s);
+// Device-to-device copy of `bytes` (a multiple of 16, both pointers 16-byte aligned) with
+// non-temporal loads and stores.
+int launch_refill_copy(void *dst, const void *src, size_t bytes, hipStream_t s);
 int launch_pack(const int32_t *idx, int64_t count, const float *src, float *dst, int32_t cols,
                 int64_t ld, hipStream_t s);
 int launch_accum(const int64_t *inv_ptr, const int32_t *inv_k, int64_t rows, const float *src,

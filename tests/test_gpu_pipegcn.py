@@ -198,3 +198,18 @@ def test_refill_from_host_needs_pinned_memory():
         B.pgcn_refill_async(dst, torch.zeros(1024), 4096, B.PGCN_REFILL_FROM_HOST)
     with pytest.raises(B.PgcnError, match="unknown flags"):
         B.pgcn_refill_async(dst, pinned, 4096, 8)
+
+
+@pytest.mark.parametrize("nbytes,offset,flags", [
+    (16, 0, 0), (4096, 0, 0), (2048 * 256 * 16 * 2 + 48, 0, 0),   # the copy kernel, one pass and grid-stride
+    (4100, 0, 0), (4096, 4, 0),                                      # size or address not 16-byte aligned
+    (4096, 0, 1), (4100, 4, 1)])                                     # the DMA engines
+def test_device_refill_copies_exactly(nbytes, offset, flags):
+    from paper_2203_10428_amd import binding as B
+    guard = 256
+    src = torch.randint(0, 256, (nbytes + offset + guard,), dtype=torch.uint8, device="cuda")
+    dst = torch.full((nbytes + offset + guard,), 0xA5, dtype=torch.uint8, device="cuda")
+    B.pgcn_refill_async(dst[offset:], src[offset:], nbytes, flags)
+    torch.cuda.synchronize()
+    assert torch.equal(dst[offset:offset + nbytes], src[offset:offset + nbytes])
+    assert (dst[:offset] == 0xA5).all() and (dst[offset + nbytes:] == 0xA5).all()
