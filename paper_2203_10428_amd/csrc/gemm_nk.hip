@@ -11,9 +11,13 @@
 //
 // The right operand (the layer's weights, at most a few MB) is first packed
 // once per call into an n-major, k-contiguous matrix zero-padded to a 128-row
-// and 64-column multiple (fp32, or bf16 rounded to nearest even for the bf16
-// path), so the main loop loads both operands as 16-byte vectors with no
-// bounds checks on the weights.
+// (bf16) or 256-row (fp32) and 64-column multiple (bf16 rounded to nearest
+// even for the bf16 path; three exact bf16 parts for fp32 by parts, below;
+// fp32 for the plain fp32 kernel), so the main loop loads both operands as
+// 16-byte vectors with no bounds checks on the weights.
+//
+// fp32 GEMMs run by parts on the bf16 matrix cores (gemm_nk_f32s) unless
+// PGCN_GEMM_F32=native selects the fp32 matrix-core kernel (gemm_nk_f32).
 //
 // Main loop for CDNA4: a 256-thread workgroup (4 wave64s, 2 x 2) computes a
 // 128 x BN tile; both tiles sit in LDS with k contiguous (rows of four
@@ -29,9 +33,13 @@
 // in LDS and load with 128-bit reads:
 //   fp32, v_mfma_f32_32x32x2f32, slab of 16: step s uses k = 8*h + s for
 //        lane half h (lanes 32h .. 32h+31);
+//   fp32 by parts, v_mfma_f32_32x32x16_bf16, slab of 16: k = 8*h .. 8*h + 7;
 //   bf16, v_mfma_f32_32x32x16_bf16, slab of 32: step j uses k = 16*h + 8*j
 //        .. 16*h + 8*j + 7 for lane half h.
 // Every k of the slab is used exactly once per output element.
+#include <cstdlib>
+#include <cstring>
+
 #include "internal.h"
 
 namespace pgcn {
@@ -51,6 +59,7 @@ struct NKParams {
   int64_t ldam;
   const void *B;           // packed weights [rows >= tiles_n * BN, ldb]
   int64_t ldb;
+  int64_t bplane;          // fp32 by parts: elements from one bf16 part of the packed weights to the next
   float *C;
   int64_t ldc;
   const float *rowscale;
@@ -85,6 +94,40 @@ __global__ __launch_bounds__(256) void pack_b_kernel(const float *W, int ldw, in
   const float v = (n < N && k < K) ? (trans ? W[(int64_t)k * ldw + n] : W[(int64_t)n * ldw + k]) : 0.f;
   if (BF16) reinterpret_cast<uint16_t *>(out)[i] = nk_bf16(v);
   else reinterpret_cast<float *>(out)[i] = v;
+}
+
+// fp32 by parts: x = hi + mid + lo exactly, each part a bf16 (8 significant
+// bits): hi is x with its low 16 bits cleared (never overflows), mid is
+// x - hi rounded to nearest, and lo is what remains (at most 8 significant
+// bits, so exact while |x| >= 2^-111; below, lo is a bf16 subnormal rounded
+// to nearest).  Both differences are exact.  |mid| < 2^-7 |x| and
+// |lo| <= 2^-15 |x|.  A non-finite x makes mid and lo NaN (Inf - Inf), so
+// its products are NaN.  Two values at a time: returns the bf16 pairs
+// (element 0 in the low half).
+typedef __bf16 nk_bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void nk_split3x2(float x0, float x1, uint32_t &hi, uint32_t &mid, uint32_t &lo) {
+  const uint32_t b0 = __float_as_uint(x0), b1 = __float_as_uint(x1);
+  const float r0 = x0 - __uint_as_float(b0 & 0xffff0000u), r1 = x1 - __uint_as_float(b1 & 0xffff0000u);
+  hi = __builtin_amdgcn_perm(b1, b0, 0x07060302u);    // the high halves of b0 (low) and b1 (high)
+  mid = __builtin_bit_cast(uint32_t, (nk_bf16x2){(__bf16)r0, (__bf16)r1});
+  const float l0 = r0 - __uint_as_float(mid << 16), l1 = r1 - __uint_as_float(mid & 0xffff0000u);
+  lo = __builtin_bit_cast(uint32_t, (nk_bf16x2){(__bf16)l0, (__bf16)l1});
+}
+
+// The packed weights as three bf16 planes (hi, mid, lo), `plane` elements apart;
+// same indexing as pack_b_kernel.
+__global__ __launch_bounds__(256) void pack_b_split_kernel(const float *W, int ldw, int trans, int N, int K, int rows,
+                                                           int ldk, uint16_t *out) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * ldk) return;
+  const int n = i / ldk, k = i - n * ldk;
+  const float v = (n < N && k < K) ? (trans ? W[(int64_t)k * ldw + n] : W[(int64_t)n * ldw + k]) : 0.f;
+  const int64_t plane = (int64_t)rows * ldk;
+  uint32_t hi, mid, lo;
+  nk_split3x2(v, 0.f, hi, mid, lo);
+  out[i] = (uint16_t)hi;
+  out[plane + i] = (uint16_t)mid;
+  out[2 * plane + i] = (uint16_t)lo;
 }
 
 // Final value of one output element.
@@ -311,6 +354,156 @@ __global__ __launch_bounds__(256, 4) void gemm_nk_f32(NKParams p) {
   nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane, smem + wave * 32 * kNkStageLd);
 }
 
+// ------------------------------------------------------- fp32 by parts ---
+//
+// The fp32 GEMM on the bf16 matrix cores: both operands enter as three exact
+// bf16 parts (nk_split3), and each 32 x 32 block accumulates, in fp32, the six
+// part products whose order is at most 2^-16 of the full product:
+//   hi.hi + hi.mid + mid.hi + hi.lo + mid.mid + lo.hi.
+// The three dropped ones (mid.lo, lo.mid, lo.lo) are below 2^-21 (1 + 2^-7)
+// |a b| together, and every part product is exact in fp32 (8 x 8 significant
+// bits), so the result carries fp32 accuracy.  Six v_mfma_f32_32x32x16_bf16 per 16
+// values of k take 192 matrix-core cycles, against 512 for the eight
+// v_mfma_f32_32x32x2f32 of the plain fp32 kernel.  The weights arrive already
+// split (pack_b_split_kernel); the activations are split once per workgroup
+// while staged.  Slabs of 16 values of k: per operand three bf16 planes of
+// 32-byte rows (two 16-byte groups, the second group first in rows 8 .. 15 of
+// every 16 so that the 16 lanes of one 16-byte access pass fall on distinct
+// banks), double buffered: 48 KB and three workgroups per CU for 128 x 128
+// tiles, 72 KB and two for 128 x 256 (64 x 128 per wave: 48 matrix-core
+// instructions per slab and wave, half the split work per instruction).  Lane
+// half h takes k = 8h .. 8h + 7 of the slab on both operands.
+
+__device__ __forceinline__ int nk_sw2(int row, int g) { return g ^ ((row >> 3) & 1); }
+
+template <int BM, int BN, int AK, int EK>
+__global__ __launch_bounds__(256, BN == 256 ? 2 : 3) void gemm_nk_f32s(NKParams p) {
+  constexpr int BK = 16;
+  constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
+  constexpr int PA = BM * BK, PB = BN * BK;             // bf16 elements of one plane
+  constexpr int NB = 3 * BN * 2;                       // 16-byte vectors of the three weight planes
+  constexpr int VB = (NB + 255) / 256;
+  static_assert(BM == 128, "one 8-value vector of A per thread");
+  constexpr int SMB = 2 * 3 * (PA + PB) * 2;
+  constexpr int SM = SMB > kNkStageFloats * 4 ? SMB : kNkStageFloats * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[SM];
+  uint16_t *As = reinterpret_cast<uint16_t *>(smem);   // [2][3][PA]
+  uint16_t *Bs = As + 2 * 3 * PA;                      // [2][3][PB]
+
+  const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
+  const int tile = nk_xcd_remap(blockIdx.x, gridDim.x);
+  const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
+  const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
+  const uint16_t *Bp = reinterpret_cast<const uint16_t *>(p.B);
+
+  // raw loads only; the row tail, the ReLU mask and the split are applied in
+  // store(), after the MFMAs that hide the loads
+  const int am = t / 2, ag = t % 2;                    // A: row am, values 8 ag .. 8 ag + 7 of the slab
+  f32x4 rx[2], rh[AK == NK_A_MASK ? 2 : 1];
+  u32x4 rb[VB];
+  int kl = 0;
+  auto load = [&](int kt) __attribute__((always_inline)) {
+    kl = kt;
+    const int gm = m0 + am, gk = kt + 8 * ag;
+    const bool ok = gm < p.M && gk < p.K, ok1 = ok && gk + 4 < p.K;   // ld is a multiple of 4
+    const float *row = p.A + (int64_t)gm * p.lda + gk;
+    rx[0] = ok ? *reinterpret_cast<const f32x4 *>(row) : f32x4{0.f, 0.f, 0.f, 0.f};
+    rx[1] = ok1 ? *reinterpret_cast<const f32x4 *>(row + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (AK == NK_A_MASK) {
+      const float *hrow = p.Am + (int64_t)gm * p.ldam + gk;
+      rh[0] = (ok && p.Am) ? *reinterpret_cast<const f32x4 *>(hrow) : f32x4{1.f, 1.f, 1.f, 1.f};
+      rh[1] = (ok1 && p.Am) ? *reinterpret_cast<const f32x4 *>(hrow + 4) : f32x4{1.f, 1.f, 1.f, 1.f};
+    }
+#pragma unroll
+    for (int v = 0; v < VB; ++v) {
+      const int idx = t + 256 * v;
+      if (NB % 256 == 0 || idx < NB) {
+        const int pl = idx / (2 * BN), n = (idx % (2 * BN)) / 2, g = idx % 2;
+        rb[v] = *reinterpret_cast<const u32x4 *>(Bp + pl * p.bplane + (int64_t)(n0 + n) * p.ldb + kt + 8 * g);
+      }
+    }
+  };
+  auto store = [&](int b) __attribute__((always_inline)) {
+    float x[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      x[q] = rx[q / 4][q % 4];
+      if constexpr (AK == NK_A_MASK) x[q] = rh[q / 4][q % 4] > 0.f ? x[q] : 0.f;
+    }
+    if (kl + BK > p.K) {                               // the last slab (uniform): zero the k >= K tail
+      const int valid = p.K - (kl + 8 * ag);
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (q >= valid) x[q] = 0.f;
+    }
+    u32x4 oh, om, ol;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      uint32_t hi, mid, lo;
+      nk_split3x2(x[2 * w], x[2 * w + 1], hi, mid, lo);
+      oh[w] = hi;
+      om[w] = mid;
+      ol[w] = lo;
+    }
+    const int off = am * BK + 8 * nk_sw2(am, ag);
+    *reinterpret_cast<u32x4 *>(As + (b * 3 + 0) * PA + off) = oh;
+    *reinterpret_cast<u32x4 *>(As + (b * 3 + 1) * PA + off) = om;
+    *reinterpret_cast<u32x4 *>(As + (b * 3 + 2) * PA + off) = ol;
+#pragma unroll
+    for (int v = 0; v < VB; ++v) {
+      const int idx = t + 256 * v;
+      if (NB % 256 == 0 || idx < NB) {
+        const int pl = idx / (2 * BN), n = (idx % (2 * BN)) / 2, g = idx % 2;
+        *reinterpret_cast<u32x4 *>(Bs + (b * 3 + pl) * PB + n * BK + 8 * nk_sw2(n, g)) = rb[v];
+      }
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
+
+  const int h = lane >> 5, r = lane & 31;
+  load(0);
+  store(0);
+  __syncthreads();
+  int it = 0;
+  for (int kt = 0; kt < p.K; kt += BK, ++it) {
+    const int cur = it & 1;
+    load(kt + BK < p.K ? kt + BK : kt);                // as in gemm_nk_f32
+    bf16x8 a[3][TM], b[3][TN];
+#pragma unroll
+    for (int pl = 0; pl < 3; ++pl) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int row = wm0 + i * 32 + r;
+        a[pl][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(
+                                                  As + (cur * 3 + pl) * PA + row * BK + 8 * nk_sw2(row, h)));
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int row = wn0 + j * 32 + r;
+        b[pl][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(
+                                                  Bs + (cur * 3 + pl) * PB + row * BK + 8 * nk_sw2(row, h)));
+      }
+    }
+    // smallest products first; the TM x TN independent blocks between dependent steps
+    constexpr int PW[6] = {2, 1, 0, 1, 0, 0}, PX[6] = {0, 1, 2, 0, 1, 0};   // parts of weights / activations
+#pragma unroll
+    for (int u = 0; u < 6; ++u)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[PW[u]][j], a[PX[u]][i], acc[i][j], 0, 0, 0);
+    store(cur ^ 1);
+    __syncthreads();
+  }
+  nk_epilogue<EK, TM, TN>(p, acc, m0 + wm0, n0 + wn0, lane, reinterpret_cast<float *>(smem) + wave * 32 * kNkStageLd);
+}
+
 // ------------------------------------------------------------------ bf16 ---
 
 template <int BM, int BN, int AK, int EK>
@@ -438,11 +631,19 @@ __global__ __launch_bounds__(256, AK == NK_A_MASK ? 3 : 4) void gemm_nk_bf16(NKP
 // ---------------------------------------------------------------- launch ---
 
 static int64_t nk_ldk(int K) { return ((int64_t)K + 63) / 64 * 64; }
-static int64_t nk_rows(int N) { return ((int64_t)N + 127) / 128 * 128; }
+static int64_t nk_rows(int N, bool bf16) { return bf16 ? ((int64_t)N + 127) / 128 * 128 : ((int64_t)N + 255) / 256 * 256; }
 
+// fp32 GEMMs by parts (the default) or on the fp32 matrix cores
+// (PGCN_GEMM_F32=native, a tuning override read per call)
+static bool nk_f32_by_parts() {
+  const char *e = std::getenv("PGCN_GEMM_F32");
+  return !(e && std::strcmp(e, "native") == 0);
+}
+
+// fp32: room for the three bf16 planes of the split weights (6 bytes per element) in either mode
 size_t gemm_nk_workspace(int32_t N, int32_t K, int32_t dtype) {
-  const size_t el = dtype == PGCN_BF16 ? 2 : 4;
-  return align_up((size_t)nk_rows(N) * (size_t)nk_ldk(K) * el, 256);
+  const size_t el = dtype == PGCN_BF16 ? 2 : 6;
+  return align_up((size_t)nk_rows(N, dtype == PGCN_BF16) * (size_t)nk_ldk(K) * el, 256);
 }
 
 template <int BN, int AK, int EK>
@@ -451,17 +652,24 @@ static void nk_launch(const NKParams &p0, bool bf16, hipStream_t s) {
   NKParams p = p0;
   const int tm = (p.M + BM - 1) / BM, tn = (p.N + BN - 1) / BN;
   p.tiles_n = tn;
-  if (bf16) {
+  if constexpr (BN == 256) {                           // fp32 by parts only
+    hipLaunchKernelGGL((gemm_nk_f32s<BM, BN, AK, EK>), dim3((unsigned)(tm * tn)), dim3(256), 0, s, p);
+  } else if (bf16) {
     constexpr int AKb = AK == NK_A_F32 ? NK_A_BF16 : AK;
     hipLaunchKernelGGL((gemm_nk_bf16<BM, BN, AKb, EK>), dim3((unsigned)(tm * tn)), dim3(256), 0, s, p);
+  } else if (p.bplane > 0) {
+    hipLaunchKernelGGL((gemm_nk_f32s<BM, BN, AK, EK>), dim3((unsigned)(tm * tn)), dim3(256), 0, s, p);
   } else {
     hipLaunchKernelGGL((gemm_nk_f32<BM, BN, AK, EK>), dim3((unsigned)(tm * tn)), dim3(256), 0, s, p);
   }
 }
 
+// Tile width: 64 for narrow outputs; by parts, 256 (twice the matrix-core work
+// per staged A value and per slab) where that pads no more columns than 128.
 template <int AK, int EK>
 static void nk_launch_bn(const NKParams &p, bool bf16, hipStream_t s) {
   if (p.N <= 64) nk_launch<64, AK, EK>(p, bf16, s);
+  else if (p.bplane > 0 && (p.N + 255) / 256 * 2 == (p.N + 127) / 128) nk_launch<256, AK, EK>(p, bf16, s);
   else nk_launch<128, AK, EK>(p, bf16, s);
 }
 
@@ -473,14 +681,18 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
   const size_t need = gemm_nk_workspace(g.N, g.K, g.dtype);
   if (!g.workspace || g.workspace_bytes < need)
     return set_error(PGCN_EWORKSPACE, "update GEMM: workspace too small for the packed weights");
-  const int rows = (int)nk_rows(g.N), ldk = (int)nk_ldk(g.K);
+  const int rows = (int)nk_rows(g.N, bf16), ldk = (int)nk_ldk(g.K);
   const bool fwd = kind == Gemm::NN_RELU || kind == Gemm::NN_PLAIN || kind == Gemm::NN_ACC_RELU ||
                    kind == Gemm::NN_ACC_PLAIN || kind == Gemm::NN_SRC32_PLAIN || kind == Gemm::NN_SRC32_ROWSCALE ||
                    kind == Gemm::NN_SRC32_RELU;
+  const bool parts = !bf16 && nk_f32_by_parts();
   {
     TraceScope ts(PGCN_TK_GEMM_PACK, s);
     const unsigned blocks = (unsigned)(((int64_t)rows * ldk + 255) / 256);
-    if (bf16)
+    if (parts)
+      hipLaunchKernelGGL(pack_b_split_kernel, dim3(blocks), dim3(256), 0, s, g.B, (int)g.ldb, fwd ? 1 : 0, g.N, g.K,
+                         rows, ldk, reinterpret_cast<uint16_t *>(g.workspace));
+    else if (bf16)
       hipLaunchKernelGGL(pack_b_kernel<true>, dim3(blocks), dim3(256), 0, s, g.B, (int)g.ldb, fwd ? 1 : 0, g.N, g.K,
                          rows, ldk, (void *)g.workspace);
     else
@@ -499,6 +711,7 @@ int launch_gemm_nk(Gemm kind, const GemmArgs &g, hipStream_t s) {
   p.ldam = g.ldm;
   p.B = g.workspace;
   p.ldb = ldk;
+  p.bplane = parts ? (int64_t)rows * ldk : 0;
   p.C = g.C;
   p.ldc = g.ldc;
   p.rowscale = g.rowscale;

@@ -17,13 +17,18 @@ Z_vc = sum_u P_vu sum_k X_uk W_kc.  The GPU sums the d_v rows of P (each as
 one term, or as three exact bf16 parts in the dense block the matrix cores
 take, plus up to four roundings for the 1/d or d^-1/2 scales and their
 products) and K products, in fp32; on the bf16 path both product operands are
-first rounded once to bf16 (nearest even).  So
+first rounded once to bf16 (nearest even).  The fp32 path takes each product
+as six exact products of bf16 parts (x = hi + mid + lo exactly, |mid| <
+2^-7 |x|, |lo| <= 2^-15 |x|; the three dropped part products are below
+2^-21 (1 + 2^-7) |x y| <= p = 2^-20 |x y|), so it sums 6K terms whose
+magnitudes add up to at most |x y| per product.  So
 
     |Z_gpu - Z| <= c_v (P|X|)|W| + (1 + c_v) (P E_X)|W|,
-    c_v = (1 + b)^2 (1 + 2^-24) (1 + gamma_K) (1 + gamma_{3 d_v + 4}) - 1,
+    c_v = (1 + b)^2 (1 + 2^-24) (1 + p) (1 + gamma_{6K}) (1 + gamma_{3 d_v + 4}) - 1,
 
-with b = 2^-8 on the bf16 path and 0 on the fp32 path, 2^-24 for the weights
-handed over in fp32, and E_X a bound on the
+with b = 2^-8 on the bf16 path and 0 on the fp32 path (p = 0 and 6K -> K
+on the bf16 path; the plain fp32 matrix-core kernel is within the same bound),
+2^-24 for the weights handed over in fp32, and E_X a bound on the
 error of the layer's input as the GPU holds it (rounding of the given inputs,
 the previous layer's own bound, the moving average's roundings).  u is taken
 as 2^-23, one unit in the last place of fp32, which bounds any faithful
@@ -49,11 +54,14 @@ def gamma(n, u=U32):
 
 def product_factor(dt: str, K: int, row_terms: np.ndarray) -> np.ndarray:
     """c_v per output row (column vector) for K products and row_terms aggregated rows."""
-    b = UBF16 if dt == "bf16" else 0.0
+    bf16 = dt == "bf16"
+    b = UBF16 if bf16 else 0.0
     w = 2.0 ** -24                     # the weights are handed to the GPU rounded to fp32
+    # fp32: six part products per product, the dropped ones below p |x y|
+    p, terms = (0.0, K) if bf16 else (2.0 ** -20, 6 * K)
     # each aggregated row may enter as three exact bf16 parts (the dense block on the matrix cores)
-    return ((1.0 + b) ** 2 * (1.0 + w) * (1.0 + gamma(K)) * (1.0 + gamma(3 * np.asarray(row_terms) + 4))
-            - 1.0)[:, None]
+    return ((1.0 + b) ** 2 * (1.0 + w) * (1.0 + p) * (1.0 + gamma(terms))
+            * (1.0 + gamma(3 * np.asarray(row_terms) + 4)) - 1.0)[:, None]
 
 
 def row_lengths(P) -> np.ndarray:

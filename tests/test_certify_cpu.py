@@ -21,25 +21,83 @@ def setup(seed, f=48, f_out=24, sage=False):
     return ref, P, X, W
 
 
-def fp32_layer(P, X, W, order, bf16):
+def split3(x):
+    """fp32 x as hi + mid + lo: hi = x with its low 16 bits cleared, mid = x - hi rounded to
+    bf16 (nearest even), lo = the rest (the split of the fp32 update GEMMs)."""
+    def rne(v):
+        vb = v.view(np.uint32).astype(np.uint64)
+        return (((vb + 0x7FFF + ((vb >> 16) & 1)) & 0xFFFF0000).astype(np.uint32)).view(np.float32)
+
+    x = np.asarray(x, dtype=np.float32)
+    hi = (x.view(np.uint32) & np.uint32(0xFFFF0000)).view(np.float32)
+    r = (x - hi).astype(np.float32)
+    mid = rne(r)
+    return hi, mid, rne((r - mid).astype(np.float32))
+
+
+def is_bf16(v):
+    return np.all((np.asarray(v, dtype=np.float32).view(np.uint32) & np.uint32(0xFFFF)) == 0)
+
+
+def test_split_is_exact_and_small():
+    rng = np.random.default_rng(4)
+    x = (rng.standard_normal(400_000) * np.exp2(rng.integers(-100, 100, 400_000))).astype(np.float32)
+    x[:4] = [0.0, -0.0, np.finfo(np.float32).max, -np.finfo(np.float32).tiny]
+    hi, mid, lo = split3(x)
+    assert is_bf16(hi) and is_bf16(mid) and is_bf16(lo)
+    # exact for |x| >= 2^-111: the three parts add up to x in fp64 (and so in any order);
+    # below, the last part is a bf16 subnormal, within half its spacing (2^-134)
+    ax = np.abs(x.astype(np.float64))
+    err = np.abs(hi.astype(np.float64) + mid.astype(np.float64) + lo.astype(np.float64) - ax * np.sign(x))
+    assert (ax < 2.0 ** -111).sum() > 0
+    assert np.all(err[ax >= 2.0 ** -111] == 0) and np.all(err <= 2.0 ** -134)
+    assert np.all(np.abs(mid) < 2.0 ** -7 * ax + (ax == 0)) and np.all(np.abs(lo) <= 2.0 ** -15 * ax)
+
+
+def test_dropped_part_products_are_below_the_bound():
+    rng = np.random.default_rng(6)
+    a = (rng.standard_normal(200_000) * np.exp2(rng.integers(-20, 20, 200_000))).astype(np.float32)
+    b = (rng.standard_normal(200_000) * np.exp2(rng.integers(-20, 20, 200_000))).astype(np.float32)
+    (a1, a2, a3), (b1, b2, b3) = [[p.astype(np.float64) for p in split3(v)] for v in (a, b)]
+    kept = a1 * b1 + a1 * b2 + a2 * b1 + a1 * b3 + a2 * b2 + a3 * b1
+    exact = a.astype(np.float64) * b.astype(np.float64)
+    assert np.all(np.abs(exact - kept) <= 2.0 ** -21 * (1 + 2.0 ** -7) * np.abs(exact))
+    # the part products are exact in fp32 (8 x 8 significant bits)
+    for p, q in ((a1, b1), (a1, b2), (a2, b1), (a1, b3), (a2, b2), (a3, b1)):
+        assert np.array_equal((p * q).astype(np.float32).astype(np.float64), p * q)
+
+
+def fp32_by_parts(A32, W32):
+    """A32 @ W32 as the fp32 GEMM by parts computes it: six part products, summed in fp32."""
+    (a1, a2, a3), (w1, w2, w3) = split3(A32), split3(W32)
+    out = np.zeros((A32.shape[0], W32.shape[1]), dtype=np.float32)
+    for p, q in ((a3, w1), (a2, w2), (a1, w3), (a2, w1), (a1, w2), (a1, w1)):
+        out = (out + (p @ q).astype(np.float32)).astype(np.float32)
+    return out
+
+
+def fp32_layer(P, X, W, order, bf16, parts=False):
     """The layer evaluated as the GPU does: fp32 inputs, fp32 sums, bf16 operands on the bf16 path."""
     P32 = P.astype(np.float32)
     X32 = X.astype(np.float32)
     W32 = W.astype(np.float32)
     q = (lambda a: layers.round_bf16(a).astype(np.float32)) if bf16 else (lambda a: a)
+    mm = fp32_by_parts if parts else (lambda a, w: a @ w)
     if order == "transform":
-        return (P32 @ (q(X32) @ q(W32))).astype(np.float64)
+        return (P32 @ mm(q(X32), q(W32))).astype(np.float64)
     A32 = (P32 @ X32).astype(np.float32)
-    return (q(A32) @ q(W32)).astype(np.float64)
+    return mm(q(A32), q(W32)).astype(np.float64)
 
 
 @pytest.mark.parametrize("order", ["agg", "transform"])
-@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("dt", ["f32", "f32-parts", "bf16"])
 @pytest.mark.parametrize("seed", [0, 1])
 def test_bound_holds_for_fp32_and_bf16_evaluations(order, dt, seed):
     ref, P, X, W = setup(seed)
     Z = P @ X @ W
-    Zg = fp32_layer(P, X, W, order, dt == "bf16")
+    parts = dt == "f32-parts"
+    dt = "f32" if parts else dt
+    Zg = fp32_layer(P, X, W, order, dt == "bf16", parts)
     B = z_bound(P, X, input_rounding(X), W, dt)
     assert np.all(np.abs(Zg - Z) <= B)
     # the bound is not vacuous: a decision is certified only for |Z| well below the layer's scale
