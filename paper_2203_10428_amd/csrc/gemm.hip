@@ -32,6 +32,7 @@
 // that operand is fp32 in memory and rounded while staged (template A32).
 #include <algorithm>
 #include <cstdlib>
+#include <cstring>
 
 #include "internal.h"
 
@@ -240,6 +241,150 @@ __global__ __launch_bounds__(256, BN == 128 ? 2 : 3) void gemm_tn_f32(TNParams p
         if (fm < p.M && fn < p.N) out[(int64_t)fm * p.N + fn] = acc[i][j][q];
       }
   }
+}
+
+// -------------------------------------------------------- fp32 by parts ---
+//
+// The fp32 weight gradient on the bf16 matrix cores, as the node-major fp32
+// GEMMs do it: A and J ∘ mask enter as three exact bf16 parts each (hi = x
+// with its low 16 bits cleared, mid = x - hi rounded to nearest, lo = the
+// rest), and each block accumulates in fp32 the six part products hi.hi,
+// hi.mid, mid.hi, hi.lo, mid.mid, lo.hi (the three dropped ones are below
+// 2^-21 (1 + 2^-7) |a b| together).  Slabs of 16 nodes, one
+// v_mfma_f32_32x32x16_bf16 step per part product; both operands transposed
+// into LDS (one row per feature, 16 nodes = two 16-byte groups, the groups
+// swapped in rows 8 .. 15 of every 16), three planes each, double buffered
+// (48 KB, three workgroups per CU).  Thread item: 4 nodes x 4 features of A
+// (threads 0 .. 127) or of J (threads 128 ..), node quad fastest, so the 32
+// lanes of one 8-byte LDS write pass cover 8 whole rows; feature 4u + e sits
+// in LDS row e U + u.  Lane half h takes nodes 8h .. 8h + 7 of the slab.
+
+__device__ __forceinline__ void tn_split3x2(float x0, float x1, uint32_t &hi, uint32_t &mid, uint32_t &lo) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const uint32_t b0 = __float_as_uint(x0), b1 = __float_as_uint(x1);
+  const float r0 = x0 - __uint_as_float(b0 & 0xffff0000u), r1 = x1 - __uint_as_float(b1 & 0xffff0000u);
+  hi = __builtin_amdgcn_perm(b1, b0, 0x07060302u);    // the high halves of b0 (low) and b1 (high)
+  mid = __builtin_bit_cast(uint32_t, (bf16x2){(__bf16)r0, (__bf16)r1});
+  const float l0 = r0 - __uint_as_float(mid << 16), l1 = r1 - __uint_as_float(mid & 0xffff0000u);
+  lo = __builtin_bit_cast(uint32_t, (bf16x2){(__bf16)l0, (__bf16)l1});
+}
+
+__device__ __forceinline__ int tn_sw2(int row, int g) { return g ^ ((row >> 3) & 1); }
+
+// Raw loads of one thread item: nodes nq .. nq + 3 (zero past kend or for an
+// absent operand), features col .. col + 3; rows >= ksplit come from src_hi
+// (row - ksplit).  hsrc: the mask source (left at 1 when null).
+__device__ __forceinline__ void tn_parts_load(f32x4 (&x)[4], f32x4 (&hm)[4], const float *src_lo, const float *src_hi,
+                                              const float *hsrc, int64_t ld_src, int64_t ld_h, int ksplit, int nq,
+                                              int kend, int col, bool fok) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int node = nq + s;
+    const bool hi = node >= ksplit;
+    const float *src = hi ? src_hi : src_lo;
+    const bool ok = fok && node < kend && src != nullptr;
+    const int64_t row = hi ? node - ksplit : node;
+    x[s] = ok ? *reinterpret_cast<const f32x4 *>(src + row * ld_src + col) : f32x4{0.f, 0.f, 0.f, 0.f};
+    if (hsrc) hm[s] = (fok && node < kend) ? *reinterpret_cast<const f32x4 *>(hsrc + (int64_t)node * ld_h + col)
+                                           : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+
+// Masks, splits and writes one thread item into the three planes at base
+// (plane elements apart): feature e of quad uq in row e U + uq, node quad kq.
+__device__ __forceinline__ void tn_parts_store(const f32x4 (&x)[4], const f32x4 (&hm)[4], uint16_t *base, int plane,
+                                               int U, int uq, int kq) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float v0 = hm[0][e] > 0.f ? x[0][e] : 0.f, v1 = hm[1][e] > 0.f ? x[1][e] : 0.f;
+    const float v2 = hm[2][e] > 0.f ? x[2][e] : 0.f, v3 = hm[3][e] > 0.f ? x[3][e] : 0.f;
+    uint32_t hi01, mi01, lo01, hi23, mi23, lo23;
+    tn_split3x2(v0, v1, hi01, mi01, lo01);
+    tn_split3x2(v2, v3, hi23, mi23, lo23);
+    const int row = e * U + uq;
+    const int off = row * 16 + 8 * tn_sw2(row, kq / 2) + 4 * (kq % 2);
+    *reinterpret_cast<u32x2 *>(base + off) = u32x2{hi01, hi23};
+    *reinterpret_cast<u32x2 *>(base + plane + off) = u32x2{mi01, mi23};
+    *reinterpret_cast<u32x2 *>(base + 2 * plane + off) = u32x2{lo01, lo23};
+  }
+}
+
+template <int BN>
+__global__ __launch_bounds__(256, 3) void gemm_tn_f32s(TNParams p) {
+  constexpr int BM = 128, BK = 16;
+  constexpr int UA = BM / 4, UB = BN / 4;              // feature quads of the tiles
+  constexpr int PA = BM * BK, PB = BN * BK;            // bf16 elements of one plane
+  constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
+  static_assert(UA * 4 == 128 && UB * 4 <= 128, "one item per thread");
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][3][PA];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][3][PB];
+
+  const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
+  int split, tile;
+  tn_coords(p.tiles, split, tile);
+  const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
+  const int kbeg = split * p.kchunk;
+  const int kend = min(p.K, kbeg + p.kchunk);
+  const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
+
+  const bool isA = t < 128;                            // wave-uniform
+  const int it = isA ? t : t - 128;
+  const int kq = it % 4, uq = it / 4;                  // node quad, feature quad
+  const bool hasB = !isA && uq < UB;
+  const bool fok = isA ? m0 + 4 * uq < p.M : (hasB && n0 + 4 * uq < p.N);
+
+  // this thread's operand rows: A (rows >= ksplit from A_hi) or J and its mask source H
+  const float *src_lo = isA ? p.A : p.J, *src_hi = isA ? p.A_hi : nullptr, *hsrc = isA ? nullptr : p.H;
+  const int64_t ld_src = isA ? p.lda : p.ldb, ld_h = p.ldh;
+  const int ksplit = isA ? p.ksplit : p.K, col = (isA ? m0 : n0) + 4 * uq;
+  f32x4 x[4], hm[4];                                   // node s of the quad: features col .. col + 3
+#pragma unroll
+  for (int s = 0; s < 4; ++s) hm[s] = f32x4{1.f, 1.f, 1.f, 1.f};
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
+
+  const int h = lane >> 5, r = lane & 31;
+  if (kbeg < kend) {
+    tn_parts_load(x, hm, src_lo, src_hi, hsrc, ld_src, ld_h, ksplit, kbeg + 4 * kq, kend, col, fok);
+    if (isA || hasB)
+      tn_parts_store(x, hm, isA ? &As[0][0][0] : &Bs[0][0][0], isA ? PA : PB, isA ? UA : UB, uq, kq);
+    __syncthreads();
+    int itn = 0;
+    for (int kt = kbeg; kt < kend; kt += BK, ++itn) {
+      const int cur = itn & 1;
+      tn_parts_load(x, hm, src_lo, src_hi, hsrc, ld_src, ld_h, ksplit, (kt + BK < kend ? kt + BK : kt) + 4 * kq,
+                    kend, col, fok);
+      bf16x8 a[3][TM], b[3][TN];
+#pragma unroll
+      for (int pl = 0; pl < 3; ++pl) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int row = wm0 + i * 32 + r;
+          a[pl][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(&As[cur][pl][row * BK + 8 * tn_sw2(row, h)]));
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int row = wn0 + j * 32 + r;
+          b[pl][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(&Bs[cur][pl][row * BK + 8 * tn_sw2(row, h)]));
+        }
+      }
+      constexpr int PX[6] = {2, 1, 0, 1, 0, 0}, PY[6] = {0, 1, 2, 0, 1, 0};   // parts of A / of J, smallest first
+#pragma unroll
+      for (int u = 0; u < 6; ++u)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[PX[u]][i], b[PY[u]][j], acc[i][j], 0, 0, 0);
+      if (isA || hasB)
+        tn_parts_store(x, hm, isA ? &As[cur ^ 1][0][0] : &Bs[cur ^ 1][0][0], isA ? PA : PB, isA ? UA : UB, uq, kq);
+      __syncthreads();
+    }
+  }
+  tn_store_partial<TM, TN, UA, 4, UB>(p, acc, split, m0, n0, wm0, wn0, lane);
 }
 
 // ------------------------------------------------------------------ bf16 ---
@@ -459,6 +604,13 @@ static int tn_bm(int M, int N, bool bf16) {
   return (M + 255) / 256 * 256 <= (M + 127) / 128 * 128 ? 256 : 128;
 }
 
+// fp32 weight gradients by parts (the default) or on the fp32 matrix cores
+// (PGCN_GEMM_F32=native, read per call)
+static bool tn_f32_by_parts() {
+  const char *e = std::getenv("PGCN_GEMM_F32");
+  return !(e && std::strcmp(e, "native") == 0);
+}
+
 static int tn_tiles(int M, int N, int bm) {
   const int BN = N <= 64 ? 64 : 128;
   return ((M + bm - 1) / bm) * ((N + BN - 1) / BN);
@@ -494,7 +646,7 @@ size_t gemm_workspace(Gemm kind, int32_t M, int32_t N, int32_t K) {
 }
 
 template <int BM, int BN>
-static void tn_launch(TNParams p, bool bf16, bool a32, int splits, hipStream_t s) {
+static void tn_launch(TNParams p, bool bf16, bool a32, bool parts, int splits, hipStream_t s) {
   p.tiles_n = (p.N + BN - 1) / BN;
   p.tiles = ((p.M + BM - 1) / BM) * p.tiles_n;
   const int slab = bf16 ? 32 : 16;
@@ -505,6 +657,7 @@ static void tn_launch(TNParams p, bool bf16, bool a32, int splits, hipStream_t s
   const dim3 grid((unsigned)(p.tiles * splits));
   if (bf16 && a32) hipLaunchKernelGGL((gemm_tn_bf16<BN, true>), grid, dim3(256), 0, s, p);
   else if (bf16) hipLaunchKernelGGL((gemm_tn_bf16<BN, false>), grid, dim3(256), 0, s, p);
+  else if (parts && BM == 128) hipLaunchKernelGGL((gemm_tn_f32s<BN>), grid, dim3(256), 0, s, p);
   else hipLaunchKernelGGL((gemm_tn_f32<BM, BN>), grid, dim3(256), 0, s, p);
 }
 
@@ -513,8 +666,9 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return PGCN_OK;
   const bool bf16 = g.dtype == PGCN_BF16;
   const bool a32 = g.k_split > 0;                      // second left matrix; fp32 left operand on both paths
-  const int bm = tn_bm(g.M, g.N, bf16);
-  const int splits = splitk_count(g.M, g.N, g.K, tn_slots(g.N, bf16, a32), bm);
+  const bool parts = !bf16 && tn_f32_by_parts();
+  const int bm = parts ? 128 : tn_bm(g.M, g.N, bf16);
+  const int splits = splitk_count(g.M, g.N, g.K, parts ? 768 : tn_slots(g.N, bf16, a32), bm);
   const size_t need = (size_t)splits * (size_t)g.M * (size_t)g.N * sizeof(float);
   if (!g.workspace || g.workspace_bytes < need)
     return set_error(PGCN_EWORKSPACE, "weight-gradient GEMM: workspace too small");
@@ -542,9 +696,9 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   }
   {
     TraceScope ts(PGCN_TK_GEMM_WGRAD, s);
-    if (g.N <= 64) tn_launch<128, 64>(p, bf16, a32, splits, s);
-    else if (bm == 256) tn_launch<256, 128>(p, bf16, a32, splits, s);
-    else tn_launch<128, 128>(p, bf16, a32, splits, s);
+    if (g.N <= 64) tn_launch<128, 64>(p, bf16, a32, parts, splits, s);
+    else if (bm == 256) tn_launch<256, 128>(p, bf16, a32, parts, splits, s);
+    else tn_launch<128, 128>(p, bf16, a32, parts, splits, s);
     PGCN_HIP(hipGetLastError());
   }
   const int64_t mn = (int64_t)g.M * g.N;

@@ -4,8 +4,9 @@ cores, fp32 accumulation) against the fp64 oracle and against the plain fp32
 matrix-core kernels (PGCN_GEMM_F32=native) on the same inputs: every element
 within the certified rounding bound (tests/certify.py), and the largest error
 no more than twice the plain kernel's (or 2^-20 of the output's scale).
-Forward (plain, ReLU) and feature gradient (masked, row-scaled operand)
-GEMMs, ragged widths and row tiles."""
+Forward (plain) GEMM, feature gradient (masked, row-scaled operand) and
+weight gradient (node-split, masked right operand); ragged widths and row
+tiles."""
 import os
 from contextlib import contextmanager
 
@@ -88,9 +89,9 @@ def test_feature_gradient_by_parts(graph, f_in, f_out):
     Z = rng.standard_normal((n, f_out))
     J = rng.standard_normal((n, f_out)) * 1e-2
     W = rng.uniform(-0.2, 0.2, (f_in, f_out)).astype(np.float32)
-    _, Jf_ref = layers.layer_backward(P, A, Z, J, W.astype(np.float64), True, True)
+    G_ref, Jf_ref = layers.layer_backward(P, A, Z, J, W.astype(np.float64), True, True)
     nb = max(B.pgcn_workspace_size(part, f_in, f_out, B.PGCN_F32), 256)
-    out = {}
+    out, outG = {}, {}
     for mode in ("parts", "native"):
         ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
         J_in, J_bd = dev(np.zeros((n, f_in))), dev(np.zeros((b, f_in)))
@@ -102,10 +103,15 @@ def test_feature_gradient_by_parts(graph, f_in, f_out):
                              workspace_bytes=nb)
         torch.cuda.synchronize()
         out[mode] = np.vstack([host(J_in, f_in), host(J_bd, f_in)])
+        outG[mode] = dG.cpu().numpy().astype(np.float64)
     e_parts, e_native = max_rel(out["parts"], Jf_ref), max_rel(out["native"], Jf_ref)
-    print(f"feature gradient {f_in}x{f_out}: max rel err by parts {e_parts:.2e}, native {e_native:.2e}")
+    g_parts, g_native = max_rel(outG["parts"], G_ref), max_rel(outG["native"], G_ref)
+    print(f"feature gradient {f_in}x{f_out}: max rel err by parts {e_parts:.2e}, native {e_native:.2e}; "
+          f"weight gradient by parts {g_parts:.2e}, native {g_native:.2e}")
     assert e_parts <= max(2.0 * e_native, 2.0 ** -20)
     assert e_parts < 1e-5
+    assert g_parts <= max(2.0 * g_native, 2.0 ** -20)
+    assert g_parts < 1e-5
 
 
 def test_non_finite_operands_stay_non_finite(graph):
