@@ -31,6 +31,13 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+# fp32 GEMMs by parts: six bf16 part products per fp32 product on the bf16 matrix cores
+F32_PARTS_CEILING_TFLOPS = MFMA_PEAK_TFLOPS["bf16"] / 6
+
+
+def f32_gemm_method() -> str:
+    """The library's fp32 GEMM path: exact bf16 parts (default) or the fp32 matrix cores."""
+    return "fp32-matrix-cores" if os.environ.get("PGCN_GEMM_F32") == "native" else "bf16-parts-x6"
 XGMI_LINK_GBPS = 153.0                   # one xGMI link of MI355X, per direction
 VARIANTS = {"PipeGCN": (False, False), "PipeGCN-G": (False, True), "PipeGCN-F": (True, False),
             "PipeGCN-GF": (True, True)}
@@ -305,6 +312,10 @@ def main():
             util[k] = {"TFLOPs": work[k] / sec / 1e12, "mfma_frac": work[k] / sec / 1e12 / MFMA_PEAK_TFLOPS[dt],
                        "flop_per_byte": ai, "attainable_TFLOPs": attain,
                        "frac_attainable": work[k] / sec / 1e12 / attain}
+            if dt == "f32" and f32_gemm_method() == "bf16-parts-x6":
+                # fp32-equivalent rate against the ceiling of the by-parts form
+                util[k]["parts_ceiling_TFLOPs"] = F32_PARTS_CEILING_TFLOPS
+                util[k]["frac_parts_ceiling"] = work[k] / sec / 1e12 / F32_PARTS_CEILING_TFLOPS
     if dominant.startswith("agg"):
         ach = util[dominant]["GBps_compulsory"]
         tr_bytes = measured_traffic(w.name, dominant)
@@ -385,6 +396,7 @@ def main():
                    "transform_first_layers": [l for l in range(1, tr.L + 1) if tr.order[l] == B.PGCN_ORDER_TRANSFORM],
                    "widths": list(w.widths),
                    "loss": w.loss, "gemm_dtype": w.gemm_dtype, "aggregation_dtype": "f32",
+                   "f32_gemm": f32_gemm_method() if w.gemm_dtype != "bf16" else None,
                    "n_inner": i["n_inner"], "n_bd": i["n_bd"], "n_send": i["n_send"], "nnz": i["nnz"],
                    "max_row_len": i["max_row_len"],
                    # the block of P_i (and of P_i^T) aggregated on the matrix cores: rows, columns, non-zeros

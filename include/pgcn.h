@@ -499,10 +499,10 @@ int pgcn_sage_layer_bwd(const pgcn_partition *part, const pgcn_sage_bwd_args *ar
 /* Refill of a stale buffer (Algorithm 1's send/receive threads; the paper runs
  * them on a second stream): an asynchronous copy of `bytes` bytes into device
  * memory `dst`, enqueued on `stream`.  flags = 0: device-to-device on the
- * compute units; when both buffers are device memory, 16-byte aligned and
- * `bytes` is a multiple of 16, by the library's copy kernel with
+ * compute units; copies of at least 4 MiB between 16-byte-aligned device
+ * buffers (`bytes` a multiple of 16) by the library's copy kernel with
  * non-temporal loads and stores (the copied rows are read in the next
- * iteration, so they bypass the caches the current one uses), otherwise by
+ * iteration, so they bypass the caches the current one uses), others by
  * the runtime's copy; PGCN_REFILL_DMA:
  * device-to-device by the DMA engines, using no compute units (as a transfer
  * arriving from a peer GPU would); PGCN_REFILL_FROM_HOST: `src` is pinned

@@ -1083,10 +1083,13 @@ extern "C" int pgcn_refill_async(void *dst, const void *src, size_t bytes, uint3
     return PGCN_OK;
   }
   TraceScope ts(PGCN_TK_REFILL, s);
-  // flags = 0 on 16-byte-aligned device buffers: the library's non-temporal copy kernel;
-  // anything else goes to the runtime's copy, which validates host pointers itself.
+  // flags = 0, at least kRefillKernelMin bytes, 16-byte-aligned device buffers: the library's
+  // non-temporal copy kernel.  Anything else goes to the runtime's copy, which validates host
+  // pointers itself; small copies skip the pointer lookups (microseconds each) that the
+  // kernel path needs.
+  constexpr size_t kRefillKernelMin = size_t(4) << 20;
   const bool vec = (bytes % 16) == 0 && ((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src)) & 15) == 0;
-  if (!(flags & PGCN_REFILL_DMA) && vec && is_device_memory(dst) && is_device_memory(src))
+  if (!(flags & PGCN_REFILL_DMA) && vec && bytes >= kRefillKernelMin && is_device_memory(dst) && is_device_memory(src))
     return launch_refill_copy(dst, src, bytes, s);
   PGCN_HIP(hipMemcpyAsync(dst, src, bytes, (flags & PGCN_REFILL_DMA) ? hipMemcpyDeviceToDeviceNoCU : hipMemcpyDeviceToDevice, s));
   return PGCN_OK;
