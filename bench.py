@@ -308,11 +308,12 @@ def main():
             # the attainable rate is the lower of the matrix-core peak and the product's arithmetic
             # intensity (flops per compulsory byte) times the HBM peak
             ai = work[k] / max(work[k + "_bytes"], 1.0)
-            attain = min(MFMA_PEAK_TFLOPS[dt], ai * HBM_PEAK_GBPS / 1e3)
+            parts = dt == "f32" and f32_gemm_method() == "bf16-parts-x6"
+            attain = min(F32_PARTS_CEILING_TFLOPS if parts else MFMA_PEAK_TFLOPS[dt], ai * HBM_PEAK_GBPS / 1e3)
             util[k] = {"TFLOPs": work[k] / sec / 1e12, "mfma_frac": work[k] / sec / 1e12 / MFMA_PEAK_TFLOPS[dt],
                        "flop_per_byte": ai, "attainable_TFLOPs": attain,
                        "frac_attainable": work[k] / sec / 1e12 / attain}
-            if dt == "f32" and f32_gemm_method() == "bf16-parts-x6":
+            if parts:
                 # fp32-equivalent rate against the ceiling of the by-parts form
                 util[k]["parts_ceiling_TFLOPs"] = F32_PARTS_CEILING_TFLOPS
                 util[k]["frac_parts_ceiling"] = work[k] / sec / 1e12 / F32_PARTS_CEILING_TFLOPS

@@ -387,6 +387,94 @@ __global__ __launch_bounds__(256, 3) void gemm_tn_f32s(TNParams p) {
   tn_store_partial<TM, TN, UA, 4, UB>(p, acc, split, m0, n0, wm0, wn0, lane);
 }
 
+// 256 x 128 tiles by parts (each wave 128 x 64): twice the matrix-core work
+// of a 128 x 128 tile for 4/3 of its staged bytes, since the staging (the
+// vector-memory path), not the matrix cores, bounds the narrower tile.  Every
+// thread stages an A item (4 nodes x 4 of the 256 features); threads 0 .. 127
+// also stage a J item.  72 KB of LDS, two workgroups per CU; the A parts are
+// read from LDS one plane at a time to leave room for the 128 accumulators.
+__global__ __launch_bounds__(256, 2) void gemm_tn_f32s_wide(TNParams p) {
+  constexpr int BM = 256, BN = 128, BK = 16;
+  constexpr int UA = BM / 4, UB = BN / 4;
+  constexpr int PA = BM * BK, PB = BN * BK;
+  constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][3][PA];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][3][PB];
+
+  const int t = threadIdx.x, lane = t % 64, wave = __builtin_amdgcn_readfirstlane(t / 64);
+  int split, tile;
+  tn_coords(p.tiles, split, tile);
+  const int m0 = (tile / p.tiles_n) * BM, n0 = (tile % p.tiles_n) * BN;
+  const int kbeg = split * p.kchunk;
+  const int kend = min(p.K, kbeg + p.kchunk);
+  const int wm0 = (wave / 2) * WM, wn0 = (wave % 2) * WN;
+
+  const int kq = t % 4, uq = t / 4;                    // node quad; feature quad (A: all, J: t < 128)
+  const bool hasB = t < 128;                           // waves 0 and 1
+  const bool fa = m0 + 4 * uq < p.M, fb = hasB && n0 + 4 * uq < p.N;
+  f32x4 xa[4], ha[4], xb[4], hb[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    ha[s] = f32x4{1.f, 1.f, 1.f, 1.f};
+    hb[s] = f32x4{1.f, 1.f, 1.f, 1.f};
+  }
+  auto load = [&](int kt) __attribute__((always_inline)) {
+    const int nq = kt + 4 * kq;
+    tn_parts_load(xa, ha, p.A, p.A_hi, nullptr, p.lda, 0, p.ksplit, nq, kend, m0 + 4 * uq, fa);
+    if (hasB) tn_parts_load(xb, hb, p.J, nullptr, p.H, p.ldb, p.ldh, p.K, nq, kend, n0 + 4 * uq, fb);
+  };
+  auto store = [&](int b) __attribute__((always_inline)) {
+    tn_parts_store(xa, ha, &As[b][0][0], PA, UA, uq, kq);
+    if (hasB) tn_parts_store(xb, hb, &Bs[b][0][0], PB, UB, uq, kq);
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x16){};
+
+  const int h = lane >> 5, r = lane & 31;
+  if (kbeg < kend) {
+    load(kbeg);
+    store(0);
+    __syncthreads();
+    int itn = 0;
+    for (int kt = kbeg; kt < kend; kt += BK, ++itn) {
+      const int cur = itn & 1;
+      load(kt + BK < kend ? kt + BK : kt);
+      bf16x8 b[3][TN];
+#pragma unroll
+      for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int row = wn0 + j * 32 + r;
+          b[pl][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(&Bs[cur][pl][row * BK + 8 * tn_sw2(row, h)]));
+        }
+      // A parts lo, mid, hi in turn, each with the J parts that keep its products (smallest first)
+#pragma unroll
+      for (int pa = 2; pa >= 0; --pa) {
+        bf16x8 a[TM];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int row = wm0 + i * 32 + r;
+          a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(&As[cur][pa][row * BK + 8 * tn_sw2(row, h)]));
+        }
+#pragma unroll
+        for (int pb = 2 - pa; pb >= 0; --pb)
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[pb][j], acc[i][j], 0, 0, 0);
+      }
+      store(cur ^ 1);
+      __syncthreads();
+    }
+  }
+  tn_store_partial<TM, TN, UA, 4, UB>(p, acc, split, m0, n0, wm0, wn0, lane);
+}
+
 // ------------------------------------------------------------------ bf16 ---
 
 template <int BN, bool A32>
@@ -589,12 +677,13 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *ws, int
 
 // ---------------------------------------------------------------- launch ---
 
-// Tile height of the fp32 kernel: 256 (each wave 128 x 64: the same staged
-// bytes feed twice the MFMAs, and staging, not the matrix cores, bounds the
-// 128-row tile) for 128-wide tiles when f_in >= 384 and 256-row tiles pad it
-// no further than 128-row tiles would; 128 otherwise and on bf16 (at f_in =
-// 256 the two tiles leave the grid short of one round of resident
-// workgroups: measured slower).  PGCN_TN_BM=128 (environment) keeps 128.
+// Tile height of the fp32 kernels (plain and by parts): 256 (each wave
+// 128 x 64: the same staged bytes feed twice the MFMAs, and staging, not the
+// matrix cores, bounds the 128-row tile) for 128-wide tiles when f_in >= 384
+// and 256-row tiles pad it no further than 128-row tiles would; 128
+// otherwise and on bf16 (at f_in = 256 the two tiles leave the grid short of
+// one round of resident workgroups: measured slower).  PGCN_TN_BM=128
+// (environment) keeps 128.
 static int tn_bm(int M, int N, bool bf16) {
   static const bool only128 = [] {
     const char *e = std::getenv("PGCN_TN_BM");
@@ -658,6 +747,7 @@ static void tn_launch(TNParams p, bool bf16, bool a32, bool parts, int splits, h
   if (bf16 && a32) hipLaunchKernelGGL((gemm_tn_bf16<BN, true>), grid, dim3(256), 0, s, p);
   else if (bf16) hipLaunchKernelGGL((gemm_tn_bf16<BN, false>), grid, dim3(256), 0, s, p);
   else if (parts && BM == 128) hipLaunchKernelGGL((gemm_tn_f32s<BN>), grid, dim3(256), 0, s, p);
+  else if (parts && BN == 128) hipLaunchKernelGGL(gemm_tn_f32s_wide, grid, dim3(256), 0, s, p);
   else hipLaunchKernelGGL((gemm_tn_f32<BM, BN>), grid, dim3(256), 0, s, p);
 }
 
@@ -667,8 +757,8 @@ int launch_gemm(Gemm kind, const GemmArgs &g, hipStream_t s) {
   const bool bf16 = g.dtype == PGCN_BF16;
   const bool a32 = g.k_split > 0;                      // second left matrix; fp32 left operand on both paths
   const bool parts = !bf16 && tn_f32_by_parts();
-  const int bm = parts ? 128 : tn_bm(g.M, g.N, bf16);
-  const int splits = splitk_count(g.M, g.N, g.K, parts ? 768 : tn_slots(g.N, bf16, a32), bm);
+  const int bm = tn_bm(g.M, g.N, bf16);
+  const int splits = splitk_count(g.M, g.N, g.K, parts ? (bm == 256 ? 512 : 768) : tn_slots(g.N, bf16, a32), bm);
   const size_t need = (size_t)splits * (size_t)g.M * (size_t)g.N * sizeof(float);
   if (!g.workspace || g.workspace_bytes < need)
     return set_error(PGCN_EWORKSPACE, "weight-gradient GEMM: workspace too small");

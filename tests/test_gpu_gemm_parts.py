@@ -80,7 +80,7 @@ def test_forward_by_parts(graph, f_in, f_out):
     assert e_parts <= max(2.0 * e_native, 2.0 ** -20)
 
 
-@pytest.mark.parametrize("f_in,f_out", [(47, 41), (512, 300), (256, 256), (130, 1100)])
+@pytest.mark.parametrize("f_in,f_out", [(47, 41), (512, 300), (256, 256), (130, 1100), (1000, 200)])
 def test_feature_gradient_by_parts(graph, f_in, f_out):
     ref, P, part = graph
     n, b = ref.n_inner, ref.n_bd
