@@ -157,7 +157,7 @@ __global__ __launch_bounds__(256) void accum_kernel(const int64_t *__restrict__ 
     float4 v = d[c4];
 #pragma unroll 4
     for (int64_t q = b; q < e; ++q) {   // ascending send-list position: ascending peer (loads are independent)
-      const float4 x = reinterpret_cast<const float4 *>(src + (int64_t)inv_k[q] * ld)[c4];
+      const ew_f32x4 x = __builtin_nontemporal_load(reinterpret_cast<const ew_f32x4 *>(src + (int64_t)inv_k[q] * ld) + c4);
       v.x += x.x;
       v.y += x.y;
       v.z += x.z;
@@ -196,10 +196,14 @@ __global__ __launch_bounds__(256) void accum_ema_kernel(const int64_t *__restric
       float4 x[4], m[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) k[j] = inv_k[q0 + (j < n ? j : n - 1)];
+      // the received rows and the moving averages are next read in a later
+      // iteration: non-temporal, so they leave the caches to the inner rows
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        x[j] = reinterpret_cast<const float4 *>(src + k[j] * ld)[c4];
-        m[j] = reinterpret_cast<const float4 *>(state + k[j] * ld)[c4];
+        const ew_f32x4 xs = __builtin_nontemporal_load(reinterpret_cast<const ew_f32x4 *>(src + k[j] * ld) + c4);
+        const ew_f32x4 ms = __builtin_nontemporal_load(reinterpret_cast<const ew_f32x4 *>(state + k[j] * ld) + c4);
+        x[j] = make_float4(xs.x, xs.y, xs.z, xs.w);
+        m[j] = make_float4(ms.x, ms.y, ms.z, ms.w);
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -207,7 +211,9 @@ __global__ __launch_bounds__(256) void accum_ema_kernel(const int64_t *__restric
         m[j].y = gamma * m[j].y + g1 * x[j].y;
         m[j].z = gamma * m[j].z + g1 * x[j].z;
         m[j].w = gamma * m[j].w + g1 * x[j].w;
-        if (j < n) reinterpret_cast<float4 *>(state + k[j] * ld)[c4] = m[j];
+        if (j < n)
+          __builtin_nontemporal_store((ew_f32x4){m[j].x, m[j].y, m[j].z, m[j].w},
+                                      reinterpret_cast<ew_f32x4 *>(state + k[j] * ld) + c4);
         const bool in = j < n;
         v.x = in ? v.x + m[j].x : v.x;
         v.y = in ? v.y + m[j].y : v.y;
