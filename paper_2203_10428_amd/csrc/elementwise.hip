@@ -35,6 +35,8 @@ static unsigned row_blocks(int64_t rows, int sh) {
   return (unsigned)((rows + rpb - 1) / rpb);
 }
 
+typedef float ew_f32x4 __attribute__((ext_vector_type(4)));
+
 __global__ __launch_bounds__(256) void ema_kernel(float *state, const float *in, int64_t rows, int f4, int64_t ld,
                                                   float gamma, int sh) {
   const int64_t r = (int64_t)blockIdx.x * (256 >> sh) + (threadIdx.x >> sh);
@@ -42,7 +44,8 @@ __global__ __launch_bounds__(256) void ema_kernel(float *state, const float *in,
   const float g1 = 1.0f - gamma;
   for (int c4 = threadIdx.x & ((1 << sh) - 1); c4 < f4; c4 += 1 << sh) {
     float4 *sp = reinterpret_cast<float4 *>(state + r * ld) + c4;
-    const float4 x = reinterpret_cast<const float4 *>(in + r * ld)[c4];
+    // the incoming rows are read once (non-temporal); the state is read next by the aggregation
+    const ew_f32x4 x = __builtin_nontemporal_load(reinterpret_cast<const ew_f32x4 *>(in + r * ld) + c4);
     float4 v = *sp;
     v.x = gamma * v.x + g1 * x.x;
     v.y = gamma * v.y + g1 * x.y;
@@ -101,7 +104,6 @@ int launch_ema(float *state, const float *in, int64_t rows, int32_t cols, int64_
   return PGCN_OK;
 }
 
-typedef float ew_f32x4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(256) void pack_kernel(const int32_t *idx, int64_t count, const float *src,
                                                    float *dst, int f4, int64_t ld, int sh) {
