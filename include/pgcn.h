@@ -58,6 +58,16 @@ enum pgcn_status {
   PGCN_EWORKSPACE = 5     /* workspace missing or smaller than required          */
 };
 
+/* Arithmetic of the update GEMMs.  PGCN_F32: fp32 operands, fp32 results
+ * and fp32 accumulation.  Each product is formed from an exact split of
+ * both fp32 operands into three bf16 parts (x = hi + mid + lo), six part
+ * products each, on the bf16 matrix cores.  Each part product is exact in
+ * fp32, and the three dropped ones are together below 2^-21 (1 + 2^-7) of
+ * the product, so results carry fp32 accuracy.  The environment variable
+ * PGCN_GEMM_F32=native (read per call) selects the fp32 matrix cores
+ * instead.  A non-finite operand gives a non-finite (NaN) result.
+ * PGCN_BF16: operands rounded once to bf16 (nearest even), products
+ * accumulated in fp32. */
 enum pgcn_dtype { PGCN_F32 = 0, PGCN_BF16 = 1 };
 
 enum pgcn_setup_flags {
