@@ -120,17 +120,29 @@ __global__ __launch_bounds__(256) void pack_kernel(const int32_t *idx, int64_t c
 
 // Device-to-device refill: 16-byte vectors with non-temporal loads and stores
 // (the copied rows are read in the next iteration, not in this one, so they
-// stay out of the caches the gathers use).
+// stay out of the caches the gathers use).  One short-lived workgroup per
+// 16 KB (four vectors per thread, loads issued together): the copy runs on a
+// side stream beside the compute kernels, and workgroups that retire often
+// let the dispatcher interleave theirs (a grid-stride copy that holds every
+// wave slot until it ends starves a compute kernel launched meanwhile).
+constexpr int kRefillVec = 4;
 __global__ __launch_bounds__(256) void refill_copy_kernel(const ew_f32x4 *src, ew_f32x4 *dst, int64_t n16) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (int64_t)gridDim.x * 256)
-    __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+  const int64_t base = (int64_t)blockIdx.x * (256 * kRefillVec) + threadIdx.x;
+  ew_f32x4 v[kRefillVec];
+#pragma unroll
+  for (int j = 0; j < kRefillVec; ++j)
+    if (base + 256 * j < n16) v[j] = __builtin_nontemporal_load(src + base + 256 * j);
+#pragma unroll
+  for (int j = 0; j < kRefillVec; ++j)
+    if (base + 256 * j < n16) __builtin_nontemporal_store(v[j], dst + base + 256 * j);
 }
 
 int launch_refill_copy(void *dst, const void *src, size_t bytes, hipStream_t s) {
   const int64_t n16 = (int64_t)(bytes / 16);
-  const unsigned blocks = (unsigned)std::min<int64_t>((n16 + 255) / 256, 2048);
-  hipLaunchKernelGGL(refill_copy_kernel, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const ew_f32x4 *>(src),
-                     reinterpret_cast<ew_f32x4 *>(dst), n16);
+  const int64_t blocks = (n16 + 256 * kRefillVec - 1) / (256 * kRefillVec);
+  PGCN_REQUIRE(blocks <= 0x7fffffff, "pgcn_refill_async: copy too large for one launch");
+  hipLaunchKernelGGL(refill_copy_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                     reinterpret_cast<const ew_f32x4 *>(src), reinterpret_cast<ew_f32x4 *>(dst), n16);
   PGCN_HIP(hipGetLastError());
   return PGCN_OK;
 }
