@@ -202,7 +202,7 @@ def test_refill_from_host_needs_pinned_memory():
 
 @pytest.mark.parametrize("nbytes,offset,flags", [
     (16, 0, 0), (4096, 0, 0),                                        # small: the runtime's copy
-    (4 << 20, 0, 0), (2048 * 256 * 16 * 2 + 48, 0, 0),               # the copy kernel, one pass and grid-stride
+    (4 << 20, 0, 0), (2048 * 256 * 16 * 2 + 48, 0, 0),               # the copy kernel: whole and partial last block
     (4100, 0, 0), (4096, 4, 0), ((4 << 20) + 4, 0, 0), (4 << 20, 4, 0),   # size or address not 16-byte aligned
     (4096, 0, 1), (4100, 4, 1)])                                     # the DMA engines
 def test_device_refill_copies_exactly(nbytes, offset, flags):
