@@ -293,7 +293,7 @@ __global__ __launch_bounds__(256) void agg_fixup_kernel(AggParams p, const Split
 // hi), lo = bf16(x - hi - mid): x = hi + mid + lo exactly for normal fp32 x),
 // feature-major with the 32 columns contiguous, in exactly the layout the
 // MFMA loop reads from LDS (an image of kHubImage bytes).  hub_kernel: a
-// workgroup (4 waves) owns kHubRowTile = 512 hub rows (128 per wave), one
+// workgroup (8 waves) owns kHubRowTile = 512 hub rows (64 per wave), one
 // feature block and a range of column tiles; it copies the next image into
 // LDS while multiplying the current one (double buffered), several
 // workgroups per CU.  v_mfma_f32_32x32x16_bf16 multiplies each part by the
@@ -388,7 +388,7 @@ __global__ __launch_bounds__(256) void hub_split_kernel(HubParams p) {
 }
 
 // Workgroup b: row tile b / (groups nfb), column range (b / nfb) % groups, feature block b % nfb.
-__global__ __launch_bounds__(256) void hub_kernel(HubParams p) {
+__global__ __launch_bounds__(512) void hub_kernel(HubParams p) {
   __shared__ __attribute__((aligned(16))) uint16_t hs[2][kHubImage / 2];       // 16,384 bytes
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -396,22 +396,19 @@ __global__ __launch_bounds__(256) void hub_kernel(HubParams p) {
   const int ct0 = g * p.tiles_per_group;
   const int ct1 = ct0 + p.tiles_per_group < p.ntiles ? ct0 + p.tiles_per_group : p.ntiles;
   const int h = lane >> 5, r32 = lane & 31;
-  const int hrow0 = rt * kHubRowTile + wave * 128 + r32;         // this lane's rows: hrow0 + 32 i, i < 4
+  const int hrow0 = rt * kHubRowTile + wave * 64 + r32;          // this lane's rows: hrow0 + 32 i, i < 2
   const uint16_t *img = p.img + (int64_t)fb * p.ntiles * (kHubImage / 2);
 
-  hub_u32x4 stg[2];
-  uint32_t pat[4];
+  hub_u32x4 stg;
+  uint32_t pat[2];
   auto load = [&](int ct) __attribute__((always_inline)) {
     const hub_u32x4 *src = reinterpret_cast<const hub_u32x4 *>(img + (int64_t)ct * (kHubImage / 2));
-    stg[0] = src[t];
-    stg[1] = src[t + 256];
+    stg = src[t];                                      // 512 threads x 16 bytes: the whole image
 #pragma unroll
-    for (int i = 0; i < 4; ++i) pat[i] = p.bits[(int64_t)ct * p.rows + hrow0 + 32 * i];
+    for (int i = 0; i < 2; ++i) pat[i] = p.bits[(int64_t)ct * p.rows + hrow0 + 32 * i];
   };
   auto store = [&](int buf) __attribute__((always_inline)) {
-    hub_u32x4 *dst = reinterpret_cast<hub_u32x4 *>(hs[buf]);
-    dst[t] = stg[0];
-    dst[t + 256] = stg[1];
+    reinterpret_cast<hub_u32x4 *>(hs[buf])[t] = stg;
   };
   auto expand = [](uint32_t byte) __attribute__((always_inline)) {
     hub_u32x4 aw;
@@ -421,9 +418,9 @@ __global__ __launch_bounds__(256) void hub_kernel(HubParams p) {
     return __builtin_bit_cast(hub_bf16x8, aw);
   };
 
-  hub_f32x16 acc[4];
+  hub_f32x16 acc[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) acc[i] = (hub_f32x16){};
+  for (int i = 0; i < 2; ++i) acc[i] = (hub_f32x16){};
   if (ct0 < ct1) {
     load(ct0);
     store(0);
@@ -431,23 +428,23 @@ __global__ __launch_bounds__(256) void hub_kernel(HubParams p) {
   __syncthreads();
   for (int ct = ct0; ct < ct1; ++ct) {
     const int cur = (ct - ct0) & 1;
-    uint32_t pc[4];
+    uint32_t pc[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) pc[i] = pat[i];
+    for (int i = 0; i < 2; ++i) pc[i] = pat[i];
     if (ct + 1 < ct1) load(ct + 1);
     const uint16_t *tile = hs[cur];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
       const int sh = 16 * st + 8 * h;
-      hub_bf16x8 a[4];
+      hub_bf16x8 a[2];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = expand((pc[i] >> sh) & 0xffu);
+      for (int i = 0; i < 2; ++i) a[i] = expand((pc[i] >> sh) & 0xffu);
 #pragma unroll
       for (int part = 0; part < 3; ++part) {
         const hub_bf16x8 b = __builtin_bit_cast(
             hub_bf16x8, *reinterpret_cast<const hub_u32x4 *>(tile + (part * 32 + r32) * kHubLds + 16 * st + 8 * h));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a[i], acc[i], 0, 0, 0);
+        for (int i = 0; i < 2; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a[i], acc[i], 0, 0, 0);
       }
     }
     if (ct + 1 < ct1) store(cur ^ 1);
@@ -455,7 +452,7 @@ __global__ __launch_bounds__(256) void hub_kernel(HubParams p) {
   }
   // partial sums of this column range: rows hrow0 + 32 i, features 32 fb + 8 q + 4 h .. +3
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < 2; ++i) {
     float *dst = p.part + ((int64_t)g * p.rows + hrow0 + 32 * i) * p.ld_part + 4 * p.c4_off + 32 * fb;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -655,7 +652,7 @@ int launch_aggregate(const AggArgs &a, hipStream_t s) {
           hp.tiles_per_group = (hp.ntiles + hp.groups - 1) / hp.groups;
           hipLaunchKernelGGL(hub_split_kernel, dim3((unsigned)(4 * hp.ntiles)), dim3(256), 0, s, hp);
           PGCN_HIP(hipGetLastError());
-          hipLaunchKernelGGL(hub_kernel, dim3((unsigned)(hub.rows / kHubRowTile * hp.groups * hp.nfb)), dim3(256), 0,
+          hipLaunchKernelGGL(hub_kernel, dim3((unsigned)(hub.rows / kHubRowTile * hp.groups * hp.nfb)), dim3(512), 0,
                              s, hp);
           PGCN_HIP(hipGetLastError());
           AggParams pc = p;
