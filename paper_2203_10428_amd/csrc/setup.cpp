@@ -63,9 +63,12 @@ int check_hip(hipError_t e, const char *what) {
 // 7-8 of its 58,000), or 32,000 rows for the narrow plans (rows of at most 256
 // bytes: the Reddit-like 41-wide output layer is fastest at 2-4 chunks), but
 // only while a row keeps >= 32 non-zeros per chunk on average.
-// PGCN_AGG_CHUNKS overrides every plan, PGCN_AGG_CHUNKS_T the transposed ones.
-static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz, bool transposed, int64_t rows_per_chunk) {
-  for (const char *name : {transposed ? "PGCN_AGG_CHUNKS_T" : "", "PGCN_AGG_CHUNKS"}) {
+// PGCN_AGG_CHUNKS overrides every plan, PGCN_AGG_CHUNKS_T the transposed ones,
+// PGCN_AGG_CHUNKS_NARROW the narrow ones (before the other two).
+static int32_t choose_chunks(int64_t nrows, int64_t ncols, int64_t nnz, bool transposed, int64_t rows_per_chunk,
+                             bool narrow = false) {
+  for (const char *name : {narrow ? "PGCN_AGG_CHUNKS_NARROW" : "", transposed ? "PGCN_AGG_CHUNKS_T" : "",
+                           "PGCN_AGG_CHUNKS"}) {
     const char *env = *name ? std::getenv(name) : nullptr;
     if (!env) continue;
     int v = std::atoi(env);
@@ -279,6 +282,21 @@ static int upload(T **dptr, const std::vector<T> &h) {
   return PGCN_OK;
 }
 
+// A narrow plan of a matrix takes its wide plan's dense block: the block's sizes, and its
+// device arrays once uploaded (borrowed: free_device frees them through the wide plan).
+static void share_hub(const Plan &wide, Plan &narrow) {
+  narrow.hub.rows = wide.hub.rows;
+  narrow.hub.rows_real = wide.hub.rows_real;
+  narrow.hub.cols = wide.hub.cols;
+  narrow.hub.cols_real = wide.hub.cols_real;
+  narrow.hub.nnz = wide.hub.nnz;
+  narrow.hub.d_row_ids = wide.hub.d_row_ids;
+  narrow.hub.d_col_ids = wide.hub.d_col_ids;
+  narrow.hub.d_bits = wide.hub.d_bits;
+  narrow.hub.d_init = wide.hub.d_init;
+  narrow.d_col_rest = wide.d_col_rest;
+}
+
 static void free_device(pgcn_partition *p) {
   void *ptrs[] = {p->d_col, p->d_col_t, p->d_send_idx, p->d_inv_k, p->d_inv_ptr, p->d_inv_deg, p->d_sym_scale,
                   p->plan.d_items, p->plan.d_splits, p->plan_t.d_items, p->plan_t.d_splits,
@@ -289,6 +307,8 @@ static void free_device(pgcn_partition *p) {
     void *hp[] = {q->d_col_rest, q->hub.d_row_ids, q->hub.d_col_ids, q->hub.d_bits, q->hub.d_init};
     for (void *x : hp)
       if (x) (void)hipFree(x);
+  }
+  for (Plan *q : {&p->plan, &p->plan_t, &p->plan_n, &p->plan_tn}) {   // the narrow plans' are borrowed
     q->d_col_rest = nullptr;
     q->hub.d_row_ids = q->hub.d_col_ids = nullptr;
     q->hub.d_bits = q->hub.d_init = nullptr;
@@ -540,19 +560,27 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
   {
     const int64_t nnz = p->nnz, wide = 8000, narrow = 32000;
     const int32_t c = choose_chunks(n_in, n_all, nnz, false, wide), ct = choose_chunks(n_all, n_in, nnz, true, wide);
-    const int32_t cn = choose_chunks(n_in, n_all, nnz, false, narrow);
-    const int32_t ctn = choose_chunks(n_all, n_in, nnz, true, narrow);
-    // the wide plans may take a dense block on the matrix cores; their items then index the rest
-    std::vector<int64_t> rp_rest;
+    const int32_t cn = choose_chunks(n_in, n_all, nnz, false, narrow, true);
+    const int32_t ctn = choose_chunks(n_all, n_in, nnz, true, narrow, true);
+    // a matrix may have a dense block on the matrix cores; every plan of it then indexes the
+    // rest, and the narrow plans use the wide plan's block (the same matrix, the same block)
+    std::vector<int64_t> rp_rest, rpt_rest;
     choose_hub(p->rowptr, p->col, n_in, n_all, p->plan.hub, rp_rest, p->plan.col_rest);
-    if (p->plan.hub.rows > 0) build_plan(rp_rest, p->plan.col_rest, n_in, n_all, p->segment, c, p->plan);
-    else build_plan(p->rowptr, p->col, n_in, n_all, p->segment, c, p->plan);
-    choose_hub(p->rowptr_t, p->col_t, n_all, n_in, p->plan_t.hub, rp_rest, p->plan_t.col_rest);
-    if (p->plan_t.hub.rows > 0) build_plan(rp_rest, p->plan_t.col_rest, n_all, n_in, p->segment, ct, p->plan_t);
-    else build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, ct, p->plan_t);
+    choose_hub(p->rowptr_t, p->col_t, n_all, n_in, p->plan_t.hub, rpt_rest, p->plan_t.col_rest);
+    const bool hub = p->plan.hub.rows > 0, hub_t = p->plan_t.hub.rows > 0;
+    build_plan(hub ? rp_rest : p->rowptr, hub ? p->plan.col_rest : p->col, n_in, n_all, p->segment, c, p->plan);
+    build_plan(hub_t ? rpt_rest : p->rowptr_t, hub_t ? p->plan_t.col_rest : p->col_t, n_all, n_in, p->segment, ct,
+               p->plan_t);
     p->plan_n.chunks = p->plan_tn.chunks = 0;
-    if (cn != c) build_plan(p->rowptr, p->col, n_in, n_all, p->segment, cn, p->plan_n);
-    if (ctn != ct) build_plan(p->rowptr_t, p->col_t, n_all, n_in, p->segment, ctn, p->plan_tn);
+    if (cn != c) {
+      build_plan(hub ? rp_rest : p->rowptr, hub ? p->plan.col_rest : p->col, n_in, n_all, p->segment, cn, p->plan_n);
+      share_hub(p->plan, p->plan_n);
+    }
+    if (ctn != ct) {
+      build_plan(hub_t ? rpt_rest : p->rowptr_t, hub_t ? p->plan_t.col_rest : p->col_t, n_all, n_in, p->segment, ctn,
+                 p->plan_tn);
+      share_hub(p->plan_t, p->plan_tn);
+    }
   }
 
   if (!p->host_only) {
@@ -581,6 +609,8 @@ extern "C" int pgcn_partition_setup(const pgcn_csr *csr, const pgcn_boundary_map
       if (!rc) rc = upload(&q->hub.d_init, q->hub.init);
     }
     if (rc) return rc;
+    if (p->plan_n.chunks > 0) share_hub(p->plan, p->plan_n);
+    if (p->plan_tn.chunks > 0) share_hub(p->plan_t, p->plan_tn);
     p->d_row_scale = p->symmetric ? p->d_sym_scale : p->d_inv_deg;
     p->d_col_scale = p->symmetric ? p->d_sym_scale : nullptr;
   }

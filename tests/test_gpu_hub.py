@@ -3,7 +3,8 @@ size on small graphs; the Reddit-like partition selects one by itself):
 layer forward and backward of every form through the C ABI against the
 oracle, element by element, with the block's rows and columns padded
 (sizes not multiples of the 512-row and 32-column tiles), three column
-chunks or one, split rows in the rest of the plan, widths of one, several and a partial
+chunks or one, a narrow plan (rows of at most 64 floats) with chunks of its
+own sharing the block, split rows in the rest of the plan, widths of one, several and a partial
 64-float4 pass, and both GEMM precisions (bf16 against both oracle
 readings).  ReLU decisions that differ from the oracle's are certified
 (tests/certify.py)."""
@@ -26,6 +27,9 @@ ORDER = {"agg": B.PGCN_ORDER_AGG, "transform": B.PGCN_ORDER_TRANSFORM}
 ENV = {"PGCN_HUB_ROWS": "600", "PGCN_HUB_COLS": "1000", "PGCN_AGG_CHUNKS": "3", "PGCN_SEGMENT": "64"}
 # one column chunk: the block sums are the rows' only other contribution
 ENV_ONE = {"PGCN_HUB_ROWS": "600", "PGCN_HUB_COLS": "1000", "PGCN_AGG_CHUNKS": "1"}
+# a narrow plan (rows of at most 64 floats, 2 chunks) beside the 3-chunk wide one, both with the block
+ENV_NARROW = {"PGCN_HUB_ROWS": "600", "PGCN_HUB_COLS": "1000", "PGCN_AGG_CHUNKS": "3", "PGCN_AGG_CHUNKS_NARROW": "2",
+              "PGCN_SEGMENT": "64"}
 _PARTS = {}
 
 
@@ -51,6 +55,8 @@ def part(model, norm, env=None):
         assert (info["spmmt_hub_rows"], info["spmmt_hub_cols"]) == (600, 1000)
         assert info["spmm_hub_nnz"] > 0 and info["spmmt_hub_nnz"] > 0
         assert info["spmm_chunks"] == int(env["PGCN_AGG_CHUNKS"])
+        narrow = int(env.get("PGCN_AGG_CHUNKS_NARROW", env["PGCN_AGG_CHUNKS"]))
+        assert (info["spmm_chunks_narrow"], info["spmmt_chunks_narrow"]) == (narrow, narrow)
         _PARTS[key] = (ref, propagation_matrix(ref, norm), h)
     return _PARTS[key]
 
@@ -72,6 +78,13 @@ def test_layer_with_dense_block(model, norm, order, dt, f_in, f_out):
 @pytest.mark.parametrize("f_in,f_out", [(256, 256), (41, 47)])
 def test_layer_with_dense_block_one_chunk(model, norm, order, dt, f_in, f_out):
     check_layer(model, norm, order, dt, f_in, f_out, ENV_ONE)
+
+
+@pytest.mark.parametrize("model,norm,order", FORMS)
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("f_in,f_out", [(41, 47), (64, 300), (300, 64), (7, 5)])
+def test_layer_with_dense_block_narrow_plan(model, norm, order, dt, f_in, f_out):
+    check_layer(model, norm, order, dt, f_in, f_out, ENV_NARROW)
 
 
 def check_layer(model, norm, order, dt, f_in, f_out, env):
