@@ -127,12 +127,16 @@ typedef struct pgcn_partition pgcn_partition;
  *                      per chunk, 32,000 for rows of at most 64 floats, while
  *                      rows keep >= 32 non-zeros per chunk);
  *   PGCN_AGG_CHUNKS_T  the same for the plans of P_i^T alone (takes precedence);
+ *   PGCN_AGG_CHUNKS_NARROW  the same for the plans of rows of at most 64 floats
+ *                      (takes precedence over both);
  *   PGCN_SEGMENT       length at which long rows are split into segments,
  *                      16..1048576 (read by pgcn_partition_setup; default 512);
  *   PGCN_AGG_SLICE_F4  float4 columns per aggregation lane slice: 16, 32 or 64
  *                      (read per call; default 64);
  *   PGCN_TN_BM=128     keeps the fp32 weight-gradient GEMM in 128-row tiles
  *                      (read once; default: 256-row tiles for f_in >= 384);
+ *   PGCN_GEMM_F32=native  fp32 update GEMMs on the fp32 matrix cores instead of
+ *                      by bf16 parts (read per call; see pgcn_dtype);
  *   PGCN_HUB=0         no dense block on the matrix cores (read by
  *                      pgcn_partition_setup; default: a block of the rows with
  *                      the most non-zeros x the most referenced columns where it
@@ -141,7 +145,8 @@ typedef struct pgcn_partition pgcn_partition;
  *                      and columns (clamped to the matrix).
  * Chunks, segments and the dense block set the order in which a row's terms are
  * added (results stay deterministic for a given setting and row width); the
- * slice width and PGCN_TN_BM change only speed. */
+ * slice width and PGCN_TN_BM change only speed; PGCN_GEMM_F32 changes the
+ * order of the GEMMs' fp32 sums within the same rounding bound. */
 
 /* Largest layer width (f_in, f_out) the layer entry points accept: the
  * aggregation covers a row in at most 32 launches of up to 512 float4
