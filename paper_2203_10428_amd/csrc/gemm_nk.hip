@@ -88,9 +88,9 @@ __device__ __forceinline__ int nk_xcd_remap(int b, int g) {
 template <bool BF16>
 __global__ __launch_bounds__(256) void pack_b_kernel(const float *W, int ldw, int trans, int N, int K, int rows,
                                                      int ldk, void *out) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= rows * ldk) return;
-  const int n = i / ldk, k = i - n * ldk;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;   // rows x ldk may pass 2^31 at the widest layers
+  if (i >= (int64_t)rows * ldk) return;
+  const int n = (int)(i / ldk), k = (int)(i - (int64_t)n * ldk);
   const float v = (n < N && k < K) ? (trans ? W[(int64_t)k * ldw + n] : W[(int64_t)n * ldw + k]) : 0.f;
   if (BF16) reinterpret_cast<uint16_t *>(out)[i] = nk_bf16(v);
   else reinterpret_cast<float *>(out)[i] = v;
@@ -118,11 +118,11 @@ __device__ __forceinline__ void nk_split3x2(float x0, float x1, uint32_t &hi, ui
 // same indexing as pack_b_kernel.
 __global__ __launch_bounds__(256) void pack_b_split_kernel(const float *W, int ldw, int trans, int N, int K, int rows,
                                                            int ldk, uint16_t *out) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= rows * ldk) return;
-  const int n = i / ldk, k = i - n * ldk;
-  const float v = (n < N && k < K) ? (trans ? W[(int64_t)k * ldw + n] : W[(int64_t)n * ldw + k]) : 0.f;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t plane = (int64_t)rows * ldk;
+  if (i >= plane) return;
+  const int n = (int)(i / ldk), k = (int)(i - (int64_t)n * ldk);
+  const float v = (n < N && k < K) ? (trans ? W[(int64_t)k * ldw + n] : W[(int64_t)n * ldw + k]) : 0.f;
   uint32_t hi, mid, lo;
   nk_split3x2(v, 0.f, hi, mid, lo);
   out[i] = (uint16_t)hi;
