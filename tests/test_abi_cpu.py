@@ -96,10 +96,11 @@ def test_setup_empty_partition_and_isolated_nodes():
 def test_setup_chunk_counts_by_row_width(monkeypatch):
     # column chunks: about 8,000 gathered rows each (32,000 for rows of at most
     # 64 floats), while rows keep >= 32 non-zeros per chunk; the overrides set
-    # every plan (PGCN_AGG_CHUNKS) or those of P_i^T (PGCN_AGG_CHUNKS_T)
+    # every plan (PGCN_AGG_CHUNKS), those of P_i^T (PGCN_AGG_CHUNKS_T) or the
+    # narrow ones (PGCN_AGG_CHUNKS_NARROW, before both)
     from gpu_helpers import random_partition_graph
     n, rowptr, col, owner = random_partition_graph(9000, 3000, 2, 120, 13)
-    for k in ("PGCN_AGG_CHUNKS", "PGCN_AGG_CHUNKS_T"):
+    for k in ("PGCN_AGG_CHUNKS", "PGCN_AGG_CHUNKS_T", "PGCN_AGG_CHUNKS_NARROW"):
         monkeypatch.delenv(k, raising=False)
 
     def counts():
@@ -116,6 +117,8 @@ def test_setup_chunk_counts_by_row_width(monkeypatch):
     assert counts()[1] == (3, 3, 3, 3)
     monkeypatch.setenv("PGCN_AGG_CHUNKS_T", "5")
     assert counts()[1] == (3, 3, 5, 5)
+    monkeypatch.setenv("PGCN_AGG_CHUNKS_NARROW", "2")
+    assert counts()[1] == (3, 2, 5, 2)
 
 
 def test_setup_heavy_rows_are_split_into_fixed_segments():
@@ -278,6 +281,32 @@ def test_binding_structs_match_the_header(tmp_path):
         assert int(c_side[name]) == C.sizeof(cls), name
         for field, _ in cls._fields_:
             assert int(c_side[f"{name}.{field}"]) == getattr(cls, field).offset, f"{name}.{field}"
+
+
+def test_narrow_plans_share_the_dense_block(monkeypatch):
+    """A narrow plan (rows of at most 64 floats, chunks of its own) aggregates with its
+    matrix's dense block: a 41-wide layer's workspace holds the block's column images and
+    sums, which a partition without the block does not need."""
+    from gpu_helpers import random_partition_graph
+    n, rowptr, col, owner = random_partition_graph(1500, 900, 3, 30, 4, hub_deg=800)
+    for k, v in (("PGCN_HUB_ROWS", "300"), ("PGCN_HUB_COLS", "700"), ("PGCN_AGG_CHUNKS", "3"),
+                 ("PGCN_AGG_CHUNKS_NARROW", "2")):
+        monkeypatch.setenv(k, v)
+
+    def sizes():
+        h = B.pgcn_partition_setup(n, rowptr, col, owner, 3, 0, host_only=True)
+        info = B.pgcn_partition_info(h)
+        assert (info["spmm_chunks"], info["spmm_chunks_narrow"]) == (3, 2)
+        return info, {(f, o): B.pgcn_layer_workspace_size(h, f, f, B.PGCN_F32, o)
+                      for f in (41, 256) for o in (B.PGCN_ORDER_AGG, B.PGCN_ORDER_TRANSFORM)}
+
+    info, with_block = sizes()
+    assert info["spmm_hub_cols"] == 700
+    monkeypatch.setenv("PGCN_HUB", "0")
+    _, without = sizes()
+    images = (700 + 31) // 32 * 8 * 8192           # column tiles x feature blocks x image bytes
+    for key in with_block:
+        assert with_block[key] - without[key] >= images, key
 
 
 def test_dense_block_selection(monkeypatch):
