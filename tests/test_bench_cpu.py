@@ -106,3 +106,22 @@ def test_committed_traffic_records_name_existing_sources():
         for name in rec["sources"]:
             assert os.path.exists(os.path.join(ROOT, "paper_2203_10428_amd", "csrc", name))
         assert rec["kernels"]["agg_fwd"] > 0 and rec["kernels"]["agg_bwd"] > 0
+
+
+def test_cpu_baseline_times_short_steps_as_a_mean():
+    """One oracle step shorter than a second is dominated by first-call costs: the baseline
+    times further steps after it (at most 200) and reports their mean."""
+    from paper_2203_10428_amd import configs
+    bench = load_bench()
+    sec, n_inner, nnz, threads, reps = bench.cpu_baseline(configs.WORKLOADS["tiny-2k-2parts"], 1.0)
+    assert reps > 1 and reps <= 200
+    assert 0 < sec < 1.0 and n_inner > 0 and nnz > 0 and threads >= 1
+
+
+def test_f32_gemm_method_follows_the_override(monkeypatch):
+    bench = load_bench()
+    monkeypatch.delenv("PGCN_GEMM_F32", raising=False)
+    assert bench.f32_gemm_method() == "bf16-parts-x6"
+    monkeypatch.setenv("PGCN_GEMM_F32", "native")
+    assert bench.f32_gemm_method() == "fp32-matrix-cores"
+    assert bench.F32_PARTS_CEILING_TFLOPS == bench.MFMA_PEAK_TFLOPS["bf16"] / 6
